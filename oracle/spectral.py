@@ -1,0 +1,118 @@
+"""ISO-Merger (Sec. 4.2; App. E; Algorithm 1), float64 (test infrastructure).
+
+One 2-D weight matrix at a time: base W_0 and K expert matrices
+W_i = W_0 + Delta_i.  The steps follow App. E in its order:
+
+  1. thin SVDs W_0 = U_0 Sigma_0 V_0^T and W_i = U_i Sigma_i V_i^T   (App. E Setup)
+  2. joint sign canonicalisation s_ik = sign(<u_0k, u_ik>), sign(0) := 1
+     applied to u_ik and v_ik                                        (App. E, gauge)
+  3. frame displacements Delta U_i = U_i - U_0, Delta V_i = V_i - V_0 and
+     tangent projection Pi_U0(D) = D - U_0 sym(U_0^T D)              (App. E, tangent)
+  4. D_keep keeps the leading k_keep = round(rho_keep q) modes       (App. E, eq. of D_keep)
+  5. proxies g_i = xi~_U,i Sigma_0 V_0^T + U_0 Sigma_0 xi~_V,i^T and
+     Gram Gamma_ij = <g_i, g_j>_F                                    (App. E, retention)
+  6. drop zero-norm proxies, solve (Gamma + lambda_ridge I) c = diag Gamma,
+     clip c to [c_min, c_max]                                        (App. E, retention)
+  7. xi_* = Pi(sum_i c_i xi~_i), U_* = polar(U_0 + xi_U*),
+     V_* = polar(V_0 + xi_V*), W_* = U_* Sigma_0 V_*^T                (App. E, retraction)
+
+The SVD is LAPACK's (numpy.linalg.svd, a library primitive); polar(X) is
+P Q^T from the thin SVD X = P S Q^T, as the paper defines it.  The Gram
+system is solved by Cholesky (the paper names no solver; the matrix is SPD).
+"""
+import math
+
+import numpy as np
+
+
+def thin_svd(w):
+    """W = U diag(s) V^T with s nonincreasing; returns (U, s, V)."""
+    u, s, vt = np.linalg.svd(np.asarray(w, dtype=np.float64), full_matrices=False)
+    return u, s, vt.T
+
+
+def sym(a):
+    return 0.5 * (a + a.T)
+
+
+def tangent_project(anchor, d):
+    """Pi_{U_0}(D) = D - U_0 sym(U_0^T D): orthogonal projection onto T_{U_0} St."""
+    return d - anchor @ sym(anchor.T @ d)
+
+
+def polar(x):
+    """polar(X) = P Q^T for the thin SVD X = P S Q^T."""
+    p, _, qt = np.linalg.svd(x, full_matrices=False)
+    return p @ qt
+
+
+def k_keep_of(rho_keep, q):
+    """k_keep = round(rho_keep * q), halves rounded up, formed in float64."""
+    return int(math.floor(rho_keep * q + 0.5))
+
+
+def canonicalize(u0, u, v):
+    """Joint sign canonicalisation against the base (App. E): sign(0) := 1."""
+    s = np.sign(np.sum(u0 * u, axis=0))
+    s[s == 0] = 1.0
+    return u * s, v * s
+
+
+def iso_merge_factors(u0, s0, v0, experts, rho_keep=0.9, ridge=1e-12, c_min=0.0, c_max=1.5):
+    """Algorithm 1 body from precomputed SVDs.
+
+    ``experts`` is a list of (U_i, s_i, V_i).  Returns a dict with W_star,
+    U_star, V_star, coefficients c (K,), Gram, the masked tangents and the
+    aggregate tangents xi_U, xi_V.
+    """
+    q = s0.size
+    kk = k_keep_of(rho_keep, q)
+    keep = (np.arange(q) < kk).astype(np.float64)            # D_keep, modes 1..k_keep
+    S0 = np.diag(s0)
+    xu_t, xv_t, g = [], [], []
+    for (u, s, v) in experts:
+        u, v = canonicalize(u0, u, v)
+        xu = tangent_project(u0, u - u0) * keep              # xi~_U,i = Pi(Delta U_i) D_keep
+        xv = tangent_project(v0, v - v0) * keep
+        xu_t.append(xu)
+        xv_t.append(xv)
+        g.append(xu @ S0 @ v0.T + u0 @ S0 @ xv.T)
+    K = len(experts)
+    nz = [i for i in range(K) if np.linalg.norm(g[i]) > 0]
+    c = np.zeros(K)
+    gram = np.zeros((K, K))
+    for i in range(K):
+        for j in range(K):
+            gram[i, j] = np.sum(g[i] * g[j])
+    if nz:
+        gam = gram[np.ix_(nz, nz)]
+        b = np.diag(gam).copy()
+        chol = np.linalg.cholesky(gam + ridge * np.eye(len(nz)))
+        y = np.linalg.solve(chol, b)
+        cbar = np.linalg.solve(chol.T, y)
+        c[nz] = np.clip(cbar, c_min, c_max)
+    agg_u = sum(c[i] * xu_t[i] for i in range(K))
+    agg_v = sum(c[i] * xv_t[i] for i in range(K))
+    xi_u = tangent_project(u0, agg_u)
+    xi_v = tangent_project(v0, agg_v)
+    u_star = polar(u0 + xi_u)
+    v_star = polar(v0 + xi_v)
+    w_star = u_star @ S0 @ v_star.T
+    return dict(w_star=w_star, u_star=u_star, v_star=v_star, c=c, gram=gram,
+                xi_u=xi_u, xi_v=xi_v, xu_masked=xu_t, xv_masked=xv_t, k_keep=kk)
+
+
+def iso_merge(w0, deltas, rho_keep=0.9, ridge=1e-12, c_min=0.0, c_max=1.5):
+    """Algorithm 1 for one matrix: W_i = W_0 + Delta_i (raw expert deltas)."""
+    w0 = np.asarray(w0, dtype=np.float64)
+    u0, s0, v0 = thin_svd(w0)
+    experts = [thin_svd(w0 + np.asarray(d, dtype=np.float64)) for d in deltas]
+    res = iso_merge_factors(u0, s0, v0, experts, rho_keep, ridge, c_min, c_max)
+    res["s0"] = s0
+    return res
+
+
+def average_1d(w0, experts):
+    """1-D parameters: w_* = w_0 + (1/K) sum_i (w_i - w_0) (App. E, scope)."""
+    w0 = np.asarray(w0, dtype=np.float64)
+    return w0 + sum(np.asarray(w, dtype=np.float64) - w0 for w in experts) / len(experts)
