@@ -1,0 +1,217 @@
+/*
+ * iso.h -- C ABI of libiso.so: the element-wise merge/update hot path of
+ * ISO ("An RLVR-Native Optimization Stack") and the data-free merges it is
+ * compared against, as MI355X (gfx950) HIP kernels.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - A call processes a table of n_t 2-D weight tensors (iso_tensor, host
+ *    memory, read before the call returns).  Each tensor has a base W_0
+ *    (theta_0 restricted to that matrix), K expert deltas tau_i = theta_i -
+ *    theta_0 of the same shape (App. F), row-major and contiguous, and
+ *    rows*cols = N elements.  1 <= K <= ISO_MAX_K.
+ *  - Storage types: ISO_F32 (IEEE binary32) or ISO_BF16 (bfloat16 bits).  One
+ *    call uses one storage type for base, deltas and the weight output.
+ *  - All data pointers are device memory owned by the caller; every one must
+ *    be 16-byte aligned (ISO_ERR_ALIGNMENT otherwise).  N need not be a
+ *    multiple of anything.
+ *  - ws / ws_bytes: caller-allocated device workspace of at least
+ *    iso_workspace_size(op, ...) bytes, 256-byte aligned, that must stay
+ *    alive until the stream work has finished.  Its contents on entry do not
+ *    matter.  The library allocates no device memory.
+ *  - stream: a hipStream_t (NULL = the default stream).  Work is queued
+ *    asynchronously on it; only iso_read_device_status synchronises.
+ *  - Errors: argument, shape, alignment and workspace-size errors are found
+ *    on the host before anything is queued and returned directly.  A
+ *    non-finite base or delta value found by a kernel sets a status word in
+ *    the workspace; iso_read_device_status returns ISO_ERR_NONFINITE then (the
+ *    outputs of such a call are unspecified).  HIP launch errors are
+ *    returned as ISO_ERR_HIP.  Nothing throws across the ABI.
+ *  - Results are deterministic and do not depend on launch geometry.
+ *
+ * Arithmetic (readings of the paper, which fixes no precision for these
+ * operators): every merged coordinate is formed in binary64 -- sums start
+ * at +0.0 and add the terms in expert order, means divide that sum by the
+ * count, then u = lambda*t and v = w0 + u -- and v is rounded ONCE to the
+ * storage type (round to nearest even; binary64 -> bf16 never passes through
+ * binary32).  The sign used by the TIES election is the sign of the exact
+ * real sum.
+ */
+#ifndef ISO_H
+#define ISO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ISO_MAX_K 8
+
+typedef enum iso_status {
+  ISO_OK = 0,
+  ISO_ERR_INVALID_ARG = 1,
+  ISO_ERR_ALIGNMENT = 2,
+  ISO_ERR_WORKSPACE = 3,
+  ISO_ERR_NONFINITE = 4,
+  ISO_ERR_HIP = 5,
+  ISO_ERR_UNSUPPORTED = 6,
+  ISO_ERR_INTERNAL = 7     /* a kernel met counts that cannot occur; outputs invalid */
+} iso_status;
+
+typedef enum iso_dtype { ISO_F32 = 0, ISO_BF16 = 1 } iso_dtype;
+
+/* App. F: Task Arithmetic, TIES-Merging, RAM. */
+typedef enum iso_merge_mode { ISO_MERGE_TA = 0, ISO_MERGE_TIES = 1, ISO_MERGE_RAM = 2 } iso_merge_mode;
+
+typedef enum iso_update_mode {
+  ISO_UPDATE_APPLY = 0,    /* out = W_0 + lambda * tau_in                                   */
+  ISO_UPDATE_FUSED = 1,    /* out = W_0 + merged update, elect + merge + apply in one pass  */
+  ISO_UPDATE_SPECTRAL = 2  /* out = W_* of ISO-Merger (Algorithm 1)                          */
+} iso_update_mode;
+
+/* Operation codes for iso_workspace_size. */
+typedef enum iso_op {
+  ISO_OP_TOPK = 0,
+  ISO_OP_SIGN = 1,
+  ISO_OP_MERGE = 2,
+  ISO_OP_UPDATE_APPLY = 3,
+  ISO_OP_UPDATE_FUSED = 4,     /* FUSED with caller descriptors, or TA / RAM                    */
+  ISO_OP_UPDATE_FUSED_SELECT = 5, /* FUSED TIES that selects inside the call (desc == NULL)     */
+  ISO_OP_UPDATE_SPECTRAL = 6,
+  ISO_OP_BLOCKDIAG = 7
+} iso_op;
+
+/* One weight tensor of the table.  Which pointers are read depends on the call. */
+typedef struct iso_tensor {
+  const void* base;                /* W_0, N elements                                           */
+  const void* deltas[ISO_MAX_K];   /* tau_1..tau_K, N elements each (entries >= K ignored)      */
+  void* out;                       /* merged weights, N elements of the storage type            */
+  int64_t rows, cols;              /* N = rows * cols, N >= 0                                    */
+  int64_t k;                       /* TopKMask count per delta, 0 <= k <= N (TIES only)          */
+} iso_tensor;
+
+/*
+ * TopKMask of one delta (App. F, TIES "Trim": m_i = TopKMask(|tau_i|, rho)),
+ * in threshold form.  key(x) is the storage bit pattern of |x| (bf16: bits &
+ * 0x7FFF, fp32: bits & 0x7FFFFFFF), which orders like |x|.  Entry p (flat,
+ * row-major) is kept iff key_p > t_key, or key_p == t_key and p < tie_cutoff:
+ * exactly k entries, the k largest magnitudes, ties at the threshold going to
+ * the lower flat index.  n_above = #{key > t_key}, tie_quota = k - n_above.
+ * tie_cutoff is N when every entry with key == t_key is kept, else one past
+ * the flat index of the tie_quota-th such entry (so the descriptor is unique).
+ * key_max is the largest key in the delta.  k == 0 gives t_key = 0xFFFFFFFF,
+ * n_above = tie_quota = tie_cutoff = 0.
+ */
+typedef struct iso_select_desc {
+  uint32_t t_key;
+  uint32_t key_max;
+  int64_t n_above;
+  int64_t tie_quota;
+  int64_t tie_cutoff;
+} iso_select_desc;
+
+/*
+ * Bytes of workspace the given operation needs for this table (0 on bad
+ * arguments).  ISO_OP_BLOCKDIAG also needs the rank: use iso_workspace_size_tsv.
+ */
+size_t iso_workspace_size(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt);
+
+/*
+ * iso_topk_mask -- TopKMask of every delta of every tensor (App. F, TIES
+ * "Trim"), k = t[j].k.  Writes desc[j*K + i] (device memory, n_t*K entries)
+ * for delta i of tensor j.  If mask_bits is not NULL it is a host array of
+ * n_t*K device pointers; pointer j*K+i receives the mask as ceil(N/32)
+ * uint32 words, bit (p % 32) of word p/32 set iff entry p is kept.  Exact
+ * radix selection over the magnitude keys; the result is unique.
+ */
+iso_status iso_topk_mask(const iso_tensor* t, int n_t, int K, iso_dtype dt, iso_select_desc* desc,
+                         uint32_t* const* mask_bits, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * iso_sign_elect -- gamma^p = sign(sum_i tilde tau_i^p) (App. F, TIES "Elect
+ * Sign"), tilde tau_i = m_i (.) tau_i with m_i from desc (device, n_t*K
+ * entries from iso_topk_mask), or tilde tau_i = tau_i when desc is NULL.
+ * The sign is that of the exact real sum.  sign_out is a host array of n_t
+ * device pointers; tensor j receives N int8 values in {-1, 0, +1}.
+ */
+iso_status iso_sign_elect(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_select_desc* desc,
+                          int8_t* const* sign_out, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * iso_merge -- the merged task vector tau_merge (App. F) as binary32:
+ *   ISO_MERGE_TA:   lambda * sum_i tau_i                                   (Task Arithmetic)
+ *   ISO_MERGE_TIES: lambda * mean over A_p = {i: tilde tau_i != 0,
+ *                   sign(tilde tau_i) = gamma^p}, 0 where A_p is empty       (TIES disjoint mean)
+ *   ISO_MERGE_RAM:  lambda * mean over A_p = {i: |tau_i| > eps_act}, 0 if
+ *                   empty (the paper's RAM has lambda = 1)                  (RAM)
+ * desc is required for TIES and ignored otherwise.  tau_out is a host array
+ * of n_t device pointers to N floats: each is the binary64 u = lambda*t
+ * rounded once to binary32.
+ */
+iso_status iso_merge(const iso_tensor* t, int n_t, int K, iso_dtype dt, iso_merge_mode mode,
+                     const iso_select_desc* desc, double lambda, double eps_act, float* const* tau_out, void* ws,
+                     size_t ws_bytes, void* stream);
+
+typedef struct iso_update_args {
+  iso_update_mode mode;
+  iso_merge_mode merge;             /* FUSED: which merge                                          */
+  double lambda;                    /* APPLY, FUSED: scale of the merged update (TIES: 1.0)         */
+  double eps_act;                   /* FUSED RAM: activity threshold (paper: 1e-5), strict >        */
+  const iso_select_desc* desc;      /* FUSED TIES: device descriptors, or NULL to select inside     */
+  const float* const* tau_in;       /* APPLY: host array of n_t device pointers, N floats each      */
+  int8_t* const* sign_out;          /* FUSED TIES: optional host array of n_t device int8 pointers  */
+  double rho_keep;                  /* SPECTRAL: keep ratio (paper 0.9)                             */
+  double ridge;                     /* SPECTRAL: lambda_ridge (paper 1e-12)                         */
+  double c_min, c_max;              /* SPECTRAL: clip range (paper [0, 1.5])                        */
+  double* coef_out;                 /* SPECTRAL: optional device array of n_t*K coefficients c*     */
+} iso_update_args;
+
+/*
+ * iso_update -- writes t[j].out.
+ *  APPLY:    out = round(W_0 + lambda * tau_in)  (theta_merge = theta_0 + tau_merge, App. F).
+ *  FUSED:    the merge of iso_merge followed by out = round(W_0 + u) in one
+ *            pass that reads each delta and the base once (App. F TIES Trim /
+ *            Elect / Merge and theta_0 + lambda tau_TIES; TA; RAM).  With TIES
+ *            and desc == NULL the TopKMask selection runs inside the call.
+ *  SPECTRAL: ISO-Merger, Sec. 4.2 / App. E / Algorithm 1, per matrix, in
+ *            binary64: SVDs of W_0 and W_i = W_0 + tau_i, joint sign
+ *            canonicalisation, tangent projection, D_keep, effect proxies and
+ *            their Gram matrix, ridge solve and clip, aggregate projection,
+ *            polar retraction, W_* = U_* Sigma_0 V_*^T (rounded once).
+ *            Deltas are the raw expert deltas (no TopKMask).  Supported for
+ *            rows, cols <= ISO_SPECTRAL_MAX_DIM.
+ */
+iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_update_args* a, void* ws,
+                      size_t ws_bytes, void* stream);
+
+#define ISO_SPECTRAL_MAX_DIM 1024
+
+/*
+ * iso_blockdiag_project -- TSV-Merge (App. F): each delta is truncated to its
+ * top-`rank` singular triplets, the left and right singular vectors are
+ * concatenated (U = [U_1 | ... | U_K], V likewise, Sigma = blockdiag of the
+ * Sigma_i), U and V are orthogonalised in the Procrustes form (U_perp = P Q^T
+ * for U = P D Q^T), and out = round(W_0 + alpha * U_perp Sigma V_perp^T).
+ * K*rank <= min(rows, cols).  If delta_hat is not NULL it is a host array of
+ * n_t device pointers receiving U_perp Sigma V_perp^T as N floats.
+ */
+iso_status iso_blockdiag_project(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank, double alpha,
+                                 float* const* delta_hat, void* ws, size_t ws_bytes, void* stream);
+
+size_t iso_workspace_size_tsv(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank);
+
+/* round(n * num / den), halves rounded up, in exact integer arithmetic; -1 on bad arguments. */
+int64_t iso_k_from_density(int64_t n, int64_t num, int64_t den);
+
+/* Synchronises `stream`, then reports what the kernels of the last call on `ws` found. */
+iso_status iso_read_device_status(const void* ws, void* stream);
+
+const char* iso_status_string(iso_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ISO_H */

@@ -48,9 +48,10 @@ def topk_descriptor(delta, k, dtype):
 
     Returns (T_key, n_above, tie_quota, tie_cutoff) where T_key is the storage
     bit pattern of the k-th largest magnitude, n_above = #{|tau| > T},
-    tie_quota = k - n_above and tie_cutoff is one past the flat index of the
-    tie_quota-th entry with |tau| == T.  Entry p is kept iff key_p > T_key or
-    (key_p == T_key and p < tie_cutoff).  For k = 0: (0xFFFFFFFF, 0, 0, 0).
+    tie_quota = k - n_above and tie_cutoff is N when every entry with
+    |tau| == T is kept, else one past the flat index of the tie_quota-th entry
+    with |tau| == T.  Entry p is kept iff key_p > T_key or (key_p == T_key and
+    p < tie_cutoff).  For k = 0: (0xFFFFFFFF, 0, 0, 0).
     """
     x = to_f64(delta, dtype).ravel()
     _check_finite(x, "delta")
@@ -64,7 +65,7 @@ def topk_descriptor(delta, k, dtype):
     n_above = int(np.count_nonzero(a > t))
     quota = k - n_above
     ties = np.flatnonzero(a == t)
-    cutoff = int(ties[quota - 1]) + 1
+    cutoff = n if quota == ties.size else int(ties[quota - 1]) + 1
     t_key = int(magnitude_key(from_f64(np.array([t]), dtype), dtype)[0])
     return (t_key, n_above, quota, cutoff)
 

@@ -1,0 +1,104 @@
+"""C ABI checks that need no GPU: the library loads, exports what include/iso.h declares,
+and rejects bad arguments on the host before anything is queued."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_19331_amd as iso
+from paper_2607_19331_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "iso.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:iso_status|size_t|int64_t|const char\*)\s+(iso_\w+)\s*\(", src, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = _lib.load()
+    names = declared_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(_lib.SYMBOLS)
+
+
+FAKE = 0x100000     # never dereferenced: every call below fails validation first
+
+
+def entry(rows=16, cols=16, k=10, K=2, misalign=False, out=True):
+    d = [FAKE + 0x1000 * (i + 1) + (8 if (misalign and i == 1) else 0) for i in range(K)]
+    return iso.Entry(rows, cols, base=FAKE, deltas=d, out=FAKE + 0x100 if out else None, k=k)
+
+
+def call_topk(es, K, ws_bytes=1 << 30, ws=FAKE * 16, desc=FAKE * 8):
+    L = _lib.load()
+    return L.iso_topk_mask(iso._table(es), len(es), K, iso.BF16, desc, None, ws, ws_bytes, None)
+
+
+def test_host_validation_errors():
+    L = _lib.load()
+    assert call_topk([entry()], 0) == _lib.ERR_INVALID_ARG
+    assert call_topk([entry(K=8)], 9) == _lib.ERR_INVALID_ARG
+    assert call_topk([entry(k=257)], 2) == _lib.ERR_INVALID_ARG
+    assert call_topk([entry(k=-1)], 2) == _lib.ERR_INVALID_ARG
+    assert call_topk([entry(misalign=True)], 2) == _lib.ERR_ALIGNMENT
+    assert call_topk([entry()], 2, ws_bytes=100) == _lib.ERR_WORKSPACE
+    assert call_topk([entry()], 2, ws=FAKE * 16 + 64) == _lib.ERR_ALIGNMENT
+    assert call_topk([entry()], 2, desc=None) == _lib.ERR_INVALID_ARG
+    assert call_topk([entry(rows=1 << 17, cols=1 << 16)], 2) == _lib.ERR_UNSUPPORTED
+    assert call_topk([], 2) == _lib.OK
+    bad = iso.Entry(-1, 3, base=FAKE, deltas=[FAKE, FAKE], out=FAKE)
+    assert call_topk([bad], 2) == _lib.ERR_INVALID_ARG
+    # iso_merge: TIES needs descriptors, eps must be >= 0, lambda finite
+    es = [entry()]
+    tau = (ctypes.c_void_p * 1)(FAKE)
+    assert L.iso_merge(iso._table(es), 1, 2, iso.BF16, 1, None, 1.0, 0.0, tau, FAKE * 16, 1 << 30, None) == 1
+    assert L.iso_merge(iso._table(es), 1, 2, iso.BF16, 0, None, float("nan"), 0.0, tau, FAKE * 16, 1 << 30, None) == 1
+    assert L.iso_merge(iso._table(es), 1, 2, iso.BF16, 2, None, 1.0, -1.0, tau, FAKE * 16, 1 << 30, None) == 1
+    assert L.iso_merge(iso._table(es), 1, 2, iso.BF16, 7, None, 1.0, 0.0, tau, FAKE * 16, 1 << 30, None) == 1
+    # iso_update: missing output, bad mode, spectral size limit
+    a = _lib.IsoUpdateArgs()
+    a.mode, a.merge, a.lambda_, a.eps_act = 1, 0, 1.0, 0.0
+    noout = [entry(out=False)]
+    assert L.iso_update(iso._table(noout), 1, 2, iso.BF16, ctypes.byref(a), FAKE * 16, 1 << 30, None) == 1
+    a.mode = 9
+    assert L.iso_update(iso._table(es), 1, 2, iso.BF16, ctypes.byref(a), FAKE * 16, 1 << 30, None) == 1
+    a.mode, a.rho_keep, a.ridge, a.c_min, a.c_max = 2, 0.9, 1e-12, 0.0, 1.5
+    big = [entry(rows=2048, cols=2048, k=0)]
+    assert L.iso_update(iso._table(big), 1, 2, iso.BF16, ctypes.byref(a), FAKE * 16, 1 << 30, None) == \
+        _lib.ERR_UNSUPPORTED
+    a.rho_keep = 0.0
+    assert L.iso_update(iso._table(es), 1, 2, iso.BF16, ctypes.byref(a), FAKE * 16, 1 << 30, None) == 1
+    assert L.iso_update(iso._table(es), 1, 2, iso.BF16, None, FAKE * 16, 1 << 30, None) == 1
+    assert L.iso_read_device_status(None, None) == 1
+
+
+def test_workspace_sizes():
+    es = [entry(rows=2048, cols=5632, k=1153434, K=2), entry(rows=7, cols=9, k=3, K=2)]
+    n_sel = iso.iso_workspace_size(iso.OP_TOPK, es, 2, iso.BF16)
+    n_fused = iso.iso_workspace_size(iso.OP_UPDATE_FUSED, es, 2, iso.BF16)
+    n_fs = iso.iso_workspace_size(iso.OP_UPDATE_FUSED_SELECT, es, 2, iso.BF16)
+    assert n_sel >= 4 * 32768 * 4 and n_fused < n_sel <= n_fs
+    assert n_sel % 256 == 0 and n_fused % 256 == 0
+    assert iso.iso_workspace_size(99, es, 2, iso.BF16) == 0
+    assert iso.iso_workspace_size(iso.OP_TOPK, es, 0, iso.BF16) == 0
+
+
+@pytest.mark.parametrize("n,num,den,k", [(65536, 1, 5, 13107), (11534336, 1, 10, 1153434), (5, 1, 10, 1),
+                                         (15, 1, 10, 2), (10, 0, 1, 0), (7, 1, 1, 7),
+                                         (545009664, 1, 10, 54500966)])
+def test_k_from_density_matches_oracle(n, num, den, k):
+    from fractions import Fraction
+    from oracle.numerics import k_from_density
+    assert iso.iso_k_from_density(n, num, den) == k == k_from_density(n, Fraction(num, den))
+
+
+def test_status_strings():
+    for s in range(8):
+        assert iso.iso_status_string(s)
+    assert "unknown" in iso.iso_status_string(42)

@@ -85,7 +85,7 @@ def test_descriptor_k_zero_and_full():
     x = _store([0.5, -0.0, 0.0, 2.0], "bf16")
     assert ties.topk_descriptor(x, 0, "bf16") == (0xFFFFFFFF, 0, 0, 0)
     d = ties.topk_descriptor(x, 4, "bf16")
-    assert d[0] == 0 and d[1] == 2 and d[2] == 2 and d[3] == 3
+    assert d[0] == 0 and d[1] == 2 and d[2] == 2 and d[3] == 4        # whole zero bucket kept: cutoff = N
     d = ties.topk_descriptor(x, 3, "bf16")           # k > nnz: the lowest-index zero is kept
     assert d == (0, 2, 1, 2)
     with pytest.raises(ValueError):
