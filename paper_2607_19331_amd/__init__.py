@@ -1,0 +1,171 @@
+"""MI355X (gfx950) merge/update hot path of ISO and the App. F merges.
+
+Thin Python binding over libiso.so (include/iso.h): functions carry the C names and only
+turn torch tensors into pointers and tables.  Every step of the path runs in the HIP
+library; there is no CPU or PyTorch fallback, and a missing library raises.
+"""
+import ctypes
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence
+
+from . import _lib
+from ._lib import (BF16, F32, MERGE_RAM, MERGE_TA, MERGE_TIES, OP_BLOCKDIAG, OP_MERGE, OP_SIGN, OP_TOPK,
+                   OP_UPDATE_APPLY, OP_UPDATE_FUSED, OP_UPDATE_FUSED_SELECT, OP_UPDATE_SPECTRAL, UPDATE_APPLY,
+                   UPDATE_FUSED, UPDATE_SPECTRAL, IsoSelectDesc)
+
+DESC_BYTES = ctypes.sizeof(IsoSelectDesc)
+
+
+class IsoError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {_lib.load().iso_status_string(status).decode()} (status {status})")
+
+
+@dataclass
+class Entry:
+    """One row of the tensor table: device tensors of one weight matrix."""
+    rows: int
+    cols: int
+    base: Optional[object] = None
+    deltas: List[object] = field(default_factory=list)
+    out: Optional[object] = None
+    k: int = 0
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _table(entries: Sequence[Entry]):
+    arr = (_lib.IsoTensor * max(1, len(entries)))()
+    for j, e in enumerate(entries):
+        if len(e.deltas) > _lib.MAX_K:
+            raise ValueError(f"at most {_lib.MAX_K} deltas per tensor")
+        arr[j].base = _ptr(e.base)
+        for i, d in enumerate(e.deltas):
+            arr[j].deltas[i] = _ptr(d)
+        arr[j].out = _ptr(e.out)
+        arr[j].rows = e.rows
+        arr[j].cols = e.cols
+        arr[j].k = e.k
+    return arr
+
+
+def _ptr_array(xs):
+    if xs is None:
+        return None
+    arr = (ctypes.c_void_p * max(1, len(xs)))()
+    for i, x in enumerate(xs):
+        arr[i] = _ptr(x)
+    return arr
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+def _check(rc, where):
+    if rc != 0:
+        raise IsoError(rc, where)
+
+
+def _ws(ws):
+    return (_ptr(ws), ws.numel() * ws.element_size()) if ws is not None else (None, 0)
+
+
+def iso_workspace_size(op, entries, K, dtype):
+    return _lib.load().iso_workspace_size(op, _table(entries), len(entries), K, dtype)
+
+
+def iso_workspace_size_tsv(entries, K, dtype, rank):
+    return _lib.load().iso_workspace_size_tsv(_table(entries), len(entries), K, dtype, rank)
+
+
+def workspace(op, entries, K, dtype, device="cuda", rank=None):
+    """Allocate a workspace tensor of the size the library asks for (caller-owned)."""
+    import torch
+    n = iso_workspace_size_tsv(entries, K, dtype, rank) if op == OP_BLOCKDIAG else iso_workspace_size(op, entries, K, dtype)
+    ws = torch.empty(max(n, 256) + 256, dtype=torch.uint8, device=device)
+    off = (-ws.data_ptr()) % 256
+    return ws[off:off + max(n, 256)]
+
+
+def iso_topk_mask(entries, K, dtype, desc, mask_bits=None, ws=None, stream=None):
+    wp, wb = _ws(ws)
+    rc = _lib.load().iso_topk_mask(_table(entries), len(entries), K, dtype, _ptr(desc), _ptr_array(mask_bits), wp, wb,
+                                   _stream(stream))
+    _check(rc, "iso_topk_mask")
+
+
+def iso_sign_elect(entries, K, dtype, desc, sign_out, ws=None, stream=None):
+    wp, wb = _ws(ws)
+    rc = _lib.load().iso_sign_elect(_table(entries), len(entries), K, dtype, _ptr(desc), _ptr_array(sign_out), wp, wb,
+                                    _stream(stream))
+    _check(rc, "iso_sign_elect")
+
+
+def iso_merge(entries, K, dtype, mode, desc, lam, eps, tau_out, ws=None, stream=None):
+    wp, wb = _ws(ws)
+    rc = _lib.load().iso_merge(_table(entries), len(entries), K, dtype, mode, _ptr(desc), float(lam), float(eps),
+                               _ptr_array(tau_out), wp, wb, _stream(stream))
+    _check(rc, "iso_merge")
+
+
+def iso_update(entries, K, dtype, mode, merge=MERGE_TIES, lam=1.0, eps=1e-5, desc=None, tau_in=None, sign_out=None,
+               rho_keep=0.9, ridge=1e-12, c_min=0.0, c_max=1.5, coef_out=None, ws=None, stream=None):
+    a = _lib.IsoUpdateArgs()
+    a.mode, a.merge, a.lambda_, a.eps_act = mode, merge, float(lam), float(eps)
+    keep = [_ptr_array(tau_in), _ptr_array(sign_out)]
+    a.desc = _ptr(desc)
+    a.tau_in = ctypes.cast(keep[0], ctypes.c_void_p).value if keep[0] is not None else None
+    a.sign_out = ctypes.cast(keep[1], ctypes.c_void_p).value if keep[1] is not None else None
+    a.rho_keep, a.ridge, a.c_min, a.c_max = float(rho_keep), float(ridge), float(c_min), float(c_max)
+    a.coef_out = _ptr(coef_out)
+    wp, wb = _ws(ws)
+    rc = _lib.load().iso_update(_table(entries), len(entries), K, dtype, ctypes.byref(a), wp, wb, _stream(stream))
+    _check(rc, "iso_update")
+
+
+def iso_blockdiag_project(entries, K, dtype, rank, alpha, delta_hat=None, ws=None, stream=None):
+    wp, wb = _ws(ws)
+    rc = _lib.load().iso_blockdiag_project(_table(entries), len(entries), K, dtype, int(rank), float(alpha),
+                                           _ptr_array(delta_hat), wp, wb, _stream(stream))
+    _check(rc, "iso_blockdiag_project")
+
+
+def iso_k_from_density(n, num, den):
+    return _lib.load().iso_k_from_density(n, num, den)
+
+
+def iso_read_device_status(ws, stream=None):
+    return _lib.load().iso_read_device_status(_ptr(ws), _stream(stream))
+
+
+def iso_status_string(s):
+    return _lib.load().iso_status_string(s).decode()
+
+
+def desc_tensor(n, device="cuda"):
+    """Device buffer for n select descriptors (32 bytes each)."""
+    import torch
+    return torch.empty(n * DESC_BYTES // 8, dtype=torch.int64, device=device)
+
+
+def decode_desc(t):
+    """Host view of descriptors: list of (t_key, key_max, n_above, tie_quota, tie_cutoff)."""
+    import numpy as np
+    a = t.detach().cpu().numpy().view(np.uint8).reshape(-1, DESC_BYTES)
+    out = []
+    for row in a:
+        u32 = row[:8].view(np.uint32)
+        i64 = row[8:].view(np.int64)
+        out.append((int(u32[0]), int(u32[1]), int(i64[0]), int(i64[1]), int(i64[2])))
+    return out

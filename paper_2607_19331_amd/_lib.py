@@ -1,0 +1,69 @@
+"""ctypes view of include/iso.h (argument marshalling only; all work runs in libiso.so)."""
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libiso.so")
+MAX_K = 8
+
+OK, ERR_INVALID_ARG, ERR_ALIGNMENT, ERR_WORKSPACE, ERR_NONFINITE, ERR_HIP, ERR_UNSUPPORTED, ERR_INTERNAL = range(8)
+F32, BF16 = 0, 1
+MERGE_TA, MERGE_TIES, MERGE_RAM = 0, 1, 2
+UPDATE_APPLY, UPDATE_FUSED, UPDATE_SPECTRAL = 0, 1, 2
+(OP_TOPK, OP_SIGN, OP_MERGE, OP_UPDATE_APPLY, OP_UPDATE_FUSED, OP_UPDATE_FUSED_SELECT, OP_UPDATE_SPECTRAL,
+ OP_BLOCKDIAG) = range(8)
+
+SYMBOLS = ["iso_workspace_size", "iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update",
+           "iso_blockdiag_project", "iso_workspace_size_tsv", "iso_k_from_density", "iso_read_device_status",
+           "iso_status_string"]
+
+
+class IsoTensor(ctypes.Structure):
+    _fields_ = [("base", ctypes.c_void_p), ("deltas", ctypes.c_void_p * MAX_K), ("out", ctypes.c_void_p),
+                ("rows", ctypes.c_int64), ("cols", ctypes.c_int64), ("k", ctypes.c_int64)]
+
+
+class IsoSelectDesc(ctypes.Structure):
+    _fields_ = [("t_key", ctypes.c_uint32), ("key_max", ctypes.c_uint32), ("n_above", ctypes.c_int64),
+                ("tie_quota", ctypes.c_int64), ("tie_cutoff", ctypes.c_int64)]
+
+
+class IsoUpdateArgs(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int), ("merge", ctypes.c_int), ("lambda_", ctypes.c_double),
+                ("eps_act", ctypes.c_double), ("desc", ctypes.c_void_p), ("tau_in", ctypes.c_void_p),
+                ("sign_out", ctypes.c_void_p), ("rho_keep", ctypes.c_double), ("ridge", ctypes.c_double),
+                ("c_min", ctypes.c_double), ("c_max", ctypes.c_double), ("coef_out", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load():
+    """Load libiso.so; raises if it has not been built (there is no fallback path)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I, Z, D = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t, ctypes.c_double
+    T = ctypes.POINTER(IsoTensor)
+    L.iso_workspace_size.argtypes = [I, T, I, I, I]
+    L.iso_workspace_size.restype = Z
+    L.iso_topk_mask.argtypes = [T, I, I, I, P, P, P, Z, P]
+    L.iso_sign_elect.argtypes = [T, I, I, I, P, P, P, Z, P]
+    L.iso_merge.argtypes = [T, I, I, I, I, P, D, D, P, P, Z, P]
+    L.iso_update.argtypes = [T, I, I, I, ctypes.POINTER(IsoUpdateArgs), P, Z, P]
+    L.iso_blockdiag_project.argtypes = [T, I, I, I, I, D, P, P, Z, P]
+    L.iso_workspace_size_tsv.argtypes = [T, I, I, I, I]
+    L.iso_workspace_size_tsv.restype = Z
+    L.iso_k_from_density.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64]
+    L.iso_k_from_density.restype = ctypes.c_int64
+    L.iso_read_device_status.argtypes = [P, P]
+    L.iso_status_string.argtypes = [I]
+    L.iso_status_string.restype = ctypes.c_char_p
+    for fn in ("iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update", "iso_blockdiag_project",
+               "iso_read_device_status"):
+        getattr(L, fn).restype = I
+    _lib = L
+    return L

@@ -1,0 +1,424 @@
+// extern "C" entry points of libiso.so: argument checks, workspace layout, tensor-table
+// upload and kernel sequencing on the caller's stream.  Declarations and the meaning
+// of every argument are in include/iso.h.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <vector>
+
+#include "iso.h"
+#include "iso_device.h"
+#include "iso_kernels.h"
+#include "iso_spectral.h"
+
+using namespace iso;
+
+namespace {
+
+constexpr int64_t kTieChunk = 1 << 16;
+constexpr int64_t kMaxElems = 0xFFFFFFFFll;   // per tensor: histogram counters are 32-bit
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+struct Need {
+  bool base = false, deltas = false, out = false, k = false;
+};
+
+iso_status check_table(const iso_tensor* t, int n_t, int K, iso_dtype dt, Need need) {
+  if (n_t < 0 || (n_t > 0 && t == nullptr)) return ISO_ERR_INVALID_ARG;
+  if (K < 1 || K > ISO_MAX_K) return ISO_ERR_INVALID_ARG;
+  if (dt != ISO_F32 && dt != ISO_BF16) return ISO_ERR_INVALID_ARG;
+  for (int j = 0; j < n_t; ++j) {
+    const iso_tensor& x = t[j];
+    if (x.rows < 0 || x.cols < 0) return ISO_ERR_INVALID_ARG;
+    if (x.cols != 0 && x.rows > kMaxElems / x.cols) return ISO_ERR_UNSUPPORTED;
+    const int64_t n = x.rows * x.cols;
+    if (need.k && (x.k < 0 || x.k > n)) return ISO_ERR_INVALID_ARG;
+    if (n == 0) continue;
+    if (need.base) {
+      if (!x.base) return ISO_ERR_INVALID_ARG;
+      if (!aligned16(x.base)) return ISO_ERR_ALIGNMENT;
+    }
+    if (need.deltas)
+      for (int i = 0; i < K; ++i) {
+        if (!x.deltas[i]) return ISO_ERR_INVALID_ARG;
+        if (!aligned16(x.deltas[i])) return ISO_ERR_ALIGNMENT;
+      }
+    if (need.out) {
+      if (!x.out) return ISO_ERR_INVALID_ARG;
+      if (!aligned16(x.out)) return ISO_ERR_ALIGNMENT;
+    }
+  }
+  return ISO_OK;
+}
+
+iso_status check_ptr_array(const void* const* p, int n, bool required) {
+  if (p == nullptr) return required ? ISO_ERR_INVALID_ARG : ISO_OK;
+  for (int i = 0; i < n; ++i) {
+    if (p[i] == nullptr) return ISO_ERR_INVALID_ARG;
+    if (!aligned16(p[i])) return ISO_ERR_ALIGNMENT;
+  }
+  return ISO_OK;
+}
+
+// Workspace regions for one call.
+struct Layout {
+  size_t table = 0, hitem0 = 0, titem0 = 0, ptrs = 0, upload_end = 0;
+  size_t states = 0, hist = 0, tiecnt = 0, desc = 0;
+  size_t spectral = 0;
+  size_t total = 0;
+  int64_t hist_chunk = 0, hist_items = 0, tie_items = 0, tiles = 0;
+  bool select = false;
+};
+
+Layout plan(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
+  Layout L;
+  size_t off = kStatusBytes;
+  L.table = off;
+  off = align_up(off + sizeof(DevTensor) * (size_t)n_t, 256);
+  L.hitem0 = off;
+  off = align_up(off + sizeof(int64_t) * (size_t)n_t, 256);
+  L.titem0 = off;
+  off = align_up(off + sizeof(int64_t) * (size_t)n_t, 256);
+  L.ptrs = off;
+  off = align_up(off + sizeof(void*) * (size_t)n_t * K, 256);
+  L.upload_end = off;
+  int64_t sumnk = 0;
+  for (int j = 0; j < n_t; ++j) sumnk += t[j].rows * t[j].cols * (int64_t)K;
+  const int64_t te = merge_tile_elems(dt);
+  for (int j = 0; j < n_t; ++j) L.tiles += (t[j].rows * t[j].cols + te - 1) / te;
+  L.select = (op == ISO_OP_TOPK || op == ISO_OP_UPDATE_FUSED_SELECT);
+  if (L.select) {
+    L.hist_chunk = hist_chunk_for(sumnk);
+    for (int j = 0; j < n_t; ++j) {
+      const int64_t n = t[j].rows * t[j].cols;
+      L.hist_items += K * ((n + L.hist_chunk - 1) / L.hist_chunk);
+      L.tie_items += K * ((n + kTieChunk - 1) / kTieChunk);
+    }
+    L.states = off;
+    off = align_up(off + sizeof(UnitState) * (size_t)n_t * K, 256);
+    L.hist = off;
+    off = align_up(off + sizeof(uint32_t) * 32768ull * (size_t)n_t * K, 256);
+    L.tiecnt = off;
+    off = align_up(off + sizeof(int32_t) * (size_t)std::max<int64_t>(L.tie_items, 1), 256);
+    L.desc = off;
+    off = align_up(off + sizeof(iso_select_desc) * (size_t)n_t * K, 256);
+  }
+  if (op == ISO_OP_UPDATE_SPECTRAL) {
+    L.spectral = off;
+    off = align_up(off + spectral_workspace_bytes(t, n_t, K), 256);
+  }
+  L.total = off;
+  return L;
+}
+
+struct Upload {
+  std::vector<uint8_t> buf;
+};
+thread_local Upload g_up;   // staging kept alive across calls
+
+// Build [table | hist_item0 | tie_item0 | pointer array] on the host and queue one copy.
+hipError_t upload(const Layout& L, const iso_tensor* t, int n_t, int K, iso_dtype dt, uint8_t* ws,
+                  void* const* aux, void* const* aux2, const void* const* ptrs, int n_ptrs, hipStream_t s) {
+  g_up.buf.assign(L.upload_end - L.table, 0);
+  uint8_t* h = g_up.buf.data();
+  DevTensor* tab = (DevTensor*)(h);
+  int64_t* hi0 = (int64_t*)(h + (L.hitem0 - L.table));
+  int64_t* ti0 = (int64_t*)(h + (L.titem0 - L.table));
+  const void** pp = (const void**)(h + (L.ptrs - L.table));
+  const int64_t te = merge_tile_elems(dt);
+  int64_t tile = 0, hitem = 0, titem = 0;
+  for (int j = 0; j < n_t; ++j) {
+    DevTensor d;
+    std::memset(&d, 0, sizeof d);
+    d.base = t[j].base;
+    for (int i = 0; i < ISO_MAX_K; ++i) d.deltas[i] = (i < K) ? t[j].deltas[i] : nullptr;
+    d.out = t[j].out;
+    d.aux = aux ? aux[j] : nullptr;
+    d.aux2 = aux2 ? aux2[j] : nullptr;
+    d.n = t[j].rows * t[j].cols;
+    d.k = t[j].k;
+    d.tile0 = tile;
+    tab[j] = d;
+    tile += (d.n + te - 1) / te;
+    hi0[j] = hitem;
+    ti0[j] = titem;
+    if (L.select) {
+      hitem += K * ((d.n + L.hist_chunk - 1) / L.hist_chunk);
+      titem += K * ((d.n + kTieChunk - 1) / kTieChunk);
+    }
+  }
+  for (int q = 0; q < n_ptrs; ++q) pp[q] = ptrs[q];
+  return hipMemcpyAsync(ws + L.table, h, g_up.buf.size(), hipMemcpyHostToDevice, s);
+}
+
+iso_status check_ws(const Layout& L, void* ws, size_t ws_bytes) {
+  if (ws == nullptr) return ISO_ERR_WORKSPACE;
+  if (((uintptr_t)ws & 255u) != 0) return ISO_ERR_ALIGNMENT;
+  if (ws_bytes < L.total) return ISO_ERR_WORKSPACE;
+  return ISO_OK;
+}
+
+#define HIP_TRY(x)                               \
+  do {                                           \
+    if ((x) != hipSuccess) return ISO_ERR_HIP;   \
+  } while (0)
+
+SelectPlan select_plan(const Layout& L, uint8_t* ws, int n_t, int K, iso_select_desc* desc) {
+  SelectPlan p;
+  p.tab = (const DevTensor*)(ws + L.table);
+  p.n_t = n_t;
+  p.K = K;
+  p.states = (UnitState*)(ws + L.states);
+  p.hist = (uint32_t*)(ws + L.hist);
+  p.hist_item0 = (const int64_t*)(ws + L.hitem0);
+  p.hist_chunk = L.hist_chunk;
+  p.hist_items = L.hist_items;
+  p.tie_item0 = (const int64_t*)(ws + L.titem0);
+  p.tie_chunk = kTieChunk;
+  p.tie_items = L.tie_items;
+  p.tie_cnt = (int32_t*)(ws + L.tiecnt);
+  p.desc = desc;
+  p.status = (uint32_t*)ws;
+  return p;
+}
+
+hipError_t start_call(uint8_t* ws, hipStream_t s) { return fill_u32((uint32_t*)ws, kStatusBytes / 4, 0u, s); }
+
+hipError_t do_select(const Layout& L, uint8_t* ws, int n_t, int K, iso_dtype dt, iso_select_desc* desc,
+                     hipStream_t s) {
+  hipError_t e = fill_u32((uint32_t*)(ws + L.hist), 32768ll * n_t * K, 0u, s);
+  if (e != hipSuccess) return e;
+  return run_select(select_plan(L, ws, n_t, K, desc), dt, s);
+}
+
+int64_t max_numel(const iso_tensor* t, int n_t) {
+  int64_t m = 0;
+  for (int j = 0; j < n_t; ++j) m = std::max(m, t[j].rows * t[j].cols);
+  return m;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t iso_workspace_size(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
+  if (n_t < 0 || (n_t > 0 && !t) || K < 1 || K > ISO_MAX_K) return 0;
+  if (op < ISO_OP_TOPK || op > ISO_OP_BLOCKDIAG) return 0;
+  for (int j = 0; j < n_t; ++j)
+    if (t[j].rows < 0 || t[j].cols < 0) return 0;
+  if (op == ISO_OP_BLOCKDIAG) return 0;
+  return plan(op, t, n_t, K, dt).total;
+}
+
+iso_status iso_topk_mask(const iso_tensor* t, int n_t, int K, iso_dtype dt, iso_select_desc* desc,
+                         uint32_t* const* mask_bits, void* ws, size_t ws_bytes, void* stream) {
+  Need nd;
+  nd.deltas = true;
+  nd.k = true;
+  iso_status st = check_table(t, n_t, K, dt, nd);
+  if (st != ISO_OK) return st;
+  if (n_t == 0) return ISO_OK;
+  if (desc == nullptr) return ISO_ERR_INVALID_ARG;
+  if (((uintptr_t)desc & 7u) != 0) return ISO_ERR_ALIGNMENT;
+  if (mask_bits != nullptr)
+    for (int q = 0; q < n_t * K; ++q)
+      if (mask_bits[q] == nullptr || ((uintptr_t)mask_bits[q] & 3u) != 0) return ISO_ERR_INVALID_ARG;
+  Layout L = plan(ISO_OP_TOPK, t, n_t, K, dt);
+  if ((st = check_ws(L, ws, ws_bytes)) != ISO_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* w = (uint8_t*)ws;
+  HIP_TRY(start_call(w, s));
+  HIP_TRY(upload(L, t, n_t, K, dt, w, nullptr, nullptr, (const void* const*)mask_bits, mask_bits ? n_t * K : 0, s));
+  HIP_TRY(do_select(L, w, n_t, K, dt, desc, s));
+  if (mask_bits != nullptr)
+    HIP_TRY(run_mask_bits((const DevTensor*)(w + L.table), n_t, K, dt, desc, (uint32_t* const*)(w + L.ptrs),
+                          max_numel(t, n_t), s));
+  return ISO_OK;
+}
+
+iso_status iso_sign_elect(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_select_desc* desc,
+                          int8_t* const* sign_out, void* ws, size_t ws_bytes, void* stream) {
+  Need nd;
+  nd.deltas = true;
+  iso_status st = check_table(t, n_t, K, dt, nd);
+  if (st != ISO_OK) return st;
+  if (n_t == 0) return ISO_OK;
+  if ((st = check_ptr_array((const void* const*)sign_out, n_t, true)) != ISO_OK) return st;
+  Layout L = plan(ISO_OP_SIGN, t, n_t, K, dt);
+  if ((st = check_ws(L, ws, ws_bytes)) != ISO_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* w = (uint8_t*)ws;
+  HIP_TRY(start_call(w, s));
+  HIP_TRY(upload(L, t, n_t, K, dt, w, (void* const*)sign_out, nullptr, nullptr, 0, s));
+  MergePlan mp;
+  mp.tab = (const DevTensor*)(w + L.table);
+  mp.n_t = n_t;
+  mp.K = K;
+  mp.mode = ISO_MERGE_TIES;
+  mp.outs = OUT_SIGN;
+  mp.desc = desc;
+  mp.lambda = 1.0;
+  mp.eps = 0.0;
+  mp.tiles = L.tiles;
+  mp.status = (uint32_t*)w;
+  HIP_TRY(run_merge(mp, dt, s));
+  return ISO_OK;
+}
+
+iso_status iso_merge(const iso_tensor* t, int n_t, int K, iso_dtype dt, iso_merge_mode mode,
+                     const iso_select_desc* desc, double lambda, double eps_act, float* const* tau_out, void* ws,
+                     size_t ws_bytes, void* stream) {
+  Need nd;
+  nd.deltas = true;
+  iso_status st = check_table(t, n_t, K, dt, nd);
+  if (st != ISO_OK) return st;
+  if (mode != ISO_MERGE_TA && mode != ISO_MERGE_TIES && mode != ISO_MERGE_RAM) return ISO_ERR_INVALID_ARG;
+  if (!(lambda == lambda) || !(eps_act == eps_act) || !(eps_act >= 0)) return ISO_ERR_INVALID_ARG;
+  if (n_t == 0) return ISO_OK;
+  if (mode == ISO_MERGE_TIES && desc == nullptr) return ISO_ERR_INVALID_ARG;
+  if ((st = check_ptr_array((const void* const*)tau_out, n_t, true)) != ISO_OK) return st;
+  Layout L = plan(ISO_OP_MERGE, t, n_t, K, dt);
+  if ((st = check_ws(L, ws, ws_bytes)) != ISO_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* w = (uint8_t*)ws;
+  HIP_TRY(start_call(w, s));
+  HIP_TRY(upload(L, t, n_t, K, dt, w, (void* const*)tau_out, nullptr, nullptr, 0, s));
+  MergePlan mp;
+  mp.tab = (const DevTensor*)(w + L.table);
+  mp.n_t = n_t;
+  mp.K = K;
+  mp.mode = mode;
+  mp.outs = OUT_TAU;
+  mp.desc = (mode == ISO_MERGE_TIES) ? desc : nullptr;
+  mp.lambda = lambda;
+  mp.eps = eps_act;
+  mp.tiles = L.tiles;
+  mp.status = (uint32_t*)w;
+  HIP_TRY(run_merge(mp, dt, s));
+  return ISO_OK;
+}
+
+iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_update_args* a, void* ws,
+                      size_t ws_bytes, void* stream) {
+  if (a == nullptr) return ISO_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* w = (uint8_t*)ws;
+  iso_status st;
+  if (a->mode == ISO_UPDATE_APPLY) {
+    Need nd;
+    nd.base = nd.out = true;
+    if ((st = check_table(t, n_t, 1, dt, nd)) != ISO_OK) return st;
+    if (!(a->lambda == a->lambda)) return ISO_ERR_INVALID_ARG;
+    if (n_t == 0) return ISO_OK;
+    if ((st = check_ptr_array((const void* const*)a->tau_in, n_t, true)) != ISO_OK) return st;
+    Layout L = plan(ISO_OP_UPDATE_APPLY, t, n_t, 1, dt);
+    if ((st = check_ws(L, ws, ws_bytes)) != ISO_OK) return st;
+    HIP_TRY(start_call(w, s));
+    HIP_TRY(upload(L, t, n_t, 1, dt, w, (void* const*)a->tau_in, nullptr, nullptr, 0, s));
+    HIP_TRY(run_apply((const DevTensor*)(w + L.table), n_t, dt, a->lambda, L.tiles, (uint32_t*)w, s));
+    return ISO_OK;
+  }
+  if (a->mode == ISO_UPDATE_FUSED) {
+    const bool ties = a->merge == ISO_MERGE_TIES;
+    if (a->merge != ISO_MERGE_TA && !ties && a->merge != ISO_MERGE_RAM) return ISO_ERR_INVALID_ARG;
+    Need nd;
+    nd.base = nd.out = nd.deltas = true;
+    nd.k = ties && a->desc == nullptr;
+    if ((st = check_table(t, n_t, K, dt, nd)) != ISO_OK) return st;
+    if (!(a->lambda == a->lambda) || !(a->eps_act == a->eps_act) || !(a->eps_act >= 0)) return ISO_ERR_INVALID_ARG;
+    if (n_t == 0) return ISO_OK;
+    const bool want_sign = ties && a->sign_out != nullptr;
+    if (want_sign && (st = check_ptr_array((const void* const*)a->sign_out, n_t, true)) != ISO_OK) return st;
+    const bool inner_select = ties && a->desc == nullptr;
+    Layout L = plan(inner_select ? ISO_OP_UPDATE_FUSED_SELECT : ISO_OP_UPDATE_FUSED, t, n_t, K, dt);
+    if ((st = check_ws(L, ws, ws_bytes)) != ISO_OK) return st;
+    HIP_TRY(start_call(w, s));
+    HIP_TRY(upload(L, t, n_t, K, dt, w, nullptr, want_sign ? (void* const*)a->sign_out : nullptr, nullptr, 0, s));
+    const iso_select_desc* desc = a->desc;
+    if (inner_select) {
+      iso_select_desc* dd = (iso_select_desc*)(w + L.desc);
+      HIP_TRY(do_select(L, w, n_t, K, dt, dd, s));
+      desc = dd;
+    }
+    MergePlan mp;
+    mp.tab = (const DevTensor*)(w + L.table);
+    mp.n_t = n_t;
+    mp.K = K;
+    mp.mode = a->merge;
+    mp.outs = OUT_W | (want_sign ? OUT_SIGN : 0);
+    mp.desc = ties ? desc : nullptr;
+    mp.lambda = a->lambda;
+    mp.eps = a->eps_act;
+    mp.tiles = L.tiles;
+    mp.status = (uint32_t*)w;
+    HIP_TRY(run_merge(mp, dt, s));
+    return ISO_OK;
+  }
+  if (a->mode == ISO_UPDATE_SPECTRAL) {
+    Need nd;
+    nd.base = nd.out = nd.deltas = true;
+    if ((st = check_table(t, n_t, K, dt, nd)) != ISO_OK) return st;
+    if (!(a->rho_keep > 0.0 && a->rho_keep <= 1.0) || !(a->ridge >= 0.0) || !(a->c_min <= a->c_max))
+      return ISO_ERR_INVALID_ARG;
+    for (int j = 0; j < n_t; ++j)
+      if (t[j].rows > ISO_SPECTRAL_MAX_DIM || t[j].cols > ISO_SPECTRAL_MAX_DIM) return ISO_ERR_UNSUPPORTED;
+    if (a->coef_out != nullptr && ((uintptr_t)a->coef_out & 7u) != 0) return ISO_ERR_ALIGNMENT;
+    if (n_t == 0) return ISO_OK;
+    Layout L = plan(ISO_OP_UPDATE_SPECTRAL, t, n_t, K, dt);
+    if ((st = check_ws(L, ws, ws_bytes)) != ISO_OK) return st;
+    HIP_TRY(start_call(w, s));
+    SpectralArgs sa;
+    sa.rho_keep = a->rho_keep;
+    sa.ridge = a->ridge;
+    sa.c_min = a->c_min;
+    sa.c_max = a->c_max;
+    sa.coef_out = a->coef_out;
+    return run_spectral(t, n_t, K, dt, sa, w + L.spectral, (uint32_t*)w, s);
+  }
+  return ISO_ERR_INVALID_ARG;
+}
+
+iso_status iso_blockdiag_project(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank, double alpha,
+                                 float* const* delta_hat, void* ws, size_t ws_bytes, void* stream) {
+  (void)t; (void)n_t; (void)K; (void)dt; (void)rank; (void)alpha; (void)delta_hat; (void)ws; (void)ws_bytes;
+  (void)stream;
+  return ISO_ERR_UNSUPPORTED;
+}
+
+size_t iso_workspace_size_tsv(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank) {
+  (void)t; (void)n_t; (void)K; (void)dt; (void)rank;
+  return 0;
+}
+
+int64_t iso_k_from_density(int64_t n, int64_t num, int64_t den) {
+  if (n < 0 || num < 0 || den <= 0 || num > den) return -1;
+  __int128 v = (__int128)2 * n * num + den;
+  return (int64_t)(v / ((__int128)2 * den));
+}
+
+iso_status iso_read_device_status(const void* ws, void* stream) {
+  if (ws == nullptr) return ISO_ERR_INVALID_ARG;
+  if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return ISO_ERR_HIP;
+  uint32_t flags = 0;
+  if (hipMemcpy(&flags, ws, sizeof flags, hipMemcpyDeviceToHost) != hipSuccess) return ISO_ERR_HIP;
+  if (flags & kStatusInternal) return ISO_ERR_INTERNAL;
+  if (flags & kStatusNonFinite) return ISO_ERR_NONFINITE;
+  return ISO_OK;
+}
+
+const char* iso_status_string(iso_status s) {
+  switch (s) {
+    case ISO_OK: return "ok";
+    case ISO_ERR_INVALID_ARG: return "invalid argument";
+    case ISO_ERR_ALIGNMENT: return "pointer not 16-byte aligned";
+    case ISO_ERR_WORKSPACE: return "workspace missing or too small";
+    case ISO_ERR_NONFINITE: return "non-finite input value";
+    case ISO_ERR_HIP: return "HIP runtime error";
+    case ISO_ERR_UNSUPPORTED: return "unsupported shape or option";
+    case ISO_ERR_INTERNAL: return "internal consistency check failed";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,150 @@
+// Internal device-side definitions shared by the libiso kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "iso.h"
+
+namespace iso {
+
+// ---- workspace layout ----------------------------------------------------------------------------
+// [0, 256)            status block (u32 flags)
+// [256, ...)          per-call tables and scratch, each region 256-byte aligned
+constexpr size_t kStatusBytes = 256;
+constexpr uint32_t kStatusNonFinite = 1u;
+constexpr uint32_t kStatusInternal = 2u;   // a kernel found counts that cannot occur; results invalid
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Table entry as the kernels see it.
+struct DevTensor {
+  const void* base;
+  const void* deltas[ISO_MAX_K];
+  void* out;        // weight output (FUSED / APPLY) or nullptr
+  void* aux;        // tau_out (float) / sign_out (int8) / tau_in (float), per entry point
+  void* aux2;       // second optional output (FUSED TIES sign_out)
+  int64_t n;        // elements
+  int64_t k;        // TopKMask count
+  int64_t tile0;    // first tile of this tensor in the launch's tile space
+  int64_t pad;
+};
+static_assert(sizeof(DevTensor) % 16 == 0, "table entry alignment");
+
+// Per (tensor, delta) select state, lives in the workspace.
+struct UnitState {
+  uint32_t prefix;     // key bits fixed so far (final: t_key)
+  uint32_t key_max;    // largest key (atomicMax in the first histogram pass)
+  int64_t k_rem;       // rank still to place inside the current prefix bucket
+  int64_t n_above;     // elements with key strictly above the prefix bucket
+  int64_t bucket;      // elements inside the current prefix bucket
+  int64_t cutoff;      // final tie cutoff
+  int32_t done;        // 1 when the descriptor is final before the tie search
+  int32_t pad[3];
+};
+static_assert(sizeof(UnitState) == 56, "unit state size");
+
+constexpr uint32_t kNoSelectKey = 0xFFFFFFFFu;
+
+// ---- storage-format helpers ----------------------------------------------------------------------
+
+template <int DT> struct Fmt;
+template <> struct Fmt<ISO_BF16> {
+  using bits_t = uint16_t;
+  static constexpr int kPerVec = 8;           // elements per 16-byte vector
+  static constexpr uint32_t kKeyMask = 0x7FFFu;
+  static constexpr int kKeyBits = 15;
+};
+template <> struct Fmt<ISO_F32> {
+  using bits_t = uint32_t;
+  static constexpr int kPerVec = 4;
+  static constexpr uint32_t kKeyMask = 0x7FFFFFFFu;
+  static constexpr int kKeyBits = 31;
+};
+
+// Streaming (read-once / write-once) 16-byte accesses.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld_stream(const uint4* p) {
+  u32x4_t v = __builtin_nontemporal_load((const u32x4_t*)p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ float4 ld_stream(const float4* p) {
+  f32x4_t v = __builtin_nontemporal_load((const f32x4_t*)p);
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void st_stream(uint4 v, uint4* p) {
+  u32x4_t w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, (u32x4_t*)p);
+}
+__device__ __forceinline__ void st_stream(float4 v, float4* p) {
+  f32x4_t w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, (f32x4_t*)p);
+}
+
+__device__ __forceinline__ float f32_from_bits(uint32_t b) { return __uint_as_float(b); }
+__device__ __forceinline__ uint32_t bits_from_f32(float f) { return __float_as_uint(f); }
+
+// bits of element e (0..7) of a 16-byte vector of bf16 held as uint4, widened to fp32 bits
+__device__ __forceinline__ uint32_t bf16_word(const uint4& v, int e) {
+  uint32_t w = (e < 2) ? v.x : (e < 4) ? v.y : (e < 6) ? v.z : v.w;
+  return (e & 1) ? (w & 0xFFFF0000u) : (w << 16);
+}
+
+// binary64 -> bf16 with one round-to-nearest-even step: round to binary32 with
+// round-to-odd (which keeps the information a second rounding needs), then
+// round that to bf16 with round-to-nearest-even.  Round-to-odd to a format
+// with at least two more significand bits than the target makes the double
+// rounding innocuous (Boldo & Melquiond, "Emulation of FMA and correctly
+// rounded sums: proved algorithms using rounding to odd", IEEE TC 2008).
+__device__ __forceinline__ uint32_t f64_to_bf16_rne(double v) {
+  float f = (float)v;                       // round to nearest even
+  uint32_t b = bits_from_f32(f);
+  double back = (double)f;
+  if (back != v) {                          // inexact (NaN compares unequal: keep NaN bits)
+    if (v == v) {
+      if (fabs(back) > fabs(v)) b -= 1u;    // step the magnitude back toward zero: truncation
+      b |= 1u;                              // sticky: odd
+    }
+  }
+  if ((b & 0x7FFFFFFFu) > 0x7F800000u) return (b >> 16) | 0x40u;   // quiet NaN
+  return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ double load_f64(const void* p, int64_t i, int dt) {
+  if (dt == ISO_BF16) return (double)f32_from_bits((uint32_t)((const uint16_t*)p)[i] << 16);
+  return (double)((const float*)p)[i];
+}
+
+// Scalar access for tails.
+template <int DT>
+__device__ __forceinline__ uint32_t elem_bits(const void* p, int64_t i) {
+  if constexpr (DT == ISO_BF16) return (uint32_t)((const uint16_t*)p)[i];
+  else return ((const uint32_t*)p)[i];
+}
+template <int DT>
+__device__ __forceinline__ double bits_to_f64(uint32_t b) {
+  if constexpr (DT == ISO_BF16) return (double)f32_from_bits(b << 16);
+  else return (double)f32_from_bits(b);
+}
+template <int DT>
+__device__ __forceinline__ bool bits_nonfinite(uint32_t b) {
+  if constexpr (DT == ISO_BF16) return (b & 0x7F80u) == 0x7F80u;
+  else return (b & 0x7F800000u) == 0x7F800000u;
+}
+
+__device__ __forceinline__ void flag_status(uint32_t* status, uint32_t f) {
+  __hip_atomic_fetch_or(status, f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Find the tensor owning global tile `tile` (tile0 ascending).
+__device__ __forceinline__ int find_tensor(const DevTensor* tab, int n_t, int64_t tile) {
+  int lo = 0, hi = n_t - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (tab[mid].tile0 <= tile) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+}  // namespace iso

@@ -1,0 +1,448 @@
+// TopKMask selection (App. F, TIES "Trim"): exact k-largest-magnitude selection by
+// radix select over the storage magnitude keys, ties at the threshold broken by
+// flat index.  bf16 keys (15 bits) take one histogram pass; fp32 keys (31 bits)
+// take three (15 + 8 + 8 bits).
+//
+// Per pass, every (tensor, delta) "unit" is cut into chunks; one 1024-thread
+// workgroup per chunk builds a 2^bits-bin histogram in LDS (128 KB for 15 bits)
+// and flushes its nonzero bins to the unit's global histogram with integer
+// atomics (deterministic: counts only).  A resolve kernel (one workgroup per
+// unit) then finds the digit holding the k-th largest key.  If only part of the
+// threshold bucket is kept, a tie pass counts threshold keys per 64K-element
+// chunk and a find kernel walks to the quota-th tie in flat order.
+#include "iso_device.h"
+#include "iso_kernels.h"
+
+namespace iso {
+
+constexpr int kHistThreads = 1024;
+constexpr int kMaxBins = 1 << 15;
+
+// ---- block helpers ------------------------------------------------------------------------------
+
+__device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, 64));
+  return v;
+}
+
+// Inclusive prefix sum over the block (blockDim.x <= 1024, multiple of 64).
+__device__ int64_t block_inclusive_scan(int64_t v, int64_t* sh /* >= 16 */) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int64_t x = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    int64_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sh[wid] = x;
+  __syncthreads();
+  if (wid == 0) {
+    int64_t t = (lane < nw) ? sh[lane] : 0;
+    for (int o = 1; o < 16; o <<= 1) {
+      int64_t y = __shfl_up(t, o, 64);
+      if (lane >= o) t += y;
+    }
+    if (lane < nw) sh[lane] = t;
+  }
+  __syncthreads();
+  int64_t add = (wid > 0) ? sh[wid - 1] : 0;
+  __syncthreads();
+  return x + add;
+}
+
+// ---- unit setup ---------------------------------------------------------------------------------
+
+__global__ void k_select_init(const DevTensor* tab, int n_t, int K, UnitState* st) {
+  int u = blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= n_t * K) return;
+  const DevTensor& T = tab[u / K];
+  UnitState s;
+  s.prefix = 0;
+  s.key_max = 0;
+  s.k_rem = T.k;
+  s.n_above = 0;
+  s.bucket = T.n;
+  s.cutoff = 0;
+  s.done = (T.k == 0) ? 1 : 0;
+  if (T.k == 0) s.prefix = kNoSelectKey;
+  s.pad[0] = s.pad[1] = s.pad[2] = 0;
+  st[u] = s;
+}
+
+// Work item -> (tensor j, delta i, chunk c), items of tensor j laid out delta-major.
+__device__ __forceinline__ void item_of(const int64_t* item0, int n_t, int K, int64_t chunk, const DevTensor* tab,
+                                        int64_t item, int& j, int& i, int64_t& c) {
+  int lo = 0, hi = n_t - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (item0[mid] <= item) lo = mid; else hi = mid - 1;
+  }
+  j = lo;
+  int64_t nch = (tab[j].n + chunk - 1) / chunk;
+  int64_t local = item - item0[j];
+  i = (int)(local / nch);
+  c = local - (int64_t)i * nch;
+}
+
+// ---- histogram pass -----------------------------------------------------------------------------
+
+template <int DT>
+__global__ void __launch_bounds__(kHistThreads) k_hist(const DevTensor* __restrict__ tab, int n_t, int K,
+                                                       const int64_t* __restrict__ item0, int64_t chunk,
+                                                       UnitState* __restrict__ st, uint32_t* __restrict__ hist,
+                                                       int shift, int bits, int first, uint32_t* status) {
+  using F = Fmt<DT>;
+  __shared__ uint32_t lds[kMaxBins];
+  __shared__ uint32_t wmax[16];
+  int j, i;
+  int64_t c;
+  item_of(item0, n_t, K, chunk, tab, blockIdx.x, j, i, c);
+  const int u = j * K + i;
+  const DevTensor& T = tab[j];
+  const bool active = !st[u].done;             // k == 0 units only need key_max from the first pass
+  if (!first && !active) return;               // uniform per block
+  const uint32_t nb = 1u << bits;
+  for (uint32_t b = threadIdx.x; b < nb; b += blockDim.x) lds[b] = 0;
+  __syncthreads();
+
+  const int hs = shift + bits;                 // bits above the digit must match the prefix
+  const uint32_t want = (hs >= 32) ? 0u : (st[u].prefix >> hs);
+  const uint32_t dmask = nb - 1u;
+  const int64_t e0 = c * chunk;
+  const int64_t e1 = min(T.n, e0 + chunk);
+  const typename F::bits_t* p = (const typename F::bits_t*)T.deltas[i];
+  uint32_t kmax = 0;
+
+  auto count = [&](uint32_t key) {
+    if (first) kmax = max(kmax, key);
+    bool match = active && (first || ((key >> hs) == want));
+    uint32_t d = (key >> shift) & dmask;
+    if (match && d != 0u) atomicAdd(&lds[d], 1u);
+  };
+
+  // vector body
+  const int64_t v0 = e0 / F::kPerVec;
+  const int64_t v1 = e1 / F::kPerVec;         // full vectors only
+  const uint4* pv = (const uint4*)p;
+  for (int64_t v = v0 + threadIdx.x; v < v1; v += 4 * blockDim.x) {
+    uint4 a[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      int64_t vv = v + (int64_t)q * blockDim.x;
+      a[q] = (vv < v1) ? ld_stream(pv + vv) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      int64_t vv = v + (int64_t)q * blockDim.x;
+      if (vv >= v1) break;
+      uint32_t w[4] = {a[q].x, a[q].y, a[q].z, a[q].w};
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        if constexpr (DT == ISO_BF16) {
+          count(w[h] & 0x7FFFu);
+          count((w[h] >> 16) & 0x7FFFu);
+        } else {
+          count(w[h] & 0x7FFFFFFFu);
+        }
+      }
+    }
+  }
+  // scalar tail (last chunk of a tensor whose size is not a multiple of the vector width)
+  for (int64_t e = v1 * F::kPerVec + threadIdx.x; e < e1; e += blockDim.x)
+    count(elem_bits<DT>(p, e) & F::kKeyMask);
+  __syncthreads();
+
+  uint32_t* gh = hist + (size_t)u * kMaxBins;
+  if (active) {
+    for (uint32_t b = threadIdx.x; b < nb; b += blockDim.x) {
+      uint32_t cnt = lds[b];
+      if (cnt) atomicAdd(&gh[b], cnt);
+    }
+  }
+  if (first) {
+    uint32_t m = wave_max_u32(kmax);
+    if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t mm = 0;
+      for (int w = 0; w < (int)(blockDim.x >> 6); ++w) mm = max(mm, wmax[w]);
+      atomicMax(&st[u].key_max, mm);
+      uint32_t expfield = (DT == ISO_BF16) ? 0x7F80u : 0x7F800000u;
+      if (mm >= expfield) flag_status(status, kStatusNonFinite);
+    }
+  }
+}
+
+// ---- resolve: pick the digit holding the k_rem-th largest key ------------------------------------
+
+__global__ void __launch_bounds__(kHistThreads) k_resolve(const DevTensor* __restrict__ tab, int K,
+                                                          UnitState* __restrict__ st, uint32_t* __restrict__ hist,
+                                                          int shift, int bits, int last, uint32_t* status) {
+  __shared__ int64_t sh[16];
+  __shared__ int64_t found_d, found_above;
+  const int u = blockIdx.x;
+  UnitState s = st[u];
+  if (s.done) return;
+  const uint32_t nb = 1u << bits;
+  uint32_t* gh = hist + (size_t)u * kMaxBins;
+  const uint32_t per = (nb + blockDim.x - 1) / blockDim.x;   // consecutive bins per thread
+  const uint32_t b0 = threadIdx.x * per;
+  // thread sums of bins >= 1 (bin 0 is reconstructed from the bucket total)
+  int64_t mine = 0;
+  for (uint32_t q = 0; q < per; ++q) {
+    uint32_t b = b0 + q;
+    if (b < nb && b > 0) mine += gh[b];
+  }
+  int64_t incl = block_inclusive_scan(mine, sh);
+  __shared__ int64_t total_nonzero;
+  if (threadIdx.x == blockDim.x - 1) total_nonzero = incl;
+  if (threadIdx.x == 0) { found_d = -1; found_above = 0; }
+  __syncthreads();
+  const int64_t zeros = s.bucket - total_nonzero;
+  // suffix (count of bins strictly above this thread's range)
+  const int64_t above_me = total_nonzero - incl;
+  const int64_t need = s.k_rem;                       // 1 <= need <= bucket
+  int64_t run = above_me;
+  for (int q = (int)per - 1; q >= 0; --q) {
+    uint32_t b = b0 + (uint32_t)q;
+    if (b >= nb) continue;
+    int64_t h = (b == 0) ? zeros : (int64_t)gh[b];
+    if (run < need && run + h >= need) { found_d = b; found_above = run; }
+    run += h;
+  }
+  __syncthreads();
+  // found_d < 0 would mean inconsistent counts (cannot happen for 1 <= k_rem <= bucket); never index with it
+  const int64_t d = found_d < 0 ? 0 : found_d;
+  if (found_d < 0 && threadIdx.x == 0) flag_status(status, kStatusInternal);
+  const int64_t h_d = (d == 0) ? zeros : (int64_t)gh[d];
+  __syncthreads();
+  // self-clean the histogram for the next pass / next call
+  for (uint32_t q = 0; q < per; ++q) {
+    uint32_t b = b0 + q;
+    if (b < nb) gh[b] = 0;
+  }
+  if (threadIdx.x == 0) {
+    s.prefix |= (uint32_t)d << shift;
+    s.n_above += found_above;
+    s.k_rem = need - found_above;
+    s.bucket = h_d;
+    if (last) {
+      const DevTensor& T = tab[u / K];
+      if (s.k_rem == s.bucket) { s.cutoff = T.n; s.done = 1; }
+    }
+    st[u] = s;
+  }
+}
+
+// ---- ties: count threshold keys per chunk, then walk to the quota-th one -------------------------
+
+template <int DT>
+__global__ void __launch_bounds__(256) k_tie_count(const DevTensor* __restrict__ tab, int n_t, int K,
+                                                   const int64_t* __restrict__ item0, int64_t chunk,
+                                                   const UnitState* __restrict__ st, int32_t* __restrict__ cnt) {
+  using F = Fmt<DT>;
+  __shared__ int64_t sh[4];
+  int j, i;
+  int64_t c;
+  item_of(item0, n_t, K, chunk, tab, blockIdx.x, j, i, c);
+  const int u = j * K + i;
+  if (st[u].done) return;
+  const uint32_t tk = st[u].prefix;
+  const DevTensor& T = tab[j];
+  const int64_t e0 = c * chunk, e1 = min(T.n, e0 + chunk);
+  const void* p = T.deltas[i];
+  int64_t m = 0;
+  const int64_t v0 = e0 / F::kPerVec, v1 = e1 / F::kPerVec;
+  for (int64_t v = v0 + threadIdx.x; v < v1; v += blockDim.x) {
+    uint4 a = ld_stream((const uint4*)p + v);
+    uint32_t w[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      if constexpr (DT == ISO_BF16) {
+        m += ((w[h] & 0x7FFFu) == tk) + (((w[h] >> 16) & 0x7FFFu) == tk);
+      } else {
+        m += ((w[h] & 0x7FFFFFFFu) == tk);
+      }
+    }
+  }
+  for (int64_t e = v1 * F::kPerVec + threadIdx.x; e < e1; e += blockDim.x)
+    m += ((elem_bits<DT>(p, e) & F::kKeyMask) == tk);
+  m = wave_sum_i64(m);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) cnt[blockIdx.x] = (int32_t)(sh[0] + sh[1] + sh[2] + sh[3]);
+}
+
+template <int DT>
+__global__ void __launch_bounds__(kHistThreads) k_tie_find(const DevTensor* __restrict__ tab, int K,
+                                                           const int64_t* __restrict__ item0, int64_t chunk,
+                                                           UnitState* __restrict__ st,
+                                                           const int32_t* __restrict__ cnt, uint32_t* cnt_status) {
+  using F = Fmt<DT>;
+  __shared__ int64_t sh[16];
+  __shared__ int64_t s_chunk, s_before;
+  __shared__ int64_t s_idx;
+  const int u = blockIdx.x;
+  if (st[u].done) return;
+  const int j = u / K, i = u % K;
+  const DevTensor& T = tab[j];
+  const int64_t nch = (T.n + chunk - 1) / chunk;
+  const int32_t* cu = cnt + item0[j] + (int64_t)i * nch;
+  const int64_t quota = st[u].k_rem;
+  const uint32_t tk = st[u].prefix;
+  if (threadIdx.x == 0) { s_chunk = -1; s_before = 0; s_idx = -1; }
+  __syncthreads();
+  // 1) chunk that holds the quota-th tie
+  int64_t base = 0;
+  for (int64_t c0 = 0; c0 < nch; c0 += blockDim.x) {
+    int64_t c = c0 + threadIdx.x;
+    int64_t v = (c < nch) ? cu[c] : 0;
+    int64_t incl = block_inclusive_scan(v, sh);
+    int64_t excl = incl - v;
+    if (c < nch && base + excl < quota && base + incl >= quota) { s_chunk = c; s_before = base + excl; }
+    __shared__ int64_t s_tot;
+    if (threadIdx.x == blockDim.x - 1) s_tot = incl;
+    __syncthreads();
+    base += s_tot;
+    __syncthreads();
+    if (s_chunk >= 0) break;
+  }
+  __syncthreads();
+  if (s_chunk < 0) {                                  // inconsistent tie counts: never walk out of range
+    if (threadIdx.x == 0) { st[u].cutoff = T.n; st[u].done = 1; flag_status(cnt_status, kStatusInternal); }
+    return;
+  }
+  const int64_t c = s_chunk;
+  int64_t want = quota - s_before;                    // 1-based rank inside the chunk
+  // 2) walk the chunk in flat order
+  const void* p = T.deltas[i];
+  const int64_t e0 = c * chunk, e1 = min(T.n, e0 + chunk);
+  int64_t seen = 0;
+  for (int64_t b = e0; b < e1; b += blockDim.x) {
+    int64_t e = b + threadIdx.x;
+    int64_t tie = (e < e1) ? ((elem_bits<DT>(p, e) & F::kKeyMask) == tk) : 0;
+    int64_t incl = block_inclusive_scan(tie, sh);
+    if (tie && seen + incl == want) s_idx = e;
+    __shared__ int64_t s_tot2;
+    if (threadIdx.x == blockDim.x - 1) s_tot2 = incl;
+    __syncthreads();
+    seen += s_tot2;
+    __syncthreads();
+    if (s_idx >= 0) break;
+  }
+  if (threadIdx.x == 0) {
+    if (s_idx < 0) flag_status(cnt_status, kStatusInternal);
+    st[u].cutoff = (s_idx < 0) ? T.n : s_idx + 1;
+    st[u].done = 1;
+  }
+}
+
+__global__ void k_emit_desc(const UnitState* __restrict__ st, int n_units, iso_select_desc* __restrict__ desc) {
+  int u = blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= n_units) return;
+  UnitState s = st[u];
+  iso_select_desc d;
+  d.t_key = s.prefix;
+  d.key_max = s.key_max;
+  if (s.prefix == kNoSelectKey) {
+    d.n_above = 0; d.tie_quota = 0; d.tie_cutoff = 0;
+  } else {
+    d.n_above = s.n_above; d.tie_quota = s.k_rem; d.tie_cutoff = s.cutoff;
+  }
+  desc[u] = d;
+}
+
+// ---- optional bitset output ---------------------------------------------------------------------
+
+template <int DT>
+__global__ void __launch_bounds__(256) k_mask_bits(const DevTensor* __restrict__ tab, int n_t, int K,
+                                                   const iso_select_desc* __restrict__ desc,
+                                                   uint32_t* const* __restrict__ bits_out, int64_t words_per_block) {
+  using F = Fmt<DT>;
+  const int u = blockIdx.y;
+  const int j = u / K, i = u % K;
+  const DevTensor& T = tab[j];
+  const iso_select_desc d = desc[u];
+  const int64_t nw = (T.n + 31) / 32;
+  uint32_t* out = bits_out[u];
+  const void* p = T.deltas[i];
+  for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < nw; w += (int64_t)gridDim.x * blockDim.x) {
+    uint32_t m = 0;
+    for (int b = 0; b < 32; ++b) {
+      int64_t e = w * 32 + b;
+      if (e >= T.n) break;
+      uint32_t key = elem_bits<DT>(p, e) & F::kKeyMask;
+      bool sel = (d.t_key != kNoSelectKey) && (key > d.t_key || (key == d.t_key && e < d.tie_cutoff));
+      m |= (uint32_t)sel << b;
+    }
+    out[w] = m;
+  }
+  (void)n_t;
+  (void)words_per_block;
+}
+
+__global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+// ---- host-side launch sequence ------------------------------------------------------------------
+
+int64_t hist_chunk_for(int64_t total_elems_times_k) {
+  int64_t c = 1 << 16;
+  while (c < (1 << 20) && total_elems_times_k / c > 2048) c <<= 1;
+  return c;
+}
+
+hipError_t fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
+  k_fill_u32<<<(unsigned)blocks, 256, 0, s>>>(p, n, v);
+  return hipGetLastError();
+}
+
+template <int DT>
+static hipError_t run_select_t(const SelectPlan& pl, hipStream_t s) {
+  const int nu = pl.n_t * pl.K;
+  k_select_init<<<(nu + 255) / 256, 256, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.states);
+  struct Pass { int shift, bits; };
+  const Pass bf[1] = {{0, 15}};
+  const Pass f32[3] = {{16, 15}, {8, 8}, {0, 8}};
+  const Pass* ps = (DT == ISO_BF16) ? bf : f32;
+  const int np = (DT == ISO_BF16) ? 1 : 3;
+  for (int q = 0; q < np; ++q) {
+    if (pl.hist_items > 0)
+      k_hist<DT><<<(unsigned)pl.hist_items, kHistThreads, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.hist_item0, pl.hist_chunk,
+                                                                  pl.states, pl.hist, ps[q].shift, ps[q].bits,
+                                                                  q == 0, pl.status);
+    k_resolve<<<nu, kHistThreads, 0, s>>>(pl.tab, pl.K, pl.states, pl.hist, ps[q].shift, ps[q].bits, q == np - 1,
+                                          pl.status);
+  }
+  if (pl.tie_items > 0)
+    k_tie_count<DT><<<(unsigned)pl.tie_items, 256, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.tie_item0, pl.tie_chunk,
+                                                           pl.states, pl.tie_cnt);
+  k_tie_find<DT><<<nu, kHistThreads, 0, s>>>(pl.tab, pl.K, pl.tie_item0, pl.tie_chunk, pl.states, pl.tie_cnt,
+                                              pl.status);
+  k_emit_desc<<<(nu + 255) / 256, 256, 0, s>>>(pl.states, nu, pl.desc);
+  return hipGetLastError();
+}
+
+hipError_t run_select(const SelectPlan& pl, int dt, hipStream_t s) {
+  return dt == ISO_BF16 ? run_select_t<ISO_BF16>(pl, s) : run_select_t<ISO_F32>(pl, s);
+}
+
+hipError_t run_mask_bits(const DevTensor* tab, int n_t, int K, int dt, const iso_select_desc* desc,
+                         uint32_t* const* bits_dev, int64_t max_n, hipStream_t s) {
+  const int nu = n_t * K;
+  int64_t nw = (max_n + 31) / 32;
+  unsigned gx = (unsigned)std::max<int64_t>(1, std::min<int64_t>((nw + 255) / 256, 2048));
+  dim3 grid(gx, nu);
+  if (dt == ISO_BF16) k_mask_bits<ISO_BF16><<<grid, 256, 0, s>>>(tab, n_t, K, desc, bits_dev, 0);
+  else k_mask_bits<ISO_F32><<<grid, 256, 0, s>>>(tab, n_t, K, desc, bits_dev, 0);
+  return hipGetLastError();
+}
+
+}  // namespace iso

@@ -1,0 +1,20 @@
+// ISO-Merger (Algorithm 1) on the GPU in binary64: host-side launcher (internal).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "iso.h"
+
+namespace iso {
+
+struct SpectralArgs {
+  double rho_keep, ridge, c_min, c_max;
+  double* coef_out;   // n_t*K device doubles or nullptr
+};
+
+size_t spectral_workspace_bytes(const iso_tensor* t, int n_t, int K);
+iso_status run_spectral(const iso_tensor* t, int n_t, int K, iso_dtype dt, const SpectralArgs& a, uint8_t* ws,
+                        uint32_t* status, hipStream_t s);
+
+}  // namespace iso
