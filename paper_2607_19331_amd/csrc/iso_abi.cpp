@@ -16,6 +16,9 @@ using namespace iso;
 namespace {
 
 constexpr int64_t kTieChunk = 1 << 16;
+// Per-chunk histograms let the tie search skip a second read of the deltas; above this
+// size the library counts ties with an extra pass instead.
+constexpr size_t kChunkHistBudget = 16ull << 30;
 constexpr int64_t kMaxElems = 0xFFFFFFFFll;   // per tensor: histogram counters are 32-bit
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
@@ -64,11 +67,11 @@ iso_status check_ptr_array(const void* const* p, int n, bool required) {
 // Workspace regions for one call.
 struct Layout {
   size_t table = 0, hitem0 = 0, titem0 = 0, ptrs = 0, upload_end = 0;
-  size_t states = 0, hist = 0, tiecnt = 0, desc = 0;
+  size_t states = 0, hist = 0, tiecnt = 0, desc = 0, chunk_hist = 0;
   size_t spectral = 0;
   size_t total = 0;
   int64_t hist_chunk = 0, hist_items = 0, tie_items = 0, tiles = 0;
-  bool select = false;
+  bool select = false, use_chunk_hist = false;
 };
 
 Layout plan(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
@@ -99,8 +102,15 @@ Layout plan(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
     off = align_up(off + sizeof(UnitState) * (size_t)n_t * K, 256);
     L.hist = off;
     off = align_up(off + sizeof(uint32_t) * 32768ull * (size_t)n_t * K, 256);
-    L.tiecnt = off;
-    off = align_up(off + sizeof(int32_t) * (size_t)std::max<int64_t>(L.tie_items, 1), 256);
+    const size_t ch_bytes = sizeof(uint32_t) * ((size_t)1 << select_last_bits(dt)) * (size_t)L.hist_items;
+    L.use_chunk_hist = ch_bytes <= kChunkHistBudget;
+    if (L.use_chunk_hist) {
+      L.chunk_hist = off;
+      off = align_up(off + ch_bytes, 256);
+    } else {
+      L.tiecnt = off;
+      off = align_up(off + sizeof(int32_t) * (size_t)std::max<int64_t>(L.tie_items, 1), 256);
+    }
     L.desc = off;
     off = align_up(off + sizeof(iso_select_desc) * (size_t)n_t * K, 256);
   }
@@ -177,7 +187,8 @@ SelectPlan select_plan(const Layout& L, uint8_t* ws, int n_t, int K, iso_select_
   p.tie_item0 = (const int64_t*)(ws + L.titem0);
   p.tie_chunk = kTieChunk;
   p.tie_items = L.tie_items;
-  p.tie_cnt = (int32_t*)(ws + L.tiecnt);
+  p.tie_cnt = L.use_chunk_hist ? nullptr : (int32_t*)(ws + L.tiecnt);
+  p.chunk_hist = L.use_chunk_hist ? (uint32_t*)(ws + L.chunk_hist) : nullptr;
   p.desc = desc;
   p.status = (uint32_t*)ws;
   return p;

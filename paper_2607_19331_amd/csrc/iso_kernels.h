@@ -20,7 +20,8 @@ struct SelectPlan {
   int64_t hist_chunk, hist_items;
   const int64_t* tie_item0;     // n_t prefix of K*ceil(n/tie_chunk)
   int64_t tie_chunk, tie_items;
-  int32_t* tie_cnt;             // tie_items
+  int32_t* tie_cnt;             // tie_items (used when chunk_hist is null)
+  uint32_t* chunk_hist;         // hist_items * 2^last_bits per-chunk histograms of the last pass, or null
   iso_select_desc* desc;        // n_t*K, device
   uint32_t* status;
 };
@@ -28,6 +29,7 @@ struct SelectPlan {
 int64_t hist_chunk_for(int64_t total_elems_times_k);
 hipError_t fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 hipError_t run_select(const SelectPlan& pl, int dt, hipStream_t s);
+int select_last_bits(int dt);
 hipError_t run_mask_bits(const DevTensor* tab, int n_t, int K, int dt, const iso_select_desc* desc,
                          uint32_t* const* bits_dev, int64_t max_n, hipStream_t s);
 

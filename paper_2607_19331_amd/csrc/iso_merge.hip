@@ -24,7 +24,8 @@
 namespace iso {
 
 constexpr int kMergeThreads = 256;
-constexpr int kMergeVPT = 2;   // 16-byte vectors per thread per array in one tile
+constexpr int kMergeVPT = 2;          // 16-byte vectors per thread per array in one tile
+constexpr int64_t kMergeMaxGrid = 0;  // 0: one block per tile; else blocks loop over tiles
 
 int64_t merge_tile_elems(int dt) {
   return (int64_t)kMergeThreads * kMergeVPT * (dt == ISO_BF16 ? Fmt<ISO_BF16>::kPerVec : Fmt<ISO_F32>::kPerVec);
@@ -176,7 +177,7 @@ __device__ __forceinline__ uint32_t round_out(double v) {
   else return bits_from_f32((float)v);
 }
 
-template <int DT, int K, int MODE, int OUTS, bool FAST, bool STRADDLE>
+template <int DT, int K, int MODE, int OUTS, int VPT, bool FAST, bool STRADDLE>
 __device__ __forceinline__ void merge_body(const DevTensor& T, int64_t vbeg, const TileThr<K>& th, double lambda,
                                            double eps, uint32_t& kacc, uint32_t& wacc) {
   using F = Fmt<DT>;
@@ -184,7 +185,7 @@ __device__ __forceinline__ void merge_body(const DevTensor& T, int64_t vbeg, con
   const int64_t n = T.n;
   const int64_t nvec = n / E;
 #pragma unroll
-  for (int q = 0; q < kMergeVPT; ++q) {
+  for (int q = 0; q < VPT; ++q) {
     const int64_t vi = vbeg + (int64_t)q * kMergeThreads + threadIdx.x;
     if (vi < nvec) {
       uint4 dv[K];
@@ -266,14 +267,13 @@ __device__ __forceinline__ void merge_body(const DevTensor& T, int64_t vbeg, con
   }
 }
 
-template <int DT, int K, int MODE, int OUTS>
-__global__ void __launch_bounds__(kMergeThreads) k_merge(const DevTensor* __restrict__ tab, int n_t,
-                                                         const iso_select_desc* __restrict__ desc, double lambda,
-                                                         double eps, uint32_t* status) {
+template <int DT, int K, int MODE, int OUTS, int VPT>
+__device__ __forceinline__ void merge_tile(const DevTensor* __restrict__ tab, int n_t,
+                                           const iso_select_desc* __restrict__ desc, double lambda, double eps,
+                                           uint32_t* status, int64_t tile) {
   using F = Fmt<DT>;
   constexpr int E = F::kPerVec;
-  constexpr int64_t TV = (int64_t)kMergeThreads * kMergeVPT;    // vectors per tile
-  const int64_t tile = blockIdx.x;
+  constexpr int64_t TV = (int64_t)kMergeThreads * VPT;    // vectors per tile
   const int j = find_tensor(tab, n_t, tile);
   const DevTensor& T = tab[j];
   const int64_t vbeg = (tile - T.tile0) * TV;
@@ -319,14 +319,22 @@ __global__ void __launch_bounds__(kMergeThreads) k_merge(const DevTensor* __rest
   constexpr bool kHasFast = (DT == ISO_BF16) && (MODE == ISO_MERGE_TIES);
   if (kHasFast && fast) {
     if constexpr (kHasFast) {
-      if (straddle) merge_body<DT, K, MODE, OUTS, true, true>(T, vbeg, th, lambda, eps, kacc, wacc);
-      else merge_body<DT, K, MODE, OUTS, true, false>(T, vbeg, th, lambda, eps, kacc, wacc);
+      if (straddle) merge_body<DT, K, MODE, OUTS, VPT, true, true>(T, vbeg, th, lambda, eps, kacc, wacc);
+      else merge_body<DT, K, MODE, OUTS, VPT, true, false>(T, vbeg, th, lambda, eps, kacc, wacc);
     }
   } else {
-    if (straddle) merge_body<DT, K, MODE, OUTS, false, true>(T, vbeg, th, lambda, eps, kacc, wacc);
-    else merge_body<DT, K, MODE, OUTS, false, false>(T, vbeg, th, lambda, eps, kacc, wacc);
+    if (straddle) merge_body<DT, K, MODE, OUTS, VPT, false, true>(T, vbeg, th, lambda, eps, kacc, wacc);
+    else merge_body<DT, K, MODE, OUTS, VPT, false, false>(T, vbeg, th, lambda, eps, kacc, wacc);
   }
   if (kacc >= expfield || wacc >= expfield) flag_status(status, kStatusNonFinite);
+}
+
+template <int DT, int K, int MODE, int OUTS, int VPT>
+__global__ void __launch_bounds__(kMergeThreads) k_merge(const DevTensor* __restrict__ tab, int n_t,
+                                                         const iso_select_desc* __restrict__ desc, double lambda,
+                                                         double eps, uint32_t* status, int64_t tiles) {
+  for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x)
+    merge_tile<DT, K, MODE, OUTS, VPT>(tab, n_t, desc, lambda, eps, status, tile);
 }
 
 // ---- APPLY: out = round(w0 + lambda * tau_in) ----------------------------------------------------
@@ -395,8 +403,9 @@ __global__ void __launch_bounds__(kMergeThreads) k_apply(const DevTensor* __rest
 
 template <int DT, int K, int MODE, int OUTS>
 static void launch_merge(const MergePlan& pl, hipStream_t s) {
-  k_merge<DT, K, MODE, OUTS><<<(unsigned)pl.tiles, kMergeThreads, 0, s>>>(pl.tab, pl.n_t, pl.desc, pl.lambda, pl.eps,
-                                                                         pl.status);
+  const int64_t grid = (kMergeMaxGrid > 0) ? std::min(pl.tiles, kMergeMaxGrid) : pl.tiles;
+  k_merge<DT, K, MODE, OUTS, kMergeVPT><<<(unsigned)grid, kMergeThreads, 0, s>>>(pl.tab, pl.n_t, pl.desc, pl.lambda,
+                                                                                 pl.eps, pl.status, pl.tiles);
 }
 
 template <int DT, int K, int MODE>

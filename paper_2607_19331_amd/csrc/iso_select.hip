@@ -88,15 +88,20 @@ __device__ __forceinline__ void item_of(const int64_t* item0, int n_t, int K, in
 }
 
 // ---- histogram pass -----------------------------------------------------------------------------
+// With `dump` set (last pass only), the block also stores its chunk histogram (bin 0 =
+// in-bucket entries whose digit is 0) so ties can later be located without another read.
 
 template <int DT>
 __global__ void __launch_bounds__(kHistThreads) k_hist(const DevTensor* __restrict__ tab, int n_t, int K,
                                                        const int64_t* __restrict__ item0, int64_t chunk,
                                                        UnitState* __restrict__ st, uint32_t* __restrict__ hist,
-                                                       int shift, int bits, int first, uint32_t* status) {
+                                                       int shift, int bits, int first, uint32_t* status,
+                                                       uint32_t* __restrict__ dump) {
   using F = Fmt<DT>;
+  constexpr int U = 8;                         // 16-byte loads in flight per thread
   __shared__ uint32_t lds[kMaxBins];
   __shared__ uint32_t wmax[16];
+  __shared__ uint32_t wzero[16];
   int j, i;
   int64_t c;
   item_of(item0, n_t, K, chunk, tab, blockIdx.x, j, i, c);
@@ -114,28 +119,28 @@ __global__ void __launch_bounds__(kHistThreads) k_hist(const DevTensor* __restri
   const int64_t e0 = c * chunk;
   const int64_t e1 = min(T.n, e0 + chunk);
   const typename F::bits_t* p = (const typename F::bits_t*)T.deltas[i];
-  uint32_t kmax = 0;
+  uint32_t kmax = 0, nzero = 0;
 
   auto count = [&](uint32_t key) {
     if (first) kmax = max(kmax, key);
     bool match = active && (first || ((key >> hs) == want));
     uint32_t d = (key >> shift) & dmask;
     if (match && d != 0u) atomicAdd(&lds[d], 1u);
+    nzero += (match && d == 0u);
   };
 
-  // vector body
   const int64_t v0 = e0 / F::kPerVec;
   const int64_t v1 = e1 / F::kPerVec;         // full vectors only
   const uint4* pv = (const uint4*)p;
-  for (int64_t v = v0 + threadIdx.x; v < v1; v += 4 * blockDim.x) {
-    uint4 a[4];
+  for (int64_t v = v0 + threadIdx.x; v < v1; v += U * blockDim.x) {
+    uint4 a[U];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < U; ++q) {
       int64_t vv = v + (int64_t)q * blockDim.x;
       a[q] = (vv < v1) ? ld_stream(pv + vv) : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < U; ++q) {
       int64_t vv = v + (int64_t)q * blockDim.x;
       if (vv >= v1) break;
       uint32_t w[4] = {a[q].x, a[q].y, a[q].z, a[q].w};
@@ -153,13 +158,24 @@ __global__ void __launch_bounds__(kHistThreads) k_hist(const DevTensor* __restri
   // scalar tail (last chunk of a tensor whose size is not a multiple of the vector width)
   for (int64_t e = v1 * F::kPerVec + threadIdx.x; e < e1; e += blockDim.x)
     count(elem_bits<DT>(p, e) & F::kKeyMask);
+  uint32_t zsum = 0;
+  if (dump != nullptr) {
+    uint32_t z = nzero;
+    for (int o = 32; o > 0; o >>= 1) z += (uint32_t)__shfl_xor((int)z, o, 64);
+    if ((threadIdx.x & 63) == 0) wzero[threadIdx.x >> 6] = z;
+  }
   __syncthreads();
+  if (dump != nullptr) {
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) zsum += wzero[w];
+  }
 
   uint32_t* gh = hist + (size_t)u * kMaxBins;
   if (active) {
+    uint32_t* dp = (dump != nullptr) ? dump + (size_t)blockIdx.x * nb : nullptr;
     for (uint32_t b = threadIdx.x; b < nb; b += blockDim.x) {
       uint32_t cnt = lds[b];
       if (cnt) atomicAdd(&gh[b], cnt);
+      if (dp) dp[b] = (b == 0) ? zsum : cnt;
     }
   }
   if (first) {
@@ -181,50 +197,50 @@ __global__ void __launch_bounds__(kHistThreads) k_hist(const DevTensor* __restri
 __global__ void __launch_bounds__(kHistThreads) k_resolve(const DevTensor* __restrict__ tab, int K,
                                                           UnitState* __restrict__ st, uint32_t* __restrict__ hist,
                                                           int shift, int bits, int last, uint32_t* status) {
+  __shared__ uint32_t sbin[kMaxBins];
   __shared__ int64_t sh[16];
   __shared__ int64_t found_d, found_above;
+  __shared__ int64_t total_nonzero;
   const int u = blockIdx.x;
   UnitState s = st[u];
   if (s.done) return;
   const uint32_t nb = 1u << bits;
   uint32_t* gh = hist + (size_t)u * kMaxBins;
+  // coalesced copy to LDS, clearing the global bins for the next pass / call
+  for (uint32_t b = threadIdx.x; b < nb; b += blockDim.x) {
+    sbin[b] = gh[b];
+    gh[b] = 0;
+  }
+  if (threadIdx.x == 0) { found_d = -1; found_above = 0; }
+  __syncthreads();
   const uint32_t per = (nb + blockDim.x - 1) / blockDim.x;   // consecutive bins per thread
   const uint32_t b0 = threadIdx.x * per;
   // thread sums of bins >= 1 (bin 0 is reconstructed from the bucket total)
   int64_t mine = 0;
   for (uint32_t q = 0; q < per; ++q) {
     uint32_t b = b0 + q;
-    if (b < nb && b > 0) mine += gh[b];
+    if (b < nb && b > 0) mine += sbin[b];
   }
   int64_t incl = block_inclusive_scan(mine, sh);
-  __shared__ int64_t total_nonzero;
   if (threadIdx.x == blockDim.x - 1) total_nonzero = incl;
-  if (threadIdx.x == 0) { found_d = -1; found_above = 0; }
   __syncthreads();
   const int64_t zeros = s.bucket - total_nonzero;
-  // suffix (count of bins strictly above this thread's range)
-  const int64_t above_me = total_nonzero - incl;
-  const int64_t need = s.k_rem;                       // 1 <= need <= bucket
+  const int64_t above_me = total_nonzero - incl;       // entries in bins above this thread's range
+  const int64_t need = s.k_rem;                        // 1 <= need <= bucket
   int64_t run = above_me;
   for (int q = (int)per - 1; q >= 0; --q) {
     uint32_t b = b0 + (uint32_t)q;
     if (b >= nb) continue;
-    int64_t h = (b == 0) ? zeros : (int64_t)gh[b];
+    int64_t h = (b == 0) ? zeros : (int64_t)sbin[b];
     if (run < need && run + h >= need) { found_d = b; found_above = run; }
     run += h;
   }
   __syncthreads();
   // found_d < 0 would mean inconsistent counts (cannot happen for 1 <= k_rem <= bucket); never index with it
   const int64_t d = found_d < 0 ? 0 : found_d;
-  if (found_d < 0 && threadIdx.x == 0) flag_status(status, kStatusInternal);
-  const int64_t h_d = (d == 0) ? zeros : (int64_t)gh[d];
-  __syncthreads();
-  // self-clean the histogram for the next pass / next call
-  for (uint32_t q = 0; q < per; ++q) {
-    uint32_t b = b0 + q;
-    if (b < nb) gh[b] = 0;
-  }
   if (threadIdx.x == 0) {
+    if (found_d < 0) flag_status(status, kStatusInternal);
+    const int64_t h_d = (d == 0) ? zeros : (int64_t)sbin[d];
     s.prefix |= (uint32_t)d << shift;
     s.n_above += found_above;
     s.k_rem = need - found_above;
@@ -234,6 +250,90 @@ __global__ void __launch_bounds__(kHistThreads) k_resolve(const DevTensor* __res
       if (s.k_rem == s.bucket) { s.cutoff = T.n; s.done = 1; }
     }
     st[u] = s;
+  }
+}
+
+// ---- ties from the chunk histograms: prefix over chunks, then one walk inside a chunk -----------
+
+template <int DT>
+__global__ void __launch_bounds__(kHistThreads) k_tie_find_dump(const DevTensor* __restrict__ tab, int K,
+                                                                const int64_t* __restrict__ item0, int64_t chunk,
+                                                                UnitState* __restrict__ st,
+                                                                const uint32_t* __restrict__ dump, int bits,
+                                                                uint32_t* status) {
+  using F = Fmt<DT>;
+  __shared__ int64_t sh[16];
+  __shared__ int64_t s_chunk, s_before, s_seg, s_segbefore, s_idx, s_tot;
+  const int u = blockIdx.x;
+  if (st[u].done) return;
+  const int j = u / K, i = u % K;
+  const DevTensor& T = tab[j];
+  const uint32_t nb = 1u << bits;
+  const int64_t nch = (T.n + chunk - 1) / chunk;
+  const int64_t first_item = item0[j] + (int64_t)i * nch;
+  const int64_t quota = st[u].k_rem;
+  const uint32_t tk = st[u].prefix;
+  const uint32_t digit = tk & (nb - 1u);
+  if (threadIdx.x == 0) { s_chunk = -1; s_before = 0; s_seg = -1; s_segbefore = 0; s_idx = -1; }
+  __syncthreads();
+  // 1) chunk holding the quota-th tie
+  int64_t base = 0;
+  for (int64_t c0 = 0; c0 < nch; c0 += blockDim.x) {
+    const int64_t c = c0 + threadIdx.x;
+    const int64_t v = (c < nch) ? (int64_t)dump[(size_t)(first_item + c) * nb + digit] : 0;
+    const int64_t incl = block_inclusive_scan(v, sh);
+    if (c < nch && base + incl - v < quota && base + incl >= quota) { s_chunk = c; s_before = base + incl - v; }
+    if (threadIdx.x == blockDim.x - 1) s_tot = incl;
+    __syncthreads();
+    base += s_tot;
+    __syncthreads();
+    if (s_chunk >= 0) break;
+  }
+  __syncthreads();
+  if (s_chunk < 0) {                                   // inconsistent counts: never walk out of range
+    if (threadIdx.x == 0) { st[u].cutoff = T.n; st[u].done = 1; flag_status(status, kStatusInternal); }
+    return;
+  }
+  const int64_t e0 = s_chunk * chunk, e1 = min(T.n, e0 + chunk);
+  const int64_t want = quota - s_before;               // 1-based rank inside the chunk
+  // 2) per-thread segments of whole vectors, in flat order
+  const void* p = T.deltas[i];
+  const int64_t len = e1 - e0;
+  int64_t seg = (len + blockDim.x - 1) / blockDim.x;
+  seg = (seg + F::kPerVec - 1) / F::kPerVec * F::kPerVec;
+  const int64_t a0 = min(e1, e0 + (int64_t)threadIdx.x * seg), a1 = min(e1, a0 + seg);
+  int64_t m = 0;
+  {
+    int64_t e = a0;
+    for (; e + F::kPerVec <= a1; e += F::kPerVec) {
+      uint4 q = *((const uint4*)p + e / F::kPerVec);
+      uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        if constexpr (DT == ISO_BF16) m += ((w[h] & 0x7FFFu) == tk) + (((w[h] >> 16) & 0x7FFFu) == tk);
+        else m += ((w[h] & 0x7FFFFFFFu) == tk);
+      }
+    }
+    for (; e < a1; ++e) m += ((elem_bits<DT>(p, e) & F::kKeyMask) == tk);
+  }
+  const int64_t incl = block_inclusive_scan(m, sh);
+  if (m > 0 && incl - m < want && incl >= want) { s_seg = threadIdx.x; s_segbefore = incl - m; }
+  __syncthreads();
+  if (s_seg < 0) {
+    if (threadIdx.x == 0) { st[u].cutoff = T.n; st[u].done = 1; flag_status(status, kStatusInternal); }
+    return;
+  }
+  // 3) the block walks that one segment (seg <= blockDim.x entries)
+  const int64_t g0 = min(e1, e0 + s_seg * seg);
+  const int64_t e = g0 + threadIdx.x;
+  const int64_t tie = (threadIdx.x < seg && e < e1) ? ((elem_bits<DT>(p, e) & F::kKeyMask) == tk) : 0;
+  const int64_t r = block_inclusive_scan(tie, sh);
+  if (tie && s_segbefore + r == want) s_idx = e;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    if (s_idx < 0) flag_status(status, kStatusInternal);
+    st[u].cutoff = (s_idx < 0) ? T.n : s_idx + 1;
+    st[u].done = 1;
   }
 }
 
@@ -414,21 +514,29 @@ static hipError_t run_select_t(const SelectPlan& pl, hipStream_t s) {
   const Pass* ps = (DT == ISO_BF16) ? bf : f32;
   const int np = (DT == ISO_BF16) ? 1 : 3;
   for (int q = 0; q < np; ++q) {
+    uint32_t* dump = (q == np - 1) ? pl.chunk_hist : nullptr;
     if (pl.hist_items > 0)
       k_hist<DT><<<(unsigned)pl.hist_items, kHistThreads, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.hist_item0, pl.hist_chunk,
                                                                   pl.states, pl.hist, ps[q].shift, ps[q].bits,
-                                                                  q == 0, pl.status);
+                                                                  q == 0, pl.status, dump);
     k_resolve<<<nu, kHistThreads, 0, s>>>(pl.tab, pl.K, pl.states, pl.hist, ps[q].shift, ps[q].bits, q == np - 1,
                                           pl.status);
   }
-  if (pl.tie_items > 0)
-    k_tie_count<DT><<<(unsigned)pl.tie_items, 256, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.tie_item0, pl.tie_chunk,
-                                                           pl.states, pl.tie_cnt);
-  k_tie_find<DT><<<nu, kHistThreads, 0, s>>>(pl.tab, pl.K, pl.tie_item0, pl.tie_chunk, pl.states, pl.tie_cnt,
-                                              pl.status);
+  if (pl.chunk_hist != nullptr) {
+    k_tie_find_dump<DT><<<nu, kHistThreads, 0, s>>>(pl.tab, pl.K, pl.hist_item0, pl.hist_chunk, pl.states,
+                                                    pl.chunk_hist, ps[np - 1].bits, pl.status);
+  } else {
+    if (pl.tie_items > 0)
+      k_tie_count<DT><<<(unsigned)pl.tie_items, 256, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.tie_item0, pl.tie_chunk,
+                                                             pl.states, pl.tie_cnt);
+    k_tie_find<DT><<<nu, kHistThreads, 0, s>>>(pl.tab, pl.K, pl.tie_item0, pl.tie_chunk, pl.states, pl.tie_cnt,
+                                                pl.status);
+  }
   k_emit_desc<<<(nu + 255) / 256, 256, 0, s>>>(pl.states, nu, pl.desc);
   return hipGetLastError();
 }
+
+int select_last_bits(int dt) { return dt == ISO_BF16 ? 15 : 8; }
 
 hipError_t run_select(const SelectPlan& pl, int dt, hipStream_t s) {
   return dt == ISO_BF16 ? run_select_t<ISO_BF16>(pl, s) : run_select_t<ISO_F32>(pl, s);
