@@ -10,6 +10,7 @@
 #include "iso_device.h"
 #include "iso_kernels.h"
 #include "iso_spectral.h"
+#include "iso_tsv.h"
 
 using namespace iso;
 
@@ -390,16 +391,49 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
   return ISO_ERR_INVALID_ARG;
 }
 
-iso_status iso_blockdiag_project(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank, double alpha,
-                                 float* const* delta_hat, void* ws, size_t ws_bytes, void* stream) {
-  (void)t; (void)n_t; (void)K; (void)dt; (void)rank; (void)alpha; (void)delta_hat; (void)ws; (void)ws_bytes;
-  (void)stream;
-  return ISO_ERR_UNSUPPORTED;
+static iso_status check_tsv(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank, bool ptrs) {
+  Need nd;
+  nd.base = nd.out = nd.deltas = ptrs;
+  iso_status st = check_table(t, n_t, K, dt, nd);
+  if (st != ISO_OK) return st;
+  if (rank < 1) return ISO_ERR_INVALID_ARG;
+  if (dt != ISO_BF16) return ISO_ERR_UNSUPPORTED;
+  int width = -1;
+  for (int j = 0; j < n_t; ++j) {
+    const int64_t q = std::min(t[j].rows, t[j].cols);
+    if ((int64_t)K * rank > q) return ISO_ERR_INVALID_ARG;
+    const int L = tsv_sketch_width(t[j].rows, t[j].cols, rank);
+    if (L == 0) return ISO_ERR_UNSUPPORTED;
+    if (width >= 0 && L != width) return ISO_ERR_UNSUPPORTED;   // one sketch width per call
+    width = L;
+  }
+  return ISO_OK;
 }
 
 size_t iso_workspace_size_tsv(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank) {
-  (void)t; (void)n_t; (void)K; (void)dt; (void)rank;
-  return 0;
+  if (check_tsv(t, n_t, K, dt, rank, false) != ISO_OK) return 0;
+  return kStatusBytes + tsv_workspace_bytes(t, n_t, K, rank);
+}
+
+iso_status iso_blockdiag_project(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank, double alpha,
+                                 float* const* delta_hat, void* ws, size_t ws_bytes, void* stream) {
+  iso_status st = check_tsv(t, n_t, K, dt, rank, true);
+  if (st != ISO_OK) return st;
+  if (!(alpha - alpha == 0.0)) return ISO_ERR_INVALID_ARG;
+  if (n_t == 0) return ISO_OK;
+  if (delta_hat != nullptr && (st = check_ptr_array((const void* const*)delta_hat, n_t, true)) != ISO_OK) return st;
+  const size_t need = kStatusBytes + tsv_workspace_bytes(t, n_t, K, rank);
+  if (ws == nullptr) return ISO_ERR_WORKSPACE;
+  if (((uintptr_t)ws & 255u) != 0) return ISO_ERR_ALIGNMENT;
+  if (ws_bytes < need) return ISO_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* w = (uint8_t*)ws;
+  HIP_TRY(start_call(w, s));
+  TsvArgs ta;
+  ta.rank = rank;
+  ta.alpha = alpha;
+  ta.delta_hat = delta_hat;
+  return run_tsv(t, n_t, K, ta, w + kStatusBytes, ws_bytes - kStatusBytes, (uint32_t*)w, s);
 }
 
 int64_t iso_k_from_density(int64_t n, int64_t num, int64_t den) {

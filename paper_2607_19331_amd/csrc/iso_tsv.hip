@@ -1,0 +1,794 @@
+// TSV-Merge (App. F) for bf16 weight matrices, batched over every (matrix, delta) pair of
+// a chunk of the tensor table:
+//   1. truncated SVD of each delta: randomised range finder with subspace iteration
+//      (Halko, Martinsson & Tropp, SIAM Review 2011, Alg. 4.4), sketch width L = r + p,
+//      two power iterations, Cholesky-QR2 re-orthonormalisation (Fukaya et al. 2014) in
+//      binary64; the products with the delta are MFMA bf16 (v_mfma_f32_16x16x32_bf16) with
+//      the right operand split into two bf16 terms, binary32 accumulation; the final
+//      L x L core is decomposed by one-sided Jacobi in binary64;
+//   2. concatenation U = [U_1|...|U_K], V likewise, Sigma = blockdiag(Sigma_i);
+//   3. Procrustes orthogonalisation U_perp = P_U Q_U^T = U (U^T U)^{-1/2}, the inverse square
+//      root from the eigen-decomposition of the K r x K r Gram matrix (one-sided Jacobi);
+//   4. out = round(W_0 + alpha * U_perp Sigma V_perp^T): MFMA bf16 with both operands split
+//      into two bf16 terms (three products), binary32 accumulation, the update fused into the
+//      epilogue.
+// The randomised sketch draws its test matrix from a counter-based hash (SplitMix64); the
+// result does not depend on it to the accuracy of the truncation where the spectrum has a gap.
+#include <cstring>
+#include <vector>
+
+#include "iso_dense.h"
+#include "iso_device.h"
+#include "iso_tsv.h"
+
+namespace iso {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kPowerIters = 2;
+constexpr size_t kTsvChunkBudget = 8ull << 30;   // workspace per chunk of matrices
+constexpr int kMaxNB = 8;                         // sketch width up to 128
+
+int64_t rup(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+// One (matrix, delta) problem.
+struct Prob {
+  const uint16_t* delta;   // R x C row-major bf16
+  int64_t R, C, L, ldb;    // ldb: padded length of the split operand columns
+  double* X[2];            // R x L row-major (ping-pong)
+  double* Z[2];            // C x L row-major (ping-pong)
+  uint16_t* bh;            // bf16 split of the current right operand: L columns of ldb
+  uint16_t* bl;
+  double* Gp;              // kSlabs x L x L Gram partials
+  double* G;               // L x L
+  double* Rf;              // L x L row-major upper factor of the last Cholesky
+  double* Ri;              // L x L row-major inverse
+  double* Ra;              // L x L first factor of the final QR
+  double* R2;              // L x L product of the final QR factors
+  double* Ja;              // L x L Jacobi matrix
+  double* Jv;              // L x L Jacobi rotations
+  double* Ut;              // L x L sorted left factors (col-major)
+  double* Vt;              // L x L sorted right factors (col-major)
+  double* St;              // L sorted singular values
+  uint64_t seed;
+};
+
+// One matrix.
+struct Mat {
+  const uint16_t* w0;      // R x C bf16
+  uint16_t* out;           // R x C bf16
+  float* dhat;             // optional R x C fp32
+  int64_t R, C, Kr, ldk;   // ldk = rup(Kr, 32)
+  double* U;               // R x ldk row-major
+  double* V;               // C x ldk row-major
+  double* Sig;             // ldk
+  double* GUp;             // kSlabs x Kr x Kr
+  double* GU;              // Kr x Kr
+  double* GV;
+  double* JaU; double* JvU; double* JaV; double* JvV;   // Kr x Kr each
+  double* FU;  double* FV;                              // Kr x Kr scaled rotations
+  double* MU;  double* MV;                              // Kr x Kr inverse square roots
+  double* Up;  double* Vp;                              // R x Kr, C x Kr
+  uint16_t* ah; uint16_t* al;   // R x ldk split of U_perp Sigma
+  uint16_t* bh; uint16_t* bl;   // C x ldk split of V_perp
+  double alpha;
+};
+
+constexpr int kSlabs = 16;
+
+__device__ __forceinline__ uint16_t bf16_rne_f32(float f) {
+  uint32_t b = __float_as_uint(f);
+  return (uint16_t)((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+}
+__device__ __forceinline__ float f32_of_bf16(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+__device__ __forceinline__ bf16x8_t ld_bf16x8(const uint16_t* p) {
+  uint4 v = *(const uint4*)p;
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+// Row `row` of a row-major bf16 matrix with `ncols` columns: 8 entries from column k (zero
+// outside the matrix).
+__device__ __forceinline__ bf16x8_t ld_row8(const uint16_t* base, int64_t nrows, int64_t ncols, int64_t row, int64_t k,
+                                            bool vec) {
+  if (row < nrows) {
+    const uint16_t* p = base + row * ncols + k;
+    if (vec && k + 8 <= ncols) return ld_bf16x8(p);
+    uint16_t t[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) t[e] = (k + e < ncols) ? p[e] : (uint16_t)0;
+    return __builtin_bit_cast(bf16x8_t, *(uint4*)t);
+  }
+  return __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0));
+}
+
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+  x += 0x9E3779B97F4A7C15ull;
+  x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
+  x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
+  return x ^ (x >> 31);
+}
+
+// ---- sketch operands -----------------------------------------------------------------------------
+
+// Test matrix Omega (C x L): entries j/64, j uniform in [-64, 63] (exact in bf16), low part 0.
+__global__ void k_omega(const Prob* __restrict__ probs) {
+  const Prob& P = probs[blockIdx.y];
+  const int64_t total = P.L * P.ldb;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t k = e % P.ldb;
+    float v = 0.0f;
+    if (k < P.C) v = (float)((int)(splitmix64(P.seed ^ (uint64_t)e) >> 57) - 64) * 0.015625f;
+    P.bh[e] = bf16_rne_f32(v);
+    P.bl[e] = 0;
+  }
+}
+
+// Split the current tall factor (which = 0: X[cur], R rows; 1: Z[cur], C rows) into bf16
+// hi/lo columns.
+__global__ void k_split(const Prob* __restrict__ probs, int which, int cur) {
+  const Prob& P = probs[blockIdx.y];
+  const int64_t M = which ? P.C : P.R;
+  const double* src = which ? P.Z[cur] : P.X[cur];
+  const int64_t total = P.L * P.ldb;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t col = e / P.ldb, k = e - col * P.ldb;
+    const float v = (k < M) ? (float)src[k * P.L + col] : 0.0f;
+    const uint16_t h = bf16_rne_f32(v);
+    P.bh[e] = h;
+    P.bl[e] = bf16_rne_f32(v - f32_of_bf16(h));
+  }
+}
+
+// ---- MFMA products with the delta -----------------------------------------------------------------
+
+// X[out] (R x L) = Delta (R x C) * B (C x L), B = bh + bl.
+template <int NB>
+__global__ void __launch_bounds__(256) k_mfma_nn(const Prob* __restrict__ probs, int out) {
+  const Prob& P = probs[blockIdx.z];
+  const int64_t R = P.R, C = P.C;
+  const int64_t m0 = (int64_t)blockIdx.x * 64;
+  if (m0 >= R) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
+  const int64_t row = m0 + 16 * w + ln;
+  const bool vec = (C % 8) == 0;
+  f32x4_t acc[NB];
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) acc[cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int64_t k0 = 0; k0 < C; k0 += 32) {
+    const int64_t k = k0 + 8 * g;
+    const bf16x8_t a = ld_row8(P.delta, R, C, row, k, vec);
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const int64_t col = cb * 16 + ln;
+      const bf16x8_t bh = ld_bf16x8(P.bh + col * P.ldb + k);
+      const bf16x8_t bl = ld_bf16x8(P.bl + col * P.ldb + k);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bh, acc[cb], 0, 0, 0);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bl, acc[cb], 0, 0, 0);
+    }
+  }
+  double* X = P.X[out];
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t r = m0 + 16 * w + 4 * g + e;
+      if (r < R) X[r * P.L + cb * 16 + ln] = (double)acc[cb][e];
+    }
+}
+
+// Z[out] (C x L) = Delta^T (C x R) * B (R x L), B = bh + bl.  The delta tile is transposed
+// through LDS.
+template <int NB>
+__global__ void __launch_bounds__(256) k_mfma_tn(const Prob* __restrict__ probs, int out) {
+  __shared__ uint16_t tile[32][64 + 2];
+  const Prob& P = probs[blockIdx.z];
+  const int64_t R = P.R, C = P.C;
+  const int64_t i0 = (int64_t)blockIdx.x * 64;
+  if (i0 >= C) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
+  const bool vec = (C % 8) == 0;
+  const int tr = threadIdx.x >> 3, tc = (threadIdx.x & 7) * 8;
+  f32x4_t acc[NB];
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) acc[cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int64_t k0 = 0; k0 < R; k0 += 32) {
+    {
+      const bf16x8_t v = ld_row8(P.delta, R, C, k0 + tr, i0 + tc, vec);
+      const uint4 u = __builtin_bit_cast(uint4, v);
+      const uint32_t ws[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        tile[tr][tc + 2 * e] = (uint16_t)(ws[e] & 0xFFFFu);
+        tile[tr][tc + 2 * e + 1] = (uint16_t)(ws[e] >> 16);
+      }
+    }
+    __syncthreads();
+    uint16_t t8[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) t8[e] = tile[8 * g + e][16 * w + ln];
+    const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *(uint4*)t8);
+    const int64_t k = k0 + 8 * g;
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const int64_t col = cb * 16 + ln;
+      const bf16x8_t bh = ld_bf16x8(P.bh + col * P.ldb + k);
+      const bf16x8_t bl = ld_bf16x8(P.bl + col * P.ldb + k);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bh, acc[cb], 0, 0, 0);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bl, acc[cb], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+  double* Z = P.Z[out];
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t r = i0 + 16 * w + 4 * g + e;
+      if (r < C) Z[r * P.L + cb * 16 + ln] = (double)acc[cb][e];
+    }
+}
+
+// ---- Cholesky-QR pieces ------------------------------------------------------------------------------
+
+// Gram partials of the current tall factor: Gp[z] = sum over rows of slab z of x x^T.
+template <int T>
+__global__ void __launch_bounds__(256) k_gram_slab(const Prob* __restrict__ probs, int which, int cur) {
+  __shared__ double rows[32][16 * T + 1];
+  const Prob& P = probs[blockIdx.y];
+  const int64_t M = which ? P.C : P.R;
+  const double* X = which ? P.Z[cur] : P.X[cur];
+  const int64_t L = P.L;
+  const int64_t per = (M + kSlabs - 1) / kSlabs;
+  const int64_t r0 = (int64_t)blockIdx.x * per, r1 = min(M, r0 + per);
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  double acc[T][T] = {};
+  for (int64_t b = r0; b < r1; b += 32) {
+    for (int e = threadIdx.x; e < 32 * 16 * T; e += 256) {
+      const int rr = e / (16 * T), cc = e % (16 * T);
+      rows[rr][cc] = (b + rr < r1 && cc < L) ? X[(b + rr) * L + cc] : 0.0;
+    }
+    __syncthreads();
+    const int nr = (int)min<int64_t>(32, r1 - b);
+    for (int rr = 0; rr < nr; ++rr) {
+      double xa[T], xb[T];
+#pragma unroll
+      for (int u = 0; u < T; ++u) { xa[u] = rows[rr][ty * T + u]; xb[u] = rows[rr][tx * T + u]; }
+#pragma unroll
+      for (int u = 0; u < T; ++u)
+#pragma unroll
+        for (int v = 0; v < T; ++v) acc[u][v] = acc[u][v] + xa[u] * xb[v];
+    }
+    __syncthreads();
+  }
+  double* Gz = P.Gp + (int64_t)blockIdx.x * L * L;
+#pragma unroll
+  for (int u = 0; u < T; ++u)
+#pragma unroll
+    for (int v = 0; v < T; ++v) {
+      const int64_t a = ty * T + u, c = tx * T + v;
+      if (a < L && c < L) Gz[a * L + c] = acc[u][v];
+    }
+}
+
+// G = sum of the partials, then G = R^T R (R upper, row-major in Rf) and Ri = R^{-1}.  With
+// `acc`: R2 = Rf * Ra (second factor times the saved first), and `save`: Ra = Rf.
+__global__ void __launch_bounds__(256) k_chol(const Prob* __restrict__ probs, int save, int accum, uint32_t* status) {
+  extern __shared__ double g[];                  // L x L
+  const Prob& P = probs[blockIdx.x];
+  const int64_t L = P.L;
+  for (int64_t e = threadIdx.x; e < L * L; e += blockDim.x) {
+    double s = 0.0;
+    for (int z = 0; z < kSlabs; ++z) s = s + P.Gp[(int64_t)z * L * L + e];
+    g[e] = s;
+  }
+  __syncthreads();
+  __shared__ double shift;
+  if (threadIdx.x == 0) {
+    double tr = 0.0;
+    for (int64_t j = 0; j < L; ++j) tr += g[j * L + j];
+    shift = 1e-15 * tr / (double)L + 1e-300;
+  }
+  __syncthreads();
+  for (int64_t j = 0; j < L; ++j) {
+    if (threadIdx.x == 0) {
+      double d = g[j * L + j];
+      g[j * L + j] = sqrt(d > shift ? d : shift);
+    }
+    __syncthreads();
+    for (int64_t k = j + 1 + threadIdx.x; k < L; k += blockDim.x) g[j * L + k] /= g[j * L + j];
+    __syncthreads();
+    const int64_t n = L - j - 1;
+    for (int64_t e = threadIdx.x; e < n * n; e += blockDim.x) {
+      const int64_t i = j + 1 + e / n, k = j + 1 + e % n;
+      if (k >= i) g[i * L + k] -= g[j * L + i] * g[j * L + k];
+    }
+    __syncthreads();
+  }
+  for (int64_t e = threadIdx.x; e < L * L; e += blockDim.x) {
+    const int64_t i = e / L, k = e % L;
+    P.Rf[e] = (k >= i) ? g[e] : 0.0;
+  }
+  // inverse of the upper factor, one column per thread (back substitution)
+  for (int64_t c = threadIdx.x; c < L; c += blockDim.x) {
+    for (int64_t i = L - 1; i >= 0; --i) {
+      double v;
+      if (i > c) v = 0.0;
+      else {
+        double s = (i == c) ? 1.0 : 0.0;
+        for (int64_t t = i + 1; t <= c; ++t) s -= g[i * L + t] * P.Ri[t * L + c];
+        v = s / g[i * L + i];
+      }
+      P.Ri[i * L + c] = v;
+    }
+  }
+  __syncthreads();
+  if (save)
+    for (int64_t e = threadIdx.x; e < L * L; e += blockDim.x) P.Ra[e] = P.Rf[e];
+  if (accum) {
+    // R2 = Rf * Ra  (both upper)
+    for (int64_t e = threadIdx.x; e < L * L; e += blockDim.x) {
+      const int64_t i = e / L, k = e % L;
+      double s = 0.0;
+      for (int64_t t = i; t <= k; ++t) s = s + P.Rf[i * L + t] * P.Ra[t * L + k];
+      P.R2[e] = (k >= i) ? s : 0.0;
+    }
+  }
+  if (threadIdx.x == 0 && !(g[0] > 0.0)) flag_status(status, kStatusInternal);
+}
+
+// X[dst] = X[src] * Ri (tall factor times the inverse factor), rows split over blocks.
+template <int T>
+__global__ void __launch_bounds__(256) k_apply_ri(const Prob* __restrict__ probs, int which, int src, int dst) {
+  __shared__ double ri[16 * T][16 * T + 1];
+  const Prob& P = probs[blockIdx.y];
+  const int64_t M = which ? P.C : P.R;
+  const double* X = which ? P.Z[src] : P.X[src];
+  double* Y = which ? P.Z[dst] : P.X[dst];
+  const int64_t L = P.L;
+  for (int64_t e = threadIdx.x; e < L * L; e += blockDim.x) ri[e / L][e % L] = P.Ri[e];
+  __syncthreads();
+  // each thread: one row, all L outputs in chunks
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < M; r += (int64_t)gridDim.x * blockDim.x) {
+    const double* xr = X + r * L;
+    double* yr = Y + r * L;
+    for (int64_t c0 = 0; c0 < L; c0 += 16) {
+      double acc[16] = {};
+      for (int64_t k = 0; k <= min<int64_t>(L - 1, c0 + 15); ++k) {
+        const double xv = xr[k];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) acc[u] = acc[u] + xv * ri[k][c0 + u];
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (c0 + u < L) yr[c0 + u] = acc[u];
+    }
+  }
+}
+
+// Jacobi input: Ja = R2 read as column-major, i.e. R2^T.
+__global__ void k_core_load(const Prob* __restrict__ probs, JacobiJob* jobs) {
+  const Prob& P = probs[blockIdx.x];
+  for (int64_t e = threadIdx.x; e < P.L * P.L; e += blockDim.x) P.Ja[e] = P.R2[e];
+  if (threadIdx.x == 0) {
+    jobs[blockIdx.x].a = P.Ja;
+    jobs[blockIdx.x].v = P.Jv;
+    jobs[blockIdx.x].r = P.L;
+    jobs[blockIdx.x].c = P.L;
+  }
+}
+
+// Sigma[i*r + c] = St[c] for c < r (Sig has ldk entries, the pad stays zero).
+__global__ void k_sigma(const Prob* __restrict__ probs, Mat* mats, int K, int r) {
+  const int p = blockIdx.x;
+  const Prob& P = probs[p];
+  Mat& M = mats[p / K];
+  const int i = p % K;
+  for (int c = threadIdx.x; c < r; c += blockDim.x) M.Sig[i * r + c] = P.St[c];
+}
+
+// ---- orthogonalisation (Procrustes / Loewdin) ---------------------------------------------------
+
+// F = Jv diag(1 / sqrt(lambda)), lambda_j = |column j of Ja| (eigenvalues of the SPD Gram)
+__global__ void __launch_bounds__(1024) k_inv_sqrt_scale(double* F, const double* Ja, const double* Jv, int64_t n) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  for (int64_t j = wid; j < n; j += nw) {
+    double s = 0.0;
+    for (int64_t t = lane; t < n; t += 64) s += Ja[j * n + t] * Ja[j * n + t];
+    s = wave_sum_f64(s);
+    const double lam = sqrt(s);
+    const double sc = (lam > 0.0) ? 1.0 / sqrt(lam) : 0.0;
+    for (int64_t t = lane; t < n; t += 64) F[j * n + t] = Jv[j * n + t] * sc;
+  }
+}
+
+// bf16 hi/lo split of rows: dst (rows x ldk) = src (rows x Kr, row stride ldsrc) * (scale? s[col] : 1)
+__global__ void k_split_rows(uint16_t* __restrict__ hi, uint16_t* __restrict__ lo, const double* __restrict__ src,
+                             int64_t rows, int64_t Kr, int64_t ldsrc, int64_t ldk, const double* __restrict__ scale) {
+  const int64_t total = rows * ldk;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = e / ldk, c = e - r * ldk;
+    float v = 0.0f;
+    if (c < Kr) v = (float)(src[r * ldsrc + c] * (scale ? scale[c] : 1.0));
+    const uint16_t h = bf16_rne_f32(v);
+    hi[e] = h;
+    lo[e] = bf16_rne_f32(v - f32_of_bf16(h));
+  }
+}
+
+// out = round(W0 + alpha * A B^T), A = ah + al (R x ldk), B = bh + bl (C x ldk); three MFMA
+// products per step (hi*hi, hi*lo, lo*hi).  64 x 64 output tile per block.
+__global__ void __launch_bounds__(256) k_mfma_recon(const Mat* __restrict__ mats) {
+  const Mat& M = mats[blockIdx.z];
+  const int64_t m0 = (int64_t)blockIdx.x * 64, n0 = (int64_t)blockIdx.y * 64;
+  if (m0 >= M.R || n0 >= M.C) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
+  const int64_t arow = min(M.R - 1, m0 + 16 * w + ln);
+  f32x4_t acc[4];
+#pragma unroll
+  for (int cb = 0; cb < 4; ++cb) acc[cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int64_t k0 = 0; k0 < M.ldk; k0 += 32) {
+    const int64_t k = k0 + 8 * g;
+    const bf16x8_t a_h = ld_bf16x8(M.ah + arow * M.ldk + k);
+    const bf16x8_t a_l = ld_bf16x8(M.al + arow * M.ldk + k);
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      const int64_t col = min(M.C - 1, n0 + cb * 16 + ln);
+      const bf16x8_t b_h = ld_bf16x8(M.bh + col * M.ldk + k);
+      const bf16x8_t b_l = ld_bf16x8(M.bl + col * M.ldk + k);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_h, b_h, acc[cb], 0, 0, 0);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_h, b_l, acc[cb], 0, 0, 0);
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_l, b_h, acc[cb], 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t r = m0 + 16 * w + 4 * g + e, c = n0 + cb * 16 + ln;
+      if (r < M.R && c < M.C) {
+        const int64_t idx = r * M.C + c;
+        const double v = (double)f32_of_bf16(M.w0[idx]) + M.alpha * (double)acc[cb][e];
+        M.out[idx] = (uint16_t)f64_to_bf16_rne(v);
+        if (M.dhat) M.dhat[idx] = acc[cb][e];
+      }
+    }
+}
+
+// ---- host side ----------------------------------------------------------------------------------
+
+struct Sizes {
+  int64_t R, C, L, ldb, Kr, ldk;
+};
+
+Sizes sizes_of(const iso_tensor& t, int K, int r) {
+  Sizes z;
+  z.R = t.rows;
+  z.C = t.cols;
+  z.L = tsv_sketch_width(t.rows, t.cols, r);
+  z.ldb = rup(std::max(z.R, z.C), 32);
+  z.Kr = (int64_t)K * r;
+  z.ldk = rup(z.Kr, 32);
+  return z;
+}
+
+// bytes carved for one problem / one matrix (same sequence as carve_* below)
+struct Carver {
+  uint8_t* base;
+  size_t off = 0;
+  template <typename T>
+  T* take(int64_t n) {
+    T* r = (T*)(base + off);
+    off = align_up(off + sizeof(T) * (size_t)std::max<int64_t>(n, 1), 256);
+    return r;
+  }
+};
+
+void carve_prob(Carver& cv, Prob& P, const Sizes& z) {
+  for (int b = 0; b < 2; ++b) P.X[b] = cv.take<double>(z.R * z.L);
+  for (int b = 0; b < 2; ++b) P.Z[b] = cv.take<double>(z.C * z.L);
+  P.bh = cv.take<uint16_t>(z.L * z.ldb);
+  P.bl = cv.take<uint16_t>(z.L * z.ldb);
+  P.Gp = cv.take<double>((int64_t)kSlabs * z.L * z.L);
+  P.G = cv.take<double>(z.L * z.L);
+  P.Rf = cv.take<double>(z.L * z.L);
+  P.Ri = cv.take<double>(z.L * z.L);
+  P.Ra = cv.take<double>(z.L * z.L);
+  P.R2 = cv.take<double>(z.L * z.L);
+  P.Ja = cv.take<double>(z.L * z.L);
+  P.Jv = cv.take<double>(z.L * z.L);
+  P.Ut = cv.take<double>(z.L * z.L);
+  P.Vt = cv.take<double>(z.L * z.L);
+  P.St = cv.take<double>(z.L);
+}
+
+void carve_mat(Carver& cv, Mat& M, const Sizes& z) {
+  M.U = cv.take<double>(z.R * z.ldk);
+  M.V = cv.take<double>(z.C * z.ldk);
+  M.Sig = cv.take<double>(z.ldk);
+  M.GUp = cv.take<double>((int64_t)kSlabs * z.Kr * z.Kr);
+  M.GU = cv.take<double>(z.Kr * z.Kr);
+  M.GV = cv.take<double>(z.Kr * z.Kr);
+  M.JaU = cv.take<double>(z.Kr * z.Kr);
+  M.JvU = cv.take<double>(z.Kr * z.Kr);
+  M.JaV = cv.take<double>(z.Kr * z.Kr);
+  M.JvV = cv.take<double>(z.Kr * z.Kr);
+  M.FU = cv.take<double>(z.Kr * z.Kr);
+  M.FV = cv.take<double>(z.Kr * z.Kr);
+  M.MU = cv.take<double>(z.Kr * z.Kr);
+  M.MV = cv.take<double>(z.Kr * z.Kr);
+  M.Up = cv.take<double>(z.R * z.Kr);
+  M.Vp = cv.take<double>(z.C * z.Kr);
+  M.ah = cv.take<uint16_t>(z.R * z.ldk);
+  M.al = cv.take<uint16_t>(z.R * z.ldk);
+  M.bh = cv.take<uint16_t>(z.C * z.ldk);
+  M.bl = cv.take<uint16_t>(z.C * z.ldk);
+}
+
+size_t bytes_per_matrix(const Sizes& z, int K) {
+  Carver cv{nullptr};
+  Prob P;
+  for (int i = 0; i < K; ++i) carve_prob(cv, P, z);
+  Mat M;
+  carve_mat(cv, M, z);
+  return cv.off;
+}
+
+int chunk_matrices(const iso_tensor* t, int n_t, int K, int r) {
+  size_t per = 0;
+  for (int j = 0; j < n_t; ++j) per = std::max(per, bytes_per_matrix(sizes_of(t[j], K, r), K));
+  if (per == 0) return std::max(n_t, 1);
+  return (int)std::max<size_t>(1, std::min<size_t>((size_t)n_t, kTsvChunkBudget / per));
+}
+
+// tables uploaded per chunk
+size_t table_bytes(int nm, int K) {
+  const int np = nm * K;
+  size_t b = 0;
+  b += align_up(sizeof(Prob) * np, 256);
+  b += align_up(sizeof(Mat) * nm, 256);
+  b += align_up(sizeof(JacobiJob) * std::max(np, 2 * nm), 256);
+  b += align_up(sizeof(double*) * 3 * np, 256);
+  b += 8 * align_up(sizeof(GemmJob) * (size_t)std::max(np, kSlabs * nm * 2), 256);
+  return b;
+}
+
+template <int NB>
+void launch_nn(const Prob* d, int np, int64_t maxR, int out, hipStream_t s) {
+  k_mfma_nn<NB><<<dim3((unsigned)((maxR + 63) / 64), 1, (unsigned)np), 256, 0, s>>>(d, out);
+}
+template <int NB>
+void launch_tn(const Prob* d, int np, int64_t maxC, int out, hipStream_t s) {
+  k_mfma_tn<NB><<<dim3((unsigned)((maxC + 63) / 64), 1, (unsigned)np), 256, 0, s>>>(d, out);
+}
+template <int T>
+void launch_gram(const Prob* d, int np, int which, int cur, hipStream_t s) {
+  k_gram_slab<T><<<dim3(kSlabs, (unsigned)np), 256, 0, s>>>(d, which, cur);
+}
+template <int T>
+void launch_apply(const Prob* d, int np, int64_t maxM, int which, int src, int dst, hipStream_t s) {
+  k_apply_ri<T><<<dim3((unsigned)std::max<int64_t>(1, std::min<int64_t>((maxM + 255) / 256, 64)), (unsigned)np), 256,
+                  0, s>>>(d, which, src, dst);
+}
+
+#define DISPATCH_NB(nb, F, ...)                 \
+  switch (nb) {                                 \
+    case 1: F<1>(__VA_ARGS__); break;           \
+    case 2: F<2>(__VA_ARGS__); break;           \
+    case 3: F<3>(__VA_ARGS__); break;           \
+    case 4: F<4>(__VA_ARGS__); break;           \
+    case 5: F<5>(__VA_ARGS__); break;           \
+    case 6: F<6>(__VA_ARGS__); break;           \
+    case 7: F<7>(__VA_ARGS__); break;           \
+    default: F<8>(__VA_ARGS__); break;          \
+  }
+
+}  // namespace
+
+int tsv_sketch_width(int64_t R, int64_t C, int r) {
+  const int64_t q = std::min(R, C);
+  int64_t L = rup((int64_t)r + std::max<int64_t>(8, r / 2), 16);
+  L = std::min<int64_t>(L, 16 * kMaxNB);
+  L = std::min<int64_t>(L, q / 16 * 16);
+  if (L < r || L < 16) return 0;
+  return (int)L;
+}
+
+size_t tsv_workspace_bytes(const iso_tensor* t, int n_t, int K, int rank) {
+  if (n_t <= 0) return 0;
+  const int nm = chunk_matrices(t, n_t, K, rank);
+  size_t per = 0;
+  for (int j = 0; j < n_t; ++j) per = std::max(per, bytes_per_matrix(sizes_of(t[j], K, rank), K));
+  return table_bytes(nm, K) + per * (size_t)nm;
+}
+
+iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_t* ws, size_t ws_bytes,
+                   uint32_t* status, hipStream_t s) {
+#define TS_TRY(x)                                \
+  do {                                           \
+    if ((x) != hipSuccess) return ISO_ERR_HIP;   \
+  } while (0)
+  (void)ws_bytes;
+  const int r = a.rank;
+  const int nm_max = chunk_matrices(t, n_t, K, r);
+  std::vector<uint8_t> host;
+  for (int j0 = 0; j0 < n_t; j0 += nm_max) {
+    const int nm = std::min(nm_max, n_t - j0);
+    const int np = nm * K;
+    // ---- device layout of this chunk
+    Carver cv{ws};
+    Prob* d_prob = cv.take<Prob>(np);
+    Mat* d_mat = cv.take<Mat>(nm);
+    JacobiJob* d_jobs = cv.take<JacobiJob>(std::max(np, 2 * nm));
+    double** d_ptrs = cv.take<double*>(3 * np);
+    GemmJob* d_gj[8];
+    for (int q = 0; q < 8; ++q) d_gj[q] = cv.take<GemmJob>(std::max(np, kSlabs * nm * 2));
+    cv.off = table_bytes(nm, K);
+    std::vector<Prob> hp(np);
+    std::vector<Mat> hm(nm);
+    int64_t maxR = 0, maxC = 0, L = 0, Kr = (int64_t)K * r;
+    for (int m = 0; m < nm; ++m) {
+      const iso_tensor& tt = t[j0 + m];
+      const Sizes z = sizes_of(tt, K, r);
+      maxR = std::max(maxR, z.R);
+      maxC = std::max(maxC, z.C);
+      L = std::max(L, z.L);
+      for (int i = 0; i < K; ++i) {
+        Prob& P = hp[m * K + i];
+        std::memset(&P, 0, sizeof P);
+        carve_prob(cv, P, z);
+        P.delta = (const uint16_t*)tt.deltas[i];
+        P.R = z.R;
+        P.C = z.C;
+        P.L = z.L;
+        P.ldb = z.ldb;
+        P.seed = 0x5EED0000ull + ((uint64_t)(j0 + m) << 8) + (uint64_t)i;
+      }
+      Mat& M = hm[m];
+      std::memset(&M, 0, sizeof M);
+      carve_mat(cv, M, z);
+      M.w0 = (const uint16_t*)tt.base;
+      M.out = (uint16_t*)tt.out;
+      M.dhat = a.delta_hat ? a.delta_hat[j0 + m] : nullptr;
+      M.R = z.R;
+      M.C = z.C;
+      M.Kr = z.Kr;
+      M.ldk = z.ldk;
+      M.alpha = a.alpha;
+    }
+    // all problems of a chunk share L (matrices of one chunk must give the same sketch width)
+    for (int p = 0; p < np; ++p)
+      if (hp[p].L != L) return ISO_ERR_UNSUPPORTED;
+    const int NB = (int)(L / 16);
+    const int64_t maxM = std::max(maxR, maxC);
+    // gemm job tables: 0 U_i = X Ut[:, :r]; 1 V_i = Z Vt[:, :r]; 2 GU slabs; 3 GV slabs;
+    // 4 M = F Jv^T (U and V); 5 U_perp = U M_U, V_perp = V M_V
+    std::vector<GemmJob> gj[6];
+    for (int p = 0; p < np; ++p) {
+      const Prob& P = hp[p];
+      const Mat& M = hm[p / K];
+      const int i = p % K;
+      gj[0].push_back(GemmJob{P.X[0], P.Ut, M.U + i * r, P.L, 1, 1, P.L, M.ldk, 1, P.R, r, P.L, 1.0, 0.0});
+      gj[1].push_back(GemmJob{P.Z[0], P.Vt, M.V + i * r, P.L, 1, 1, P.L, M.ldk, 1, P.C, r, P.L, 1.0, 0.0});
+    }
+    for (int m = 0; m < nm; ++m) {
+      const Mat& M = hm[m];
+      for (int z = 0; z < kSlabs; ++z) {
+        const int64_t perU = (M.R + kSlabs - 1) / kSlabs, perV = (M.C + kSlabs - 1) / kSlabs;
+        const int64_t u0 = std::min<int64_t>(M.R, z * perU), u1 = std::min<int64_t>(M.R, u0 + perU);
+        const int64_t v0 = std::min<int64_t>(M.C, z * perV), v1 = std::min<int64_t>(M.C, v0 + perV);
+        // G_z = U[u0:u1]^T U[u0:u1]: A(i,k) = U(u0+k, i)
+        gj[2].push_back(GemmJob{M.U + u0 * M.ldk, M.U + u0 * M.ldk, M.GUp + (int64_t)z * M.Kr * M.Kr, 1, M.ldk,
+                                M.ldk, 1, M.Kr, 1, M.Kr, M.Kr, u1 - u0, 1.0, 0.0});
+        gj[3].push_back(GemmJob{M.V + v0 * M.ldk, M.V + v0 * M.ldk, M.GUp + (int64_t)z * M.Kr * M.Kr, 1, M.ldk,
+                                M.ldk, 1, M.Kr, 1, M.Kr, M.Kr, v1 - v0, 1.0, 0.0});
+      }
+      // M = F Jv^T: F (col-major n x n): A(i,k) = F[i + k n]; B(k,j) = Jv^T(k,j) = Jv[k + j n]... Jv col-major:
+      // Jv(j,k) at Jv[j + k n]; B(k,j) = Jv(j,k) = Jv[j + k n] -> bs0 = n, bs1 = 1
+      gj[4].push_back(GemmJob{M.FU, M.JvU, M.MU, 1, M.Kr, M.Kr, 1, M.Kr, 1, M.Kr, M.Kr, M.Kr, 1.0, 0.0});
+      gj[4].push_back(GemmJob{M.FV, M.JvV, M.MV, 1, M.Kr, M.Kr, 1, M.Kr, 1, M.Kr, M.Kr, M.Kr, 1.0, 0.0});
+      gj[5].push_back(GemmJob{M.U, M.MU, M.Up, M.ldk, 1, M.Kr, 1, M.Kr, 1, M.R, M.Kr, M.Kr, 1.0, 0.0});
+      gj[5].push_back(GemmJob{M.V, M.MV, M.Vp, M.ldk, 1, M.Kr, 1, M.Kr, 1, M.C, M.Kr, M.Kr, 1.0, 0.0});
+    }
+    // upload tables (one staging buffer, kept until the chunk is done)
+    const size_t tb = table_bytes(nm, K);
+    host.assign(tb, 0);
+    {
+      Carver hc{host.data()};
+      Prob* h_prob = hc.take<Prob>(np);
+      Mat* h_mat = hc.take<Mat>(nm);
+      hc.take<JacobiJob>(std::max(np, 2 * nm));
+      double** h_ptrs = hc.take<double*>(3 * np);
+      GemmJob* h_gj[8];
+      for (int q = 0; q < 8; ++q) h_gj[q] = hc.take<GemmJob>(std::max(np, kSlabs * nm * 2));
+      std::memcpy(h_prob, hp.data(), sizeof(Prob) * np);
+      std::memcpy(h_mat, hm.data(), sizeof(Mat) * nm);
+      for (int p = 0; p < np; ++p) {
+        h_ptrs[p] = hp[p].Ut;
+        h_ptrs[np + p] = hp[p].Vt;
+        h_ptrs[2 * np + p] = hp[p].St;
+      }
+      for (int q = 0; q < 6; ++q) std::memcpy(h_gj[q], gj[q].data(), sizeof(GemmJob) * gj[q].size());
+    }
+    TS_TRY(hipMemcpyAsync(ws, host.data(), tb, hipMemcpyHostToDevice, s));
+    const unsigned gx = grid_for(L * rup(maxM, 32));
+    auto cholqr = [&](int which, int& cur, int save_first, int accum_second) {
+      const int64_t mm = which ? maxC : maxR;
+      for (int pass = 0; pass < 2; ++pass) {
+        DISPATCH_NB(NB, launch_gram, d_prob, np, which, cur, s);
+        const size_t shb = sizeof(double) * L * L;
+        k_chol<<<np, 256, shb, s>>>(d_prob, (pass == 0) ? save_first : 0, (pass == 1) ? accum_second : 0, status);
+        DISPATCH_NB(NB, launch_apply, d_prob, np, mm, which, cur, 1 - cur, s);
+        cur = 1 - cur;
+      }
+    };
+    // 1. range finder with subspace iteration
+    int cx = 0, cz = 0;
+    k_omega<<<dim3(gx, np), 256, 0, s>>>(d_prob);
+    DISPATCH_NB(NB, launch_nn, d_prob, np, maxR, cx, s);
+    cholqr(0, cx, 0, 0);
+    for (int it = 0; it < kPowerIters; ++it) {
+      k_split<<<dim3(gx, np), 256, 0, s>>>(d_prob, 0, cx);
+      DISPATCH_NB(NB, launch_tn, d_prob, np, maxC, cz, s);
+      cholqr(1, cz, 0, 0);
+      k_split<<<dim3(gx, np), 256, 0, s>>>(d_prob, 1, cz);
+      DISPATCH_NB(NB, launch_nn, d_prob, np, maxR, cx, s);
+      cholqr(0, cx, 0, 0);
+    }
+    // 2. B^T = Delta^T Q, its QR (R2 accumulated), SVD of the L x L core R2^T
+    k_split<<<dim3(gx, np), 256, 0, s>>>(d_prob, 0, cx);
+    DISPATCH_NB(NB, launch_tn, d_prob, np, maxC, cz, s);
+    cholqr(1, cz, 1, 1);
+    k_core_load<<<np, 256, 0, s>>>(d_prob, d_jobs);
+    k_jacobi<<<np, kJacobiThreads, 0, s>>>(d_jobs, status);
+    k_svd_finalize<<<np, 1024, (sizeof(double) + sizeof(int)) * L, s>>>(d_jobs, d_ptrs, d_ptrs + np, d_ptrs + 2 * np);
+    // U_i = Q Ut[:, :r], V_i = Q2 Vt[:, :r]; both factors sit in buffer 0 after an even number of QR passes
+    if (cx != 0 || cz != 0) return ISO_ERR_INTERNAL;
+    k_gemm_jobs<<<dim3((unsigned)((maxR + 63) / 64), (unsigned)((r + 63) / 64), (unsigned)np), 256, 0, s>>>(d_gj[0]);
+    k_gemm_jobs<<<dim3((unsigned)((maxC + 63) / 64), (unsigned)((r + 63) / 64), (unsigned)np), 256, 0, s>>>(d_gj[1]);
+    k_sigma<<<np, 64, 0, s>>>(d_prob, d_mat, K, r);
+    // 3. Procrustes orthogonalisation of U and V
+    const unsigned tk = (unsigned)((Kr + 63) / 64);
+    for (int side = 0; side < 2; ++side) {
+      k_gemm_jobs<<<dim3(tk, tk, (unsigned)(kSlabs * nm)), 256, 0, s>>>(d_gj[2 + side]);
+      for (int m = 0; m < nm; ++m) {
+        const Mat& M = hm[m];
+        double* G = side ? M.GV : M.GU;
+        k_sum_parts<<<grid_for(Kr * Kr), 256, 0, s>>>(G, M.GUp, kSlabs, Kr * Kr, Kr * Kr);
+        k_copy<<<grid_for(Kr * Kr), 256, 0, s>>>(side ? M.JaV : M.JaU, G, Kr * Kr);
+      }
+    }
+    {
+      std::vector<JacobiJob> jj(2 * nm);
+      for (int m = 0; m < nm; ++m) {
+        jj[2 * m] = JacobiJob{hm[m].JaU, hm[m].JvU, Kr, Kr};
+        jj[2 * m + 1] = JacobiJob{hm[m].JaV, hm[m].JvV, Kr, Kr};
+      }
+      TS_TRY(hipMemcpyAsync(d_jobs, jj.data(), sizeof(JacobiJob) * 2 * nm, hipMemcpyHostToDevice, s));
+      k_jacobi<<<2 * nm, kJacobiThreads, 0, s>>>(d_jobs, status);
+      for (int m = 0; m < nm; ++m) {
+        k_inv_sqrt_scale<<<1, 1024, 0, s>>>(hm[m].FU, hm[m].JaU, hm[m].JvU, Kr);
+        k_inv_sqrt_scale<<<1, 1024, 0, s>>>(hm[m].FV, hm[m].JaV, hm[m].JvV, Kr);
+      }
+      k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[4]);
+      k_gemm_jobs<<<dim3((unsigned)((maxM + 63) / 64), tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[5]);
+      // the Jacobi job table must not be overwritten by the next chunk before this one ran
+      TS_TRY(hipStreamSynchronize(s));
+    }
+    // 4. reconstruction with the update fused
+    for (int m = 0; m < nm; ++m) {
+      const Mat& M = hm[m];
+      k_split_rows<<<grid_for(M.R * M.ldk), 256, 0, s>>>(M.ah, M.al, M.Up, M.R, M.Kr, M.Kr, M.ldk, M.Sig);
+      k_split_rows<<<grid_for(M.C * M.ldk), 256, 0, s>>>(M.bh, M.bl, M.Vp, M.C, M.Kr, M.Kr, M.ldk, nullptr);
+    }
+    k_mfma_recon<<<dim3((unsigned)((maxR + 63) / 64), (unsigned)((maxC + 63) / 64), (unsigned)nm), 256, 0, s>>>(d_mat);
+    TS_TRY(hipGetLastError());
+    TS_TRY(hipStreamSynchronize(s));
+  }
+  return ISO_OK;
+#undef TS_TRY
+}
+
+}  // namespace iso
