@@ -75,7 +75,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="7b", choices=["layer", "1.5b", "7b"])
+    ap.add_argument("--config", default="7b", choices=["layer", "1.5b", "7b", "7b-tsv"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -92,7 +92,7 @@ def main():
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream().cuda_stream
     K = wl.K
-    entries = []
+    entries, tsv_entries = [], []
     for t, spec in enumerate(wl.tensors):
         n = spec.numel
         base = torch.empty(n, dtype=torch.int16, device=dev)
@@ -104,41 +104,58 @@ def main():
             ds.append(d)
         out = torch.empty(n, dtype=torch.int16, device=dev)
         k = iso.iso_k_from_density(n, wl.density.numerator, wl.density.denominator)
-        entries.append(iso.Entry(spec.rows, spec.cols, base=base, deltas=ds, out=out, k=k))
+        e = iso.Entry(spec.rows, spec.cols, base=base, deltas=ds, out=out, k=k)
+        if wl.tsv_rank and spec.name.split(".")[-1] in wl.tsv_names:
+            tsv_entries.append(e)
+        else:
+            entries.append(e)
     N = wl.numel
     desc = iso.desc_tensor(len(entries) * K, dev)
     ws_sel = iso.workspace(iso.OP_TOPK, entries, K, iso.BF16, dev)
     ws_upd = iso.workspace(iso.OP_UPDATE_FUSED, entries, K, iso.BF16, dev)
+    ws_tsv = iso.workspace(iso.OP_BLOCKDIAG, tsv_entries, K, iso.BF16, dev, rank=wl.tsv_rank) if tsv_entries else None
     torch.cuda.synchronize()
 
-    def step():
+    def step(ev=None):
+        if ev:
+            ev[0].record()
         iso.iso_topk_mask(entries, K, iso.BF16, desc, ws=ws_sel)
+        if ev:
+            ev[1].record()
         iso.iso_update(entries, K, iso.BF16, iso.UPDATE_FUSED, merge=iso.MERGE_TIES, lam=1.0, desc=desc, ws=ws_upd)
+        if ev:
+            ev[2].record()
+        if tsv_entries:
+            iso.iso_blockdiag_project(tsv_entries, K, iso.BF16, wl.tsv_rank, 1.0, ws=ws_tsv)
+        if ev:
+            ev[3].record()
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    if iso.iso_read_device_status(ws_upd) != 0 or iso.iso_read_device_status(ws_sel) != 0:
-        raise RuntimeError("device status reports an error")
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    for w in (ws_sel, ws_upd, ws_tsv):
+        if w is not None and iso.iso_read_device_status(w) != 0:
+            raise RuntimeError("device status reports an error")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
-        ev[s][0].record()
-        iso.iso_topk_mask(entries, K, iso.BF16, desc, ws=ws_sel)
-        ev[s][1].record()
-        iso.iso_update(entries, K, iso.BF16, iso.UPDATE_FUSED, merge=iso.MERGE_TIES, lam=1.0, desc=desc, ws=ws_upd)
-        ev[s][2].record()
+        step(ev[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     sel_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
     mrg_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
+    tsv_ms = sum(e[2].elapsed_time(e[3]) for e in ev) / args.steps
     ms_per_step = wall * 1e3 / args.steps
 
+    n_elem = sum(e.rows * e.cols for e in entries)
     alg_bytes_step = N * (K * 2 + 2 + 2)            # each delta and the base read once, weights written once
-    merge_alg = alg_bytes_step                      # the fused pass moves exactly the algorithmic bytes
+    merge_alg = n_elem * (K * 2 + 2 + 2)            # the fused pass moves exactly the algorithmic bytes
     merge_gbps = merge_alg / (mrg_ms * 1e-3) / 1e9
     traffic = measured_traffic(args.config)
+    what = "TopKMask select + elect + disjoint mean + update"
+    if tsv_entries:
+        what += f"; TSV rank {wl.tsv_rank} on the {len(tsv_entries)} MLP matrices"
     rec = {
         "metric": "merged params/sec and achieved HBM GB/s (% of peak), 7B-shaped K=4 merge",
         "value": N / (ms_per_step * 1e-3),
@@ -154,7 +171,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{wl.name}-shaped stack, {len(wl.tensors)} bf16 tensors, {N} params, K={K} deltas "
                                f"({float(wl.delta.p_zero):.0%} zeros), TIES per-tensor density "
-                               f"{float(wl.density)}, lambda 1: TopKMask select + elect + disjoint mean + update",
+                               f"{float(wl.density)}, lambda 1: {what}",
                    "global_batch": 1, "seq_len": 0, "parallelism": "single GPU"},
         "algorithmic_gbps": alg_bytes_step / (ms_per_step * 1e-3) / 1e9,
         "hbm_frac_step": alg_bytes_step / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBPS,
@@ -164,6 +181,8 @@ def main():
                      "achieved": merge_gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": merge_gbps / PEAK_HBM_GBPS, "traffic": traffic},
     }
+    if tsv_entries:
+        rec["tsv_ms"] = tsv_ms
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline()
     print(json.dumps(rec), flush=True)

@@ -8,7 +8,8 @@
 //      L x L core is decomposed by one-sided Jacobi in binary64;
 //   2. concatenation U = [U_1|...|U_K], V likewise, Sigma = blockdiag(Sigma_i);
 //   3. Procrustes orthogonalisation U_perp = P_U Q_U^T = U (U^T U)^{-1/2}, the inverse square
-//      root from the eigen-decomposition of the K r x K r Gram matrix (one-sided Jacobi);
+//      root of the K r x K r Gram matrix by the coupled Newton-Schulz iteration (binary64);
+//      it needs U and V of full column rank (generic experts), else the status reports it;
 //   4. out = round(W_0 + alpha * U_perp Sigma V_perp^T): MFMA bf16 with both operands split
 //      into two bf16 terms (three products), binary32 accumulation, the update fused into the
 //      epilogue.
@@ -67,9 +68,10 @@ struct Mat {
   double* GUp;             // kSlabs x Kr x Kr
   double* GU;              // Kr x Kr
   double* GV;
-  double* JaU; double* JvU; double* JaV; double* JvV;   // Kr x Kr each
-  double* FU;  double* FV;                              // Kr x Kr scaled rotations
-  double* MU;  double* MV;                              // Kr x Kr inverse square roots
+  double* ns[2][5];         // per side (U, V): Newton-Schulz Y0, Z0, Y1, Z1, T (Kr x Kr each)
+  double* eye;              // Kr x Kr identity
+  double* cs;               // 2 scale factors
+  double* MU;  double* MV;  // Kr x Kr inverse square roots
   double* Up;  double* Vp;                              // R x Kr, C x Kr
   uint16_t* ah; uint16_t* al;   // R x ldk split of U_perp Sigma
   uint16_t* bh; uint16_t* bl;   // C x ldk split of V_perp
@@ -77,6 +79,7 @@ struct Mat {
 };
 
 constexpr int kSlabs = 16;
+constexpr int kNsIters = 18;     // coupled Newton-Schulz steps (quadratic convergence from |I - A| < 1)
 
 __device__ __forceinline__ uint16_t bf16_rne_f32(float f) {
   uint32_t b = __float_as_uint(f);
@@ -144,60 +147,93 @@ __global__ void k_split(const Prob* __restrict__ probs, int which, int cur) {
 
 // ---- MFMA products with the delta -----------------------------------------------------------------
 
-// X[out] (R x L) = Delta (R x C) * B (C x L), B = bh + bl.
+// Rows per block of the skinny products: 4 waves x 4 row blocks of 16.
+constexpr int kSkRows = 256;
+
+// X[out] (R x L) = Delta (R x C) * B (C x L), B = bh + bl.  Each wave owns 64 rows (four
+// 16-row blocks) so every right-operand fragment feeds four MFMAs per half.
 template <int NB>
 __global__ void __launch_bounds__(256) k_mfma_nn(const Prob* __restrict__ probs, int out) {
   const Prob& P = probs[blockIdx.z];
   const int64_t R = P.R, C = P.C;
-  const int64_t m0 = (int64_t)blockIdx.x * 64;
+  const int64_t m0 = (int64_t)blockIdx.x * kSkRows;
   if (m0 >= R) return;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
-  const int64_t row = m0 + 16 * w + ln;
+  const int64_t wrow = m0 + 64 * w;
   const bool vec = (C % 8) == 0;
-  f32x4_t acc[NB];
+  f32x4_t acc[4][NB];
 #pragma unroll
-  for (int cb = 0; cb < NB; ++cb) acc[cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  for (int64_t k0 = 0; k0 < C; k0 += 32) {
-    const int64_t k = k0 + 8 * g;
-    const bf16x8_t a = ld_row8(P.delta, R, C, row, k, vec);
+  for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-    for (int cb = 0; cb < NB; ++cb) {
-      const int64_t col = cb * 16 + ln;
-      const bf16x8_t bh = ld_bf16x8(P.bh + col * P.ldb + k);
-      const bf16x8_t bl = ld_bf16x8(P.bl + col * P.ldb + k);
-      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bh, acc[cb], 0, 0, 0);
-      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bl, acc[cb], 0, 0, 0);
+    for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  if (wrow < R) {
+    // the delta stream is software-pipelined: the next step's fragments are in flight while
+    // the current step's MFMAs run
+    bf16x8_t a[4], an[4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) a[rb] = ld_row8(P.delta, R, C, wrow + 16 * rb + ln, 8 * g, vec);
+    for (int64_t k0 = 0; k0 < C; k0 += 32) {
+      const int64_t k = k0 + 8 * g;
+      const bool more = k0 + 32 < C;
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb)
+        an[rb] = more ? ld_row8(P.delta, R, C, wrow + 16 * rb + ln, k + 32, vec) : a[rb];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const int64_t col = cb * 16 + ln;
+        const bf16x8_t bh = ld_bf16x8(P.bh + col * P.ldb + k);
+        const bf16x8_t bl = ld_bf16x8(P.bl + col * P.ldb + k);
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb) {
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rb], bh, acc[rb][cb], 0, 0, 0);
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rb], bl, acc[rb][cb], 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) a[rb] = an[rb];
     }
   }
   double* X = P.X[out];
 #pragma unroll
-  for (int cb = 0; cb < NB; ++cb)
+  for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int64_t r = m0 + 16 * w + 4 * g + e;
-      if (r < R) X[r * P.L + cb * 16 + ln] = (double)acc[cb][e];
-    }
+    for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t r = wrow + 16 * rb + 4 * g + e;
+        if (r < R) X[r * P.L + cb * 16 + ln] = (double)acc[rb][cb][e];
+      }
 }
 
-// Z[out] (C x L) = Delta^T (C x R) * B (R x L), B = bh + bl.  The delta tile is transposed
-// through LDS.
+// Z[out] (C x L) = Delta^T (C x R) * B (R x L), B = bh + bl.  A 32 x 256 tile of the delta
+// is staged in LDS and read transposed; each wave owns 64 output rows.
 template <int NB>
 __global__ void __launch_bounds__(256) k_mfma_tn(const Prob* __restrict__ probs, int out) {
-  __shared__ uint16_t tile[32][64 + 2];
+  __shared__ uint16_t tile[32][kSkRows + 2];
   const Prob& P = probs[blockIdx.z];
   const int64_t R = P.R, C = P.C;
-  const int64_t i0 = (int64_t)blockIdx.x * 64;
+  const int64_t i0 = (int64_t)blockIdx.x * kSkRows;
   if (i0 >= C) return;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
   const bool vec = (C % 8) == 0;
-  const int tr = threadIdx.x >> 3, tc = (threadIdx.x & 7) * 8;
-  f32x4_t acc[NB];
+  f32x4_t acc[4][NB];
 #pragma unroll
-  for (int cb = 0; cb < NB; ++cb) acc[cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // the next 32 x 256 delta tile is loaded into registers while the current one is used
+  bf16x8_t pre[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int piece = threadIdx.x + 256 * q;
+    pre[q] = ld_row8(P.delta, R, C, piece >> 5, i0 + (piece & 31) * 8, vec);
+  }
   for (int64_t k0 = 0; k0 < R; k0 += 32) {
-    {
-      const bf16x8_t v = ld_row8(P.delta, R, C, k0 + tr, i0 + tc, vec);
-      const uint4 u = __builtin_bit_cast(uint4, v);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int piece = threadIdx.x + 256 * q;
+      const int tr = piece >> 5, tc = (piece & 31) * 8;
+      const uint4 u = __builtin_bit_cast(uint4, pre[q]);
       const uint32_t ws[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -206,29 +242,45 @@ __global__ void __launch_bounds__(256) k_mfma_tn(const Prob* __restrict__ probs,
       }
     }
     __syncthreads();
-    uint16_t t8[8];
+    if (k0 + 32 < R) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) t8[e] = tile[8 * g + e][16 * w + ln];
-    const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *(uint4*)t8);
+      for (int q = 0; q < 4; ++q) {
+        const int piece = threadIdx.x + 256 * q;
+        pre[q] = ld_row8(P.delta, R, C, k0 + 32 + (piece >> 5), i0 + (piece & 31) * 8, vec);
+      }
+    }
+    bf16x8_t a[4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+      uint16_t t8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t8[e] = tile[8 * g + e][64 * w + 16 * rb + ln];
+      a[rb] = __builtin_bit_cast(bf16x8_t, *(uint4*)t8);
+    }
     const int64_t k = k0 + 8 * g;
 #pragma unroll
     for (int cb = 0; cb < NB; ++cb) {
       const int64_t col = cb * 16 + ln;
       const bf16x8_t bh = ld_bf16x8(P.bh + col * P.ldb + k);
       const bf16x8_t bl = ld_bf16x8(P.bl + col * P.ldb + k);
-      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bh, acc[cb], 0, 0, 0);
-      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bl, acc[cb], 0, 0, 0);
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rb], bh, acc[rb][cb], 0, 0, 0);
+        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rb], bl, acc[rb][cb], 0, 0, 0);
+      }
     }
     __syncthreads();
   }
   double* Z = P.Z[out];
 #pragma unroll
-  for (int cb = 0; cb < NB; ++cb)
+  for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int64_t r = i0 + 16 * w + 4 * g + e;
-      if (r < C) Z[r * P.L + cb * 16 + ln] = (double)acc[cb][e];
-    }
+    for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t r = i0 + 64 * w + 16 * rb + 4 * g + e;
+        if (r < C) Z[r * P.L + cb * 16 + ln] = (double)acc[rb][cb][e];
+      }
 }
 
 // ---- Cholesky-QR pieces ------------------------------------------------------------------------------
@@ -391,19 +443,6 @@ __global__ void k_sigma(const Prob* __restrict__ probs, Mat* mats, int K, int r)
 
 // ---- orthogonalisation (Procrustes / Loewdin) ---------------------------------------------------
 
-// F = Jv diag(1 / sqrt(lambda)), lambda_j = |column j of Ja| (eigenvalues of the SPD Gram)
-__global__ void __launch_bounds__(1024) k_inv_sqrt_scale(double* F, const double* Ja, const double* Jv, int64_t n) {
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  for (int64_t j = wid; j < n; j += nw) {
-    double s = 0.0;
-    for (int64_t t = lane; t < n; t += 64) s += Ja[j * n + t] * Ja[j * n + t];
-    s = wave_sum_f64(s);
-    const double lam = sqrt(s);
-    const double sc = (lam > 0.0) ? 1.0 / sqrt(lam) : 0.0;
-    for (int64_t t = lane; t < n; t += 64) F[j * n + t] = Jv[j * n + t] * sc;
-  }
-}
-
 // bf16 hi/lo split of rows: dst (rows x ldk) = src (rows x Kr, row stride ldsrc) * (scale? s[col] : 1)
 __global__ void k_split_rows(uint16_t* __restrict__ hi, uint16_t* __restrict__ lo, const double* __restrict__ src,
                              int64_t rows, int64_t Kr, int64_t ldsrc, int64_t ldk, const double* __restrict__ scale) {
@@ -419,42 +458,163 @@ __global__ void k_split_rows(uint16_t* __restrict__ hi, uint16_t* __restrict__ l
 }
 
 // out = round(W0 + alpha * A B^T), A = ah + al (R x ldk), B = bh + bl (C x ldk); three MFMA
-// products per step (hi*hi, hi*lo, lo*hi).  64 x 64 output tile per block.
+// products per step (hi*hi, hi*lo, lo*hi).  128 x 128 output tile per block: each wave owns
+// 32 rows; the 128 x 32 slice of B (both halves) is staged in LDS once per step.
+constexpr int kRecT = 128;
 __global__ void __launch_bounds__(256) k_mfma_recon(const Mat* __restrict__ mats) {
+  __shared__ uint4 bsh[2][kRecT][4];     // [half][column][k-group of 8]
   const Mat& M = mats[blockIdx.z];
-  const int64_t m0 = (int64_t)blockIdx.x * 64, n0 = (int64_t)blockIdx.y * 64;
+  const int64_t m0 = (int64_t)blockIdx.x * kRecT, n0 = (int64_t)blockIdx.y * kRecT;
   if (m0 >= M.R || n0 >= M.C) return;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
-  const int64_t arow = min(M.R - 1, m0 + 16 * w + ln);
-  f32x4_t acc[4];
+  f32x4_t acc[2][8];
 #pragma unroll
-  for (int cb = 0; cb < 4; ++cb) acc[cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb) acc[rb][cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  int64_t arow[2];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) arow[rb] = min(M.R - 1, m0 + 32 * w + 16 * rb + ln);
   for (int64_t k0 = 0; k0 < M.ldk; k0 += 32) {
-    const int64_t k = k0 + 8 * g;
-    const bf16x8_t a_h = ld_bf16x8(M.ah + arow * M.ldk + k);
-    const bf16x8_t a_l = ld_bf16x8(M.al + arow * M.ldk + k);
+    // stage B: 2 halves x 128 columns x 4 k-groups = 1024 16-byte pieces, four per thread
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) {
-      const int64_t col = min(M.C - 1, n0 + cb * 16 + ln);
-      const bf16x8_t b_h = ld_bf16x8(M.bh + col * M.ldk + k);
-      const bf16x8_t b_l = ld_bf16x8(M.bl + col * M.ldk + k);
-      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_h, b_h, acc[cb], 0, 0, 0);
-      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_h, b_l, acc[cb], 0, 0, 0);
-      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_l, b_h, acc[cb], 0, 0, 0);
+    for (int q = 0; q < 4; ++q) {
+      const int piece = threadIdx.x + 256 * q;
+      const int half = piece >> 9, col = (piece >> 2) & 127, kg = piece & 3;
+      const int64_t gc = min(M.C - 1, n0 + col);
+      const uint16_t* src = (half ? M.bl : M.bh) + gc * M.ldk + k0 + 8 * kg;
+      bsh[half][col][kg] = *(const uint4*)src;
     }
-  }
+    __syncthreads();
+    const int64_t k = k0 + 8 * g;
+    bf16x8_t ah[2], al[2];
 #pragma unroll
-  for (int cb = 0; cb < 4; ++cb)
+    for (int rb = 0; rb < 2; ++rb) {
+      ah[rb] = ld_bf16x8(M.ah + arow[rb] * M.ldk + k);
+      al[rb] = ld_bf16x8(M.al + arow[rb] * M.ldk + k);
+    }
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int64_t r = m0 + 16 * w + 4 * g + e, c = n0 + cb * 16 + ln;
-      if (r < M.R && c < M.C) {
-        const int64_t idx = r * M.C + c;
-        const double v = (double)f32_of_bf16(M.w0[idx]) + M.alpha * (double)acc[cb][e];
-        M.out[idx] = (uint16_t)f64_to_bf16_rne(v);
-        if (M.dhat) M.dhat[idx] = acc[cb][e];
+    for (int cb = 0; cb < 8; ++cb) {
+      const bf16x8_t bh = __builtin_bit_cast(bf16x8_t, bsh[0][cb * 16 + ln][g]);
+      const bf16x8_t bl = __builtin_bit_cast(bf16x8_t, bsh[1][cb * 16 + ln][g]);
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[rb], bh, acc[rb][cb], 0, 0, 0);
+        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[rb], bl, acc[rb][cb], 0, 0, 0);
+        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[rb], bh, acc[rb][cb], 0, 0, 0);
       }
     }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t r = m0 + 32 * w + 16 * rb + 4 * g + e, c = n0 + cb * 16 + ln;
+        if (r < M.R && c < M.C) {
+          const int64_t idx = r * M.C + c;
+          const double v = (double)f32_of_bf16(M.w0[idx]) + M.alpha * (double)acc[rb][cb][e];
+          M.out[idx] = (uint16_t)f64_to_bf16_rne(v);
+          if (M.dhat) M.dhat[idx] = acc[rb][cb][e];
+        }
+      }
+}
+
+// ---- per-matrix helpers, batched over the matrices of a chunk (grid.y / grid.x = matrix) ----------
+
+// G = sum of the Gram partials of one side for every matrix
+__global__ void k_sum_gram(const Mat* __restrict__ mats, int side) {
+  const Mat& M = mats[blockIdx.y];
+  const int64_t n = M.Kr * M.Kr;
+  double* G = side ? M.GV : M.GU;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
+    double acc = 0.0;
+    for (int z = 0; z < kSlabs; ++z) acc = acc + M.GUp[(int64_t)z * n + e];
+    G[e] = acc;
+  }
+}
+
+// bf16 hi/lo split of U_perp Sigma (side 0) or V_perp (side 1) for every matrix
+__global__ void k_split_mats(const Mat* __restrict__ mats, int side) {
+  const Mat& M = mats[blockIdx.y];
+  const int64_t rows = side ? M.C : M.R;
+  const double* src = side ? M.Vp : M.Up;
+  uint16_t* hi = side ? M.bh : M.ah;
+  uint16_t* lo = side ? M.bl : M.al;
+  const int64_t total = rows * M.ldk;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = e / M.ldk, c = e - r * M.ldk;
+    float v = 0.0f;
+    if (c < M.Kr) v = (float)(src[r * M.Kr + c] * (side ? 1.0 : M.Sig[c]));
+    const uint16_t h = bf16_rne_f32(v);
+    hi[e] = h;
+    lo[e] = bf16_rne_f32(v - f32_of_bf16(h));
+  }
+}
+
+// ---- inverse square root of the SPD Gram matrices (coupled Newton-Schulz) ------------------------
+// Higham, "Functions of Matrices" (2008), Sec. 6.7: with A = G / c scaled so that its
+// spectrum lies in (0, 1], Y_0 = A, Z_0 = I and T_k = (3I - Z_k Y_k) / 2, Y_{k+1} = Y_k T_k,
+// Z_{k+1} = T_k Z_k converge quadratically to A^{1/2} and A^{-1/2}.
+
+// c = max row sum of |G| (>= the largest eigenvalue); Y = G / c; Z = I; also writes I into `eye`.
+__global__ void __launch_bounds__(256) k_ns_init(const Mat* __restrict__ mats, int side) {
+  __shared__ double red[256];
+  const Mat& M = mats[blockIdx.x];
+  const int64_t n = M.Kr;
+  const double* G = side ? M.GV : M.GU;
+  double* Y = M.ns[side][0];
+  double* Z = M.ns[side][1];
+  double* eye = M.eye;
+  double* cscale = M.cs + side;
+  double m = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += blockDim.x) {
+    double s = 0.0;
+    for (int64_t j = 0; j < n; ++j) s += fabs(G[i * n + j]);
+    m = fmax(m, s);
+  }
+  red[threadIdx.x] = m;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + o]);
+    __syncthreads();
+  }
+  const double c = (red[0] > 0.0) ? red[0] : 1.0;
+  if (threadIdx.x == 0) *cscale = c;
+  for (int64_t e = threadIdx.x; e < n * n; e += blockDim.x) {
+    const double id = ((e / n) == (e % n)) ? 1.0 : 0.0;
+    Y[e] = G[e] / c;
+    Z[e] = id;
+    eye[e] = id;
+  }
+}
+
+// T = 1.5 I - 0.5 (Z Y) is formed by a GEMM with beta on a copy of I; this copies I into T.
+__global__ void k_copy_jobs(double* const* dst, const double* const* src, int64_t n) {
+  const double* a = src[blockIdx.y];
+  double* b = dst[blockIdx.y];
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x)
+    b[e] = a[e];
+}
+
+// M = Z / sqrt(c), and flag non-convergence (|T - I| large at the last step).
+__global__ void __launch_bounds__(256) k_ns_finish(const Mat* __restrict__ mats, int par, uint32_t* status) {
+  const Mat& M = mats[blockIdx.x];
+  const int side = blockIdx.y;
+  const int64_t n = M.Kr;
+  double* Mout = side ? M.MV : M.MU;
+  const double* Z = M.ns[side][2 * par + 1];
+  const double* T = M.ns[side][4];
+  const double inv = 1.0 / sqrt(M.cs[side]);
+  bool bad = false;
+  for (int64_t e = threadIdx.x; e < n * n; e += blockDim.x) {
+    Mout[e] = Z[e] * inv;
+    const double id = ((e / n) == (e % n)) ? 1.0 : 0.0;
+    bad |= !(fabs(T[e] - id) < 1e-6);
+  }
+  if (bad) flag_status(status, kStatusInternal);
 }
 
 // ---- host side ----------------------------------------------------------------------------------
@@ -511,12 +671,10 @@ void carve_mat(Carver& cv, Mat& M, const Sizes& z) {
   M.GUp = cv.take<double>((int64_t)kSlabs * z.Kr * z.Kr);
   M.GU = cv.take<double>(z.Kr * z.Kr);
   M.GV = cv.take<double>(z.Kr * z.Kr);
-  M.JaU = cv.take<double>(z.Kr * z.Kr);
-  M.JvU = cv.take<double>(z.Kr * z.Kr);
-  M.JaV = cv.take<double>(z.Kr * z.Kr);
-  M.JvV = cv.take<double>(z.Kr * z.Kr);
-  M.FU = cv.take<double>(z.Kr * z.Kr);
-  M.FV = cv.take<double>(z.Kr * z.Kr);
+  for (int sd = 0; sd < 2; ++sd)
+    for (int q = 0; q < 5; ++q) M.ns[sd][q] = cv.take<double>(z.Kr * z.Kr);
+  M.eye = cv.take<double>(z.Kr * z.Kr);
+  M.cs = cv.take<double>(2);
   M.MU = cv.take<double>(z.Kr * z.Kr);
   M.MV = cv.take<double>(z.Kr * z.Kr);
   M.Up = cv.take<double>(z.R * z.Kr);
@@ -551,17 +709,18 @@ size_t table_bytes(int nm, int K) {
   b += align_up(sizeof(Mat) * nm, 256);
   b += align_up(sizeof(JacobiJob) * std::max(np, 2 * nm), 256);
   b += align_up(sizeof(double*) * 3 * np, 256);
-  b += 8 * align_up(sizeof(GemmJob) * (size_t)std::max(np, kSlabs * nm * 2), 256);
+  b += 12 * align_up(sizeof(GemmJob) * (size_t)std::max(np, kSlabs * nm * 2), 256);
+  b += 2 * align_up(sizeof(double*) * 2 * nm, 256);
   return b;
 }
 
 template <int NB>
 void launch_nn(const Prob* d, int np, int64_t maxR, int out, hipStream_t s) {
-  k_mfma_nn<NB><<<dim3((unsigned)((maxR + 63) / 64), 1, (unsigned)np), 256, 0, s>>>(d, out);
+  k_mfma_nn<NB><<<dim3((unsigned)((maxR + kSkRows - 1) / kSkRows), 1, (unsigned)np), 256, 0, s>>>(d, out);
 }
 template <int NB>
 void launch_tn(const Prob* d, int np, int64_t maxC, int out, hipStream_t s) {
-  k_mfma_tn<NB><<<dim3((unsigned)((maxC + 63) / 64), 1, (unsigned)np), 256, 0, s>>>(d, out);
+  k_mfma_tn<NB><<<dim3((unsigned)((maxC + kSkRows - 1) / kSkRows), 1, (unsigned)np), 256, 0, s>>>(d, out);
 }
 template <int T>
 void launch_gram(const Prob* d, int np, int which, int cur, hipStream_t s) {
@@ -623,8 +782,10 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     Mat* d_mat = cv.take<Mat>(nm);
     JacobiJob* d_jobs = cv.take<JacobiJob>(std::max(np, 2 * nm));
     double** d_ptrs = cv.take<double*>(3 * np);
-    GemmJob* d_gj[8];
-    for (int q = 0; q < 8; ++q) d_gj[q] = cv.take<GemmJob>(std::max(np, kSlabs * nm * 2));
+    GemmJob* d_gj[12];
+    for (int q = 0; q < 12; ++q) d_gj[q] = cv.take<GemmJob>(std::max(np, kSlabs * nm * 2));
+    const double** d_nsrc = cv.take<const double*>(2 * nm);
+    double** d_ndst = cv.take<double*>(2 * nm);
     cv.off = table_bytes(nm, K);
     std::vector<Prob> hp(np);
     std::vector<Mat> hm(nm);
@@ -664,8 +825,10 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     const int NB = (int)(L / 16);
     const int64_t maxM = std::max(maxR, maxC);
     // gemm job tables: 0 U_i = X Ut[:, :r]; 1 V_i = Z Vt[:, :r]; 2 GU slabs; 3 GV slabs;
-    // 4 M = F Jv^T (U and V); 5 U_perp = U M_U, V_perp = V M_V
-    std::vector<GemmJob> gj[6];
+    // 5 U_perp = U M_U, V_perp = V M_V; 6..11 Newton-Schulz steps (T, Y, Z) for parities 0, 1
+    std::vector<GemmJob> gj[12];
+    std::vector<const double*> ns_src;
+    std::vector<double*> ns_dst;
     for (int p = 0; p < np; ++p) {
       const Prob& P = hp[p];
       const Mat& M = hm[p / K];
@@ -685,10 +848,23 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
         gj[3].push_back(GemmJob{M.V + v0 * M.ldk, M.V + v0 * M.ldk, M.GUp + (int64_t)z * M.Kr * M.Kr, 1, M.ldk,
                                 M.ldk, 1, M.Kr, 1, M.Kr, M.Kr, v1 - v0, 1.0, 0.0});
       }
-      // M = F Jv^T: F (col-major n x n): A(i,k) = F[i + k n]; B(k,j) = Jv^T(k,j) = Jv[k + j n]... Jv col-major:
-      // Jv(j,k) at Jv[j + k n]; B(k,j) = Jv(j,k) = Jv[j + k n] -> bs0 = n, bs1 = 1
-      gj[4].push_back(GemmJob{M.FU, M.JvU, M.MU, 1, M.Kr, M.Kr, 1, M.Kr, 1, M.Kr, M.Kr, M.Kr, 1.0, 0.0});
-      gj[4].push_back(GemmJob{M.FV, M.JvV, M.MV, 1, M.Kr, M.Kr, 1, M.Kr, 1, M.Kr, M.Kr, M.Kr, 1.0, 0.0});
+      // Newton-Schulz on both sides: parity a uses (Y_a, Z_a) -> (Y_b, Z_b), b = 1 - a
+      const int64_t n = M.Kr;
+      for (int sd = 0; sd < 2; ++sd) {
+        double* const* q = M.ns[sd];
+        for (int a = 0; a < 2; ++a) {
+          double* Ya = q[2 * a];
+          double* Za = q[2 * a + 1];
+          double* Yb = q[2 * (1 - a)];
+          double* Zb = q[2 * (1 - a) + 1];
+          double* T = q[4];
+          gj[6 + 3 * a].push_back(GemmJob{Za, Ya, T, n, 1, n, 1, n, 1, n, n, n, -0.5, 1.5});   // T = 1.5 I - Z Y / 2
+          gj[7 + 3 * a].push_back(GemmJob{Ya, T, Yb, n, 1, n, 1, n, 1, n, n, n, 1.0, 0.0});    // Y' = Y T
+          gj[8 + 3 * a].push_back(GemmJob{T, Za, Zb, n, 1, n, 1, n, 1, n, n, n, 1.0, 0.0});    // Z' = T Z
+        }
+        ns_src.push_back(M.eye);
+        ns_dst.push_back(q[4]);
+      }
       gj[5].push_back(GemmJob{M.U, M.MU, M.Up, M.ldk, 1, M.Kr, 1, M.Kr, 1, M.R, M.Kr, M.Kr, 1.0, 0.0});
       gj[5].push_back(GemmJob{M.V, M.MV, M.Vp, M.ldk, 1, M.Kr, 1, M.Kr, 1, M.C, M.Kr, M.Kr, 1.0, 0.0});
     }
@@ -701,8 +877,10 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
       Mat* h_mat = hc.take<Mat>(nm);
       hc.take<JacobiJob>(std::max(np, 2 * nm));
       double** h_ptrs = hc.take<double*>(3 * np);
-      GemmJob* h_gj[8];
-      for (int q = 0; q < 8; ++q) h_gj[q] = hc.take<GemmJob>(std::max(np, kSlabs * nm * 2));
+      GemmJob* h_gj[12];
+      for (int q = 0; q < 12; ++q) h_gj[q] = hc.take<GemmJob>(std::max(np, kSlabs * nm * 2));
+      const double** h_nsrc = hc.take<const double*>(2 * nm);
+      double** h_ndst = hc.take<double*>(2 * nm);
       std::memcpy(h_prob, hp.data(), sizeof(Prob) * np);
       std::memcpy(h_mat, hm.data(), sizeof(Mat) * nm);
       for (int p = 0; p < np; ++p) {
@@ -710,13 +888,16 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
         h_ptrs[np + p] = hp[p].Vt;
         h_ptrs[2 * np + p] = hp[p].St;
       }
-      for (int q = 0; q < 6; ++q) std::memcpy(h_gj[q], gj[q].data(), sizeof(GemmJob) * gj[q].size());
+      for (int q = 0; q < 12; ++q)
+        if (!gj[q].empty()) std::memcpy(h_gj[q], gj[q].data(), sizeof(GemmJob) * gj[q].size());
+      std::memcpy(h_nsrc, ns_src.data(), sizeof(double*) * ns_src.size());
+      std::memcpy(h_ndst, ns_dst.data(), sizeof(double*) * ns_dst.size());
     }
     TS_TRY(hipMemcpyAsync(ws, host.data(), tb, hipMemcpyHostToDevice, s));
     const unsigned gx = grid_for(L * rup(maxM, 32));
-    auto cholqr = [&](int which, int& cur, int save_first, int accum_second) {
+    auto cholqr = [&](int which, int& cur, int save_first, int accum_second, int passes) {
       const int64_t mm = which ? maxC : maxR;
-      for (int pass = 0; pass < 2; ++pass) {
+      for (int pass = 0; pass < passes; ++pass) {
         DISPATCH_NB(NB, launch_gram, d_prob, np, which, cur, s);
         const size_t shb = sizeof(double) * L * L;
         k_chol<<<np, 256, shb, s>>>(d_prob, (pass == 0) ? save_first : 0, (pass == 1) ? accum_second : 0, status);
@@ -727,63 +908,54 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     // 1. range finder with subspace iteration
     int cx = 0, cz = 0;
     k_omega<<<dim3(gx, np), 256, 0, s>>>(d_prob);
+    // Cholesky-QR2 where orthogonality is carried forward (first sketch, final factor); one
+    // pass inside the power iteration, whose next product and QR absorb its rounding
     DISPATCH_NB(NB, launch_nn, d_prob, np, maxR, cx, s);
-    cholqr(0, cx, 0, 0);
+    cholqr(0, cx, 0, 0, 2);
     for (int it = 0; it < kPowerIters; ++it) {
       k_split<<<dim3(gx, np), 256, 0, s>>>(d_prob, 0, cx);
       DISPATCH_NB(NB, launch_tn, d_prob, np, maxC, cz, s);
-      cholqr(1, cz, 0, 0);
+      cholqr(1, cz, 0, 0, 1);
       k_split<<<dim3(gx, np), 256, 0, s>>>(d_prob, 1, cz);
       DISPATCH_NB(NB, launch_nn, d_prob, np, maxR, cx, s);
-      cholqr(0, cx, 0, 0);
+      cholqr(0, cx, 0, 0, 1);
     }
     // 2. B^T = Delta^T Q, its QR (R2 accumulated), SVD of the L x L core R2^T
     k_split<<<dim3(gx, np), 256, 0, s>>>(d_prob, 0, cx);
     DISPATCH_NB(NB, launch_tn, d_prob, np, maxC, cz, s);
-    cholqr(1, cz, 1, 1);
+    cholqr(1, cz, 1, 1, 2);
     k_core_load<<<np, 256, 0, s>>>(d_prob, d_jobs);
     k_jacobi<<<np, kJacobiThreads, 0, s>>>(d_jobs, status);
     k_svd_finalize<<<np, 1024, (sizeof(double) + sizeof(int)) * L, s>>>(d_jobs, d_ptrs, d_ptrs + np, d_ptrs + 2 * np);
-    // U_i = Q Ut[:, :r], V_i = Q2 Vt[:, :r]; both factors sit in buffer 0 after an even number of QR passes
+    // U_i = Q Ut[:, :r], V_i = Q2 Vt[:, :r]: both factors end in buffer 0 (an even number of QR
+    // passes: 2 + kPowerIters for X, kPowerIters + 2 for Z)
+    static_assert(kPowerIters % 2 == 0, "ping-pong parity");
     if (cx != 0 || cz != 0) return ISO_ERR_INTERNAL;
     k_gemm_jobs<<<dim3((unsigned)((maxR + 63) / 64), (unsigned)((r + 63) / 64), (unsigned)np), 256, 0, s>>>(d_gj[0]);
     k_gemm_jobs<<<dim3((unsigned)((maxC + 63) / 64), (unsigned)((r + 63) / 64), (unsigned)np), 256, 0, s>>>(d_gj[1]);
     k_sigma<<<np, 64, 0, s>>>(d_prob, d_mat, K, r);
-    // 3. Procrustes orthogonalisation of U and V
+    // 3. Procrustes orthogonalisation of U and V: U_perp = U (U^T U)^{-1/2}
     const unsigned tk = (unsigned)((Kr + 63) / 64);
     for (int side = 0; side < 2; ++side) {
       k_gemm_jobs<<<dim3(tk, tk, (unsigned)(kSlabs * nm)), 256, 0, s>>>(d_gj[2 + side]);
-      for (int m = 0; m < nm; ++m) {
-        const Mat& M = hm[m];
-        double* G = side ? M.GV : M.GU;
-        k_sum_parts<<<grid_for(Kr * Kr), 256, 0, s>>>(G, M.GUp, kSlabs, Kr * Kr, Kr * Kr);
-        k_copy<<<grid_for(Kr * Kr), 256, 0, s>>>(side ? M.JaV : M.JaU, G, Kr * Kr);
-      }
+      k_sum_gram<<<dim3(grid_for(Kr * Kr), (unsigned)nm), 256, 0, s>>>(d_mat, side);
+      k_ns_init<<<nm, 256, 0, s>>>(d_mat, side);
     }
-    {
-      std::vector<JacobiJob> jj(2 * nm);
-      for (int m = 0; m < nm; ++m) {
-        jj[2 * m] = JacobiJob{hm[m].JaU, hm[m].JvU, Kr, Kr};
-        jj[2 * m + 1] = JacobiJob{hm[m].JaV, hm[m].JvV, Kr, Kr};
-      }
-      TS_TRY(hipMemcpyAsync(d_jobs, jj.data(), sizeof(JacobiJob) * 2 * nm, hipMemcpyHostToDevice, s));
-      k_jacobi<<<2 * nm, kJacobiThreads, 0, s>>>(d_jobs, status);
-      for (int m = 0; m < nm; ++m) {
-        k_inv_sqrt_scale<<<1, 1024, 0, s>>>(hm[m].FU, hm[m].JaU, hm[m].JvU, Kr);
-        k_inv_sqrt_scale<<<1, 1024, 0, s>>>(hm[m].FV, hm[m].JaV, hm[m].JvV, Kr);
-      }
-      k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[4]);
-      k_gemm_jobs<<<dim3((unsigned)((maxM + 63) / 64), tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[5]);
-      // the Jacobi job table must not be overwritten by the next chunk before this one ran
-      TS_TRY(hipStreamSynchronize(s));
+    int par = 0;
+    for (int it = 0; it < kNsIters; ++it) {
+      k_copy_jobs<<<dim3(grid_for(Kr * Kr), (unsigned)(2 * nm)), 256, 0, s>>>(d_ndst, d_nsrc, Kr * Kr);
+      k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[6 + 3 * par]);
+      k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[7 + 3 * par]);
+      k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[8 + 3 * par]);
+      par = 1 - par;
     }
+    k_ns_finish<<<dim3((unsigned)nm, 2), 256, 0, s>>>(d_mat, par, status);
+    k_gemm_jobs<<<dim3((unsigned)((maxM + 63) / 64), tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[5]);
     // 4. reconstruction with the update fused
-    for (int m = 0; m < nm; ++m) {
-      const Mat& M = hm[m];
-      k_split_rows<<<grid_for(M.R * M.ldk), 256, 0, s>>>(M.ah, M.al, M.Up, M.R, M.Kr, M.Kr, M.ldk, M.Sig);
-      k_split_rows<<<grid_for(M.C * M.ldk), 256, 0, s>>>(M.bh, M.bl, M.Vp, M.C, M.Kr, M.Kr, M.ldk, nullptr);
-    }
-    k_mfma_recon<<<dim3((unsigned)((maxR + 63) / 64), (unsigned)((maxC + 63) / 64), (unsigned)nm), 256, 0, s>>>(d_mat);
+    k_split_mats<<<dim3(grid_for(maxR * rup(Kr, 32)), (unsigned)nm), 256, 0, s>>>(d_mat, 0);
+    k_split_mats<<<dim3(grid_for(maxC * rup(Kr, 32)), (unsigned)nm), 256, 0, s>>>(d_mat, 1);
+    k_mfma_recon<<<dim3((unsigned)((maxR + kRecT - 1) / kRecT), (unsigned)((maxC + kRecT - 1) / kRecT), (unsigned)nm),
+                   256, 0, s>>>(d_mat);
     TS_TRY(hipGetLastError());
     TS_TRY(hipStreamSynchronize(s));
   }
