@@ -20,6 +20,7 @@
 //    (S + gamma*sum|x|)/2 are exact real values and equal the binary64 sequence.
 #include "iso_device.h"
 #include "iso_kernels.h"
+#include "iso_merge_math.h"
 
 namespace iso {
 
@@ -29,44 +30,6 @@ constexpr int64_t kMergeMaxGrid = 0;  // 0: one block per tile; else blocks loop
 
 int64_t merge_tile_elems(int dt) {
   return (int64_t)kMergeThreads * kMergeVPT * (dt == ISO_BF16 ? Fmt<ISO_BF16>::kPerVec : Fmt<ISO_F32>::kPerVec);
-}
-
-__device__ __forceinline__ void two_sum(double a, double b, double& s, double& e) {
-  s = a + b;
-  double bb = s - a;
-  e = (a - (s - bb)) + (b - bb);
-}
-
-// Exact sign of x[0] + ... + x[K-1] (Shewchuk 1997, Grow-Expansion).
-template <int K>
-__device__ __forceinline__ int exact_sign(const double (&x)[K]) {
-  double e[K];
-#pragma unroll
-  for (int i = 0; i < K; ++i) {
-    double q = x[i];
-#pragma unroll
-    for (int j = 0; j < i; ++j) {
-      double s, h;
-      two_sum(q, e[j], s, h);
-      e[j] = h;
-      q = s;
-    }
-    e[i] = q;
-  }
-  int sg = 0;
-#pragma unroll
-  for (int i = 0; i < K; ++i)
-    if (e[i] != 0.0) sg = (e[i] > 0.0) ? 1 : -1;
-  return sg;
-}
-
-// t / n for a count n >= 1: powers of two scale exactly, others divide (IEEE).
-__device__ __forceinline__ double div_count(double t, int n) {
-  if ((n & (n - 1)) == 0) {
-    int s = __ffs(n) - 1;
-    return t * __hiloint2double((1023 - s) << 20, 0);
-  }
-  return t / (double)n;
 }
 
 template <int K>
@@ -94,58 +57,15 @@ __device__ __forceinline__ double merge_coord(const uint32_t (&b)[K], int64_t id
                                               double lambda, double eps, int& gamma, uint32_t& kacc) {
   double t;
   if constexpr (MODE == ISO_MERGE_TIES) {
-    if constexpr (FAST) {
-      float x[K];
+    uint32_t km = 0;
 #pragma unroll
-      for (int i = 0; i < K; ++i) {
-        bool k = kept<DT, K, STRADDLE>(th, i, key_of<DT>(b[i]), idx);
-        x[i] = k ? f32_from_bits(b[i] << 16) : 0.0f;
-      }
-      float S = x[0], A = fabsf(x[0]);
-      int np = x[0] > 0.0f, nn = x[0] < 0.0f;
-#pragma unroll
-      for (int i = 1; i < K; ++i) {
-        S = S + x[i];
-        A = A + fabsf(x[i]);
-        np += x[i] > 0.0f;
-        nn += x[i] < 0.0f;
-      }
-      float g = (S > 0.0f) ? 1.0f : ((S < 0.0f) ? -1.0f : 0.0f);
-      float ts = (S + g * A) * 0.5f;                  // exact: sum over the agreeing set
-      int n = (S > 0.0f) ? np : ((S < 0.0f) ? nn : 0);
-      gamma = (int)g;
-      t = (n == 0) ? 0.0 : div_count((double)ts, n);
-    } else {
-      double x[K];
-#pragma unroll
-      for (int i = 0; i < K; ++i) {
-        uint32_t key = key_of<DT>(b[i]);
-        kacc = max(kacc, key);
-        bool k = kept<DT, K, STRADDLE>(th, i, key, idx);
-        x[i] = k ? bits_to_f64<DT>(b[i]) : 0.0;
-      }
-      double S = x[0], A = fabs(x[0]);
-#pragma unroll
-      for (int i = 1; i < K; ++i) {
-        S = S + x[i];
-        A = A + fabs(x[i]);
-      }
-      int g;
-      if (fabs(S) > A * ((double)K * 0x1p-52)) g = (S > 0.0) ? 1 : -1;
-      else if (A == 0.0) g = 0;
-      else g = exact_sign<K>(x);
-      const double gd = (double)g;
-      double M = 0.0;
-      int n = 0;
-#pragma unroll
-      for (int i = 0; i < K; ++i) {
-        double y = gd * x[i];
-        M = M + fmax(y, 0.0);
-        n += y > 0.0;
-      }
-      gamma = g;
-      t = (n == 0) ? 0.0 : div_count(gd * M, n);
+    for (int i = 0; i < K; ++i) {
+      const uint32_t key = key_of<DT>(b[i]);
+      if constexpr (!FAST) kacc = max(kacc, key);
+      km |= (uint32_t)kept<DT, K, STRADDLE>(th, i, key, idx) << i;
     }
+    if constexpr (FAST) t = ties_fast_bf16<K>(b, km, gamma);
+    else t = ties_general<DT, K>(b, km, gamma);
   } else if constexpr (MODE == ISO_MERGE_TA) {
     t = 0.0;
 #pragma unroll
