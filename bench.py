@@ -1,10 +1,12 @@
 """Benchmark of the element-wise merge/update hot path on one MI355X.
 
 One step = the whole path over the 7B-shaped stack (28 layers of q/k/v/o/gate/up/down,
-embedding and lm_head: 198 bf16 tensors, 7,615,283,200 parameters), K = 4 deltas:
-TopKMask selection of every delta (iso_topk_mask), then sign election + disjoint mean +
-theta_0 + lambda*tau in one fused pass (iso_update FUSED, TIES, lambda = 1).  Inputs are
-synthetic (seeded generator, written straight into HBM) and resident before timing.
+embedding and lm_head: 198 bf16 tensors, 7,615,283,200 parameters), K = 4 deltas, in one
+call: TopKMask selection of every delta, sign election, disjoint mean and
+theta_0 + lambda*tau (iso_update FUSED, TIES, lambda = 1, selection inside the call).  The
+default single-read path reads each delta and the base once; --path two-pass times the
+histogram select (iso_topk_mask) followed by the merge pass instead.  Inputs are synthetic
+(seeded generator, written straight into HBM) and resident before timing.
 
 Prints one JSON line.  Only one GPU is used; --gpus above 1 exits with a message.
 """
@@ -20,54 +22,55 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCES = {"single-read": ("iso_fused.hip", "iso_merge_math.h", "iso_device.h"),
+                  "two-pass": ("iso_merge.hip", "iso_merge_math.h", "iso_device.h")}
+KERNEL_NAMES = {"single-read": "k_fs_main (single read: bracketed TopKMask + elect + disjoint mean + update)",
+                "two-pass": "k_merge (elect + disjoint mean + update, thresholds known)"}
 
 
-def kernel_source_hash():
+def kernel_source_hash(path):
     h = hashlib.sha256()
-    for f in ("iso_merge.hip", "iso_device.h"):
+    for f in KERNEL_SOURCES[path]:
         h.update(open(os.path.join(ROOT, "paper_2607_19331_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(config_name):
-    """HBM bytes per merge launch from the committed rocprofv3 counter runs, if they
-    were taken on the current kernel source (else None)."""
+def measured_traffic(key, path):
+    """HBM bytes per launch of the main kernel from the committed rocprofv3 counter runs,
+    if they were taken on the current kernel source (else None)."""
     try:
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
-    r = rec.get(config_name)
-    if not r or r.get("kernel_hash") != kernel_source_hash():
+    r = rec.get(key)
+    if not r or r.get("kernel_hash") != kernel_source_hash(path):
         return None
     return r.get("bytes_per_launch")
 
 
-def cpu_baseline(seconds_hint=20.0):
+def cpu_baseline():
     """The oracle, as it is, on a bounded sample of the same workload: the TIES path
-    (full-sort TopKMask, exact election, disjoint mean, update) over layer 0's
-    k_proj, v_proj and q_proj, K = 4, on the host."""
-    import numpy as np  # noqa: F401
-
+    (full-sort TopKMask, exact election, disjoint mean, update) over layer 0's k_proj,
+    v_proj, q_proj, o_proj and gate_proj, K = 4, on the host."""
     import synth
     from oracle import ties
     wl = synth.stack_7b()
-    picks = [1, 2, 0]                  # layers.0.k_proj, v_proj, q_proj
-    inputs = []
+    picks = [1, 2, 0, 3, 4]
+    n = 0
+    dt = 0.0
     for t in picks:
         spec = wl.tensors[t]
         base = synth.fill_host(wl, t, 0)
         ds = [synth.fill_host(wl, t, 1 + i) for i in range(wl.K)]
         k = (spec.numel * wl.density.numerator * 2 + wl.density.denominator) // (2 * wl.density.denominator)
-        inputs.append((spec, base, ds, k))
-    n = 0
-    t0 = time.perf_counter()
-    for spec, base, ds, k in inputs:
+        t0 = time.perf_counter()
         ties.merge_unit(base, ds, "bf16", "ties", k=k)
+        dt += time.perf_counter() - t0
         n += spec.numel
-    dt = time.perf_counter() - t0
-    names = "+".join(wl.tensors[t].name for t in picks)
+        del base, ds
+    names = "+".join(wl.tensors[t].name.split(".")[-1] for t in picks)
     return {"value": n / dt, "unit": "params/s", "cores": 1, "kind": "oracle",
-            "sample": f"{names} ({n} params, K=4, TIES density 0.1) in {dt:.1f} s; numpy, single thread"}
+            "sample": f"layers.0 {names} ({n} params, K=4, TIES density 0.1) in {dt:.1f} s; numpy, one thread"}
 
 
 def main():
@@ -76,11 +79,12 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="7b", choices=["layer", "1.5b", "7b", "7b-tsv"])
+    ap.add_argument("--path", default="single-read", choices=["single-read", "two-pass"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the merge path is per-tensor "
-              "independent and this build does not shard it across GPUs.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the merge path is independent per "
+              "tensor and is not sharded across GPUs here.", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -110,25 +114,29 @@ def main():
         else:
             entries.append(e)
     N = wl.numel
-    desc = iso.desc_tensor(len(entries) * K, dev)
-    ws_sel = iso.workspace(iso.OP_TOPK, entries, K, iso.BF16, dev)
-    ws_upd = iso.workspace(iso.OP_UPDATE_FUSED, entries, K, iso.BF16, dev)
+    single = args.path == "single-read"
+    if single:
+        ws_upd = iso.workspace(iso.OP_UPDATE_FUSED_SELECT, entries, K, iso.BF16, dev)
+        ws_sel, desc = None, None
+    else:
+        desc = iso.desc_tensor(len(entries) * K, dev)
+        ws_sel = iso.workspace(iso.OP_TOPK, entries, K, iso.BF16, dev)
+        ws_upd = iso.workspace(iso.OP_UPDATE_FUSED, entries, K, iso.BF16, dev)
     ws_tsv = iso.workspace(iso.OP_BLOCKDIAG, tsv_entries, K, iso.BF16, dev, rank=wl.tsv_rank) if tsv_entries else None
     torch.cuda.synchronize()
 
     def step(ev=None):
         if ev:
             ev[0].record()
-        iso.iso_topk_mask(entries, K, iso.BF16, desc, ws=ws_sel)
-        if ev:
-            ev[1].record()
+        if not single:
+            iso.iso_topk_mask(entries, K, iso.BF16, desc, ws=ws_sel)
         iso.iso_update(entries, K, iso.BF16, iso.UPDATE_FUSED, merge=iso.MERGE_TIES, lam=1.0, desc=desc, ws=ws_upd)
         if ev:
-            ev[2].record()
+            ev[1].record()
         if tsv_entries:
             iso.iso_blockdiag_project(tsv_entries, K, iso.BF16, wl.tsv_rank, 1.0, ws=ws_tsv)
         if ev:
-            ev[3].record()
+            ev[2].record()
 
     for _ in range(args.warmup):
         step()
@@ -136,24 +144,28 @@ def main():
     for w in (ws_sel, ws_upd, ws_tsv):
         if w is not None and iso.iso_read_device_status(w) != 0:
             raise RuntimeError("device status reports an error")
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    fallbacks = iso.iso_read_fallback_count(ws_upd) if single else None
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    iso.iso_profile_begin()                     # HIP events around the main kernel, on this stream
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
         step(ev[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    sel_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
-    mrg_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
-    tsv_ms = sum(e[2].elapsed_time(e[3]) for e in ev) / args.steps
+    main_total, launches = iso.iso_profile_end()
+    if launches != args.steps:
+        raise RuntimeError(f"timed {launches} main-kernel launches for {args.steps} steps")
+    main_ms = main_total / launches
+    merge_call_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
+    tsv_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
     ms_per_step = wall * 1e3 / args.steps
 
     n_elem = sum(e.rows * e.cols for e in entries)
     alg_bytes_step = N * (K * 2 + 2 + 2)            # each delta and the base read once, weights written once
-    merge_alg = n_elem * (K * 2 + 2 + 2)            # the fused pass moves exactly the algorithmic bytes
-    merge_gbps = merge_alg / (mrg_ms * 1e-3) / 1e9
-    traffic = measured_traffic(args.config)
-    what = "TopKMask select + elect + disjoint mean + update"
+    main_alg = n_elem * (K * 2 + 2 + 2)             # the main kernel's algorithmic bytes per launch
+    main_gbps = main_alg / (main_ms * 1e-3) / 1e9
+    what = "TopKMask select + elect + disjoint mean + update in one call"
     if tsv_entries:
         what += f"; TSV rank {wl.tsv_rank} on the {len(tsv_entries)} MLP matrices"
     rec = {
@@ -169,18 +181,21 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"{wl.name}-shaped stack, {len(wl.tensors)} bf16 tensors, {N} params, K={K} deltas "
+        "config": {"workload": f"{wl.name}-shaped stack: {len(wl.tensors)} bf16 tensors, {N} params, K={K} deltas "
                                f"({float(wl.delta.p_zero):.0%} zeros), TIES per-tensor density "
                                f"{float(wl.density)}, lambda 1: {what}",
-                   "global_batch": 1, "seq_len": 0, "parallelism": "single GPU"},
+                   "path": args.path},
         "algorithmic_gbps": alg_bytes_step / (ms_per_step * 1e-3) / 1e9,
         "hbm_frac_step": alg_bytes_step / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBPS,
-        "select_ms": sel_ms,
-        "merge_ms": mrg_ms,
-        "roofline": {"bound": "hbm", "kernel": "k_merge (fused elect + disjoint mean + update)",
-                     "achieved": merge_gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": merge_gbps / PEAK_HBM_GBPS, "traffic": traffic},
+        "merge_call_ms": merge_call_ms,
+        "main_kernel_ms": main_ms,
+        "roofline": {"bound": "hbm", "kernel": KERNEL_NAMES[args.path],
+                     "achieved": main_gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": main_gbps / PEAK_HBM_GBPS,
+                     "traffic": measured_traffic(f"{args.config}/{args.path}", args.path)},
     }
+    if single:
+        rec["fallback_tensors"] = fallbacks
     if tsv_entries:
         rec["tsv_ms"] = tsv_ms
     if not args.no_cpu_baseline:

@@ -174,7 +174,13 @@ typedef struct iso_update_args {
  *  FUSED:    the merge of iso_merge followed by out = round(W_0 + u) in one
  *            pass that reads each delta and the base once (App. F TIES Trim /
  *            Elect / Merge and theta_0 + lambda tau_TIES; TA; RAM).  With TIES
- *            and desc == NULL the TopKMask selection runs inside the call.
+ *            and desc == NULL the TopKMask selection runs inside the call; for
+ *            bf16 (n_t <= 65535) it then reads each delta and the base only
+ *            once as well: a sampled key histogram brackets each threshold,
+ *            coordinates with a key inside the bracket are logged and fixed up
+ *            once the exact threshold is known.  A tensor whose threshold the
+ *            bracket misses takes the two-pass path on the device; the result
+ *            is the same (iso_read_fallback_count reports how many did).
  *  SPECTRAL: ISO-Merger, Sec. 4.2 / App. E / Algorithm 1, per matrix, in
  *            binary64: SVDs of W_0 and W_i = W_0 + tau_i, joint sign
  *            canonicalisation, tangent projection, D_keep, effect proxies and
@@ -207,6 +213,21 @@ int64_t iso_k_from_density(int64_t n, int64_t num, int64_t den);
 
 /* Synchronises `stream`, then reports what the kernels of the last call on `ws` found. */
 iso_status iso_read_device_status(const void* ws, void* stream);
+
+/* Synchronises `stream`, then stores in *count the number of tensors that the last
+ * single-read fused TIES call on `ws` (iso_update, FUSED, TIES, desc NULL, bf16) sent to
+ * the exact two-pass path; 0 after any other call.  A performance diagnostic only: the
+ * outputs do not depend on it. */
+iso_status iso_read_fallback_count(const void* ws, void* stream, int32_t* count);
+
+/* Benchmark timing.  Between iso_profile_begin and iso_profile_end, every iso_update
+ * FUSED call records a pair of HIP events on its stream around its main streaming kernel
+ * (the single-read pass of the bf16 TIES path with inner selection, else the merge
+ * kernel).  iso_profile_end waits for those events and returns the summed elapsed time in
+ * milliseconds and the number of launches timed; the library keeps its events for reuse.
+ * Calls on several host threads at once are timed too, in no particular order. */
+iso_status iso_profile_begin(void);
+iso_status iso_profile_end(double* total_ms, int32_t* launches);
 
 const char* iso_status_string(iso_status s);
 

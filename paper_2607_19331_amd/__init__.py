@@ -149,6 +149,32 @@ def iso_read_device_status(ws, stream=None):
     return _lib.load().iso_read_device_status(_ptr(ws), _stream(stream))
 
 
+def iso_read_fallback_count(ws, stream=None):
+    """Tensors that the last single-read fused TIES call on ws sent to the two-pass path."""
+    import ctypes
+    c = ctypes.c_int32(0)
+    st = _lib.load().iso_read_fallback_count(_ptr(ws), _stream(stream), ctypes.byref(c))
+    if st != 0:
+        raise IsoError(st, "iso_read_fallback_count")
+    return c.value
+
+
+def iso_profile_begin():
+    st = _lib.load().iso_profile_begin()
+    if st != 0:
+        raise IsoError(st, "iso_profile_begin")
+
+
+def iso_profile_end():
+    """(total milliseconds, launches) of the main kernels timed since iso_profile_begin."""
+    import ctypes
+    ms, n = ctypes.c_double(0.0), ctypes.c_int32(0)
+    st = _lib.load().iso_profile_end(ctypes.byref(ms), ctypes.byref(n))
+    if st != 0:
+        raise IsoError(st, "iso_profile_end")
+    return ms.value, n.value
+
+
 def iso_status_string(s):
     return _lib.load().iso_status_string(s).decode()
 

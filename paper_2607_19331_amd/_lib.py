@@ -15,7 +15,7 @@ UPDATE_APPLY, UPDATE_FUSED, UPDATE_SPECTRAL = 0, 1, 2
 
 SYMBOLS = ["iso_workspace_size", "iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update",
            "iso_blockdiag_project", "iso_workspace_size_tsv", "iso_k_from_density", "iso_read_device_status",
-           "iso_status_string"]
+           "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end", "iso_status_string"]
 
 
 class IsoTensor(ctypes.Structure):
@@ -60,10 +60,13 @@ def load():
     L.iso_k_from_density.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64]
     L.iso_k_from_density.restype = ctypes.c_int64
     L.iso_read_device_status.argtypes = [P, P]
+    L.iso_read_fallback_count.argtypes = [P, P, ctypes.POINTER(ctypes.c_int32)]
+    L.iso_profile_begin.argtypes = []
+    L.iso_profile_end.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32)]
     L.iso_status_string.argtypes = [I]
     L.iso_status_string.restype = ctypes.c_char_p
     for fn in ("iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update", "iso_blockdiag_project",
-               "iso_read_device_status"):
+               "iso_read_device_status", "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end"):
         getattr(L, fn).restype = I
     _lib = L
     return L

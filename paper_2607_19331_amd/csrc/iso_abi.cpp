@@ -4,10 +4,12 @@
 #include <hip/hip_runtime.h>
 
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "iso.h"
 #include "iso_device.h"
+#include "iso_fused.h"
 #include "iso_kernels.h"
 #include "iso_spectral.h"
 #include "iso_tsv.h"
@@ -67,13 +69,19 @@ iso_status check_ptr_array(const void* const* p, int n, bool required) {
 
 // Workspace regions for one call.
 struct Layout {
-  size_t table = 0, hitem0 = 0, titem0 = 0, ptrs = 0, upload_end = 0;
+  size_t table = 0, hitem0 = 0, titem0 = 0, ritem0 = 0, ptrs = 0, upload_end = 0;
   size_t states = 0, hist = 0, tiecnt = 0, desc = 0, chunk_hist = 0;
+  size_t fu = 0, tflag = 0, tstat = 0, tinfo = 0, csum = 0, rec = 0;
   size_t spectral = 0;
   size_t total = 0;
-  int64_t hist_chunk = 0, hist_items = 0, tie_items = 0, tiles = 0;
-  bool select = false, use_chunk_hist = false;
+  int64_t hist_chunk = 0, hist_items = 0, tie_items = 0, tiles = 0, groups = 0, ritems = 0, tile_cap = 0;
+  bool select = false, use_chunk_hist = false, fused = false;
 };
+
+// The single-read TIES path serves bf16 calls that select inside iso_update.
+bool fused_eligible(int op, int n_t, iso_dtype dt) {
+  return op == ISO_OP_UPDATE_FUSED_SELECT && dt == ISO_BF16 && n_t <= kFusedMaxTensors;
+}
 
 Layout plan(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
   Layout L;
@@ -83,6 +91,8 @@ Layout plan(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
   L.hitem0 = off;
   off = align_up(off + sizeof(int64_t) * (size_t)n_t, 256);
   L.titem0 = off;
+  off = align_up(off + sizeof(int64_t) * (size_t)n_t, 256);
+  L.ritem0 = off;
   off = align_up(off + sizeof(int64_t) * (size_t)n_t, 256);
   L.ptrs = off;
   off = align_up(off + sizeof(void*) * (size_t)n_t * K, 256);
@@ -115,12 +125,55 @@ Layout plan(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
     L.desc = off;
     off = align_up(off + sizeof(iso_select_desc) * (size_t)n_t * K, 256);
   }
+  L.fused = fused_eligible(op, n_t, dt);
+  if (L.fused) {
+    for (int j = 0; j < n_t; ++j) L.ritems += fused_reduce_items(t[j].rows * t[j].cols, K);
+    for (int j = 0; j < n_t; ++j) L.groups += fused_groups(t[j].rows * t[j].cols);
+    L.tile_cap = fused_tile_cap(K);
+    const size_t nu = (size_t)n_t * K;
+    L.fu = off;
+    off = align_up(off + sizeof(FusedUnit) * nu, 256);
+    L.tflag = off;
+    off = align_up(off + sizeof(int) * (size_t)n_t, 256);
+    L.tstat = off;
+    off = align_up(off + sizeof(uint32_t) * kFusedStat * (size_t)L.tiles * K, 256);
+    L.tinfo = off;
+    off = align_up(off + sizeof(uint2) * (size_t)L.tiles, 256);
+    L.csum = off;
+    off = align_up(off + sizeof(uint32_t) * kFusedStat * (size_t)L.ritems, 256);
+    L.rec = off;
+    off = align_up(off + fused_record_bytes(K) * (size_t)L.tile_cap * (size_t)L.tiles, 256);
+  }
   if (op == ISO_OP_UPDATE_SPECTRAL) {
     L.spectral = off;
     off = align_up(off + spectral_workspace_bytes(t, n_t, K), 256);
   }
   L.total = off;
   return L;
+}
+
+// Benchmark timing: event pairs recorded around the main streaming kernel of each call.
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  std::vector<hipEvent_t> pool;   // 2 per call
+  size_t used = 0;
+};
+Profiler g_prof;
+
+// Next event pair, or {null, null} when profiling is off (or events cannot be created).
+void prof_take(hipEvent_t (&ev)[2]) {
+  ev[0] = ev[1] = nullptr;
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on) return;
+  while (g_prof.pool.size() < g_prof.used + 2) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return;
+    g_prof.pool.push_back(e);
+  }
+  ev[0] = g_prof.pool[g_prof.used];
+  ev[1] = g_prof.pool[g_prof.used + 1];
+  g_prof.used += 2;
 }
 
 struct Upload {
@@ -136,9 +189,10 @@ hipError_t upload(const Layout& L, const iso_tensor* t, int n_t, int K, iso_dtyp
   DevTensor* tab = (DevTensor*)(h);
   int64_t* hi0 = (int64_t*)(h + (L.hitem0 - L.table));
   int64_t* ti0 = (int64_t*)(h + (L.titem0 - L.table));
+  int64_t* ri0 = (int64_t*)(h + (L.ritem0 - L.table));
   const void** pp = (const void**)(h + (L.ptrs - L.table));
   const int64_t te = merge_tile_elems(dt);
-  int64_t tile = 0, hitem = 0, titem = 0;
+  int64_t tile = 0, hitem = 0, titem = 0, ritem = 0, group = 0;
   for (int j = 0; j < n_t; ++j) {
     DevTensor d;
     std::memset(&d, 0, sizeof d);
@@ -150,10 +204,14 @@ hipError_t upload(const Layout& L, const iso_tensor* t, int n_t, int K, iso_dtyp
     d.n = t[j].rows * t[j].cols;
     d.k = t[j].k;
     d.tile0 = tile;
+    d.group0 = group;
     tab[j] = d;
     tile += (d.n + te - 1) / te;
+    group += fused_groups(d.n);
     hi0[j] = hitem;
     ti0[j] = titem;
+    ri0[j] = ritem;
+    if (L.fused) ritem += fused_reduce_items(d.n, K);
     if (L.select) {
       hitem += K * ((d.n + L.hist_chunk - 1) / L.hist_chunk);
       titem += K * ((d.n + kTieChunk - 1) / kTieChunk);
@@ -347,23 +405,49 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
     if ((st = check_ws(L, ws, ws_bytes)) != ISO_OK) return st;
     HIP_TRY(start_call(w, s));
     HIP_TRY(upload(L, t, n_t, K, dt, w, nullptr, want_sign ? (void* const*)a->sign_out : nullptr, nullptr, 0, s));
-    const iso_select_desc* desc = a->desc;
-    if (inner_select) {
-      iso_select_desc* dd = (iso_select_desc*)(w + L.desc);
-      HIP_TRY(do_select(L, w, n_t, K, dt, dd, s));
-      desc = dd;
-    }
     MergePlan mp;
     mp.tab = (const DevTensor*)(w + L.table);
     mp.n_t = n_t;
     mp.K = K;
     mp.mode = a->merge;
     mp.outs = OUT_W | (want_sign ? OUT_SIGN : 0);
-    mp.desc = ties ? desc : nullptr;
+    mp.desc = ties ? a->desc : nullptr;
     mp.lambda = a->lambda;
     mp.eps = a->eps_act;
     mp.tiles = L.tiles;
     mp.status = (uint32_t*)w;
+    if (L.fused) {
+      iso_select_desc* dd = (iso_select_desc*)(w + L.desc);
+      FusedPlan fp;
+      fp.tab = mp.tab;
+      fp.n_t = n_t;
+      fp.K = K;
+      fp.tiles = L.tiles;
+      fp.groups = L.groups;
+      fp.fu = (FusedUnit*)(w + L.fu);
+      fp.tflag = (int*)(w + L.tflag);
+      fp.tstat = (uint32_t*)(w + L.tstat);
+      fp.tinfo = (uint2*)(w + L.tinfo);
+      fp.rec = (uint32_t*)(w + L.rec);
+      fp.tile_cap = L.tile_cap;
+      fp.ritem0 = (const int64_t*)(w + L.ritem0);
+      fp.ritems = L.ritems;
+      fp.csum = (uint32_t*)(w + L.csum);
+      fp.lambda = a->lambda;
+      fp.want_sign = want_sign ? 1 : 0;
+      fp.status = (uint32_t*)w;
+      fp.sel = select_plan(L, w, n_t, K, dd);
+      fp.mrg = mp;
+      prof_take(fp.prof);
+      HIP_TRY(run_fused(fp, s));
+      return ISO_OK;
+    }
+    if (inner_select) {
+      iso_select_desc* dd = (iso_select_desc*)(w + L.desc);
+      HIP_TRY(do_select(L, w, n_t, K, dt, dd, s));
+      mp.desc = dd;
+    }
+    prof_take(mp.prof);
     HIP_TRY(run_merge(mp, dt, s));
     return ISO_OK;
   }
@@ -449,6 +533,39 @@ iso_status iso_read_device_status(const void* ws, void* stream) {
   if (hipMemcpy(&flags, ws, sizeof flags, hipMemcpyDeviceToHost) != hipSuccess) return ISO_ERR_HIP;
   if (flags & kStatusInternal) return ISO_ERR_INTERNAL;
   if (flags & kStatusNonFinite) return ISO_ERR_NONFINITE;
+  return ISO_OK;
+}
+
+iso_status iso_profile_begin(void) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.on = true;
+  g_prof.used = 0;
+  return ISO_OK;
+}
+
+iso_status iso_profile_end(double* total_ms, int32_t* launches) {
+  if (total_ms == nullptr || launches == nullptr) return ISO_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.on = false;
+  double sum = 0.0;
+  for (size_t q = 0; q + 1 < g_prof.used; q += 2) {
+    if (hipEventSynchronize(g_prof.pool[q + 1]) != hipSuccess) return ISO_ERR_HIP;
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, g_prof.pool[q], g_prof.pool[q + 1]) != hipSuccess) return ISO_ERR_HIP;
+    sum += ms;
+  }
+  *total_ms = sum;
+  *launches = (int32_t)(g_prof.used / 2);
+  g_prof.used = 0;
+  return ISO_OK;
+}
+
+iso_status iso_read_fallback_count(const void* ws, void* stream, int32_t* count) {
+  if (ws == nullptr || count == nullptr) return ISO_ERR_INVALID_ARG;
+  if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return ISO_ERR_HIP;
+  uint32_t v = 0;
+  if (hipMemcpy(&v, (const uint32_t*)ws + 1, sizeof v, hipMemcpyDeviceToHost) != hipSuccess) return ISO_ERR_HIP;
+  *count = (int32_t)v;
   return ISO_OK;
 }
 

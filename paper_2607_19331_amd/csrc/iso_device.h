@@ -27,7 +27,7 @@ struct DevTensor {
   int64_t n;        // elements
   int64_t k;        // TopKMask count
   int64_t tile0;    // first tile of this tensor in the launch's tile space
-  int64_t pad;
+  int64_t group0;   // first record region of this tensor (single-read fused path)
 };
 static_assert(sizeof(DevTensor) % 16 == 0, "table entry alignment");
 
@@ -111,6 +111,19 @@ __device__ __forceinline__ uint32_t f64_to_bf16_rne(double v) {
   return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
 }
 
+// The same rounding for finite v without the NaN case (callers that flag non-finite
+// inputs elsewhere and leave such outputs unspecified).
+__device__ __forceinline__ uint32_t f64_to_bf16_rne_finite(double v) {
+  const float f = (float)v;
+  uint32_t b = bits_from_f32(f);
+  const double back = (double)f;
+  if (back != v) {
+    if (fabs(back) > fabs(v)) b -= 1u;
+    b |= 1u;
+  }
+  return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+}
+
 __device__ __forceinline__ double load_f64(const void* p, int64_t i, int dt) {
   if (dt == ISO_BF16) return (double)f32_from_bits((uint32_t)((const uint16_t*)p)[i] << 16);
   return (double)((const float*)p)[i];
@@ -145,6 +158,32 @@ __device__ __forceinline__ int find_tensor(const DevTensor* tab, int n_t, int64_
     if (tab[mid].tile0 <= tile) lo = mid; else hi = mid - 1;
   }
   return lo;
+}
+
+// Persistent-grid walk over the work of flagged tensors only.  Every block scans the flags
+// (through LDS, 1024 at a time) in tensor order and takes every gridDim.x-th work item of
+// the flagged tensors; count(j) gives tensor j's item count.  With no flag set a block
+// only reads the flags.  body(j, item) may synchronise the block: the loop is uniform.
+template <class Count, class Body>
+__device__ __forceinline__ void for_flagged_items(const int* __restrict__ flags, int n_t, int* sflag, Count count,
+                                                  Body body) {
+  const int64_t G = gridDim.x;
+  int64_t run = 0;   // items of flagged tensors before tensor j
+  for (int j0 = 0; j0 < n_t; j0 += 1024) {
+    __syncthreads();
+    for (int q = threadIdx.x; q < 1024; q += blockDim.x) sflag[q] = (j0 + q < n_t) ? flags[j0 + q] : 0;
+    __syncthreads();
+    const int nq = min(1024, n_t - j0);
+    for (int q = 0; q < nq; ++q) {
+      if (!sflag[q]) continue;
+      const int j = j0 + q;
+      const int64_t m = count(j);
+      int64_t first = ((int64_t)blockIdx.x - run) % G;
+      if (first < 0) first += G;
+      for (int64_t it = first; it < m; it += G) body(j, it);
+      run += m;
+    }
+  }
 }
 
 }  // namespace iso

@@ -24,6 +24,9 @@ struct SelectPlan {
   uint32_t* chunk_hist;         // hist_items * 2^last_bits per-chunk histograms of the last pass, or null
   iso_select_desc* desc;        // n_t*K, device
   uint32_t* status;
+  const int* filter = nullptr;  // n_t device flags: only flagged tensors are selected (others get
+                                // t_key = none); null: every tensor.  Histograms of flagged units are
+                                // cleared by the launch itself.
 };
 
 int64_t hist_chunk_for(int64_t total_elems_times_k);
@@ -46,6 +49,8 @@ struct MergePlan {
   double lambda, eps;
   int64_t tiles;                // total tiles over the table
   uint32_t* status;
+  const int* filter = nullptr;  // n_t device flags: only flagged tensors are merged; null: every tensor
+  hipEvent_t prof[2] = {nullptr, nullptr};   // recorded around the merge kernel when set
 };
 
 int64_t merge_tile_elems(int dt);

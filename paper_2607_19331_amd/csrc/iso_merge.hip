@@ -257,6 +257,21 @@ __global__ void __launch_bounds__(kMergeThreads) k_merge(const DevTensor* __rest
     merge_tile<DT, K, MODE, OUTS, VPT>(tab, n_t, desc, lambda, eps, status, tile);
 }
 
+// Persistent form over the tiles of flagged tensors only.
+template <int DT, int K, int MODE, int OUTS, int VPT>
+__global__ void __launch_bounds__(kMergeThreads) k_merge_flagged(const DevTensor* __restrict__ tab, int n_t,
+                                                                 const iso_select_desc* __restrict__ desc,
+                                                                 double lambda, double eps, uint32_t* status,
+                                                                 const int* __restrict__ filter) {
+  __shared__ int sflag[1024];
+  constexpr int64_t te = (int64_t)kMergeThreads * VPT * Fmt<DT>::kPerVec;
+  for_flagged_items(
+      filter, n_t, sflag, [&](int j) { return (tab[j].n + te - 1) / te; },
+      [&](int j, int64_t it) {
+        merge_tile<DT, K, MODE, OUTS, VPT>(tab, n_t, desc, lambda, eps, status, tab[j].tile0 + it);
+      });
+}
+
 // ---- APPLY: out = round(w0 + lambda * tau_in) ----------------------------------------------------
 
 template <int DT>
@@ -323,9 +338,16 @@ __global__ void __launch_bounds__(kMergeThreads) k_apply(const DevTensor* __rest
 
 template <int DT, int K, int MODE, int OUTS>
 static void launch_merge(const MergePlan& pl, hipStream_t s) {
+  if (pl.filter != nullptr) {
+    k_merge_flagged<DT, K, MODE, OUTS, kMergeVPT><<<1024, kMergeThreads, 0, s>>>(pl.tab, pl.n_t, pl.desc, pl.lambda,
+                                                                                 pl.eps, pl.status, pl.filter);
+    return;
+  }
   const int64_t grid = (kMergeMaxGrid > 0) ? std::min(pl.tiles, kMergeMaxGrid) : pl.tiles;
+  if (pl.prof[0]) (void)hipEventRecord(pl.prof[0], s);
   k_merge<DT, K, MODE, OUTS, kMergeVPT><<<(unsigned)grid, kMergeThreads, 0, s>>>(pl.tab, pl.n_t, pl.desc, pl.lambda,
                                                                                  pl.eps, pl.status, pl.tiles);
+  if (pl.prof[1]) (void)hipEventRecord(pl.prof[1], s);
 }
 
 template <int DT, int K, int MODE>

@@ -55,10 +55,13 @@ __device__ int64_t block_inclusive_scan(int64_t v, int64_t* sh /* >= 16 */) {
 
 // ---- unit setup ---------------------------------------------------------------------------------
 
-__global__ void k_select_init(const DevTensor* tab, int n_t, int K, UnitState* st) {
+// With `filter` set, only units of flagged tensors take part; the others are finished
+// (no key selected) before the first pass.
+__global__ void k_select_init(const DevTensor* tab, int n_t, int K, UnitState* st, const int* filter) {
   int u = blockIdx.x * blockDim.x + threadIdx.x;
   if (u >= n_t * K) return;
   const DevTensor& T = tab[u / K];
+  const bool skip = (filter != nullptr) && !filter[u / K];
   UnitState s;
   s.prefix = 0;
   s.key_max = 0;
@@ -66,8 +69,8 @@ __global__ void k_select_init(const DevTensor* tab, int n_t, int K, UnitState* s
   s.n_above = 0;
   s.bucket = T.n;
   s.cutoff = 0;
-  s.done = (T.k == 0) ? 1 : 0;
-  if (T.k == 0) s.prefix = kNoSelectKey;
+  s.done = (T.k == 0 || skip) ? 1 : 0;
+  if (T.k == 0 || skip) s.prefix = kNoSelectKey;
   s.pad[0] = s.pad[1] = s.pad[2] = 0;
   st[u] = s;
 }
@@ -91,20 +94,22 @@ __device__ __forceinline__ void item_of(const int64_t* item0, int n_t, int K, in
 // With `dump` set (last pass only), the block also stores its chunk histogram (bin 0 =
 // in-bucket entries whose digit is 0) so ties can later be located without another read.
 
+struct HistLds {
+  uint32_t bins[kMaxBins];
+  uint32_t wmax[16];
+  uint32_t wzero[16];
+};
+
+// One histogram work item: chunk c of delta i of tensor j; `item` numbers its dump slot.
 template <int DT>
-__global__ void __launch_bounds__(kHistThreads) k_hist(const DevTensor* __restrict__ tab, int n_t, int K,
-                                                       const int64_t* __restrict__ item0, int64_t chunk,
-                                                       UnitState* __restrict__ st, uint32_t* __restrict__ hist,
-                                                       int shift, int bits, int first, uint32_t* status,
-                                                       uint32_t* __restrict__ dump) {
+__device__ void hist_item(const DevTensor* __restrict__ tab, int K, int j, int i, int64_t c, int64_t item,
+                          int64_t chunk, UnitState* __restrict__ st, uint32_t* __restrict__ hist, int shift,
+                          int bits, int first, uint32_t* status, uint32_t* __restrict__ dump, HistLds& sm) {
   using F = Fmt<DT>;
   constexpr int U = 8;                         // 16-byte loads in flight per thread
-  __shared__ uint32_t lds[kMaxBins];
-  __shared__ uint32_t wmax[16];
-  __shared__ uint32_t wzero[16];
-  int j, i;
-  int64_t c;
-  item_of(item0, n_t, K, chunk, tab, blockIdx.x, j, i, c);
+  uint32_t* lds = sm.bins;
+  uint32_t* wmax = sm.wmax;
+  uint32_t* wzero = sm.wzero;
   const int u = j * K + i;
   const DevTensor& T = tab[j];
   const bool active = !st[u].done;             // k == 0 units only need key_max from the first pass
@@ -171,7 +176,7 @@ __global__ void __launch_bounds__(kHistThreads) k_hist(const DevTensor* __restri
 
   uint32_t* gh = hist + (size_t)u * kMaxBins;
   if (active) {
-    uint32_t* dp = (dump != nullptr) ? dump + (size_t)blockIdx.x * nb : nullptr;
+    uint32_t* dp = (dump != nullptr) ? dump + (size_t)item * nb : nullptr;
     for (uint32_t b = threadIdx.x; b < nb; b += blockDim.x) {
       uint32_t cnt = lds[b];
       if (cnt) atomicAdd(&gh[b], cnt);
@@ -190,6 +195,50 @@ __global__ void __launch_bounds__(kHistThreads) k_hist(const DevTensor* __restri
       if (mm >= expfield) flag_status(status, kStatusNonFinite);
     }
   }
+  __syncthreads();                             // LDS is reused by the block's next item
+}
+
+template <int DT>
+__global__ void __launch_bounds__(kHistThreads) k_hist(const DevTensor* __restrict__ tab, int n_t, int K,
+                                                       const int64_t* __restrict__ item0, int64_t chunk,
+                                                       UnitState* __restrict__ st, uint32_t* __restrict__ hist,
+                                                       int shift, int bits, int first, uint32_t* status,
+                                                       uint32_t* __restrict__ dump) {
+  __shared__ HistLds sm;
+  int j, i;
+  int64_t c;
+  item_of(item0, n_t, K, chunk, tab, blockIdx.x, j, i, c);
+  hist_item<DT>(tab, K, j, i, c, blockIdx.x, chunk, st, hist, shift, bits, first, status, dump, sm);
+}
+
+// Persistent form over the flagged tensors only (items numbered as in k_hist).
+template <int DT>
+__global__ void __launch_bounds__(kHistThreads) k_hist_flagged(const DevTensor* __restrict__ tab, int n_t, int K,
+                                                               const int64_t* __restrict__ item0, int64_t chunk,
+                                                               UnitState* __restrict__ st,
+                                                               uint32_t* __restrict__ hist, int shift, int bits,
+                                                               int first, uint32_t* status,
+                                                               uint32_t* __restrict__ dump,
+                                                               const int* __restrict__ filter) {
+  __shared__ HistLds sm;
+  __shared__ int sflag[1024];
+  for_flagged_items(
+      filter, n_t, sflag, [&](int j) { return (int64_t)K * ((tab[j].n + chunk - 1) / chunk); },
+      [&](int j, int64_t it) {
+        const int64_t nch = (tab[j].n + chunk - 1) / chunk;
+        const int i = (int)(it / nch);
+        const int64_t c = it - (int64_t)i * nch;
+        hist_item<DT>(tab, K, j, i, c, item0[j] + it, chunk, st, hist, shift, bits, first, status, dump, sm);
+      });
+}
+
+// Clears the global histograms of the flagged tensors' units.
+__global__ void __launch_bounds__(1024) k_clear_hist_flagged(int n_t, int K, uint32_t* __restrict__ hist,
+                                                             const int* __restrict__ filter) {
+  __shared__ int sflag[1024];
+  for_flagged_items(
+      filter, n_t, sflag, [&](int) { return (int64_t)K * (kMaxBins / 1024); },
+      [&](int j, int64_t it) { hist[(size_t)j * K * kMaxBins + (size_t)it * 1024 + threadIdx.x] = 0u; });
 }
 
 // ---- resolve: pick the digit holding the k_rem-th largest key ------------------------------------
@@ -340,14 +389,10 @@ __global__ void __launch_bounds__(kHistThreads) k_tie_find_dump(const DevTensor*
 // ---- ties: count threshold keys per chunk, then walk to the quota-th one -------------------------
 
 template <int DT>
-__global__ void __launch_bounds__(256) k_tie_count(const DevTensor* __restrict__ tab, int n_t, int K,
-                                                   const int64_t* __restrict__ item0, int64_t chunk,
-                                                   const UnitState* __restrict__ st, int32_t* __restrict__ cnt) {
+__device__ void tie_count_item(const DevTensor* __restrict__ tab, int K, int j, int i, int64_t c, int64_t item,
+                               int64_t chunk, const UnitState* __restrict__ st, int32_t* __restrict__ cnt,
+                               int64_t* sh) {
   using F = Fmt<DT>;
-  __shared__ int64_t sh[4];
-  int j, i;
-  int64_t c;
-  item_of(item0, n_t, K, chunk, tab, blockIdx.x, j, i, c);
   const int u = j * K + i;
   if (st[u].done) return;
   const uint32_t tk = st[u].prefix;
@@ -373,7 +418,35 @@ __global__ void __launch_bounds__(256) k_tie_count(const DevTensor* __restrict__
   m = wave_sum_i64(m);
   if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = m;
   __syncthreads();
-  if (threadIdx.x == 0) cnt[blockIdx.x] = (int32_t)(sh[0] + sh[1] + sh[2] + sh[3]);
+  if (threadIdx.x == 0) cnt[item] = (int32_t)(sh[0] + sh[1] + sh[2] + sh[3]);
+  __syncthreads();
+}
+
+template <int DT>
+__global__ void __launch_bounds__(256) k_tie_count(const DevTensor* __restrict__ tab, int n_t, int K,
+                                                   const int64_t* __restrict__ item0, int64_t chunk,
+                                                   const UnitState* __restrict__ st, int32_t* __restrict__ cnt) {
+  __shared__ int64_t sh[4];
+  int j, i;
+  int64_t c;
+  item_of(item0, n_t, K, chunk, tab, blockIdx.x, j, i, c);
+  tie_count_item<DT>(tab, K, j, i, c, blockIdx.x, chunk, st, cnt, sh);
+}
+
+template <int DT>
+__global__ void __launch_bounds__(256) k_tie_count_flagged(const DevTensor* __restrict__ tab, int n_t, int K,
+                                                           const int64_t* __restrict__ item0, int64_t chunk,
+                                                           const UnitState* __restrict__ st,
+                                                           int32_t* __restrict__ cnt, const int* __restrict__ filter) {
+  __shared__ int64_t sh[4];
+  __shared__ int sflag[1024];
+  for_flagged_items(
+      filter, n_t, sflag, [&](int j) { return (int64_t)K * ((tab[j].n + chunk - 1) / chunk); },
+      [&](int j, int64_t it) {
+        const int64_t nch = (tab[j].n + chunk - 1) / chunk;
+        const int i = (int)(it / nch);
+        tie_count_item<DT>(tab, K, j, i, it - (int64_t)i * nch, item0[j] + it, chunk, st, cnt, sh);
+      });
 }
 
 template <int DT>
@@ -507,7 +580,10 @@ hipError_t fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
 template <int DT>
 static hipError_t run_select_t(const SelectPlan& pl, hipStream_t s) {
   const int nu = pl.n_t * pl.K;
-  k_select_init<<<(nu + 255) / 256, 256, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.states);
+  const bool flt = pl.filter != nullptr;
+  constexpr unsigned kFlaggedGrid = 256;
+  if (flt) k_clear_hist_flagged<<<kFlaggedGrid, 1024, 0, s>>>(pl.n_t, pl.K, pl.hist, pl.filter);
+  k_select_init<<<(nu + 255) / 256, 256, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.states, pl.filter);
   struct Pass { int shift, bits; };
   const Pass bf[1] = {{0, 15}};
   const Pass f32[3] = {{16, 15}, {8, 8}, {0, 8}};
@@ -515,7 +591,11 @@ static hipError_t run_select_t(const SelectPlan& pl, hipStream_t s) {
   const int np = (DT == ISO_BF16) ? 1 : 3;
   for (int q = 0; q < np; ++q) {
     uint32_t* dump = (q == np - 1) ? pl.chunk_hist : nullptr;
-    if (pl.hist_items > 0)
+    if (pl.hist_items > 0 && flt)
+      k_hist_flagged<DT><<<kFlaggedGrid, kHistThreads, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.hist_item0, pl.hist_chunk,
+                                                               pl.states, pl.hist, ps[q].shift, ps[q].bits, q == 0,
+                                                               pl.status, dump, pl.filter);
+    else if (pl.hist_items > 0)
       k_hist<DT><<<(unsigned)pl.hist_items, kHistThreads, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.hist_item0, pl.hist_chunk,
                                                                   pl.states, pl.hist, ps[q].shift, ps[q].bits,
                                                                   q == 0, pl.status, dump);
@@ -526,7 +606,10 @@ static hipError_t run_select_t(const SelectPlan& pl, hipStream_t s) {
     k_tie_find_dump<DT><<<nu, kHistThreads, 0, s>>>(pl.tab, pl.K, pl.hist_item0, pl.hist_chunk, pl.states,
                                                     pl.chunk_hist, ps[np - 1].bits, pl.status);
   } else {
-    if (pl.tie_items > 0)
+    if (pl.tie_items > 0 && flt)
+      k_tie_count_flagged<DT><<<kFlaggedGrid * 4, 256, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.tie_item0, pl.tie_chunk,
+                                                               pl.states, pl.tie_cnt, pl.filter);
+    else if (pl.tie_items > 0)
       k_tie_count<DT><<<(unsigned)pl.tie_items, 256, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.tie_item0, pl.tie_chunk,
                                                              pl.states, pl.tie_cnt);
     k_tie_find<DT><<<nu, kHistThreads, 0, s>>>(pl.tab, pl.K, pl.tie_item0, pl.tie_chunk, pl.states, pl.tie_cnt,
