@@ -6,7 +6,7 @@
 // path reads each delta and the base once:
 //   1. sample (one workgroup per delta): the exact key histogram of the whole delta when it
 //      is small, else of 4096 evenly spaced 256-entry blocks.  From it a bracket [lo, hi]
-//      of keys that holds the threshold with a binomial margin (6 standard deviations of
+//      of keys that holds the threshold with a binomial margin (5 standard deviations of
 //      the sample rank, plus 2) and a provisional threshold prov;
 //   2. main pass: a key above hi is kept, a key below lo is not; a nonzero key inside the
 //      bracket is kept provisionally if key >= prov and its coordinate is logged as a
@@ -38,7 +38,7 @@ constexpr int64_t kTileElems = (int64_t)kThreads * kVPT * 8;
 constexpr int kSampleSpan = 256;                 // entries per sampled block
 constexpr int kSampleBlocks = 4096;              // sampled blocks per delta (1M entries)
 constexpr int64_t kExactMax = 2ll << 20;         // deltas up to this size are histogrammed whole
-constexpr double kMarginSd = 6.0;
+constexpr double kMarginSd = 5.0;
 constexpr int kBins = 1 << 15;
 
 constexpr int kFlagWide = 1, kFlagFull = 2, kFlagMiss = 4;   // reasons, OR-ed into tflag
@@ -230,9 +230,10 @@ __global__ void __launch_bounds__(1024) k_fs_sample(const DevTensor* __restrict_
 // can be kept here (all partial sums are then multiples of 2^(E - 7) below 2^(E + 17)), and
 // a thread with any coordinate outside that bound redoes its coordinates in the general
 // binary64 form.  The mean t = RN64(ts / n) of the agreeing sum ts over n entries is formed
-// branch-free as q = ts * r, rem = fma(-q, n, ts), t = fma(rem, r, q) with r = RN64(1/n):
-// the remainder is exact and the correction gives the correctly rounded quotient
-// (Markstein, IBM J. Res. Dev. 34(1), 1990); for n a power of two q is already exact.
+// branch-free from D = 2 ts as q = D * r, rem = fma(-q, 2n, D), t = fma(rem, r, q) with
+// r = RN64(1/n) / 2: the remainder is exact and the correction gives the correctly rounded
+// quotient (Markstein, IBM J. Res. Dev. 34(1), 1990); for n a power of two q is already
+// exact.  Halving r and doubling the divisor scale every step by exactly 1/2.
 
 typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
 typedef int16_t i16x2 __attribute__((ext_vector_type(2)));
@@ -284,7 +285,7 @@ __global__ void __launch_bounds__(kThreads) k_fs_main(MainArgs a) {
   __shared__ uint32_t hcnt[K][kFusedMaxW];
   __shared__ uint32_t s_kept[K][kThreads / 64];
   __shared__ uint32_t s_wtot[kThreads / 64];
-  __shared__ double rtab[K + 1];
+  __shared__ double2 rtab[K + 1];                   // {RN(1/n) / 2, 2n}
   __shared__ uint4 s_rec[kTileCapK<K> * (RW / 4)];   // the tile's records, staged
   __shared__ int s_skip, s_redo;
   const int64_t tile = blockIdx.x;
@@ -296,7 +297,8 @@ __global__ void __launch_bounds__(kThreads) k_fs_main(MainArgs a) {
     s_skip = a.tflag[j];
     s_redo = 0;
   }
-  if (threadIdx.x <= K) rtab[threadIdx.x] = (threadIdx.x == 0) ? 0.0 : 1.0 / (double)threadIdx.x;
+  if (threadIdx.x <= K)
+    rtab[threadIdx.x] = make_double2((threadIdx.x == 0) ? 0.0 : 0.5 / (double)threadIdx.x, 2.0 * (double)threadIdx.x);
   for (int e = threadIdx.x; e < K * kFusedMaxW; e += kThreads) hcnt[e / kFusedMaxW][e % kFusedMaxW] = 0;
   // per-delta constants (two 16-bit copies): provisional key, bracket start and width - 1
   uint32_t p1x2[K], lo1x2[K], wm1x2[K], lo1[K], hi1[K], lo0[K];
@@ -403,24 +405,24 @@ __global__ void __launch_bounds__(kThreads) k_fs_main(MainArgs a) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
           const bool def = ((dm[q][h] >> (16 * c)) & 0xFFFFu) == 0u;
-          uint32_t wds[RW];
+          if (def) {                               // rare per lane: waves with no such lane skip the site
+            uint32_t wds[RW];
 #pragma unroll
-          for (int z = 0; z < RW; ++z) wds[z] = 0;
-          wds[0] = i0 + (uint32_t)(2 * h + c);
-          wds[1] = (uint32_t)j;
+            for (int z = 0; z < RW; ++z) wds[z] = 0;
+            wds[0] = i0 + (uint32_t)(2 * h + c);
+            wds[1] = (uint32_t)j;
 #pragma unroll
-          for (int x = 0; x <= K; ++x) {
-            const uint32_t w = (x < K) ? word_of(dv[q][x < K ? x : 0], h) : word_of(wv[q], h);
-            const int hw = 3 + x;
-            const uint32_t v = c ? (w >> 16) : (w & 0xFFFFu);
-            wds[hw >> 1] |= v << (16 * (hw & 1));
-          }
-          if (def) {
+            for (int x = 0; x <= K; ++x) {
+              const uint32_t w = (x < K) ? word_of(dv[q][x < K ? x : 0], h) : word_of(wv[q], h);
+              const int hw = 3 + x;
+              const uint32_t v = c ? (w >> 16) : (w & 0xFFFFu);
+              wds[hw >> 1] |= v << (16 * (hw & 1));
+            }
 #pragma unroll
             for (int z = 0; z < RW / 4; ++z)
               s_rec[slot * (RW / 4) + z] = make_uint4(wds[4 * z], wds[4 * z + 1], wds[4 * z + 2], wds[4 * z + 3]);
+            ++slot;
           }
-          slot += def ? 1u : 0u;
         }
       }
     }
@@ -466,18 +468,18 @@ __global__ void __launch_bounds__(kThreads) k_fs_main(MainArgs a) {
         const int nneg = (int)(c ? (nn >> 16) : (nn & 0xFFFFu));
         const bool pos = S > 0.0f, neg = S < 0.0f;
         const int cnt = pos ? nkeep - nneg : (neg ? nneg : 0);
-        const float g = pos ? 1.0f : (neg ? -1.0f : 0.0f);
-        const float ts = (S + g * A) * 0.5f;
-        const double t64 = (double)ts;
-        const double r = rtab[cnt];
-        const double qd = t64 * r;
-        const double rem = fma(-qd, (double)cnt, t64);
-        double t = fma(rem, r, qd);
+        // D = S + gamma * A is twice the agreeing sum (exact); t = RN64(D / 2cnt)
+        const float D = S + (pos ? A : (neg ? -A : 0.0f));
+        const double d64 = (double)D;
+        const double2 rn = rtab[cnt];
+        const double qd = d64 * rn.x;
+        const double rem = fma(-qd, rn.y, d64);
+        double t = fma(rem, rn.x, qd);
         if (!LAM1) t = lambda * t;
         const float w0 = __uint_as_float(c ? (wb & 0xFFFF0000u) : (wb << 16));
         const uint32_t o = f64_to_bf16_rne_finite((double)w0 + t);
         o2 |= o << (16 * c);
-        s2 |= ((uint32_t)(int)g & 0xFFu) << (8 * c);
+        if (a.want_sign) s2 |= (pos ? 0x01u : (neg ? 0xFFu : 0x00u)) << (8 * c);
       }
       ob[h] = o2;
       sg[h] = s2;
@@ -502,10 +504,14 @@ __global__ void __launch_bounds__(kThreads) k_fs_main(MainArgs a) {
   if (amax >= abound) s_redo = 1;
   // tile statistics: provisionally kept entries and bracket counts per delta
 #pragma unroll
-  for (int i = 0; i < K; ++i) {
+  for (int i = 0; i < K; i += 2) {                 // two deltas per reduction (16-bit halves, <= 1024 each)
     uint32_t x = (uint32_t)(16 + lo_s16(kc[i]) + hi_s16(kc[i]));
+    if (i + 1 < K) x |= (uint32_t)(16 + lo_s16(kc[i + 1 < K ? i + 1 : i]) + hi_s16(kc[i + 1 < K ? i + 1 : i])) << 16;
     for (int o = 32; o > 0; o >>= 1) x += (uint32_t)__shfl_xor((int)x, o, 64);
-    if (lane == 0) s_kept[i][wid] = x;
+    if (lane == 0) {
+      s_kept[i][wid] = x & 0xFFFFu;
+      if (i + 1 < K) s_kept[i + 1 < K ? i + 1 : i][wid] = x >> 16;
+    }
   }
   __syncthreads();                                 // staged records, s_kept, s_redo
   if (threadIdx.x == 0) a.tinfo[tile].y = (uint32_t)s_redo;
