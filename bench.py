@@ -81,6 +81,9 @@ def main():
     ap.add_argument("--config", default="7b", choices=["layer", "1.5b", "7b", "7b-tsv"])
     ap.add_argument("--path", default="single-read", choices=["single-read", "two-pass"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run only a plain elementwise copy (1 GiB read, 1 GiB written, 3 launches) to scale "
+                         "the HBM byte counters of a profiler")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the merge path is independent per "
@@ -88,6 +91,17 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.calibrate_copy:
+        n = 1 << 29                                 # 2-byte elements: 1 GiB each way
+        src = torch.ones(n, dtype=torch.float16, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy": {"bytes_read": 2 * n, "bytes_written": 2 * n, "launches": 3}}), flush=True)
+        return
 
     import paper_2607_19331_amd as iso
     import synth
