@@ -260,6 +260,30 @@ __device__ __forceinline__ uint32_t word_of(const uint4& v, int h) {
   return (h == 0) ? v.x : (h == 1) ? v.y : (h == 2) ? v.z : v.w;
 }
 
+// Workgroup barrier that orders LDS only: outstanding global loads and stores stay in flight
+// (the main pass never reads global data another thread of the block wrote).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Inclusive prefix sum over a wave64 with DPP row shifts and row broadcasts (no LDS).
+__device__ __forceinline__ uint32_t wave_scan_u32(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, true);   // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, true);   // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, true);   // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, true);   // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15 -> rows 1, 3
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31 -> rows 2, 3
+  return x;
+}
+
+// {RN(1/n) / 2, 2n} for the branch-free mean, n = 0..8 (entry 0 is never divided by)
+__constant__ double2 kHalfRecip[9] = {{0.0, 0.0},       {0.5 / 1.0, 2.0},  {0.5 / 2.0, 4.0},
+                                      {0.5 / 3.0, 6.0}, {0.5 / 4.0, 8.0},  {0.5 / 5.0, 10.0},
+                                      {0.5 / 6.0, 12.0}, {0.5 / 7.0, 14.0}, {0.5 / 8.0, 16.0}};
+
 // Provisional threshold of a delta in the main pass: kept iff key >= prov_key.
 __device__ __forceinline__ uint32_t prov_key(const FusedUnit& F) {
   return (F.flags & kFusedNone) ? 0x8000u : max(F.prov, 1u);
@@ -279,8 +303,11 @@ struct MainArgs {
   uint32_t* status;
 };
 
+// Up to K = 4 the pass fits 96 VGPRs without spilling: five waves per SIMD instead of four,
+// which is what keeps enough loads in flight (the waves' lifetimes are latency-bound).
 template <int K, bool LAM1>
-__global__ void __launch_bounds__(kThreads) k_fs_main(MainArgs a) {
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(K <= 4 ? 5 : 1)))
+k_fs_main(MainArgs a) {
   constexpr int RW = rec_words<K>();
   __shared__ uint32_t hcnt[K][kFusedMaxW];
   __shared__ uint32_t s_kept[K][kThreads / 64];
@@ -297,8 +324,7 @@ __global__ void __launch_bounds__(kThreads) k_fs_main(MainArgs a) {
     s_skip = a.tflag[j];
     s_redo = 0;
   }
-  if (threadIdx.x <= K)
-    rtab[threadIdx.x] = make_double2((threadIdx.x == 0) ? 0.0 : 0.5 / (double)threadIdx.x, 2.0 * (double)threadIdx.x);
+  if (threadIdx.x <= K) rtab[threadIdx.x] = kHalfRecip[threadIdx.x];
   for (int e = threadIdx.x; e < K * kFusedMaxW; e += kThreads) hcnt[e / kFusedMaxW][e % kFusedMaxW] = 0;
   // per-delta constants (two 16-bit copies): provisional key, bracket start and width - 1
   uint32_t p1x2[K], lo1x2[K], wm1x2[K], lo1[K], hi1[K], lo0[K];
@@ -369,13 +395,9 @@ __global__ void __launch_bounds__(kThreads) k_fs_main(MainArgs a) {
   // record slots: flat index order inside the tile (vector q, then thread, then element)
   static_assert(kVPT == 2, "the record scan packs two vector counts");
   const uint32_t packed = ndef[0] | (ndef[1] << 16);
-  uint32_t inc = packed;
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t y = (uint32_t)__shfl_up((int)inc, o, 64);
-    if (lane >= o) inc += y;
-  }
+  const uint32_t inc = wave_scan_u32(packed);
   if (lane == 63) s_wtot[wid] = inc;
-  __syncthreads();                                 // s_skip, rtab, hcnt, s_wtot
+  lds_barrier();                                 // s_skip, rtab, hcnt, s_wtot
   if (s_skip) {                                    // the whole tensor takes the two-pass path
     if (threadIdx.x == 0) a.tinfo[tile] = make_uint2(0u, 0u);
     return;
@@ -507,13 +529,13 @@ __global__ void __launch_bounds__(kThreads) k_fs_main(MainArgs a) {
   for (int i = 0; i < K; i += 2) {                 // two deltas per reduction (16-bit halves, <= 1024 each)
     uint32_t x = (uint32_t)(16 + lo_s16(kc[i]) + hi_s16(kc[i]));
     if (i + 1 < K) x |= (uint32_t)(16 + lo_s16(kc[i + 1 < K ? i + 1 : i]) + hi_s16(kc[i + 1 < K ? i + 1 : i])) << 16;
-    for (int o = 32; o > 0; o >>= 1) x += (uint32_t)__shfl_xor((int)x, o, 64);
-    if (lane == 0) {
+    x = wave_scan_u32(x);                          // lane 63 holds the wave total
+    if (lane == 63) {
       s_kept[i][wid] = x & 0xFFFFu;
       if (i + 1 < K) s_kept[i + 1 < K ? i + 1 : i][wid] = x >> 16;
     }
   }
-  __syncthreads();                                 // staged records, s_kept, s_redo
+  lds_barrier();                                 // staged records, s_kept, s_redo
   if (threadIdx.x == 0) a.tinfo[tile].y = (uint32_t)s_redo;
   if (rec_ok) {
     uint4* dst = (uint4*)(a.rec + (size_t)tile * a.tile_cap * RW);
@@ -532,7 +554,7 @@ __global__ void __launch_bounds__(kThreads) k_fs_main(MainArgs a) {
           atomicAdd(&hcnt[i][min(key - lo0[i], (uint32_t)kFusedMaxW - 1u)], 1u);   // bracket <= kFusedMaxW codes
       }
     }
-    __syncthreads();                               // hcnt complete
+    lds_barrier();                               // hcnt complete
   }
   for (int e = threadIdx.x; e < K * kFusedStat; e += kThreads) {
     const int i = e / kFusedStat, c = e % kFusedStat;
@@ -840,21 +862,48 @@ __global__ void __launch_bounds__(256) k_fs_fixup(FixArgs a) {
 #pragma unroll
   for (int i = 0; i < K; ++i) { tk[i] = s_tk[i]; cut[i] = s_cut[i]; }
   const uint32_t total = s_pre[kFusedGroupTiles];
-  for (uint32_t r = threadIdx.x; r < total; r += blockDim.x) {
-    int l = 0;                                     // tile of record r: last l with s_pre[l] <= r
-    for (int step = 32; step > 0; step >>= 1)
-      if (s_pre[l + step] <= r) l += step;
-    const uint32_t* w = a.rec + ((size_t)(t0 + l) * a.tile_cap + (r - s_pre[l])) * RW;
-    const int64_t idx = w[0];
-    uint32_t b[K];
-    uint32_t kprov = 0;
+  const uint32_t* __restrict__ rec = a.rec;
+  uint16_t* __restrict__ out = (uint16_t*)T.out;
+  constexpr int NB = 4;                            // records in flight per thread
+  int l = 0;                                       // tile of the thread's current record (advances monotonically)
+  for (uint32_t r0 = threadIdx.x; r0 < total; r0 += NB * blockDim.x) {
+    uint4 wv[NB][RW / 4];
+    uint32_t rr[NB];
 #pragma unroll
-    for (int i = 0; i < K; ++i) {
-      b[i] = rec_half(w, 3 + i);
-      kprov |= (uint32_t)(bkey(b[i]) >= s_p1[i]) << i;
+    for (int m = 0; m < NB; ++m) {
+      const uint32_t r = r0 + (uint32_t)m * blockDim.x;
+      rr[m] = r;
+      if (r < total) {
+        while (s_pre[l + 1] <= r) ++l;
+        const uint4* w = (const uint4*)(rec + ((size_t)(t0 + l) * a.tile_cap + (r - s_pre[l])) * RW);
+#pragma unroll
+        for (int z = 0; z < RW / 4; ++z) wv[m][z] = w[z];
+      }
     }
-    const uint32_t kfin = final_mask<K>(b, idx, tk, cut);
-    if (kprov != kfin) store_final<K>(T, idx, b, kfin, rec_half(w, 3 + K), a.lambda, a.want_sign);
+#pragma unroll
+    for (int m = 0; m < NB; ++m) {
+      if (rr[m] >= total) break;
+      uint32_t w[RW];
+#pragma unroll
+      for (int z = 0; z < RW / 4; ++z) {
+        w[4 * z] = wv[m][z].x; w[4 * z + 1] = wv[m][z].y; w[4 * z + 2] = wv[m][z].z; w[4 * z + 3] = wv[m][z].w;
+      }
+      const int64_t idx = w[0];
+      uint32_t b[K];
+      uint32_t kprov = 0;
+#pragma unroll
+      for (int i = 0; i < K; ++i) {
+        b[i] = rec_half(w, 3 + i);
+        kprov |= (uint32_t)(bkey(b[i]) >= s_p1[i]) << i;
+      }
+      const uint32_t kfin = final_mask<K>(b, idx, tk, cut);
+      if (kprov != kfin) {
+        int gam;
+        const double t = ties_general<ISO_BF16, K>(b, kfin, gam);
+        out[idx] = (uint16_t)f64_to_bf16_rne(bits_to_f64<ISO_BF16>(rec_half(w, 3 + K)) + a.lambda * t);
+        if (a.want_sign) ((int8_t*)T.aux2)[idx] = (int8_t)gam;
+      }
+    }
   }
   if (!s_anyredo) return;
   uint32_t kmax = 0;
