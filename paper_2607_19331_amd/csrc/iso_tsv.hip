@@ -146,52 +146,126 @@ __global__ void k_split(const Prob* __restrict__ probs, int which, int cur) {
 }
 
 // ---- MFMA products with the delta -----------------------------------------------------------------
+//
+// Both products stream the delta once per call and keep the skinny right operand B (hi and,
+// when LO, lo bf16 parts; L columns of ldb entries, ldb a multiple of 64 and zero beyond the
+// operand's rows) in LDS, one k-step at a time, double-buffered: the next step's delta and B
+// pieces are loaded into registers before the current step's MFMAs and written to LDS after
+// them, with one workgroup barrier per step.  Each wave owns 64 output rows (four 16-row
+// blocks), so every B fragment read from LDS feeds four MFMAs per part.
+//
+// Workgroups are renumbered so that the consecutive row blocks of one problem run on the same
+// XCD (the hardware deals workgroups to the eight XCDs round-robin): the B window of a problem
+// is then fetched from HBM into one XCD's L2, not into all eight.
 
-// Rows per block of the skinny products: 4 waves x 4 row blocks of 16.
-constexpr int kSkRows = 256;
+constexpr int kSkRows = 256;   // output rows per workgroup: 4 waves x 64
+constexpr int kXcds = 8;
 
-// X[out] (R x L) = Delta (R x C) * B (C x L), B = bh + bl.  Each wave owns 64 rows (four
-// 16-row blocks) so every right-operand fragment feeds four MFMAs per half.
+// Linear workgroup id -> logical id, a bijection on [0, G) that gives each XCD a contiguous
+// range of logical ids.
+__device__ __forceinline__ int64_t xcd_logical_block(int64_t b, int64_t G) {
+  const int64_t q = G / kXcds, rem = G % kXcds;
+  const int64_t x = b % kXcds, i = b / kXcds;
+  return (x < rem) ? x * (q + 1) + i : rem * (q + 1) + (x - rem) * q + i;
+}
+
+// B pieces of one k-step: H parts x NB*16 columns x KG 16-byte groups of 8 k.
+template <int NB, int H, int KG>
+struct SkB {
+  static constexpr int kPieces = H * NB * 16 * KG;
+  static constexpr int kPerThread = (kPieces + 255) / 256;
+  bf16x8_t q[kPerThread];
+  __device__ __forceinline__ void load(const Prob& P, int64_t k0) {
+#pragma unroll
+    for (int j = 0; j < kPerThread; ++j) {
+      const int t = threadIdx.x + 256 * j;
+      if (kPieces % 256 == 0 || t < kPieces) {
+        const int h = t / (NB * 16 * KG), rem = t % (NB * 16 * KG), col = rem / KG, kg = rem % KG;
+        q[j] = ld_bf16x8((h ? P.bl : P.bh) + (int64_t)col * P.ldb + k0 + 8 * kg);
+      }
+    }
+  }
+  __device__ __forceinline__ void store(bf16x8_t (*sh)[NB * 16][KG + 1]) const {
+#pragma unroll
+    for (int j = 0; j < kPerThread; ++j) {
+      const int t = threadIdx.x + 256 * j;
+      if (kPieces % 256 == 0 || t < kPieces) {
+        const int h = t / (NB * 16 * KG), rem = t % (NB * 16 * KG), col = rem / KG, kg = rem % KG;
+        sh[h][col][kg] = q[j];
+      }
+    }
+  }
+};
+
+// X[out] (R x L) = Delta (R x C) * bh (C x L), hi part only (every product of this kind feeds a
+// QR of the range finder).  64 k per step: each delta row is read 128 bytes at a time, straight
+// into MFMA A fragments (lane (ln, g) holds row ln, k = 8g..8g+7 of each 32-k half).  Rows past R are clamped to R - 1 and not stored; with C % 8 == 0, k groups past
+// C are clamped into the row (B is zero there), otherwise entries are loaded one by one and
+// zero-filled.
 template <int NB>
-__global__ void __launch_bounds__(256) k_mfma_nn(const Prob* __restrict__ probs, int out) {
-  const Prob& P = probs[blockIdx.z];
+__global__ void __launch_bounds__(256) k_sk_nn(const Prob* __restrict__ probs, int out, int64_t nbx) {
+  constexpr int KS = 64, KG = KS / 8, H = 1;
+  __shared__ bf16x8_t bsh[2][H][NB * 16][KG + 1];
+  const int64_t lb = xcd_logical_block(blockIdx.x + (int64_t)gridDim.x * blockIdx.z, (int64_t)gridDim.x * gridDim.z);
+  const Prob& P = probs[lb / nbx];
   const int64_t R = P.R, C = P.C;
-  const int64_t m0 = (int64_t)blockIdx.x * kSkRows;
+  const int64_t m0 = (lb % nbx) * kSkRows;
   if (m0 >= R) return;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
   const int64_t wrow = m0 + 64 * w;
   const bool vec = (C % 8) == 0;
+  const uint16_t* arow[4];
+  int64_t rr[4];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) {
+    rr[rb] = min(R - 1, wrow + 16 * rb + ln);
+    arow[rb] = P.delta + rr[rb] * C;
+  }
+  auto load_a = [&](int64_t k0, bf16x8_t (&a)[4][2]) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const int64_t k = k0 + 32 * kb + 8 * g;
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        if (vec) a[rb][kb] = ld_bf16x8(arow[rb] + min(k, C - 8));
+        else a[rb][kb] = ld_row8(P.delta, R, C, rr[rb], k, false);
+      }
+    }
+  };
   f32x4_t acc[4][NB];
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
     for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  if (wrow < R) {
-    // the delta stream is software-pipelined: the next step's fragments are in flight while
-    // the current step's MFMAs run
-    bf16x8_t a[4], an[4];
+  const int64_t steps = (C + KS - 1) / KS;
+  bf16x8_t a[4][2], an[4][2];
+  SkB<NB, H, KG> bq;
+  load_a(0, a);
+  bq.load(P, 0);
+  bq.store(bsh[0]);
+  __syncthreads();
+  for (int64_t s = 0; s < steps; ++s) {
+    const bool more = s + 1 < steps;
+    if (more) {
+      bq.load(P, (s + 1) * KS);
+      load_a((s + 1) * KS, an);
+    }
+    const int buf = (int)(s & 1);
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb) a[rb] = ld_row8(P.delta, R, C, wrow + 16 * rb + ln, 8 * g, vec);
-    for (int64_t k0 = 0; k0 < C; k0 += 32) {
-      const int64_t k = k0 + 8 * g;
-      const bool more = k0 + 32 < C;
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
-        an[rb] = more ? ld_row8(P.delta, R, C, wrow + 16 * rb + ln, k + 32, vec) : a[rb];
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
-        const int64_t col = cb * 16 + ln;
-        const bf16x8_t bh = ld_bf16x8(P.bh + col * P.ldb + k);
-        const bf16x8_t bl = ld_bf16x8(P.bl + col * P.ldb + k);
+        const bf16x8_t bh = bsh[buf][0][cb * 16 + ln][4 * kb + g];
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb) {
-          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rb], bh, acc[rb][cb], 0, 0, 0);
-          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rb], bl, acc[rb][cb], 0, 0, 0);
-        }
+        for (int rb = 0; rb < 4; ++rb)
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rb][kb], bh, acc[rb][cb], 0, 0, 0);
       }
+    if (more) bq.store(bsh[buf ^ 1]);
+    __syncthreads();
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb) a[rb] = an[rb];
-    }
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) a[rb][kb] = an[rb][kb];
   }
   double* X = P.X[out];
 #pragma unroll
@@ -205,10 +279,122 @@ __global__ void __launch_bounds__(256) k_mfma_nn(const Prob* __restrict__ probs,
       }
 }
 
-// Z[out] (C x L) = Delta^T (C x R) * B (R x L), B = bh + bl.  A 32 x 256 tile of the delta
-// is staged in LDS and read transposed; each wave owns 64 output rows.
+// Swizzle of the delta tile in LDS (32 rows x 256 columns, row-major, no padding): the 8-byte
+// chunk c of row r is stored at chunk c ^ 4*s(r).  s takes eight distinct values over the
+// rows {0..3, 8..11} (and {4..7, 12..15}, ...), so each transposed read of 16 rows x 32 bytes
+// below touches every LDS bank exactly twice.
+__device__ __forceinline__ int sk_swz(int r) { return ((r & 3) | (((r >> 3) & 1) << 2)) << 2; }
+
+typedef __bf16 bf16x4v_t __attribute__((__vector_size__(4 * sizeof(__bf16))));
+
+// Z[out] (C x L) = Delta^T (C x R) * B (R x L).  Each workgroup owns 256 delta columns and walks
+// the delta rows 32 at a time: the 32 x 256 tile (row segments of 512 bytes) goes through LDS and
+// the A fragments of Delta^T are read from it with ds_read_b64_tr_b16.  Within a 16-lane group
+// that instruction hands lane i, element m, the (i & 3)-th value of the 8 bytes that lane
+// 4m + (i >> 2) addressed; with lane 4m + q pointing at columns 4q..4q+3 of row m, lane i
+// receives column i of four consecutive rows.  Two such reads (rows 8g..8g+3, 8g+4..8g+7) form
+// the fragment lane (ln, g) needs: column ln, k = 8g..8g+7.  Rows past R are clamped (B is zero
+// there); columns past C are clamped and not stored.  Requires C % 8 == 0 (the host routes other
+// shapes to k_sk_tn_any).
+template <int NB, bool LO>
+__global__ void __launch_bounds__(256) k_sk_tn(const Prob* __restrict__ probs, int out, int64_t nbx) {
+  constexpr int KS = 32, KG = KS / 8, H = LO ? 2 : 1;
+  __shared__ __align__(16) uint16_t atile[2][KS][kSkRows];
+  __shared__ bf16x8_t bsh[2][H][NB * 16][KG + 1];
+  const int64_t lb = xcd_logical_block(blockIdx.x + (int64_t)gridDim.x * blockIdx.z, (int64_t)gridDim.x * gridDim.z);
+  const Prob& P = probs[lb / nbx];
+  const int64_t R = P.R, C = P.C;
+  const int64_t i0 = (lb % nbx) * kSkRows;
+  if (i0 >= C) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
+  // tile pieces: 32 rows x 32 pieces of 16 bytes, four per thread
+  bf16x8_t pa[4];
+  auto load_a = [&](int64_t k0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int t = threadIdx.x + 256 * j, row = t >> 5, pc = t & 31;
+      const int64_t gr = min(R - 1, k0 + row), gc = min(C - 8, i0 + 8 * pc);
+      pa[j] = ld_bf16x8(P.delta + gr * C + gc);
+    }
+  };
+  auto store_a = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int t = threadIdx.x + 256 * j, row = t >> 5, pc = t & 31;
+      *(bf16x8_t*)&atile[buf][row][(8 * pc) ^ (4 * sk_swz(row))] = pa[j];
+    }
+  };
+  // transposed-read addresses: lane 16G + 4m + q reads row 8G + 4h + m, logical chunk 16w + 4rb + q
+  const int G = lane >> 4, m = (lane >> 2) & 3, q = lane & 3;
+  f32x4_t acc[4][NB];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int64_t steps = (R + KS - 1) / KS;
+  SkB<NB, H, KG> bq;
+  load_a(0);
+  bq.load(P, 0);
+  store_a(0);
+  bq.store(bsh[0]);
+  __syncthreads();
+  for (int64_t s = 0; s < steps; ++s) {
+    const bool more = s + 1 < steps;
+    if (more) {
+      bq.load(P, (s + 1) * KS);
+      load_a((s + 1) * KS);
+    }
+    const int buf = (int)(s & 1);
+    bf16x8_t a[4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+      bf16x4v_t h2[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int row = 8 * G + 4 * h + m;
+        const int chunk = (16 * w + 4 * rb + q) ^ sk_swz(row);
+        h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (__attribute__((address_space(3))) bf16x4v_t*)&atile[buf][row][4 * chunk]);
+      }
+      const uint2 u0 = __builtin_bit_cast(uint2, h2[0]), u1 = __builtin_bit_cast(uint2, h2[1]);
+      a[rb] = __builtin_bit_cast(bf16x8_t, make_uint4(u0.x, u0.y, u1.x, u1.y));
+    }
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const bf16x8_t bh = bsh[buf][0][cb * 16 + ln][g];
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb)
+        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rb], bh, acc[rb][cb], 0, 0, 0);
+      if (LO) {
+        const bf16x8_t bl = bsh[buf][H - 1][cb * 16 + ln][g];
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb)
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rb], bl, acc[rb][cb], 0, 0, 0);
+      }
+    }
+    if (more) {
+      store_a(buf ^ 1);
+      bq.store(bsh[buf ^ 1]);
+    }
+    __syncthreads();
+  }
+  double* Z = P.Z[out];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t r = i0 + 64 * w + 16 * rb + 4 * g + e;
+        if (r < C) Z[r * P.L + cb * 16 + ln] = (double)acc[rb][cb][e];
+      }
+}
+
+// Z[out] (C x L) = Delta^T (C x R) * (bh + bl) for any C (rows not 16-byte aligned): a 32 x 256
+// tile of the delta is staged in LDS and read transposed one entry at a time; B is read from
+// global memory.  Each wave owns 64 output rows.
 template <int NB>
-__global__ void __launch_bounds__(256) k_mfma_tn(const Prob* __restrict__ probs, int out) {
+__global__ void __launch_bounds__(256) k_sk_tn_any(const Prob* __restrict__ probs, int out) {
   __shared__ uint16_t tile[32][kSkRows + 2];
   const Prob& P = probs[blockIdx.z];
   const int64_t R = P.R, C = P.C;
@@ -628,7 +814,7 @@ Sizes sizes_of(const iso_tensor& t, int K, int r) {
   z.R = t.rows;
   z.C = t.cols;
   z.L = tsv_sketch_width(t.rows, t.cols, r);
-  z.ldb = rup(std::max(z.R, z.C), 32);
+  z.ldb = rup(std::max(z.R, z.C), 64);
   z.Kr = (int64_t)K * r;
   z.ldk = rup(z.Kr, 32);
   return z;
@@ -716,11 +902,18 @@ size_t table_bytes(int nm, int K) {
 
 template <int NB>
 void launch_nn(const Prob* d, int np, int64_t maxR, int out, hipStream_t s) {
-  k_mfma_nn<NB><<<dim3((unsigned)((maxR + kSkRows - 1) / kSkRows), 1, (unsigned)np), 256, 0, s>>>(d, out);
+  const int64_t nbx = (maxR + kSkRows - 1) / kSkRows;
+  k_sk_nn<NB><<<dim3((unsigned)nbx, 1, (unsigned)np), 256, 0, s>>>(d, out, nbx);
 }
+// lo: include the lo part of B (the last product, whose values form the result)
+// aligned: every delta of the chunk has C % 8 == 0 (rows start 16-byte aligned)
 template <int NB>
-void launch_tn(const Prob* d, int np, int64_t maxC, int out, hipStream_t s) {
-  k_mfma_tn<NB><<<dim3((unsigned)((maxC + kSkRows - 1) / kSkRows), 1, (unsigned)np), 256, 0, s>>>(d, out);
+void launch_tn(const Prob* d, int np, int64_t maxC, int out, bool lo, bool aligned, hipStream_t s) {
+  const int64_t nbx = (maxC + kSkRows - 1) / kSkRows;
+  const dim3 grid((unsigned)nbx, 1, (unsigned)np);
+  if (!aligned) k_sk_tn_any<NB><<<grid, 256, 0, s>>>(d, out);
+  else if (lo) k_sk_tn<NB, true><<<grid, 256, 0, s>>>(d, out, nbx);
+  else k_sk_tn<NB, false><<<grid, 256, 0, s>>>(d, out, nbx);
 }
 template <int T>
 void launch_gram(const Prob* d, int np, int which, int cur, hipStream_t s) {
@@ -823,6 +1016,8 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     for (int p = 0; p < np; ++p)
       if (hp[p].L != L) return ISO_ERR_UNSUPPORTED;
     const int NB = (int)(L / 16);
+    bool aligned = true;
+    for (int p = 0; p < np; ++p) aligned = aligned && hp[p].C % 8 == 0;
     const int64_t maxM = std::max(maxR, maxC);
     // gemm job tables: 0 U_i = X Ut[:, :r]; 1 V_i = Z Vt[:, :r]; 2 GU slabs; 3 GV slabs;
     // 5 U_perp = U M_U, V_perp = V M_V; 6..11 Newton-Schulz steps (T, Y, Z) for parities 0, 1
@@ -894,7 +1089,7 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
       std::memcpy(h_ndst, ns_dst.data(), sizeof(double*) * ns_dst.size());
     }
     TS_TRY(hipMemcpyAsync(ws, host.data(), tb, hipMemcpyHostToDevice, s));
-    const unsigned gx = grid_for(L * rup(maxM, 32));
+    const unsigned gx = grid_for(L * rup(maxM, 64));
     auto cholqr = [&](int which, int& cur, int save_first, int accum_second, int passes) {
       const int64_t mm = which ? maxC : maxR;
       for (int pass = 0; pass < passes; ++pass) {
@@ -910,11 +1105,15 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     k_omega<<<dim3(gx, np), 256, 0, s>>>(d_prob);
     // Cholesky-QR2 where orthogonality is carried forward (first sketch, final factor); one
     // pass inside the power iteration, whose next product and QR absorb its rounding
+    // The sketches of the range finder only have to span the dominant subspace: rounding their
+    // right operand to bf16 (relative 2^-9) tilts the next iterate by about 2^-9 sigma_{r+1} /
+    // sigma_r, which the following QR and product absorb; the last product, whose values form
+    // the result, takes both parts (relative 2^-17).
     DISPATCH_NB(NB, launch_nn, d_prob, np, maxR, cx, s);
     cholqr(0, cx, 0, 0, 2);
     for (int it = 0; it < kPowerIters; ++it) {
       k_split<<<dim3(gx, np), 256, 0, s>>>(d_prob, 0, cx);
-      DISPATCH_NB(NB, launch_tn, d_prob, np, maxC, cz, s);
+      DISPATCH_NB(NB, launch_tn, d_prob, np, maxC, cz, false, aligned, s);
       cholqr(1, cz, 0, 0, 1);
       k_split<<<dim3(gx, np), 256, 0, s>>>(d_prob, 1, cz);
       DISPATCH_NB(NB, launch_nn, d_prob, np, maxR, cx, s);
@@ -922,7 +1121,7 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     }
     // 2. B^T = Delta^T Q, its QR (R2 accumulated), SVD of the L x L core R2^T
     k_split<<<dim3(gx, np), 256, 0, s>>>(d_prob, 0, cx);
-    DISPATCH_NB(NB, launch_tn, d_prob, np, maxC, cz, s);
+    DISPATCH_NB(NB, launch_tn, d_prob, np, maxC, cz, true, aligned, s);
     cholqr(1, cz, 1, 1, 2);
     k_core_load<<<np, 256, 0, s>>>(d_prob, d_jobs);
     k_jacobi<<<np, kJacobiThreads, 0, s>>>(d_jobs, status);

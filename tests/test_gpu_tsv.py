@@ -4,8 +4,10 @@ The truncation to the top r singular triplets is only well defined when sigma_r 
 sigma_{r+1}; the deltas here are planted: Delta_i = P_i diag(s_i) Q_i^T plus small noise,
 rounded to bf16, so the gap is wide and the oracle's exact (LAPACK) truncation is what the
 GPU's randomised subspace iteration must reproduce.  Tolerances come from the GPU arithmetic:
-the products with the delta and the reconstruction use bf16-split MFMA with binary32
-accumulation (about 2^-16 relative per operand), so the fp32 Delta_hat must agree to 1e-3
+the last product with the delta and the reconstruction use bf16-split MFMA with binary32
+accumulation (about 2^-16 relative per operand; the earlier sketches of the range finder use the
+bf16 hi part only, which tilts the subspace by about 2^-9 sigma_{r+1}/sigma_r before the next QR
+absorbs it), so the fp32 Delta_hat must agree to 1e-3
 of max|Delta_hat| elementwise and 2e-4 relative in Frobenius norm.  A merged bf16 weight must
 lie within half an ulp of W_0 + alpha*Delta_hat (exact reference) plus |alpha| times that
 Delta_hat bound; where the update is small against the weights (the realistic regime) it is
