@@ -242,7 +242,9 @@ namespace iso {
 namespace {
 
 // A batch of independent GEMMs in one launch: grid.z indexes the job; blocks outside a
-// job's M x N exit.  Same arithmetic as k_gemm.
+// job's M x N exit.  C(i,j) = alpha * sum_k A(i,k) B(k,j) + beta * C(i,j) with X(i,k) at
+// X[i*xs0 + k*xs1].  `upper`: only the tiles on or above the diagonal are computed (for a
+// symmetric product whose lower triangle the caller fills in).
 struct GemmJob {
   const double* A;
   const double* B;
@@ -250,46 +252,84 @@ struct GemmJob {
   int64_t as0, as1, bs0, bs1, cs0, cs1;
   int64_t M, N, K;
   double alpha, beta;
+  int upper;
 };
 
+typedef double gemm_f64x4_t __attribute__((ext_vector_type(4)));
+
+// 64 x 64 output tile per workgroup on v_mfma_f64_16x16x4_f64 (lane (ln, g) supplies A[ln][g]
+// and B[g][ln], receives D[g + 4v][ln] in register pair v): four waves as 2 x 2, each a 32 x 32 block of four
+// MFMA tiles; k in steps of 16 staged in LDS.  Operands are loaded along whichever of their
+// strides is 1, so row- and column-major inputs both read whole cache lines.  LDS rows are 80
+// doubles apart, which puts the four k rows of a fragment read on disjoint bank halves.
+constexpr int GJP = 80;
 __global__ void __launch_bounds__(256) k_gemm_jobs(const GemmJob* __restrict__ jobs) {
-  __shared__ double As[GK][GT + 1];
-  __shared__ double Bs[GK][GT + 1];
+  __shared__ double As[GK][GJP];
+  __shared__ double Bs[GK][GJP];
   const GemmJob J = jobs[blockIdx.z];
   const int64_t i0 = (int64_t)blockIdx.x * GT, j0 = (int64_t)blockIdx.y * GT;
-  if (i0 >= J.M || j0 >= J.N) return;
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  double acc[4][4] = {};
+  if (i0 >= J.M || j0 >= J.N || (J.upper && i0 > j0)) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
+  const int wm = w >> 1, wn = w & 1;
+  const bool a_kfast = J.as1 == 1, b_kfast = J.bs0 == 1;
+  gemm_f64x4_t acc[2][2];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = gemm_f64x4_t{0.0, 0.0, 0.0, 0.0};
+  // the next k-tile is loaded into registers while the current one is multiplied
+  constexpr int PT = (GK * GT) / 256;
+  double pa[PT], pb[PT];
+  auto load = [&](int64_t k0) {
+#pragma unroll
+    for (int q = 0; q < PT; ++q) {
+      const int e = threadIdx.x + 256 * q;
+      const int ka = a_kfast ? (e & 15) : (e >> 6), ia = a_kfast ? (e >> 4) : (e & 63);
+      const int kb = b_kfast ? (e & 15) : (e >> 6), jb = b_kfast ? (e >> 4) : (e & 63);
+      const int64_t gi = i0 + ia, gka = k0 + ka, gj = j0 + jb, gkb = k0 + kb;
+      pa[q] = (gi < J.M && gka < J.K) ? J.A[gi * J.as0 + gka * J.as1] : 0.0;
+      pb[q] = (gj < J.N && gkb < J.K) ? J.B[gkb * J.bs0 + gj * J.bs1] : 0.0;
+    }
+  };
+  load(0);
   for (int64_t k0 = 0; k0 < J.K; k0 += GK) {
-    for (int e = threadIdx.x; e < GK * GT; e += 256) {
-      const int kk = e / GT, ii = e % GT;
-      const int64_t gi = i0 + ii, gk = k0 + kk, gj = j0 + ii;
-      As[kk][ii] = (gi < J.M && gk < J.K) ? J.A[gi * J.as0 + gk * J.as1] : 0.0;
-      Bs[kk][ii] = (gj < J.N && gk < J.K) ? J.B[gk * J.bs0 + gj * J.bs1] : 0.0;
+#pragma unroll
+    for (int q = 0; q < PT; ++q) {
+      const int e = threadIdx.x + 256 * q;
+      const int ka = a_kfast ? (e & 15) : (e >> 6), ia = a_kfast ? (e >> 4) : (e & 63);
+      const int kb = b_kfast ? (e & 15) : (e >> 6), jb = b_kfast ? (e >> 4) : (e & 63);
+      As[ka][ia] = pa[q];
+      Bs[kb][jb] = pb[q];
     }
     __syncthreads();
+    if (k0 + GK < J.K) load(k0 + GK);
 #pragma unroll
-    for (int kk = 0; kk < GK; ++kk) {
-      double a[4], b[4];
+    for (int sub = 0; sub < GK / 4; ++sub) {
+      double a[2], b[2];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) { a[u] = As[kk][tx + 16 * u]; b[u] = Bs[kk][ty + 16 * u]; }
+      for (int rb = 0; rb < 2; ++rb) a[rb] = As[4 * sub + g][32 * wm + 16 * rb + ln];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int cb = 0; cb < 2; ++cb) b[cb] = Bs[4 * sub + g][32 * wn + 16 * cb + ln];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) acc[u][v] = acc[u][v] + a[u] * b[v];
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+          acc[rb][cb] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[rb], b[cb], acc[rb][cb], 0, 0, 0);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int64_t gi = i0 + tx + 16 * u, gj = j0 + ty + 16 * v;
-      if (gi < J.M && gj < J.N) {
-        double* cp = J.C + gi * J.cs0 + gj * J.cs1;
-        *cp = (J.beta == 0.0) ? J.alpha * acc[u][v] : J.alpha * acc[u][v] + J.beta * *cp;
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int64_t gi = i0 + 32 * wm + 16 * rb + g + 4 * v, gj = j0 + 32 * wn + 16 * cb + ln;
+        if (gi < J.M && gj < J.N) {
+          double* cp = J.C + gi * J.cs0 + gj * J.cs1;
+          *cp = (J.beta == 0.0) ? J.alpha * acc[rb][cb][v] : J.alpha * acc[rb][cb][v] + J.beta * *cp;
+        }
       }
-    }
 }
 
 }  // namespace

@@ -16,6 +16,7 @@
 // The randomised sketch draws its test matrix from a counter-based hash (SplitMix64); the
 // result does not depend on it to the accuracy of the truncation where the spectrum has a gap.
 #include <cstring>
+#include <utility>
 #include <vector>
 
 #include "iso_dense.h"
@@ -126,22 +127,6 @@ __global__ void k_omega(const Prob* __restrict__ probs) {
     if (k < P.C) v = (float)((int)(splitmix64(P.seed ^ (uint64_t)e) >> 57) - 64) * 0.015625f;
     P.bh[e] = bf16_rne_f32(v);
     P.bl[e] = 0;
-  }
-}
-
-// Split the current tall factor (which = 0: X[cur], R rows; 1: Z[cur], C rows) into bf16
-// hi/lo columns.
-__global__ void k_split(const Prob* __restrict__ probs, int which, int cur) {
-  const Prob& P = probs[blockIdx.y];
-  const int64_t M = which ? P.C : P.R;
-  const double* src = which ? P.Z[cur] : P.X[cur];
-  const int64_t total = P.L * P.ldb;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t col = e / P.ldb, k = e - col * P.ldb;
-    const float v = (k < M) ? (float)src[k * P.L + col] : 0.0f;
-    const uint16_t h = bf16_rne_f32(v);
-    P.bh[e] = h;
-    P.bl[e] = bf16_rne_f32(v - f32_of_bf16(h));
   }
 }
 
@@ -470,140 +455,341 @@ __global__ void __launch_bounds__(256) k_sk_tn_any(const Prob* __restrict__ prob
 }
 
 // ---- Cholesky-QR pieces ------------------------------------------------------------------------------
+//
+// Binary64 throughout, on v_mfma_f64_16x16x4_f64: lane (ln, g) supplies A[ln][g] and B[g][ln] and
+// receives D[g + 4v][ln] in its v-th register pair, v = 0..3 (probed on the device).
 
-// Gram partials of the current tall factor: Gp[z] = sum over rows of slab z of x x^T.
-template <int T>
-__global__ void __launch_bounds__(256) k_gram_slab(const Prob* __restrict__ probs, int which, int cur) {
-  __shared__ double rows[32][16 * T + 1];
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f64x4_t mfma64(double a, double b, f64x4_t c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
+// Tile pair p of the upper triangle (rb <= cb) of an nb x nb grid of 16 x 16 tiles, row by row.
+constexpr int pair_rb(int p, int nb) {
+  int rb = 0;
+  while (p >= nb - rb) { p -= nb - rb; ++rb; }
+  return rb;
+}
+constexpr int pair_cb(int p, int nb) {
+  int rb = 0;
+  while (p >= nb - rb) { p -= nb - rb; ++rb; }
+  return rb + p;
+}
+
+template <int NB, int P>
+struct TilePair {
+  static constexpr int rb = pair_rb(P, NB), cb = pair_cb(P, NB);
+};
+
+// acc[i] += x[rb] x[cb]^T for the pairs W + 4i (compile-time indices throughout)
+template <int NB, int W, int... I>
+__device__ __forceinline__ void gram_mfmas(f64x4_t* acc, const double* x, std::integer_sequence<int, I...>) {
+  ((acc[I] = mfma64(x[TilePair<NB, W + 4 * I>::rb], x[TilePair<NB, W + 4 * I>::cb], acc[I])), ...);
+}
+template <int NB, int W, int... I>
+__device__ __forceinline__ void gram_store(const f64x4_t* acc, double* __restrict__ Gz, int g, int ln,
+                                           std::integer_sequence<int, I...>) {
+  constexpr int L = 16 * NB;
+  (
+      [&] {
+        constexpr int rb = TilePair<NB, W + 4 * I>::rb, cb = TilePair<NB, W + 4 * I>::cb;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          Gz[(16 * rb + g + 4 * v) * L + 16 * cb + ln] = acc[I][v];
+          if (rb != cb) Gz[(16 * cb + ln) * L + 16 * rb + g + 4 * v] = acc[I][v];
+        }
+      }(),
+      ...);
+}
+
+// One wave's share of a Gram partial: pairs W, W + 4, ... of the upper triangle, over rows
+// [r0, r1) of X (row-major, L = 16 NB columns), eight rows per step.  Writes both triangles.
+template <int NB, int W>
+__device__ __forceinline__ void gram_wave(const double* __restrict__ X, int64_t r0, int64_t r1, double* __restrict__ Gz,
+                                          int lane) {
+  constexpr int L = 16 * NB, NP = NB * (NB + 1) / 2, PW = (NP - W + 3) / 4;
+  if constexpr (PW > 0) {
+    using Seq = std::make_integer_sequence<int, PW>;
+    const int g = lane >> 4, ln = lane & 15;
+    f64x4_t acc[PW];
+#pragma unroll
+    for (int i = 0; i < PW; ++i) acc[i] = f64x4_t{0.0, 0.0, 0.0, 0.0};
+    for (int64_t k0 = r0; k0 < r1; k0 += 8) {
+      double x0[NB], x1[NB];
+      const int64_t ra = k0 + g, rc = k0 + 4 + g;
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        x0[j] = (ra < r1) ? X[ra * L + 16 * j + ln] : 0.0;
+        x1[j] = (rc < r1) ? X[rc * L + 16 * j + ln] : 0.0;
+      }
+      gram_mfmas<NB, W>(acc, x0, Seq{});
+      gram_mfmas<NB, W>(acc, x1, Seq{});
+    }
+    gram_store<NB, W>(acc, Gz, g, ln, Seq{});
+  }
+}
+
+// Gram partials of the current tall factor: Gp[z] = sum over the rows of slab z of x x^T.
+template <int NB>
+__global__ void __launch_bounds__(256) k_gram_mf(const Prob* __restrict__ probs, int which, int cur) {
   const Prob& P = probs[blockIdx.y];
   const int64_t M = which ? P.C : P.R;
   const double* X = which ? P.Z[cur] : P.X[cur];
-  const int64_t L = P.L;
   const int64_t per = (M + kSlabs - 1) / kSlabs;
-  const int64_t r0 = (int64_t)blockIdx.x * per, r1 = min(M, r0 + per);
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  double acc[T][T] = {};
-  for (int64_t b = r0; b < r1; b += 32) {
-    for (int e = threadIdx.x; e < 32 * 16 * T; e += 256) {
-      const int rr = e / (16 * T), cc = e % (16 * T);
-      rows[rr][cc] = (b + rr < r1 && cc < L) ? X[(b + rr) * L + cc] : 0.0;
-    }
-    __syncthreads();
-    const int nr = (int)min<int64_t>(32, r1 - b);
-    for (int rr = 0; rr < nr; ++rr) {
-      double xa[T], xb[T];
-#pragma unroll
-      for (int u = 0; u < T; ++u) { xa[u] = rows[rr][ty * T + u]; xb[u] = rows[rr][tx * T + u]; }
-#pragma unroll
-      for (int u = 0; u < T; ++u)
-#pragma unroll
-        for (int v = 0; v < T; ++v) acc[u][v] = acc[u][v] + xa[u] * xb[v];
-    }
-    __syncthreads();
+  const int64_t r0 = min(M, (int64_t)blockIdx.x * per), r1 = min(M, r0 + per);
+  double* Gz = P.Gp + (int64_t)blockIdx.x * P.L * P.L;
+  const int lane = threadIdx.x & 63;
+  switch (threadIdx.x >> 6) {
+    case 0: gram_wave<NB, 0>(X, r0, r1, Gz, lane); break;
+    case 1: gram_wave<NB, 1>(X, r0, r1, Gz, lane); break;
+    case 2: gram_wave<NB, 2>(X, r0, r1, Gz, lane); break;
+    default: gram_wave<NB, 3>(X, r0, r1, Gz, lane); break;
   }
-  double* Gz = P.Gp + (int64_t)blockIdx.x * L * L;
-#pragma unroll
-  for (int u = 0; u < T; ++u)
-#pragma unroll
-    for (int v = 0; v < T; ++v) {
-      const int64_t a = ty * T + u, c = tx * T + v;
-      if (a < L && c < L) Gz[a * L + c] = acc[u][v];
-    }
 }
 
 // G = sum of the partials, then G = R^T R (R upper, row-major in Rf) and Ri = R^{-1}.  With
-// `acc`: R2 = Rf * Ra (second factor times the saved first), and `save`: Ra = Rf.
+// `acc`: R2 = Rf * Ra (second factor times the saved first), and `save`: Ra = Rf.  Both the
+// factorisation and the inverse run pivot by pivot with the work of a pivot spread over the
+// workgroup.  The inverse X = R^{-1} is formed column-oriented from X = I: for i = L-1 down to 0,
+// row i of X is divided by R[i][i], then X[t][c] -= R[t][i] X[i][c] for t < i <= c.  X is upper
+// triangular and is kept transposed in the unused lower triangle of g (X[t][c] at g[c][t]), its
+// diagonal in di.
 __global__ void __launch_bounds__(256) k_chol(const Prob* __restrict__ probs, int save, int accum, uint32_t* status) {
-  extern __shared__ double g[];                  // L x L
+  extern __shared__ double g[];                  // L x L, then L diagonal entries of the inverse
   const Prob& P = probs[blockIdx.x];
-  const int64_t L = P.L;
-  for (int64_t e = threadIdx.x; e < L * L; e += blockDim.x) {
-    double s = 0.0;
-    for (int z = 0; z < kSlabs; ++z) s = s + P.Gp[(int64_t)z * L * L + e];
-    g[e] = s;
-  }
-  __syncthreads();
-  __shared__ double shift;
-  if (threadIdx.x == 0) {
-    double tr = 0.0;
-    for (int64_t j = 0; j < L; ++j) tr += g[j * L + j];
-    shift = 1e-15 * tr / (double)L + 1e-300;
-  }
-  __syncthreads();
-  for (int64_t j = 0; j < L; ++j) {
-    if (threadIdx.x == 0) {
-      double d = g[j * L + j];
-      g[j * L + j] = sqrt(d > shift ? d : shift);
-    }
-    __syncthreads();
-    for (int64_t k = j + 1 + threadIdx.x; k < L; k += blockDim.x) g[j * L + k] /= g[j * L + j];
-    __syncthreads();
-    const int64_t n = L - j - 1;
-    for (int64_t e = threadIdx.x; e < n * n; e += blockDim.x) {
-      const int64_t i = j + 1 + e / n, k = j + 1 + e % n;
-      if (k >= i) g[i * L + k] -= g[j * L + i] * g[j * L + k];
-    }
-    __syncthreads();
-  }
-  for (int64_t e = threadIdx.x; e < L * L; e += blockDim.x) {
-    const int64_t i = e / L, k = e % L;
-    P.Rf[e] = (k >= i) ? g[e] : 0.0;
-  }
-  // inverse of the upper factor, one column per thread (back substitution)
-  for (int64_t c = threadIdx.x; c < L; c += blockDim.x) {
-    for (int64_t i = L - 1; i >= 0; --i) {
-      double v;
-      if (i > c) v = 0.0;
-      else {
-        double s = (i == c) ? 1.0 : 0.0;
-        for (int64_t t = i + 1; t <= c; ++t) s -= g[i * L + t] * P.Ri[t * L + c];
-        v = s / g[i * L + i];
+  const int L = (int)P.L;
+  const double* __restrict__ Gp = P.Gp;
+  double* di = g + L * L;
+  for (int e0 = threadIdx.x; e0 < L * L; e0 += 4 * blockDim.x) {
+    double s[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int z = 0; z < kSlabs; ++z)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int e = e0 + u * blockDim.x;
+        if (e < L * L) s[u] = s[u] + Gp[(int64_t)z * L * L + e];
       }
-      P.Ri[i * L + c] = v;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (e0 + u * (int)blockDim.x < L * L) g[e0 + u * blockDim.x] = s[u];
+  }
+  __syncthreads();
+  double tr = 0.0;
+  for (int j = 0; j < L; ++j) tr += g[j * L + j];
+  const double shift = 1e-15 * tr / (double)L + 1e-300;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  for (int j = 0; j < L; ++j) {
+    // every thread forms the pivot itself and row j is scaled; the pivot is stored once every
+    // thread has read the old diagonal, then the trailing triangle is updated
+    __syncthreads();
+    const double d = g[j * L + j];
+    const double piv = sqrt(d > shift ? d : shift);
+    for (int k = j + 1 + threadIdx.x; k < L; k += blockDim.x) g[j * L + k] /= piv;
+    __syncthreads();
+    if (threadIdx.x == 0) g[j * L + j] = piv;
+    for (int i = j + 1 + ty; i < L; i += 16) {
+      const double a = g[j * L + i];
+#pragma unroll 4
+      for (int k = i + tx; k < L; k += 16) g[i * L + k] -= a * g[j * L + k];
+    }
+  }
+  // inverse: X = I, then pivots from the last
+  for (int e = threadIdx.x; e < L; e += blockDim.x) di[e] = 1.0;
+  for (int c = ty; c < L; c += 16)
+    for (int t = tx; t < c; t += 16) g[c * L + t] = 0.0;
+  for (int i = L - 1; i >= 0; --i) {
+    __syncthreads();
+    const double rii = g[i * L + i];
+    for (int c = i + threadIdx.x; c < L; c += blockDim.x) {
+      if (c == i) di[i] = 1.0 / rii;
+      else g[c * L + i] /= rii;
+    }
+    __syncthreads();
+    for (int c = i + ty; c < L; c += 16) {
+      const double xic = (c == i) ? di[i] : g[c * L + i];
+#pragma unroll 4
+      for (int t = tx; t < i; t += 16) g[c * L + t] -= g[t * L + i] * xic;
     }
   }
   __syncthreads();
-  if (save)
-    for (int64_t e = threadIdx.x; e < L * L; e += blockDim.x) P.Ra[e] = P.Rf[e];
-  if (accum) {
-    // R2 = Rf * Ra  (both upper)
-    for (int64_t e = threadIdx.x; e < L * L; e += blockDim.x) {
-      const int64_t i = e / L, k = e % L;
-      double s = 0.0;
-      for (int64_t t = i; t <= k; ++t) s = s + P.Rf[i * L + t] * P.Ra[t * L + k];
-      P.R2[e] = (k >= i) ? s : 0.0;
+  for (int i = ty; i < L; i += 16)
+    for (int k = tx; k < L; k += 16) {
+      const int e = i * L + k;
+      P.Rf[e] = (k >= i) ? g[e] : 0.0;
+      P.Ri[e] = (k > i) ? g[k * L + i] : ((k == i) ? di[i] : 0.0);
+      if (save) P.Ra[e] = (k >= i) ? g[e] : 0.0;
     }
+  if (accum) {
+    // R2 = Rf * Ra  (both upper; Rf read from LDS, Ra saved by an earlier launch)
+    const double* __restrict__ Ra = P.Ra;
+    double* __restrict__ R2 = P.R2;
+    for (int i = ty; i < L; i += 16)
+      for (int k = tx; k < L; k += 16) {
+        double s = 0.0;
+#pragma unroll 8
+        for (int t = i; t <= k; ++t) s = s + g[i * L + t] * Ra[t * L + k];
+        R2[i * L + k] = (k >= i) ? s : 0.0;
+      }
   }
   if (threadIdx.x == 0 && !(g[0] > 0.0)) flag_status(status, kStatusInternal);
 }
 
-// X[dst] = X[src] * Ri (tall factor times the inverse factor), rows split over blocks.
-template <int T>
-__global__ void __launch_bounds__(256) k_apply_ri(const Prob* __restrict__ probs, int which, int src, int dst) {
-  __shared__ double ri[16 * T][16 * T + 1];
+// Y = X Ri (tall factor times the upper-triangular inverse factor), X and Y row-major M x L.
+// Ri sits in LDS; each wave takes 16 rows per 64-row chunk, its A fragments straight from X
+// (the next chunk's in flight), and the triangle is skipped at 16-column granularity.  Lane ln
+// feeds row 4(ln % 4) + ln / 4 of the wave's 16, so that result register v of lane (ln, g),
+// D row g + 4v, is row 4g + v: four consecutive rows per lane.  With
+// `split`, the rows are also written as the bf16 hi/lo parts of the next product's operand
+// (L columns of ldb, rows past M zero up to the next multiple of 64).
+template <int NB>
+__global__ void __launch_bounds__(256) k_apply_mf(const Prob* __restrict__ probs, int which, int src, int dst,
+                                                  int split) {
+  constexpr int L = 16 * NB;
+  __shared__ double ri[L][L + 1];
   const Prob& P = probs[blockIdx.y];
   const int64_t M = which ? P.C : P.R;
   const double* X = which ? P.Z[src] : P.X[src];
   double* Y = which ? P.Z[dst] : P.X[dst];
-  const int64_t L = P.L;
-  for (int64_t e = threadIdx.x; e < L * L; e += blockDim.x) ri[e / L][e % L] = P.Ri[e];
+  for (int e = threadIdx.x; e < L * L; e += blockDim.x) ri[e / L][e % L] = P.Ri[e];
   __syncthreads();
-  // each thread: one row, all L outputs in chunks
-  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < M; r += (int64_t)gridDim.x * blockDim.x) {
-    const double* xr = X + r * L;
-    double* yr = Y + r * L;
-    for (int64_t c0 = 0; c0 < L; c0 += 16) {
-      double acc[16] = {};
-      for (int64_t k = 0; k <= min<int64_t>(L - 1, c0 + 15); ++k) {
-        const double xv = xr[k];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
+  const int64_t nchunks = (M + 63) / 64;
+  double xa[4 * NB];
+  const int lrow = 4 * (ln & 3) + (ln >> 2);
+  auto load = [&](int64_t chunk, double (&x)[4 * NB]) {
+    const int64_t r = chunk * 64 + 16 * w + lrow;
+    const bool ok = chunk < nchunks && r < M;
 #pragma unroll
-        for (int u = 0; u < 16; ++u) acc[u] = acc[u] + xv * ri[k][c0 + u];
+    for (int s = 0; s < 4 * NB; ++s) x[s] = ok ? X[r * L + 4 * s + g] : 0.0;
+  };
+  int64_t chunk = blockIdx.x;
+  load(chunk, xa);
+  for (; chunk < nchunks; chunk += gridDim.x) {
+    // keeps the Ri fragments in LDS (read per chunk) instead of hoisted into registers
+    asm volatile("" ::: "memory");
+    const int64_t rn = (chunk + gridDim.x) * 64 + 16 * w + lrow;
+    const bool nok = chunk + gridDim.x < nchunks && rn < M;
+    f64x4_t acc[NB];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) acc[cb] = f64x4_t{0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int s = 0; s < 4 * NB; ++s) {
+      const double a = xa[s];
+      xa[s] = nok ? X[rn * L + 4 * s + g] : 0.0;      // the next chunk's fragment, one chunk ahead
+#pragma unroll
+      for (int cb = s / 4; cb < NB; ++cb) acc[cb] = mfma64(a, ri[4 * s + g][16 * cb + ln], acc[cb]);
+    }
+    const int64_t row0 = chunk * 64 + 16 * w + 4 * g;
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        if (row0 + v < M) Y[(row0 + v) * L + 16 * cb + ln] = acc[cb][v];
+      if (split) {
+        uint16_t h[4], l[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float f = (float)acc[cb][v];
+          h[v] = bf16_rne_f32(f);
+          l[v] = bf16_rne_f32(f - f32_of_bf16(h[v]));
+        }
+        const int64_t o = (int64_t)(16 * cb + ln) * P.ldb + row0;
+        *(uint2*)(P.bh + o) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
+        *(uint2*)(P.bl + o) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
       }
-#pragma unroll
-      for (int u = 0; u < 16; ++u)
-        if (c0 + u < L) yr[c0 + u] = acc[u];
     }
   }
+}
+
+// Sum over the 16 lanes of a DPP row (xor 1, xor 2, then the half-row and row mirrors pair
+// the quads and the halves), the result in every lane of the row.
+__device__ __forceinline__ double row16_sum_f64(double x) {
+  auto step = [](double v, int ctrl) {
+    const uint64_t b = __double_as_longlong(v);
+    int lo = (int)(uint32_t)b, hi = (int)(uint32_t)(b >> 32);
+    switch (ctrl) {
+      case 0: lo = __builtin_amdgcn_mov_dpp(lo, 0xB1, 0xF, 0xF, false); hi = __builtin_amdgcn_mov_dpp(hi, 0xB1, 0xF, 0xF, false); break;
+      case 1: lo = __builtin_amdgcn_mov_dpp(lo, 0x4E, 0xF, 0xF, false); hi = __builtin_amdgcn_mov_dpp(hi, 0x4E, 0xF, 0xF, false); break;
+      case 2: lo = __builtin_amdgcn_mov_dpp(lo, 0x141, 0xF, 0xF, false); hi = __builtin_amdgcn_mov_dpp(hi, 0x141, 0xF, 0xF, false); break;
+      default: lo = __builtin_amdgcn_mov_dpp(lo, 0x140, 0xF, 0xF, false); hi = __builtin_amdgcn_mov_dpp(hi, 0x140, 0xF, 0xF, false); break;
+    }
+    return v + __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+  };
+  x = step(x, 0);
+  x = step(x, 1);
+  x = step(x, 2);
+  return step(x, 3);
+}
+
+// The one-sided Jacobi sweep of k_jacobi (same round-robin pairing, rotation and stopping rule)
+// with A (r x c) and V (c x c) held in LDS, for cores small enough to fit; one 16-lane row per
+// column pair, so a wave rotates four pairs at once.  A and V are written back at the end.
+constexpr size_t kJacobiLdsMax = 150 * 1024;
+__global__ void __launch_bounds__(kJacobiThreads) k_jacobi_lds(const JacobiJob* __restrict__ jobs, uint32_t* status) {
+  extern __shared__ double jsh[];
+  __shared__ int s_rot;
+  const JacobiJob J = jobs[blockIdx.x];
+  const int r = (int)J.r, c = (int)J.c;
+  double* A = jsh;
+  double* V = jsh + r * c;
+  const int sub = threadIdx.x & 15, grp = threadIdx.x >> 4, ngrp = blockDim.x >> 4;
+  for (int e = threadIdx.x; e < r * c; e += blockDim.x) A[e] = J.a[e];
+  for (int e = threadIdx.x; e < c * c; e += blockDim.x) V[e] = ((e % c) == (e / c)) ? 1.0 : 0.0;
+  __syncthreads();
+  const int cp = c + (c & 1);
+  const double tol = (double)r * 1.1102230246251565e-16;
+  bool converged = (c < 2);
+  for (int sweep = 0; sweep < kJacobiMaxSweeps && !converged; ++sweep) {
+    if (threadIdx.x == 0) s_rot = 0;
+    __syncthreads();
+    for (int round = 0; round < cp - 1; ++round) {
+      for (int pr = grp; pr < cp / 2; pr += ngrp) {
+        const int x = (pr == 0) ? 0 : 1 + (pr - 1 + round) % (cp - 1);
+        const int y = 1 + (cp - 2 - pr + round) % (cp - 1);
+        const bool live = x < c && y < c;
+        const int p = min(x, y), q = max(x, y);
+        double* ap = A + p * r;
+        double* aq = A + q * r;
+        double al = 0.0, be = 0.0, ga = 0.0;
+        if (live)
+          for (int t = sub; t < r; t += 16) {
+            const double u = ap[t], w = aq[t];
+            al += u * u;
+            be += w * w;
+            ga += u * w;
+          }
+        al = row16_sum_f64(al);
+        be = row16_sum_f64(be);
+        ga = row16_sum_f64(ga);
+        if (live && fabs(ga) > tol * sqrt(al * be) && ga != 0.0) {
+          const double zeta = (be - al) / (2.0 * ga);
+          const double t = ((zeta >= 0.0) ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
+          const double cs = 1.0 / sqrt(1.0 + t * t);
+          const double sn = cs * t;
+          for (int i = sub; i < r; i += 16) {
+            const double u = ap[i], w = aq[i];
+            ap[i] = cs * u - sn * w;
+            aq[i] = sn * u + cs * w;
+          }
+          double* vp = V + p * c;
+          double* vq = V + q * c;
+          for (int i = sub; i < c; i += 16) {
+            const double u = vp[i], w = vq[i];
+            vp[i] = cs * u - sn * w;
+            vq[i] = sn * u + cs * w;
+          }
+          if (sub == 0) s_rot = 1;
+        }
+      }
+      __syncthreads();
+    }
+    converged = (s_rot == 0);
+    __syncthreads();
+  }
+  for (int e = threadIdx.x; e < r * c; e += blockDim.x) J.a[e] = A[e];
+  for (int e = threadIdx.x; e < c * c; e += blockDim.x) J.v[e] = V[e];
+  if (!converged && threadIdx.x == 0) flag_status(status, kStatusInternal);
 }
 
 // Jacobi input: Ja = R2 read as column-major, i.e. R2^T.
@@ -710,14 +896,17 @@ __global__ void __launch_bounds__(256) k_mfma_recon(const Mat* __restrict__ mats
 
 // ---- per-matrix helpers, batched over the matrices of a chunk (grid.y / grid.x = matrix) ----------
 
-// G = sum of the Gram partials of one side for every matrix
+// G = sum of the Gram partials of one side for every matrix (the partials hold the tiles on
+// and above the diagonal; the lower triangle is mirrored)
 __global__ void k_sum_gram(const Mat* __restrict__ mats, int side) {
   const Mat& M = mats[blockIdx.y];
   const int64_t n = M.Kr * M.Kr;
   double* G = side ? M.GV : M.GU;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = e / M.Kr, j = e - i * M.Kr;
+    const int64_t src = (i > j) ? j * M.Kr + i : e;
     double acc = 0.0;
-    for (int z = 0; z < kSlabs; ++z) acc = acc + M.GUp[(int64_t)z * n + e];
+    for (int z = 0; z < kSlabs; ++z) acc = acc + M.GUp[(int64_t)z * n + src];
     G[e] = acc;
   }
 }
@@ -915,14 +1104,14 @@ void launch_tn(const Prob* d, int np, int64_t maxC, int out, bool lo, bool align
   else if (lo) k_sk_tn<NB, true><<<grid, 256, 0, s>>>(d, out, nbx);
   else k_sk_tn<NB, false><<<grid, 256, 0, s>>>(d, out, nbx);
 }
-template <int T>
+template <int NB>
 void launch_gram(const Prob* d, int np, int which, int cur, hipStream_t s) {
-  k_gram_slab<T><<<dim3(kSlabs, (unsigned)np), 256, 0, s>>>(d, which, cur);
+  k_gram_mf<NB><<<dim3(kSlabs, (unsigned)np), 256, 0, s>>>(d, which, cur);
 }
-template <int T>
-void launch_apply(const Prob* d, int np, int64_t maxM, int which, int src, int dst, hipStream_t s) {
-  k_apply_ri<T><<<dim3((unsigned)std::max<int64_t>(1, std::min<int64_t>((maxM + 255) / 256, 64)), (unsigned)np), 256,
-                  0, s>>>(d, which, src, dst);
+template <int NB>
+void launch_apply(const Prob* d, int np, int64_t maxM, int which, int src, int dst, int split, hipStream_t s) {
+  const unsigned gx = (unsigned)std::max<int64_t>(1, std::min<int64_t>((maxM + 63) / 64, 16));
+  k_apply_mf<NB><<<dim3(gx, (unsigned)np), 256, 0, s>>>(d, which, src, dst, split);
 }
 
 #define DISPATCH_NB(nb, F, ...)                 \
@@ -1039,9 +1228,9 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
         const int64_t v0 = std::min<int64_t>(M.C, z * perV), v1 = std::min<int64_t>(M.C, v0 + perV);
         // G_z = U[u0:u1]^T U[u0:u1]: A(i,k) = U(u0+k, i)
         gj[2].push_back(GemmJob{M.U + u0 * M.ldk, M.U + u0 * M.ldk, M.GUp + (int64_t)z * M.Kr * M.Kr, 1, M.ldk,
-                                M.ldk, 1, M.Kr, 1, M.Kr, M.Kr, u1 - u0, 1.0, 0.0});
+                                M.ldk, 1, M.Kr, 1, M.Kr, M.Kr, u1 - u0, 1.0, 0.0, 1});
         gj[3].push_back(GemmJob{M.V + v0 * M.ldk, M.V + v0 * M.ldk, M.GUp + (int64_t)z * M.Kr * M.Kr, 1, M.ldk,
-                                M.ldk, 1, M.Kr, 1, M.Kr, M.Kr, v1 - v0, 1.0, 0.0});
+                                M.ldk, 1, M.Kr, 1, M.Kr, M.Kr, v1 - v0, 1.0, 0.0, 1});
       }
       // Newton-Schulz on both sides: parity a uses (Y_a, Z_a) -> (Y_b, Z_b), b = 1 - a
       const int64_t n = M.Kr;
@@ -1090,13 +1279,14 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     }
     TS_TRY(hipMemcpyAsync(ws, host.data(), tb, hipMemcpyHostToDevice, s));
     const unsigned gx = grid_for(L * rup(maxM, 64));
-    auto cholqr = [&](int which, int& cur, int save_first, int accum_second, int passes) {
+    // split: the last pass also writes the bf16 hi/lo operand of the next product
+    auto cholqr = [&](int which, int& cur, int save_first, int accum_second, int passes, int split) {
       const int64_t mm = which ? maxC : maxR;
       for (int pass = 0; pass < passes; ++pass) {
         DISPATCH_NB(NB, launch_gram, d_prob, np, which, cur, s);
-        const size_t shb = sizeof(double) * L * L;
+        const size_t shb = sizeof(double) * (L * L + L);
         k_chol<<<np, 256, shb, s>>>(d_prob, (pass == 0) ? save_first : 0, (pass == 1) ? accum_second : 0, status);
-        DISPATCH_NB(NB, launch_apply, d_prob, np, mm, which, cur, 1 - cur, s);
+        DISPATCH_NB(NB, launch_apply, d_prob, np, mm, which, cur, 1 - cur, (pass == passes - 1) ? split : 0, s);
         cur = 1 - cur;
       }
     };
@@ -1110,21 +1300,20 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     // sigma_r, which the following QR and product absorb; the last product, whose values form
     // the result, takes both parts (relative 2^-17).
     DISPATCH_NB(NB, launch_nn, d_prob, np, maxR, cx, s);
-    cholqr(0, cx, 0, 0, 2);
+    cholqr(0, cx, 0, 0, 2, 1);
     for (int it = 0; it < kPowerIters; ++it) {
-      k_split<<<dim3(gx, np), 256, 0, s>>>(d_prob, 0, cx);
       DISPATCH_NB(NB, launch_tn, d_prob, np, maxC, cz, false, aligned, s);
-      cholqr(1, cz, 0, 0, 1);
-      k_split<<<dim3(gx, np), 256, 0, s>>>(d_prob, 1, cz);
+      cholqr(1, cz, 0, 0, 1, 1);
       DISPATCH_NB(NB, launch_nn, d_prob, np, maxR, cx, s);
-      cholqr(0, cx, 0, 0, 1);
+      cholqr(0, cx, 0, 0, 1, 1);
     }
     // 2. B^T = Delta^T Q, its QR (R2 accumulated), SVD of the L x L core R2^T
-    k_split<<<dim3(gx, np), 256, 0, s>>>(d_prob, 0, cx);
     DISPATCH_NB(NB, launch_tn, d_prob, np, maxC, cz, true, aligned, s);
-    cholqr(1, cz, 1, 1, 2);
+    cholqr(1, cz, 1, 1, 2, 0);
     k_core_load<<<np, 256, 0, s>>>(d_prob, d_jobs);
-    k_jacobi<<<np, kJacobiThreads, 0, s>>>(d_jobs, status);
+    const size_t jlds = sizeof(double) * 2 * (size_t)L * L;
+    if (jlds <= kJacobiLdsMax) k_jacobi_lds<<<np, kJacobiThreads, jlds, s>>>(d_jobs, status);
+    else k_jacobi<<<np, kJacobiThreads, 0, s>>>(d_jobs, status);
     k_svd_finalize<<<np, 1024, (sizeof(double) + sizeof(int)) * L, s>>>(d_jobs, d_ptrs, d_ptrs + np, d_ptrs + 2 * np);
     // U_i = Q Ut[:, :r], V_i = Q2 Vt[:, :r]: both factors end in buffer 0 (an even number of QR
     // passes: 2 + kPowerIters for X, kPowerIters + 2 for Z)
