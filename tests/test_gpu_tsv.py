@@ -71,7 +71,13 @@ def check(u, K, r, alpha, out, dh, ulp1=False):
         assert np.all(np.abs(have - ref_v) <= _ulp_bf16(mag))
 
 
-@pytest.mark.parametrize("R,C,K,r", [(512, 384, 4, 8), (256, 640, 3, 8), (300, 200, 2, 16), (1024, 512, 4, 16)])
+# (1024, 768, 4, 64): sketch width 96 as in the 7B workload; (250, 203) and (203, 250): rows not
+# 16-byte aligned (entry-wise delta loads, the generic transposed product); (777, 520): ragged row
+# blocks and k tail; (640, 512, 2, 80): sketch width 128 (the largest), whose Jacobi core does
+# not fit in LDS
+@pytest.mark.parametrize("R,C,K,r", [(512, 384, 4, 8), (256, 640, 3, 8), (300, 200, 2, 16), (1024, 512, 4, 16),
+                                     (1024, 768, 4, 64), (250, 203, 2, 8), (203, 250, 2, 8), (777, 520, 3, 16),
+                                     (640, 512, 2, 80)])
 def test_planted_shapes(R, C, K, r):
     rng = np.random.default_rng(R + C + K + r)
     base, ds = planted(rng, R, C, r, K)
