@@ -829,69 +829,141 @@ __global__ void k_split_rows(uint16_t* __restrict__ hi, uint16_t* __restrict__ l
   }
 }
 
+// bf16 nearest-even of w + s (w a bf16 value, s binary32), rounded once: the binary32 sum and
+// its exact error (TwoSum, Knuth) give w + s exactly as hi + lo; hi is replaced by its
+// round-to-odd neighbour when lo != 0 (24 >= 8 + 2 bits, so the following nearest-even rounding
+// to 8 bits is the correct rounding of w + s).
+__device__ __forceinline__ uint32_t bf16_of_sum(float w, float s) {
+  const float hi = w + s;
+  const float bb = hi - w;
+  const float lo = (w - (hi - bb)) + (s - bb);
+  uint32_t b = __float_as_uint(hi);
+  if (lo != 0.0f && (b & 1u) == 0u) b += ((__float_as_uint(lo) ^ b) >> 31) ? 0xFFFFFFFFu : 1u;
+  return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+}
+
 // out = round(W0 + alpha * A B^T), A = ah + al (R x ldk), B = bh + bl (C x ldk); three MFMA
-// products per step (hi*hi, hi*lo, lo*hi).  128 x 128 output tile per block: each wave owns
-// 32 rows; the 128 x 32 slice of B (both halves) is staged in LDS once per step.
-constexpr int kRecT = 128;
-__global__ void __launch_bounds__(256) k_mfma_recon(const Mat* __restrict__ mats) {
-  __shared__ uint4 bsh[2][kRecT][4];     // [half][column][k-group of 8]
-  const Mat& M = mats[blockIdx.z];
-  const int64_t m0 = (int64_t)blockIdx.x * kRecT, n0 = (int64_t)blockIdx.y * kRecT;
-  if (m0 >= M.R || n0 >= M.C) return;
+// products per step (hi*hi, hi*lo, lo*hi), binary32 accumulation.  128 x 128 output tile per
+// workgroup, four waves as 2 x 2 of 64 x 64 (4 x 4 MFMA tiles); both operands go through LDS
+// 32 k at a time, double-buffered, the next step's pieces loaded into registers while the
+// current step's MFMAs run.  The MFMA computes the transposed tile (B fragments as its A operand)
+// so that lane (ln, g) ends with four consecutive columns 4g..4g+3 of output row ln: W0 is read
+// (before the last step) and the result written 8 bytes at a time (entry by entry when
+// C % 4 != 0).  The update is W0 + fl32(alpha * acc) rounded once to bf16 (bf16_of_sum).
+//
+// The grid is one-dimensional, `tiles` slots per matrix.  Workgroups are renumbered so that each
+// XCD takes a contiguous range, and within a matrix the tiles go column by column down groups of
+// eight tile rows: the 64 tiles an XCD has in flight then share eight row panels of A and eight
+// of B (2 MB of operands), which its L2 holds, instead of streaming 256 KB per tile from HBM.
+constexpr int kRecT = 128, kRecK = 32, kRecKG = kRecK / 8, kRecGroup = 8;
+__global__ void __launch_bounds__(256) k_mfma_recon(const Mat* __restrict__ mats, int64_t tiles) {
+  __shared__ bf16x8_t ash[2][2][kRecT][kRecKG + 1];     // [buffer][hi, lo][row][k group]
+  __shared__ bf16x8_t bsh[2][2][kRecT][kRecKG + 1];
+  const int64_t lb = xcd_logical_block(blockIdx.x, gridDim.x);
+  const Mat& M = mats[lb / tiles];
+  const int64_t R = M.R, C = M.C, ldk = M.ldk;
+  const int64_t ntr = (R + kRecT - 1) / kRecT, ntc = (C + kRecT - 1) / kRecT;
+  const int64_t t = lb % tiles;
+  if (t >= ntr * ntc) return;
+  const int64_t grp = t / (kRecGroup * ntc), r0 = grp * kRecGroup, gm = min<int64_t>(kRecGroup, ntr - r0);
+  const int64_t loc = t - grp * kRecGroup * ntc;
+  const int64_t m0 = (r0 + loc % gm) * kRecT, n0 = (loc / gm) * kRecT;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
-  f32x4_t acc[2][8];
+  const int wm = w >> 1, wn = w & 1;
+  // staging: 2 operands x 2 halves x 128 rows x 4 k groups = 2048 pieces, eight per thread
+  bf16x8_t pq[8];
+  auto load = [&](int64_t k0) {
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-    for (int cb = 0; cb < 8; ++cb) acc[rb][cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  int64_t arow[2];
-#pragma unroll
-  for (int rb = 0; rb < 2; ++rb) arow[rb] = min(M.R - 1, m0 + 32 * w + 16 * rb + ln);
-  for (int64_t k0 = 0; k0 < M.ldk; k0 += 32) {
-    // stage B: 2 halves x 128 columns x 4 k-groups = 1024 16-byte pieces, four per thread
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int piece = threadIdx.x + 256 * q;
-      const int half = piece >> 9, col = (piece >> 2) & 127, kg = piece & 3;
-      const int64_t gc = min(M.C - 1, n0 + col);
-      const uint16_t* src = (half ? M.bl : M.bh) + gc * M.ldk + k0 + 8 * kg;
-      bsh[half][col][kg] = *(const uint4*)src;
+    for (int j = 0; j < 8; ++j) {
+      const int t = threadIdx.x + 256 * j;
+      const int op = t >> 10, h = (t >> 9) & 1, row = (t >> 2) & 127, kg = t & 3;
+      const uint16_t* base = op ? (h ? M.bl : M.bh) : (h ? M.al : M.ah);
+      const int64_t gr = op ? min(C - 1, n0 + row) : min(R - 1, m0 + row);
+      pq[j] = ld_bf16x8(base + gr * ldk + k0 + 8 * kg);
     }
-    __syncthreads();
-    const int64_t k = k0 + 8 * g;
-    bf16x8_t ah[2], al[2];
+  };
+  auto store = [&](int buf) {
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-      ah[rb] = ld_bf16x8(M.ah + arow[rb] * M.ldk + k);
-      al[rb] = ld_bf16x8(M.al + arow[rb] * M.ldk + k);
+    for (int j = 0; j < 8; ++j) {
+      const int t = threadIdx.x + 256 * j;
+      const int op = t >> 10, h = (t >> 9) & 1, row = (t >> 2) & 127, kg = t & 3;
+      if (op) bsh[buf][h][row][kg] = pq[j];
+      else ash[buf][h][row][kg] = pq[j];
+    }
+  };
+  f32x4_t acc[4][4];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int64_t steps = ldk / kRecK;
+  load(0);
+  store(0);
+  __syncthreads();
+  const bool vec = (C % 4) == 0;
+  uint2 wv[4][4];
+  for (int64_t s = 0; s < steps; ++s) {
+    const bool more = s + 1 < steps;
+    if (more) load((s + 1) * kRecK);
+    else if (vec) {
+      // the epilogue's W0 values, in flight during the last step's MFMAs
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+          const int64_t r = min(R - 1, m0 + 64 * wm + 16 * rb + ln), c0 = min(C - 4, n0 + 64 * wn + 16 * cb + 4 * g);
+          wv[rb][cb] = *(const uint2*)(M.w0 + r * C + c0);
+        }
+    }
+    const int buf = (int)(s & 1);
+    bf16x8_t ah[4], al[4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+      ah[rb] = ash[buf][0][64 * wm + 16 * rb + ln][g];
+      al[rb] = ash[buf][1][64 * wm + 16 * rb + ln][g];
     }
 #pragma unroll
-    for (int cb = 0; cb < 8; ++cb) {
-      const bf16x8_t bh = __builtin_bit_cast(bf16x8_t, bsh[0][cb * 16 + ln][g]);
-      const bf16x8_t bl = __builtin_bit_cast(bf16x8_t, bsh[1][cb * 16 + ln][g]);
+    for (int cb = 0; cb < 4; ++cb) {
+      const bf16x8_t bh = bsh[buf][0][64 * wn + 16 * cb + ln][g];
+      const bf16x8_t bl = bsh[buf][1][64 * wn + 16 * cb + ln][g];
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[rb], bh, acc[rb][cb], 0, 0, 0);
-        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[rb], bl, acc[rb][cb], 0, 0, 0);
-        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[rb], bh, acc[rb][cb], 0, 0, 0);
+      for (int rb = 0; rb < 4; ++rb) {
+        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh, ah[rb], acc[rb][cb], 0, 0, 0);
+        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bl, ah[rb], acc[rb][cb], 0, 0, 0);
+        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh, al[rb], acc[rb][cb], 0, 0, 0);
       }
     }
+    if (more) store(buf ^ 1);
     __syncthreads();
   }
+  const float alpha = (float)M.alpha;
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
+  for (int rb = 0; rb < 4; ++rb) {
+    const int64_t r = m0 + 64 * wm + 16 * rb + ln;
+    if (r >= R) continue;
 #pragma unroll
-    for (int cb = 0; cb < 8; ++cb)
+    for (int cb = 0; cb < 4; ++cb) {
+      const int64_t c0 = n0 + 64 * wn + 16 * cb + 4 * g;
+      if (c0 >= C) continue;
+      const int64_t idx = r * C + c0;
+      if (vec) {
+        const uint32_t wi[4] = {wv[rb][cb].x << 16, wv[rb][cb].x & 0xFFFF0000u, wv[rb][cb].y << 16,
+                                wv[rb][cb].y & 0xFFFF0000u};
+        uint32_t o[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t r = m0 + 32 * w + 16 * rb + 4 * g + e, c = n0 + cb * 16 + ln;
-        if (r < M.R && c < M.C) {
-          const int64_t idx = r * M.C + c;
-          const double v = (double)f32_of_bf16(M.w0[idx]) + M.alpha * (double)acc[rb][cb][e];
-          M.out[idx] = (uint16_t)f64_to_bf16_rne(v);
-          if (M.dhat) M.dhat[idx] = acc[rb][cb][e];
-        }
+        for (int e = 0; e < 4; ++e) o[e] = bf16_of_sum(__uint_as_float(wi[e]), alpha * acc[rb][cb][e]);
+        *(uint2*)(M.out + idx) = make_uint2(o[0] | (o[1] << 16), o[2] | (o[3] << 16));
+        if (M.dhat) *(float4*)(M.dhat + idx) = make_float4(acc[rb][cb][0], acc[rb][cb][1], acc[rb][cb][2], acc[rb][cb][3]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (c0 + e < C) {
+            M.out[idx + e] = (uint16_t)bf16_of_sum(f32_of_bf16(M.w0[idx + e]), alpha * acc[rb][cb][e]);
+            if (M.dhat) M.dhat[idx + e] = acc[rb][cb][e];
+          }
       }
+    }
+  }
 }
 
 // ---- per-matrix helpers, batched over the matrices of a chunk (grid.y / grid.x = matrix) ----------
@@ -1342,8 +1414,9 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     // 4. reconstruction with the update fused
     k_split_mats<<<dim3(grid_for(maxR * rup(Kr, 32)), (unsigned)nm), 256, 0, s>>>(d_mat, 0);
     k_split_mats<<<dim3(grid_for(maxC * rup(Kr, 32)), (unsigned)nm), 256, 0, s>>>(d_mat, 1);
-    k_mfma_recon<<<dim3((unsigned)((maxR + kRecT - 1) / kRecT), (unsigned)((maxC + kRecT - 1) / kRecT), (unsigned)nm),
-                   256, 0, s>>>(d_mat);
+    int64_t rtiles = 0;
+    for (int m = 0; m < nm; ++m) rtiles = std::max(rtiles, ((hm[m].R + kRecT - 1) / kRecT) * ((hm[m].C + kRecT - 1) / kRecT));
+    k_mfma_recon<<<(unsigned)(rtiles * nm), 256, 0, s>>>(d_mat, rtiles);
     TS_TRY(hipGetLastError());
     TS_TRY(hipStreamSynchronize(s));
   }
