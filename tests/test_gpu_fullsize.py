@@ -1,0 +1,117 @@
+"""Parity at the full workload sizes, in the launch configuration bench.py times.
+
+Each workload's whole stack is generated on the device by the seeded generator and merged by
+one iso_update call (FUSED, TIES, lambda 1, the selection inside the call: the single-read path
+for bf16, the two-pass path for fp32), as bench.py times it; iso_topk_mask is also run over the
+whole stack.  Every tensor's descriptors (the 545M-entry embeddings included) must satisfy what
+holds at any size: n_above + tie_quota = k, a cutoff inside the tensor, the threshold key at most
+the largest key.  Sampled tensors are then checked against the oracle: their base and K deltas
+are regenerated on the host, the oracle's TopKMask descriptors are computed over the whole delta
+(partial selection), the GPU descriptors must equal them, and the merged weights must equal the
+oracle's bit for bit -- on every coordinate for the Tiny and single-layer workloads, and for the
+1.5B and 7B stacks on a million random coordinates per tensor, a window around every delta's tie
+cutoff and the ragged tail.  The sampled tensors are one of each shape class (GQA k, attention
+square, MLP) small enough for the oracle's time budget.
+"""
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+
+from oracle import ties
+
+import paper_2607_19331_amd as iso
+import synth
+from tests.gpu_helpers import say
+
+pytestmark = pytest.mark.gpu
+
+# workload, sampled tensor indices, "all" (every coordinate) or "sample"
+CASES = [
+    ("tiny", [0], "all"),
+    ("layer", [1, 4, 6], "all"),
+    ("1.5b", [1, 3, 4, 6], "sample"),
+    ("7b", [1, 3, 4], "sample"),
+]
+
+
+def _stack(wl):
+    import torch
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream().cuda_stream
+    st = torch.int16 if wl.dtype == "bf16" else torch.int32
+    entries = []
+    for t, spec in enumerate(wl.tensors):
+        n = spec.numel
+        base = torch.empty(n, dtype=st, device=dev)
+        synth.fill_device(base.data_ptr(), n, wl, t, 0, stream)
+        ds = []
+        for i in range(wl.K):
+            d = torch.empty(n, dtype=st, device=dev)
+            synth.fill_device(d.data_ptr(), n, wl, t, 1 + i, stream)
+            ds.append(d)
+        out = torch.empty(n, dtype=st, device=dev)
+        k = iso.iso_k_from_density(n, wl.density.numerator, wl.density.denominator)
+        entries.append(iso.Entry(spec.rows, spec.cols, base=base, deltas=ds, out=out, k=k))
+    return entries
+
+
+def _sample_idx(rng, n, descs):
+    parts = [rng.integers(0, n, size=min(n, 1 << 20)), np.arange(max(0, n - 4096), n)]
+    for d in descs:
+        c = int(d[3])
+        parts.append(np.arange(max(0, c - 2048), min(n, c + 2048)))
+    return np.unique(np.concatenate(parts))
+
+
+@pytest.mark.parametrize("name,picks,how", CASES, ids=[c[0] for c in CASES])
+def test_full_workload(name, picks, how):
+    import torch
+    wl = synth.workload(name)
+    dt = iso.BF16 if wl.dtype == "bf16" else iso.F32
+    say(f"full-size {name}: {len(wl.tensors)} tensors, {wl.numel} params, K={wl.K}")
+    entries = _stack(wl)
+    ws = iso.workspace(iso.OP_UPDATE_FUSED_SELECT, entries, wl.K, dt)
+    iso.iso_update(entries, wl.K, dt, iso.UPDATE_FUSED, merge=iso.MERGE_TIES, lam=1.0, desc=None, ws=ws)
+    assert iso.iso_read_device_status(ws) == 0
+    if dt == iso.BF16:
+        say(f"full-size {name}: tensors sent to the two-pass path: {iso.iso_read_fallback_count(ws)}")
+    wsel = iso.workspace(iso.OP_TOPK, entries, wl.K, dt)
+    desc = iso.desc_tensor(len(entries) * wl.K)
+    iso.iso_topk_mask(entries, wl.K, dt, desc, ws=wsel)
+    assert iso.iso_read_device_status(wsel) == 0
+    gdesc = iso.decode_desc(desc)
+    del wsel
+    torch.cuda.synchronize()
+    for t, e in enumerate(entries):
+        for i in range(wl.K):
+            t_key, key_max, n_above, quota, cutoff = gdesc[t * wl.K + i]
+            assert n_above + quota == e.k and 0 <= quota, (t, i)
+            assert 0 <= cutoff <= wl.tensors[t].numel, (t, i)
+            assert e.k == 0 or t_key <= key_max, (t, i)
+    rng = np.random.default_rng(7)
+    sdt = "bf16" if wl.dtype == "bf16" else "f32"
+    for t in picks:
+        spec, e = wl.tensors[t], entries[t]
+        say(f"full-size {name}: {spec.name} {spec.rows}x{spec.cols}")
+        base = synth.fill_host(wl, t, 0)
+        ds = [synth.fill_host(wl, t, 1 + i) for i in range(wl.K)]
+        with ThreadPoolExecutor(wl.K) as ex:
+            want = list(ex.map(lambda d: ties.topk_descriptor(d, e.k, sdt), ds))
+        for i in range(wl.K):
+            g = gdesc[t * wl.K + i]
+            assert (g[0], g[2], g[3], g[4]) == want[i], (spec.name, i)
+        out = e.out.cpu().numpy()
+        out = out.view(np.uint16) if sdt == "bf16" else out.view(np.float32)
+        if how == "all":
+            masks = [ties.mask_from_descriptor(d, w, sdt) for d, w in zip(ds, want)]
+            ref = ties.merge_unit(base, ds, sdt, "ties", masks=masks)["out"]
+            assert np.array_equal(out, ref), spec.name
+        else:
+            idx = _sample_idx(rng, spec.numel, want)
+            r = ties.merge_at(base[idx], np.stack([d[idx] for d in ds]), "ties", descs=want, idx=idx, dtype=sdt)
+            bad = np.flatnonzero(out[idx] != r["out"])
+            assert bad.size == 0, (spec.name, idx[bad[:8]])
+        del base, ds, out
+    del entries
+    torch.cuda.empty_cache()
