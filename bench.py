@@ -73,12 +73,109 @@ def cpu_baseline():
             "sample": f"layers.0 {names} ({n} params, K=4, TIES density 0.1) in {dt:.1f} s; numpy, one thread"}
 
 
+def svd_flops(m, n):
+    """Golub & Van Loan's operation count for an SVD with both factors (m >= n):
+    4 m^2 n + 8 m n^2 + 9 n^3."""
+    m, n = max(m, n), min(m, n)
+    return 4 * m * m * n + 8 * m * n * n + 9 * n ** 3
+
+
+def bench_tiny(args, iso, synth, torch):
+    """Tiny (fp32 256x256, K = 3): per step, the TIES update (selection inside the call) and
+    ISO-Merger (Algorithm 1, iso_update SPECTRAL) on the same inputs, each timed with HIP
+    events on the current stream.  The roofline is that of the SPECTRAL call: binary64, its
+    algorithmic flops those of the K + 1 thin SVDs and the two polar SVDs it performs."""
+    from oracle import numerics as nm
+    from oracle import spectral as sp
+    wl = synth.workload("tiny")
+    spec = wl.tensors[0]
+    n, K = spec.numel, wl.K
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream().cuda_stream
+    base = torch.empty(n, dtype=torch.int32, device=dev)
+    synth.fill_device(base.data_ptr(), n, wl, 0, 0, stream)
+    ds = []
+    for i in range(K):
+        d = torch.empty(n, dtype=torch.int32, device=dev)
+        synth.fill_device(d.data_ptr(), n, wl, 0, 1 + i, stream)
+        ds.append(d)
+    out_t = torch.empty(n, dtype=torch.int32, device=dev)
+    out_s = torch.empty(n, dtype=torch.int32, device=dev)
+    k = iso.iso_k_from_density(n, wl.density.numerator, wl.density.denominator)
+    et = [iso.Entry(spec.rows, spec.cols, base=base, deltas=ds, out=out_t, k=k)]
+    es = [iso.Entry(spec.rows, spec.cols, base=base, deltas=ds, out=out_s, k=k)]
+    ws_t = iso.workspace(iso.OP_UPDATE_FUSED_SELECT, et, K, iso.F32, dev)
+    ws_s = iso.workspace(iso.OP_UPDATE_SPECTRAL, es, K, iso.F32, dev)
+
+    def step(ev=None):
+        if ev:
+            ev[0].record()
+        iso.iso_update(et, K, iso.F32, iso.UPDATE_FUSED, merge=iso.MERGE_TIES, lam=1.0, desc=None, ws=ws_t)
+        if ev:
+            ev[1].record()
+        iso.iso_update(es, K, iso.F32, iso.UPDATE_SPECTRAL, ws=ws_s)
+        if ev:
+            ev[2].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    for w in (ws_t, ws_s):
+        if iso.iso_read_device_status(w) != 0:
+            raise RuntimeError("device status reports an error")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s_ in range(args.steps):
+        step(ev[s_])
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    ties_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
+    spec_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
+    m_, n_ = spec.rows, spec.cols
+    q = min(m_, n_)
+    flops = (K + 1) * svd_flops(m_, n_) + svd_flops(m_, q) + svd_flops(n_, q)
+    rec = {
+        "metric": "merged params/sec and achieved HBM GB/s (% of peak), 7B-shaped K=4 merge",
+        "value": n / (ms_per_step * 1e-3),
+        "unit": "params/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": f"Tiny: one fp32 {m_}x{n_} base, K={K} deltas (nonzero prob 0.3), TIES density "
+                               f"{float(wl.density)}: TIES update and ISO-Merger (Algorithm 1) per step"},
+        "ties_ms": ties_ms,
+        "spectral_ms": spec_ms,
+        "roofline": {"bound": "fp64", "kernel": "iso_update SPECTRAL (Algorithm 1: Jacobi SVDs, dense binary64 steps)",
+                     "achieved": flops / (spec_ms * 1e-3) / 1e12, "peak": 78.6, "unit": "TFLOP/s",
+                     "frac": flops / (spec_ms * 1e-3) / 1e12 / 78.6, "traffic": None,
+                     "flops_per_call": flops},
+    }
+    if not args.no_cpu_baseline:
+        w0 = nm.to_f64(synth.fill_host(wl, 0, 0), "f32").reshape(m_, n_)
+        dh = [nm.to_f64(synth.fill_host(wl, 0, 1 + i), "f32").reshape(m_, n_) for i in range(K)]
+        reps, t1 = 0, time.perf_counter()
+        while reps < 3 or time.perf_counter() - t1 < 10.0:
+            sp.iso_merge(w0, dh)
+            reps += 1
+        dt = (time.perf_counter() - t1) / reps
+        try:
+            from threadpoolctl import threadpool_info
+            cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        except ImportError:
+            cores = len(os.sched_getaffinity(0))
+        rec["cpu_baseline"] = {"value": n / dt, "unit": "params/s", "cores": cores,
+                               "kind": "oracle",
+                               "sample": f"Algorithm 1 (LAPACK SVDs, numpy) on the whole Tiny matrix, {reps} runs, "
+                                         f"{dt * 1e3:.1f} ms each"}
+    return rec
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="7b", choices=["layer", "1.5b", "7b", "7b-tsv"])
+    ap.add_argument("--config", default="7b", choices=["tiny", "layer", "1.5b", "7b", "7b-tsv"])
     ap.add_argument("--path", default="single-read", choices=["single-read", "two-pass"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -105,6 +202,10 @@ def main():
 
     import paper_2607_19331_amd as iso
     import synth
+
+    if args.config == "tiny":
+        print(json.dumps(bench_tiny(args, iso, synth, torch)), flush=True)
+        return
 
     wl = synth.workload(args.config)
     dev = torch.device("cuda:0")

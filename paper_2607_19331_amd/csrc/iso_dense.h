@@ -4,6 +4,7 @@
 #pragma once
 
 #include <algorithm>
+#include <vector>
 
 #include "iso_device.h"
 
@@ -14,6 +15,128 @@ constexpr int kJacobiThreads = 1024;
 constexpr int kJacobiMaxSweeps = 60;
 
 // ---- one-sided Jacobi SVD ------------------------------------------------------------------------
+
+__device__ __forceinline__ double wave_sum_f64(double x) {
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+// Sum over the 16 lanes of a DPP row (xor 1, xor 2, then the half-row and row mirrors pair
+// the quads and the halves), the result in every lane of the row.
+__device__ __forceinline__ double row16_sum_f64(double x) {
+  auto step = [](double v, int ctrl) {
+    const uint64_t b = __double_as_longlong(v);
+    int lo = (int)(uint32_t)b, hi = (int)(uint32_t)(b >> 32);
+    switch (ctrl) {
+      case 0: lo = __builtin_amdgcn_mov_dpp(lo, 0xB1, 0xF, 0xF, false); hi = __builtin_amdgcn_mov_dpp(hi, 0xB1, 0xF, 0xF, false); break;
+      case 1: lo = __builtin_amdgcn_mov_dpp(lo, 0x4E, 0xF, 0xF, false); hi = __builtin_amdgcn_mov_dpp(hi, 0x4E, 0xF, 0xF, false); break;
+      case 2: lo = __builtin_amdgcn_mov_dpp(lo, 0x141, 0xF, 0xF, false); hi = __builtin_amdgcn_mov_dpp(hi, 0x141, 0xF, 0xF, false); break;
+      default: lo = __builtin_amdgcn_mov_dpp(lo, 0x140, 0xF, 0xF, false); hi = __builtin_amdgcn_mov_dpp(hi, 0x140, 0xF, 0xF, false); break;
+    }
+    return v + __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+  };
+  x = step(x, 0);
+  x = step(x, 1);
+  x = step(x, 2);
+  return step(x, 3);
+}
+
+// Rotation of the column pair (p, q) of A (r rows) and V (c rows) by one 16-lane row of the
+// workgroup.  RT > 0: the lane keeps its RT entries of each A column in registers between the
+// dot products and the rotation (r <= 16 RT); RT = 0: two passes over memory.
+template <int RT>
+__device__ __forceinline__ bool jacobi_pair(double* A, double* V, int r, int c, int p, int q, int sub, double tol) {
+  double* ap = A + (int64_t)p * r;
+  double* aq = A + (int64_t)q * r;
+  double al = 0.0, be = 0.0, ga = 0.0;
+  double xu[RT > 0 ? RT : 1], xw[RT > 0 ? RT : 1];
+  if constexpr (RT > 0) {
+#pragma unroll
+    for (int e = 0; e < RT; ++e) {
+      const int t = sub + 16 * e;
+      xu[e] = (t < r) ? ap[t] : 0.0;
+      xw[e] = (t < r) ? aq[t] : 0.0;
+    }
+#pragma unroll
+    for (int e = 0; e < RT; ++e) {
+      al += xu[e] * xu[e];
+      be += xw[e] * xw[e];
+      ga += xu[e] * xw[e];
+    }
+  } else {
+#pragma unroll 4
+    for (int t = sub; t < r; t += 16) {
+      const double u = ap[t], w = aq[t];
+      al += u * u;
+      be += w * w;
+      ga += u * w;
+    }
+  }
+  al = row16_sum_f64(al);
+  be = row16_sum_f64(be);
+  ga = row16_sum_f64(ga);
+  if (!(fabs(ga) > tol * sqrt(al * be) && ga != 0.0)) return false;
+  const double zeta = (be - al) / (2.0 * ga);
+  const double t = ((zeta >= 0.0) ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
+  const double cs = 1.0 / sqrt(1.0 + t * t);
+  const double sn = cs * t;
+  if constexpr (RT > 0) {
+#pragma unroll
+    for (int e = 0; e < RT; ++e) {
+      const int i = sub + 16 * e;
+      if (i < r) {
+        ap[i] = cs * xu[e] - sn * xw[e];
+        aq[i] = sn * xu[e] + cs * xw[e];
+      }
+    }
+  } else {
+#pragma unroll 4
+    for (int i = sub; i < r; i += 16) {
+      const double u = ap[i], w = aq[i];
+      ap[i] = cs * u - sn * w;
+      aq[i] = sn * u + cs * w;
+    }
+  }
+  double* vp = V + (int64_t)p * c;
+  double* vq = V + (int64_t)q * c;
+#pragma unroll 4
+  for (int i = sub; i < c; i += 16) {
+    const double u = vp[i], w = vq[i];
+    vp[i] = cs * u - sn * w;
+    vq[i] = sn * u + cs * w;
+  }
+  return true;
+}
+
+// One-sided Jacobi sweeps on A (r x c col-major, r >= c), rotations accumulated into V (c x c,
+// the identity on entry), until a sweep rotates nothing (relative tolerance r * u) or
+// kJacobiMaxSweeps.  Columns are paired round-robin (position 0 fixed, the others rotating; a
+// phantom column when c is odd); one 16-lane row of the workgroup per pair, so a wave rotates
+// four pairs at once.  Block-uniform result: converged.
+template <int RT>
+__device__ bool jacobi_sweeps(double* A, double* V, int r, int c, int* s_rot) {
+  const int sub = threadIdx.x & 15, grp = threadIdx.x >> 4, ngrp = blockDim.x >> 4;
+  const int cp = c + (c & 1);
+  const double tol = (double)r * 1.1102230246251565e-16;
+  bool converged = (c < 2);
+  for (int sweep = 0; sweep < kJacobiMaxSweeps && !converged; ++sweep) {
+    if (threadIdx.x == 0) *s_rot = 0;
+    __syncthreads();
+    for (int round = 0; round < cp - 1; ++round) {
+      for (int pr = grp; pr < cp / 2; pr += ngrp) {
+        const int x = (pr == 0) ? 0 : 1 + (pr - 1 + round) % (cp - 1);
+        const int y = 1 + (cp - 2 - pr + round) % (cp - 1);
+        if (x >= c || y >= c) continue;                    // the whole 16-lane row skips
+        if (jacobi_pair<RT>(A, V, r, c, min(x, y), max(x, y), sub, tol) && sub == 0) *s_rot = 1;
+      }
+      __syncthreads();
+    }
+    converged = (*s_rot == 0);
+    __syncthreads();
+  }
+  return converged;
+}
+
 // A: r x c col-major (r >= c), overwritten by A V = U Sigma; V: c x c col-major, written.
 struct JacobiJob {
   double* a;
@@ -21,71 +144,176 @@ struct JacobiJob {
   int64_t r, c;
 };
 
-__device__ __forceinline__ double wave_sum_f64(double x) {
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
-  return x;
-}
-
 __global__ void __launch_bounds__(kJacobiThreads) k_jacobi(const JacobiJob* __restrict__ jobs, uint32_t* status) {
   __shared__ int s_rot;
   const JacobiJob J = jobs[blockIdx.x];
-  const int64_t r = J.r, c = J.c;
-  double* A = J.a;
-  double* V = J.v;
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  for (int64_t e = threadIdx.x; e < c * c; e += blockDim.x) V[e] = ((e % c) == (e / c)) ? 1.0 : 0.0;
+  const int r = (int)J.r, c = (int)J.c;
+  for (int64_t e = threadIdx.x; e < (int64_t)c * c; e += blockDim.x) J.v[e] = ((e % c) == (e / c)) ? 1.0 : 0.0;
   __syncthreads();
-  const int64_t cp = c + (c & 1);          // even count: a phantom column pairs with nobody
-  const double tol = (double)r * 1.1102230246251565e-16;   // r * unit roundoff
-  bool converged = (c < 2);
-  for (int sweep = 0; sweep < kJacobiMaxSweeps && !converged; ++sweep) {
-    if (threadIdx.x == 0) s_rot = 0;
-    __syncthreads();
-    for (int64_t round = 0; round < cp - 1; ++round) {
-      // round-robin pairing: position 0 fixed, positions 1..cp-1 rotate
-      for (int64_t pr = wid; pr < cp / 2; pr += nw) {
-        int64_t x = (pr == 0) ? 0 : 1 + (pr - 1 + round) % (cp - 1);
-        int64_t y = 1 + (cp - 2 - pr + round) % (cp - 1);
-        if (x >= c || y >= c) continue;
-        int64_t p = min(x, y), q = max(x, y);
-        double* ap = A + p * r;
-        double* aq = A + q * r;
-        double al = 0.0, be = 0.0, ga = 0.0;
-        for (int64_t t = lane; t < r; t += 64) {
-          double u = ap[t], w = aq[t];
-          al += u * u;
-          be += w * w;
-          ga += u * w;
-        }
-        al = wave_sum_f64(al);
-        be = wave_sum_f64(be);
-        ga = wave_sum_f64(ga);
-        if (fabs(ga) > tol * sqrt(al * be) && ga != 0.0) {
-          const double zeta = (be - al) / (2.0 * ga);
-          const double t = ((zeta >= 0.0) ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
-          const double cs = 1.0 / sqrt(1.0 + t * t);
-          const double sn = cs * t;
-          for (int64_t i = lane; i < r; i += 64) {
-            double u = ap[i], w = aq[i];
-            ap[i] = cs * u - sn * w;
-            aq[i] = sn * u + cs * w;
-          }
-          double* vp = V + p * c;
-          double* vq = V + q * c;
-          for (int64_t i = lane; i < c; i += 64) {
-            double u = vp[i], w = vq[i];
-            vp[i] = cs * u - sn * w;
-            vq[i] = sn * u + cs * w;
-          }
-          if (lane == 0) s_rot = 1;
-        }
-      }
-      __syncthreads();
+  const bool converged = (r <= 256) ? jacobi_sweeps<16>(J.a, J.v, r, c, &s_rot) : jacobi_sweeps<0>(J.a, J.v, r, c, &s_rot);
+  if (!converged && threadIdx.x == 0) flag_status(status, kStatusInternal);
+}
+
+// ---- the same sweeps spread over many workgroups ---------------------------------------------------
+// The pairs of one round are independent, so each round is one launch over all jobs (16 pairs per
+// 256-thread workgroup): the kernel boundary is the barrier between rounds.  Per job, `rot` records
+// a rotation in the current sweep and `done` a sweep that rotated nothing; converged jobs' rounds
+// exit at once.  Same pairing, rotation and stopping rule as jacobi_sweeps.
+struct JacobiState {
+  int rot, done;
+};
+
+__global__ void k_jacobi_begin(const JacobiJob* __restrict__ jobs, JacobiState* __restrict__ st) {
+  const JacobiJob J = jobs[blockIdx.y];
+  const int64_t c = J.c, cc = c * c;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < cc; e += (int64_t)gridDim.x * blockDim.x)
+    J.v[e] = ((e % c) == (e / c)) ? 1.0 : 0.0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) st[blockIdx.y] = JacobiState{0, c < 2 ? 1 : 0};
+}
+
+__global__ void __launch_bounds__(256) k_jacobi_round(const JacobiJob* __restrict__ jobs, JacobiState* st, int round) {
+  const int job = blockIdx.y;
+  if (st[job].done) return;
+  const JacobiJob J = jobs[job];
+  const int r = (int)J.r, c = (int)J.c, cp = c + (c & 1);
+  if (round >= cp - 1) return;
+  const int sub = threadIdx.x & 15, pr = blockIdx.x * 16 + (threadIdx.x >> 4);
+  if (pr >= cp / 2) return;                            // whole 16-lane rows
+  const int x = (pr == 0) ? 0 : 1 + (pr - 1 + round) % (cp - 1);
+  const int y = 1 + (cp - 2 - pr + round) % (cp - 1);
+  if (x >= c || y >= c) return;
+  const double tol = (double)r * 1.1102230246251565e-16;
+  const bool rot = (r <= 256) ? jacobi_pair<16>(J.a, J.v, r, c, min(x, y), max(x, y), sub, tol)
+                              : jacobi_pair<0>(J.a, J.v, r, c, min(x, y), max(x, y), sub, tol);
+  if (rot && sub == 0) st[job].rot = 1;                // every writer stores 1
+}
+
+__global__ void k_jacobi_sweep_end(JacobiState* st, int njobs) {
+  for (int j = threadIdx.x; j < njobs; j += blockDim.x)
+    if (!st[j].done) {
+      if (st[j].rot == 0) st[j].done = 1;
+      st[j].rot = 0;
     }
-    converged = (s_rot == 0);
+}
+
+__global__ void k_jacobi_check(const JacobiState* st, int njobs, uint32_t* status) {
+  for (int j = threadIdx.x; j < njobs; j += blockDim.x)
+    if (!st[j].done) flag_status(status, kStatusInternal);
+}
+
+constexpr int kJacobiCheckSweeps = 4;   // sweeps queued between host checks of the done flags
+
+// Runs the Jacobi sweeps of njobs jobs (device table, max_c the largest column count).  The host
+// reads the done flags every kJacobiCheckSweeps sweeps and stops queueing once all are set, so
+// the call synchronises the stream a few times.
+inline hipError_t jacobi_multi(const JacobiJob* jobs, int njobs, int64_t max_c, JacobiState* st, uint32_t* status,
+                               hipStream_t s) {
+  const unsigned gb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_c * max_c + 255) / 256, 4096));
+  k_jacobi_begin<<<dim3(gb, (unsigned)njobs), 256, 0, s>>>(jobs, st);
+  const int cpm = (int)(max_c + (max_c & 1));
+  const dim3 g((unsigned)std::max(1, (cpm / 2 + 15) / 16), (unsigned)njobs);
+  std::vector<JacobiState> h(njobs);
+  for (int sweep = 0; sweep < kJacobiMaxSweeps;) {
+    for (int b = 0; b < kJacobiCheckSweeps && sweep < kJacobiMaxSweeps; ++b, ++sweep) {
+      for (int round = 0; round < cpm - 1; ++round) k_jacobi_round<<<g, 256, 0, s>>>(jobs, st, round);
+      k_jacobi_sweep_end<<<1, 256, 0, s>>>(st, njobs);
+    }
+    hipError_t e = hipMemcpyAsync(h.data(), st, sizeof(JacobiState) * njobs, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return e;
+    bool all = true;
+    for (int j = 0; j < njobs; ++j) all = all && h[j].done;
+    if (all) break;
+  }
+  k_jacobi_check<<<1, 256, 0, s>>>(st, njobs, status);
+  return hipGetLastError();
+}
+
+// ---- block one-sided Jacobi ------------------------------------------------------------------------
+// Columns in blocks of w (the last may be short; a phantom block when the count is odd), blocks
+// paired round-robin.  Per outer round, each workgroup takes one pair of blocks, stages their
+// (at most 2w) columns of A and V in LDS, runs one round-robin sweep over them (inner pairs, one
+// 16-lane row each) and writes them back; every column pair is checked at least once per outer
+// sweep, so a sweep that rotates nothing means the whole job has converged (same test as
+// jacobi_sweeps).  Far fewer launches than one per column round.
+__global__ void __launch_bounds__(256) k_bjacobi_round(const JacobiJob* __restrict__ jobs, JacobiState* st, int round,
+                                                       int w) {
+  extern __shared__ double bsh[];
+  __shared__ int s_rot;
+  const int job = blockIdx.y;
+  if (st[job].done) return;
+  const JacobiJob J = jobs[job];
+  const int r = (int)J.r, c = (int)J.c;
+  const int nb = (c + w - 1) / w, nbp = nb + (nb & 1);
+  if (round >= nbp - 1) return;
+  const int pr = blockIdx.x;
+  if (pr >= nbp / 2) return;
+  const int bx = (pr == 0) ? 0 : 1 + (pr - 1 + round) % (nbp - 1);
+  const int by = 1 + (nbp - 2 - pr + round) % (nbp - 1);
+  if (bx >= nb || by >= nb) return;
+  const int c0 = min(bx, by) * w, c1 = max(bx, by) * w;
+  const int n0 = min(w, c - c0), n1 = min(w, c - c1), nc = n0 + n1;
+  double* A = bsh;                                  // nc columns of r
+  double* V = bsh + (int64_t)2 * w * r;             // nc columns of c
+  auto gcol = [&](int l) { return (l < n0) ? c0 + l : c1 + (l - n0); };
+  for (int l = 0; l < nc; ++l) {
+    const int g = gcol(l);
+    for (int i = threadIdx.x; i < r; i += blockDim.x) A[(int64_t)l * r + i] = J.a[(int64_t)g * r + i];
+    for (int i = threadIdx.x; i < c; i += blockDim.x) V[(int64_t)l * c + i] = J.v[(int64_t)g * c + i];
+  }
+  if (threadIdx.x == 0) s_rot = 0;
+  __syncthreads();
+  const int sub = threadIdx.x & 15, grp = threadIdx.x >> 4, ngrp = blockDim.x >> 4;
+  const int cp = nc + (nc & 1);
+  const double tol = (double)r * 1.1102230246251565e-16;
+  for (int ir = 0; ir < cp - 1; ++ir) {
+    for (int q = grp; q < cp / 2; q += ngrp) {
+      const int x = (q == 0) ? 0 : 1 + (q - 1 + ir) % (cp - 1);
+      const int y = 1 + (cp - 2 - q + ir) % (cp - 1);
+      if (x >= nc || y >= nc) continue;
+      const bool rot = (r <= 256) ? jacobi_pair<16>(A, V, r, c, min(x, y), max(x, y), sub, tol)
+                                  : jacobi_pair<0>(A, V, r, c, min(x, y), max(x, y), sub, tol);
+      if (rot && sub == 0) s_rot = 1;
+    }
     __syncthreads();
   }
-  if (!converged && threadIdx.x == 0) flag_status(status, kStatusInternal);
+  for (int l = 0; l < nc; ++l) {
+    const int g = gcol(l);
+    for (int i = threadIdx.x; i < r; i += blockDim.x) J.a[(int64_t)g * r + i] = A[(int64_t)l * r + i];
+    for (int i = threadIdx.x; i < c; i += blockDim.x) J.v[(int64_t)g * c + i] = V[(int64_t)l * c + i];
+  }
+  if (threadIdx.x == 0 && s_rot) st[job].rot = 1;
+}
+
+constexpr size_t kBJacobiLds = 150 * 1024;
+
+// Block one-sided Jacobi over njobs jobs (max_r, max_c the largest row and column counts): the
+// block width is the largest that lets 2w columns of A and V fit the LDS budget (at most 16).
+// As jacobi_multi, the host checks the done flags every kJacobiCheckSweeps sweeps.
+inline hipError_t jacobi_block(const JacobiJob* jobs, int njobs, int64_t max_r, int64_t max_c, JacobiState* st,
+                               uint32_t* status, hipStream_t s) {
+  const int w = (int)std::min<int64_t>(16, (int64_t)(kBJacobiLds / (16 * (size_t)(max_r + max_c))));
+  if (w < 2) return jacobi_multi(jobs, njobs, max_c, st, status, s);
+  const size_t lds = sizeof(double) * 2 * (size_t)w * (size_t)(max_r + max_c);
+  const unsigned gb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_c * max_c + 255) / 256, 4096));
+  k_jacobi_begin<<<dim3(gb, (unsigned)njobs), 256, 0, s>>>(jobs, st);
+  const int nb = (int)((max_c + w - 1) / w), nbp = nb + (nb & 1);
+  const dim3 g((unsigned)std::max(1, nbp / 2), (unsigned)njobs);
+  std::vector<JacobiState> h(njobs);
+  for (int sweep = 0; sweep < kJacobiMaxSweeps;) {
+    for (int b = 0; b < kJacobiCheckSweeps && sweep < kJacobiMaxSweeps; ++b, ++sweep) {
+      for (int round = 0; round < nbp - 1; ++round) k_bjacobi_round<<<g, 256, lds, s>>>(jobs, st, round, w);
+      k_jacobi_sweep_end<<<1, 256, 0, s>>>(st, njobs);
+    }
+    hipError_t e = hipMemcpyAsync(h.data(), st, sizeof(JacobiState) * njobs, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return e;
+    bool all = true;
+    for (int j = 0; j < njobs; ++j) all = all && h[j].done;
+    if (all) break;
+  }
+  k_jacobi_check<<<1, 256, 0, s>>>(st, njobs, status);
+  return hipGetLastError();
 }
 
 // Sorted thin factors from a converged Jacobi job: left (r x c) = A's columns normalised,

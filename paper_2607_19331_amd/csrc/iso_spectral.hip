@@ -186,6 +186,7 @@ struct Bump {
 // Device blocks of one matrix; the same sequence of take() calls sizes the workspace.
 struct Bufs {
   JacobiJob* jobs;          // K+1 SVD jobs, then the two polar jobs
+  JacobiState* jst;         // K+3 convergence states
   double** ptrs;            // 3*(K+1) finalize outputs
   double *ja[ISO_MAX_K + 1], *jv[ISO_MAX_K + 1], *U[ISO_MAX_K + 1], *V[ISO_MAX_K + 1], *S[ISO_MAX_K + 1];
   double *XU, *XV, *P, *Sq, *FU, *FV, *G, *gram, *coef, *AU, *AV, *PA, *PV, *PL, *Wst;
@@ -196,6 +197,7 @@ Bufs carve(uint8_t* base, int64_t m, int64_t n, int K, size_t* used) {
   Bump bp{base};
   Bufs b;
   b.jobs = bp.take<JacobiJob>(K + 3);
+  b.jst = bp.take<JacobiState>(K + 3);
   b.ptrs = bp.take<double*>(3 * (K + 1));
   for (int i = 0; i <= K; ++i) {
     b.ja[i] = bp.take(r * q);
@@ -232,12 +234,15 @@ void tangent_project(double* d, const double* u0, int64_t r, int64_t q, double* 
 
 // X <- polar(X) = P Q^T for X (r x q col-major, r >= q).  Jacobi gives X Q = P diag(s);
 // P Q^T does not depend on the column order, so no sort is needed.
-void polar(double* X, int64_t r, int64_t q, const Bufs& b, const JacobiJob* job_dev, uint32_t* status, hipStream_t s) {
+hipError_t polar(double* X, int64_t r, int64_t q, const Bufs& b, const JacobiJob* job_dev, uint32_t* status,
+                 hipStream_t s) {
   k_copy<<<grid_for(r * q), 256, 0, s>>>(b.PA, X, r * q);
-  k_jacobi<<<1, kJacobiThreads, 0, s>>>(job_dev, status);
+  const hipError_t e = jacobi_block(job_dev, 1, r, q, b.jst, status, s);
+  if (e != hipSuccess) return e;
   k_normalize_cols<<<(unsigned)std::max<int64_t>(1, std::min<int64_t>((q + 15) / 16, 1024)), 1024, 0, s>>>(b.PL, b.PA, r,
                                                                                                         q);
   gemm(r, q, q, 1.0, b.PL, 1, r, b.PV, q, 1, 0.0, X, 1, r, s);     // X = P Q^T
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -285,7 +290,7 @@ iso_status run_spectral(const iso_tensor* t, int n_t, int K, iso_dtype dt, const
     for (int i = 0; i <= K; ++i)
       k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.ja[i], t[jt].base, i ? t[jt].deltas[i - 1] : nullptr, m, n,
                                                   wide ? 1 : 0, dt);
-    k_jacobi<<<K + 1, kJacobiThreads, 0, s>>>(b.jobs, status);
+    SP_TRY(jacobi_block(b.jobs, K + 1, r, q, b.jst, status, s));
     k_svd_finalize<<<K + 1, 1024, (sizeof(double) + sizeof(int)) * q, s>>>(b.jobs, b.ptrs, b.ptrs + (K + 1),
                                                                           b.ptrs + 2 * (K + 1));
     const int64_t keep = std::min<int64_t>(q, (int64_t)std::floor(a.rho_keep * (double)q + 0.5));
@@ -319,8 +324,8 @@ iso_status run_spectral(const iso_tensor* t, int n_t, int K, iso_dtype dt, const
     tangent_project(b.AV, b.V[0], n, q, b.P, b.Sq, s);
     k_add<<<grid_for(m * q), 256, 0, s>>>(b.AU, b.AU, b.U[0], m * q);
     k_add<<<grid_for(n * q), 256, 0, s>>>(b.AV, b.AV, b.V[0], n * q);
-    polar(b.AU, m, q, b, b.jobs + (K + 1), status, s);
-    polar(b.AV, n, q, b, b.jobs + (K + 2), status, s);
+    SP_TRY(polar(b.AU, m, q, b, b.jobs + (K + 1), status, s));
+    SP_TRY(polar(b.AV, n, q, b, b.jobs + (K + 2), status, s));
     // 7. W_* = U_* Sigma_0 V_*^T
     k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, b.AU, b.S[0], m, q);
     gemm(m, n, q, 1.0, b.FU, 1, m, b.AV, n, 1, 0.0, b.Wst, 1, m, s);

@@ -702,29 +702,8 @@ __global__ void __launch_bounds__(256) k_apply_mf(const Prob* __restrict__ probs
   }
 }
 
-// Sum over the 16 lanes of a DPP row (xor 1, xor 2, then the half-row and row mirrors pair
-// the quads and the halves), the result in every lane of the row.
-__device__ __forceinline__ double row16_sum_f64(double x) {
-  auto step = [](double v, int ctrl) {
-    const uint64_t b = __double_as_longlong(v);
-    int lo = (int)(uint32_t)b, hi = (int)(uint32_t)(b >> 32);
-    switch (ctrl) {
-      case 0: lo = __builtin_amdgcn_mov_dpp(lo, 0xB1, 0xF, 0xF, false); hi = __builtin_amdgcn_mov_dpp(hi, 0xB1, 0xF, 0xF, false); break;
-      case 1: lo = __builtin_amdgcn_mov_dpp(lo, 0x4E, 0xF, 0xF, false); hi = __builtin_amdgcn_mov_dpp(hi, 0x4E, 0xF, 0xF, false); break;
-      case 2: lo = __builtin_amdgcn_mov_dpp(lo, 0x141, 0xF, 0xF, false); hi = __builtin_amdgcn_mov_dpp(hi, 0x141, 0xF, 0xF, false); break;
-      default: lo = __builtin_amdgcn_mov_dpp(lo, 0x140, 0xF, 0xF, false); hi = __builtin_amdgcn_mov_dpp(hi, 0x140, 0xF, 0xF, false); break;
-    }
-    return v + __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
-  };
-  x = step(x, 0);
-  x = step(x, 1);
-  x = step(x, 2);
-  return step(x, 3);
-}
-
-// The one-sided Jacobi sweep of k_jacobi (same round-robin pairing, rotation and stopping rule)
-// with A (r x c) and V (c x c) held in LDS, for cores small enough to fit; one 16-lane row per
-// column pair, so a wave rotates four pairs at once.  A and V are written back at the end.
+// The one-sided Jacobi sweeps of k_jacobi with A (r x c) and V (c x c) held in LDS, for cores
+// small enough to fit; A and V are written back at the end.
 constexpr size_t kJacobiLdsMax = 150 * 1024;
 __global__ void __launch_bounds__(kJacobiThreads) k_jacobi_lds(const JacobiJob* __restrict__ jobs, uint32_t* status) {
   extern __shared__ double jsh[];
@@ -733,60 +712,10 @@ __global__ void __launch_bounds__(kJacobiThreads) k_jacobi_lds(const JacobiJob* 
   const int r = (int)J.r, c = (int)J.c;
   double* A = jsh;
   double* V = jsh + r * c;
-  const int sub = threadIdx.x & 15, grp = threadIdx.x >> 4, ngrp = blockDim.x >> 4;
   for (int e = threadIdx.x; e < r * c; e += blockDim.x) A[e] = J.a[e];
   for (int e = threadIdx.x; e < c * c; e += blockDim.x) V[e] = ((e % c) == (e / c)) ? 1.0 : 0.0;
   __syncthreads();
-  const int cp = c + (c & 1);
-  const double tol = (double)r * 1.1102230246251565e-16;
-  bool converged = (c < 2);
-  for (int sweep = 0; sweep < kJacobiMaxSweeps && !converged; ++sweep) {
-    if (threadIdx.x == 0) s_rot = 0;
-    __syncthreads();
-    for (int round = 0; round < cp - 1; ++round) {
-      for (int pr = grp; pr < cp / 2; pr += ngrp) {
-        const int x = (pr == 0) ? 0 : 1 + (pr - 1 + round) % (cp - 1);
-        const int y = 1 + (cp - 2 - pr + round) % (cp - 1);
-        const bool live = x < c && y < c;
-        const int p = min(x, y), q = max(x, y);
-        double* ap = A + p * r;
-        double* aq = A + q * r;
-        double al = 0.0, be = 0.0, ga = 0.0;
-        if (live)
-          for (int t = sub; t < r; t += 16) {
-            const double u = ap[t], w = aq[t];
-            al += u * u;
-            be += w * w;
-            ga += u * w;
-          }
-        al = row16_sum_f64(al);
-        be = row16_sum_f64(be);
-        ga = row16_sum_f64(ga);
-        if (live && fabs(ga) > tol * sqrt(al * be) && ga != 0.0) {
-          const double zeta = (be - al) / (2.0 * ga);
-          const double t = ((zeta >= 0.0) ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
-          const double cs = 1.0 / sqrt(1.0 + t * t);
-          const double sn = cs * t;
-          for (int i = sub; i < r; i += 16) {
-            const double u = ap[i], w = aq[i];
-            ap[i] = cs * u - sn * w;
-            aq[i] = sn * u + cs * w;
-          }
-          double* vp = V + p * c;
-          double* vq = V + q * c;
-          for (int i = sub; i < c; i += 16) {
-            const double u = vp[i], w = vq[i];
-            vp[i] = cs * u - sn * w;
-            vq[i] = sn * u + cs * w;
-          }
-          if (sub == 0) s_rot = 1;
-        }
-      }
-      __syncthreads();
-    }
-    converged = (s_rot == 0);
-    __syncthreads();
-  }
+  const bool converged = (r <= 128) ? jacobi_sweeps<8>(A, V, r, c, &s_rot) : jacobi_sweeps<0>(A, V, r, c, &s_rot);
   for (int e = threadIdx.x; e < r * c; e += blockDim.x) J.a[e] = A[e];
   for (int e = threadIdx.x; e < c * c; e += blockDim.x) J.v[e] = V[e];
   if (!converged && threadIdx.x == 0) flag_status(status, kStatusInternal);
