@@ -140,3 +140,23 @@ def test_argument_errors():
         iso.iso_blockdiag_project(es, 2, iso.BF16, 40, 1.0, ws=iso.workspace(iso.OP_TOPK, es, 2, iso.BF16))
     with pytest.raises(iso.IsoError):
         iso.iso_blockdiag_project(es, 2, iso.F32, 4, 1.0, ws=iso.workspace(iso.OP_TOPK, es, 2, iso.BF16))
+
+
+def test_full_mlp_shape():
+    """The 7B MLP shape of the TSV workload (3584 x 18944, K = 4, rank 64), planted so that the
+    truncation is well posed; the same tolerance as the small shapes."""
+    rng = np.random.default_rng(31)
+    R, C, K, r = 3584, 18944, 4, 64
+    ds = []
+    for _ in range(K):
+        P, _ = np.linalg.qr(rng.standard_normal((R, r)))
+        Q, _ = np.linalg.qr(rng.standard_normal((C, r)))
+        d = (P * np.linspace(0.08, 0.04, r)) @ Q.T + 2e-7 * rng.standard_normal((R, C))
+        ds.append(nm.f64_to_bf16(d.ravel()))
+        del P, Q, d
+    base = nm.f64_to_bf16(rng.standard_normal(R * C) * 0.02)
+    u = Unit(R, C, base, ds, "bf16")
+    say("tsv full MLP shape 3584x18944 K=4 r=64")
+    outs, dhs, st = run_tsv([u], K, r)
+    assert st == 0
+    check(u, K, r, 1.0, outs[0], dhs[0])
