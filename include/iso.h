@@ -192,7 +192,7 @@ typedef struct iso_update_args {
 iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_update_args* a, void* ws,
                       size_t ws_bytes, void* stream);
 
-#define ISO_SPECTRAL_MAX_DIM 1024
+#define ISO_SPECTRAL_MAX_DIM 16384
 
 /*
  * iso_blockdiag_project -- TSV-Merge (App. F): each delta is truncated to its

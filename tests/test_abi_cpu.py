@@ -69,7 +69,7 @@ def test_host_validation_errors():
     a.mode = 9
     assert L.iso_update(iso._table(es), 1, 2, iso.BF16, ctypes.byref(a), FAKE * 16, 1 << 30, None) == 1
     a.mode, a.rho_keep, a.ridge, a.c_min, a.c_max = 2, 0.9, 1e-12, 0.0, 1.5
-    big = [entry(rows=2048, cols=2048, k=0)]
+    big = [entry(rows=16385, cols=64, k=0)]
     assert L.iso_update(iso._table(big), 1, 2, iso.BF16, ctypes.byref(a), FAKE * 16, 1 << 30, None) == \
         _lib.ERR_UNSUPPORTED
     a.rho_keep = 0.0

@@ -108,3 +108,22 @@ def test_keep_ratio_and_clip_range():
     ref = _ref(u, 3, "f32", rho_keep=0.5, c_min=0.2, c_max=0.9)
     assert _close(outs[0], "f32", ref["w_star"])
     assert np.allclose(coef[0], ref["c"], rtol=1e-9)
+
+
+@pytest.mark.parametrize("t_idx", [0, 4], ids=["q_proj_2048x2048", "gate_proj_2048x5632"])
+def test_single_layer_shapes(t_idx):
+    """Algorithm 1 at the single-layer workload's shapes (bf16, K = 2), from the seeded generator."""
+    import time
+    wl = synth.workload("layer")
+    spec = wl.tensors[t_idx]
+    base = synth.fill_host(wl, t_idx, 0)
+    ds = [synth.fill_host(wl, t_idx, 1 + i) for i in range(wl.K)]
+    u = Unit(spec.rows, spec.cols, base, ds, "bf16")
+    say(f"spectral layer {spec.name} {spec.rows}x{spec.cols} K={wl.K}")
+    t0 = time.perf_counter()
+    outs, coef, st = run_spectral([u], wl.K, "bf16")
+    say(f"spectral layer {spec.name}: {time.perf_counter() - t0:.2f} s on the GPU")
+    assert st == 0
+    ref = _ref(u, wl.K, "bf16")
+    assert _close(outs[0], "bf16", ref["w_star"])
+    assert np.allclose(coef[0], ref["c"], rtol=1e-9, atol=1e-12)
