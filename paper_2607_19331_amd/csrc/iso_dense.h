@@ -114,12 +114,12 @@ __device__ __forceinline__ bool jacobi_pair(double* A, double* V, int r, int c, 
 // phantom column when c is odd); one 16-lane row of the workgroup per pair, so a wave rotates
 // four pairs at once.  Block-uniform result: converged.
 template <int RT>
-__device__ bool jacobi_sweeps(double* A, double* V, int r, int c, int* s_rot) {
+__device__ bool jacobi_sweeps(double* A, double* V, int r, int c, int* s_rot, int max_sweeps = kJacobiMaxSweeps) {
   const int sub = threadIdx.x & 15, grp = threadIdx.x >> 4, ngrp = blockDim.x >> 4;
   const int cp = c + (c & 1);
   const double tol = (double)r * 1.1102230246251565e-16;
   bool converged = (c < 2);
-  for (int sweep = 0; sweep < kJacobiMaxSweeps && !converged; ++sweep) {
+  for (int sweep = 0; sweep < max_sweeps && !converged; ++sweep) {
     if (threadIdx.x == 0) *s_rot = 0;
     __syncthreads();
     for (int round = 0; round < cp - 1; ++round) {
@@ -285,6 +285,149 @@ __global__ void __launch_bounds__(256) k_bjacobi_round(const JacobiJob* __restri
   if (threadIdx.x == 0 && s_rot) st[job].rot = 1;
 }
 
+// ---- block Jacobi step through the pair's Gram matrix (long columns) --------------------------------
+// For columns too long to stage: the pair's (at most 64) columns stay in global memory.  Their
+// 64 x 64 Gram matrix is formed on v_mfma_f64_16x16x4_f64 (lane (ln, g) supplies A[ln][g] and
+// B[g][ln] and receives D[g + 4v][ln]) from 64-row chunks staged in LDS; if some column pair fails
+// the rotation test, one-sided Jacobi on the Gram itself gives a rotation Q towards its
+// eigenvectors (for a symmetric positive semidefinite matrix the right singular vectors are the
+// eigenvectors), and the columns of A and of V are multiplied by Q, chunk by chunk, again on MFMA
+// through LDS.
+typedef double jac_f64x4_t __attribute__((ext_vector_type(4)));
+constexpr int kGW = 32, kGN = 64, kGP = kGN + 1;
+// Sweeps of the inner Jacobi on a block pair's Gram matrix.  One sweep suffices: the block pair
+// comes round again in the next outer sweep, and the outer test (every scaled off-diagonal Gram
+// entry below tolerance) is what ends the iteration, so an inner solve run to convergence only
+// buys fewer outer sweeps at a higher price each (at 2048 x 2048 one inner sweep is 18% faster
+// end to end than full inner convergence, with identical merged weights).
+constexpr int kGramInnerSweeps = 1;
+
+// X[:, cols] <- X[:, cols] Q for nrows rows (X col-major with leading dimension ld); ch is a
+// kGN x kGP LDS chunk, q the kGN x kGN LDS rotation (col-major).
+__device__ __forceinline__ void gram_apply(double* X, int64_t ld, int nrows, const int* gc, int nc, double* ch,
+                                           const double* q) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
+  for (int k0 = 0; k0 < nrows; k0 += kGN) {
+    for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
+      const int l = e / kGN, i = e % kGN;
+      ch[l * kGP + i] = (l < nc && k0 + i < nrows) ? X[(int64_t)gc[l] * ld + k0 + i] : 0.0;
+    }
+    __syncthreads();
+    jac_f64x4_t acc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[t] = jac_f64x4_t{0.0, 0.0, 0.0, 0.0};
+#pragma unroll 4
+    for (int s = 0; s < kGN / 4; ++s) {
+      const double a = ch[(4 * s + g) * kGP + 16 * w + ln];          // chunk row 16w + ln, k = 4s + g
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, q[(16 * t + ln) * kGN + 4 * s + g], acc[t], 0, 0, 0);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) ch[(16 * t + ln) * kGP + 16 * w + g + 4 * v] = acc[t][v];
+    __syncthreads();
+    for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
+      const int l = e / kGN, i = e % kGN;
+      if (l < nc && k0 + i < nrows) X[(int64_t)gc[l] * ld + k0 + i] = ch[l * kGP + i];
+    }
+    __syncthreads();
+  }
+}
+
+__global__ void __launch_bounds__(256) k_bjacobi_gram(const JacobiJob* __restrict__ jobs, JacobiState* st, int round) {
+  __shared__ double G[kGN * kGN];          // Gram, col-major; then the Jacobi matrix
+  __shared__ double Q[kGN * kGN];          // rotations (col-major)
+  __shared__ double ch[kGN * kGP];         // row chunk [column][row]
+  __shared__ int gc[kGN];
+  __shared__ int s_need, s_rot;
+  const int job = blockIdx.y;
+  if (st[job].done) return;
+  const JacobiJob J = jobs[job];
+  const int r = (int)J.r, c = (int)J.c;
+  const int nb = (c + kGW - 1) / kGW, nbp = nb + (nb & 1);
+  if (round >= nbp - 1) return;
+  const int pr = blockIdx.x;
+  if (pr >= nbp / 2) return;
+  const int bx = (pr == 0) ? 0 : 1 + (pr - 1 + round) % (nbp - 1);
+  const int by = 1 + (nbp - 2 - pr + round) % (nbp - 1);
+  if (bx >= nb || by >= nb) return;
+  const int c0 = min(bx, by) * kGW, c1 = max(bx, by) * kGW;
+  const int n0 = min(kGW, c - c0), n1 = min(kGW, c - c1), nc = n0 + n1;
+  if (threadIdx.x < kGN) gc[threadIdx.x] = (threadIdx.x < n0) ? c0 + threadIdx.x : c1 + (threadIdx.x - n0);
+  if (threadIdx.x == 0) { s_need = 0; s_rot = 0; }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
+  // 1. Gram: wave w owns the tile row w (four 16 x 16 tiles)
+  jac_f64x4_t acc[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) acc[t] = jac_f64x4_t{0.0, 0.0, 0.0, 0.0};
+  __syncthreads();
+  for (int k0 = 0; k0 < r; k0 += kGN) {
+    for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
+      const int l = e / kGN, i = e % kGN;
+      ch[l * kGP + i] = (l < nc && k0 + i < r) ? J.a[(int64_t)gc[l] * r + k0 + i] : 0.0;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int s = 0; s < kGN / 4; ++s) {
+      const double a = ch[(16 * w + ln) * kGP + 4 * s + g];          // X^T[16w + ln][k]
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, ch[(16 * t + ln) * kGP + 4 * s + g], acc[t], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) G[(16 * t + ln) * kGN + 16 * w + g + 4 * v] = acc[t][v];   // G[i][j] at j*64+i
+  __syncthreads();
+  // 2. rotation test on every column pair (the test of jacobi_pair)
+  const double tol = (double)r * 1.1102230246251565e-16;
+  for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
+    const int i = e % kGN, j = e / kGN;
+    if (i < j && j < nc) {
+      const double gij = G[j * kGN + i];
+      if (fabs(gij) > tol * sqrt(G[i * kGN + i] * G[j * kGN + j]) && gij != 0.0) s_need = 1;
+    }
+  }
+  for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) Q[e] = ((e % kGN) == (e / kGN)) ? 1.0 : 0.0;
+  __syncthreads();
+  if (!s_need) return;
+  // 3. rotations that diagonalise G: one-sided Jacobi on G (its columns orthogonalised, one sweep),
+  //    accumulated into Q
+  jacobi_sweeps<4>(G, Q, kGN, kGN, &s_rot, kGramInnerSweeps);
+  // 4. A and V columns times Q
+  gram_apply(J.a, r, r, gc, nc, ch, Q);
+  gram_apply(J.v, c, c, gc, nc, ch, Q);
+  if (threadIdx.x == 0) st[job].rot = 1;
+}
+
+inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_c, JacobiState* st, uint32_t* status,
+                              hipStream_t s) {
+  const unsigned gb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_c * max_c + 255) / 256, 4096));
+  k_jacobi_begin<<<dim3(gb, (unsigned)njobs), 256, 0, s>>>(jobs, st);
+  const int nb = (int)((max_c + kGW - 1) / kGW), nbp = nb + (nb & 1);
+  const dim3 g((unsigned)std::max(1, nbp / 2), (unsigned)njobs);
+  std::vector<JacobiState> h(njobs);
+  for (int sweep = 0; sweep < kJacobiMaxSweeps;) {
+    for (int b = 0; b < kJacobiCheckSweeps && sweep < kJacobiMaxSweeps; ++b, ++sweep) {
+      for (int round = 0; round < nbp - 1; ++round) k_bjacobi_gram<<<g, 256, 0, s>>>(jobs, st, round);
+      k_jacobi_sweep_end<<<1, 256, 0, s>>>(st, njobs);
+    }
+    hipError_t e = hipMemcpyAsync(h.data(), st, sizeof(JacobiState) * njobs, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return e;
+    bool all = true;
+    for (int j = 0; j < njobs; ++j) all = all && h[j].done;
+    if (all) break;
+  }
+  k_jacobi_check<<<1, 256, 0, s>>>(st, njobs, status);
+  return hipGetLastError();
+}
+
 constexpr size_t kBJacobiLds = 150 * 1024;
 
 // Block one-sided Jacobi over njobs jobs (max_r, max_c the largest row and column counts): the
@@ -293,7 +436,7 @@ constexpr size_t kBJacobiLds = 150 * 1024;
 inline hipError_t jacobi_block(const JacobiJob* jobs, int njobs, int64_t max_r, int64_t max_c, JacobiState* st,
                                uint32_t* status, hipStream_t s) {
   const int w = (int)std::min<int64_t>(16, (int64_t)(kBJacobiLds / (16 * (size_t)(max_r + max_c))));
-  if (w < 2) return jacobi_multi(jobs, njobs, max_c, st, status, s);
+  if (w < 16) return jacobi_gram(jobs, njobs, max_c, st, status, s);
   const size_t lds = sizeof(double) * 2 * (size_t)w * (size_t)(max_r + max_c);
   const unsigned gb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_c * max_c + 255) / 256, 4096));
   k_jacobi_begin<<<dim3(gb, (unsigned)njobs), 256, 0, s>>>(jobs, st);
@@ -320,11 +463,9 @@ inline hipError_t jacobi_block(const JacobiJob* jobs, int njobs, int64_t max_r, 
 // right (c x c) = V, s (c), all permuted to nonincreasing s.  Zero columns give zero vectors.
 __global__ void __launch_bounds__(1024) k_svd_finalize(const JacobiJob* __restrict__ jobs, double* const* left,
                                                        double* const* right, double* const* sv) {
-  extern __shared__ double sh[];           // c norms + c ranks
+  extern __shared__ double nrm[];          // c column norms (8 c bytes: 128 KiB at c = 16384)
   const JacobiJob J = jobs[blockIdx.x];
   const int64_t r = J.r, c = J.c;
-  double* nrm = sh;
-  int* rank = (int*)(sh + c);
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
   for (int64_t j = wid; j < c; j += nw) {
     double s = 0.0;
@@ -333,18 +474,15 @@ __global__ void __launch_bounds__(1024) k_svd_finalize(const JacobiJob* __restri
     if (lane == 0) nrm[j] = sqrt(s);
   }
   __syncthreads();
-  for (int64_t j = threadIdx.x; j < c; j += blockDim.x) {
-    int rk = 0;
-    for (int64_t k = 0; k < c; ++k) rk += (nrm[k] > nrm[j]) || (nrm[k] == nrm[j] && k < j);
-    rank[j] = rk;
-  }
-  __syncthreads();
   double* L = left[blockIdx.x];
   double* R = right[blockIdx.x];
   double* S = sv[blockIdx.x];
   for (int64_t j = wid; j < c; j += nw) {
-    const int64_t d = rank[j];
+    // rank of column j: columns with a larger norm, or an equal norm and a smaller index
     const double s = nrm[j];
+    double cnt = 0.0;
+    for (int64_t k = lane; k < c; k += 64) cnt += ((nrm[k] > s) || (nrm[k] == s && k < j)) ? 1.0 : 0.0;
+    const int64_t d = (int64_t)wave_sum_f64(cnt);
     const double inv = (s > 0.0) ? 1.0 / s : 0.0;
     for (int64_t t = lane; t < r; t += 64) L[d * r + t] = J.a[j * r + t] * inv;
     for (int64_t t = lane; t < c; t += 64) R[d * c + t] = J.v[j * c + t];
@@ -472,7 +610,8 @@ namespace {
 // A batch of independent GEMMs in one launch: grid.z indexes the job; blocks outside a
 // job's M x N exit.  C(i,j) = alpha * sum_k A(i,k) B(k,j) + beta * C(i,j) with X(i,k) at
 // X[i*xs0 + k*xs1].  `upper`: only the tiles on or above the diagonal are computed (for a
-// symmetric product whose lower triangle the caller fills in).
+// symmetric product whose lower triangle the caller fills in).  `skip`: if set and *skip is
+// nonzero when the kernel runs, the job is left out (an iteration whose job has converged).
 struct GemmJob {
   const double* A;
   const double* B;
@@ -481,6 +620,7 @@ struct GemmJob {
   int64_t M, N, K;
   double alpha, beta;
   int upper;
+  const int* skip;
 };
 
 typedef double gemm_f64x4_t __attribute__((ext_vector_type(4)));
@@ -497,6 +637,7 @@ __global__ void __launch_bounds__(256) k_gemm_jobs(const GemmJob* __restrict__ j
   const GemmJob J = jobs[blockIdx.z];
   const int64_t i0 = (int64_t)blockIdx.x * GT, j0 = (int64_t)blockIdx.y * GT;
   if (i0 >= J.M || j0 >= J.N || (J.upper && i0 > j0)) return;
+  if (J.skip != nullptr && *J.skip != 0) return;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
   const int wm = w >> 1, wn = w & 1;
   const bool a_kfast = J.as1 == 1, b_kfast = J.bs0 == 1;

@@ -2,9 +2,8 @@
 // runs every SVD of ISO in FP64).  Per 2-D matrix W_0 (m x n, q = min(m, n)) and experts
 // W_i = W_0 + tau_i:
 //   1. thin SVDs of W_0 and every W_i: one-sided Jacobi (Hestenes 1958; Demmel & Veselic
-//      1992, "Jacobi's method is more accurate than QR"), one workgroup per matrix, columns
-//      paired in round-robin order, rotations accumulated into V; singular values sorted
-//      nonincreasing;
+//      1992, on its accuracy), by column blocks paired round-robin over many workgroups,
+//      rotations accumulated into V; singular values sorted nonincreasing;
 //   2. joint sign canonicalisation s_ik = sign(<u_0k, u_ik>), sign(0) = 1, on u and v;
 //   3. tangent projections xi = D - U_0 sym(U_0^T D) of D = U_i - U_0 (and V), then the
 //      trailing modes k > k_keep = round(rho_keep q) are zeroed;
@@ -14,8 +13,9 @@
 //   6. xi_* = Pi(sum_i c_i xi_i), U_* = polar(U_0 + xi_U*), V_* = polar(V_0 + xi_V*) with
 //      polar(X) = P Q^T from the SVD of X (one-sided Jacobi again);
 //   7. W_* = U_* Sigma_0 V_*^T, rounded once to the storage type.
-// Matrices are held column-major in the workspace; small dense products use a tiled
-// binary64 GEMM.  Sizes up to ISO_SPECTRAL_MAX_DIM per side.
+// Matrices are held column-major in the workspace; dense products use a tiled binary64 GEMM on
+// MFMA.  The matrices of one call go in batches whose SVDs (and then whose polar retractions)
+// run as one Jacobi job set.  Sizes up to ISO_SPECTRAL_MAX_DIM per side.
 #include <vector>
 
 #include "iso_dense.h"
@@ -170,6 +170,93 @@ __global__ void k_combine(double* __restrict__ out, const double* __restrict__ x
   }
 }
 
+// ---- polar retraction by Newton-Schulz ----------------------------------------------------------
+// polar(X) = P_X Q_X^T equals X (X^T X)^{-1/2} when X has full column rank, which the retraction
+// arguments have: U_0 + xi_U with xi_U tangent gives X^T X = I + xi^T xi (Sec. 4.2, App. E).
+// The iteration X <- X (3 I - X^T X) / 2 maps each singular value s to s (3 - s^2) / 2 and
+// converges quadratically to the polar factor for s in (0, sqrt 3); the first step scales X by
+// 1 / sqrt(c), c the largest absolute column sum of X^T X (at least its largest eigenvalue), so
+// that every s lies in (0, 1].  A job stops once max |X^T X - I| <= kNsTol, after one more step.
+struct NsJob {
+  double* g;        // q x q: X^T X, then the step matrix T in place
+  int64_t q;
+};
+
+struct NsState {
+  unsigned long long err;    // max |G - I| (bit pattern of a nonnegative double)
+  unsigned long long csum;   // max absolute column sum of G (likewise)
+  int done;                  // no further steps
+  int last;                  // the step being taken is the last
+  int steps;                 // steps taken: the result is in buffer (steps & 1)
+  int pad;
+};
+
+constexpr double kNsTol = 1e-10;
+constexpr int kNsMaxSteps = 48;
+constexpr int kNsCheckSteps = 4;   // steps queued between host reads of the done flags
+
+__global__ void k_ns_begin(NsState* st, int njobs) {
+  for (int j = threadIdx.x; j < njobs; j += blockDim.x) st[j] = NsState{0ull, 0ull, 0, 0, 0, 0};
+}
+
+__global__ void k_ns_reset(NsState* st, int njobs) {
+  for (int j = threadIdx.x; j < njobs; j += blockDim.x)
+    if (!st[j].done) {
+      st[j].err = 0ull;
+      st[j].csum = 0ull;
+    }
+}
+
+// one wave per column of G: its absolute sum and its largest deviation from the identity
+__global__ void __launch_bounds__(256) k_ns_stats(const NsJob* __restrict__ jobs, NsState* st) {
+  const int job = blockIdx.y;
+  if (st[job].done) return;
+  const NsJob J = jobs[job];
+  const int lane = threadIdx.x & 63, nw = blockDim.x >> 6;
+  for (int64_t j = (int64_t)blockIdx.x * nw + (threadIdx.x >> 6); j < J.q; j += (int64_t)gridDim.x * nw) {
+    double cs = 0.0, dev = 0.0;
+    for (int64_t i = lane; i < J.q; i += 64) {
+      const double v = J.g[j * J.q + i];
+      cs += fabs(v);
+      dev = fmax(dev, fabs(v - (i == j ? 1.0 : 0.0)));
+    }
+    cs = wave_sum_f64(cs);
+    for (int o = 32; o > 0; o >>= 1) dev = fmax(dev, __shfl_xor(dev, o, 64));
+    if (lane == 0) {
+      atomicMax(&st[job].csum, (unsigned long long)__double_as_longlong(cs));
+      atomicMax(&st[job].err, (unsigned long long)__double_as_longlong(dev));
+    }
+  }
+}
+
+// G <- T = (3 I - G / c) / (2 sqrt c), c the scale on the first step and 1 after it
+__global__ void k_ns_form(const NsJob* __restrict__ jobs, NsState* st) {
+  const int job = blockIdx.y;
+  if (st[job].done) return;
+  const NsJob J = jobs[job];
+  const double c = (st[job].steps == 0) ? __longlong_as_double((long long)st[job].csum) : 1.0;
+  const double ic = (c > 0.0) ? 1.0 / c : 1.0, is = sqrt(ic);
+  const int64_t n = J.q * J.q;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = e % J.q, j = e / J.q;
+    J.g[e] = ((i == j ? 3.0 : 0.0) - J.g[e] * ic) * (0.5 * is);
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) st[job].last = __longlong_as_double((long long)st[job].err) <= kNsTol;
+}
+
+__global__ void k_ns_check(const NsState* st, int njobs, uint32_t* status) {
+  for (int j = threadIdx.x; j < njobs; j += blockDim.x)
+    if (!st[j].done) flag_status(status, kStatusInternal);
+}
+
+__global__ void k_ns_step_end(NsState* st, int njobs) {
+  for (int j = threadIdx.x; j < njobs; j += blockDim.x)
+    if (!st[j].done) {
+      st[j].steps += 1;
+      if (st[j].last) st[j].done = 1;
+    }
+}
+
 // ---- host orchestration --------------------------------------------------------------------------
 
 struct Bump {
@@ -185,20 +272,15 @@ struct Bump {
 
 // Device blocks of one matrix; the same sequence of take() calls sizes the workspace.
 struct Bufs {
-  JacobiJob* jobs;          // K+1 SVD jobs, then the two polar jobs
-  JacobiState* jst;         // K+3 convergence states
-  double** ptrs;            // 3*(K+1) finalize outputs
   double *ja[ISO_MAX_K + 1], *jv[ISO_MAX_K + 1], *U[ISO_MAX_K + 1], *V[ISO_MAX_K + 1], *S[ISO_MAX_K + 1];
-  double *XU, *XV, *P, *Sq, *FU, *FV, *G, *gram, *coef, *AU, *AV, *PA, *PV, *PL, *Wst;
+  double *XU, *XV, *P, *Sq, *FU, *FV, *G, *gram, *coef, *AU, *AV, *Wst;
+  double *PX[2][2], *PG[2];   // polar of U_0 + xi_U (m x q) and of V_0 + xi_V (n x q): the two buffers
+                              // of the iterate X, the q x q Gram / step matrix
 };
 
-Bufs carve(uint8_t* base, int64_t m, int64_t n, int K, size_t* used) {
+Bufs carve(Bump& bp, int64_t m, int64_t n, int K) {
   const int64_t q = std::min(m, n), r = std::max(m, n);
-  Bump bp{base};
   Bufs b;
-  b.jobs = bp.take<JacobiJob>(K + 3);
-  b.jst = bp.take<JacobiState>(K + 3);
-  b.ptrs = bp.take<double*>(3 * (K + 1));
   for (int i = 0; i <= K; ++i) {
     b.ja[i] = bp.take(r * q);
     b.jv[i] = bp.take(q * q);
@@ -217,12 +299,75 @@ Bufs carve(uint8_t* base, int64_t m, int64_t n, int K, size_t* used) {
   b.coef = bp.take(K);
   b.AU = bp.take(m * q);
   b.AV = bp.take(n * q);
-  b.PA = bp.take(r * q);    // polar: Jacobi copy
-  b.PV = bp.take(q * q);    // polar: rotations
-  b.PL = bp.take(r * q);    // polar: normalised columns
+  for (int h = 0; h < 2; ++h) {
+    const int64_t rows = h ? n : m;
+    b.PX[h][0] = bp.take(rows * q);
+    b.PX[h][1] = bp.take(rows * q);
+    b.PG[h] = bp.take(q * q);
+  }
   b.Wst = bp.take(m * n);
-  if (used) *used = bp.off;
   return b;
+}
+
+// Job tables of a batch of nm matrices: K+1 SVD jobs per matrix with their convergence states
+// and 3 finalize pointer arrays; two polar jobs per matrix (U side, V side) with their states and
+// four GEMM tables (X^T X and X T for either buffer holding X).
+struct Tables {
+  JacobiJob* jobs;
+  JacobiState* jst;
+  double** ptrs;
+  NsJob* ns;
+  NsState* nst;
+  GemmJob* ngj[4];   // [2 p]: G = X_p^T X_p, [2 p + 1]: X_{1-p} = X_p T
+};
+
+Tables carve_tables(Bump& bp, int nm, int K) {
+  Tables tb;
+  tb.jobs = bp.take<JacobiJob>((int64_t)nm * (K + 1));
+  tb.jst = bp.take<JacobiState>((int64_t)nm * (K + 1));
+  tb.ptrs = bp.take<double*>((int64_t)3 * nm * (K + 1));
+  tb.ns = bp.take<NsJob>(2 * nm);
+  tb.nst = bp.take<NsState>(2 * nm);
+  for (int k = 0; k < 4; ++k) tb.ngj[k] = bp.take<GemmJob>(2 * nm);
+  return tb;
+}
+
+// Matrices of one call are merged in batches: consecutive nonempty matrices, at most
+// kSpectralBatch of them and at most kSpectralBatchBytes of workspace (a matrix larger than that
+// forms a batch of its own).  A batch runs its SVDs as one set of Jacobi jobs, so that a few
+// mid-sized matrices fill the chip together where each alone would occupy a fraction of it.
+constexpr int kSpectralBatch = 8;
+constexpr size_t kSpectralBatchBytes = size_t(32) << 30;
+
+size_t matrix_bytes(int64_t m, int64_t n, int K) {
+  Bump bp{nullptr};
+  carve(bp, m, n, K);
+  return bp.off;
+}
+
+size_t tables_bytes(int nm, int K) {
+  Bump bp{nullptr};
+  carve_tables(bp, nm, K);
+  return bp.off;
+}
+
+std::vector<std::vector<int>> spectral_batches(const iso_tensor* t, int n_t, int K) {
+  std::vector<std::vector<int>> out;
+  std::vector<int> cur;
+  size_t bytes = 0;
+  for (int j = 0; j < n_t; ++j) {
+    if (t[j].rows == 0 || t[j].cols == 0) continue;
+    const size_t mb = matrix_bytes(t[j].rows, t[j].cols, K);
+    if (!cur.empty() && ((int)cur.size() == kSpectralBatch || bytes + mb > kSpectralBatchBytes)) {
+      out.push_back(cur);
+      cur.clear();
+      bytes = 0;
+    }
+    cur.push_back(j);
+    bytes += mb;
+  }
+  if (!cur.empty()) out.push_back(cur);
+  return out;
 }
 
 // xi = D - U0 sym(U0^T D) in place on D (r x q col-major), using P, S (q x q) as scratch
@@ -232,110 +377,186 @@ void tangent_project(double* d, const double* u0, int64_t r, int64_t q, double* 
   gemm(r, q, q, -1.0, u0, 1, r, S, 1, q, 1.0, d, 1, r, s);          // D -= U0 S
 }
 
-// X <- polar(X) = P Q^T for X (r x q col-major, r >= q).  Jacobi gives X Q = P diag(s);
-// P Q^T does not depend on the column order, so no sort is needed.
-hipError_t polar(double* X, int64_t r, int64_t q, const Bufs& b, const JacobiJob* job_dev, uint32_t* status,
-                 hipStream_t s) {
-  k_copy<<<grid_for(r * q), 256, 0, s>>>(b.PA, X, r * q);
-  const hipError_t e = jacobi_block(job_dev, 1, r, q, b.jst, status, s);
-  if (e != hipSuccess) return e;
-  k_normalize_cols<<<(unsigned)std::max<int64_t>(1, std::min<int64_t>((q + 15) / 16, 1024)), 1024, 0, s>>>(b.PL, b.PA, r,
-                                                                                                        q);
-  gemm(r, q, q, 1.0, b.PL, 1, r, b.PV, q, 1, 0.0, X, 1, r, s);     // X = P Q^T
+// Steps 2 - 6 up to the polar inputs for one matrix whose K+1 SVDs are final: canonicalisation,
+// tangent projections, D_keep, effect proxies, Gram, ridge solve and clip, aggregate projection;
+// leaves U_0 + xi_U* in AU and V_0 + xi_V* in AV.
+void middle_steps(const Bufs& b, int64_t m, int64_t n, int K, const SpectralArgs& a, double* coef_out,
+                  uint32_t* status, hipStream_t s) {
+  const int64_t q = std::min(m, n);
+  const int64_t keep = std::min<int64_t>(q, (int64_t)std::floor(a.rho_keep * (double)q + 0.5));
+  for (int i = 1; i <= K; ++i) {
+    double* xu = b.XU + (int64_t)(i - 1) * m * q;
+    double* xv = b.XV + (int64_t)(i - 1) * n * q;
+    // 2. sign canonicalisation against the base
+    k_canonicalize<<<grid_for(q * 64), 256, 0, s>>>(b.U[0], b.U[i], b.V[i], m, n, q);
+    // 3. displacements, tangent projection, D_keep
+    k_sub<<<grid_for(m * q), 256, 0, s>>>(xu, b.U[i], b.U[0], m * q);
+    k_sub<<<grid_for(n * q), 256, 0, s>>>(xv, b.V[i], b.V[0], n * q);
+    tangent_project(xu, b.U[0], m, q, b.P, b.Sq, s);
+    tangent_project(xv, b.V[0], n, q, b.P, b.Sq, s);
+    k_mask_cols<<<grid_for(m * q), 256, 0, s>>>(xu, m, q, keep);
+    k_mask_cols<<<grid_for(n * q), 256, 0, s>>>(xv, n, q, keep);
+    // 4. g_i = xi_U Sigma_0 V_0^T + U_0 Sigma_0 xi_V^T  (m x n col-major)
+    double* g = b.G + (int64_t)(i - 1) * m * n;
+    k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, xu, b.S[0], m, q);
+    gemm(m, n, q, 1.0, b.FU, 1, m, b.V[0], n, 1, 0.0, g, 1, m, s);
+    k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, b.U[0], b.S[0], m, q);
+    gemm(m, n, q, 1.0, b.FU, 1, m, xv, n, 1, 1.0, g, 1, m, s);
+  }
+  // 5. Gram, ridge solve, clip
+  k_gram<<<K * (K + 1) / 2, 1024, 0, s>>>(b.G, m * n, K, b.gram);
+  k_solve<<<1, 64, 0, s>>>(b.gram, K, a.ridge, a.c_min, a.c_max, b.coef, coef_out, status);
+  // 6. aggregate, project, shift to the base factors
+  k_combine<<<grid_for(m * q), 256, 0, s>>>(b.AU, b.XU, b.coef, K, m * q);
+  k_combine<<<grid_for(n * q), 256, 0, s>>>(b.AV, b.XV, b.coef, K, n * q);
+  tangent_project(b.AU, b.U[0], m, q, b.P, b.Sq, s);
+  tangent_project(b.AV, b.V[0], n, q, b.P, b.Sq, s);
+  k_add<<<grid_for(m * q), 256, 0, s>>>(b.AU, b.AU, b.U[0], m * q);
+  k_add<<<grid_for(n * q), 256, 0, s>>>(b.AV, b.AV, b.V[0], n * q);
+}
+
+// Newton-Schulz polar over the batch's 2 nm jobs (X of job p in buffer 0 on entry); the host
+// reads the done flags every kNsCheckSteps steps.  On return hst holds every job's state.
+hipError_t polar_batch(const Tables& tb, int njobs, int64_t max_rows, int64_t max_q, std::vector<NsState>& hst,
+                       uint32_t* status, hipStream_t s) {
+  const unsigned tq = (unsigned)((max_q + GT - 1) / GT), tr = (unsigned)((max_rows + GT - 1) / GT);
+  const unsigned cb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_q + 3) / 4, 1024));
+  const unsigned fb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_q * max_q + 255) / 256, 2048));
+  k_ns_begin<<<1, 256, 0, s>>>(tb.nst, njobs);
+  hst.assign(njobs, NsState{});
+  for (int step = 0; step < kNsMaxSteps;) {
+    for (int b = 0; b < kNsCheckSteps && step < kNsMaxSteps; ++b, ++step) {
+      const int p = step & 1;
+      k_ns_reset<<<1, 256, 0, s>>>(tb.nst, njobs);
+      k_gemm_jobs<<<dim3(tq, tq, (unsigned)njobs), 256, 0, s>>>(tb.ngj[2 * p]);
+      k_ns_stats<<<dim3(cb, (unsigned)njobs), 256, 0, s>>>(tb.ns, tb.nst);
+      k_ns_form<<<dim3(fb, (unsigned)njobs), 256, 0, s>>>(tb.ns, tb.nst);
+      k_gemm_jobs<<<dim3(tr, tq, (unsigned)njobs), 256, 0, s>>>(tb.ngj[2 * p + 1]);
+      k_ns_step_end<<<1, 256, 0, s>>>(tb.nst, njobs);
+    }
+    hipError_t e = hipMemcpyAsync(hst.data(), tb.nst, sizeof(NsState) * njobs, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return e;
+    bool all = true;
+    for (int j = 0; j < njobs; ++j) all = all && hst[j].done;
+    if (all) return hipGetLastError();
+  }
+  k_ns_check<<<1, 256, 0, s>>>(tb.nst, njobs, status);
   return hipGetLastError();
+}
+
+// One batch: every SVD of its matrices as one Jacobi job set, the per-matrix middle steps, both
+// polar retractions of every matrix as one Newton-Schulz job set, then W_*.
+iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, iso_dtype dt, const SpectralArgs& a,
+                     uint8_t* ws, uint32_t* status, hipStream_t s, std::vector<uint8_t>& host) {
+#define SP_TRY(x)                                \
+  do {                                           \
+    if ((x) != hipSuccess) return ISO_ERR_HIP;   \
+  } while (0)
+  const int nm = (int)ids.size(), nsvd = nm * (K + 1), npol = 2 * nm;
+  Bump bp{ws};
+  const Tables tb = carve_tables(bp, nm, K);
+  const size_t tables_end = bp.off;
+  std::vector<Bufs> bs(nm);
+  for (int e = 0; e < nm; ++e) bs[e] = carve(bp, t[ids[e]].rows, t[ids[e]].cols, K);
+  // host image of the tables (same layout as on the device): the nm (K+1) SVDs (matrix e's job i
+  // at e (K+1) + i) with their finalize pointers (left, right, singular values); the polar jobs
+  // (matrix e's U side at 2 e, V side at 2 e + 1) with their GEMM tables
+  host.assign(tables_end, 0);
+  const auto at = [&](const void* dev) { return host.data() + ((const uint8_t*)dev - ws); };
+  JacobiJob* hj = (JacobiJob*)at(tb.jobs);
+  double** hp = (double**)at(tb.ptrs);
+  NsJob* hn = (NsJob*)at(tb.ns);
+  GemmJob* hg[4];
+  for (int k = 0; k < 4; ++k) hg[k] = (GemmJob*)at(tb.ngj[k]);
+  int64_t svd_r = 1, svd_c = 1;
+  for (int e = 0; e < nm; ++e) {
+    const int64_t m = t[ids[e]].rows, n = t[ids[e]].cols, q = std::min(m, n), r = std::max(m, n);
+    const bool wide = m < n;
+    const Bufs& b = bs[e];
+    for (int i = 0; i <= K; ++i) {
+      const int j = e * (K + 1) + i;
+      hj[j] = JacobiJob{b.ja[i], b.jv[i], r, q};
+      hp[j] = wide ? b.V[i] : b.U[i];                 // left factor of the Jacobi matrix
+      hp[nsvd + j] = wide ? b.U[i] : b.V[i];          // right factor
+      hp[2 * nsvd + j] = b.S[i];
+    }
+    for (int h = 0; h < 2; ++h) {
+      const int pj = 2 * e + h;
+      const int64_t rows = h ? n : m;
+      const int* skip = &tb.nst[pj].done;
+      hn[pj] = NsJob{b.PG[h], q};
+      for (int p = 0; p < 2; ++p) {
+        const double* X = b.PX[h][p];
+        double* Y = b.PX[h][1 - p];
+        // G = X^T X (q x q), X (rows x q) col-major
+        hg[2 * p][pj] = GemmJob{X, X, b.PG[h], rows, 1, 1, rows, 1, q, q, q, rows, 1.0, 0.0, 0, skip};
+        // Y = X T (rows x q)
+        hg[2 * p + 1][pj] = GemmJob{X, b.PG[h], Y, 1, rows, 1, q, 1, rows, rows, q, q, 1.0, 0.0, 0, skip};
+      }
+    }
+    svd_r = std::max(svd_r, r);
+    svd_c = std::max(svd_c, q);
+  }
+  SP_TRY(hipMemcpyAsync(ws, host.data(), tables_end, hipMemcpyHostToDevice, s));
+  // 1. W_0 and W_i = W_0 + tau_i as A = W (tall) or W^T (wide), r x q col-major; SVDs
+  for (int e = 0; e < nm; ++e) {
+    const iso_tensor& x = t[ids[e]];
+    for (int i = 0; i <= K; ++i)
+      k_load_f64<<<grid_for(x.rows * x.cols), 256, 0, s>>>(bs[e].ja[i], x.base, i ? x.deltas[i - 1] : nullptr, x.rows,
+                                                           x.cols, x.rows < x.cols ? 1 : 0, dt);
+  }
+  SP_TRY(jacobi_block(tb.jobs, nsvd, svd_r, svd_c, tb.jst, status, s));
+  k_svd_finalize<<<nsvd, 1024, sizeof(double) * svd_c, s>>>(tb.jobs, tb.ptrs, tb.ptrs + nsvd, tb.ptrs + 2 * nsvd);
+  // 2 - 6 per matrix; the polar arguments go to the first iterate buffers
+  for (int e = 0; e < nm; ++e) {
+    const int64_t m = t[ids[e]].rows, n = t[ids[e]].cols, q = std::min(m, n);
+    const Bufs& b = bs[e];
+    middle_steps(b, m, n, K, a, a.coef_out ? a.coef_out + (int64_t)ids[e] * K : nullptr, status, s);
+    k_copy<<<grid_for(m * q), 256, 0, s>>>(b.PX[0][0], b.AU, m * q);
+    k_copy<<<grid_for(n * q), 256, 0, s>>>(b.PX[1][0], b.AV, n * q);
+  }
+  // 6'. U_* = polar(U_0 + xi_U*), V_* = polar(V_0 + xi_V*)
+  std::vector<NsState> hst;
+  SP_TRY(polar_batch(tb, npol, svd_r, svd_c, hst, status, s));
+  for (int e = 0; e < nm; ++e) {
+    const iso_tensor& x = t[ids[e]];
+    const int64_t m = x.rows, n = x.cols, q = std::min(m, n);
+    const Bufs& b = bs[e];
+    const double* Us = b.PX[0][hst[2 * e].steps & 1];
+    const double* Vs = b.PX[1][hst[2 * e + 1].steps & 1];
+    // 7. W_* = U_* Sigma_0 V_*^T
+    k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, Us, b.S[0], m, q);
+    gemm(m, n, q, 1.0, b.FU, 1, m, Vs, n, 1, 0.0, b.Wst, 1, m, s);
+    k_store_w<<<grid_for(m * n), 256, 0, s>>>(x.out, b.Wst, m, n, dt, status);
+  }
+  SP_TRY(hipGetLastError());
+  // the next batch reuses the workspace and the host staging: let this one finish first
+  SP_TRY(hipStreamSynchronize(s));
+  return ISO_OK;
+#undef SP_TRY
 }
 
 }  // namespace
 
 size_t spectral_workspace_bytes(const iso_tensor* t, int n_t, int K) {
-  size_t b = 0;
-  for (int j = 0; j < n_t; ++j) {
-    size_t u = 0;
-    carve(nullptr, std::max<int64_t>(t[j].rows, 1), std::max<int64_t>(t[j].cols, 1), K, &u);
-    b = std::max(b, u);
+  size_t most = 0;
+  for (const auto& ids : spectral_batches(t, n_t, K)) {
+    size_t b = tables_bytes((int)ids.size(), K);
+    for (int j : ids) b += matrix_bytes(t[j].rows, t[j].cols, K);
+    most = std::max(most, b);
   }
-  return b;
+  return most;
 }
 
 iso_status run_spectral(const iso_tensor* t, int n_t, int K, iso_dtype dt, const SpectralArgs& a, uint8_t* ws,
                         uint32_t* status, hipStream_t s) {
-#define SP_TRY(x)                                \
-  do {                                           \
-    if ((x) != hipSuccess) return ISO_ERR_HIP;   \
-  } while (0)
-  // host staging for the job tables; kept until the stream has consumed them
-  std::vector<uint8_t> host;
-  for (int jt = 0; jt < n_t; ++jt) {
-    const int64_t m = t[jt].rows, n = t[jt].cols;
-    if (m == 0 || n == 0) continue;
-    const int64_t q = std::min(m, n), r = std::max(m, n);
-    const bool wide = m < n;
-    const Bufs b = carve(ws, m, n, K, nullptr);
-    // job table: K+1 SVDs, polar of U_0 + xi_U (m x q), polar of V_0 + xi_V (n x q); finalize pointers
-    const size_t jb = sizeof(JacobiJob) * (K + 3), pb = sizeof(double*) * 3 * (K + 1);
-    host.assign(jb + pb, 0);
-    JacobiJob* hj = (JacobiJob*)host.data();
-    double** hp = (double**)(host.data() + jb);
-    for (int i = 0; i <= K; ++i) {
-      hj[i] = JacobiJob{b.ja[i], b.jv[i], r, q};
-      hp[i] = wide ? b.V[i] : b.U[i];                 // left factor of the Jacobi matrix
-      hp[(K + 1) + i] = wide ? b.U[i] : b.V[i];       // right factor
-      hp[2 * (K + 1) + i] = b.S[i];
-    }
-    hj[K + 1] = JacobiJob{b.PA, b.PV, m, q};
-    hj[K + 2] = JacobiJob{b.PA, b.PV, n, q};
-    SP_TRY(hipMemcpyAsync(b.jobs, hj, jb, hipMemcpyHostToDevice, s));
-    SP_TRY(hipMemcpyAsync(b.ptrs, hp, pb, hipMemcpyHostToDevice, s));
-    // 1. W_0 and W_i = W_0 + tau_i as A = W (tall) or W^T (wide), r x q col-major; SVDs
-    for (int i = 0; i <= K; ++i)
-      k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.ja[i], t[jt].base, i ? t[jt].deltas[i - 1] : nullptr, m, n,
-                                                  wide ? 1 : 0, dt);
-    SP_TRY(jacobi_block(b.jobs, K + 1, r, q, b.jst, status, s));
-    k_svd_finalize<<<K + 1, 1024, (sizeof(double) + sizeof(int)) * q, s>>>(b.jobs, b.ptrs, b.ptrs + (K + 1),
-                                                                          b.ptrs + 2 * (K + 1));
-    const int64_t keep = std::min<int64_t>(q, (int64_t)std::floor(a.rho_keep * (double)q + 0.5));
-    for (int i = 1; i <= K; ++i) {
-      double* xu = b.XU + (int64_t)(i - 1) * m * q;
-      double* xv = b.XV + (int64_t)(i - 1) * n * q;
-      // 2. sign canonicalisation against the base
-      k_canonicalize<<<grid_for(q * 64), 256, 0, s>>>(b.U[0], b.U[i], b.V[i], m, n, q);
-      // 3. displacements, tangent projection, D_keep
-      k_sub<<<grid_for(m * q), 256, 0, s>>>(xu, b.U[i], b.U[0], m * q);
-      k_sub<<<grid_for(n * q), 256, 0, s>>>(xv, b.V[i], b.V[0], n * q);
-      tangent_project(xu, b.U[0], m, q, b.P, b.Sq, s);
-      tangent_project(xv, b.V[0], n, q, b.P, b.Sq, s);
-      k_mask_cols<<<grid_for(m * q), 256, 0, s>>>(xu, m, q, keep);
-      k_mask_cols<<<grid_for(n * q), 256, 0, s>>>(xv, n, q, keep);
-      // 4. g_i = xi_U Sigma_0 V_0^T + U_0 Sigma_0 xi_V^T  (m x n col-major)
-      double* g = b.G + (int64_t)(i - 1) * m * n;
-      k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, xu, b.S[0], m, q);
-      gemm(m, n, q, 1.0, b.FU, 1, m, b.V[0], n, 1, 0.0, g, 1, m, s);
-      k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, b.U[0], b.S[0], m, q);
-      gemm(m, n, q, 1.0, b.FU, 1, m, xv, n, 1, 1.0, g, 1, m, s);
-    }
-    // 5. Gram, ridge solve, clip
-    k_gram<<<K * (K + 1) / 2, 1024, 0, s>>>(b.G, m * n, K, b.gram);
-    k_solve<<<1, 64, 0, s>>>(b.gram, K, a.ridge, a.c_min, a.c_max, b.coef,
-                             a.coef_out ? a.coef_out + (int64_t)jt * K : nullptr, status);
-    // 6. aggregate, project, retract
-    k_combine<<<grid_for(m * q), 256, 0, s>>>(b.AU, b.XU, b.coef, K, m * q);
-    k_combine<<<grid_for(n * q), 256, 0, s>>>(b.AV, b.XV, b.coef, K, n * q);
-    tangent_project(b.AU, b.U[0], m, q, b.P, b.Sq, s);
-    tangent_project(b.AV, b.V[0], n, q, b.P, b.Sq, s);
-    k_add<<<grid_for(m * q), 256, 0, s>>>(b.AU, b.AU, b.U[0], m * q);
-    k_add<<<grid_for(n * q), 256, 0, s>>>(b.AV, b.AV, b.V[0], n * q);
-    SP_TRY(polar(b.AU, m, q, b, b.jobs + (K + 1), status, s));
-    SP_TRY(polar(b.AV, n, q, b, b.jobs + (K + 2), status, s));
-    // 7. W_* = U_* Sigma_0 V_*^T
-    k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, b.AU, b.S[0], m, q);
-    gemm(m, n, q, 1.0, b.FU, 1, m, b.AV, n, 1, 0.0, b.Wst, 1, m, s);
-    k_store_w<<<grid_for(m * n), 256, 0, s>>>(t[jt].out, b.Wst, m, n, dt, status);
-    SP_TRY(hipGetLastError());
-    // the next tensor reuses the workspace and the host staging: let this one finish first
-    SP_TRY(hipStreamSynchronize(s));
+  std::vector<uint8_t> host;    // host staging for the job tables; kept until the stream has consumed them
+  for (const auto& ids : spectral_batches(t, n_t, K)) {
+    const iso_status r = run_batch(t, ids, K, dt, a, ws, status, s, host);
+    if (r != ISO_OK) return r;
   }
   return ISO_OK;
-#undef SP_TRY
 }
 
 }  // namespace iso

@@ -1315,7 +1315,7 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     const size_t jlds = sizeof(double) * 2 * (size_t)L * L;
     if (jlds <= kJacobiLdsMax) k_jacobi_lds<<<np, kJacobiThreads, jlds, s>>>(d_jobs, status);
     else k_jacobi<<<np, kJacobiThreads, 0, s>>>(d_jobs, status);
-    k_svd_finalize<<<np, 1024, (sizeof(double) + sizeof(int)) * L, s>>>(d_jobs, d_ptrs, d_ptrs + np, d_ptrs + 2 * np);
+    k_svd_finalize<<<np, 1024, sizeof(double) * L, s>>>(d_jobs, d_ptrs, d_ptrs + np, d_ptrs + 2 * np);
     // U_i = Q Ut[:, :r], V_i = Q2 Vt[:, :r]: both factors end in buffer 0 (an even number of QR
     // passes: 2 + kPowerIters for X, kPowerIters + 2 for Z)
     static_assert(kPowerIters % 2 == 0, "ping-pong parity");

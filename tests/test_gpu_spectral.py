@@ -110,6 +110,33 @@ def test_keep_ratio_and_clip_range():
     assert np.allclose(coef[0], ref["c"], rtol=1e-9)
 
 
+# one call over several matrices: they run as one batch of Jacobi jobs of different shapes.  The
+# first set's longest columns (700) take the Gram-based block Jacobi for the whole batch, the
+# second set fits LDS; an empty matrix sits between the others
+MIXED = {
+    "gram_path": [(300, 200), (200, 300), (0, 0), (96, 700), (64, 64)],
+    "lds_path": [(120, 80), (80, 120), (0, 0), (64, 64), (17, 33)],
+}
+
+
+@pytest.mark.parametrize("name", list(MIXED))
+def test_batched_mixed_shapes(name):
+    rng = np.random.default_rng(len(name))
+    K = 3
+    units = [_unit(rng, r, c, K, "f32") if r * c else Unit(0, 0, np.zeros(0, np.float32),
+                                                          [np.zeros(0, np.float32)] * K, "f32")
+             for r, c in MIXED[name]]
+    say(f"spectral batch {name}: {MIXED[name]} K={K}")
+    outs, coef, st = run_spectral(units, K, "f32")
+    assert st == 0
+    for u, o, c in zip(units, outs, coef):
+        if u.n == 0:
+            continue
+        ref = _ref(u, K, "f32")
+        assert _close(o, "f32", ref["w_star"]), (u.rows, u.cols)
+        assert np.allclose(c, ref["c"], rtol=1e-9, atol=1e-12), (u.rows, u.cols)
+
+
 @pytest.mark.parametrize("t_idx", [0, 4], ids=["q_proj_2048x2048", "gate_proj_2048x5632"])
 def test_single_layer_shapes(t_idx):
     """Algorithm 1 at the single-layer workload's shapes (bf16, K = 2), from the seeded generator."""
