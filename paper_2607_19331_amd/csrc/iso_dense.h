@@ -302,17 +302,40 @@ constexpr int kGW = 32, kGN = 64, kGP = kGN + 1;
 // end to end than full inner convergence, with identical merged weights).
 constexpr int kGramInnerSweeps = 1;
 
+// Row chunk loads: thread t holds entries e = t + 256 u (u < 16) of a kGN x kGN chunk, column
+// l = e / kGN (the l-th of the pair's columns), row i = e % kGN: each wave reads one column's 64
+// consecutive rows.
+constexpr int kGChunkPer = kGN * kGN / 256;
+
+__device__ __forceinline__ void gram_load(double (&pf)[kGChunkPer], const double* X, int64_t ld, int nrows,
+                                          const int* gc, int nc, int k0) {
+#pragma unroll
+  for (int u = 0; u < kGChunkPer; ++u) {
+    const int e = threadIdx.x + 256 * u, l = e / kGN, i = e % kGN;
+    pf[u] = (l < nc && k0 + i < nrows) ? X[(int64_t)gc[l] * ld + k0 + i] : 0.0;
+  }
+}
+
+__device__ __forceinline__ void gram_stage(double* ch, const double (&pf)[kGChunkPer]) {
+#pragma unroll
+  for (int u = 0; u < kGChunkPer; ++u) {
+    const int e = threadIdx.x + 256 * u;
+    ch[(e / kGN) * kGP + e % kGN] = pf[u];
+  }
+}
+
 // X[:, cols] <- X[:, cols] Q for nrows rows (X col-major with leading dimension ld); ch is a
-// kGN x kGP LDS chunk, q the kGN x kGN LDS rotation (col-major).
+// kGN x kGP LDS chunk, q the kGN x kGN LDS rotation (col-major).  The next chunk is loaded into
+// registers while the current one is multiplied.
 __device__ __forceinline__ void gram_apply(double* X, int64_t ld, int nrows, const int* gc, int nc, double* ch,
                                            const double* q) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
+  double pf[kGChunkPer];
+  gram_load(pf, X, ld, nrows, gc, nc, 0);
   for (int k0 = 0; k0 < nrows; k0 += kGN) {
-    for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
-      const int l = e / kGN, i = e % kGN;
-      ch[l * kGP + i] = (l < nc && k0 + i < nrows) ? X[(int64_t)gc[l] * ld + k0 + i] : 0.0;
-    }
+    gram_stage(ch, pf);
     __syncthreads();
+    if (k0 + kGN < nrows) gram_load(pf, X, ld, nrows, gc, nc, k0 + kGN);
     jac_f64x4_t acc[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[t] = jac_f64x4_t{0.0, 0.0, 0.0, 0.0};
@@ -338,11 +361,15 @@ __device__ __forceinline__ void gram_apply(double* X, int64_t ld, int nrows, con
 }
 
 __global__ void __launch_bounds__(256) k_bjacobi_gram(const JacobiJob* __restrict__ jobs, JacobiState* st, int round) {
-  __shared__ double G[kGN * kGN];          // Gram, col-major; then the Jacobi matrix
+  // GC: the row chunk [column][row] while the Gram is formed and while A and V are multiplied by
+  // Q; in between the Gram (col-major, leading dimension kGN), then the Jacobi matrix.  About
+  // 66 KB in all: two workgroups per CU.
+  __shared__ double GC[kGN * kGP];
   __shared__ double Q[kGN * kGN];          // rotations (col-major)
-  __shared__ double ch[kGN * kGP];         // row chunk [column][row]
   __shared__ int gc[kGN];
   __shared__ int s_need, s_rot;
+  double* const G = GC;
+  double* const ch = GC;
   const int job = blockIdx.y;
   if (st[job].done) return;
   const JacobiJob J = jobs[job];
@@ -364,12 +391,12 @@ __global__ void __launch_bounds__(256) k_bjacobi_gram(const JacobiJob* __restric
 #pragma unroll
   for (int t = 0; t < 4; ++t) acc[t] = jac_f64x4_t{0.0, 0.0, 0.0, 0.0};
   __syncthreads();
+  double pf[kGChunkPer];
+  gram_load(pf, J.a, r, r, gc, nc, 0);
   for (int k0 = 0; k0 < r; k0 += kGN) {
-    for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
-      const int l = e / kGN, i = e % kGN;
-      ch[l * kGP + i] = (l < nc && k0 + i < r) ? J.a[(int64_t)gc[l] * r + k0 + i] : 0.0;
-    }
+    gram_stage(ch, pf);
     __syncthreads();
+    if (k0 + kGN < r) gram_load(pf, J.a, r, r, gc, nc, k0 + kGN);
 #pragma unroll 4
     for (int s = 0; s < kGN / 4; ++s) {
       const double a = ch[(16 * w + ln) * kGP + 4 * s + g];          // X^T[16w + ln][k]
@@ -399,7 +426,8 @@ __global__ void __launch_bounds__(256) k_bjacobi_gram(const JacobiJob* __restric
   // 3. rotations that diagonalise G: one-sided Jacobi on G (its columns orthogonalised, one sweep),
   //    accumulated into Q
   jacobi_sweeps<4>(G, Q, kGN, kGN, &s_rot, kGramInnerSweeps);
-  // 4. A and V columns times Q
+  __syncthreads();
+  // 4. A and V columns times Q (G is no longer needed: its space takes the row chunks)
   gram_apply(J.a, r, r, gc, nc, ch, Q);
   gram_apply(J.v, c, c, gc, nc, ch, Q);
   if (threadIdx.x == 0) st[job].rot = 1;
