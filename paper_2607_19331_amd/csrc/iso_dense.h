@@ -163,11 +163,13 @@ struct JacobiState {
   int rot, done;
 };
 
-__global__ void k_jacobi_begin(const JacobiJob* __restrict__ jobs, JacobiState* __restrict__ st) {
+// V <- I unless v_given (V then holds a starting orthogonal factor: the rotations multiply it)
+__global__ void k_jacobi_begin(const JacobiJob* __restrict__ jobs, JacobiState* __restrict__ st, int v_given = 0) {
   const JacobiJob J = jobs[blockIdx.y];
   const int64_t c = J.c, cc = c * c;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < cc; e += (int64_t)gridDim.x * blockDim.x)
-    J.v[e] = ((e % c) == (e / c)) ? 1.0 : 0.0;
+  if (!v_given)
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < cc; e += (int64_t)gridDim.x * blockDim.x)
+      J.v[e] = ((e % c) == (e / c)) ? 1.0 : 0.0;
   if (blockIdx.x == 0 && threadIdx.x == 0) st[blockIdx.y] = JacobiState{0, c < 2 ? 1 : 0};
 }
 
@@ -434,9 +436,9 @@ __global__ void __launch_bounds__(256) k_bjacobi_gram(const JacobiJob* __restric
 }
 
 inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_c, JacobiState* st, uint32_t* status,
-                              hipStream_t s) {
+                              hipStream_t s, bool v_given) {
   const unsigned gb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_c * max_c + 255) / 256, 4096));
-  k_jacobi_begin<<<dim3(gb, (unsigned)njobs), 256, 0, s>>>(jobs, st);
+  k_jacobi_begin<<<dim3(gb, (unsigned)njobs), 256, 0, s>>>(jobs, st, v_given ? 1 : 0);
   const int nb = (int)((max_c + kGW - 1) / kGW), nbp = nb + (nb & 1);
   const dim3 g((unsigned)std::max(1, nbp / 2), (unsigned)njobs);
   std::vector<JacobiState> h(njobs);
@@ -458,16 +460,31 @@ inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_c, J
 
 constexpr size_t kBJacobiLds = 150 * 1024;
 
+// Column block width of jacobi_block for the given largest row and column counts, and how many
+// of its workgroups one CU holds at once (LDS bound).
+inline void jacobi_block_shape(int64_t max_r, int64_t max_c, int64_t* width, int64_t* per_cu) {
+  const int64_t w = std::min<int64_t>(16, (int64_t)(kBJacobiLds / (16 * (size_t)(max_r + max_c))));
+  if (w < 16) {
+    *width = kGW;
+    *per_cu = 2;
+  } else {
+    *width = w;
+    *per_cu = std::max<int64_t>(1, std::min<int64_t>(8, (int64_t)((160 * 1024) / (16 * w * (max_r + max_c)))));
+  }
+}
+
 // Block one-sided Jacobi over njobs jobs (max_r, max_c the largest row and column counts): the
-// block width is the largest that lets 2w columns of A and V fit the LDS budget (at most 16).
-// As jacobi_multi, the host checks the done flags every kJacobiCheckSweeps sweeps.
+// block width is the largest that lets 2w columns of A and V fit the LDS budget (at most 16);
+// longer columns take the Gram-based step.  As jacobi_multi, the host checks the done flags every
+// kJacobiCheckSweeps sweeps.  v_given: each job's V already holds an orthogonal starting factor
+// (A then being the matrix times it), which the rotations multiply.
 inline hipError_t jacobi_block(const JacobiJob* jobs, int njobs, int64_t max_r, int64_t max_c, JacobiState* st,
-                               uint32_t* status, hipStream_t s) {
+                               uint32_t* status, hipStream_t s, bool v_given = false) {
   const int w = (int)std::min<int64_t>(16, (int64_t)(kBJacobiLds / (16 * (size_t)(max_r + max_c))));
-  if (w < 16) return jacobi_gram(jobs, njobs, max_c, st, status, s);
+  if (w < 16) return jacobi_gram(jobs, njobs, max_c, st, status, s, v_given);
   const size_t lds = sizeof(double) * 2 * (size_t)w * (size_t)(max_r + max_c);
   const unsigned gb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_c * max_c + 255) / 256, 4096));
-  k_jacobi_begin<<<dim3(gb, (unsigned)njobs), 256, 0, s>>>(jobs, st);
+  k_jacobi_begin<<<dim3(gb, (unsigned)njobs), 256, 0, s>>>(jobs, st, v_given ? 1 : 0);
   const int nb = (int)((max_c + w - 1) / w), nbp = nb + (nb & 1);
   const dim3 g((unsigned)std::max(1, nbp / 2), (unsigned)njobs);
   std::vector<JacobiState> h(njobs);

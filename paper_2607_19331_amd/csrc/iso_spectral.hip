@@ -311,7 +311,8 @@ Bufs carve(Bump& bp, int64_t m, int64_t n, int K) {
 
 // Job tables of a batch of nm matrices: K+1 SVD jobs per matrix with their convergence states
 // and 3 finalize pointer arrays; two polar jobs per matrix (U side, V side) with their states and
-// four GEMM tables (X^T X and X T for either buffer holding X).
+// four GEMM tables (X^T X and X T for either buffer holding X); the K warm-start products per
+// matrix.
 struct Tables {
   JacobiJob* jobs;
   JacobiState* jst;
@@ -319,6 +320,7 @@ struct Tables {
   NsJob* ns;
   NsState* nst;
   GemmJob* ngj[4];   // [2 p]: G = X_p^T X_p, [2 p + 1]: X_{1-p} = X_p T
+  GemmJob* wgj;      // warm start of the expert SVDs: A_i V_0
 };
 
 Tables carve_tables(Bump& bp, int nm, int K) {
@@ -329,6 +331,7 @@ Tables carve_tables(Bump& bp, int nm, int K) {
   tb.ns = bp.take<NsJob>(2 * nm);
   tb.nst = bp.take<NsState>(2 * nm);
   for (int k = 0; k < 4; ++k) tb.ngj[k] = bp.take<GemmJob>(2 * nm);
+  tb.wgj = bp.take<GemmJob>((int64_t)nm * K);
   return tb;
 }
 
@@ -459,9 +462,9 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
   const size_t tables_end = bp.off;
   std::vector<Bufs> bs(nm);
   for (int e = 0; e < nm; ++e) bs[e] = carve(bp, t[ids[e]].rows, t[ids[e]].cols, K);
-  // host image of the tables (same layout as on the device): the nm (K+1) SVDs (matrix e's job i
-  // at e (K+1) + i) with their finalize pointers (left, right, singular values); the polar jobs
-  // (matrix e's U side at 2 e, V side at 2 e + 1) with their GEMM tables
+  // host image of the tables (same layout as on the device): the nm (K+1) SVDs (matrix e's W_0 at
+  // e, its W_i at nm + e K + i - 1) with their finalize pointers (left, right, singular values);
+  // the polar jobs (matrix e's U side at 2 e, V side at 2 e + 1) with their GEMM tables
   host.assign(tables_end, 0);
   const auto at = [&](const void* dev) { return host.data() + ((const uint8_t*)dev - ws); };
   JacobiJob* hj = (JacobiJob*)at(tb.jobs);
@@ -469,18 +472,23 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
   NsJob* hn = (NsJob*)at(tb.ns);
   GemmJob* hg[4];
   for (int k = 0; k < 4; ++k) hg[k] = (GemmJob*)at(tb.ngj[k]);
+  GemmJob* hw = (GemmJob*)at(tb.wgj);
   int64_t svd_r = 1, svd_c = 1;
   for (int e = 0; e < nm; ++e) {
     const int64_t m = t[ids[e]].rows, n = t[ids[e]].cols, q = std::min(m, n), r = std::max(m, n);
     const bool wide = m < n;
     const Bufs& b = bs[e];
     for (int i = 0; i <= K; ++i) {
-      const int j = e * (K + 1) + i;
+      const int j = i ? nm + e * K + i - 1 : e;
       hj[j] = JacobiJob{b.ja[i], b.jv[i], r, q};
       hp[j] = wide ? b.V[i] : b.U[i];                 // left factor of the Jacobi matrix
       hp[nsvd + j] = wide ? b.U[i] : b.V[i];          // right factor
       hp[2 * nsvd + j] = b.S[i];
     }
+    // A_i V_0 as (A_0 V_0) + T_i V_0 (r x q), the first term the base's converged Jacobi matrix,
+    // T_i (tau_i or its transpose) staged in the proxy buffer
+    for (int i = 1; i <= K; ++i)
+      hw[e * K + i - 1] = GemmJob{b.G + (int64_t)(i - 1) * m * n, b.jv[0], b.ja[i], 1, r, 1, q, 1, r, r, q, q, 1.0, 1.0};
     for (int h = 0; h < 2; ++h) {
       const int pj = 2 * e + h;
       const int64_t rows = h ? n : m;
@@ -499,14 +507,48 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
     svd_c = std::max(svd_c, q);
   }
   SP_TRY(hipMemcpyAsync(ws, host.data(), tables_end, hipMemcpyHostToDevice, s));
-  // 1. W_0 and W_i = W_0 + tau_i as A = W (tall) or W^T (wide), r x q col-major; SVDs
+  // 1. W_0 and W_i = W_0 + tau_i as A = W (tall) or W^T (wide), r x q col-major; SVDs.  When the
+  //    batch's Jacobi workgroups outnumber what the chip holds at once, the base goes first and
+  //    each expert's Jacobi starts from the base's right factor V_0 (A_i V_0, rotations
+  //    accumulated onto V_0): W_i is a small perturbation of W_0, so A_i V_0 has nearly
+  //    orthogonal columns and needs fewer sweeps.  A_i V_0 is formed as the base's converged
+  //    matrix plus T_i V_0, so that tau_i = 0 gives the base's SVD exactly.  Otherwise every SVD
+  //    runs at once from the identity (the rounds then cost the same with or without the experts).
+  int64_t width = 0, per_cu = 0, wgs = 0;
+  jacobi_block_shape(svd_r, svd_c, &width, &per_cu);
+  for (int e = 0; e < nm; ++e) {
+    const int64_t nb = (std::min(t[ids[e]].rows, t[ids[e]].cols) + width - 1) / width;
+    wgs += (int64_t)(K + 1) * ((nb + 1) / 2);
+  }
+  int dev = 0, cus = 0;
+  SP_TRY(hipGetDevice(&dev));
+  SP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  const bool warm = wgs > per_cu * (int64_t)cus;
   for (int e = 0; e < nm; ++e) {
     const iso_tensor& x = t[ids[e]];
-    for (int i = 0; i <= K; ++i)
+    for (int i = 0; i <= (warm ? 0 : K); ++i)
       k_load_f64<<<grid_for(x.rows * x.cols), 256, 0, s>>>(bs[e].ja[i], x.base, i ? x.deltas[i - 1] : nullptr, x.rows,
                                                            x.cols, x.rows < x.cols ? 1 : 0, dt);
   }
-  SP_TRY(jacobi_block(tb.jobs, nsvd, svd_r, svd_c, tb.jst, status, s));
+  if (!warm) {
+    SP_TRY(jacobi_block(tb.jobs, nsvd, svd_r, svd_c, tb.jst, status, s));
+  } else {
+    SP_TRY(jacobi_block(tb.jobs, nm, svd_r, svd_c, tb.jst, status, s));
+    for (int e = 0; e < nm; ++e) {
+      const iso_tensor& x = t[ids[e]];
+      const int64_t q = std::min(x.rows, x.cols);
+      for (int i = 1; i <= K; ++i) {
+        k_load_f64<<<grid_for(x.rows * x.cols), 256, 0, s>>>(bs[e].G + (int64_t)(i - 1) * x.rows * x.cols,
+                                                             x.deltas[i - 1], nullptr, x.rows, x.cols,
+                                                             x.rows < x.cols ? 1 : 0, dt);
+        k_copy<<<grid_for(x.rows * x.cols), 256, 0, s>>>(bs[e].ja[i], bs[e].ja[0], x.rows * x.cols);
+        k_copy<<<grid_for(q * q), 256, 0, s>>>(bs[e].jv[i], bs[e].jv[0], q * q);
+      }
+    }
+    k_gemm_jobs<<<dim3((unsigned)((svd_r + GT - 1) / GT), (unsigned)((svd_c + GT - 1) / GT), (unsigned)(nm * K)), 256,
+                  0, s>>>(tb.wgj);
+    SP_TRY(jacobi_block(tb.jobs + nm, nm * K, svd_r, svd_c, tb.jst + nm, status, s, true));
+  }
   k_svd_finalize<<<nsvd, 1024, sizeof(double) * svd_c, s>>>(tb.jobs, tb.ptrs, tb.ptrs + nsvd, tb.ptrs + 2 * nsvd);
   // 2 - 6 per matrix; the polar arguments go to the first iterate buffers
   for (int e = 0; e < nm; ++e) {

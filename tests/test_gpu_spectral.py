@@ -154,3 +154,41 @@ def test_single_layer_shapes(t_idx):
     ref = _ref(u, wl.K, "bf16")
     assert _close(outs[0], "bf16", ref["w_star"])
     assert np.allclose(coef[0], ref["c"], rtol=1e-9, atol=1e-12)
+
+
+def test_warm_started_batch_lds_path():
+    """Eight 256 x 256 matrices with K = 4 in one call: their Jacobi workgroups outnumber what the
+    chip holds at once, so the experts' SVDs start from the base's right factor."""
+    rng = np.random.default_rng(41)
+    K = 4
+    units = [_unit(rng, 256, 256, K, "f32") for _ in range(8)]
+    say("spectral warm-started batch 8 x 256x256 K=4")
+    outs, coef, st = run_spectral(units, K, "f32")
+    assert st == 0
+    for u, o, c in zip(units, outs, coef):
+        ref = _ref(u, K, "f32")
+        assert _close(o, "f32", ref["w_star"])
+        assert np.allclose(c, ref["c"], rtol=1e-9, atol=1e-12)
+
+
+def test_whole_layer_one_call():
+    """The single-layer workload's seven matrices in one call (the warm-started Gram path, as
+    bench.py times it); q_proj and gate_proj checked against the oracle."""
+    import time
+    wl = synth.workload("layer")
+    units = []
+    for t, spec in enumerate(wl.tensors):
+        base = synth.fill_host(wl, t, 0)
+        ds = [synth.fill_host(wl, t, 1 + i) for i in range(wl.K)]
+        units.append(Unit(spec.rows, spec.cols, base, ds, "bf16"))
+    say(f"spectral whole layer, {len(units)} matrices, K={wl.K}")
+    t0 = time.perf_counter()
+    outs, coef, st = run_spectral(units, wl.K, "bf16")
+    say(f"spectral whole layer: {time.perf_counter() - t0:.2f} s on the GPU")
+    assert st == 0
+    for t in (0, 4):
+        ref = _ref(units[t], wl.K, "bf16")
+        assert _close(outs[t], "bf16", ref["w_star"]), wl.tensors[t].name
+        assert np.allclose(coef[t], ref["c"], rtol=1e-9, atol=1e-12), wl.tensors[t].name
+    assert np.all((coef >= 0.0) & (coef <= 1.5))
+
