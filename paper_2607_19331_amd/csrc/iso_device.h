@@ -111,6 +111,29 @@ __device__ __forceinline__ uint32_t f64_to_bf16_rne(double v) {
   return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
 }
 
+// The first half of that rounding for finite v: binary64 to binary32 with round-to-odd, as bits.
+__device__ __forceinline__ uint32_t f64_to_f32_odd_bits(double v) {
+  const float f = (float)v;
+  uint32_t b = bits_from_f32(f);
+  const double back = (double)f;
+  if (back != v) {
+    if (fabs(back) > fabs(v)) b -= 1u;
+    b |= 1u;
+  }
+  return b;
+}
+
+typedef __bf16 iso_bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float iso_f32x2_t __attribute__((ext_vector_type(2)));
+
+// The second half for two values at once: finite binary32 bit patterns to bf16 with
+// round-to-nearest-even in one v_cvt_pk_bf16_f32 (lo in bits 0-15, hi in 16-31); the same
+// result as the integer rounding below for every finite input, denormals included.
+__device__ __forceinline__ uint32_t pack_bf16_rne(uint32_t lo, uint32_t hi) {
+  const iso_f32x2_t v = {__uint_as_float(lo), __uint_as_float(hi)};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, iso_bf16x2_t));
+}
+
 // The same rounding for finite v without the NaN case (callers that flag non-finite
 // inputs elsewhere and leave such outputs unspecified).
 __device__ __forceinline__ uint32_t f64_to_bf16_rne_finite(double v) {

@@ -299,13 +299,13 @@ struct MainArgs {
   uint32_t* rec;
   int64_t tile_cap;
   double lambda;
-  int want_sign;
   uint32_t* status;
 };
 
 // Up to K = 4 the pass fits 96 VGPRs without spilling: five waves per SIMD instead of four,
 // which is what keeps enough loads in flight (the waves' lifetimes are latency-bound).
-template <int K, bool LAM1>
+// LAM1: lambda = 1 (no product); SIGN: the elected signs are written too.
+template <int K, bool LAM1, bool SIGN>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(K <= 4 ? 5 : 1)))
 k_fs_main(MainArgs a) {
   constexpr int RW = rec_words<K>();
@@ -481,7 +481,7 @@ k_fs_main(MainArgs a) {
       }
       const uint32_t wb = word_of(wv[q], h);
       bmax = pk_max(bmax, wb & 0x7FFF7FFFu);
-      uint32_t o2 = 0, s2 = 0;
+      uint32_t o32[2], s2 = 0;
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         const float S = c ? S1 : S0, A = c ? A1 : A0;
@@ -499,24 +499,22 @@ k_fs_main(MainArgs a) {
         double t = fma(rem, rn.x, qd);
         if (!LAM1) t = lambda * t;
         const float w0 = __uint_as_float(c ? (wb & 0xFFFF0000u) : (wb << 16));
-        const uint32_t o = f64_to_bf16_rne_finite((double)w0 + t);
-        o2 |= o << (16 * c);
-        if (a.want_sign) s2 |= (pos ? 0x01u : (neg ? 0xFFu : 0x00u)) << (8 * c);
+        o32[c] = f64_to_f32_odd_bits((double)w0 + t);
+        if (SIGN) s2 |= (pos ? 0x01u : (neg ? 0xFFu : 0x00u)) << (8 * c);
       }
-      ob[h] = o2;
+      ob[h] = pack_bf16_rne(o32[0], o32[1]);
       sg[h] = s2;
     }
     const int64_t vi = vbeg + (int64_t)q * kThreads + threadIdx.x;
     if (nv[q] == 8) {
       st_stream(make_uint4(ob[0], ob[1], ob[2], ob[3]), (uint4*)T.out + vi);
-      if (a.want_sign)
-        *((uint2*)T.aux2 + vi) = make_uint2(sg[0] | (sg[1] << 16), sg[2] | (sg[3] << 16));
+      if (SIGN) *((uint2*)T.aux2 + vi) = make_uint2(sg[0] | (sg[1] << 16), sg[2] | (sg[3] << 16));
     } else {
       for (int e = 0; e < nv[q]; ++e) {
         const uint32_t ow = (e < 2) ? ob[0] : (e < 4) ? ob[1] : (e < 6) ? ob[2] : ob[3];
         const uint32_t sw = (e < 2) ? sg[0] : (e < 4) ? sg[1] : (e < 6) ? sg[2] : sg[3];
         ((uint16_t*)T.out)[vi * 8 + e] = (uint16_t)((e & 1) ? (ow >> 16) : ow);
-        if (a.want_sign) ((int8_t*)T.aux2)[vi * 8 + e] = (int8_t)((e & 1) ? (sw >> 8) : sw);
+        if (SIGN) ((int8_t*)T.aux2)[vi * 8 + e] = (int8_t)((e & 1) ? (sw >> 8) : sw);
       }
     }
   }
@@ -945,11 +943,11 @@ hipError_t launch_k(const FusedPlan& pl, hipStream_t s) {
     m.rec = pl.rec;
     m.tile_cap = pl.tile_cap;
     m.lambda = pl.lambda;
-    m.want_sign = pl.want_sign;
     m.status = pl.status;
     if (pl.prof[0]) (void)hipEventRecord(pl.prof[0], s);
-    if (pl.lambda == 1.0) k_fs_main<K, true><<<(unsigned)pl.tiles, kThreads, 0, s>>>(m);
-    else k_fs_main<K, false><<<(unsigned)pl.tiles, kThreads, 0, s>>>(m);
+    if (pl.want_sign) k_fs_main<K, false, true><<<(unsigned)pl.tiles, kThreads, 0, s>>>(m);
+    else if (pl.lambda == 1.0) k_fs_main<K, true, false><<<(unsigned)pl.tiles, kThreads, 0, s>>>(m);
+    else k_fs_main<K, false, false><<<(unsigned)pl.tiles, kThreads, 0, s>>>(m);
     if (pl.prof[1]) (void)hipEventRecord(pl.prof[1], s);
   }
   if (pl.ritems > 0)
