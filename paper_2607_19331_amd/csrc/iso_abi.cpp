@@ -69,7 +69,7 @@ iso_status check_ptr_array(const void* const* p, int n, bool required) {
 
 // Workspace regions for one call.
 struct Layout {
-  size_t table = 0, hitem0 = 0, titem0 = 0, ritem0 = 0, ptrs = 0, upload_end = 0;
+  size_t table = 0, hitem0 = 0, titem0 = 0, ritem0 = 0, ptrs = 0, tmap = 0, upload_end = 0;
   size_t states = 0, hist = 0, tiecnt = 0, desc = 0, chunk_hist = 0;
   size_t fu = 0, tflag = 0, tstat = 0, tinfo = 0, csum = 0, rec = 0;
   size_t spectral = 0;
@@ -96,11 +96,13 @@ Layout plan(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
   off = align_up(off + sizeof(int64_t) * (size_t)n_t, 256);
   L.ptrs = off;
   off = align_up(off + sizeof(void*) * (size_t)n_t * K, 256);
-  L.upload_end = off;
   int64_t sumnk = 0;
   for (int j = 0; j < n_t; ++j) sumnk += t[j].rows * t[j].cols * (int64_t)K;
   const int64_t te = merge_tile_elems(dt);
   for (int j = 0; j < n_t; ++j) L.tiles += (t[j].rows * t[j].cols + te - 1) / te;
+  L.tmap = off;
+  off = align_up(off + sizeof(int) * (size_t)tile_map_entries(L.tiles), 256);
+  L.upload_end = off;
   L.select = (op == ISO_OP_TOPK || op == ISO_OP_UPDATE_FUSED_SELECT);
   if (L.select) {
     L.hist_chunk = hist_chunk_for(sumnk);
@@ -218,6 +220,13 @@ hipError_t upload(const Layout& L, const iso_tensor* t, int n_t, int K, iso_dtyp
     }
   }
   for (int q = 0; q < n_ptrs; ++q) pp[q] = ptrs[q];
+  // coarse tile map: the last tensor whose first tile is at or before m << kTileMapShift
+  int* tm = (int*)(h + (L.tmap - L.table));
+  const int64_t nmap = tile_map_entries(L.tiles);
+  for (int64_t m = 0, j = 0; m < nmap; ++m) {
+    while (j + 1 < n_t && tab[j + 1].tile0 <= (m << kTileMapShift)) ++j;
+    tm[m] = (int)j;
+  }
   return hipMemcpyAsync(ws + L.table, h, g_up.buf.size(), hipMemcpyHostToDevice, s);
 }
 
@@ -420,6 +429,7 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
       iso_select_desc* dd = (iso_select_desc*)(w + L.desc);
       FusedPlan fp;
       fp.tab = mp.tab;
+      fp.tmap = (const int*)(w + L.tmap);
       fp.n_t = n_t;
       fp.K = K;
       fp.tiles = L.tiles;

@@ -183,6 +183,18 @@ __device__ __forceinline__ int find_tensor(const DevTensor* tab, int n_t, int64_
   return lo;
 }
 
+// Coarse tile map: entry m holds the tensor owning tile m << kTileMapShift, so a lookup is one
+// read and a short forward walk (none at all when every tensor spans at least 2^kTileMapShift
+// tiles and the tile is not in the first block of a tensor's range).
+constexpr int kTileMapShift = 8;
+inline int64_t tile_map_entries(int64_t tiles) { return (tiles >> kTileMapShift) + 1; }
+
+__device__ __forceinline__ int find_tensor_mapped(const DevTensor* tab, const int* tmap, int n_t, int64_t tile) {
+  int j = tmap[tile >> kTileMapShift];
+  while (j + 1 < n_t && tab[j + 1].tile0 <= tile) ++j;
+  return j;
+}
+
 // Persistent-grid walk over the work of flagged tensors only.  Every block scans the flags
 // (through LDS, 1024 at a time) in tensor order and takes every gridDim.x-th work item of
 // the flagged tensors; count(j) gives tensor j's item count.  With no flag set a block

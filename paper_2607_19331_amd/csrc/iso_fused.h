@@ -33,6 +33,7 @@ constexpr uint32_t kFusedAll = 2u;    // k == n
 
 struct FusedPlan {
   const DevTensor* tab;
+  const int* tmap;         // coarse tile -> tensor map (find_tensor_mapped)
   int n_t, K;
   int64_t tiles, groups;   // groups: runs of up to kFusedGroupTiles tiles of one tensor (fix-up work)
   FusedUnit* fu;           // n_t * K

@@ -279,11 +279,6 @@ __device__ __forceinline__ uint32_t wave_scan_u32(uint32_t x) {
   return x;
 }
 
-// {RN(1/n) / 2, 2n} for the branch-free mean, n = 0..8 (entry 0 is never divided by)
-__constant__ double2 kHalfRecip[9] = {{0.0, 0.0},       {0.5 / 1.0, 2.0},  {0.5 / 2.0, 4.0},
-                                      {0.5 / 3.0, 6.0}, {0.5 / 4.0, 8.0},  {0.5 / 5.0, 10.0},
-                                      {0.5 / 6.0, 12.0}, {0.5 / 7.0, 14.0}, {0.5 / 8.0, 16.0}};
-
 // Provisional threshold of a delta in the main pass: kept iff key >= prov_key.
 __device__ __forceinline__ uint32_t prov_key(const FusedUnit& F) {
   return (F.flags & kFusedNone) ? 0x8000u : max(F.prov, 1u);
@@ -291,6 +286,7 @@ __device__ __forceinline__ uint32_t prov_key(const FusedUnit& F) {
 
 struct MainArgs {
   const DevTensor* tab;
+  const int* tmap;
   int n_t;
   const FusedUnit* fu;
   int* tflag;
@@ -316,35 +312,10 @@ k_fs_main(MainArgs a) {
   __shared__ uint4 s_rec[kTileCapK<K> * (RW / 4)];   // the tile's records, staged
   __shared__ int s_skip, s_redo;
   const int64_t tile = blockIdx.x;
-  const int j = find_tensor(a.tab, a.n_t, tile);
+  const int j = find_tensor_mapped(a.tab, a.tmap, a.n_t, tile);
   const DevTensor& T = a.tab[j];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  // another block may flag this tensor while this one runs: one read, shared by the block
-  if (threadIdx.x == 0) {
-    s_skip = a.tflag[j];
-    s_redo = 0;
-  }
-  if (threadIdx.x <= K) rtab[threadIdx.x] = kHalfRecip[threadIdx.x];
-  for (int e = threadIdx.x; e < K * kFusedMaxW; e += kThreads) hcnt[e / kFusedMaxW][e % kFusedMaxW] = 0;
-  // per-delta constants (two 16-bit copies): provisional key, bracket start and width - 1
-  uint32_t p1x2[K], lo1x2[K], wm1x2[K], lo1[K], hi1[K], lo0[K];
-  uint32_t emin = 0xFFu;
-#pragma unroll
-  for (int i = 0; i < K; ++i) {
-    const FusedUnit& F = a.fu[j * K + i];
-    const uint32_t p1 = prov_key(F);
-    p1x2[i] = p1 | (p1 << 16);
-    const uint32_t l1 = max(F.lo, 1u);
-    const bool br = !(F.flags & (kFusedNone | kFusedAll)) && F.hi >= l1;
-    lo0[i] = F.lo;
-    lo1[i] = br ? l1 : 0x8000u;                    // 0x8000: no key is inside
-    hi1[i] = br ? F.hi : 0u;
-    lo1x2[i] = lo1[i] | (lo1[i] << 16);
-    wm1x2[i] = br ? ((F.hi - l1) | ((F.hi - l1) << 16)) : 0u;
-    if (!(F.flags & kFusedNone)) emin = min(emin, p1 >> 7);
-  }
-  const int ebound = (int)max(emin, 1u) - 127 + 17;             // A < 2^ebound: binary32 sums exact
-  const uint32_t abound = (ebound >= 128) ? 0x7F800000u : ((uint32_t)(ebound + 127) << 23);
+  // the stream loads first: nothing below delays their issue
   const int64_t n = T.n, nvec = n / 8;
   const int64_t vbeg = (tile - T.tile0) * (int64_t)(kThreads * kVPT);
   uint4 dv[kVPT][K], wv[kVPT];
@@ -373,6 +344,35 @@ k_fs_main(MainArgs a) {
       wv[q] = make_uint4(tmp[K][0], tmp[K][1], tmp[K][2], tmp[K][3]);
     }
   }
+  // another block may flag this tensor while this one runs: one read, shared by the block
+  if (threadIdx.x == 0) {
+    s_skip = a.tflag[j];
+    s_redo = 0;
+  }
+  if (threadIdx.x <= K) {
+    const double nn = (double)threadIdx.x;
+    rtab[threadIdx.x] = (threadIdx.x == 0) ? make_double2(0.0, 0.0) : make_double2(0.5 / nn, 2.0 * nn);
+  }
+  for (int e = threadIdx.x; e < K * kFusedMaxW; e += kThreads) hcnt[e / kFusedMaxW][e % kFusedMaxW] = 0;
+  // per-delta constants (two 16-bit copies): provisional key, bracket start and width - 1
+  uint32_t p1x2[K], lo1x2[K], wm1x2[K], lo1[K], hi1[K], lo0[K];
+  uint32_t emin = 0xFFu;
+#pragma unroll
+  for (int i = 0; i < K; ++i) {
+    const FusedUnit& F = a.fu[j * K + i];
+    const uint32_t p1 = prov_key(F);
+    p1x2[i] = p1 | (p1 << 16);
+    const uint32_t l1 = max(F.lo, 1u);
+    const bool br = !(F.flags & (kFusedNone | kFusedAll)) && F.hi >= l1;
+    lo0[i] = F.lo;
+    lo1[i] = br ? l1 : 0x8000u;                    // 0x8000: no key is inside
+    hi1[i] = br ? F.hi : 0u;
+    lo1x2[i] = lo1[i] | (lo1[i] << 16);
+    wm1x2[i] = br ? ((F.hi - l1) | ((F.hi - l1) << 16)) : 0u;
+    if (!(F.flags & kFusedNone)) emin = min(emin, p1 >> 7);
+  }
+  const int ebound = (int)max(emin, 1u) - 127 + 17;             // A < 2^ebound: binary32 sums exact
+  const uint32_t abound = (ebound >= 128) ? 0x7F800000u : ((uint32_t)(ebound + 127) << 23);
   // deferred coordinates: some nonzero key inside its delta's bracket (a zero half of dm)
   uint32_t dm[kVPT][4];
   uint32_t ndef[kVPT];
@@ -935,6 +935,7 @@ hipError_t launch_k(const FusedPlan& pl, hipStream_t s) {
   if (pl.tiles > 0) {
     MainArgs m;
     m.tab = pl.tab;
+    m.tmap = pl.tmap;
     m.n_t = pl.n_t;
     m.fu = pl.fu;
     m.tflag = pl.tflag;
