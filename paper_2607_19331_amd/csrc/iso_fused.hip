@@ -284,6 +284,58 @@ __device__ __forceinline__ uint32_t prov_key(const FusedUnit& F) {
   return (F.flags & kFusedNone) ? 0x8000u : max(F.prov, 1u);
 }
 
+// One pair of coordinates (word h of the K deltas' vectors w and of the base wb): provisional
+// TopKMask (ms: 0xFFFF where not kept), elected sign, disjoint mean and theta_0 + lambda t in
+// binary64; Sv, Av: the binary32 sums S and A; o32: each result rounded to binary32.  EXACT:
+// round-to-odd, after which round-to-nearest-even to bf16 is the correct rounding of the binary64
+// value.  Otherwise round-to-nearest-even, which gives the same bf16 unless the binary32 result
+// has low half 0x8000: bf16 values and the midpoints between them are binary32 values, and
+// rounding to binary32 is monotone, so a result that is not such a midpoint lies strictly on
+// the same side of every midpoint as the binary64 value (or on the same bf16 value).  The
+// caller redoes a pair with such a result with EXACT (the same ms, Sv and Av).
+template <int K, bool LAM1, bool EXACT>
+__device__ __forceinline__ void merge_pair(const uint32_t (&w)[K], uint32_t wb, const uint32_t (&p1x2)[K],
+                                           const double2* rtab, double lambda, uint32_t (&ms)[K], float (&Sv)[2],
+                                           float (&Av)[2], uint32_t (&o32)[2]) {
+  uint32_t nk = 0, nn = 0;
+  float S0 = 0.0f, S1 = 0.0f, A0 = 0.0f, A1 = 0.0f;
+#pragma unroll
+  for (int i = 0; i < K; ++i) {
+    const uint32_t key = w[i] & 0x7FFF7FFFu;
+    ms[i] = pk_sign_fill(pk_sub(key, p1x2[i]));   // 0xFFFF: not kept
+    const uint32_t wk = w[i] & ~ms[i];
+    nk = pk_add(nk, ms[i]);
+    nn = pk_add(nn, pk_bit15(wk));
+    const float x0 = __uint_as_float(wk << 16), x1 = __uint_as_float(wk & 0xFFFF0000u);
+    if (i == 0) {
+      S0 = x0; S1 = x1; A0 = fabsf(x0); A1 = fabsf(x1);
+    } else {
+      S0 = S0 + x0; S1 = S1 + x1; A0 = A0 + fabsf(x0); A1 = A1 + fabsf(x1);
+    }
+  }
+  // agreeing count if the elected sign is +: kept (K + nk) less negative, both halves
+  const uint32_t npos = pk_sub(pk_add(nk, (uint32_t)K | ((uint32_t)K << 16)), nn);
+  Sv[0] = S0; Sv[1] = S1; Av[0] = A0; Av[1] = A1;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const float S = c ? S1 : S0, A = c ? A1 : A0;
+    uint32_t cnt = (S < 0.0f) ? (c ? (nn >> 16) : (nn & 0xFFFFu)) : (c ? (npos >> 16) : (npos & 0xFFFFu));
+    // D = S + gamma * A is twice the agreeing sum (exact); t = RN64(D / 2cnt).  With S = 0 no
+    // sign is elected: entry 0 of the table, {0, 0}, gives t = +0 for any finite D
+    cnt = (S != 0.0f) ? cnt : 0u;
+    const float D = S + copysignf(A, S);
+    const double d64 = (double)D;
+    const double2 rn = rtab[cnt];
+    const double qd = d64 * rn.x;
+    const double rem = fma(-qd, rn.y, d64);
+    double t = fma(rem, rn.x, qd);
+    if (!LAM1) t = lambda * t;
+    const float w0 = __uint_as_float(c ? (wb & 0xFFFF0000u) : (wb << 16));
+    const double v = (double)w0 + t;
+    o32[c] = EXACT ? f64_to_f32_odd_bits(v) : __float_as_uint((float)v);
+  }
+}
+
 struct MainArgs {
   const DevTensor* tab;
   const int* tmap;
@@ -461,49 +513,25 @@ k_fs_main(MainArgs a) {
     uint32_t sg[4];
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
-      uint32_t nk = 0, nn = 0;
-      float S0 = 0.0f, S1 = 0.0f, A0 = 0.0f, A1 = 0.0f;
+      uint32_t w[K], ms[K], o32[2];
+      float Sv[2], Av[2];
 #pragma unroll
-      for (int i = 0; i < K; ++i) {
-        const uint32_t w = word_of(dv[q][i], h);
-        const uint32_t key = w & 0x7FFF7FFFu;
-        const uint32_t ms = pk_sign_fill(pk_sub(key, p1x2[i]));   // 0xFFFF: not kept
-        const uint32_t wk = w & ~ms;
-        nk = pk_add(nk, ms);
-        kc[i] = pk_add(kc[i], ms);
-        nn = pk_add(nn, pk_bit15(wk));
-        const float x0 = __uint_as_float(wk << 16), x1 = __uint_as_float(wk & 0xFFFF0000u);
-        if (i == 0) {
-          S0 = x0; S1 = x1; A0 = fabsf(x0); A1 = fabsf(x1);
-        } else {
-          S0 = S0 + x0; S1 = S1 + x1; A0 = A0 + fabsf(x0); A1 = A1 + fabsf(x1);
-        }
-      }
+      for (int i = 0; i < K; ++i) w[i] = word_of(dv[q][i], h);
       const uint32_t wb = word_of(wv[q], h);
-      bmax = pk_max(bmax, wb & 0x7FFF7FFFu);
-      uint32_t o32[2], s2 = 0;
+      merge_pair<K, LAM1, false>(w, wb, p1x2, rtab, lambda, ms, Sv, Av, o32);
+      if (((uint16_t)o32[0] == 0x8000u) | ((uint16_t)o32[1] == 0x8000u))   // rare: redo with round-to-odd
+        merge_pair<K, LAM1, true>(w, wb, p1x2, rtab, lambda, ms, Sv, Av, o32);
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const float S = c ? S1 : S0, A = c ? A1 : A0;
-        amax = max(amax, __float_as_uint(A));
-        const int nkeep = K + (c ? hi_s16(nk) : lo_s16(nk));
-        const int nneg = (int)(c ? (nn >> 16) : (nn & 0xFFFFu));
-        const bool pos = S > 0.0f, neg = S < 0.0f;
-        const int cnt = pos ? nkeep - nneg : (neg ? nneg : 0);
-        // D = S + gamma * A is twice the agreeing sum (exact); t = RN64(D / 2cnt)
-        const float D = S + (pos ? A : (neg ? -A : 0.0f));
-        const double d64 = (double)D;
-        const double2 rn = rtab[cnt];
-        const double qd = d64 * rn.x;
-        const double rem = fma(-qd, rn.y, d64);
-        double t = fma(rem, rn.x, qd);
-        if (!LAM1) t = lambda * t;
-        const float w0 = __uint_as_float(c ? (wb & 0xFFFF0000u) : (wb << 16));
-        o32[c] = f64_to_f32_odd_bits((double)w0 + t);
-        if (SIGN) s2 |= (pos ? 0x01u : (neg ? 0xFFu : 0x00u)) << (8 * c);
-      }
+      for (int i = 0; i < K; ++i) kc[i] = pk_add(kc[i], ms[i]);
+      bmax = pk_max(bmax, wb & 0x7FFF7FFFu);
+      amax = max(amax, max(__float_as_uint(Av[0]), __float_as_uint(Av[1])));
       ob[h] = pack_bf16_rne(o32[0], o32[1]);
-      sg[h] = s2;
+      if (SIGN) {
+        uint32_t s2 = 0;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) s2 |= (Sv[c] > 0.0f ? 0x01u : (Sv[c] < 0.0f ? 0xFFu : 0x00u)) << (8 * c);
+        sg[h] = s2;
+      }
     }
     const int64_t vi = vbeg + (int64_t)q * kThreads + threadIdx.x;
     if (nv[q] == 8) {

@@ -160,3 +160,29 @@ def test_repeat_calls_reuse_the_workspace():
         outs = [from_dev(u.dout, u.n, "bf16") for u in units]
         check(units, 2, outs, None)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("want_sign", [False, True], ids=["no_sign", "sign"])
+def test_binary32_midpoints_take_the_exact_rounding(want_sign):
+    """Dense deltas (every entry kept) and lambda = 0.3 put a few dozen results of a 4M-entry
+    tensor on a bf16 midpoint once rounded to binary32 (low half 0x8000) while the binary64
+    value is not one; rounding the binary32 value again would miss the correct bf16 in about
+    half of them.  The pass redoes those pairs with round-to-odd: bit-exact with the oracle."""
+    rng = np.random.default_rng(3)
+    R, C, K, lam = 2048, 2048, 3, 0.3
+    n = R * C
+    base = nm.from_f64(rng.standard_normal(n) * 0.02, "bf16")
+    ds = [nm.from_f64(rng.standard_normal(n) * 1e-3, "bf16") for _ in range(K)]
+    u = Unit(R, C, base, ds, "bf16", n)
+    ref = ties.merge_unit(base, ds, "bf16", "ties", k=n, lam=lam)
+    v = nm.to_f64(base, "bf16") + ref["u"]
+    f = v.astype(np.float32)
+    mid = ((f.view(np.uint32) & 0xFFFF) == 0x8000) & (f.astype(np.float64) != v)
+    assert mid.sum() >= 16
+    assert np.any(nm.f64_to_bf16(f.astype(np.float64)) != ref["out"])   # the case is not vacuous
+    say(f"fused bf16 midpoints: {int(mid.sum())} binary32 midpoints, sign output {want_sign}")
+    outs, sg, st, fb = fused([u], K, lam=lam, want_sign=want_sign)
+    assert st == 0 and fb == 0
+    assert np.array_equal(outs[0], ref["out"])
+    if want_sign:
+        assert np.array_equal(sg[0], ref["gamma"])
