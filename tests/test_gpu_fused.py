@@ -186,3 +186,24 @@ def test_binary32_midpoints_take_the_exact_rounding(want_sign):
     assert np.array_equal(outs[0], ref["out"])
     if want_sign:
         assert np.array_equal(sg[0], ref["gamma"])
+
+
+def test_cancelling_base_takes_the_exact_rounding():
+    """A base that nearly cancels the merged update (w0 = -bf16(lambda tau)): results far below
+    the base's magnitude, where any shortcut in the binary64 sequence would show; bit-exact with
+    the oracle, lambda 1 and 0.3."""
+    rng = np.random.default_rng(4)
+    R, C, K = 512, 512, 3
+    n = R * C
+    ds = [nm.from_f64(rng.standard_normal(n) * 1e-3, "bf16") for _ in range(K)]
+    for lam in (1.0, 0.3):
+        probe = ties.merge_unit(nm.from_f64(np.zeros(n), "bf16"), ds, "bf16", "ties", k=n, lam=lam)
+        base = nm.f64_to_bf16(-probe["u"])
+        u = Unit(R, C, base, ds, "bf16", n)
+        ref = ties.merge_unit(base, ds, "bf16", "ties", k=n, lam=lam)
+        w0 = np.abs(nm.to_f64(base, "bf16"))
+        assert np.mean(w0 > 16 * np.abs(nm.to_f64(ref["out"], "bf16"))) > 0.5   # mostly cancelling
+        say(f"fused cancelling base, lambda {lam}")
+        outs, sg, st, fb = fused([u], K, lam=lam, want_sign=False)
+        assert st == 0 and fb == 0
+        assert np.array_equal(outs[0], ref["out"])
