@@ -285,18 +285,24 @@ __device__ __forceinline__ uint32_t prov_key(const FusedUnit& F) {
 }
 
 // One pair of coordinates (word h of the K deltas' vectors w and of the base wb): provisional
-// TopKMask (ms: 0xFFFF where not kept), elected sign, disjoint mean and theta_0 + lambda t in
-// binary64; Sv, Av: the binary32 sums S and A; o32: each result rounded to binary32.  EXACT:
-// round-to-odd, after which round-to-nearest-even to bf16 is the correct rounding of the binary64
-// value.  Otherwise round-to-nearest-even, which gives the same bf16 unless the binary32 result
-// has low half 0x8000: bf16 values and the midpoints between them are binary32 values, and
-// rounding to binary32 is monotone, so a result that is not such a midpoint lies strictly on
-// the same side of every midpoint as the binary64 value (or on the same bf16 value).  The
-// caller redoes a pair with such a result with EXACT (the same ms, Sv and Av).
+// TopKMask (ms: 0xFFFF where not kept), elected sign, disjoint mean and theta_0 + lambda t;
+// Sv, Av: the binary32 sums S and A; o32: each result as binary32 bits, which round-to-nearest-
+// even to bf16 turns into the output.  The reference value is v = RN64(w0 + t) with
+// t = RN64(lambda RN64(D / 2cnt)).
+//   EXACT: that binary64 sequence, rounded to binary32 with round-to-odd, after which the bf16
+//   rounding is the correct one of v.
+//   Otherwise round-to-nearest-even to binary32, which gives the same bf16 unless the binary32
+//   result has low half 0x8000: bf16 values and the midpoints between them are binary32 values,
+//   and rounding is monotone, so a result that is not such a midpoint lies strictly on the same
+//   side of every midpoint as v.  With lambda = 1 and cnt a power of two, D / 2cnt is exact and
+//   one binary32 fma gives RN32(w0 + t) from the exact sum (the same midpoint argument covers
+//   v, which is within half a binary64 ulp of that sum); other counts (3, 5, 6, 7) read NaN from
+//   the table and go to EXACT.
+// Returns true when the pair is to be redone with EXACT (rare).
 template <int K, bool LAM1, bool EXACT>
-__device__ __forceinline__ void merge_pair(const uint32_t (&w)[K], uint32_t wb, const uint32_t (&p1x2)[K],
-                                           const double2* rtab, double lambda, uint32_t (&ms)[K], float (&Sv)[2],
-                                           float (&Av)[2], uint32_t (&o32)[2]) {
+__device__ __forceinline__ bool merge_pair(const uint32_t (&w)[K], uint32_t wb, const uint32_t (&p1x2)[K],
+                                           const double2* rtab, const float* rtab32, double lambda,
+                                           uint32_t (&ms)[K], float (&Sv)[2], float (&Av)[2], uint32_t (&o32)[2]) {
   uint32_t nk = 0, nn = 0;
   float S0 = 0.0f, S1 = 0.0f, A0 = 0.0f, A1 = 0.0f;
 #pragma unroll
@@ -316,24 +322,33 @@ __device__ __forceinline__ void merge_pair(const uint32_t (&w)[K], uint32_t wb, 
   // agreeing count if the elected sign is +: kept (K + nk) less negative, both halves
   const uint32_t npos = pk_sub(pk_add(nk, (uint32_t)K | ((uint32_t)K << 16)), nn);
   Sv[0] = S0; Sv[1] = S1; Av[0] = A0; Av[1] = A1;
+  bool redo = false;
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
     const float S = c ? S1 : S0, A = c ? A1 : A0;
     uint32_t cnt = (S < 0.0f) ? (c ? (nn >> 16) : (nn & 0xFFFFu)) : (c ? (npos >> 16) : (npos & 0xFFFFu));
-    // D = S + gamma * A is twice the agreeing sum (exact); t = RN64(D / 2cnt).  With S = 0 no
-    // sign is elected: entry 0 of the table, {0, 0}, gives t = +0 for any finite D
+    // D = S + gamma * A is twice the agreeing sum (exact).  With S = 0 no sign is elected:
+    // entry 0 of the tables (zeros) gives t = +0 for any finite D
     cnt = (S != 0.0f) ? cnt : 0u;
     const float D = S + copysignf(A, S);
-    const double d64 = (double)D;
-    const double2 rn = rtab[cnt];
-    const double qd = d64 * rn.x;
-    const double rem = fma(-qd, rn.y, d64);
-    double t = fma(rem, rn.x, qd);
-    if (!LAM1) t = lambda * t;
     const float w0 = __uint_as_float(c ? (wb & 0xFFFF0000u) : (wb << 16));
-    const double v = (double)w0 + t;
-    o32[c] = EXACT ? f64_to_f32_odd_bits(v) : __float_as_uint((float)v);
+    if (EXACT || !LAM1) {
+      const double d64 = (double)D;
+      const double2 rn = rtab[cnt];
+      const double qd = d64 * rn.x;
+      const double rem = fma(-qd, rn.y, d64);
+      double t = fma(rem, rn.x, qd);
+      if (!LAM1) t = lambda * t;
+      const double v = (double)w0 + t;
+      o32[c] = EXACT ? f64_to_f32_odd_bits(v) : __float_as_uint((float)v);
+    } else {
+      const float sv = fmaf(D, rtab32[cnt], w0);
+      o32[c] = __float_as_uint(sv);
+      redo |= !(sv == sv);
+    }
+    if (!EXACT) redo |= (uint16_t)o32[c] == 0x8000u;
   }
+  return redo;
 }
 
 struct MainArgs {
@@ -361,6 +376,7 @@ k_fs_main(MainArgs a) {
   __shared__ uint32_t s_kept[K][kThreads / 64];
   __shared__ uint32_t s_wtot[kThreads / 64];
   __shared__ double2 rtab[K + 1];                   // {RN(1/n) / 2, 2n}
+  __shared__ float rtab32[K + 1];                   // 1 / 2n for n a power of two, else NaN; 0 for n = 0
   __shared__ uint4 s_rec[kTileCapK<K> * (RW / 4)];   // the tile's records, staged
   __shared__ int s_skip, s_redo;
   const int64_t tile = blockIdx.x;
@@ -402,8 +418,10 @@ k_fs_main(MainArgs a) {
     s_redo = 0;
   }
   if (threadIdx.x <= K) {
-    const double nn = (double)threadIdx.x;
-    rtab[threadIdx.x] = (threadIdx.x == 0) ? make_double2(0.0, 0.0) : make_double2(0.5 / nn, 2.0 * nn);
+    const unsigned n1 = threadIdx.x;
+    const double nn = (double)n1;
+    rtab[n1] = (n1 == 0) ? make_double2(0.0, 0.0) : make_double2(0.5 / nn, 2.0 * nn);
+    rtab32[n1] = (n1 == 0) ? 0.0f : ((n1 & (n1 - 1)) == 0 ? 0.5f / (float)n1 : __uint_as_float(0x7FC00000u));
   }
   for (int e = threadIdx.x; e < K * kFusedMaxW; e += kThreads) hcnt[e / kFusedMaxW][e % kFusedMaxW] = 0;
   // per-delta constants (two 16-bit copies): provisional key, bracket start and width - 1
@@ -518,9 +536,8 @@ k_fs_main(MainArgs a) {
 #pragma unroll
       for (int i = 0; i < K; ++i) w[i] = word_of(dv[q][i], h);
       const uint32_t wb = word_of(wv[q], h);
-      merge_pair<K, LAM1, false>(w, wb, p1x2, rtab, lambda, ms, Sv, Av, o32);
-      if (((uint16_t)o32[0] == 0x8000u) | ((uint16_t)o32[1] == 0x8000u))   // rare: redo with round-to-odd
-        merge_pair<K, LAM1, true>(w, wb, p1x2, rtab, lambda, ms, Sv, Av, o32);
+      if (merge_pair<K, LAM1, false>(w, wb, p1x2, rtab, rtab32, lambda, ms, Sv, Av, o32))   // rare
+        merge_pair<K, LAM1, true>(w, wb, p1x2, rtab, rtab32, lambda, ms, Sv, Av, o32);
 #pragma unroll
       for (int i = 0; i < K; ++i) kc[i] = pk_add(kc[i], ms[i]);
       bmax = pk_max(bmax, wb & 0x7FFF7FFFu);
