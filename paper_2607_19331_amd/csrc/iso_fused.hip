@@ -458,9 +458,9 @@ k_fs_main(MainArgs a) {
         d = pk_min(d, pk_subsat(pk_sub(key, lo1x2[i]), wm1x2[i]));
       }
       dm[q][h] = d;
-      nd = pk_add(nd, pk_min(d, 0x00010001u));
+      nd = __builtin_amdgcn_sad_u16(pk_min(d, 0x00010001u), 0u, nd);   // + nonzero halves
     }
-    ndef[q] = 8u - ((nd & 0xFFFFu) + (nd >> 16));
+    ndef[q] = 8u - nd;
   }
   // record slots: flat index order inside the tile (vector q, then thread, then element)
   static_assert(kVPT == 2, "the record scan packs two vector counts");
@@ -498,17 +498,22 @@ k_fs_main(MainArgs a) {
         for (int c = 0; c < 2; ++c) {
           const bool def = ((dm[q][h] >> (16 * c)) & 0xFFFFu) == 0u;
           if (def) {                               // rare per lane: waves with no such lane skip the site
+            // halfword 3 + x holds value x (deltas, then the base); words from 2 on pair two
+            // values, each taken from half c of its vector word with one byte permute
             uint32_t wds[RW];
 #pragma unroll
             for (int z = 0; z < RW; ++z) wds[z] = 0;
+            const auto val = [&](int x) { return (x < K) ? word_of(dv[q][x < K ? x : 0], h) : word_of(wv[q], h); };
             wds[0] = i0 + (uint32_t)(2 * h + c);
-            wds[1] = (uint32_t)j;
+            wds[1] = c ? __builtin_amdgcn_perm(val(0), (uint32_t)j, 0x07060100u)
+                       : __builtin_amdgcn_perm(val(0), (uint32_t)j, 0x05040100u);
 #pragma unroll
-            for (int x = 0; x <= K; ++x) {
-              const uint32_t w = (x < K) ? word_of(dv[q][x < K ? x : 0], h) : word_of(wv[q], h);
-              const int hw = 3 + x;
-              const uint32_t v = c ? (w >> 16) : (w & 0xFFFFu);
-              wds[hw >> 1] |= v << (16 * (hw & 1));
+            for (int z = 2; z < RW; ++z) {
+              const int x0 = 2 * z - 3, x1 = 2 * z - 2;
+              if (x1 <= K)
+                wds[z] = __builtin_amdgcn_perm(val(x1), val(x0), c ? 0x07060302u : 0x05040100u);
+              else if (x0 <= K)
+                wds[z] = c ? (val(x0) >> 16) : (val(x0) & 0xFFFFu);
             }
 #pragma unroll
             for (int z = 0; z < RW / 4; ++z)
