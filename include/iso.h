@@ -90,6 +90,8 @@ typedef struct iso_tensor {
   void* out;                       /* merged weights, N elements of the storage type            */
   int64_t rows, cols;              /* N = rows * cols, N >= 0                                    */
   int64_t k;                       /* TopKMask count per delta, 0 <= k <= N (TIES only)          */
+  int32_t select_group;            /* 0: selected alone; > 0: selected jointly with the tensors   */
+                                   /* of the same id (see iso_topk_mask)                          */
 } iso_tensor;
 
 /*
@@ -103,6 +105,16 @@ typedef struct iso_tensor {
  * the flat index of the tie_quota-th such entry (so the descriptor is unique).
  * key_max is the largest key in the delta.  k == 0 gives t_key = 0xFFFFFFFF,
  * n_above = tie_quota = tie_cutoff = 0.
+ *
+ * Joint selection (the paper's TopKMask of a whole-model delta tau_i, App. F):
+ * the tensors of one select_group > 0 are selected together, per delta, as
+ * if their deltas were concatenated in table order: the K_g largest keys of
+ * the concatenation, ties at the threshold going to the earlier tensor and
+ * then the lower flat index, with K_g the sum of the members' k (put the
+ * whole count on one member or spread it).  The descriptors stay per tensor
+ * and per delta, each describing that tensor's part of the joint mask (its
+ * n_above + tie_quota is its share of K_g).  bf16 only (ISO_ERR_UNSUPPORTED
+ * for an fp32 call with a group); calls with groups take the two-pass path.
  */
 typedef struct iso_select_desc {
   uint32_t t_key;

@@ -43,6 +43,19 @@ def topk_mask(delta, k, dtype):
     return m
 
 
+def topk_mask_joint(deltas, k, dtype):
+    """TopKMask of one delta held in pieces (App. F, TIES "Trim" with tau_i the whole-model
+    delta): the mask of the pieces concatenated in order, split back into one mask per piece."""
+    flat = np.concatenate([np.asarray(d).ravel() for d in deltas])
+    m = topk_mask(flat, k, dtype)
+    out, o = [], 0
+    for d in deltas:
+        n = np.asarray(d).size
+        out.append(m[o:o + n])
+        o += n
+    return out
+
+
 def topk_descriptor(delta, k, dtype):
     """Threshold description of the same TopKMask, found by partial selection.
 

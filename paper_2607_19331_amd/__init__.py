@@ -31,6 +31,7 @@ class Entry:
     deltas: List[object] = field(default_factory=list)
     out: Optional[object] = None
     k: int = 0
+    group: int = 0          # select_group: 0 alone, > 0 joint TopKMask with the same id
 
 
 def _ptr(x):
@@ -53,6 +54,7 @@ def _table(entries: Sequence[Entry]):
         arr[j].rows = e.rows
         arr[j].cols = e.cols
         arr[j].k = e.k
+        arr[j].select_group = e.group
     return arr
 
 

@@ -20,7 +20,8 @@ SYMBOLS = ["iso_workspace_size", "iso_topk_mask", "iso_sign_elect", "iso_merge",
 
 class IsoTensor(ctypes.Structure):
     _fields_ = [("base", ctypes.c_void_p), ("deltas", ctypes.c_void_p * MAX_K), ("out", ctypes.c_void_p),
-                ("rows", ctypes.c_int64), ("cols", ctypes.c_int64), ("k", ctypes.c_int64)]
+                ("rows", ctypes.c_int64), ("cols", ctypes.c_int64), ("k", ctypes.c_int64),
+                ("select_group", ctypes.c_int32)]
 
 
 class IsoSelectDesc(ctypes.Structure):

@@ -5,6 +5,7 @@
 
 #include <cstring>
 #include <mutex>
+#include <unordered_map>
 #include <vector>
 
 #include "iso.h"
@@ -36,10 +37,10 @@ iso_status check_table(const iso_tensor* t, int n_t, int K, iso_dtype dt, Need n
   if (dt != ISO_F32 && dt != ISO_BF16) return ISO_ERR_INVALID_ARG;
   for (int j = 0; j < n_t; ++j) {
     const iso_tensor& x = t[j];
-    if (x.rows < 0 || x.cols < 0) return ISO_ERR_INVALID_ARG;
+    if (x.rows < 0 || x.cols < 0 || x.select_group < 0) return ISO_ERR_INVALID_ARG;
     if (x.cols != 0 && x.rows > kMaxElems / x.cols) return ISO_ERR_UNSUPPORTED;
     const int64_t n = x.rows * x.cols;
-    if (need.k && (x.k < 0 || x.k > n)) return ISO_ERR_INVALID_ARG;
+    if (need.k && (x.k < 0 || (x.select_group == 0 && x.k > n))) return ISO_ERR_INVALID_ARG;   // groups: check_groups
     if (n == 0) continue;
     if (need.base) {
       if (!x.base) return ISO_ERR_INVALID_ARG;
@@ -67,12 +68,60 @@ iso_status check_ptr_array(const void* const* p, int n, bool required) {
   return ISO_OK;
 }
 
+// Joint-selection groups of a table: dense group index per tensor (-1 alone), members of each
+// group in table order, the group's count (sum of its members' k) and size.
+struct GroupMap {
+  int n = 0;
+  std::vector<int> gid, mem, mem0;
+  std::vector<int64_t> gk, gn;
+};
+
+GroupMap group_map(const iso_tensor* t, int n_t) {
+  GroupMap G;
+  G.gid.assign(n_t, -1);
+  std::unordered_map<int32_t, int> index;
+  for (int j = 0; j < n_t; ++j) {
+    if (t[j].select_group <= 0) continue;
+    auto it = index.find(t[j].select_group);
+    if (it == index.end()) it = index.emplace(t[j].select_group, (int)index.size()).first;
+    G.gid[j] = it->second;
+  }
+  G.n = (int)index.size();
+  G.mem0.assign(G.n + 1, 0);
+  G.gk.assign(G.n, 0);
+  G.gn.assign(G.n, 0);
+  for (int j = 0; j < n_t; ++j)
+    if (G.gid[j] >= 0) {
+      G.mem0[G.gid[j] + 1] += 1;
+      G.gk[G.gid[j]] += t[j].k;
+      G.gn[G.gid[j]] += t[j].rows * t[j].cols;
+    }
+  for (int g = 0; g < G.n; ++g) G.mem0[g + 1] += G.mem0[g];
+  G.mem.assign(G.mem0[G.n], 0);
+  std::vector<int> fill(G.mem0.begin(), G.mem0.end() - 1);
+  for (int j = 0; j < n_t; ++j)
+    if (G.gid[j] >= 0) G.mem[fill[G.gid[j]]++] = j;
+  return G;
+}
+
+// Groups are bf16 only, and a group's count cannot exceed its size.
+iso_status check_groups(const iso_tensor* t, int n_t, iso_dtype dt) {
+  const GroupMap G = group_map(t, n_t);
+  if (G.n == 0) return ISO_OK;
+  if (dt != ISO_BF16) return ISO_ERR_UNSUPPORTED;
+  for (int g = 0; g < G.n; ++g)
+    if (G.gk[g] > G.gn[g]) return ISO_ERR_INVALID_ARG;
+  return ISO_OK;
+}
+
 // Workspace regions for one call.
 struct Layout {
   size_t table = 0, hitem0 = 0, titem0 = 0, ritem0 = 0, ptrs = 0, tmap = 0, upload_end = 0;
   size_t states = 0, hist = 0, tiecnt = 0, desc = 0, chunk_hist = 0;
   size_t fu = 0, tflag = 0, tstat = 0, tinfo = 0, csum = 0, rec = 0;
   size_t spectral = 0;
+  size_t ggid = 0, gmem = 0, gmem0 = 0, gk = 0, ghist = 0, gstate = 0, mcnt = 0;
+  int n_groups = 0;
   size_t total = 0;
   int64_t hist_chunk = 0, hist_items = 0, tie_items = 0, tiles = 0, groups = 0, ritems = 0, tile_cap = 0;
   bool select = false, use_chunk_hist = false, fused = false;
@@ -102,8 +151,22 @@ Layout plan(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
   for (int j = 0; j < n_t; ++j) L.tiles += (t[j].rows * t[j].cols + te - 1) / te;
   L.tmap = off;
   off = align_up(off + sizeof(int) * (size_t)tile_map_entries(L.tiles), 256);
-  L.upload_end = off;
   L.select = (op == ISO_OP_TOPK || op == ISO_OP_UPDATE_FUSED_SELECT);
+  if (L.select) {
+    const GroupMap G = group_map(t, n_t);
+    L.n_groups = G.n;
+    if (G.n > 0) {
+      L.ggid = off;
+      off = align_up(off + sizeof(int) * (size_t)n_t, 256);
+      L.gmem = off;
+      off = align_up(off + sizeof(int) * (size_t)std::max(1, (int)G.mem.size()), 256);
+      L.gmem0 = off;
+      off = align_up(off + sizeof(int) * (size_t)(G.n + 1), 256);
+      L.gk = off;
+      off = align_up(off + sizeof(int64_t) * (size_t)G.n, 256);
+    }
+  }
+  L.upload_end = off;
   if (L.select) {
     L.hist_chunk = hist_chunk_for(sumnk);
     for (int j = 0; j < n_t; ++j) {
@@ -126,8 +189,16 @@ Layout plan(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
     }
     L.desc = off;
     off = align_up(off + sizeof(iso_select_desc) * (size_t)n_t * K, 256);
+    if (L.n_groups > 0) {
+      L.ghist = off;
+      off = align_up(off + sizeof(uint32_t) * 32768ull * (size_t)L.n_groups * K, 256);
+      L.gstate = off;
+      off = align_up(off + sizeof(GroupState) * (size_t)L.n_groups * K, 256);
+      L.mcnt = off;
+      off = align_up(off + sizeof(int64_t) * 2 * (size_t)n_t * K, 256);
+    }
   }
-  L.fused = fused_eligible(op, n_t, dt);
+  L.fused = fused_eligible(op, n_t, dt) && L.n_groups == 0;
   if (L.fused) {
     for (int j = 0; j < n_t; ++j) L.ritems += fused_reduce_items(t[j].rows * t[j].cols, K);
     for (int j = 0; j < n_t; ++j) L.groups += fused_groups(t[j].rows * t[j].cols);
@@ -220,6 +291,13 @@ hipError_t upload(const Layout& L, const iso_tensor* t, int n_t, int K, iso_dtyp
     }
   }
   for (int q = 0; q < n_ptrs; ++q) pp[q] = ptrs[q];
+  if (L.n_groups > 0) {
+    const GroupMap G = group_map(t, n_t);
+    std::memcpy(h + (L.ggid - L.table), G.gid.data(), sizeof(int) * (size_t)n_t);
+    if (!G.mem.empty()) std::memcpy(h + (L.gmem - L.table), G.mem.data(), sizeof(int) * G.mem.size());
+    std::memcpy(h + (L.gmem0 - L.table), G.mem0.data(), sizeof(int) * G.mem0.size());
+    std::memcpy(h + (L.gk - L.table), G.gk.data(), sizeof(int64_t) * G.gk.size());
+  }
   // coarse tile map: the last tensor whose first tile is at or before m << kTileMapShift
   int* tm = (int*)(h + (L.tmap - L.table));
   const int64_t nmap = tile_map_entries(L.tiles);
@@ -259,6 +337,16 @@ SelectPlan select_plan(const Layout& L, uint8_t* ws, int n_t, int K, iso_select_
   p.chunk_hist = L.use_chunk_hist ? (uint32_t*)(ws + L.chunk_hist) : nullptr;
   p.desc = desc;
   p.status = (uint32_t*)ws;
+  if (L.n_groups > 0) {
+    p.n_groups = L.n_groups;
+    p.gid = (const int*)(ws + L.ggid);
+    p.gmem = (const int*)(ws + L.gmem);
+    p.gmem0 = (const int*)(ws + L.gmem0);
+    p.gk = (const int64_t*)(ws + L.gk);
+    p.ghist = (uint32_t*)(ws + L.ghist);
+    p.gstate = (GroupState*)(ws + L.gstate);
+    p.mcnt = (int64_t*)(ws + L.mcnt);
+  }
   return p;
 }
 
@@ -297,6 +385,7 @@ iso_status iso_topk_mask(const iso_tensor* t, int n_t, int K, iso_dtype dt, iso_
   nd.k = true;
   iso_status st = check_table(t, n_t, K, dt, nd);
   if (st != ISO_OK) return st;
+  if ((st = check_groups(t, n_t, dt)) != ISO_OK) return st;
   if (n_t == 0) return ISO_OK;
   if (desc == nullptr) return ISO_ERR_INVALID_ARG;
   if (((uintptr_t)desc & 7u) != 0) return ISO_ERR_ALIGNMENT;
@@ -405,6 +494,7 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
     nd.base = nd.out = nd.deltas = true;
     nd.k = ties && a->desc == nullptr;
     if ((st = check_table(t, n_t, K, dt, nd)) != ISO_OK) return st;
+    if (nd.k && (st = check_groups(t, n_t, dt)) != ISO_OK) return st;
     if (!(a->lambda == a->lambda) || !(a->eps_act == a->eps_act) || !(a->eps_act >= 0)) return ISO_ERR_INVALID_ARG;
     if (n_t == 0) return ISO_OK;
     const bool want_sign = ties && a->sign_out != nullptr;

@@ -11,6 +11,14 @@
 
 namespace iso {
 
+// Per (group, delta) of a joint selection: threshold key and how many entries with that key
+// the group keeps.
+struct GroupState {
+  uint32_t t_key;
+  int32_t none;      // 1: the group keeps nothing
+  int64_t quota;
+};
+
 struct SelectPlan {
   const DevTensor* tab;
   int n_t, K;
@@ -27,6 +35,15 @@ struct SelectPlan {
   const int* filter = nullptr;  // n_t device flags: only flagged tensors are selected (others get
                                 // t_key = none); null: every tensor.  Histograms of flagged units are
                                 // cleared by the launch itself.
+  // joint selection (bf16): n_groups groups of tensors selected together per delta
+  int n_groups = 0;
+  const int* gid = nullptr;         // n_t: dense group index or -1
+  const int* gmem = nullptr;        // members of every group, in table order
+  const int* gmem0 = nullptr;       // n_groups + 1 offsets into gmem
+  const int64_t* gk = nullptr;      // n_groups: the group's count (sum of its members' k)
+  uint32_t* ghist = nullptr;        // n_groups * K * 32768
+  GroupState* gstate = nullptr;     // n_groups * K
+  int64_t* mcnt = nullptr;          // 2 * n_t * K: per unit, entries above the group threshold and ties
 };
 
 int64_t hist_chunk_for(int64_t total_elems_times_k);

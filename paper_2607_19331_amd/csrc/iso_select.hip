@@ -57,20 +57,25 @@ __device__ int64_t block_inclusive_scan(int64_t v, int64_t* sh /* >= 16 */) {
 
 // With `filter` set, only units of flagged tensors take part; the others are finished
 // (no key selected) before the first pass.
-__global__ void k_select_init(const DevTensor* tab, int n_t, int K, UnitState* st, const int* filter) {
+// A member of a joint selection starts with its group's count (so that it is histogrammed
+// whenever the group keeps anything); k_group_assign sets its own share before the resolve.
+__global__ void k_select_init(const DevTensor* tab, int n_t, int K, UnitState* st, const int* filter,
+                              const int* gid, const int64_t* gk) {
   int u = blockIdx.x * blockDim.x + threadIdx.x;
   if (u >= n_t * K) return;
   const DevTensor& T = tab[u / K];
   const bool skip = (filter != nullptr) && !filter[u / K];
+  const int g = (gid != nullptr) ? gid[u / K] : -1;
+  const int64_t k = (g >= 0) ? gk[g] : T.k;
   UnitState s;
   s.prefix = 0;
   s.key_max = 0;
-  s.k_rem = T.k;
+  s.k_rem = k;
   s.n_above = 0;
   s.bucket = T.n;
   s.cutoff = 0;
-  s.done = (T.k == 0 || skip) ? 1 : 0;
-  if (T.k == 0 || skip) s.prefix = kNoSelectKey;
+  s.done = (k == 0 || T.n == 0 || skip) ? 1 : 0;
+  if (s.done) s.prefix = kNoSelectKey;
   s.pad[0] = s.pad[1] = s.pad[2] = 0;
   st[u] = s;
 }
@@ -299,6 +304,121 @@ __global__ void __launch_bounds__(kHistThreads) k_resolve(const DevTensor* __res
       if (s.k_rem == s.bucket) { s.cutoff = T.n; s.done = 1; }
     }
     st[u] = s;
+  }
+}
+
+// ---- joint selection (bf16, one pass) -------------------------------------------------------------
+// The group's histogram is the sum of its members'; its threshold key and the number of entries
+// with that key it keeps follow from it as for one tensor.  Each member then keeps its entries
+// above the threshold and the next share of the threshold entries in table order, which is
+// exactly a TopKMask of the member with that count: the per-unit resolve and tie search then
+// give its descriptor unchanged.
+
+__global__ void __launch_bounds__(256) k_group_sum(int K, const int* __restrict__ gmem, const int* __restrict__ gmem0,
+                                                   const uint32_t* __restrict__ hist, uint32_t* __restrict__ ghist) {
+  const int gi = blockIdx.y, g = gi / K, i = gi % K;
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= kMaxBins) return;
+  uint32_t sum = 0;
+  for (int m = gmem0[g]; m < gmem0[g + 1]; ++m) sum += hist[((size_t)gmem[m] * K + i) * kMaxBins + b];
+  ghist[(size_t)gi * kMaxBins + b] = sum;
+}
+
+__global__ void __launch_bounds__(kHistThreads) k_group_resolve(const DevTensor* __restrict__ tab, int K,
+                                                                const int* __restrict__ gmem,
+                                                                const int* __restrict__ gmem0,
+                                                                const int64_t* __restrict__ gk,
+                                                                const uint32_t* __restrict__ ghist,
+                                                                GroupState* __restrict__ gst, uint32_t* status) {
+  __shared__ uint32_t sbin[kMaxBins];
+  __shared__ int64_t sh[16];
+  __shared__ int64_t found_d, found_above, total_nonzero;
+  const int gi = blockIdx.x, g = gi / K;
+  const int64_t need = gk[g];
+  if (need == 0) {
+    if (threadIdx.x == 0) gst[gi] = GroupState{kNoSelectKey, 1, 0};
+    return;
+  }
+  int64_t n_g = 0;
+  for (int m = gmem0[g]; m < gmem0[g + 1]; ++m) n_g += tab[gmem[m]].n;
+  for (uint32_t b = threadIdx.x; b < kMaxBins; b += blockDim.x) sbin[b] = ghist[(size_t)gi * kMaxBins + b];
+  if (threadIdx.x == 0) { found_d = -1; found_above = 0; }
+  __syncthreads();
+  const uint32_t per = (kMaxBins + blockDim.x - 1) / blockDim.x;
+  const uint32_t b0 = threadIdx.x * per;
+  int64_t mine = 0;
+  for (uint32_t q = 0; q < per; ++q) {
+    const uint32_t b = b0 + q;
+    if (b < kMaxBins && b > 0) mine += sbin[b];
+  }
+  const int64_t incl = block_inclusive_scan(mine, sh);
+  if (threadIdx.x == blockDim.x - 1) total_nonzero = incl;
+  __syncthreads();
+  const int64_t zeros = n_g - total_nonzero;
+  int64_t run = total_nonzero - incl;
+  for (int q = (int)per - 1; q >= 0; --q) {
+    const uint32_t b = b0 + (uint32_t)q;
+    if (b >= kMaxBins) continue;
+    const int64_t h = (b == 0) ? zeros : (int64_t)sbin[b];
+    if (run < need && run + h >= need) { found_d = b; found_above = run; }
+    run += h;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    if (found_d < 0) flag_status(status, kStatusInternal);
+    gst[gi] = GroupState{(uint32_t)(found_d < 0 ? 0 : found_d), 0, need - found_above};
+  }
+}
+
+// Per member unit: entries above the group's threshold key and entries equal to it.
+__global__ void __launch_bounds__(1024) k_member_counts(const DevTensor* __restrict__ tab, int K,
+                                                        const int* __restrict__ gid,
+                                                        const GroupState* __restrict__ gst,
+                                                        const uint32_t* __restrict__ hist, int64_t* __restrict__ mcnt) {
+  __shared__ int64_t sh[16];
+  const int u = blockIdx.x, j = u / K, i = u % K;
+  const int g = gid[j];
+  if (g < 0) return;
+  const GroupState G = gst[g * K + i];
+  if (G.none) return;
+  const uint32_t* h = hist + (size_t)u * kMaxBins;
+  int64_t above = 0, nonzero = 0;
+  for (uint32_t b = threadIdx.x + 1; b < kMaxBins; b += blockDim.x) {
+    const int64_t v = h[b];
+    nonzero += v;
+    if (b > G.t_key) above += v;
+  }
+  above = block_inclusive_scan(above, sh);
+  __syncthreads();
+  nonzero = block_inclusive_scan(nonzero, sh);
+  if (threadIdx.x == blockDim.x - 1) {
+    mcnt[2 * (size_t)u] = above;
+    mcnt[2 * (size_t)u + 1] = (G.t_key == 0) ? tab[j].n - nonzero : (int64_t)h[G.t_key];
+  }
+}
+
+// One thread per (group, delta): the threshold entries go to the members in table order.
+__global__ void k_group_assign(int n_groups, int K, const int* __restrict__ gmem, const int* __restrict__ gmem0,
+                               const GroupState* __restrict__ gst, const int64_t* __restrict__ mcnt,
+                               UnitState* __restrict__ st) {
+  const int gi = blockIdx.x * blockDim.x + threadIdx.x;
+  if (gi >= n_groups * K) return;
+  const int g = gi / K, i = gi % K;
+  const GroupState G = gst[gi];
+  if (G.none) return;
+  int64_t rem = G.quota;
+  for (int m = gmem0[g]; m < gmem0[g + 1]; ++m) {
+    const int u = gmem[m] * K + i;
+    if (st[u].done) continue;                       // an empty member
+    const int64_t ties = mcnt[2 * (size_t)u + 1];
+    const int64_t take = rem < ties ? rem : ties;
+    rem -= take;
+    const int64_t kk = mcnt[2 * (size_t)u] + take;
+    st[u].k_rem = kk;
+    if (kk == 0) {
+      st[u].done = 1;
+      st[u].prefix = kNoSelectKey;
+    }
   }
 }
 
@@ -583,7 +703,9 @@ static hipError_t run_select_t(const SelectPlan& pl, hipStream_t s) {
   const bool flt = pl.filter != nullptr;
   constexpr unsigned kFlaggedGrid = 256;
   if (flt) k_clear_hist_flagged<<<kFlaggedGrid, 1024, 0, s>>>(pl.n_t, pl.K, pl.hist, pl.filter);
-  k_select_init<<<(nu + 255) / 256, 256, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.states, pl.filter);
+  if (pl.n_groups > 0 && DT != ISO_BF16) return hipErrorInvalidValue;   // the entry points reject these
+  k_select_init<<<(nu + 255) / 256, 256, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.states, pl.filter,
+                                                 pl.n_groups > 0 ? pl.gid : nullptr, pl.gk);
   struct Pass { int shift, bits; };
   const Pass bf[1] = {{0, 15}};
   const Pass f32[3] = {{16, 15}, {8, 8}, {0, 8}};
@@ -599,6 +721,15 @@ static hipError_t run_select_t(const SelectPlan& pl, hipStream_t s) {
       k_hist<DT><<<(unsigned)pl.hist_items, kHistThreads, 0, s>>>(pl.tab, pl.n_t, pl.K, pl.hist_item0, pl.hist_chunk,
                                                                   pl.states, pl.hist, ps[q].shift, ps[q].bits,
                                                                   q == 0, pl.status, dump);
+    if (pl.n_groups > 0) {
+      const int ngk = pl.n_groups * pl.K;
+      k_group_sum<<<dim3(kMaxBins / 256, (unsigned)ngk), 256, 0, s>>>(pl.K, pl.gmem, pl.gmem0, pl.hist, pl.ghist);
+      k_group_resolve<<<ngk, kHistThreads, 0, s>>>(pl.tab, pl.K, pl.gmem, pl.gmem0, pl.gk, pl.ghist, pl.gstate,
+                                                   pl.status);
+      k_member_counts<<<nu, 1024, 0, s>>>(pl.tab, pl.K, pl.gid, pl.gstate, pl.hist, pl.mcnt);
+      k_group_assign<<<(ngk + 63) / 64, 64, 0, s>>>(pl.n_groups, pl.K, pl.gmem, pl.gmem0, pl.gstate, pl.mcnt,
+                                                    pl.states);
+    }
     k_resolve<<<nu, kHistThreads, 0, s>>>(pl.tab, pl.K, pl.states, pl.hist, ps[q].shift, ps[q].bits, q == np - 1,
                                           pl.status);
   }

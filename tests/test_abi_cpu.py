@@ -78,6 +78,25 @@ def test_host_validation_errors():
     assert L.iso_read_device_status(None, None) == 1
 
 
+def test_group_validation():
+    """Joint selection: negative ids and a group count above the group's size are invalid, an
+    fp32 call with a group is unsupported; a member's own k may exceed its size."""
+    L = _lib.load()
+    a, b = entry(rows=16, cols=16, k=300), entry(rows=16, cols=16, k=0)
+    a.group = b.group = 3
+    assert call_topk([a, b], 2) != _lib.ERR_INVALID_ARG          # 300 <= 512: passes validation
+    a.k = 600
+    assert call_topk([a, b], 2) == _lib.ERR_INVALID_ARG
+    a.k, a.group = 10, -1
+    assert call_topk([a, b], 2) == _lib.ERR_INVALID_ARG
+    a.group = 3
+    es = [a, b]
+    assert L.iso_topk_mask(iso._table(es), 2, 2, iso.F32, FAKE * 8, None, FAKE * 16, 1 << 30, None) == \
+        _lib.ERR_UNSUPPORTED
+    n_alone = iso.iso_workspace_size(iso.OP_TOPK, [entry(), entry()], 2, iso.BF16)
+    assert iso.iso_workspace_size(iso.OP_TOPK, es, 2, iso.BF16) >= n_alone + 2 * 32768 * 4
+
+
 def test_workspace_sizes():
     es = [entry(rows=2048, cols=5632, k=1153434, K=2), entry(rows=7, cols=9, k=3, K=2)]
     n_sel = iso.iso_workspace_size(iso.OP_TOPK, es, 2, iso.BF16)

@@ -224,3 +224,45 @@ def test_nonfinite_input_raises():
         ties.topk_mask(x, 1, "f32")
     with pytest.raises(FloatingPointError):
         ties.merge_unit(x, [x], "f32", "ta")
+
+
+def _brute_joint(pieces, k):
+    """Joint TopKMask by repeated maximum over (|x| desc, piece, index) in pure Python."""
+    items = [(abs(v), p, i) for p, vals in enumerate(pieces) for i, v in enumerate(vals)]
+    left = list(range(len(items)))
+    keep = set()
+    for _ in range(k):
+        best = None
+        for q in left:
+            a, p, i = items[q]
+            if best is None or a > items[best][0]:
+                best = q
+        keep.add(best)
+        left.remove(best)
+    out = [np.zeros(len(v), dtype=bool) for v in pieces]
+    for q in keep:
+        _, p, i = items[q]
+        out[p][i] = True
+    return out
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_joint_topk_matches_pure_python_selection(dtype):
+    """Ties across pieces go to the earlier piece, then the lower index; k spans pieces."""
+    rng = np.random.default_rng(8)
+    lens = [7, 1, 12, 0, 9]
+    pieces_f = [list(rng.choice([0.0, 0.5, -0.5, 1.0, -2.0, 0.25], size=n)) for n in lens]
+    pieces = [_store(v, dtype) for v in pieces_f]
+    vals = [list(nm.to_f64(p, dtype)) for p in pieces]
+    for k in (0, 1, 5, 13, 20, sum(lens)):
+        got = ties.topk_mask_joint(pieces, k, dtype)
+        want = _brute_joint(vals, k)
+        assert all(np.array_equal(g, w) for g, w in zip(got, want)), k
+        assert sum(int(g.sum()) for g in got) == k
+
+
+def test_joint_topk_of_one_piece_is_topk():
+    rng = np.random.default_rng(9)
+    d = _store(rng.standard_normal(300) * 1e-3, "bf16")
+    for k in (0, 17, 300):
+        assert np.array_equal(ties.topk_mask_joint([d], k, "bf16")[0], ties.topk_mask(d, k, "bf16"))
