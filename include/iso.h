@@ -220,6 +220,27 @@ iso_status iso_blockdiag_project(const iso_tensor* t, int n_t, int K, iso_dtype 
 
 size_t iso_workspace_size_tsv(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank);
 
+/* Truncated factors of one delta (App. F, TSV step 1): Delta_i ~ U_i diag(s_i) V_i^T.
+ * Device memory, binary64, row-major: u is rows x rank, v is cols x rank, s has rank values. */
+typedef struct iso_factors {
+  const double* u;
+  const double* s;
+  const double* v;
+} iso_factors;
+
+/*
+ * iso_blockdiag_project_factors -- the same projection (concatenation, Procrustes
+ * orthogonalisation, reconstruction and update) from given truncated factors
+ * instead of the library's own truncated SVD: factors[j*K + i] belong to delta i
+ * of tensor j (host array of device pointers).  For callers that already hold
+ * the factors, and so that the steps after the SVD can be checked on their own.
+ * The deltas of the table are not read; base and out are.  Same workspace as
+ * iso_blockdiag_project (iso_workspace_size_tsv) and the same errors.
+ */
+iso_status iso_blockdiag_project_factors(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank, double alpha,
+                                         const iso_factors* factors, float* const* delta_hat, void* ws,
+                                         size_t ws_bytes, void* stream);
+
 /* round(n * num / den), halves rounded up, in exact integer arithmetic; -1 on bad arguments. */
 int64_t iso_k_from_density(int64_t n, int64_t num, int64_t den);
 

@@ -143,6 +143,18 @@ def iso_blockdiag_project(entries, K, dtype, rank, alpha, delta_hat=None, ws=Non
     _check(rc, "iso_blockdiag_project")
 
 
+def iso_blockdiag_project_factors(entries, K, dtype, rank, alpha, factors, delta_hat=None, ws=None, stream=None):
+    """factors[j * K + i] = (U, s, V) device float64 tensors of delta i of tensor j (U rows x rank and
+    V cols x rank row-major, s of length rank)."""
+    arr = (_lib.IsoFactors * max(1, len(factors)))()
+    for q, (u, s_, v) in enumerate(factors):
+        arr[q].u, arr[q].s, arr[q].v = _ptr(u), _ptr(s_), _ptr(v)
+    wp, wb = _ws(ws)
+    rc = _lib.load().iso_blockdiag_project_factors(_table(entries), len(entries), K, dtype, int(rank), float(alpha),
+                                                   arr, _ptr_array(delta_hat), wp, wb, _stream(stream))
+    _check(rc, "iso_blockdiag_project_factors")
+
+
 def iso_k_from_density(n, num, den):
     return _lib.load().iso_k_from_density(n, num, den)
 

@@ -14,7 +14,7 @@ UPDATE_APPLY, UPDATE_FUSED, UPDATE_SPECTRAL = 0, 1, 2
  OP_BLOCKDIAG) = range(8)
 
 SYMBOLS = ["iso_workspace_size", "iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update",
-           "iso_blockdiag_project", "iso_workspace_size_tsv", "iso_k_from_density", "iso_read_device_status",
+           "iso_blockdiag_project", "iso_blockdiag_project_factors", "iso_workspace_size_tsv", "iso_k_from_density", "iso_read_device_status",
            "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end", "iso_status_string"]
 
 
@@ -22,6 +22,10 @@ class IsoTensor(ctypes.Structure):
     _fields_ = [("base", ctypes.c_void_p), ("deltas", ctypes.c_void_p * MAX_K), ("out", ctypes.c_void_p),
                 ("rows", ctypes.c_int64), ("cols", ctypes.c_int64), ("k", ctypes.c_int64),
                 ("select_group", ctypes.c_int32)]
+
+
+class IsoFactors(ctypes.Structure):
+    _fields_ = [("u", ctypes.c_void_p), ("s", ctypes.c_void_p), ("v", ctypes.c_void_p)]
 
 
 class IsoSelectDesc(ctypes.Structure):
@@ -56,6 +60,7 @@ def load():
     L.iso_merge.argtypes = [T, I, I, I, I, P, D, D, P, P, Z, P]
     L.iso_update.argtypes = [T, I, I, I, ctypes.POINTER(IsoUpdateArgs), P, Z, P]
     L.iso_blockdiag_project.argtypes = [T, I, I, I, I, D, P, P, Z, P]
+    L.iso_blockdiag_project_factors.argtypes = [T, I, I, I, I, D, ctypes.POINTER(IsoFactors), P, P, Z, P]
     L.iso_workspace_size_tsv.argtypes = [T, I, I, I, I]
     L.iso_workspace_size_tsv.restype = Z
     L.iso_k_from_density.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64]
@@ -67,6 +72,7 @@ def load():
     L.iso_status_string.argtypes = [I]
     L.iso_status_string.restype = ctypes.c_char_p
     for fn in ("iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update", "iso_blockdiag_project",
+               "iso_blockdiag_project_factors",
                "iso_read_device_status", "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end"):
         getattr(L, fn).restype = I
     _lib = L

@@ -620,6 +620,35 @@ iso_status iso_blockdiag_project(const iso_tensor* t, int n_t, int K, iso_dtype 
   return run_tsv(t, n_t, K, ta, w + kStatusBytes, ws_bytes - kStatusBytes, (uint32_t*)w, s);
 }
 
+iso_status iso_blockdiag_project_factors(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank, double alpha,
+                                         const iso_factors* factors, float* const* delta_hat, void* ws,
+                                         size_t ws_bytes, void* stream) {
+  iso_status st = check_tsv(t, n_t, K, dt, rank, false);
+  if (st != ISO_OK) return st;
+  Need nd;
+  nd.base = nd.out = true;
+  if ((st = check_table(t, n_t, K, dt, nd)) != ISO_OK) return st;
+  if (!(alpha - alpha == 0.0)) return ISO_ERR_INVALID_ARG;
+  if (n_t == 0) return ISO_OK;
+  if (factors == nullptr) return ISO_ERR_INVALID_ARG;
+  for (int q = 0; q < n_t * K; ++q)
+    if (factors[q].u == nullptr || factors[q].s == nullptr || factors[q].v == nullptr) return ISO_ERR_INVALID_ARG;
+  if (delta_hat != nullptr && (st = check_ptr_array((const void* const*)delta_hat, n_t, true)) != ISO_OK) return st;
+  const size_t need = kStatusBytes + tsv_workspace_bytes(t, n_t, K, rank);
+  if (ws == nullptr) return ISO_ERR_WORKSPACE;
+  if (((uintptr_t)ws & 255u) != 0) return ISO_ERR_ALIGNMENT;
+  if (ws_bytes < need) return ISO_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* w = (uint8_t*)ws;
+  HIP_TRY(start_call(w, s));
+  TsvArgs ta;
+  ta.rank = rank;
+  ta.alpha = alpha;
+  ta.delta_hat = delta_hat;
+  ta.factors = factors;
+  return run_tsv(t, n_t, K, ta, w + kStatusBytes, ws_bytes - kStatusBytes, (uint32_t*)w, s);
+}
+
 int64_t iso_k_from_density(int64_t n, int64_t num, int64_t den) {
   if (n < 0 || num < 0 || den <= 0 || num > den) return -1;
   __int128 v = (__int128)2 * n * num + den;

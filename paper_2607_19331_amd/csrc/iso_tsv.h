@@ -12,6 +12,7 @@ struct TsvArgs {
   int rank;          // r: top singular triplets kept per delta
   double alpha;      // W = W_0 + alpha * Delta_hat
   float* const* delta_hat;   // optional: n_t device pointers, N floats each (row-major)
+  const iso_factors* factors = nullptr;   // optional: n_t*K given truncated factors (skip the SVD)
 };
 
 // Sketch width used for rank r on an R x C matrix, or 0 if the shape is too small.

@@ -55,6 +55,9 @@ struct Prob {
   double* Vt;              // L x L sorted right factors (col-major)
   double* St;              // L sorted singular values
   uint64_t seed;
+  const double* fu;        // given factors (or null): R x r, r, C x r row-major
+  const double* fs;
+  const double* fv;
 };
 
 // One matrix.
@@ -742,6 +745,25 @@ __global__ void k_sigma(const Prob* __restrict__ probs, Mat* mats, int K, int r)
   for (int c = threadIdx.x; c < r; c += blockDim.x) M.Sig[i * r + c] = P.St[c];
 }
 
+// Given factors: U_i and V_i into column block i of the concatenated U and V, s_i into Sig.
+__global__ void k_load_factors(const Prob* __restrict__ probs, Mat* mats, int K, int r) {
+  const int p = blockIdx.y;
+  const Prob& P = probs[p];
+  Mat& M = mats[p / K];
+  const int i = p % K;
+  const int64_t nu = P.R * r, nv = P.C * r;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < nu + nv; e += (int64_t)gridDim.x * blockDim.x) {
+    if (e < nu) {
+      M.U[(e / r) * M.ldk + i * r + e % r] = P.fu[e];
+    } else {
+      const int64_t f = e - nu;
+      M.V[(f / r) * M.ldk + i * r + f % r] = P.fv[f];
+    }
+  }
+  if (blockIdx.x == 0)
+    for (int c = threadIdx.x; c < r; c += blockDim.x) M.Sig[i * r + c] = P.fs[c];
+}
+
 // ---- orthogonalisation (Procrustes / Loewdin) ---------------------------------------------------
 
 // bf16 hi/lo split of rows: dst (rows x ldk) = src (rows x Kr, row stride ldsrc) * (scale? s[col] : 1)
@@ -1189,6 +1211,12 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
         P.L = z.L;
         P.ldb = z.ldb;
         P.seed = 0x5EED0000ull + ((uint64_t)(j0 + m) << 8) + (uint64_t)i;
+        if (a.factors != nullptr) {
+          const iso_factors& f = a.factors[(size_t)(j0 + m) * K + i];
+          P.fu = f.u;
+          P.fs = f.s;
+          P.fv = f.v;
+        }
       }
       Mat& M = hm[m];
       std::memset(&M, 0, sizeof M);
@@ -1291,6 +1319,9 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
         cur = 1 - cur;
       }
     };
+    if (a.factors != nullptr) {
+      k_load_factors<<<dim3(grid_for(maxM * r), (unsigned)np), 256, 0, s>>>(d_prob, d_mat, K, r);
+    } else {
     // 1. range finder with subspace iteration
     int cx = 0, cz = 0;
     k_omega<<<dim3(gx, np), 256, 0, s>>>(d_prob);
@@ -1323,6 +1354,7 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     k_gemm_jobs<<<dim3((unsigned)((maxR + 63) / 64), (unsigned)((r + 63) / 64), (unsigned)np), 256, 0, s>>>(d_gj[0]);
     k_gemm_jobs<<<dim3((unsigned)((maxC + 63) / 64), (unsigned)((r + 63) / 64), (unsigned)np), 256, 0, s>>>(d_gj[1]);
     k_sigma<<<np, 64, 0, s>>>(d_prob, d_mat, K, r);
+    }
     // 3. Procrustes orthogonalisation of U and V: U_perp = U (U^T U)^{-1/2}
     const unsigned tk = (unsigned)((Kr + 63) / 64);
     for (int side = 0; side < 2; ++side) {

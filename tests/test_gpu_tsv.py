@@ -160,3 +160,35 @@ def test_full_mlp_shape():
     outs, dhs, st = run_tsv([u], K, r)
     assert st == 0
     check(u, K, r, 1.0, outs[0], dhs[0])
+
+
+@pytest.mark.parametrize("R,C,K,r", [(512, 384, 4, 16), (777, 520, 3, 16), (203, 250, 2, 8)])
+def test_given_factors_steps_after_the_svd(R, C, K, r):
+    """iso_blockdiag_project_factors with the oracle's exact truncated factors: only the
+    concatenation, the Procrustes orthogonalisation (binary64 Newton-Schulz) and the bf16-split
+    MFMA reconstruction remain, so Delta_hat must match the oracle's to the reconstruction's
+    rounding (about 2^-16 relative per operand): 1e-4 of max|Delta_hat| elementwise, 5e-5
+    relative in Frobenius norm.  No spectral gap is needed: the factors are given."""
+    import torch
+    rng = np.random.default_rng(R * 7 + C + K + r)
+    base = nm.f64_to_bf16(rng.standard_normal(R * C) * 0.02)
+    ds = [nm.f64_to_bf16(rng.standard_normal(R * C) * 1e-3) for _ in range(K)]
+    u = Unit(R, C, base, ds, "bf16")
+    mats = [nm.to_f64(d, "bf16").reshape(R, C) for d in ds]
+    fac = [tsv.truncated_svd(m, r) for m in mats]
+    dev = [(torch.tensor(np.ascontiguousarray(a), device="cuda"), torch.tensor(s, device="cuda"),
+            torch.tensor(np.ascontiguousarray(b), device="cuda")) for a, s, b in fac]
+    es = [u.entry()]
+    ws = iso.workspace(iso.OP_BLOCKDIAG, es, K, iso.BF16, rank=r)
+    dh = [torch.empty(R * C, dtype=torch.float32, device="cuda")]
+    say(f"tsv given factors {R}x{C} K={K} r={r}")
+    iso.iso_blockdiag_project_factors(es, K, iso.BF16, r, 1.0, dev, delta_hat=dh, ws=ws)
+    assert iso.iso_read_device_status(ws) == 0
+    ref_out, ref_dh, _ = tsv.tsv_merge(base, ds, r, 1.0, "bf16", shape=(R, C), factors=fac)
+    got = dh[0].cpu().numpy().astype(np.float64).reshape(R, C)
+    tol = 1e-4 * np.abs(ref_dh).max()
+    assert np.abs(got - ref_dh).max() <= tol
+    assert np.linalg.norm(got - ref_dh) <= 5e-5 * np.linalg.norm(ref_dh)
+    exact = nm.to_f64(base, "bf16") + ref_dh.ravel()
+    have = nm.to_f64(from_dev(u.dout, u.n, "bf16"), "bf16")
+    assert np.all(np.abs(have - exact) <= 0.5 * _ulp_bf16(exact) + tol)
