@@ -207,6 +207,43 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
 #define ISO_SPECTRAL_MAX_DIM 16384
 
 /*
+ * ISO-Optimizer step with AdamW as the base rule (ISO-AdamW, Sec. 4.3): one
+ * weight matrix W = U Sigma_0 V^T is trained through its frame variables U
+ * (rows x rank) and V (cols x rank) with Sigma_0 fixed.  Per frame, in binary64:
+ *   G_U = G_W V Sigma_0,  G_V = G_W^T U Sigma_0            (factor gradients)
+ *   AdamW on U with (m_u, v_u) and on V with (m_v, v_v):
+ *     m <- b1 m + (1 - b1) g,  v <- b2 v + (1 - b2) g^2,
+ *     x <- x - lr * ((m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps) + wd x)
+ *   U <- polar(U), V <- polar(V),  w_out <- U Sigma_0 V^T (rounded once).
+ * U, V, the moments and sigma are device binary64 arrays owned by the caller,
+ * column-major (entry (i, k) of U at u[i + k * rows]); U, V and the moments
+ * are updated in place.  grad (G_W) and w_out are rows x cols row-major in the
+ * storage type.  polar(X) = X (X^T X)^{-1/2} (full column rank), computed as
+ * for ISO-Merger.  rank <= min(rows, cols) <= ISO_SPECTRAL_MAX_DIM.
+ */
+typedef struct iso_frame {
+  double* u;            /* rows x rank */
+  double* v;            /* cols x rank */
+  const double* sigma;  /* rank */
+  double* m_u;          /* AdamW first and second moments of U and of V */
+  double* v_u;
+  double* m_v;
+  double* v_v;
+  const void* grad;     /* G_W */
+  void* w_out;          /* W+ */
+  int64_t rows, cols, rank;
+} iso_frame;
+
+typedef struct iso_adamw {
+  double lr, beta1, beta2, eps, weight_decay;
+  int64_t step;         /* t >= 1: the step being taken (bias corrections 1 - beta^t) */
+} iso_adamw;
+
+size_t iso_workspace_size_optimizer(const iso_frame* f, int n_f);
+iso_status iso_optimizer_step(const iso_frame* f, int n_f, iso_dtype dt, const iso_adamw* opt, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/*
  * iso_blockdiag_project -- TSV-Merge (App. F): each delta is truncated to its
  * top-`rank` singular triplets, the left and right singular vectors are
  * concatenated (U = [U_1 | ... | U_K], V likewise, Sigma = blockdiag of the

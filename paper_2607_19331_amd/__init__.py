@@ -155,6 +155,48 @@ def iso_blockdiag_project_factors(entries, K, dtype, rank, alpha, factors, delta
     _check(rc, "iso_blockdiag_project_factors")
 
 
+@dataclass
+class Frame:
+    """One matrix trained by ISO-AdamW: float64 device tensors (column-major frames and moments)."""
+    u: object
+    v: object
+    sigma: object
+    m_u: object
+    v_u: object
+    m_v: object
+    v_v: object
+    grad: object
+    w_out: object
+    rows: int
+    cols: int
+    rank: int
+
+
+def _frames(frames):
+    arr = (_lib.IsoFrame * max(1, len(frames)))()
+    for q, f in enumerate(frames):
+        for name in ("u", "v", "sigma", "m_u", "v_u", "m_v", "v_v", "grad", "w_out"):
+            setattr(arr[q], name, _ptr(getattr(f, name)))
+        arr[q].rows, arr[q].cols, arr[q].rank = f.rows, f.cols, f.rank
+    return arr
+
+
+def optimizer_workspace(frames, device="cuda"):
+    import torch
+    n = _lib.load().iso_workspace_size_optimizer(_frames(frames), len(frames))
+    if n == 0:
+        raise ValueError("bad frame table")
+    return torch.empty((n + 7) // 8, dtype=torch.float64, device=device)
+
+
+def iso_optimizer_step(frames, dtype, lr, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, step=1, ws=None,
+                       stream=None):
+    o = _lib.IsoAdamW(lr, beta1, beta2, eps, weight_decay, step)
+    wp, wb = _ws(ws)
+    rc = _lib.load().iso_optimizer_step(_frames(frames), len(frames), dtype, ctypes.byref(o), wp, wb, _stream(stream))
+    _check(rc, "iso_optimizer_step")
+
+
 def iso_k_from_density(n, num, den):
     return _lib.load().iso_k_from_density(n, num, den)
 

@@ -15,7 +15,8 @@ UPDATE_APPLY, UPDATE_FUSED, UPDATE_SPECTRAL = 0, 1, 2
 
 SYMBOLS = ["iso_workspace_size", "iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update",
            "iso_blockdiag_project", "iso_blockdiag_project_factors", "iso_workspace_size_tsv", "iso_k_from_density", "iso_read_device_status",
-           "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end", "iso_status_string"]
+           "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end", "iso_status_string",
+           "iso_workspace_size_optimizer", "iso_optimizer_step"]
 
 
 class IsoTensor(ctypes.Structure):
@@ -26,6 +27,16 @@ class IsoTensor(ctypes.Structure):
 
 class IsoFactors(ctypes.Structure):
     _fields_ = [("u", ctypes.c_void_p), ("s", ctypes.c_void_p), ("v", ctypes.c_void_p)]
+
+
+class IsoFrame(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("u", "v", "sigma", "m_u", "v_u", "m_v", "v_v", "grad", "w_out")] + \
+        [("rows", ctypes.c_int64), ("cols", ctypes.c_int64), ("rank", ctypes.c_int64)]
+
+
+class IsoAdamW(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_double), ("beta1", ctypes.c_double), ("beta2", ctypes.c_double),
+                ("eps", ctypes.c_double), ("weight_decay", ctypes.c_double), ("step", ctypes.c_int64)]
 
 
 class IsoSelectDesc(ctypes.Structure):
@@ -69,10 +80,13 @@ def load():
     L.iso_read_fallback_count.argtypes = [P, P, ctypes.POINTER(ctypes.c_int32)]
     L.iso_profile_begin.argtypes = []
     L.iso_profile_end.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32)]
+    L.iso_workspace_size_optimizer.argtypes = [ctypes.POINTER(IsoFrame), I]
+    L.iso_workspace_size_optimizer.restype = Z
+    L.iso_optimizer_step.argtypes = [ctypes.POINTER(IsoFrame), I, I, ctypes.POINTER(IsoAdamW), P, Z, P]
     L.iso_status_string.argtypes = [I]
     L.iso_status_string.restype = ctypes.c_char_p
     for fn in ("iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update", "iso_blockdiag_project",
-               "iso_blockdiag_project_factors",
+               "iso_blockdiag_project_factors", "iso_optimizer_step",
                "iso_read_device_status", "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end"):
         getattr(L, fn).restype = I
     _lib = L

@@ -649,6 +649,50 @@ iso_status iso_blockdiag_project_factors(const iso_tensor* t, int n_t, int K, is
   return run_tsv(t, n_t, K, ta, w + kStatusBytes, ws_bytes - kStatusBytes, (uint32_t*)w, s);
 }
 
+static iso_status check_frames(const iso_frame* f, int n_f) {
+  if (n_f < 0 || (n_f > 0 && f == nullptr)) return ISO_ERR_INVALID_ARG;
+  for (int e = 0; e < n_f; ++e) {
+    const iso_frame& F = f[e];
+    if (F.rows < 1 || F.cols < 1 || F.rank < 1 || F.rank > std::min(F.rows, F.cols)) return ISO_ERR_INVALID_ARG;
+    if (std::min(F.rows, F.cols) > ISO_SPECTRAL_MAX_DIM || std::max(F.rows, F.cols) > kMaxElems / std::min(F.rows, F.cols))
+      return ISO_ERR_UNSUPPORTED;
+    const void* p[9] = {F.u, F.v, F.sigma, F.m_u, F.v_u, F.m_v, F.v_v, F.grad, F.w_out};
+    for (const void* x : p)
+      if (x == nullptr) return ISO_ERR_INVALID_ARG;
+    for (int q = 0; q < 7; ++q)
+      if (((uintptr_t)p[q] & 7u) != 0) return ISO_ERR_ALIGNMENT;
+    if (((uintptr_t)F.grad & 3u) != 0 || ((uintptr_t)F.w_out & 3u) != 0) return ISO_ERR_ALIGNMENT;
+  }
+  return ISO_OK;
+}
+
+size_t iso_workspace_size_optimizer(const iso_frame* f, int n_f) {
+  if (check_frames(f, n_f) != ISO_OK) return 0;
+  return kStatusBytes + optimizer_workspace_bytes(f, n_f);
+}
+
+iso_status iso_optimizer_step(const iso_frame* f, int n_f, iso_dtype dt, const iso_adamw* opt, void* ws,
+                              size_t ws_bytes, void* stream) {
+  iso_status st = check_frames(f, n_f);
+  if (st != ISO_OK) return st;
+  if (dt != ISO_F32 && dt != ISO_BF16) return ISO_ERR_INVALID_ARG;
+  if (opt == nullptr || opt->step < 1) return ISO_ERR_INVALID_ARG;
+  const double h[5] = {opt->lr, opt->beta1, opt->beta2, opt->eps, opt->weight_decay};
+  for (double x : h)
+    if (!(x - x == 0.0)) return ISO_ERR_INVALID_ARG;
+  if (!(opt->beta1 >= 0.0 && opt->beta1 < 1.0 && opt->beta2 >= 0.0 && opt->beta2 < 1.0 && opt->eps > 0.0))
+    return ISO_ERR_INVALID_ARG;
+  if (n_f == 0) return ISO_OK;
+  const size_t need = kStatusBytes + optimizer_workspace_bytes(f, n_f);
+  if (ws == nullptr) return ISO_ERR_WORKSPACE;
+  if (((uintptr_t)ws & 255u) != 0) return ISO_ERR_ALIGNMENT;
+  if (ws_bytes < need) return ISO_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* w = (uint8_t*)ws;
+  HIP_TRY(start_call(w, s));
+  return run_optimizer(f, n_f, dt, *opt, w + kStatusBytes, (uint32_t*)w, s);
+}
+
 int64_t iso_k_from_density(int64_t n, int64_t num, int64_t den) {
   if (n < 0 || num < 0 || den <= 0 || num > den) return -1;
   __int128 v = (__int128)2 * n * num + den;

@@ -16,6 +16,7 @@
 // Matrices are held column-major in the workspace; dense products use a tiled binary64 GEMM on
 // MFMA.  The matrices of one call go in batches whose SVDs (and then whose polar retractions)
 // run as one Jacobi job set.  Sizes up to ISO_SPECTRAL_MAX_DIM per side.
+#include <cmath>
 #include <vector>
 
 #include "iso_dense.h"
@@ -579,6 +580,54 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
 #undef SP_TRY
 }
 
+// ---- ISO-Optimizer step (ISO-AdamW) ------------------------------------------------------------
+
+// AdamW on n entries of x with gradient g and moments m, v (decoupled weight decay), in the
+// order written in the interface: m, v, then x - lr ((m / bc1) / (sqrt(v / bc2) + eps) + wd x).
+__global__ void k_adamw(double* __restrict__ x, const double* __restrict__ g, double* __restrict__ m,
+                        double* __restrict__ v, int64_t n, double lr, double b1, double b2, double eps, double wd,
+                        double bc1, double bc2) {
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
+    const double gi = g[e];
+    const double mi = b1 * m[e] + (1.0 - b1) * gi;
+    const double vi = b2 * v[e] + (1.0 - b2) * (gi * gi);
+    m[e] = mi;
+    v[e] = vi;
+    const double xi = x[e];
+    x[e] = xi - lr * ((mi / bc1) / (sqrt(vi / bc2) + eps) + wd * xi);
+  }
+}
+
+struct OptBufs {
+  double *G, *FU, *FV, *GU, *GV, *Wst;
+  double *PX[2][2], *PG[2];
+};
+
+OptBufs carve_opt(Bump& bp, int64_t m, int64_t n, int64_t q) {
+  OptBufs b;
+  b.G = bp.take(m * n);
+  b.FU = bp.take(m * q);
+  b.FV = bp.take(n * q);
+  b.GU = bp.take(m * q);
+  b.GV = bp.take(n * q);
+  b.Wst = bp.take(m * n);
+  for (int h = 0; h < 2; ++h) {
+    const int64_t rows = h ? n : m;
+    b.PX[h][0] = bp.take(rows * q);
+    b.PX[h][1] = bp.take(rows * q);
+    b.PG[h] = bp.take(q * q);
+  }
+  return b;
+}
+
+Tables carve_opt_tables(Bump& bp, int n_f) {
+  Tables tb{};
+  tb.ns = bp.take<NsJob>(2 * n_f);
+  tb.nst = bp.take<NsState>(2 * n_f);
+  for (int k = 0; k < 4; ++k) tb.ngj[k] = bp.take<GemmJob>(2 * n_f);
+  return tb;
+}
+
 }  // namespace
 
 size_t spectral_workspace_bytes(const iso_tensor* t, int n_t, int K) {
@@ -599,6 +648,91 @@ iso_status run_spectral(const iso_tensor* t, int n_t, int K, iso_dtype dt, const
     if (r != ISO_OK) return r;
   }
   return ISO_OK;
+}
+
+size_t optimizer_workspace_bytes(const iso_frame* f, int n_f) {
+  Bump bp{nullptr};
+  carve_opt_tables(bp, n_f);
+  for (int e = 0; e < n_f; ++e) carve_opt(bp, f[e].rows, f[e].cols, f[e].rank);
+  return bp.off;
+}
+
+// All frames of the call at once: gradients, AdamW, both polar factors of every frame as one
+// Newton-Schulz job set, then W+ = U+ Sigma_0 V+^T and the frames written back.
+iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_adamw& o, uint8_t* ws,
+                         uint32_t* status, hipStream_t s) {
+#define OP_TRY(x)                                \
+  do {                                           \
+    if ((x) != hipSuccess) return ISO_ERR_HIP;   \
+  } while (0)
+  Bump bp{ws};
+  const Tables tb = carve_opt_tables(bp, n_f);
+  const size_t tables_end = bp.off;
+  std::vector<OptBufs> bs(n_f);
+  for (int e = 0; e < n_f; ++e) bs[e] = carve_opt(bp, f[e].rows, f[e].cols, f[e].rank);
+  std::vector<uint8_t> host(tables_end, 0);
+  const auto at = [&](const void* dev) { return host.data() + ((const uint8_t*)dev - ws); };
+  NsJob* hn = (NsJob*)at(tb.ns);
+  GemmJob* hg[4];
+  for (int k = 0; k < 4; ++k) hg[k] = (GemmJob*)at(tb.ngj[k]);
+  int64_t max_rows = 1, max_q = 1;
+  for (int e = 0; e < n_f; ++e) {
+    const int64_t m = f[e].rows, n = f[e].cols, q = f[e].rank;
+    const OptBufs& b = bs[e];
+    for (int h = 0; h < 2; ++h) {
+      const int pj = 2 * e + h;
+      const int64_t rows = h ? n : m;
+      const int* skip = &tb.nst[pj].done;
+      hn[pj] = NsJob{b.PG[h], q};
+      for (int p = 0; p < 2; ++p) {
+        const double* X = b.PX[h][p];
+        double* Y = b.PX[h][1 - p];
+        hg[2 * p][pj] = GemmJob{X, X, b.PG[h], rows, 1, 1, rows, 1, q, q, q, rows, 1.0, 0.0, 0, skip};
+        hg[2 * p + 1][pj] = GemmJob{X, b.PG[h], Y, 1, rows, 1, q, 1, rows, rows, q, q, 1.0, 0.0, 0, skip};
+      }
+    }
+    max_rows = std::max(max_rows, std::max(m, n));
+    max_q = std::max(max_q, q);
+  }
+  OP_TRY(hipMemcpyAsync(ws, host.data(), tables_end, hipMemcpyHostToDevice, s));
+  const double bc1 = 1.0 - std::pow(o.beta1, (double)o.step), bc2 = 1.0 - std::pow(o.beta2, (double)o.step);
+  for (int e = 0; e < n_f; ++e) {
+    const iso_frame& F = f[e];
+    const int64_t m = F.rows, n = F.cols, q = F.rank;
+    const OptBufs& b = bs[e];
+    // G_U = G_W V Sigma_0 (m x q), G_V = G_W^T U Sigma_0 (n x q); G col-major m x n
+    k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.G, F.grad, nullptr, m, n, 0, dt);
+    k_scale_cols<<<grid_for(n * q), 256, 0, s>>>(b.FV, F.v, F.sigma, n, q);
+    k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, F.u, F.sigma, m, q);
+    gemm(m, q, n, 1.0, b.G, 1, m, b.FV, 1, n, 0.0, b.GU, 1, m, s);
+    gemm(n, q, m, 1.0, b.G, m, 1, b.FU, 1, m, 0.0, b.GV, 1, n, s);
+    // AdamW on the frames (in place), then the tentative frames go to the iterate buffers
+    k_adamw<<<grid_for(m * q), 256, 0, s>>>(F.u, b.GU, F.m_u, F.v_u, m * q, o.lr, o.beta1, o.beta2, o.eps,
+                                           o.weight_decay, bc1, bc2);
+    k_adamw<<<grid_for(n * q), 256, 0, s>>>(F.v, b.GV, F.m_v, F.v_v, n * q, o.lr, o.beta1, o.beta2, o.eps,
+                                           o.weight_decay, bc1, bc2);
+    k_copy<<<grid_for(m * q), 256, 0, s>>>(b.PX[0][0], F.u, m * q);
+    k_copy<<<grid_for(n * q), 256, 0, s>>>(b.PX[1][0], F.v, n * q);
+  }
+  // U+ = polar(U), V+ = polar(V)
+  std::vector<NsState> hst;
+  OP_TRY(polar_batch(tb, 2 * n_f, max_rows, max_q, hst, status, s));
+  for (int e = 0; e < n_f; ++e) {
+    const iso_frame& F = f[e];
+    const int64_t m = F.rows, n = F.cols, q = F.rank;
+    const OptBufs& b = bs[e];
+    const double* Us = b.PX[0][hst[2 * e].steps & 1];
+    const double* Vs = b.PX[1][hst[2 * e + 1].steps & 1];
+    k_copy<<<grid_for(m * q), 256, 0, s>>>(F.u, Us, m * q);
+    k_copy<<<grid_for(n * q), 256, 0, s>>>(F.v, Vs, n * q);
+    k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, Us, F.sigma, m, q);
+    gemm(m, n, q, 1.0, b.FU, 1, m, Vs, n, 1, 0.0, b.Wst, 1, m, s);
+    k_store_w<<<grid_for(m * n), 256, 0, s>>>(F.w_out, b.Wst, m, n, dt, status);
+  }
+  OP_TRY(hipGetLastError());
+  OP_TRY(hipStreamSynchronize(s));   // the host staging of the tables ends with this call
+  return ISO_OK;
+#undef OP_TRY
 }
 
 }  // namespace iso

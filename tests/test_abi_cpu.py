@@ -121,3 +121,26 @@ def test_status_strings():
     for s in range(8):
         assert iso.iso_status_string(s)
     assert "unknown" in iso.iso_status_string(42)
+
+
+def test_optimizer_validation():
+    L = _lib.load()
+    f = (_lib.IsoFrame * 1)()
+    for i, name in enumerate(("u", "v", "sigma", "m_u", "v_u", "m_v", "v_v", "grad", "w_out")):
+        setattr(f[0], name, FAKE + 0x1000 * i)
+    f[0].rows, f[0].cols, f[0].rank = 64, 48, 48
+    o = _lib.IsoAdamW(1e-3, 0.9, 0.999, 1e-8, 0.0, 1)
+    assert L.iso_workspace_size_optimizer(f, 1) > 0
+    f[0].rank = 49
+    assert L.iso_optimizer_step(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 1 << 30, None) == _lib.ERR_INVALID_ARG
+    assert L.iso_workspace_size_optimizer(f, 1) == 0
+    f[0].rank = 48
+    o.beta2 = 1.0
+    assert L.iso_optimizer_step(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 1 << 30, None) == _lib.ERR_INVALID_ARG
+    o.beta2, o.step = 0.999, 0
+    assert L.iso_optimizer_step(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 1 << 30, None) == _lib.ERR_INVALID_ARG
+    o.step = 1
+    f[0].u = FAKE + 4
+    assert L.iso_optimizer_step(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 1 << 30, None) == _lib.ERR_ALIGNMENT
+    f[0].u = None
+    assert L.iso_optimizer_step(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 1 << 30, None) == _lib.ERR_INVALID_ARG
