@@ -249,12 +249,98 @@ def bench_layer_spectral(args, iso, synth, torch):
     return rec
 
 
+def bench_layer_optimizer(args, iso, synth, torch):
+    """One ISO-AdamW step (iso_optimizer_step) over the single layer's seven matrices (q/k/v/o
+    2048x2048, gate/up 2048x5632, down 5632x2048) with full-rank frames, bf16 weights and
+    gradients, timed with HIP events.  Roofline: binary64, the algorithmic flops of the two
+    factor-gradient products, the two polar SVDs (Golub & Van Loan's count) and W+."""
+    import numpy as np
+    from oracle import optimizer as op
+    wl = synth.workload("layer")
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream().cuda_stream
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+    frames, flops = [], 0
+    for t, spec in enumerate(wl.tensors):
+        m, n = spec.rows, spec.cols
+        q = min(m, n)
+        u, _ = torch.linalg.qr(torch.randn(m, q, dtype=torch.float64, device=dev, generator=gen))
+        v, _ = torch.linalg.qr(torch.randn(n, q, dtype=torch.float64, device=dev, generator=gen))
+        s = torch.sort(torch.rand(q, dtype=torch.float64, device=dev, generator=gen) + 0.5, descending=True)[0]
+        grad = torch.empty(m * n, dtype=torch.int16, device=dev)
+        synth.fill_device(grad.data_ptr(), m * n, wl, t, 1, stream)     # delta-shaped values as G_W
+        z = lambda r: torch.zeros(r * q, dtype=torch.float64, device=dev)
+        frames.append(iso.Frame(u=u.t().contiguous().view(-1), v=v.t().contiguous().view(-1), sigma=s,
+                                m_u=z(m), v_u=z(m), m_v=z(n), v_v=z(n), grad=grad,
+                                w_out=torch.empty(m * n, dtype=torch.int16, device=dev), rows=m, cols=n, rank=q))
+        flops += 2 * (2 * m * n * q) + svd_flops(m, q) + svd_flops(n, q) + 2 * m * n * q
+    ws = iso.optimizer_workspace(frames, dev)
+    hp = dict(lr=1e-6, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0)
+    step_no = [0]
+
+    def step():
+        step_no[0] += 1
+        iso.iso_optimizer_step(frames, iso.BF16, step=step_no[0], ws=ws, **hp)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if iso.iso_read_device_status(ws) != 0:
+        raise RuntimeError("device status reports an error")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s_ in range(args.steps):
+        ev[s_][0].record()
+        step()
+        ev[s_][1].record()
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    opt_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
+    N = wl.numel
+    rec = {
+        "metric": "merged params/sec and achieved HBM GB/s (% of peak), 7B-shaped K=4 merge",
+        "value": N / (ms_per_step * 1e-3),
+        "unit": "params/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": f"single bf16 layer ({len(wl.tensors)} matrices, {N} params): one ISO-AdamW step "
+                               "(factor gradients, AdamW, polar retraction, W+) on full-rank frames"},
+        "optimizer_ms": opt_ms,
+        "roofline": {"bound": "fp64", "kernel": "iso_optimizer_step (binary64 GEMMs and Newton-Schulz polar)",
+                     "achieved": flops / (opt_ms * 1e-3) / 1e12, "peak": 78.6, "unit": "TFLOP/s",
+                     "frac": flops / (opt_ms * 1e-3) / 1e12 / 78.6, "traffic": None, "flops_per_call": flops},
+    }
+    if not args.no_cpu_baseline:
+        spec = wl.tensors[0]
+        m, n = spec.rows, spec.cols
+        rng = np.random.default_rng(0)
+        u0, _ = np.linalg.qr(rng.standard_normal((m, m)))
+        v0, _ = np.linalg.qr(rng.standard_normal((n, n)))
+        s0 = np.sort(rng.uniform(0.5, 1.5, m))[::-1]
+        g = rng.standard_normal((m, n)) * 1e-4
+        st = tuple(np.zeros((r, m)) for r in (m, m, n, n))
+        t1 = time.perf_counter()
+        op.iso_adamw_step(u0, v0, s0, g, st, 1, 1e-6)
+        dt = time.perf_counter() - t1
+        try:
+            from threadpoolctl import threadpool_info
+            cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        except ImportError:
+            cores = len(os.sched_getaffinity(0))
+        rec["cpu_baseline"] = {"value": spec.numel / dt, "unit": "params/s", "cores": cores, "kind": "oracle",
+                               "sample": f"one ISO-AdamW step (LAPACK polar, numpy) on {spec.name} ({m}x{n}), {dt:.1f} s"}
+    return rec
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="7b", choices=["tiny", "layer", "1.5b", "7b", "7b-tsv", "layer-spectral"])
+    ap.add_argument("--config", default="7b", choices=["tiny", "layer", "1.5b", "7b", "7b-tsv", "layer-spectral",
+                                                      "layer-optimizer"])
     ap.add_argument("--path", default="single-read", choices=["single-read", "two-pass"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -287,6 +373,9 @@ def main():
         return
     if args.config == "layer-spectral":
         print(json.dumps(bench_layer_spectral(args, iso, synth, torch)), flush=True)
+        return
+    if args.config == "layer-optimizer":
+        print(json.dumps(bench_layer_optimizer(args, iso, synth, torch)), flush=True)
         return
 
     wl = synth.workload(args.config)
