@@ -207,6 +207,28 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
 #define ISO_SPECTRAL_MAX_DIM 16384
 
 /*
+ * Spectral drift diagnostics (Sec. 3), per tensor, in binary64: base = W_0,
+ * deltas[0] = Delta W (W_1 = W_0 + Delta W).  out is a device array of 3 n_t
+ * doubles, per tensor {delta_Sigma, rho_Sigma, kappa_spec}:
+ *   delta_Sigma = |sigma(W_1) - sigma(W_0)|_2 / |W_0|_F,
+ *   rho_Sigma   = |sigma(W_1) - sigma(W_0)|_2 / |Delta W|_F,
+ *   kappa_spec  = (rows cols / q) |diag(U_0^T Delta W V_0)|_2^2 / |Delta W|_F^2.
+ * Workspace: iso_workspace_size(ISO_OP_UPDATE_SPECTRAL, t, n_t, 1, dt); the
+ * size limit of ISO-Merger (rows, cols <= ISO_SPECTRAL_MAX_DIM).
+ */
+iso_status iso_spectral_diagnostics(const iso_tensor* t, int n_t, iso_dtype dt, double* out, void* ws,
+                                    size_t ws_bytes, void* stream);
+
+/*
+ * Spectrum interpolation (Sec. 3): out = U_RL [(1 - alpha) Sigma_0 + alpha
+ * Sigma_RL] V_RL^T for W_RL = base + deltas[0] and Sigma_0 the spectrum of base
+ * (alpha = 0 restores the base spectrum on the trained frames), rounded once.
+ * Same workspace and limits as iso_spectral_diagnostics.
+ */
+iso_status iso_spectrum_interpolate(const iso_tensor* t, int n_t, iso_dtype dt, double alpha, void* ws,
+                                    size_t ws_bytes, void* stream);
+
+/*
  * ISO-Optimizer step with AdamW as the base rule (ISO-AdamW, Sec. 4.3): one
  * weight matrix W = U Sigma_0 V^T is trained through its frame variables U
  * (rows x rank) and V (cols x rank) with Sigma_0 fixed.  Per frame, in binary64:

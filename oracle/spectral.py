@@ -116,3 +116,29 @@ def average_1d(w0, experts):
     """1-D parameters: w_* = w_0 + (1/K) sum_i (w_i - w_0) (App. E, scope)."""
     w0 = np.asarray(w0, dtype=np.float64)
     return w0 + sum(np.asarray(w, dtype=np.float64) - w0 for w in experts) / len(experts)
+
+
+def spectral_diagnostics(w0, w1):
+    """Spectral drift of one matrix from W_0 to W_1 = W_0 + Delta W (Sec. 3):
+    delta_Sigma = |sigma(W_1) - sigma(W_0)|_2 / |W_0|_F,
+    rho_Sigma = |sigma(W_1) - sigma(W_0)|_2 / |Delta W|_F,
+    kappa_spec = (d_out d_in / q) |diag(U_0^T Delta W V_0)|_2^2 / |Delta W|_F^2."""
+    w0 = np.asarray(w0, dtype=np.float64)
+    w1 = np.asarray(w1, dtype=np.float64)
+    dw = w1 - w0
+    u0, s0, v0 = thin_svd(w0)
+    s1 = np.linalg.svd(w1, compute_uv=False)
+    d = np.linalg.norm(s1 - s0)
+    ndw = np.linalg.norm(dw)
+    diag = np.einsum("ik,ij,jk->k", u0, dw, v0)
+    m, n = w0.shape
+    return dict(delta_sigma=d / np.linalg.norm(w0), rho_sigma=d / ndw,
+                kappa_spec=(m * n / min(m, n)) * np.sum(diag ** 2) / ndw ** 2)
+
+
+def spectrum_interpolate(w0, w_rl, alpha):
+    """W~(alpha) = U_RL [(1 - alpha) Sigma_0 + alpha Sigma_RL] V_RL^T (Sec. 3, base spectrum restored
+    at alpha = 0 with the trained frames kept)."""
+    s0 = np.linalg.svd(np.asarray(w0, dtype=np.float64), compute_uv=False)
+    u, s, v = thin_svd(w_rl)
+    return (u * ((1.0 - alpha) * s0 + alpha * s)) @ v.T

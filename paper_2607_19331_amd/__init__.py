@@ -197,6 +197,20 @@ def iso_optimizer_step(frames, dtype, lr, beta1=0.9, beta2=0.999, eps=1e-8, weig
     _check(rc, "iso_optimizer_step")
 
 
+def iso_spectral_diagnostics(entries, dtype, out, ws=None, stream=None):
+    """out: device float64 tensor of 3 * len(entries): {delta_Sigma, rho_Sigma, kappa_spec} per tensor."""
+    wp, wb = _ws(ws)
+    rc = _lib.load().iso_spectral_diagnostics(_table(entries), len(entries), dtype, _ptr(out), wp, wb, _stream(stream))
+    _check(rc, "iso_spectral_diagnostics")
+
+
+def iso_spectrum_interpolate(entries, dtype, alpha, ws=None, stream=None):
+    wp, wb = _ws(ws)
+    rc = _lib.load().iso_spectrum_interpolate(_table(entries), len(entries), dtype, float(alpha), wp, wb,
+                                              _stream(stream))
+    _check(rc, "iso_spectrum_interpolate")
+
+
 def iso_k_from_density(n, num, den):
     return _lib.load().iso_k_from_density(n, num, den)
 

@@ -649,6 +649,26 @@ iso_status iso_blockdiag_project_factors(const iso_tensor* t, int n_t, int K, is
   return run_tsv(t, n_t, K, ta, w + kStatusBytes, ws_bytes - kStatusBytes, (uint32_t*)w, s);
 }
 
+static iso_status spectrum_op(const iso_tensor* t, int n_t, iso_dtype dt, double* out, double alpha, bool write,
+                              void* ws, size_t ws_bytes, void* stream) {
+  Need nd;
+  nd.base = nd.deltas = true;
+  nd.out = write;
+  iso_status st = check_table(t, n_t, 1, dt, nd);
+  if (st != ISO_OK) return st;
+  for (int j = 0; j < n_t; ++j)
+    if (t[j].rows > ISO_SPECTRAL_MAX_DIM || t[j].cols > ISO_SPECTRAL_MAX_DIM) return ISO_ERR_UNSUPPORTED;
+  if (!write && (out == nullptr || ((uintptr_t)out & 7u) != 0)) return out ? ISO_ERR_ALIGNMENT : ISO_ERR_INVALID_ARG;
+  if (write && !(alpha - alpha == 0.0)) return ISO_ERR_INVALID_ARG;
+  if (n_t == 0) return ISO_OK;
+  Layout L = plan(ISO_OP_UPDATE_SPECTRAL, t, n_t, 1, dt);
+  if ((st = check_ws(L, ws, ws_bytes)) != ISO_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* w = (uint8_t*)ws;
+  HIP_TRY(start_call(w, s));
+  return run_spectrum_ops(t, n_t, dt, write ? nullptr : out, alpha, w + L.spectral, (uint32_t*)w, s);
+}
+
 static iso_status check_frames(const iso_frame* f, int n_f) {
   if (n_f < 0 || (n_f > 0 && f == nullptr)) return ISO_ERR_INVALID_ARG;
   for (int e = 0; e < n_f; ++e) {
@@ -691,6 +711,16 @@ iso_status iso_optimizer_step(const iso_frame* f, int n_f, iso_dtype dt, const i
   uint8_t* w = (uint8_t*)ws;
   HIP_TRY(start_call(w, s));
   return run_optimizer(f, n_f, dt, *opt, w + kStatusBytes, (uint32_t*)w, s);
+}
+
+iso_status iso_spectral_diagnostics(const iso_tensor* t, int n_t, iso_dtype dt, double* out, void* ws,
+                                    size_t ws_bytes, void* stream) {
+  return spectrum_op(t, n_t, dt, out, 0.0, false, ws, ws_bytes, stream);
+}
+
+iso_status iso_spectrum_interpolate(const iso_tensor* t, int n_t, iso_dtype dt, double alpha, void* ws,
+                                    size_t ws_bytes, void* stream) {
+  return spectrum_op(t, n_t, dt, nullptr, alpha, true, ws, ws_bytes, stream);
 }
 
 int64_t iso_k_from_density(int64_t n, int64_t num, int64_t den) {

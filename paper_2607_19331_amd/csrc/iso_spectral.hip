@@ -628,6 +628,58 @@ Tables carve_opt_tables(Bump& bp, int n_f) {
   return tb;
 }
 
+// ---- spectral diagnostics and spectrum interpolation ----------------------------------------------
+
+// One workgroup: {delta_Sigma, rho_Sigma, kappa_spec} from the sorted spectra s0, s1 (q), U_0
+// (m x q col-major), P = Delta W V_0 (m x q col-major), W_0 and Delta W (m n entries).
+__global__ void __launch_bounds__(1024) k_diag_final(const double* __restrict__ s0, const double* __restrict__ s1,
+                                                     int64_t q, const double* __restrict__ u0,
+                                                     const double* __restrict__ p, int64_t m, int64_t n,
+                                                     const double* __restrict__ w0, const double* __restrict__ dw,
+                                                     double* __restrict__ out) {
+  __shared__ double red[4][16];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  double d2 = 0.0, nw0 = 0.0, ndw = 0.0, dg = 0.0;
+  for (int64_t k = threadIdx.x; k < q; k += blockDim.x) d2 += (s1[k] - s0[k]) * (s1[k] - s0[k]);
+  for (int64_t e = threadIdx.x; e < m * n; e += blockDim.x) {
+    nw0 += w0[e] * w0[e];
+    ndw += dw[e] * dw[e];
+  }
+  for (int64_t k = wid; k < q; k += nw) {
+    double x = 0.0;
+    for (int64_t i = lane; i < m; i += 64) x += u0[k * m + i] * p[k * m + i];
+    x = wave_sum_f64(x);
+    if (lane == 0) dg += x * x;
+  }
+  d2 = wave_sum_f64(d2);
+  nw0 = wave_sum_f64(nw0);
+  ndw = wave_sum_f64(ndw);
+  dg = wave_sum_f64(dg);
+  if (lane == 0) {
+    red[0][wid] = d2;
+    red[1][wid] = nw0;
+    red[2][wid] = ndw;
+    red[3][wid] = dg;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double a[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int c = 0; c < 4; ++c)
+      for (int w = 0; w < nw; ++w) a[c] += red[c][w];
+    const double dist = sqrt(a[0]);
+    out[0] = dist / sqrt(a[1]);
+    out[1] = dist / sqrt(a[2]);
+    out[2] = ((double)m * (double)n / (double)q) * a[3] / a[2];
+  }
+}
+
+// s = (1 - alpha) s0 + alpha s1
+__global__ void k_mix(double* __restrict__ s, const double* __restrict__ s0, const double* __restrict__ s1, int64_t q,
+                      double alpha) {
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < q; k += (int64_t)gridDim.x * blockDim.x)
+    s[k] = (1.0 - alpha) * s0[k] + alpha * s1[k];
+}
+
 }  // namespace
 
 size_t spectral_workspace_bytes(const iso_tensor* t, int n_t, int K) {
@@ -733,6 +785,57 @@ iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_ad
   OP_TRY(hipStreamSynchronize(s));   // the host staging of the tables ends with this call
   return ISO_OK;
 #undef OP_TRY
+}
+
+iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, double* out, double alpha, uint8_t* ws,
+                            uint32_t* status, hipStream_t s) {
+#define SO_TRY(x)                                \
+  do {                                           \
+    if ((x) != hipSuccess) return ISO_ERR_HIP;   \
+  } while (0)
+  std::vector<uint8_t> host;
+  for (int j = 0; j < n_t; ++j) {
+    const int64_t m = t[j].rows, n = t[j].cols;
+    if (m == 0 || n == 0) continue;
+    const int64_t q = std::min(m, n), r = std::max(m, n);
+    const bool wide = m < n;
+    Bump bp{ws};
+    const Tables tb = carve_tables(bp, 1, 1);
+    const size_t tables_end = bp.off;
+    const Bufs b = carve(bp, m, n, 1);
+    host.assign(tables_end, 0);
+    const auto at = [&](const void* dev) { return host.data() + ((const uint8_t*)dev - ws); };
+    JacobiJob* hj = (JacobiJob*)at(tb.jobs);
+    double** hp = (double**)at(tb.ptrs);
+    for (int i = 0; i < 2; ++i) {
+      hj[i] = JacobiJob{b.ja[i], b.jv[i], r, q};
+      hp[i] = wide ? b.V[i] : b.U[i];
+      hp[2 + i] = wide ? b.U[i] : b.V[i];
+      hp[4 + i] = b.S[i];
+    }
+    SO_TRY(hipMemcpyAsync(ws, host.data(), tables_end, hipMemcpyHostToDevice, s));
+    for (int i = 0; i < 2; ++i)
+      k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.ja[i], t[j].base, i ? t[j].deltas[0] : nullptr, m, n, wide ? 1 : 0,
+                                                  dt);
+    SO_TRY(jacobi_block(tb.jobs, 2, r, q, tb.jst, status, s));
+    k_svd_finalize<<<2, 1024, sizeof(double) * q, s>>>(tb.jobs, tb.ptrs, tb.ptrs + 2, tb.ptrs + 4);
+    if (out != nullptr) {
+      // Delta W and W_0 col-major, P = Delta W V_0
+      k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.G, t[j].deltas[0], nullptr, m, n, 0, dt);
+      k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.Wst, t[j].base, nullptr, m, n, 0, dt);
+      gemm(m, q, n, 1.0, b.G, 1, m, b.V[0], 1, n, 0.0, b.FU, 1, m, s);
+      k_diag_final<<<1, 1024, 0, s>>>(b.S[0], b.S[1], q, b.U[0], b.FU, m, n, b.Wst, b.G, out + 3 * (int64_t)j);
+    } else {
+      k_mix<<<grid_for(q), 256, 0, s>>>(b.P, b.S[0], b.S[1], q, alpha);
+      k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, b.U[1], b.P, m, q);
+      gemm(m, n, q, 1.0, b.FU, 1, m, b.V[1], n, 1, 0.0, b.Wst, 1, m, s);
+      k_store_w<<<grid_for(m * n), 256, 0, s>>>(t[j].out, b.Wst, m, n, dt, status);
+    }
+    SO_TRY(hipGetLastError());
+    SO_TRY(hipStreamSynchronize(s));   // the next tensor reuses the workspace and the staging
+  }
+  return ISO_OK;
+#undef SO_TRY
 }
 
 }  // namespace iso
