@@ -326,15 +326,15 @@ __device__ __forceinline__ void gram_stage(double* ch, const double (&pf)[kGChun
   }
 }
 
-// X[:, cols] <- X[:, cols] Q for nrows rows (X col-major with leading dimension ld); ch is a
+// X[row0:nrows, cols] <- X[row0:nrows, cols] Q (X col-major with leading dimension ld); ch is a
 // kGN x kGP LDS chunk, q the kGN x kGN LDS rotation (col-major).  The next chunk is loaded into
 // registers while the current one is multiplied.
-__device__ __forceinline__ void gram_apply(double* X, int64_t ld, int nrows, const int* gc, int nc, double* ch,
-                                           const double* q) {
+__device__ __forceinline__ void gram_apply(double* X, int64_t ld, int row0, int nrows, const int* gc, int nc,
+                                           double* ch, const double* q) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
   double pf[kGChunkPer];
-  gram_load(pf, X, ld, nrows, gc, nc, 0);
-  for (int k0 = 0; k0 < nrows; k0 += kGN) {
+  gram_load(pf, X, ld, nrows, gc, nc, row0);
+  for (int k0 = row0; k0 < nrows; k0 += kGN) {
     gram_stage(ch, pf);
     __syncthreads();
     if (k0 + kGN < nrows) gram_load(pf, X, ld, nrows, gc, nc, k0 + kGN);
@@ -430,21 +430,188 @@ __global__ void __launch_bounds__(256) k_bjacobi_gram(const JacobiJob* __restric
   jacobi_sweeps<4>(G, Q, kGN, kGN, &s_rot, kGramInnerSweeps);
   __syncthreads();
   // 4. A and V columns times Q (G is no longer needed: its space takes the row chunks)
-  gram_apply(J.a, r, r, gc, nc, ch, Q);
-  gram_apply(J.v, c, c, gc, nc, ch, Q);
+  gram_apply(J.a, r, 0, r, gc, nc, ch, Q);
+  gram_apply(J.v, c, 0, c, gc, nc, ch, Q);
   if (threadIdx.x == 0) st[job].rot = 1;
 }
 
-inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_c, JacobiState* st, uint32_t* status,
-                              hipStream_t s, bool v_given) {
+// ---- the same step with the rows of a block pair split over workgroups ---------------------------
+// Three launches per round: partial Grams of kGSliceRows-row slices of A (one workgroup per pair
+// and slice), the sum of a pair's partials in slice order with the rotation test and the inner
+// sweep (one workgroup per pair; the rotation and a flag go to global memory), and the rotation of
+// every slice of A and of V (one workgroup per pair and slice).  Long columns then take many
+// short workgroups instead of one long one; the result is the same step.
+constexpr int kGSliceRows = 1024;
+
+struct GramPair {     // the block pair a workgroup of round `round` works on, or none
+  int ok, nc;
+  int c0, n0, c1;
+};
+
+__device__ __forceinline__ GramPair gram_pair_of(int c, int pr, int round) {
+  GramPair P{0, 0, 0, 0, 0};
+  const int nb = (c + kGW - 1) / kGW, nbp = nb + (nb & 1);
+  if (round >= nbp - 1 || pr >= nbp / 2) return P;
+  const int bx = (pr == 0) ? 0 : 1 + (pr - 1 + round) % (nbp - 1);
+  const int by = 1 + (nbp - 2 - pr + round) % (nbp - 1);
+  if (bx >= nb || by >= nb) return P;
+  P.c0 = min(bx, by) * kGW;
+  P.c1 = max(bx, by) * kGW;
+  P.n0 = min(kGW, c - P.c0);
+  P.nc = P.n0 + min(kGW, c - P.c1);
+  P.ok = 1;
+  return P;
+}
+
+struct GramSplit {
+  double* part;     // njobs x npairs x nslices x kGN^2: partial Grams
+  double* qrot;     // njobs x npairs x kGN^2: rotations
+  int* need;        // njobs x npairs: 1 if the pair rotates this round
+  int npairs, nslices;
+};
+
+__global__ void __launch_bounds__(256) k_bjg_part(const JacobiJob* __restrict__ jobs, const JacobiState* st,
+                                                  int round, GramSplit S) {
+  __shared__ double ch[kGN * kGP];
+  __shared__ int gc[kGN];
+  const int job = blockIdx.y;
+  if (st[job].done) return;
+  const JacobiJob J = jobs[job];
+  const int r = (int)J.r, c = (int)J.c;
+  const int pr = blockIdx.x / S.nslices, z = blockIdx.x % S.nslices;
+  const GramPair P = gram_pair_of(c, pr, round);
+  const int row0 = z * kGSliceRows, row1 = min(r, row0 + kGSliceRows);
+  if (!P.ok || row0 >= r) return;
+  if (threadIdx.x < kGN) gc[threadIdx.x] = (threadIdx.x < P.n0) ? P.c0 + threadIdx.x : P.c1 + (threadIdx.x - P.n0);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
+  jac_f64x4_t acc[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) acc[t] = jac_f64x4_t{0.0, 0.0, 0.0, 0.0};
+  __syncthreads();
+  double pf[kGChunkPer];
+  gram_load(pf, J.a, r, row1, gc, P.nc, row0);
+  for (int k0 = row0; k0 < row1; k0 += kGN) {
+    gram_stage(ch, pf);
+    __syncthreads();
+    if (k0 + kGN < row1) gram_load(pf, J.a, r, row1, gc, P.nc, k0 + kGN);
+#pragma unroll 4
+    for (int s = 0; s < kGN / 4; ++s) {
+      const double a = ch[(16 * w + ln) * kGP + 4 * s + g];
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, ch[(16 * t + ln) * kGP + 4 * s + g], acc[t], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+  double* out = S.part + (((size_t)job * S.npairs + pr) * S.nslices + z) * (kGN * kGN);
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) out[(16 * t + ln) * kGN + 16 * w + g + 4 * v] = acc[t][v];
+}
+
+__global__ void __launch_bounds__(256) k_bjg_rot(const JacobiJob* __restrict__ jobs, JacobiState* st, int round,
+                                                 GramSplit S) {
+  __shared__ double G[kGN * kGN];
+  __shared__ double Q[kGN * kGN];
+  __shared__ int s_need, s_rot;
+  const int job = blockIdx.y, pr = blockIdx.x;
+  if (st[job].done) return;
+  const JacobiJob J = jobs[job];
+  const int r = (int)J.r, c = (int)J.c;
+  const GramPair P = gram_pair_of(c, pr, round);
+  int* need = S.need + (size_t)job * S.npairs + pr;
+  if (!P.ok) {
+    if (threadIdx.x == 0 && pr < S.npairs) *need = 0;
+    return;
+  }
+  const int ns = (r + kGSliceRows - 1) / kGSliceRows;
+  const double* part = S.part + ((size_t)job * S.npairs + pr) * S.nslices * (kGN * kGN);
+  for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
+    double x = 0.0;
+    for (int z = 0; z < ns; ++z) x += part[(size_t)z * (kGN * kGN) + e];
+    G[e] = x;
+  }
+  if (threadIdx.x == 0) { s_need = 0; s_rot = 0; }
+  __syncthreads();
+  const double tol = (double)r * 1.1102230246251565e-16;
+  for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
+    const int i = e % kGN, j = e / kGN;
+    if (i < j && j < P.nc) {
+      const double gij = G[j * kGN + i];
+      if (fabs(gij) > tol * sqrt(G[i * kGN + i] * G[j * kGN + j]) && gij != 0.0) s_need = 1;
+    }
+  }
+  for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) Q[e] = ((e % kGN) == (e / kGN)) ? 1.0 : 0.0;
+  __syncthreads();
+  if (threadIdx.x == 0) *need = s_need;
+  if (!s_need) return;
+  jacobi_sweeps<4>(G, Q, kGN, kGN, &s_rot, kGramInnerSweeps);
+  __syncthreads();
+  double* q = S.qrot + ((size_t)job * S.npairs + pr) * (kGN * kGN);
+  for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) q[e] = Q[e];
+  if (threadIdx.x == 0) st[job].rot = 1;
+}
+
+__global__ void __launch_bounds__(256) k_bjg_apply(const JacobiJob* __restrict__ jobs, const JacobiState* st,
+                                                   int round, GramSplit S, int slices_a, int slices_v) {
+  __shared__ double ch[kGN * kGP];
+  __shared__ double Q[kGN * kGN];
+  __shared__ int gc[kGN];
+  const int job = blockIdx.y;
+  if (st[job].done) return;
+  const JacobiJob J = jobs[job];
+  const int r = (int)J.r, c = (int)J.c;
+  const int per = slices_a + slices_v;
+  const int pr = blockIdx.x / per, z = blockIdx.x % per;
+  const GramPair P = gram_pair_of(c, pr, round);
+  if (!P.ok || S.need[(size_t)job * S.npairs + pr] == 0) return;
+  const bool on_a = z < slices_a;
+  const int rows = on_a ? r : c;
+  const int row0 = (on_a ? z : z - slices_a) * kGSliceRows, row1 = min(rows, row0 + kGSliceRows);
+  if (row0 >= rows) return;
+  if (threadIdx.x < kGN) gc[threadIdx.x] = (threadIdx.x < P.n0) ? P.c0 + threadIdx.x : P.c1 + (threadIdx.x - P.n0);
+  const double* q = S.qrot + ((size_t)job * S.npairs + pr) * (kGN * kGN);
+  for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) Q[e] = q[e];
+  __syncthreads();
+  gram_apply(on_a ? J.a : J.v, rows, row0, row1, gc, P.nc, ch, Q);
+}
+
+// Scratch of the split step for njobs jobs of at most max_r rows and max_c columns.
+inline size_t gram_split_bytes(int njobs, int64_t max_r, int64_t max_c) {
+  const int64_t nb = (max_c + kGW - 1) / kGW, np = (nb + (nb & 1)) / 2;
+  const int64_t ns = (max_r + kGSliceRows - 1) / kGSliceRows;
+  return ((size_t)njobs * np * (size_t)(ns + 1) * kGN * kGN) * sizeof(double) + (size_t)njobs * np * sizeof(int) + 256;
+}
+
+inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_r, int64_t max_c, JacobiState* st,
+                              uint32_t* status, hipStream_t s, bool v_given, void* scratch) {
   const unsigned gb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_c * max_c + 255) / 256, 4096));
   k_jacobi_begin<<<dim3(gb, (unsigned)njobs), 256, 0, s>>>(jobs, st, v_given ? 1 : 0);
   const int nb = (int)((max_c + kGW - 1) / kGW), nbp = nb + (nb & 1);
   const dim3 g((unsigned)std::max(1, nbp / 2), (unsigned)njobs);
+  GramSplit S{};
+  if (scratch != nullptr) {
+    S.npairs = std::max(1, nbp / 2);
+    S.nslices = (int)((max_r + kGSliceRows - 1) / kGSliceRows);
+    S.part = (double*)scratch;
+    S.qrot = S.part + (size_t)njobs * S.npairs * S.nslices * kGN * kGN;
+    S.need = (int*)(S.qrot + (size_t)njobs * S.npairs * kGN * kGN);
+  }
+  const int slices_a = S.nslices, slices_v = (int)((max_c + kGSliceRows - 1) / kGSliceRows);
   std::vector<JacobiState> h(njobs);
   for (int sweep = 0; sweep < kJacobiMaxSweeps;) {
     for (int b = 0; b < kJacobiCheckSweeps && sweep < kJacobiMaxSweeps; ++b, ++sweep) {
-      for (int round = 0; round < nbp - 1; ++round) k_bjacobi_gram<<<g, 256, 0, s>>>(jobs, st, round);
+      for (int round = 0; round < nbp - 1; ++round) {
+        if (scratch == nullptr) {
+          k_bjacobi_gram<<<g, 256, 0, s>>>(jobs, st, round);
+        } else {
+          k_bjg_part<<<dim3((unsigned)(S.npairs * S.nslices), (unsigned)njobs), 256, 0, s>>>(jobs, st, round, S);
+          k_bjg_rot<<<dim3((unsigned)S.npairs, (unsigned)njobs), 256, 0, s>>>(jobs, st, round, S);
+          k_bjg_apply<<<dim3((unsigned)(S.npairs * (slices_a + slices_v)), (unsigned)njobs), 256, 0, s>>>(
+              jobs, st, round, S, slices_a, slices_v);
+        }
+      }
       k_jacobi_sweep_end<<<1, 256, 0, s>>>(st, njobs);
     }
     hipError_t e = hipMemcpyAsync(h.data(), st, sizeof(JacobiState) * njobs, hipMemcpyDeviceToHost, s);
@@ -479,9 +646,9 @@ inline void jacobi_block_shape(int64_t max_r, int64_t max_c, int64_t* width, int
 // kJacobiCheckSweeps sweeps.  v_given: each job's V already holds an orthogonal starting factor
 // (A then being the matrix times it), which the rotations multiply.
 inline hipError_t jacobi_block(const JacobiJob* jobs, int njobs, int64_t max_r, int64_t max_c, JacobiState* st,
-                               uint32_t* status, hipStream_t s, bool v_given = false) {
+                               uint32_t* status, hipStream_t s, bool v_given = false, void* split = nullptr) {
   const int w = (int)std::min<int64_t>(16, (int64_t)(kBJacobiLds / (16 * (size_t)(max_r + max_c))));
-  if (w < 16) return jacobi_gram(jobs, njobs, max_c, st, status, s, v_given);
+  if (w < 16) return jacobi_gram(jobs, njobs, max_r, max_c, st, status, s, v_given, split);
   const size_t lds = sizeof(double) * 2 * (size_t)w * (size_t)(max_r + max_c);
   const unsigned gb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_c * max_c + 255) / 256, 4096));
   k_jacobi_begin<<<dim3(gb, (unsigned)njobs), 256, 0, s>>>(jobs, st, v_given ? 1 : 0);

@@ -463,6 +463,12 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
   const size_t tables_end = bp.off;
   std::vector<Bufs> bs(nm);
   for (int e = 0; e < nm; ++e) bs[e] = carve(bp, t[ids[e]].rows, t[ids[e]].cols, K);
+  int64_t split_r = 1, split_q = 1;
+  for (int e = 0; e < nm; ++e) {
+    split_r = std::max(split_r, std::max(t[ids[e]].rows, t[ids[e]].cols));
+    split_q = std::max(split_q, std::min(t[ids[e]].rows, t[ids[e]].cols));
+  }
+  void* split = bp.take<uint8_t>((int64_t)gram_split_bytes(nsvd, split_r, split_q));
   // host image of the tables (same layout as on the device): the nm (K+1) SVDs (matrix e's W_0 at
   // e, its W_i at nm + e K + i - 1) with their finalize pointers (left, right, singular values);
   // the polar jobs (matrix e's U side at 2 e, V side at 2 e + 1) with their GEMM tables
@@ -532,9 +538,9 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
                                                            x.cols, x.rows < x.cols ? 1 : 0, dt);
   }
   if (!warm) {
-    SP_TRY(jacobi_block(tb.jobs, nsvd, svd_r, svd_c, tb.jst, status, s));
+    SP_TRY(jacobi_block(tb.jobs, nsvd, svd_r, svd_c, tb.jst, status, s, false, split));
   } else {
-    SP_TRY(jacobi_block(tb.jobs, nm, svd_r, svd_c, tb.jst, status, s));
+    SP_TRY(jacobi_block(tb.jobs, nm, svd_r, svd_c, tb.jst, status, s, false, split));
     for (int e = 0; e < nm; ++e) {
       const iso_tensor& x = t[ids[e]];
       const int64_t q = std::min(x.rows, x.cols);
@@ -548,7 +554,7 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
     }
     k_gemm_jobs<<<dim3((unsigned)((svd_r + GT - 1) / GT), (unsigned)((svd_c + GT - 1) / GT), (unsigned)(nm * K)), 256,
                   0, s>>>(tb.wgj);
-    SP_TRY(jacobi_block(tb.jobs + nm, nm * K, svd_r, svd_c, tb.jst + nm, status, s, true));
+    SP_TRY(jacobi_block(tb.jobs + nm, nm * K, svd_r, svd_c, tb.jst + nm, status, s, true, split));
   }
   k_svd_finalize<<<nsvd, 1024, sizeof(double) * svd_c, s>>>(tb.jobs, tb.ptrs, tb.ptrs + nsvd, tb.ptrs + 2 * nsvd);
   // 2 - 6 per matrix; the polar arguments go to the first iterate buffers
@@ -686,7 +692,13 @@ size_t spectral_workspace_bytes(const iso_tensor* t, int n_t, int K) {
   size_t most = 0;
   for (const auto& ids : spectral_batches(t, n_t, K)) {
     size_t b = tables_bytes((int)ids.size(), K);
-    for (int j : ids) b += matrix_bytes(t[j].rows, t[j].cols, K);
+    int64_t r = 1, q = 1;
+    for (int j : ids) {
+      b += matrix_bytes(t[j].rows, t[j].cols, K);
+      r = std::max(r, std::max(t[j].rows, t[j].cols));
+      q = std::max(q, std::min(t[j].rows, t[j].cols));
+    }
+    b += align_up(gram_split_bytes((int)ids.size() * (K + 1), r, q), 256);
     most = std::max(most, b);
   }
   return most;
@@ -803,6 +815,7 @@ iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, double* 
     const Tables tb = carve_tables(bp, 1, 1);
     const size_t tables_end = bp.off;
     const Bufs b = carve(bp, m, n, 1);
+    void* split = bp.take<uint8_t>((int64_t)gram_split_bytes(2, r, q));
     host.assign(tables_end, 0);
     const auto at = [&](const void* dev) { return host.data() + ((const uint8_t*)dev - ws); };
     JacobiJob* hj = (JacobiJob*)at(tb.jobs);
@@ -817,7 +830,7 @@ iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, double* 
     for (int i = 0; i < 2; ++i)
       k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.ja[i], t[j].base, i ? t[j].deltas[0] : nullptr, m, n, wide ? 1 : 0,
                                                   dt);
-    SO_TRY(jacobi_block(tb.jobs, 2, r, q, tb.jst, status, s));
+    SO_TRY(jacobi_block(tb.jobs, 2, r, q, tb.jst, status, s, false, split));
     k_svd_finalize<<<2, 1024, sizeof(double) * q, s>>>(tb.jobs, tb.ptrs, tb.ptrs + 2, tb.ptrs + 4);
     if (out != nullptr) {
       // Delta W and W_0 col-major, P = Delta W V_0
