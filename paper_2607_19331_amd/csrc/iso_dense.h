@@ -556,7 +556,6 @@ __global__ void __launch_bounds__(256) k_bjg_rot(const JacobiJob* __restrict__ j
 __global__ void __launch_bounds__(256) k_bjg_apply(const JacobiJob* __restrict__ jobs, const JacobiState* st,
                                                    int round, GramSplit S, int slices_a, int slices_v) {
   __shared__ double ch[kGN * kGP];
-  __shared__ double Q[kGN * kGN];
   __shared__ int gc[kGN];
   const int job = blockIdx.y;
   if (st[job].done) return;
@@ -572,9 +571,42 @@ __global__ void __launch_bounds__(256) k_bjg_apply(const JacobiJob* __restrict__
   if (row0 >= rows) return;
   if (threadIdx.x < kGN) gc[threadIdx.x] = (threadIdx.x < P.n0) ? P.c0 + threadIdx.x : P.c1 + (threadIdx.x - P.n0);
   const double* q = S.qrot + ((size_t)job * S.npairs + pr) * (kGN * kGN);
-  for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) Q[e] = q[e];
+  // this lane's MFMA operands of Q (the same for every chunk) in registers
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
+  double qr[kGN / 4][4];
+#pragma unroll
+  for (int s4 = 0; s4 < kGN / 4; ++s4)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) qr[s4][t] = q[(16 * t + ln) * kGN + 4 * s4 + g];
   __syncthreads();
-  gram_apply(on_a ? J.a : J.v, rows, row0, row1, gc, P.nc, ch, Q);
+  double* X = on_a ? J.a : J.v;
+  double pf[kGChunkPer];
+  gram_load(pf, X, rows, row1, gc, P.nc, row0);
+  for (int k0 = row0; k0 < row1; k0 += kGN) {
+    gram_stage(ch, pf);
+    __syncthreads();
+    if (k0 + kGN < row1) gram_load(pf, X, rows, row1, gc, P.nc, k0 + kGN);
+    jac_f64x4_t acc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[t] = jac_f64x4_t{0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int s4 = 0; s4 < kGN / 4; ++s4) {
+      const double a = ch[(4 * s4 + g) * kGP + 16 * w + ln];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, qr[s4][t], acc[t], 0, 0, 0);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) ch[(16 * t + ln) * kGP + 16 * w + g + 4 * v] = acc[t][v];
+    __syncthreads();
+    for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
+      const int l = e / kGN, i = e % kGN;
+      if (l < P.nc && k0 + i < row1) X[(int64_t)gc[l] * rows + k0 + i] = ch[l * kGP + i];
+    }
+    __syncthreads();
+  }
 }
 
 // Scratch of the split step for njobs jobs of at most max_r rows and max_c columns.
