@@ -510,7 +510,8 @@ __global__ void __launch_bounds__(256) k_bjg_part(const JacobiJob* __restrict__ 
     for (int v = 0; v < 4; ++v) out[(16 * t + ln) * kGN + 16 * w + g + 4 * v] = acc[t][v];
 }
 
-__global__ void __launch_bounds__(256) k_bjg_rot(const JacobiJob* __restrict__ jobs, JacobiState* st, int round,
+// 512 threads: 32 sixteen-lane rows, one per column pair of the 64 x 64 inner sweep
+__global__ void __launch_bounds__(512) k_bjg_rot(const JacobiJob* __restrict__ jobs, JacobiState* st, int round,
                                                  GramSplit S) {
   __shared__ double G[kGN * kGN];
   __shared__ double Q[kGN * kGN];
@@ -639,7 +640,7 @@ inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_r, i
           k_bjacobi_gram<<<g, 256, 0, s>>>(jobs, st, round);
         } else {
           k_bjg_part<<<dim3((unsigned)(S.npairs * S.nslices), (unsigned)njobs), 256, 0, s>>>(jobs, st, round, S);
-          k_bjg_rot<<<dim3((unsigned)S.npairs, (unsigned)njobs), 256, 0, s>>>(jobs, st, round, S);
+          k_bjg_rot<<<dim3((unsigned)S.npairs, (unsigned)njobs), 512, 0, s>>>(jobs, st, round, S);
           k_bjg_apply<<<dim3((unsigned)(S.npairs * (slices_a + slices_v)), (unsigned)njobs), 256, 0, s>>>(
               jobs, st, round, S, slices_a, slices_v);
         }
