@@ -92,3 +92,50 @@ def test_joint_selection_descriptors_and_merge():
             continue
         ref = ties.merge_unit(u.base, u.deltas, "bf16", "ties", masks=want[j])["out"]
         assert np.array_equal(from_dev(u.dout, u.n, "bf16"), ref), j
+
+
+def test_whole_layer_as_one_group():
+    """The single-layer workload (seven bf16 matrices, K = 2) selected as one whole-model delta with
+    density 0.1 of the layer: per delta the members' shares add up to the group's count, and the
+    descriptors of q_proj and down_proj (first and last member) give exactly the oracle's joint
+    masks; the merged weights of down_proj match the oracle bit for bit."""
+    import torch
+    import synth
+    wl = synth.workload("layer")
+    K = wl.K
+    n_all = sum(s.numel for s in wl.tensors)
+    k_all = iso.iso_k_from_density(n_all, wl.density.numerator, wl.density.denominator)
+    units = []
+    for t, spec in enumerate(wl.tensors):
+        base = synth.fill_host(wl, t, 0)
+        ds = [synth.fill_host(wl, t, 1 + i) for i in range(K)]
+        units.append(Unit(spec.rows, spec.cols, base, ds, "bf16", k_all if t == 0 else 0))
+    es = []
+    for u in units:
+        e = u.entry()
+        e.group = 7
+        es.append(e)
+    say(f"groups: whole layer as one group, k = {k_all} of {n_all}")
+    ws = iso.workspace(iso.OP_TOPK, es, K, iso.BF16)
+    desc = iso.desc_tensor(len(es) * K)
+    iso.iso_topk_mask(es, K, iso.BF16, desc, ws=ws)
+    assert iso.iso_read_device_status(ws) == 0
+    d = iso.decode_desc(desc)
+    for i in range(K):
+        assert sum(d[j * K + i][2] + d[j * K + i][3] for j in range(len(es))) == k_all
+        want = ties.topk_mask_joint([u.deltas[i] for u in units], k_all, "bf16")
+        for j in (0, len(units) - 1):
+            t_key, _, n_above, quota, cutoff = d[j * K + i]
+            got = ties.mask_from_descriptor(units[j].deltas[i], (t_key, n_above, quota, cutoff), "bf16")
+            assert np.array_equal(got, want[j]), (j, i)
+        if i == 0:
+            masks_last = [None] * K
+        masks_last[i] = want[-1]
+        del want
+    wsu = iso.workspace(iso.OP_UPDATE_FUSED_SELECT, es, K, iso.BF16)
+    iso.iso_update(es, K, iso.BF16, iso.UPDATE_FUSED, merge=iso.MERGE_TIES, lam=1.0, desc=None, ws=wsu)
+    assert iso.iso_read_device_status(wsu) == 0
+    torch.cuda.synchronize()
+    u = units[-1]
+    ref = ties.merge_unit(u.base, u.deltas, "bf16", "ties", masks=masks_last)["out"]
+    assert np.array_equal(from_dev(u.dout, u.n, "bf16"), ref)
