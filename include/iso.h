@@ -13,8 +13,10 @@
  *  - Storage types: ISO_F32 (IEEE binary32) or ISO_BF16 (bfloat16 bits).  One
  *    call uses one storage type for base, deltas and the weight output.
  *  - All data pointers are device memory owned by the caller; every one must
- *    be 16-byte aligned (ISO_ERR_ALIGNMENT otherwise).  N need not be a
- *    multiple of anything.
+ *    be 16-byte aligned (ISO_ERR_ALIGNMENT otherwise), except the binary64
+ *    arrays of iso_frame and iso_spectral_diagnostics (8-byte) and the
+ *    gradient and weight of iso_frame (4-byte).  N need not be a multiple of
+ *    anything.
  *  - ws / ws_bytes: caller-allocated device workspace of at least
  *    iso_workspace_size(op, ...) bytes, 256-byte aligned, that must stay
  *    alive until the stream work has finished.  Its contents on entry do not
@@ -33,9 +35,16 @@
  * operators): every merged coordinate is formed in binary64 -- sums start
  * at +0.0 and add the terms in expert order, means divide that sum by the
  * count, then u = lambda*t and v = w0 + u -- and v is rounded ONCE to the
- * storage type (round to nearest even; binary64 -> bf16 never passes through
- * binary32).  The sign used by the TIES election is the sign of the exact
- * real sum.
+ * storage type (round to nearest even): the bf16 output is the correct
+ * rounding of v, never a double rounding through binary32.  The sign used by
+ * the TIES election is the sign of the exact real sum.
+ *
+ * Entry points: TopKMask (iso_topk_mask, joint over tensor groups), sign
+ * election (iso_sign_elect), TIES / TA / RAM merges (iso_merge), the update
+ * theta_0 + lambda tau and ISO-Merger (iso_update), TSV (iso_blockdiag_project,
+ * iso_blockdiag_project_factors), the ISO-AdamW step (iso_optimizer_step) and
+ * the spectral diagnostics of Sec. 3 (iso_spectral_diagnostics,
+ * iso_spectrum_interpolate).
  */
 #ifndef ISO_H
 #define ISO_H
