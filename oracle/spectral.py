@@ -142,3 +142,43 @@ def spectrum_interpolate(w0, w_rl, alpha):
     s0 = np.linalg.svd(np.asarray(w0, dtype=np.float64), compute_uv=False)
     u, s, v = thin_svd(w_rl)
     return (u * ((1.0 - alpha) * s0 + alpha * s)) @ v.T
+
+
+def truncation_rank(q, rank_frac):
+    """r = max(1, floor(rank_frac q)), the integer truncation rank of the rank-sensitivity study."""
+    return max(1, int(math.floor(rank_frac * q)))
+
+
+def transport_ratios(w_in, w_end, rank_frac=0.9):
+    """Unexplained-update ratios of one transition W_j -> W_i (Sec. 3, Prop. 3.1), with W_j = w_in the
+    incoming checkpoint and W_i = w_end the learned endpoint, both truncated to their top-r SVD:
+      W_mix = P_j W_i^(r) Q_j,  W_L = P_j W_i^(r),  W_R = W_i^(r) Q_j,  W_iso = U_i^(r) Sigma_j^(r) V_i^(r)T,
+      u_h = |W_i^(r) - W_h|_F / |W_i^(r) - W_j^(r)|_F   (NaN when the denominator is zero),
+    with P_j = U_j^(r) U_j^(r)T and Q_j = V_j^(r) V_j^(r)T.  Also returns the rank-r boundary gap,
+    min over both endpoints of sigma_r - sigma_{r+1} (sigma_{q+1} := 0): the transition is admissible
+    when it is positive."""
+    w_in = np.asarray(w_in, dtype=np.float64)
+    w_end = np.asarray(w_end, dtype=np.float64)
+    q = min(w_in.shape)
+    r = truncation_rank(q, rank_frac)
+    uj, sj, vj = thin_svd(w_in)
+    ui, si, vi = thin_svd(w_end)
+    wi = (ui[:, :r] * si[:r]) @ vi[:, :r].T
+    wj = (uj[:, :r] * sj[:r]) @ vj[:, :r].T
+    p = uj[:, :r] @ uj[:, :r].T
+    qm = vj[:, :r] @ vj[:, :r].T
+    recon = {
+        "mix": p @ wi @ qm,
+        "L": p @ wi,
+        "R": wi @ qm,
+        "iso": (ui[:, :r] * sj[:r]) @ vi[:, :r].T,
+    }
+    den = np.linalg.norm(wi - wj)
+    u = {h: (np.linalg.norm(wi - x) / den if den > 0 else math.nan) for h, x in recon.items()}
+
+    def gap(s):
+        return s[r - 1] - (s[r] if r < q else 0.0)
+
+    u["gap"] = min(gap(sj), gap(si))
+    u["rank"] = r
+    return u
