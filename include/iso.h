@@ -14,9 +14,9 @@
  *    call uses one storage type for base, deltas and the weight output.
  *  - All data pointers are device memory owned by the caller; every one must
  *    be 16-byte aligned (ISO_ERR_ALIGNMENT otherwise), except the binary64
- *    arrays of iso_frame and iso_spectral_diagnostics (8-byte) and the
- *    gradient and weight of iso_frame (4-byte).  N need not be a multiple of
- *    anything.
+ *    arrays of iso_frame, iso_spectral_diagnostics and iso_transport_ratios
+ *    (8-byte) and the gradient and weight of iso_frame (4-byte).  N need not
+ *    be a multiple of anything.
  *  - ws / ws_bytes: caller-allocated device workspace of at least
  *    iso_workspace_size(op, ...) bytes, 256-byte aligned, that must stay
  *    alive until the stream work has finished.  Its contents on entry do not
@@ -44,7 +44,7 @@
  * theta_0 + lambda tau and ISO-Merger (iso_update), TSV (iso_blockdiag_project,
  * iso_blockdiag_project_factors), the ISO-AdamW step (iso_optimizer_step) and
  * the spectral diagnostics of Sec. 3 (iso_spectral_diagnostics,
- * iso_spectrum_interpolate).
+ * iso_spectrum_interpolate, iso_transport_ratios).
  */
 #ifndef ISO_H
 #define ISO_H
@@ -236,6 +236,27 @@ iso_status iso_spectral_diagnostics(const iso_tensor* t, int n_t, iso_dtype dt, 
  */
 iso_status iso_spectrum_interpolate(const iso_tensor* t, int n_t, iso_dtype dt, double alpha, void* ws,
                                     size_t ws_bytes, void* stream);
+
+/*
+ * Unexplained-update ratios (Sec. 3, Prop. 3.1), per tensor, in binary64: the
+ * transition from the incoming checkpoint W_j = base to the learned endpoint
+ * W_i = base + deltas[0], both truncated to their top-r SVD with
+ * r = max(1, floor(rank_frac q)), q = min(rows, cols), 0 < rank_frac <= 1
+ * (the paper's main text takes 0.9).  With P_j = U_j^(r) U_j^(r)T and
+ * Q_j = V_j^(r) V_j^(r)T the reconstructions are W_mix = P_j W_i^(r) Q_j,
+ * W_L = P_j W_i^(r), W_R = W_i^(r) Q_j and W_iso = U_i^(r) Sigma_j^(r) V_i^(r)T,
+ * and u_h = |W_i^(r) - W_h|_F / |W_i^(r) - W_j^(r)|_F (u_iso in its closed form
+ * |sigma_i^(r) - sigma_j^(r)|_2 / |W_i^(r) - W_j^(r)|_F).  out is a device
+ * array of 5 n_t doubles, per tensor {u_mix, u_L, u_R, u_iso, gap}, where gap
+ * = min over both endpoints of sigma_r - sigma_{r+1} (sigma_{q+1} := 0): the
+ * transition is admissible (its top-r projectors well defined) only when gap
+ * > 0, which the caller checks; the ratios are NaN when W_i^(r) = W_j^(r).
+ * Tensors with no elements are skipped (their entries of out are not
+ * written).  Workspace and size limits of iso_spectral_diagnostics;
+ * ISO_ERR_INVALID_ARG for rank_frac outside (0, 1].
+ */
+iso_status iso_transport_ratios(const iso_tensor* t, int n_t, iso_dtype dt, double rank_frac, double* out, void* ws,
+                                size_t ws_bytes, void* stream);
 
 /*
  * ISO-Optimizer step with AdamW as the base rule (ISO-AdamW, Sec. 4.3): one

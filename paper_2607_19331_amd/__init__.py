@@ -211,6 +211,15 @@ def iso_spectrum_interpolate(entries, dtype, alpha, ws=None, stream=None):
     _check(rc, "iso_spectrum_interpolate")
 
 
+def iso_transport_ratios(entries, dtype, rank_frac, out, ws=None, stream=None):
+    """out: device float64 tensor of 5 * len(entries): {u_mix, u_L, u_R, u_iso, gap} per tensor, for the
+    transition base -> base + deltas[0] truncated to rank max(1, floor(rank_frac q))."""
+    wp, wb = _ws(ws)
+    rc = _lib.load().iso_transport_ratios(_table(entries), len(entries), dtype, float(rank_frac), _ptr(out), wp, wb,
+                                          _stream(stream))
+    _check(rc, "iso_transport_ratios")
+
+
 def iso_k_from_density(n, num, den):
     return _lib.load().iso_k_from_density(n, num, den)
 

@@ -649,8 +649,9 @@ iso_status iso_blockdiag_project_factors(const iso_tensor* t, int n_t, int K, is
   return run_tsv(t, n_t, K, ta, w + kStatusBytes, ws_bytes - kStatusBytes, (uint32_t*)w, s);
 }
 
-static iso_status spectrum_op(const iso_tensor* t, int n_t, iso_dtype dt, double* out, double alpha, bool write,
+static iso_status spectrum_op(const iso_tensor* t, int n_t, iso_dtype dt, SpectrumOp op, double* out, double param,
                               void* ws, size_t ws_bytes, void* stream) {
+  const bool write = op == SpectrumOp::kInterpolate;
   Need nd;
   nd.base = nd.deltas = true;
   nd.out = write;
@@ -659,14 +660,15 @@ static iso_status spectrum_op(const iso_tensor* t, int n_t, iso_dtype dt, double
   for (int j = 0; j < n_t; ++j)
     if (t[j].rows > ISO_SPECTRAL_MAX_DIM || t[j].cols > ISO_SPECTRAL_MAX_DIM) return ISO_ERR_UNSUPPORTED;
   if (!write && (out == nullptr || ((uintptr_t)out & 7u) != 0)) return out ? ISO_ERR_ALIGNMENT : ISO_ERR_INVALID_ARG;
-  if (write && !(alpha - alpha == 0.0)) return ISO_ERR_INVALID_ARG;
+  if (write && !(param - param == 0.0)) return ISO_ERR_INVALID_ARG;
+  if (op == SpectrumOp::kTransport && !(param > 0.0 && param <= 1.0)) return ISO_ERR_INVALID_ARG;
   if (n_t == 0) return ISO_OK;
   Layout L = plan(ISO_OP_UPDATE_SPECTRAL, t, n_t, 1, dt);
   if ((st = check_ws(L, ws, ws_bytes)) != ISO_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   uint8_t* w = (uint8_t*)ws;
   HIP_TRY(start_call(w, s));
-  return run_spectrum_ops(t, n_t, dt, write ? nullptr : out, alpha, w + L.spectral, (uint32_t*)w, s);
+  return run_spectrum_ops(t, n_t, dt, op, out, param, w + L.spectral, (uint32_t*)w, s);
 }
 
 static iso_status check_frames(const iso_frame* f, int n_f) {
@@ -715,12 +717,17 @@ iso_status iso_optimizer_step(const iso_frame* f, int n_f, iso_dtype dt, const i
 
 iso_status iso_spectral_diagnostics(const iso_tensor* t, int n_t, iso_dtype dt, double* out, void* ws,
                                     size_t ws_bytes, void* stream) {
-  return spectrum_op(t, n_t, dt, out, 0.0, false, ws, ws_bytes, stream);
+  return spectrum_op(t, n_t, dt, SpectrumOp::kDiagnostics, out, 0.0, ws, ws_bytes, stream);
 }
 
 iso_status iso_spectrum_interpolate(const iso_tensor* t, int n_t, iso_dtype dt, double alpha, void* ws,
                                     size_t ws_bytes, void* stream) {
-  return spectrum_op(t, n_t, dt, nullptr, alpha, true, ws, ws_bytes, stream);
+  return spectrum_op(t, n_t, dt, SpectrumOp::kInterpolate, nullptr, alpha, ws, ws_bytes, stream);
+}
+
+iso_status iso_transport_ratios(const iso_tensor* t, int n_t, iso_dtype dt, double rank_frac, double* out, void* ws,
+                                size_t ws_bytes, void* stream) {
+  return spectrum_op(t, n_t, dt, SpectrumOp::kTransport, out, rank_frac, ws, ws_bytes, stream);
 }
 
 int64_t iso_k_from_density(int64_t n, int64_t num, int64_t den) {

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <cmath>
+
 #include "iso.h"
 
 namespace iso {
@@ -15,9 +17,19 @@ struct SpectralArgs {
 
 size_t spectral_workspace_bytes(const iso_tensor* t, int n_t, int K);
 size_t optimizer_workspace_bytes(const iso_frame* f, int n_f);
-// diagnostics (out != nullptr) or spectrum interpolation (alpha) of each tensor, one at a time
-iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, double* out, double alpha, uint8_t* ws,
-                            uint32_t* status, hipStream_t s);
+enum class SpectrumOp { kDiagnostics, kInterpolate, kTransport };
+
+// Truncation rank r = max(1, floor(frac q)) of the unexplained-update ratios.
+inline int64_t transport_rank(int64_t q, double frac) {
+  const int64_t r = (int64_t)std::floor(frac * (double)q);
+  return r < 1 ? 1 : r;
+}
+
+// Per tensor, one at a time: drift diagnostics (3 doubles of out), spectrum interpolation
+// (param = alpha, writes the tensor's out) or unexplained-update ratios (param = rank
+// fraction, 5 doubles of out).
+iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, SpectrumOp op, double* out, double param,
+                            uint8_t* ws, uint32_t* status, hipStream_t s);
 iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_adamw& o, uint8_t* ws,
                          uint32_t* status, hipStream_t s);
 iso_status run_spectral(const iso_tensor* t, int n_t, int K, iso_dtype dt, const SpectralArgs& a, uint8_t* ws,

@@ -679,6 +679,42 @@ __global__ void __launch_bounds__(1024) k_diag_final(const double* __restrict__ 
   }
 }
 
+// out[0] = |a - b|_F^2 over len entries (one workgroup, fixed summation order).
+__global__ void __launch_bounds__(1024) k_sqdist(const double* __restrict__ a, const double* __restrict__ b,
+                                                 int64_t len, double* __restrict__ out) {
+  __shared__ double red[16];
+  double x = 0.0;
+  for (int64_t e = threadIdx.x; e < len; e += blockDim.x) {
+    const double d = a[e] - b[e];
+    x += d * d;
+  }
+  x = wave_sum_f64(x);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double t = 0.0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) t += red[w];
+    out[0] = t;
+  }
+}
+
+// Unexplained-update ratios from the squared residuals held in out[0..3] (|W_i^(r) - W_j^(r)|^2,
+// then those of the mix, L and R reconstructions) and the two spectra s0 (incoming W_j) and s1
+// (endpoint W_i): out = {u_mix, u_L, u_R, u_iso, gap}.  u_iso takes the closed form of Prop. 3.1,
+// |sigma_i^(r) - sigma_j^(r)| / |W_i^(r) - W_j^(r)|.  One thread.
+__global__ void k_transport_final(const double* __restrict__ s0, const double* __restrict__ s1, int64_t q, int64_t r,
+                                  double* __restrict__ out) {
+  if (threadIdx.x != 0) return;
+  double ds = 0.0;
+  for (int64_t k = 0; k < r; ++k) ds += (s1[k] - s0[k]) * (s1[k] - s0[k]);
+  const double den = sqrt(out[0]);
+  const double nan = __builtin_nan("");
+  const double e[4] = {sqrt(out[1]), sqrt(out[2]), sqrt(out[3]), sqrt(ds)};
+  for (int h = 0; h < 4; ++h) out[h] = den > 0.0 ? e[h] / den : nan;
+  const double g0 = s0[r - 1] - (r < q ? s0[r] : 0.0), g1 = s1[r - 1] - (r < q ? s1[r] : 0.0);
+  out[4] = fmin(g0, g1);
+}
+
 // s = (1 - alpha) s0 + alpha s1
 __global__ void k_mix(double* __restrict__ s, const double* __restrict__ s0, const double* __restrict__ s1, int64_t q,
                       double alpha) {
@@ -799,8 +835,8 @@ iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_ad
 #undef OP_TRY
 }
 
-iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, double* out, double alpha, uint8_t* ws,
-                            uint32_t* status, hipStream_t s) {
+iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, SpectrumOp op, double* out, double param,
+                            uint8_t* ws, uint32_t* status, hipStream_t s) {
 #define SO_TRY(x)                                \
   do {                                           \
     if ((x) != hipSuccess) return ISO_ERR_HIP;   \
@@ -832,17 +868,43 @@ iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, double* 
                                                   dt);
     SO_TRY(jacobi_block(tb.jobs, 2, r, q, tb.jst, status, s, false, split));
     k_svd_finalize<<<2, 1024, sizeof(double) * q, s>>>(tb.jobs, tb.ptrs, tb.ptrs + 2, tb.ptrs + 4);
-    if (out != nullptr) {
+    if (op == SpectrumOp::kDiagnostics) {
       // Delta W and W_0 col-major, P = Delta W V_0
       k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.G, t[j].deltas[0], nullptr, m, n, 0, dt);
       k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.Wst, t[j].base, nullptr, m, n, 0, dt);
       gemm(m, q, n, 1.0, b.G, 1, m, b.V[0], 1, n, 0.0, b.FU, 1, m, s);
       k_diag_final<<<1, 1024, 0, s>>>(b.S[0], b.S[1], q, b.U[0], b.FU, m, n, b.Wst, b.G, out + 3 * (int64_t)j);
-    } else {
-      k_mix<<<grid_for(q), 256, 0, s>>>(b.P, b.S[0], b.S[1], q, alpha);
+    } else if (op == SpectrumOp::kInterpolate) {
+      k_mix<<<grid_for(q), 256, 0, s>>>(b.P, b.S[0], b.S[1], q, param);
       k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, b.U[1], b.P, m, q);
       gemm(m, n, q, 1.0, b.FU, 1, m, b.V[1], n, 1, 0.0, b.Wst, 1, m, s);
       k_store_w<<<grid_for(m * n), 256, 0, s>>>(t[j].out, b.Wst, m, n, dt, status);
+    } else {
+      // Prop. 3.1 with W_j = base (factors 0) and W_i = base + delta (factors 1), all col-major.
+      // The Jacobi matrices are free after the finalize: ja[0] = W_i^(r), ja[1] = W_j^(r).
+      const int64_t rk = transport_rank(q, param);
+      double* o = out + 5 * (int64_t)j;
+      double* wi = b.ja[0];
+      double* wj = b.ja[1];
+      k_scale_cols<<<grid_for(m * rk), 256, 0, s>>>(b.FU, b.U[1], b.S[1], m, rk);
+      gemm(m, n, rk, 1.0, b.FU, 1, m, b.V[1], n, 1, 0.0, wi, 1, m, s);
+      k_scale_cols<<<grid_for(m * rk), 256, 0, s>>>(b.FU, b.U[0], b.S[0], m, rk);
+      gemm(m, n, rk, 1.0, b.FU, 1, m, b.V[0], n, 1, 0.0, wj, 1, m, s);
+      k_sqdist<<<1, 1024, 0, s>>>(wi, wj, m * n, o);
+      // T1 = U_j^T W_i^(r) (rk x n), W_L = U_j T1
+      gemm(rk, n, m, 1.0, b.U[0], m, 1, wi, 1, m, 0.0, b.FV, 1, rk, s);
+      gemm(m, n, rk, 1.0, b.U[0], 1, m, b.FV, 1, rk, 0.0, b.G, 1, m, s);
+      k_sqdist<<<1, 1024, 0, s>>>(wi, b.G, m * n, o + 2);
+      // T2 = W_i^(r) V_j (m x rk), W_R = T2 V_j^T
+      gemm(m, rk, n, 1.0, wi, 1, m, b.V[0], 1, n, 0.0, b.XU, 1, m, s);
+      gemm(m, n, rk, 1.0, b.XU, 1, m, b.V[0], n, 1, 0.0, b.G, 1, m, s);
+      k_sqdist<<<1, 1024, 0, s>>>(wi, b.G, m * n, o + 3);
+      // core B = T1 V_j (rk x rk), W_mix = (U_j B) V_j^T
+      gemm(rk, rk, n, 1.0, b.FV, 1, rk, b.V[0], 1, n, 0.0, b.P, 1, rk, s);
+      gemm(m, rk, rk, 1.0, b.U[0], 1, m, b.P, 1, rk, 0.0, b.AU, 1, m, s);
+      gemm(m, n, rk, 1.0, b.AU, 1, m, b.V[0], n, 1, 0.0, b.G, 1, m, s);
+      k_sqdist<<<1, 1024, 0, s>>>(wi, b.G, m * n, o + 1);
+      k_transport_final<<<1, 64, 0, s>>>(b.S[0], b.S[1], q, rk, o);
     }
     SO_TRY(hipGetLastError());
     SO_TRY(hipStreamSynchronize(s));   // the next tensor reuses the workspace and the staging

@@ -144,3 +144,19 @@ def test_optimizer_validation():
     assert L.iso_optimizer_step(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 1 << 30, None) == _lib.ERR_ALIGNMENT
     f[0].u = None
     assert L.iso_optimizer_step(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 1 << 30, None) == _lib.ERR_INVALID_ARG
+
+
+def test_transport_ratio_validation():
+    L = _lib.load()
+    es = [entry(K=1, out=False)]
+    t = iso._table(es)
+    for frac in (0.0, -0.5, 1.5, float("nan")):
+        assert L.iso_transport_ratios(t, 1, iso.F32, frac, FAKE * 8, FAKE * 16, 1 << 30, None) == \
+            _lib.ERR_INVALID_ARG, frac
+    assert L.iso_transport_ratios(t, 1, iso.F32, 0.9, None, FAKE * 16, 1 << 30, None) == _lib.ERR_INVALID_ARG
+    assert L.iso_transport_ratios(t, 1, iso.F32, 0.9, FAKE * 8 + 4, FAKE * 16, 1 << 30, None) == _lib.ERR_ALIGNMENT
+    big = [iso.Entry(16385, 8, base=FAKE, deltas=[FAKE + 0x1000], out=None, k=0)]
+    assert L.iso_transport_ratios(iso._table(big), 1, iso.F32, 0.9, FAKE * 8, FAKE * 16, 1 << 30, None) == \
+        _lib.ERR_UNSUPPORTED
+    assert L.iso_transport_ratios(t, 1, iso.F32, 0.9, FAKE * 8, FAKE * 16, 100, None) == _lib.ERR_WORKSPACE
+    assert L.iso_transport_ratios(t, 0, iso.F32, 0.9, FAKE * 8, FAKE * 16, 1 << 30, None) == _lib.OK
