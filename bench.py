@@ -250,10 +250,12 @@ def bench_layer_spectral(args, iso, synth, torch):
 
 
 def bench_layer_optimizer(args, iso, synth, torch):
-    """One ISO-AdamW step (iso_optimizer_step) over the single layer's seven matrices (q/k/v/o
-    2048x2048, gate/up 2048x5632, down 5632x2048) with full-rank frames, bf16 weights and
-    gradients, timed with HIP events.  Roofline: binary64, the algorithmic flops of the two
-    factor-gradient products, the two polar SVDs (Golub & Van Loan's count) and W+."""
+    """One ISO-AdamW step (iso_optimizer_step) or, with --rule muon, one ISO-Muon step
+    (iso_optimizer_step_muon) over the single layer's seven matrices (q/k/v/o 2048x2048, gate/up
+    2048x5632, down 5632x2048) with full-rank frames, bf16 weights and gradients, timed with HIP
+    events.  Roofline: binary64, the algorithmic flops of the two factor-gradient products, the
+    two polar SVDs of the retraction (Golub & Van Loan's count; Muon adds two for its
+    directions) and W+."""
     import numpy as np
     from oracle import optimizer as op
     wl = synth.workload("layer")
@@ -274,14 +276,21 @@ def bench_layer_optimizer(args, iso, synth, torch):
         frames.append(iso.Frame(u=u.t().contiguous().view(-1), v=v.t().contiguous().view(-1), sigma=s,
                                 m_u=z(m), v_u=z(m), m_v=z(n), v_v=z(n), grad=grad,
                                 w_out=torch.empty(m * n, dtype=torch.int16, device=dev), rows=m, cols=n, rank=q))
-        flops += 2 * (2 * m * n * q) + svd_flops(m, q) + svd_flops(n, q) + 2 * m * n * q
+        polars = 2 if args.rule == "adamw" else 4
+        flops += 2 * (2 * m * n * q) + polars // 2 * (svd_flops(m, q) + svd_flops(n, q)) + 2 * m * n * q
     ws = iso.optimizer_workspace(frames, dev)
-    hp = dict(lr=1e-6, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0)
+    muon = args.rule == "muon"
+    hp = dict(lr=1e-6, weight_decay=0.0) if muon else dict(lr=1e-6, beta1=0.9, beta2=0.999, eps=1e-8,
+                                                          weight_decay=0.0)
+    name = "ISO-Muon" if muon else "ISO-AdamW"
     step_no = [0]
 
     def step():
         step_no[0] += 1
-        iso.iso_optimizer_step(frames, iso.BF16, step=step_no[0], ws=ws, **hp)
+        if muon:
+            iso.iso_optimizer_step_muon(frames, iso.BF16, momentum=0.95, nesterov=True, ws=ws, **hp)
+        else:
+            iso.iso_optimizer_step(frames, iso.BF16, step=step_no[0], ws=ws, **hp)
 
     for _ in range(args.warmup):
         step()
@@ -305,10 +314,12 @@ def bench_layer_optimizer(args, iso, synth, torch):
         "unit": "params/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
-        "config": {"workload": f"single bf16 layer ({len(wl.tensors)} matrices, {N} params): one ISO-AdamW step "
-                               "(factor gradients, AdamW, polar retraction, W+) on full-rank frames"},
+        "config": {"workload": f"single bf16 layer ({len(wl.tensors)} matrices, {N} params): one {name} step "
+                               f"(factor gradients, {'Muon with polar directions' if muon else 'AdamW'}, polar "
+                               "retraction, W+) on full-rank frames"},
         "optimizer_ms": opt_ms,
-        "roofline": {"bound": "fp64", "kernel": "iso_optimizer_step (binary64 GEMMs and Newton-Schulz polar)",
+        "roofline": {"bound": "fp64", "kernel": ("iso_optimizer_step_muon" if muon else "iso_optimizer_step") +
+                     " (binary64 GEMMs and Newton-Schulz polar)",
                      "achieved": flops / (opt_ms * 1e-3) / 1e12, "peak": 78.6, "unit": "TFLOP/s",
                      "frac": flops / (opt_ms * 1e-3) / 1e12 / 78.6, "traffic": None, "flops_per_call": flops},
     }
@@ -320,9 +331,11 @@ def bench_layer_optimizer(args, iso, synth, torch):
         v0, _ = np.linalg.qr(rng.standard_normal((n, n)))
         s0 = np.sort(rng.uniform(0.5, 1.5, m))[::-1]
         g = rng.standard_normal((m, n)) * 1e-4
-        st = tuple(np.zeros((r, m)) for r in (m, m, n, n))
         t1 = time.perf_counter()
-        op.iso_adamw_step(u0, v0, s0, g, st, 1, 1e-6)
+        if muon:
+            op.iso_muon_step(u0, v0, s0, g, (np.zeros((m, m)), np.zeros((n, m))), 1e-6, 0.95)
+        else:
+            op.iso_adamw_step(u0, v0, s0, g, tuple(np.zeros((r, m)) for r in (m, m, n, n)), 1, 1e-6)
         dt = time.perf_counter() - t1
         try:
             from threadpoolctl import threadpool_info
@@ -330,7 +343,7 @@ def bench_layer_optimizer(args, iso, synth, torch):
         except ImportError:
             cores = len(os.sched_getaffinity(0))
         rec["cpu_baseline"] = {"value": spec.numel / dt, "unit": "params/s", "cores": cores, "kind": "oracle",
-                               "sample": f"one ISO-AdamW step (LAPACK polar, numpy) on {spec.name} ({m}x{n}), {dt:.1f} s"}
+                               "sample": f"one {name} step (LAPACK polar, numpy) on {spec.name} ({m}x{n}), {dt:.1f} s"}
     return rec
 
 
@@ -342,6 +355,8 @@ def main():
     ap.add_argument("--config", default="7b", choices=["tiny", "layer", "1.5b", "7b", "7b-tsv", "layer-spectral",
                                                       "layer-optimizer"])
     ap.add_argument("--path", default="single-read", choices=["single-read", "two-pass"])
+    ap.add_argument("--rule", default="adamw", choices=["adamw", "muon"],
+                    help="base rule of the ISO-Optimizer step (--config layer-optimizer)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain elementwise copy (1 GiB read, 1 GiB written, 3 launches) to scale "

@@ -42,7 +42,8 @@
  * Entry points: TopKMask (iso_topk_mask, joint over tensor groups), sign
  * election (iso_sign_elect), TIES / TA / RAM merges (iso_merge), the update
  * theta_0 + lambda tau and ISO-Merger (iso_update), TSV (iso_blockdiag_project,
- * iso_blockdiag_project_factors), the ISO-AdamW step (iso_optimizer_step) and
+ * iso_blockdiag_project_factors), the ISO-AdamW and ISO-Muon steps
+ * (iso_optimizer_step, iso_optimizer_step_muon) and
  * the spectral diagnostics of Sec. 3 (iso_spectral_diagnostics,
  * iso_spectrum_interpolate, iso_transport_ratios).
  */
@@ -294,6 +295,29 @@ typedef struct iso_adamw {
 size_t iso_workspace_size_optimizer(const iso_frame* f, int n_f);
 iso_status iso_optimizer_step(const iso_frame* f, int n_f, iso_dtype dt, const iso_adamw* opt, void* ws,
                               size_t ws_bytes, void* stream);
+
+/*
+ * ISO-Optimizer step with Muon as the base rule (ISO-Muon, Sec. 4.3; the
+ * paper names the rule without restating it, this is its usual form): the
+ * same frames, factor gradients, retraction and output as iso_optimizer_step,
+ * with Muon on U (momentum buffer m_u) and on V (momentum buffer m_v):
+ *   b <- mu b + g,  d = g + mu b (nesterov != 0) or d = b,  o = polar(d),
+ *   x <- x - lr * (sqrt(max(1, rows_x / rank)) o + wd x)
+ * where rows_x is rows for U and cols for V.  Muon itself approximates
+ * polar(d) by a few quintic Newton-Schulz steps; here o is the polar factor,
+ * computed as for the retraction.  v_u and v_v are not used (they may be
+ * NULL).  d needs full column rank: otherwise (a zero gradient, say) it has
+ * no unique polar factor, the iteration does not converge and
+ * iso_read_device_status reports ISO_ERR_INTERNAL.  Workspace:
+ * iso_workspace_size_optimizer.
+ */
+typedef struct iso_muon {
+  double lr, momentum, weight_decay;
+  int32_t nesterov;
+} iso_muon;
+
+iso_status iso_optimizer_step_muon(const iso_frame* f, int n_f, iso_dtype dt, const iso_muon* opt, void* ws,
+                                   size_t ws_bytes, void* stream);
 
 /*
  * iso_blockdiag_project -- TSV-Merge (App. F): each delta is truncated to its

@@ -157,7 +157,8 @@ def iso_blockdiag_project_factors(entries, K, dtype, rank, alpha, factors, delta
 
 @dataclass
 class Frame:
-    """One matrix trained by ISO-AdamW: float64 device tensors (column-major frames and moments)."""
+    """One matrix trained by ISO-AdamW or ISO-Muon: float64 device tensors (column-major frames and
+    optimizer state; ISO-Muon uses m_u and m_v as its momentum buffers and takes v_u = v_v = None)."""
     u: object
     v: object
     sigma: object
@@ -195,6 +196,14 @@ def iso_optimizer_step(frames, dtype, lr, beta1=0.9, beta2=0.999, eps=1e-8, weig
     wp, wb = _ws(ws)
     rc = _lib.load().iso_optimizer_step(_frames(frames), len(frames), dtype, ctypes.byref(o), wp, wb, _stream(stream))
     _check(rc, "iso_optimizer_step")
+
+
+def iso_optimizer_step_muon(frames, dtype, lr, momentum=0.95, weight_decay=0.0, nesterov=True, ws=None, stream=None):
+    o = _lib.IsoMuon(lr, momentum, weight_decay, 1 if nesterov else 0)
+    wp, wb = _ws(ws)
+    rc = _lib.load().iso_optimizer_step_muon(_frames(frames), len(frames), dtype, ctypes.byref(o), wp, wb,
+                                             _stream(stream))
+    _check(rc, "iso_optimizer_step_muon")
 
 
 def iso_spectral_diagnostics(entries, dtype, out, ws=None, stream=None):

@@ -16,7 +16,7 @@ UPDATE_APPLY, UPDATE_FUSED, UPDATE_SPECTRAL = 0, 1, 2
 SYMBOLS = ["iso_workspace_size", "iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update",
            "iso_blockdiag_project", "iso_blockdiag_project_factors", "iso_workspace_size_tsv", "iso_k_from_density", "iso_read_device_status",
            "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end", "iso_status_string",
-           "iso_workspace_size_optimizer", "iso_optimizer_step", "iso_spectral_diagnostics",
+           "iso_workspace_size_optimizer", "iso_optimizer_step", "iso_optimizer_step_muon", "iso_spectral_diagnostics",
            "iso_spectrum_interpolate", "iso_transport_ratios"]
 
 
@@ -38,6 +38,11 @@ class IsoFrame(ctypes.Structure):
 class IsoAdamW(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_double), ("beta1", ctypes.c_double), ("beta2", ctypes.c_double),
                 ("eps", ctypes.c_double), ("weight_decay", ctypes.c_double), ("step", ctypes.c_int64)]
+
+
+class IsoMuon(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_double), ("momentum", ctypes.c_double), ("weight_decay", ctypes.c_double),
+                ("nesterov", ctypes.c_int32)]
 
 
 class IsoSelectDesc(ctypes.Structure):
@@ -84,13 +89,15 @@ def load():
     L.iso_workspace_size_optimizer.argtypes = [ctypes.POINTER(IsoFrame), I]
     L.iso_workspace_size_optimizer.restype = Z
     L.iso_optimizer_step.argtypes = [ctypes.POINTER(IsoFrame), I, I, ctypes.POINTER(IsoAdamW), P, Z, P]
+    L.iso_optimizer_step_muon.argtypes = [ctypes.POINTER(IsoFrame), I, I, ctypes.POINTER(IsoMuon), P, Z, P]
     L.iso_spectral_diagnostics.argtypes = [T, I, I, P, P, Z, P]
     L.iso_spectrum_interpolate.argtypes = [T, I, I, D, P, Z, P]
     L.iso_transport_ratios.argtypes = [T, I, I, D, P, P, Z, P]
     L.iso_status_string.argtypes = [I]
     L.iso_status_string.restype = ctypes.c_char_p
     for fn in ("iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update", "iso_blockdiag_project",
-               "iso_blockdiag_project_factors", "iso_optimizer_step", "iso_spectral_diagnostics",
+               "iso_blockdiag_project_factors", "iso_optimizer_step", "iso_optimizer_step_muon",
+               "iso_spectral_diagnostics",
                "iso_spectrum_interpolate", "iso_transport_ratios",
                "iso_read_device_status", "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end"):
         getattr(L, fn).restype = I

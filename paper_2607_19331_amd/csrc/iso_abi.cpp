@@ -671,7 +671,8 @@ static iso_status spectrum_op(const iso_tensor* t, int n_t, iso_dtype dt, Spectr
   return run_spectrum_ops(t, n_t, dt, op, out, param, w + L.spectral, (uint32_t*)w, s);
 }
 
-static iso_status check_frames(const iso_frame* f, int n_f) {
+// second_moments: the AdamW state v_u, v_v must be given (Muon does not use them).
+static iso_status check_frames(const iso_frame* f, int n_f, bool second_moments = true) {
   if (n_f < 0 || (n_f > 0 && f == nullptr)) return ISO_ERR_INVALID_ARG;
   for (int e = 0; e < n_f; ++e) {
     const iso_frame& F = f[e];
@@ -679,8 +680,10 @@ static iso_status check_frames(const iso_frame* f, int n_f) {
     if (std::min(F.rows, F.cols) > ISO_SPECTRAL_MAX_DIM || std::max(F.rows, F.cols) > kMaxElems / std::min(F.rows, F.cols))
       return ISO_ERR_UNSUPPORTED;
     const void* p[9] = {F.u, F.v, F.sigma, F.m_u, F.v_u, F.m_v, F.v_v, F.grad, F.w_out};
-    for (const void* x : p)
-      if (x == nullptr) return ISO_ERR_INVALID_ARG;
+    for (int q = 0; q < 9; ++q) {
+      const bool used = second_moments || (q != 4 && q != 6);
+      if (used && p[q] == nullptr) return ISO_ERR_INVALID_ARG;
+    }
     for (int q = 0; q < 7; ++q)
       if (((uintptr_t)p[q] & 7u) != 0) return ISO_ERR_ALIGNMENT;
     if (((uintptr_t)F.grad & 3u) != 0 || ((uintptr_t)F.w_out & 3u) != 0) return ISO_ERR_ALIGNMENT;
@@ -689,7 +692,7 @@ static iso_status check_frames(const iso_frame* f, int n_f) {
 }
 
 size_t iso_workspace_size_optimizer(const iso_frame* f, int n_f) {
-  if (check_frames(f, n_f) != ISO_OK) return 0;
+  if (check_frames(f, n_f, false) != ISO_OK) return 0;
   return kStatusBytes + optimizer_workspace_bytes(f, n_f);
 }
 
@@ -712,7 +715,28 @@ iso_status iso_optimizer_step(const iso_frame* f, int n_f, iso_dtype dt, const i
   hipStream_t s = (hipStream_t)stream;
   uint8_t* w = (uint8_t*)ws;
   HIP_TRY(start_call(w, s));
-  return run_optimizer(f, n_f, dt, *opt, w + kStatusBytes, (uint32_t*)w, s);
+  return run_optimizer(f, n_f, dt, opt, nullptr, w + kStatusBytes, (uint32_t*)w, s);
+}
+
+iso_status iso_optimizer_step_muon(const iso_frame* f, int n_f, iso_dtype dt, const iso_muon* opt, void* ws,
+                                   size_t ws_bytes, void* stream) {
+  iso_status st = check_frames(f, n_f, false);
+  if (st != ISO_OK) return st;
+  if (dt != ISO_F32 && dt != ISO_BF16) return ISO_ERR_INVALID_ARG;
+  if (opt == nullptr) return ISO_ERR_INVALID_ARG;
+  const double h[3] = {opt->lr, opt->momentum, opt->weight_decay};
+  for (double x : h)
+    if (!(x - x == 0.0)) return ISO_ERR_INVALID_ARG;
+  if (!(opt->momentum >= 0.0 && opt->momentum < 1.0)) return ISO_ERR_INVALID_ARG;
+  if (n_f == 0) return ISO_OK;
+  const size_t need = kStatusBytes + optimizer_workspace_bytes(f, n_f);
+  if (ws == nullptr) return ISO_ERR_WORKSPACE;
+  if (((uintptr_t)ws & 255u) != 0) return ISO_ERR_ALIGNMENT;
+  if (ws_bytes < need) return ISO_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* w = (uint8_t*)ws;
+  HIP_TRY(start_call(w, s));
+  return run_optimizer(f, n_f, dt, nullptr, opt, w + kStatusBytes, (uint32_t*)w, s);
 }
 
 iso_status iso_spectral_diagnostics(const iso_tensor* t, int n_t, iso_dtype dt, double* out, void* ws,

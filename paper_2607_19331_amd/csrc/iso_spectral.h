@@ -30,8 +30,9 @@ inline int64_t transport_rank(int64_t q, double frac) {
 // fraction, 5 doubles of out).
 iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, SpectrumOp op, double* out, double param,
                             uint8_t* ws, uint32_t* status, hipStream_t s);
-iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_adamw& o, uint8_t* ws,
-                         uint32_t* status, hipStream_t s);
+// One ISO-Optimizer step with AdamW (adam != nullptr) or Muon (muon != nullptr) as the base rule.
+iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_adamw* adam, const iso_muon* muon,
+                         uint8_t* ws, uint32_t* status, hipStream_t s);
 iso_status run_spectral(const iso_tensor* t, int n_t, int K, iso_dtype dt, const SpectralArgs& a, uint8_t* ws,
                         uint32_t* status, hipStream_t s);
 

@@ -604,6 +604,26 @@ __global__ void k_adamw(double* __restrict__ x, const double* __restrict__ g, do
   }
 }
 
+// Muon's momentum on n entries: b <- mu b + g, then the direction d = g + mu b (Nesterov) or b.
+__global__ void k_muon_momentum(double* __restrict__ d, const double* __restrict__ g, double* __restrict__ b,
+                                int64_t n, double mu, int nesterov) {
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
+    const double gi = g[e];
+    const double bi = mu * b[e] + gi;
+    b[e] = bi;
+    d[e] = nesterov ? gi + mu * bi : bi;
+  }
+}
+
+// Muon's step on n entries of x along the orthogonalised direction o: x - lr (scale o + wd x).
+__global__ void k_muon_apply(double* __restrict__ x, const double* __restrict__ o, int64_t n, double lr, double scale,
+                             double wd) {
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
+    const double xi = x[e];
+    x[e] = xi - lr * (scale * o[e] + wd * xi);
+  }
+}
+
 struct OptBufs {
   double *G, *FU, *FV, *GU, *GV, *Wst;
   double *PX[2][2], *PG[2];
@@ -759,8 +779,8 @@ size_t optimizer_workspace_bytes(const iso_frame* f, int n_f) {
 
 // All frames of the call at once: gradients, AdamW, both polar factors of every frame as one
 // Newton-Schulz job set, then W+ = U+ Sigma_0 V+^T and the frames written back.
-iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_adamw& o, uint8_t* ws,
-                         uint32_t* status, hipStream_t s) {
+iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_adamw* adam, const iso_muon* muon,
+                         uint8_t* ws, uint32_t* status, hipStream_t s) {
 #define OP_TRY(x)                                \
   do {                                           \
     if ((x) != hipSuccess) return ISO_ERR_HIP;   \
@@ -795,7 +815,8 @@ iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_ad
     max_q = std::max(max_q, q);
   }
   OP_TRY(hipMemcpyAsync(ws, host.data(), tables_end, hipMemcpyHostToDevice, s));
-  const double bc1 = 1.0 - std::pow(o.beta1, (double)o.step), bc2 = 1.0 - std::pow(o.beta2, (double)o.step);
+  const double bc1 = adam ? 1.0 - std::pow(adam->beta1, (double)adam->step) : 1.0;
+  const double bc2 = adam ? 1.0 - std::pow(adam->beta2, (double)adam->step) : 1.0;
   for (int e = 0; e < n_f; ++e) {
     const iso_frame& F = f[e];
     const int64_t m = F.rows, n = F.cols, q = F.rank;
@@ -806,16 +827,39 @@ iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_ad
     k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, F.u, F.sigma, m, q);
     gemm(m, q, n, 1.0, b.G, 1, m, b.FV, 1, n, 0.0, b.GU, 1, m, s);
     gemm(n, q, m, 1.0, b.G, m, 1, b.FU, 1, m, 0.0, b.GV, 1, n, s);
-    // AdamW on the frames (in place), then the tentative frames go to the iterate buffers
-    k_adamw<<<grid_for(m * q), 256, 0, s>>>(F.u, b.GU, F.m_u, F.v_u, m * q, o.lr, o.beta1, o.beta2, o.eps,
-                                           o.weight_decay, bc1, bc2);
-    k_adamw<<<grid_for(n * q), 256, 0, s>>>(F.v, b.GV, F.m_v, F.v_v, n * q, o.lr, o.beta1, o.beta2, o.eps,
-                                           o.weight_decay, bc1, bc2);
-    k_copy<<<grid_for(m * q), 256, 0, s>>>(b.PX[0][0], F.u, m * q);
-    k_copy<<<grid_for(n * q), 256, 0, s>>>(b.PX[1][0], F.v, n * q);
+    if (adam) {
+      // AdamW on the frames (in place), then the tentative frames go to the iterate buffers
+      k_adamw<<<grid_for(m * q), 256, 0, s>>>(F.u, b.GU, F.m_u, F.v_u, m * q, adam->lr, adam->beta1, adam->beta2,
+                                             adam->eps, adam->weight_decay, bc1, bc2);
+      k_adamw<<<grid_for(n * q), 256, 0, s>>>(F.v, b.GV, F.m_v, F.v_v, n * q, adam->lr, adam->beta1, adam->beta2,
+                                             adam->eps, adam->weight_decay, bc1, bc2);
+      k_copy<<<grid_for(m * q), 256, 0, s>>>(b.PX[0][0], F.u, m * q);
+      k_copy<<<grid_for(n * q), 256, 0, s>>>(b.PX[1][0], F.v, n * q);
+    } else {
+      // Muon: momentum and direction; the directions are orthogonalised below
+      k_muon_momentum<<<grid_for(m * q), 256, 0, s>>>(b.PX[0][0], b.GU, F.m_u, m * q, muon->momentum, muon->nesterov);
+      k_muon_momentum<<<grid_for(n * q), 256, 0, s>>>(b.PX[1][0], b.GV, F.m_v, n * q, muon->momentum, muon->nesterov);
+    }
+  }
+  std::vector<NsState> hst;
+  if (muon) {
+    // o = polar(d) for every frame's two directions, then the step and the tentative frames
+    OP_TRY(polar_batch(tb, 2 * n_f, max_rows, max_q, hst, status, s));
+    for (int e = 0; e < n_f; ++e) {
+      const iso_frame& F = f[e];
+      const int64_t m = F.rows, n = F.cols, q = F.rank;
+      const OptBufs& b = bs[e];
+      const double su = std::sqrt(std::max(1.0, (double)m / (double)q));
+      const double sv = std::sqrt(std::max(1.0, (double)n / (double)q));
+      k_muon_apply<<<grid_for(m * q), 256, 0, s>>>(F.u, b.PX[0][hst[2 * e].steps & 1], m * q, muon->lr, su,
+                                                   muon->weight_decay);
+      k_muon_apply<<<grid_for(n * q), 256, 0, s>>>(F.v, b.PX[1][hst[2 * e + 1].steps & 1], n * q, muon->lr, sv,
+                                                   muon->weight_decay);
+      k_copy<<<grid_for(m * q), 256, 0, s>>>(b.PX[0][0], F.u, m * q);
+      k_copy<<<grid_for(n * q), 256, 0, s>>>(b.PX[1][0], F.v, n * q);
+    }
   }
   // U+ = polar(U), V+ = polar(V)
-  std::vector<NsState> hst;
   OP_TRY(polar_batch(tb, 2 * n_f, max_rows, max_q, hst, status, s));
   for (int e = 0; e < n_f; ++e) {
     const iso_frame& F = f[e];

@@ -160,3 +160,30 @@ def test_transport_ratio_validation():
         _lib.ERR_UNSUPPORTED
     assert L.iso_transport_ratios(t, 1, iso.F32, 0.9, FAKE * 8, FAKE * 16, 100, None) == _lib.ERR_WORKSPACE
     assert L.iso_transport_ratios(t, 0, iso.F32, 0.9, FAKE * 8, FAKE * 16, 1 << 30, None) == _lib.OK
+
+
+def test_muon_validation():
+    L = _lib.load()
+    f = (_lib.IsoFrame * 1)()
+    for i, name in enumerate(("u", "v", "sigma", "m_u", "v_u", "m_v", "v_v", "grad", "w_out")):
+        setattr(f[0], name, FAKE + 0x1000 * i)
+    f[0].rows, f[0].cols, f[0].rank = 64, 48, 48
+    f[0].v_u = None                     # Muon keeps no second moments
+    f[0].v_v = None
+    o = _lib.IsoMuon(0.02, 0.95, 0.0, 1)
+    assert L.iso_workspace_size_optimizer(f, 1) > 0
+    assert L.iso_optimizer_step_muon(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 100, None) == _lib.ERR_WORKSPACE
+    adam = _lib.IsoAdamW(1e-3, 0.9, 0.999, 1e-8, 0.0, 1)
+    assert L.iso_optimizer_step(f, 1, iso.F32, ctypes.byref(adam), FAKE * 16, 1 << 30, None) == _lib.ERR_INVALID_ARG
+    for bad in (1.0, -0.1, float("nan")):
+        o.momentum = bad
+        assert L.iso_optimizer_step_muon(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 1 << 30, None) == \
+            _lib.ERR_INVALID_ARG, bad
+    o.momentum, o.lr = 0.95, float("inf")
+    assert L.iso_optimizer_step_muon(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 1 << 30, None) == _lib.ERR_INVALID_ARG
+    o.lr = 0.02
+    assert L.iso_optimizer_step_muon(f, 1, iso.F32, None, FAKE * 16, 1 << 30, None) == _lib.ERR_INVALID_ARG
+    f[0].m_u = None
+    assert L.iso_optimizer_step_muon(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 1 << 30, None) == _lib.ERR_INVALID_ARG
+    f[0].m_u = FAKE + 0x3000 + 4
+    assert L.iso_optimizer_step_muon(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 1 << 30, None) == _lib.ERR_ALIGNMENT

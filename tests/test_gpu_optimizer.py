@@ -1,4 +1,4 @@
-"""GPU ISO-AdamW step (iso_optimizer_step) against the float64 oracle.
+"""GPU ISO-AdamW and ISO-Muon steps (iso_optimizer_step, iso_optimizer_step_muon) against the float64 oracle.
 
 Frames, moments and Sigma_0 are binary64 on both sides; the GPU's products sum in another
 order and its polar factor comes from Newton-Schulz instead of an SVD, so frames and moments
@@ -60,6 +60,53 @@ def test_three_steps_match_the_oracle(dtype):
             assert np.abs(_back(F.v, n, q) - R["v"]).max() <= 1e-10
             for name, a, rows in (("m_u", R["st"][0], m), ("v_u", R["st"][1], m), ("m_v", R["st"][2], n),
                                   ("v_v", R["st"][3], n)):
+                got = _back(getattr(F, name), rows, q)
+                assert np.abs(got - a).max() <= 1e-10 * max(1.0, np.abs(a).max()), name
+            w = from_dev(F.w_out, m * n, dtype)
+            if dtype == "f32":
+                ref_w = w_ref.ravel()
+                scale = np.maximum(np.abs(ref_w), 2.0 ** -10 * np.abs(ref_w).max())
+                assert np.max(np.abs(w.astype(np.float64) - ref_w) / scale) <= 1e-6
+            else:
+                want = nm.f64_to_bf16(w_ref.ravel()).astype(np.int32)
+                assert np.max(np.abs(w.astype(np.int32) - want)) <= 1
+
+
+@pytest.mark.parametrize("dtype,nesterov", [("f32", True), ("bf16", False)])
+def test_muon_three_steps_match_the_oracle(dtype, nesterov):
+    """ISO-Muon (iso_optimizer_step_muon): frames, momentum buffers and weights over three steps, to the
+    bars of the ISO-AdamW test; the direction's polar factor is Newton-Schulz on the GPU, an SVD in the
+    oracle."""
+    import torch
+    rng = np.random.default_rng(31 if nesterov else 32)
+    shapes = [(96, 64, 64), (80, 120, 80), (256, 200, 150)]
+    frames, ref = [], []
+    for m, n, q in shapes:
+        u, _ = np.linalg.qr(rng.standard_normal((m, q)))
+        v, _ = np.linalg.qr(rng.standard_normal((n, q)))
+        s = np.sort(rng.uniform(0.5, 2.0, q))[::-1].copy()
+        g_store = nm.from_f64(rng.standard_normal(m * n) * 0.1, dtype)
+        g = nm.to_f64(g_store, dtype).reshape(m, n)
+        z = (np.zeros((m, q)), np.zeros((n, q)))
+        dev = dict(u=_colmajor(u), v=_colmajor(v), sigma=torch.tensor(s, device="cuda"),
+                   m_u=_colmajor(z[0]), v_u=None, m_v=_colmajor(z[1]), v_v=None, grad=to_dev(g_store),
+                   w_out=torch.empty(m * n, dtype=torch.int16 if dtype == "bf16" else torch.int32, device="cuda"))
+        frames.append(iso.Frame(rows=m, cols=n, rank=q, **dev))
+        ref.append(dict(u=u, v=v, s=s, g=g, st=z))
+    ws = iso.optimizer_workspace(frames)
+    dt = iso.BF16 if dtype == "bf16" else iso.F32
+    hp = dict(lr=0.02, momentum=0.9, weight_decay=0.01)
+    for t in (1, 2, 3):
+        say(f"iso-muon {dtype} nesterov={nesterov} step {t}: {shapes}")
+        iso.iso_optimizer_step_muon(frames, dt, nesterov=nesterov, ws=ws, **hp)
+        assert iso.iso_read_device_status(ws) == 0
+        for F, R in zip(frames, ref):
+            R["u"], R["v"], w_ref, R["st"] = op.iso_muon_step(R["u"], R["v"], R["s"], R["g"], R["st"], hp["lr"],
+                                                              hp["momentum"], hp["weight_decay"], nesterov)
+            m, n, q = F.rows, F.cols, F.rank
+            assert np.abs(_back(F.u, m, q) - R["u"]).max() <= 1e-10
+            assert np.abs(_back(F.v, n, q) - R["v"]).max() <= 1e-10
+            for name, a, rows in (("m_u", R["st"][0], m), ("m_v", R["st"][1], n)):
                 got = _back(getattr(F, name), rows, q)
                 assert np.abs(got - a).max() <= 1e-10 * max(1.0, np.abs(a).max()), name
             w = from_dev(F.w_out, m * n, dtype)
