@@ -242,22 +242,29 @@ iso_status iso_spectrum_interpolate(const iso_tensor* t, int n_t, iso_dtype dt, 
  * Unexplained-update ratios (Sec. 3, Prop. 3.1), per tensor, in binary64: the
  * transition from the incoming checkpoint W_j = base to the learned endpoint
  * W_i = base + deltas[0], both truncated to their top-r SVD with
- * r = max(1, floor(rank_frac q)), q = min(rows, cols), 0 < rank_frac <= 1
- * (the paper's main text takes 0.9).  With P_j = U_j^(r) U_j^(r)T and
- * Q_j = V_j^(r) V_j^(r)T the reconstructions are W_mix = P_j W_i^(r) Q_j,
- * W_L = P_j W_i^(r), W_R = W_i^(r) Q_j and W_iso = U_i^(r) Sigma_j^(r) V_i^(r)T,
- * and u_h = |W_i^(r) - W_h|_F / |W_i^(r) - W_j^(r)|_F (u_iso in its closed form
- * |sigma_i^(r) - sigma_j^(r)|_2 / |W_i^(r) - W_j^(r)|_F).  out is a device
- * array of 5 n_t doubles, per tensor {u_mix, u_L, u_R, u_iso, gap}, where gap
- * = min over both endpoints of sigma_r - sigma_{r+1} (sigma_{q+1} := 0): the
- * transition is admissible (its top-r projectors well defined) only when gap
- * > 0, which the caller checks; the ratios are NaN when W_i^(r) = W_j^(r).
- * Tensors with no elements are skipped (their entries of out are not
- * written).  Workspace and size limits of iso_spectral_diagnostics;
- * ISO_ERR_INVALID_ARG for rank_frac outside (0, 1].
+ * r = max(1, floor(f q)), q = min(rows, cols), for each of the n_frac rank
+ * fractions f = rank_frac[0 .. n_frac-1] (a host array, 0 < f <= 1,
+ * 1 <= n_frac <= ISO_MAX_RANK_FRACS; the paper's main text takes 0.9, its
+ * rank-sensitivity study 0.2, 0.4, 0.6, 0.8 and 0.9).  With
+ * P_j = U_j^(r) U_j^(r)T and Q_j = V_j^(r) V_j^(r)T the reconstructions are
+ * W_mix = P_j W_i^(r) Q_j, W_L = P_j W_i^(r), W_R = W_i^(r) Q_j and
+ * W_iso = U_i^(r) Sigma_j^(r) V_i^(r)T, and
+ * u_h = |W_i^(r) - W_h|_F / |W_i^(r) - W_j^(r)|_F (u_iso in its closed form
+ * |sigma_i^(r) - sigma_j^(r)|_2 / |W_i^(r) - W_j^(r)|_F).  The SVDs are taken
+ * once per tensor.  out is a device array of 5 n_frac n_t doubles: tensor j,
+ * fraction f at out[5 (j n_frac + f) ...] = {u_mix, u_L, u_R, u_iso, gap},
+ * where gap = min over both endpoints of sigma_r - sigma_{r+1}
+ * (sigma_{q+1} := 0): the transition is admissible at that rank (its top-r
+ * projectors well defined) only when gap > 0, which the caller checks; the
+ * ratios are NaN when W_i^(r) = W_j^(r).  Tensors with no elements are
+ * skipped (their entries of out are not written).  Workspace and size limits
+ * of iso_spectral_diagnostics; ISO_ERR_INVALID_ARG for a fraction outside
+ * (0, 1] or n_frac outside [1, ISO_MAX_RANK_FRACS].
  */
-iso_status iso_transport_ratios(const iso_tensor* t, int n_t, iso_dtype dt, double rank_frac, double* out, void* ws,
-                                size_t ws_bytes, void* stream);
+#define ISO_MAX_RANK_FRACS 16
+
+iso_status iso_transport_ratios(const iso_tensor* t, int n_t, iso_dtype dt, const double* rank_frac, int n_frac,
+                                double* out, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * ISO-Optimizer step with AdamW as the base rule (ISO-AdamW, Sec. 4.3): one

@@ -221,10 +221,13 @@ def iso_spectrum_interpolate(entries, dtype, alpha, ws=None, stream=None):
 
 
 def iso_transport_ratios(entries, dtype, rank_frac, out, ws=None, stream=None):
-    """out: device float64 tensor of 5 * len(entries): {u_mix, u_L, u_R, u_iso, gap} per tensor, for the
-    transition base -> base + deltas[0] truncated to rank max(1, floor(rank_frac q))."""
+    """rank_frac: one fraction or a sequence of them.  out: device float64 tensor of
+    5 * len(rank_frac) * len(entries): {u_mix, u_L, u_R, u_iso, gap} per tensor and fraction (tensor
+    major), for the transition base -> base + deltas[0] truncated to rank max(1, floor(f q))."""
+    fr = [float(rank_frac)] if isinstance(rank_frac, (int, float)) else [float(f) for f in rank_frac]
+    arr = (ctypes.c_double * max(1, len(fr)))(*fr)
     wp, wb = _ws(ws)
-    rc = _lib.load().iso_transport_ratios(_table(entries), len(entries), dtype, float(rank_frac), _ptr(out), wp, wb,
+    rc = _lib.load().iso_transport_ratios(_table(entries), len(entries), dtype, arr, len(fr), _ptr(out), wp, wb,
                                           _stream(stream))
     _check(rc, "iso_transport_ratios")
 

@@ -92,7 +92,7 @@ def load():
     L.iso_optimizer_step_muon.argtypes = [ctypes.POINTER(IsoFrame), I, I, ctypes.POINTER(IsoMuon), P, Z, P]
     L.iso_spectral_diagnostics.argtypes = [T, I, I, P, P, Z, P]
     L.iso_spectrum_interpolate.argtypes = [T, I, I, D, P, Z, P]
-    L.iso_transport_ratios.argtypes = [T, I, I, D, P, P, Z, P]
+    L.iso_transport_ratios.argtypes = [T, I, I, ctypes.POINTER(ctypes.c_double), I, P, P, Z, P]
     L.iso_status_string.argtypes = [I]
     L.iso_status_string.restype = ctypes.c_char_p
     for fn in ("iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update", "iso_blockdiag_project",

@@ -650,7 +650,7 @@ iso_status iso_blockdiag_project_factors(const iso_tensor* t, int n_t, int K, is
 }
 
 static iso_status spectrum_op(const iso_tensor* t, int n_t, iso_dtype dt, SpectrumOp op, double* out, double param,
-                              void* ws, size_t ws_bytes, void* stream) {
+                              void* ws, size_t ws_bytes, void* stream, const double* fracs = nullptr, int n_frac = 0) {
   const bool write = op == SpectrumOp::kInterpolate;
   Need nd;
   nd.base = nd.deltas = true;
@@ -661,14 +661,18 @@ static iso_status spectrum_op(const iso_tensor* t, int n_t, iso_dtype dt, Spectr
     if (t[j].rows > ISO_SPECTRAL_MAX_DIM || t[j].cols > ISO_SPECTRAL_MAX_DIM) return ISO_ERR_UNSUPPORTED;
   if (!write && (out == nullptr || ((uintptr_t)out & 7u) != 0)) return out ? ISO_ERR_ALIGNMENT : ISO_ERR_INVALID_ARG;
   if (write && !(param - param == 0.0)) return ISO_ERR_INVALID_ARG;
-  if (op == SpectrumOp::kTransport && !(param > 0.0 && param <= 1.0)) return ISO_ERR_INVALID_ARG;
+  if (op == SpectrumOp::kTransport) {
+    if (fracs == nullptr || n_frac < 1 || n_frac > ISO_MAX_RANK_FRACS) return ISO_ERR_INVALID_ARG;
+    for (int i = 0; i < n_frac; ++i)
+      if (!(fracs[i] > 0.0 && fracs[i] <= 1.0)) return ISO_ERR_INVALID_ARG;
+  }
   if (n_t == 0) return ISO_OK;
   Layout L = plan(ISO_OP_UPDATE_SPECTRAL, t, n_t, 1, dt);
   if ((st = check_ws(L, ws, ws_bytes)) != ISO_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   uint8_t* w = (uint8_t*)ws;
   HIP_TRY(start_call(w, s));
-  return run_spectrum_ops(t, n_t, dt, op, out, param, w + L.spectral, (uint32_t*)w, s);
+  return run_spectrum_ops(t, n_t, dt, op, out, param, fracs, n_frac, w + L.spectral, (uint32_t*)w, s);
 }
 
 // second_moments: the AdamW state v_u, v_v must be given (Muon does not use them).
@@ -749,9 +753,9 @@ iso_status iso_spectrum_interpolate(const iso_tensor* t, int n_t, iso_dtype dt, 
   return spectrum_op(t, n_t, dt, SpectrumOp::kInterpolate, nullptr, alpha, ws, ws_bytes, stream);
 }
 
-iso_status iso_transport_ratios(const iso_tensor* t, int n_t, iso_dtype dt, double rank_frac, double* out, void* ws,
-                                size_t ws_bytes, void* stream) {
-  return spectrum_op(t, n_t, dt, SpectrumOp::kTransport, out, rank_frac, ws, ws_bytes, stream);
+iso_status iso_transport_ratios(const iso_tensor* t, int n_t, iso_dtype dt, const double* rank_frac, int n_frac,
+                                double* out, void* ws, size_t ws_bytes, void* stream) {
+  return spectrum_op(t, n_t, dt, SpectrumOp::kTransport, out, 0.0, ws, ws_bytes, stream, rank_frac, n_frac);
 }
 
 int64_t iso_k_from_density(int64_t n, int64_t num, int64_t den) {

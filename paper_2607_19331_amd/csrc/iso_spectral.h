@@ -26,10 +26,10 @@ inline int64_t transport_rank(int64_t q, double frac) {
 }
 
 // Per tensor, one at a time: drift diagnostics (3 doubles of out), spectrum interpolation
-// (param = alpha, writes the tensor's out) or unexplained-update ratios (param = rank
-// fraction, 5 doubles of out).
+// (param = alpha, writes the tensor's out) or unexplained-update ratios (5 doubles of out for
+// each of the n_frac host rank fractions).
 iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, SpectrumOp op, double* out, double param,
-                            uint8_t* ws, uint32_t* status, hipStream_t s);
+                            const double* fracs, int n_frac, uint8_t* ws, uint32_t* status, hipStream_t s);
 // One ISO-Optimizer step with AdamW (adam != nullptr) or Muon (muon != nullptr) as the base rule.
 iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_adamw* adam, const iso_muon* muon,
                          uint8_t* ws, uint32_t* status, hipStream_t s);

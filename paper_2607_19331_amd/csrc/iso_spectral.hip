@@ -880,7 +880,7 @@ iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_ad
 }
 
 iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, SpectrumOp op, double* out, double param,
-                            uint8_t* ws, uint32_t* status, hipStream_t s) {
+                            const double* fracs, int n_frac, uint8_t* ws, uint32_t* status, hipStream_t s) {
 #define SO_TRY(x)                                \
   do {                                           \
     if ((x) != hipSuccess) return ISO_ERR_HIP;   \
@@ -924,31 +924,33 @@ iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, Spectrum
       gemm(m, n, q, 1.0, b.FU, 1, m, b.V[1], n, 1, 0.0, b.Wst, 1, m, s);
       k_store_w<<<grid_for(m * n), 256, 0, s>>>(t[j].out, b.Wst, m, n, dt, status);
     } else {
-      // Prop. 3.1 with W_j = base (factors 0) and W_i = base + delta (factors 1), all col-major.
-      // The Jacobi matrices are free after the finalize: ja[0] = W_i^(r), ja[1] = W_j^(r).
-      const int64_t rk = transport_rank(q, param);
-      double* o = out + 5 * (int64_t)j;
-      double* wi = b.ja[0];
-      double* wj = b.ja[1];
-      k_scale_cols<<<grid_for(m * rk), 256, 0, s>>>(b.FU, b.U[1], b.S[1], m, rk);
-      gemm(m, n, rk, 1.0, b.FU, 1, m, b.V[1], n, 1, 0.0, wi, 1, m, s);
-      k_scale_cols<<<grid_for(m * rk), 256, 0, s>>>(b.FU, b.U[0], b.S[0], m, rk);
-      gemm(m, n, rk, 1.0, b.FU, 1, m, b.V[0], n, 1, 0.0, wj, 1, m, s);
-      k_sqdist<<<1, 1024, 0, s>>>(wi, wj, m * n, o);
-      // T1 = U_j^T W_i^(r) (rk x n), W_L = U_j T1
-      gemm(rk, n, m, 1.0, b.U[0], m, 1, wi, 1, m, 0.0, b.FV, 1, rk, s);
-      gemm(m, n, rk, 1.0, b.U[0], 1, m, b.FV, 1, rk, 0.0, b.G, 1, m, s);
-      k_sqdist<<<1, 1024, 0, s>>>(wi, b.G, m * n, o + 2);
-      // T2 = W_i^(r) V_j (m x rk), W_R = T2 V_j^T
-      gemm(m, rk, n, 1.0, wi, 1, m, b.V[0], 1, n, 0.0, b.XU, 1, m, s);
-      gemm(m, n, rk, 1.0, b.XU, 1, m, b.V[0], n, 1, 0.0, b.G, 1, m, s);
-      k_sqdist<<<1, 1024, 0, s>>>(wi, b.G, m * n, o + 3);
-      // core B = T1 V_j (rk x rk), W_mix = (U_j B) V_j^T
-      gemm(rk, rk, n, 1.0, b.FV, 1, rk, b.V[0], 1, n, 0.0, b.P, 1, rk, s);
-      gemm(m, rk, rk, 1.0, b.U[0], 1, m, b.P, 1, rk, 0.0, b.AU, 1, m, s);
-      gemm(m, n, rk, 1.0, b.AU, 1, m, b.V[0], n, 1, 0.0, b.G, 1, m, s);
-      k_sqdist<<<1, 1024, 0, s>>>(wi, b.G, m * n, o + 1);
-      k_transport_final<<<1, 64, 0, s>>>(b.S[0], b.S[1], q, rk, o);
+      // Prop. 3.1 with W_j = base (factors 0) and W_i = base + delta (factors 1), all col-major, at
+      // each rank.  The Jacobi matrices are free after the finalize: ja[0] = W_i^(r), ja[1] = W_j^(r).
+      for (int fi = 0; fi < n_frac; ++fi) {
+        const int64_t rk = transport_rank(q, fracs[fi]);
+        double* o = out + 5 * ((int64_t)j * n_frac + fi);
+        double* wi = b.ja[0];
+        double* wj = b.ja[1];
+        k_scale_cols<<<grid_for(m * rk), 256, 0, s>>>(b.FU, b.U[1], b.S[1], m, rk);
+        gemm(m, n, rk, 1.0, b.FU, 1, m, b.V[1], n, 1, 0.0, wi, 1, m, s);
+        k_scale_cols<<<grid_for(m * rk), 256, 0, s>>>(b.FU, b.U[0], b.S[0], m, rk);
+        gemm(m, n, rk, 1.0, b.FU, 1, m, b.V[0], n, 1, 0.0, wj, 1, m, s);
+        k_sqdist<<<1, 1024, 0, s>>>(wi, wj, m * n, o);
+        // T1 = U_j^T W_i^(r) (rk x n), W_L = U_j T1
+        gemm(rk, n, m, 1.0, b.U[0], m, 1, wi, 1, m, 0.0, b.FV, 1, rk, s);
+        gemm(m, n, rk, 1.0, b.U[0], 1, m, b.FV, 1, rk, 0.0, b.G, 1, m, s);
+        k_sqdist<<<1, 1024, 0, s>>>(wi, b.G, m * n, o + 2);
+        // T2 = W_i^(r) V_j (m x rk), W_R = T2 V_j^T
+        gemm(m, rk, n, 1.0, wi, 1, m, b.V[0], 1, n, 0.0, b.XU, 1, m, s);
+        gemm(m, n, rk, 1.0, b.XU, 1, m, b.V[0], n, 1, 0.0, b.G, 1, m, s);
+        k_sqdist<<<1, 1024, 0, s>>>(wi, b.G, m * n, o + 3);
+        // core B = T1 V_j (rk x rk), W_mix = (U_j B) V_j^T
+        gemm(rk, rk, n, 1.0, b.FV, 1, rk, b.V[0], 1, n, 0.0, b.P, 1, rk, s);
+        gemm(m, rk, rk, 1.0, b.U[0], 1, m, b.P, 1, rk, 0.0, b.AU, 1, m, s);
+        gemm(m, n, rk, 1.0, b.AU, 1, m, b.V[0], n, 1, 0.0, b.G, 1, m, s);
+        k_sqdist<<<1, 1024, 0, s>>>(wi, b.G, m * n, o + 1);
+        k_transport_final<<<1, 64, 0, s>>>(b.S[0], b.S[1], q, rk, o);
+      }
     }
     SO_TRY(hipGetLastError());
     SO_TRY(hipStreamSynchronize(s));   // the next tensor reuses the workspace and the staging

@@ -150,16 +150,24 @@ def test_transport_ratio_validation():
     L = _lib.load()
     es = [entry(K=1, out=False)]
     t = iso._table(es)
+
+    def fr(*xs):
+        return (ctypes.c_double * max(1, len(xs)))(*xs)
+
+    def call(fracs, n, out=FAKE * 8, table=t, n_t=1, ws_bytes=1 << 30):
+        return L.iso_transport_ratios(table, n_t, iso.F32, fracs, n, out, FAKE * 16, ws_bytes, None)
+
     for frac in (0.0, -0.5, 1.5, float("nan")):
-        assert L.iso_transport_ratios(t, 1, iso.F32, frac, FAKE * 8, FAKE * 16, 1 << 30, None) == \
-            _lib.ERR_INVALID_ARG, frac
-    assert L.iso_transport_ratios(t, 1, iso.F32, 0.9, None, FAKE * 16, 1 << 30, None) == _lib.ERR_INVALID_ARG
-    assert L.iso_transport_ratios(t, 1, iso.F32, 0.9, FAKE * 8 + 4, FAKE * 16, 1 << 30, None) == _lib.ERR_ALIGNMENT
+        assert call(fr(0.9, frac), 2) == _lib.ERR_INVALID_ARG, frac
+    assert call(fr(0.9), 0) == _lib.ERR_INVALID_ARG
+    assert call(fr(*([0.5] * 17)), 17) == _lib.ERR_INVALID_ARG
+    assert call(None, 1) == _lib.ERR_INVALID_ARG
+    assert call(fr(0.9), 1, out=None) == _lib.ERR_INVALID_ARG
+    assert call(fr(0.9), 1, out=FAKE * 8 + 4) == _lib.ERR_ALIGNMENT
     big = [iso.Entry(16385, 8, base=FAKE, deltas=[FAKE + 0x1000], out=None, k=0)]
-    assert L.iso_transport_ratios(iso._table(big), 1, iso.F32, 0.9, FAKE * 8, FAKE * 16, 1 << 30, None) == \
-        _lib.ERR_UNSUPPORTED
-    assert L.iso_transport_ratios(t, 1, iso.F32, 0.9, FAKE * 8, FAKE * 16, 100, None) == _lib.ERR_WORKSPACE
-    assert L.iso_transport_ratios(t, 0, iso.F32, 0.9, FAKE * 8, FAKE * 16, 1 << 30, None) == _lib.OK
+    assert call(fr(0.9), 1, table=iso._table(big)) == _lib.ERR_UNSUPPORTED
+    assert call(fr(0.2, 0.9), 2, ws_bytes=100) == _lib.ERR_WORKSPACE
+    assert call(fr(*([0.5] * 16)), 16, n_t=0) == _lib.OK
 
 
 def test_muon_validation():

@@ -23,13 +23,16 @@ KEYS = ("mix", "L", "R", "iso")
 
 
 def _run(units, dtype, frac):
+    """frac: one fraction (rows per tensor) or a list (an array tensors x fractions x 5)."""
     import torch
     es = [u.entry() for u in units]
+    nf = 1 if isinstance(frac, float) else len(frac)
     ws = iso.workspace(iso.OP_UPDATE_SPECTRAL, es, 1, dt_code(dtype))
-    out = torch.full((5 * len(es),), -7.0, dtype=torch.float64, device="cuda")
+    out = torch.full((5 * nf * len(es),), -7.0, dtype=torch.float64, device="cuda")
     iso.iso_transport_ratios(es, dt_code(dtype), frac, out, ws=ws)
     assert iso.iso_read_device_status(ws) == 0
-    return out.cpu().numpy().reshape(-1, 5)
+    got = out.cpu().numpy()
+    return got.reshape(-1, 5) if isinstance(frac, float) else got.reshape(len(es), nf, 5)
 
 
 def _check(u, dtype, frac, got):
@@ -63,6 +66,20 @@ def test_ratios_match_the_oracle(dtype, frac):
             continue
         ref = _check(u, dtype, frac, g)
         assert 0.0 <= g[3] <= 1.0 + 1e-12 and ref["gap"] > 0
+
+
+def test_rank_sensitivity_sweep_in_one_call():
+    """The rank-sensitivity fractions 0.2, 0.4, 0.6, 0.8, 0.9 (and a tiny one that floors to rank one)
+    in one call over two tensors: each (tensor, fraction) entry equals the oracle at that rank."""
+    rng = np.random.default_rng(77)
+    fracs = [0.2, 0.4, 0.6, 0.8, 0.9, 0.01]
+    units = [_unit(rng, 120, 90, "f32"), _unit(rng, 70, 150, "bf16")]
+    for u in units:
+        say(f"transport ratios sweep {u.rows}x{u.cols} {u.dtype}: {fracs}")
+        got = _run([u], u.dtype, fracs)[0]
+        for g, f in zip(got, fracs):
+            ref = _check(u, u.dtype, f, g)
+            assert ref["rank"] == max(1, int(np.floor(f * min(u.rows, u.cols))))
 
 
 def test_rescaled_endpoint():
