@@ -285,7 +285,8 @@ typedef struct iso_frame {
   double* u;            /* rows x rank */
   double* v;            /* cols x rank */
   const double* sigma;  /* rank */
-  double* m_u;          /* AdamW first and second moments of U and of V */
+  double* m_u;          /* AdamW: first and second moments of U and of V; */
+                        /* Muon: m_u, m_v are the momentum buffers, v_u, v_v unused */
   double* v_u;
   double* m_v;
   double* v_v;
