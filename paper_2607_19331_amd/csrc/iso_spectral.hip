@@ -178,6 +178,14 @@ __global__ void k_combine(double* __restrict__ out, const double* __restrict__ x
 // converges quadratically to the polar factor for s in (0, sqrt 3); the first step scales X by
 // 1 / sqrt(c), c the largest absolute column sum of X^T X (at least its largest eigenvalue), so
 // that every s lies in (0, 1].  A job stops once max |X^T X - I| <= kNsTol, after one more step.
+//
+// Scaled variant (for arguments far from orthonormal): Chen and Chow's scaling (SIAM J. Matrix
+// Anal. Appl., 2014).  If every s lies in [l, 1], the step X <- a X (3 I - a^2 X^T X) / 2 with
+// a^2 = 3 / (1 + l + l^2) maps both l and 1 to l' = a l (3 - a^2 l^2) / 2 and every s into
+// [l', 1]; l' grows about 2.6-fold per step while l is small and goes to one quadratically.
+// The schedule starts from kNsScaledL0 (a singular value below kNsScaledL0 times the largest
+// still grows at least 1.5-fold per step); from the second step on, l is raised to the bound
+// s_min^2 >= 1 - q max |X^T X - I| when that is larger, and the last step is a plain one.
 struct NsJob {
   double* g;        // q x q: X^T X, then the step matrix T in place
   int64_t q;
@@ -190,14 +198,18 @@ struct NsState {
   int last;                  // the step being taken is the last
   int steps;                 // steps taken: the result is in buffer (steps & 1)
   int pad;
+  double lb;                 // scaled variant: lower bound l of the singular values, this step
+  double lb_next;            // ... and after it
 };
 
 constexpr double kNsTol = 1e-10;
 constexpr int kNsMaxSteps = 48;
 constexpr int kNsCheckSteps = 4;   // steps queued between host reads of the done flags
+constexpr double kNsScaledL0 = 1e-6;
 
 __global__ void k_ns_begin(NsState* st, int njobs) {
-  for (int j = threadIdx.x; j < njobs; j += blockDim.x) st[j] = NsState{0ull, 0ull, 0, 0, 0, 0};
+  for (int j = threadIdx.x; j < njobs; j += blockDim.x)
+    st[j] = NsState{0ull, 0ull, 0, 0, 0, 0, kNsScaledL0, kNsScaledL0};
 }
 
 __global__ void k_ns_reset(NsState* st, int njobs) {
@@ -230,19 +242,35 @@ __global__ void __launch_bounds__(256) k_ns_stats(const NsJob* __restrict__ jobs
   }
 }
 
-// G <- T = (3 I - G / c) / (2 sqrt c), c the scale on the first step and 1 after it
-__global__ void k_ns_form(const NsJob* __restrict__ jobs, NsState* st) {
+// G <- T = (3 I - G / c) / (2 sqrt c), c the scale on the first step and 1 after it; with
+// `scaled`, T = a (3 I - a^2 G / c) / (2 sqrt c) with a from the job's lower bound (a = 1 on the
+// last step).
+__global__ void k_ns_form(const NsJob* __restrict__ jobs, NsState* st, int scaled) {
   const int job = blockIdx.y;
   if (st[job].done) return;
   const NsJob J = jobs[job];
-  const double c = (st[job].steps == 0) ? __longlong_as_double((long long)st[job].csum) : 1.0;
+  const bool first = st[job].steps == 0;
+  const double err = __longlong_as_double((long long)st[job].err);
+  const bool last = err <= kNsTol;
+  const double c = first ? __longlong_as_double((long long)st[job].csum) : 1.0;
   const double ic = (c > 0.0) ? 1.0 / c : 1.0, is = sqrt(ic);
+  double a = 1.0, l = 1.0;
+  if (scaled && !last) {
+    l = st[job].lb;
+    if (!first) l = fmax(l, sqrt(fmax(0.0, 1.0 - (double)J.q * err)));
+    l = fmin(l, 1.0);
+    a = sqrt(3.0 / (1.0 + l + l * l));
+  }
+  const double a2 = a * a;
   const int64_t n = J.q * J.q;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
     const int64_t i = e % J.q, j = e / J.q;
-    J.g[e] = ((i == j ? 3.0 : 0.0) - J.g[e] * ic) * (0.5 * is);
+    J.g[e] = ((i == j ? 3.0 : 0.0) - J.g[e] * (a2 * ic)) * (0.5 * a * is);
   }
-  if (blockIdx.x == 0 && threadIdx.x == 0) st[job].last = __longlong_as_double((long long)st[job].err) <= kNsTol;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    st[job].last = last;
+    st[job].lb_next = 0.5 * a * l * (3.0 - a2 * l * l);
+  }
 }
 
 __global__ void k_ns_check(const NsState* st, int njobs, uint32_t* status) {
@@ -254,6 +282,7 @@ __global__ void k_ns_step_end(NsState* st, int njobs) {
   for (int j = threadIdx.x; j < njobs; j += blockDim.x)
     if (!st[j].done) {
       st[j].steps += 1;
+      st[j].lb = st[j].lb_next;
       if (st[j].last) st[j].done = 1;
     }
 }
@@ -422,7 +451,7 @@ void middle_steps(const Bufs& b, int64_t m, int64_t n, int K, const SpectralArgs
 // Newton-Schulz polar over the batch's 2 nm jobs (X of job p in buffer 0 on entry); the host
 // reads the done flags every kNsCheckSteps steps.  On return hst holds every job's state.
 hipError_t polar_batch(const Tables& tb, int njobs, int64_t max_rows, int64_t max_q, std::vector<NsState>& hst,
-                       uint32_t* status, hipStream_t s) {
+                       uint32_t* status, hipStream_t s, bool scaled = false) {
   const unsigned tq = (unsigned)((max_q + GT - 1) / GT), tr = (unsigned)((max_rows + GT - 1) / GT);
   const unsigned cb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_q + 3) / 4, 1024));
   const unsigned fb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_q * max_q + 255) / 256, 2048));
@@ -434,7 +463,7 @@ hipError_t polar_batch(const Tables& tb, int njobs, int64_t max_rows, int64_t ma
       k_ns_reset<<<1, 256, 0, s>>>(tb.nst, njobs);
       k_gemm_jobs<<<dim3(tq, tq, (unsigned)njobs), 256, 0, s>>>(tb.ngj[2 * p]);
       k_ns_stats<<<dim3(cb, (unsigned)njobs), 256, 0, s>>>(tb.ns, tb.nst);
-      k_ns_form<<<dim3(fb, (unsigned)njobs), 256, 0, s>>>(tb.ns, tb.nst);
+      k_ns_form<<<dim3(fb, (unsigned)njobs), 256, 0, s>>>(tb.ns, tb.nst, scaled ? 1 : 0);
       k_gemm_jobs<<<dim3(tr, tq, (unsigned)njobs), 256, 0, s>>>(tb.ngj[2 * p + 1]);
       k_ns_step_end<<<1, 256, 0, s>>>(tb.nst, njobs);
     }
@@ -843,8 +872,9 @@ iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_ad
   }
   std::vector<NsState> hst;
   if (muon) {
-    // o = polar(d) for every frame's two directions, then the step and the tentative frames
-    OP_TRY(polar_batch(tb, 2 * n_f, max_rows, max_q, hst, status, s));
+    // o = polar(d) for every frame's two directions (far from orthonormal: the scaled iteration),
+    // then the step and the tentative frames
+    OP_TRY(polar_batch(tb, 2 * n_f, max_rows, max_q, hst, status, s, true));
     for (int e = 0; e < n_f; ++e) {
       const iso_frame& F = f[e];
       const int64_t m = F.rows, n = F.cols, q = F.rank;
