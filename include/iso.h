@@ -14,7 +14,7 @@
  *    call uses one storage type for base, deltas and the weight output.
  *  - All data pointers are device memory owned by the caller; every one must
  *    be 16-byte aligned (ISO_ERR_ALIGNMENT otherwise), except the binary64
- *    arrays of iso_frame, iso_spectral_diagnostics and iso_transport_ratios
+ *    arrays of iso_frame, iso_spectral_diagnostics, iso_spectral_error and iso_transport_ratios
  *    (8-byte) and the gradient and weight of iso_frame (4-byte).  N need not
  *    be a multiple of anything.
  *  - ws / ws_bytes: caller-allocated device workspace of at least
@@ -45,7 +45,8 @@
  * iso_blockdiag_project_factors), the ISO-AdamW and ISO-Muon steps
  * (iso_optimizer_step, iso_optimizer_step_muon) and
  * the spectral diagnostics of Sec. 3 (iso_spectral_diagnostics,
- * iso_spectrum_interpolate, iso_transport_ratios).
+ * iso_spectrum_interpolate, iso_transport_ratios) and the mean squared
+ * spectral error of App. G (iso_spectral_error).
  */
 #ifndef ISO_H
 #define ISO_H
@@ -228,6 +229,24 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
  */
 iso_status iso_spectral_diagnostics(const iso_tensor* t, int n_t, iso_dtype dt, double* out, void* ws,
                                     size_t ws_bytes, void* stream);
+
+/*
+ * Mean squared spectral error (App. G, the precision study of the SVD behind the
+ * polar retraction), per tensor, in binary64:
+ *   eps_sigma = (1/q) |sigma(W_rec) - sigma(W_0)|_2^2,  q = min(rows, cols),
+ * with W_0 = base and
+ *   self_recon = 0: W_rec = deltas[0], a whole matrix of the same shape and
+ *                   storage type (not a difference);
+ *   self_recon = 1: W_rec = U Sigma V^T formed in binary64 from the library's
+ *                   own SVD of W_0 (deltas are not read), the reconstruction
+ *                   the appendix measures for each SVD configuration.
+ * Singular values come from the binary64 one-sided Jacobi SVD of ISO-Merger.
+ * out is a device array of n_t doubles (8-byte aligned); tensors with no
+ * elements are skipped.  ISO_ERR_INVALID_ARG for self_recon outside {0, 1}.
+ * Same workspace and size limits as iso_spectral_diagnostics.
+ */
+iso_status iso_spectral_error(const iso_tensor* t, int n_t, iso_dtype dt, int self_recon, double* out, void* ws,
+                              size_t ws_bytes, void* stream);
 
 /*
  * Spectrum interpolation (Sec. 3): out = U_RL [(1 - alpha) Sigma_0 + alpha

@@ -182,3 +182,19 @@ def transport_ratios(w_in, w_end, rank_frac=0.9):
     u["gap"] = min(gap(sj), gap(si))
     u["rank"] = r
     return u
+
+
+def svd_reconstruction(w0):
+    """W_rec = U Sigma V^T from the thin SVD of W_0 (App. G, the reconstruction whose spectrum the
+    precision study compares with W_0's)."""
+    u, s, v = thin_svd(w0)
+    return (u * s) @ v.T
+
+
+def spectral_error(w0, w_rec):
+    """Mean squared spectral error of App. G: eps_sigma = (1/q) |sigma(W_rec) - sigma(W_0)|_2^2,
+    q = min(d_out, d_in), both spectra sorted nonincreasing."""
+    w0 = np.asarray(w0, dtype=np.float64)
+    s0 = np.linalg.svd(w0, compute_uv=False)
+    s1 = np.linalg.svd(np.asarray(w_rec, dtype=np.float64), compute_uv=False)
+    return float(np.sum((s1 - s0) ** 2) / min(w0.shape))

@@ -83,6 +83,40 @@ def topk_descriptor(delta, k, dtype):
     return (t_key, n_above, quota, cutoff)
 
 
+def topk_descriptor_counting(delta, k, dtype="bf16"):
+    """The same threshold description as ``topk_descriptor``, found by counting (bf16 only).
+
+    The bf16 magnitude key (the bit pattern of |tau|, 15 bits) is monotone in
+    |tau|, so the k-th largest magnitude is the largest key T whose count of
+    keys >= T reaches k.  n_above counts the keys > T; the tie cutoff is one
+    past the flat index of the quota-th entry with key T (N when all of them
+    are kept).  Linear in N, for the 10^8-10^9-entry tensors of the
+    whole-stack parity checks.
+    """
+    if dtype != "bf16":
+        raise ValueError("counting form is for 15-bit bf16 keys")
+    b = np.asarray(delta, dtype=np.uint16).ravel()
+    n = b.size
+    if not 0 <= k <= n:
+        raise ValueError("k out of range")
+    key = b & np.uint16(0x7FFF)
+    hist = np.bincount(key, minlength=1 << 15).astype(np.int64)
+    if np.any(hist[0x7F80:]):
+        raise FloatingPointError("non-finite value in delta")
+    if k == 0:
+        return (NO_SELECT_KEY, 0, 0, 0)
+    at_or_above = np.cumsum(hist[::-1])[::-1]          # at_or_above[c] = #{key >= c}
+    t_key = int(np.flatnonzero(at_or_above >= k)[-1])
+    n_above = int(at_or_above[t_key] - hist[t_key])
+    quota = k - n_above
+    if quota == hist[t_key]:
+        cutoff = n
+    else:
+        ties = np.flatnonzero(key == np.uint16(t_key))
+        cutoff = int(ties[quota - 1]) + 1
+    return (t_key, n_above, quota, cutoff)
+
+
 def mask_from_descriptor(delta, desc, dtype):
     t_key, _, _, cutoff = desc
     key = magnitude_key(np.asarray(delta).ravel(), dtype).astype(np.int64)

@@ -213,6 +213,15 @@ def iso_spectral_diagnostics(entries, dtype, out, ws=None, stream=None):
     _check(rc, "iso_spectral_diagnostics")
 
 
+def iso_spectral_error(entries, dtype, out, self_recon=False, ws=None, stream=None):
+    """out: device float64 tensor of len(entries): eps_sigma per tensor, W_0 = base and W_rec = deltas[0]
+    (a whole matrix), or with self_recon the reconstruction from the library's own SVD of the base."""
+    wp, wb = _ws(ws)
+    rc = _lib.load().iso_spectral_error(_table(entries), len(entries), dtype, 1 if self_recon else 0, _ptr(out), wp,
+                                        wb, _stream(stream))
+    _check(rc, "iso_spectral_error")
+
+
 def iso_spectrum_interpolate(entries, dtype, alpha, ws=None, stream=None):
     wp, wb = _ws(ws)
     rc = _lib.load().iso_spectrum_interpolate(_table(entries), len(entries), dtype, float(alpha), wp, wb,

@@ -17,7 +17,7 @@ SYMBOLS = ["iso_workspace_size", "iso_topk_mask", "iso_sign_elect", "iso_merge",
            "iso_blockdiag_project", "iso_blockdiag_project_factors", "iso_workspace_size_tsv", "iso_k_from_density", "iso_read_device_status",
            "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end", "iso_status_string",
            "iso_workspace_size_optimizer", "iso_optimizer_step", "iso_optimizer_step_muon", "iso_spectral_diagnostics",
-           "iso_spectrum_interpolate", "iso_transport_ratios"]
+           "iso_spectrum_interpolate", "iso_transport_ratios", "iso_spectral_error"]
 
 
 class IsoTensor(ctypes.Structure):
@@ -92,13 +92,14 @@ def load():
     L.iso_optimizer_step_muon.argtypes = [ctypes.POINTER(IsoFrame), I, I, ctypes.POINTER(IsoMuon), P, Z, P]
     L.iso_spectral_diagnostics.argtypes = [T, I, I, P, P, Z, P]
     L.iso_spectrum_interpolate.argtypes = [T, I, I, D, P, Z, P]
+    L.iso_spectral_error.argtypes = [T, I, I, I, P, P, Z, P]
     L.iso_transport_ratios.argtypes = [T, I, I, ctypes.POINTER(ctypes.c_double), I, P, P, Z, P]
     L.iso_status_string.argtypes = [I]
     L.iso_status_string.restype = ctypes.c_char_p
     for fn in ("iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update", "iso_blockdiag_project",
                "iso_blockdiag_project_factors", "iso_optimizer_step", "iso_optimizer_step_muon",
                "iso_spectral_diagnostics",
-               "iso_spectrum_interpolate", "iso_transport_ratios",
+               "iso_spectrum_interpolate", "iso_transport_ratios", "iso_spectral_error",
                "iso_read_device_status", "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end"):
         getattr(L, fn).restype = I
     _lib = L

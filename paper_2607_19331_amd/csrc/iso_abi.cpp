@@ -46,11 +46,12 @@ iso_status check_table(const iso_tensor* t, int n_t, int K, iso_dtype dt, Need n
       if (!x.base) return ISO_ERR_INVALID_ARG;
       if (!aligned16(x.base)) return ISO_ERR_ALIGNMENT;
     }
-    if (need.deltas)
+    if (need.deltas) {
       for (int i = 0; i < K; ++i) {
         if (!x.deltas[i]) return ISO_ERR_INVALID_ARG;
         if (!aligned16(x.deltas[i])) return ISO_ERR_ALIGNMENT;
       }
+    }
     if (need.out) {
       if (!x.out) return ISO_ERR_INVALID_ARG;
       if (!aligned16(x.out)) return ISO_ERR_ALIGNMENT;
@@ -93,7 +94,9 @@ GroupMap group_map(const iso_tensor* t, int n_t) {
   for (int j = 0; j < n_t; ++j)
     if (G.gid[j] >= 0) {
       G.mem0[G.gid[j] + 1] += 1;
-      G.gk[G.gid[j]] += t[j].k;
+      // saturating: a count past any group's size is rejected by check_groups
+      const __int128 sum = (__int128)G.gk[G.gid[j]] + t[j].k;
+      G.gk[G.gid[j]] = sum > (__int128)INT64_MAX ? INT64_MAX : (int64_t)sum;
       G.gn[G.gid[j]] += t[j].rows * t[j].cols;
     }
   for (int g = 0; g < G.n; ++g) G.mem0[g + 1] += G.mem0[g];
@@ -104,7 +107,8 @@ GroupMap group_map(const iso_tensor* t, int n_t) {
   return G;
 }
 
-// Groups are bf16 only, and a group's count cannot exceed its size.
+// Groups are bf16 only, and a group's count cannot exceed its size.  A group may hold more than
+// 2^32 entries (its histogram bins are 64-bit); each member stays within the per-tensor limit.
 iso_status check_groups(const iso_tensor* t, int n_t, iso_dtype dt) {
   const GroupMap G = group_map(t, n_t);
   if (G.n == 0) return ISO_OK;
@@ -191,7 +195,7 @@ Layout plan(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
     off = align_up(off + sizeof(iso_select_desc) * (size_t)n_t * K, 256);
     if (L.n_groups > 0) {
       L.ghist = off;
-      off = align_up(off + sizeof(uint32_t) * 32768ull * (size_t)L.n_groups * K, 256);
+      off = align_up(off + sizeof(uint64_t) * 32768ull * (size_t)L.n_groups * K, 256);
       L.gstate = off;
       off = align_up(off + sizeof(GroupState) * (size_t)L.n_groups * K, 256);
       L.mcnt = off;
@@ -343,7 +347,7 @@ SelectPlan select_plan(const Layout& L, uint8_t* ws, int n_t, int K, iso_select_
     p.gmem = (const int*)(ws + L.gmem);
     p.gmem0 = (const int*)(ws + L.gmem0);
     p.gk = (const int64_t*)(ws + L.gk);
-    p.ghist = (uint32_t*)(ws + L.ghist);
+    p.ghist = (uint64_t*)(ws + L.ghist);
     p.gstate = (GroupState*)(ws + L.gstate);
     p.mcnt = (int64_t*)(ws + L.mcnt);
   }
@@ -653,7 +657,8 @@ static iso_status spectrum_op(const iso_tensor* t, int n_t, iso_dtype dt, Spectr
                               void* ws, size_t ws_bytes, void* stream, const double* fracs = nullptr, int n_frac = 0) {
   const bool write = op == SpectrumOp::kInterpolate;
   Need nd;
-  nd.base = nd.deltas = true;
+  nd.base = true;
+  nd.deltas = op != SpectrumOp::kSelfSpectralError;
   nd.out = write;
   iso_status st = check_table(t, n_t, 1, dt, nd);
   if (st != ISO_OK) return st;
@@ -746,6 +751,13 @@ iso_status iso_optimizer_step_muon(const iso_frame* f, int n_f, iso_dtype dt, co
 iso_status iso_spectral_diagnostics(const iso_tensor* t, int n_t, iso_dtype dt, double* out, void* ws,
                                     size_t ws_bytes, void* stream) {
   return spectrum_op(t, n_t, dt, SpectrumOp::kDiagnostics, out, 0.0, ws, ws_bytes, stream);
+}
+
+iso_status iso_spectral_error(const iso_tensor* t, int n_t, iso_dtype dt, int self_recon, double* out, void* ws,
+                              size_t ws_bytes, void* stream) {
+  if (self_recon != 0 && self_recon != 1) return ISO_ERR_INVALID_ARG;
+  return spectrum_op(t, n_t, dt, self_recon ? SpectrumOp::kSelfSpectralError : SpectrumOp::kSpectralError, out, 0.0,
+                     ws, ws_bytes, stream);
 }
 
 iso_status iso_spectrum_interpolate(const iso_tensor* t, int n_t, iso_dtype dt, double alpha, void* ws,

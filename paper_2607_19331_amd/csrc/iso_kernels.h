@@ -41,7 +41,7 @@ struct SelectPlan {
   const int* gmem = nullptr;        // members of every group, in table order
   const int* gmem0 = nullptr;       // n_groups + 1 offsets into gmem
   const int64_t* gk = nullptr;      // n_groups: the group's count (sum of its members' k)
-  uint32_t* ghist = nullptr;        // n_groups * K * 32768
+  uint64_t* ghist = nullptr;        // n_groups * K * 32768
   GroupState* gstate = nullptr;     // n_groups * K
   int64_t* mcnt = nullptr;          // 2 * n_t * K: per unit, entries above the group threshold and ties
 };

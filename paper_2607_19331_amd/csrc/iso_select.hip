@@ -314,23 +314,26 @@ __global__ void __launch_bounds__(kHistThreads) k_resolve(const DevTensor* __res
 // exactly a TopKMask of the member with that count: the per-unit resolve and tie search then
 // give its descriptor unchanged.
 
+// Group bins are 64-bit: a group (a whole-model delta) can hold more than 2^32 entries even
+// though each member's own counts fit 32 bits.
 __global__ void __launch_bounds__(256) k_group_sum(int K, const int* __restrict__ gmem, const int* __restrict__ gmem0,
-                                                   const uint32_t* __restrict__ hist, uint32_t* __restrict__ ghist) {
+                                                   const uint32_t* __restrict__ hist, uint64_t* __restrict__ ghist) {
   const int gi = blockIdx.y, g = gi / K, i = gi % K;
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= kMaxBins) return;
-  uint32_t sum = 0;
+  uint64_t sum = 0;
   for (int m = gmem0[g]; m < gmem0[g + 1]; ++m) sum += hist[((size_t)gmem[m] * K + i) * kMaxBins + b];
   ghist[(size_t)gi * kMaxBins + b] = sum;
 }
 
+// The group histogram (256 KB of 64-bit bins) does not fit LDS: each thread reads its run of
+// consecutive bins from global memory twice (sum, then the walk from the top).
 __global__ void __launch_bounds__(kHistThreads) k_group_resolve(const DevTensor* __restrict__ tab, int K,
                                                                 const int* __restrict__ gmem,
                                                                 const int* __restrict__ gmem0,
                                                                 const int64_t* __restrict__ gk,
-                                                                const uint32_t* __restrict__ ghist,
+                                                                const uint64_t* __restrict__ ghist,
                                                                 GroupState* __restrict__ gst, uint32_t* status) {
-  __shared__ uint32_t sbin[kMaxBins];
   __shared__ int64_t sh[16];
   __shared__ int64_t found_d, found_above, total_nonzero;
   const int gi = blockIdx.x, g = gi / K;
@@ -341,7 +344,7 @@ __global__ void __launch_bounds__(kHistThreads) k_group_resolve(const DevTensor*
   }
   int64_t n_g = 0;
   for (int m = gmem0[g]; m < gmem0[g + 1]; ++m) n_g += tab[gmem[m]].n;
-  for (uint32_t b = threadIdx.x; b < kMaxBins; b += blockDim.x) sbin[b] = ghist[(size_t)gi * kMaxBins + b];
+  const uint64_t* gh = ghist + (size_t)gi * kMaxBins;
   if (threadIdx.x == 0) { found_d = -1; found_above = 0; }
   __syncthreads();
   const uint32_t per = (kMaxBins + blockDim.x - 1) / blockDim.x;
@@ -349,7 +352,7 @@ __global__ void __launch_bounds__(kHistThreads) k_group_resolve(const DevTensor*
   int64_t mine = 0;
   for (uint32_t q = 0; q < per; ++q) {
     const uint32_t b = b0 + q;
-    if (b < kMaxBins && b > 0) mine += sbin[b];
+    if (b < kMaxBins && b > 0) mine += (int64_t)gh[b];
   }
   const int64_t incl = block_inclusive_scan(mine, sh);
   if (threadIdx.x == blockDim.x - 1) total_nonzero = incl;
@@ -359,7 +362,7 @@ __global__ void __launch_bounds__(kHistThreads) k_group_resolve(const DevTensor*
   for (int q = (int)per - 1; q >= 0; --q) {
     const uint32_t b = b0 + (uint32_t)q;
     if (b >= kMaxBins) continue;
-    const int64_t h = (b == 0) ? zeros : (int64_t)sbin[b];
+    const int64_t h = (b == 0) ? zeros : (int64_t)gh[b];
     if (run < need && run + h >= need) { found_d = b; found_above = run; }
     run += h;
   }

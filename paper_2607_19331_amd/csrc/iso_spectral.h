@@ -17,7 +17,7 @@ struct SpectralArgs {
 
 size_t spectral_workspace_bytes(const iso_tensor* t, int n_t, int K);
 size_t optimizer_workspace_bytes(const iso_frame* f, int n_f);
-enum class SpectrumOp { kDiagnostics, kInterpolate, kTransport };
+enum class SpectrumOp { kDiagnostics, kInterpolate, kTransport, kSpectralError, kSelfSpectralError };
 
 // Truncation rank r = max(1, floor(frac q)) of the unexplained-update ratios.
 inline int64_t transport_rank(int64_t q, double frac) {
@@ -26,8 +26,9 @@ inline int64_t transport_rank(int64_t q, double frac) {
 }
 
 // Per tensor, one at a time: drift diagnostics (3 doubles of out), spectrum interpolation
-// (param = alpha, writes the tensor's out) or unexplained-update ratios (5 doubles of out for
-// each of the n_frac host rank fractions).
+// (param = alpha, writes the tensor's out), unexplained-update ratios (5 doubles of out for
+// each of the n_frac host rank fractions) or the mean squared spectral error (1 double of out;
+// W_rec = deltas[0], or the reconstruction from the library's own SVD of the base).
 iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, SpectrumOp op, double* out, double param,
                             const double* fracs, int n_frac, uint8_t* ws, uint32_t* status, hipStream_t s);
 // One ISO-Optimizer step with AdamW (adam != nullptr) or Muon (muon != nullptr) as the base rule.

@@ -747,6 +747,23 @@ __global__ void __launch_bounds__(1024) k_sqdist(const double* __restrict__ a, c
   }
 }
 
+// Mean squared spectral error (App. G): out[0] = (1/q) sum_k (s1_k - s0_k)^2 over the sorted spectra
+// (one workgroup, fixed summation order).
+__global__ void __launch_bounds__(1024) k_spectral_error(const double* __restrict__ s0, const double* __restrict__ s1,
+                                                         int64_t q, double* __restrict__ out) {
+  __shared__ double red[16];
+  double x = 0.0;
+  for (int64_t k = threadIdx.x; k < q; k += blockDim.x) x += (s1[k] - s0[k]) * (s1[k] - s0[k]);
+  x = wave_sum_f64(x);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double t = 0.0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) t += red[w];
+    out[0] = t / (double)q;
+  }
+}
+
 // Unexplained-update ratios from the squared residuals held in out[0..3] (|W_i^(r) - W_j^(r)|^2,
 // then those of the mix, L and R reconstructions) and the two spectra s0 (incoming W_j) and s1
 // (endpoint W_i): out = {u_mix, u_L, u_R, u_iso, gap}.  u_iso takes the closed form of Prop. 3.1,
@@ -937,12 +954,34 @@ iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, Spectrum
       hp[4 + i] = b.S[i];
     }
     SO_TRY(hipMemcpyAsync(ws, host.data(), tables_end, hipMemcpyHostToDevice, s));
-    for (int i = 0; i < 2; ++i)
-      k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.ja[i], t[j].base, i ? t[j].deltas[0] : nullptr, m, n, wide ? 1 : 0,
-                                                  dt);
+    if (op == SpectrumOp::kSelfSpectralError) {
+      // App. G: W_0 = L S R^T by the Jacobi SVD of the Jacobi matrix A (W_0 or W_0^T), then
+      // A_rec = (L S) R^T in binary64 into the second job's matrix and its own SVD
+      k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.ja[0], t[j].base, nullptr, m, n, wide ? 1 : 0, dt);
+      SO_TRY(jacobi_block(tb.jobs, 1, r, q, tb.jst, status, s, false, split));
+      k_svd_finalize<<<1, 1024, sizeof(double) * q, s>>>(tb.jobs, tb.ptrs, tb.ptrs + 2, tb.ptrs + 4);
+      const double* lf = wide ? b.V[0] : b.U[0];     // r x q left factor of A
+      const double* rf = wide ? b.U[0] : b.V[0];     // q x q right factor
+      k_scale_cols<<<grid_for(r * q), 256, 0, s>>>(b.G, lf, b.S[0], r, q);
+      gemm(r, q, q, 1.0, b.G, 1, r, rf, q, 1, 0.0, b.ja[1], 1, r, s);
+      SO_TRY(jacobi_block(tb.jobs + 1, 1, r, q, tb.jst + 1, status, s, false, split));
+      k_svd_finalize<<<1, 1024, sizeof(double) * q, s>>>(tb.jobs + 1, tb.ptrs + 1, tb.ptrs + 3, tb.ptrs + 5);
+      k_spectral_error<<<1, 1024, 0, s>>>(b.S[0], b.S[1], q, out + j);
+      SO_TRY(hipGetLastError());
+      SO_TRY(hipStreamSynchronize(s));
+      continue;
+    }
+    for (int i = 0; i < 2; ++i) {
+      // the spectral error compares two whole matrices; the other ops take W_0 and W_0 + Delta W
+      const bool whole = op == SpectrumOp::kSpectralError && i == 1;
+      k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.ja[i], whole ? t[j].deltas[0] : t[j].base,
+                                                  (i && !whole) ? t[j].deltas[0] : nullptr, m, n, wide ? 1 : 0, dt);
+    }
     SO_TRY(jacobi_block(tb.jobs, 2, r, q, tb.jst, status, s, false, split));
     k_svd_finalize<<<2, 1024, sizeof(double) * q, s>>>(tb.jobs, tb.ptrs, tb.ptrs + 2, tb.ptrs + 4);
-    if (op == SpectrumOp::kDiagnostics) {
+    if (op == SpectrumOp::kSpectralError) {
+      k_spectral_error<<<1, 1024, 0, s>>>(b.S[0], b.S[1], q, out + j);
+    } else if (op == SpectrumOp::kDiagnostics) {
       // Delta W and W_0 col-major, P = Delta W V_0
       k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.G, t[j].deltas[0], nullptr, m, n, 0, dt);
       k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.Wst, t[j].base, nullptr, m, n, 0, dt);

@@ -170,14 +170,31 @@ def dev_lib():
     return _dev
 
 
-def fill_host(wl, t_idx, role, first=0, n=None):
-    """Storage array (uint16 bf16 bits or float32) for elements [first, first+n) of a tensor."""
+def fill_host(wl, t_idx, role, first=0, n=None, threads=1):
+    """Storage array (uint16 bf16 bits or float32) for elements [first, first+n) of a tensor.
+
+    With threads > 1 the range is split into that many contiguous pieces filled
+    concurrently (each element depends only on its own counter, so the bits are
+    the same)."""
     spec = wl.tensors[t_idx]
     if n is None:
         n = spec.numel - first
     out = np.empty(n, dtype=wl.np_dtype())
     r = wl.recipe(t_idx, role)
-    host_lib().synth_fill_host(out.ctypes.data, n, wl.sdtype, ctypes.byref(r), first)
+    lib = host_lib()
+    parts = max(1, min(int(threads), n // (1 << 20)))
+    if parts == 1:
+        lib.synth_fill_host(out.ctypes.data, n, wl.sdtype, ctypes.byref(r), first)
+        return out
+    from concurrent.futures import ThreadPoolExecutor
+    edges = [n * p // parts for p in range(parts + 1)]
+
+    def piece(p):
+        a, b = edges[p], edges[p + 1]
+        lib.synth_fill_host(out[a:].ctypes.data, b - a, wl.sdtype, ctypes.byref(r), first + a)
+
+    with ThreadPoolExecutor(parts) as ex:
+        list(ex.map(piece, range(parts)))
     return out
 
 

@@ -84,7 +84,7 @@ def test_group_validation():
     L = _lib.load()
     a, b = entry(rows=16, cols=16, k=300), entry(rows=16, cols=16, k=0)
     a.group = b.group = 3
-    assert call_topk([a, b], 2) != _lib.ERR_INVALID_ARG          # 300 <= 512: passes validation
+    assert call_topk([a, b], 2, ws_bytes=100) == _lib.ERR_WORKSPACE    # 300 <= 512: passes validation
     a.k = 600
     assert call_topk([a, b], 2) == _lib.ERR_INVALID_ARG
     a.k, a.group = 10, -1
@@ -94,7 +94,25 @@ def test_group_validation():
     assert L.iso_topk_mask(iso._table(es), 2, 2, iso.F32, FAKE * 8, None, FAKE * 16, 1 << 30, None) == \
         _lib.ERR_UNSUPPORTED
     n_alone = iso.iso_workspace_size(iso.OP_TOPK, [entry(), entry()], 2, iso.BF16)
-    assert iso.iso_workspace_size(iso.OP_TOPK, es, 2, iso.BF16) >= n_alone + 2 * 32768 * 4
+    assert iso.iso_workspace_size(iso.OP_TOPK, es, 2, iso.BF16) >= n_alone + 2 * 32768 * 8
+
+
+def test_group_beyond_32_bits():
+    """A joint selection over more than 2^32 entries (a whole-model delta at 7B scale): three
+    members of 2^31 entries, group count 2^32 + 5.  The planner accepts it (64-bit group bins)
+    and sizes its workspace; a count above the group's size is still rejected, and so is an
+    overflowing sum of member counts."""
+    es = [entry(rows=1 << 16, cols=1 << 15, k=0) for _ in range(3)]
+    for e in es:
+        e.group = 1
+    es[0].k = (1 << 32) + 5
+    assert call_topk(es, 2, ws_bytes=100) == _lib.ERR_WORKSPACE
+    need = iso.iso_workspace_size(iso.OP_TOPK, es, 2, iso.BF16)
+    assert need >= 2 * 32768 * 8
+    es[1].k = 3 * (1 << 31) - es[0].k + 1
+    assert call_topk(es, 2, ws_bytes=100) == _lib.ERR_INVALID_ARG
+    es[1].k = (1 << 63) - 1                                     # the member sum saturates
+    assert call_topk(es, 2, ws_bytes=100) == _lib.ERR_INVALID_ARG
 
 
 def test_workspace_sizes():
@@ -195,3 +213,23 @@ def test_muon_validation():
     assert L.iso_optimizer_step_muon(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 1 << 30, None) == _lib.ERR_INVALID_ARG
     f[0].m_u = FAKE + 0x3000 + 4
     assert L.iso_optimizer_step_muon(f, 1, iso.F32, ctypes.byref(o), FAKE * 16, 1 << 30, None) == _lib.ERR_ALIGNMENT
+
+
+def test_spectral_error_validation():
+    L = _lib.load()
+    t = iso._table([entry(K=1, out=False)])
+
+    def call(self_recon=0, out=FAKE * 8, table=t, n_t=1, ws_bytes=1 << 30):
+        return L.iso_spectral_error(table, n_t, iso.F32, self_recon, out, FAKE * 16, ws_bytes, None)
+
+    assert call(self_recon=2) == _lib.ERR_INVALID_ARG
+    assert call(self_recon=-1) == _lib.ERR_INVALID_ARG
+    assert call(out=None) == _lib.ERR_INVALID_ARG
+    assert call(out=FAKE * 8 + 4) == _lib.ERR_ALIGNMENT
+    assert call(ws_bytes=100) == _lib.ERR_WORKSPACE
+    assert call(n_t=0) == _lib.OK
+    nodelta = iso._table([iso.Entry(16, 16, base=FAKE, deltas=[None], out=None, k=0)])
+    assert call(table=nodelta) == _lib.ERR_INVALID_ARG          # W_rec is required unless self_recon
+    assert call(self_recon=1, table=nodelta, ws_bytes=100) == _lib.ERR_WORKSPACE
+    big = iso._table([iso.Entry(16385, 8, base=FAKE, deltas=[FAKE + 0x1000], out=None, k=0)])
+    assert call(table=big) == _lib.ERR_UNSUPPORTED

@@ -6,12 +6,14 @@ for bf16, the two-pass path for fp32), as bench.py times it; iso_topk_mask is al
 whole stack.  Every tensor's descriptors (the 545M-entry embeddings included) must satisfy what
 holds at any size: n_above + tie_quota = k, a cutoff inside the tensor, the threshold key at most
 the largest key.  Sampled tensors are then checked against the oracle: their base and K deltas
-are regenerated on the host, the oracle's TopKMask descriptors are computed over the whole delta
-(partial selection), the GPU descriptors must equal them, and the merged weights must equal the
+are regenerated on the host, the oracle's TopKMask descriptors are computed over the whole delta,
+the GPU descriptors must equal them, and the merged weights must equal the
 oracle's bit for bit -- on every coordinate for the Tiny and single-layer workloads, and for the
 1.5B and 7B stacks on a million random coordinates per tensor, a window around every delta's tie
 cutoff and the ragged tail.  The sampled tensors are one of each shape class (GQA k, attention
-square, MLP) small enough for the oracle's time budget.
+square, both MLP orientations) and, for the 1.5B and 7B stacks, the 10^8-entry embedding and
+unembedding matrices; bf16 descriptors come from the oracle's linear-time counting form (pinned
+against brute force and partial selection), fp32 ones from partial selection.
 """
 from concurrent.futures import ThreadPoolExecutor
 
@@ -30,8 +32,8 @@ pytestmark = pytest.mark.gpu
 CASES = [
     ("tiny", [0], "all"),
     ("layer", [1, 4, 6], "all"),
-    ("1.5b", [1, 3, 4, 6], "sample"),
-    ("7b", [1, 3, 4], "sample"),
+    ("1.5b", [1, 3, 4, 6, 196], "sample"),
+    ("7b", [1, 3, 4, 6, 196, 197], "sample"),
 ]
 
 
@@ -64,6 +66,13 @@ def _sample_idx(rng, n, descs):
     return np.unique(np.concatenate(parts))
 
 
+def _descriptor(d, k, sdt):
+    if sdt == "bf16":
+        return ties.topk_descriptor_counting(d, k)
+    return ties.topk_descriptor(d, k, sdt)
+
+
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name,picks,how", CASES, ids=[c[0] for c in CASES])
 def test_full_workload(name, picks, how):
     import torch
@@ -94,10 +103,10 @@ def test_full_workload(name, picks, how):
     for t in picks:
         spec, e = wl.tensors[t], entries[t]
         say(f"full-size {name}: {spec.name} {spec.rows}x{spec.cols}")
-        base = synth.fill_host(wl, t, 0)
-        ds = [synth.fill_host(wl, t, 1 + i) for i in range(wl.K)]
+        base = synth.fill_host(wl, t, 0, threads=8)
+        ds = [synth.fill_host(wl, t, 1 + i, threads=8) for i in range(wl.K)]
         with ThreadPoolExecutor(wl.K) as ex:
-            want = list(ex.map(lambda d: ties.topk_descriptor(d, e.k, sdt), ds))
+            want = list(ex.map(lambda d: _descriptor(d, e.k, sdt), ds))
         for i in range(wl.K):
             g = gdesc[t * wl.K + i]
             assert (g[0], g[2], g[3], g[4]) == want[i], (spec.name, i)

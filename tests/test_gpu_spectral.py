@@ -192,3 +192,47 @@ def test_whole_layer_one_call():
         assert np.allclose(coef[t], ref["c"], rtol=1e-9, atol=1e-12), wl.tensors[t].name
     assert np.all((coef >= 0.0) & (coef <= 1.5))
 
+
+
+def test_sign_zero_inner_product():
+    """sign(0) := 1 in the joint canonicalisation (App. E).  W_0 = [diag(8..1); 0] (12 x 8) and an
+    expert W_1 = R W_0 with R turning the planes (e_1, e_2) and (e_3, e_10) by pi/2: its columns
+    8 e_2, -7 e_1, 6 e_10, 5 e_4, ... are mutually orthogonal, so one-sided Jacobi rotates nothing
+    and its factors are the normalised columns U_1 = [e_2, -e_1, e_10, e_4 .. e_8], V_1 = I -- the
+    gauge the canonicalisation sees.  Modes 1-3 then have <u_0k, u_1k> = 0 exactly and must be
+    kept as they are.  A second, generic expert makes the Gram system 2 x 2.  The results of
+    zeroing those modes (sign(0) = 0) or flipping them (sign(0) = -1) are far from the answer."""
+    m, n = 12, 8
+    s0 = np.arange(n, 0, -1).astype(np.float64)
+    w0 = np.zeros((m, n))
+    w0[:n, :n] = np.diag(s0)
+    rmat = np.eye(m)
+    for a, b in ((0, 1), (2, 9)):
+        rmat[:, [a, b]] = 0.0
+        rmat[b, a], rmat[a, b] = 1.0, -1.0
+    w1 = rmat @ w0
+    rng = np.random.default_rng(12)
+    d2 = (rng.standard_normal((m, n)) * 0.05).astype(np.float32).astype(np.float64)
+    base = w0.astype(np.float32).ravel()
+    ds = [(w1 - w0).astype(np.float32).ravel(), d2.astype(np.float32).ravel()]
+    u = Unit(m, n, base, ds, "f32")
+    say("spectral sign(0) := 1, 12x8 K=2")
+    outs, coef, st = run_spectral([u], 2, "f32")
+    assert st == 0
+    u0 = np.eye(m)[:, :n]
+    u1 = w1 / s0                                        # normalised columns
+    assert np.all(np.sum(u0[:, :3] * u1[:, :3], axis=0) == 0.0)
+    e2 = sp.thin_svd(w0 + d2)
+
+    def cand(scale):
+        uu, vv = u1.copy(), np.eye(n)
+        uu[:, :3] *= scale
+        vv[:, :3] *= scale
+        return sp.iso_merge_factors(u0, s0, np.eye(n), [(uu, s0, vv), e2])
+
+    ref = cand(1.0)
+    assert _close(outs[0], "f32", ref["w_star"])
+    assert np.allclose(coef[0], ref["c"], rtol=1e-9, atol=1e-12)
+    got = outs[0].astype(np.float64).reshape(m, n)
+    for wrong in (cand(0.0), cand(-1.0)):
+        assert np.max(np.abs(got - wrong["w_star"])) > 0.1

@@ -165,3 +165,38 @@ def test_worked_example_with_known_frames():
     assert u["R"] < 1e-13
     assert abs(u["iso"] - np.sqrt(2.0) / den) < 1e-13
     assert abs(u["gap"] - 1.0) < 1e-13                  # min(2 - 1, 3 - 1/2)
+
+
+def _orth(rng, n):
+    q, r = np.linalg.qr(rng.standard_normal((n, n)))
+    return q * np.sign(np.diag(r))
+
+
+def test_spectral_error_zero_for_orthogonal_equivalence():
+    """eps_sigma (App. G) vanishes for W_rec = P W_0 Q with P, Q orthogonal: the spectrum is an
+    orthogonal invariant."""
+    rng = np.random.default_rng(21)
+    for m, n in [(30, 20), (20, 30), (16, 16)]:
+        w0 = rng.standard_normal((m, n))
+        w_rec = _orth(rng, m) @ w0 @ _orth(rng, n)
+        assert sp.spectral_error(w0, w_rec) < 1e-28
+
+
+def test_spectral_error_closed_forms():
+    """W_rec = W_0 + t u_k v_k^T moves sigma_k to sigma_k + t and leaves the rest (t small enough to
+    keep the order): eps_sigma = t^2 / q.  W_rec = c W_0 scales every value: eps_sigma =
+    (c - 1)^2 |W_0|_F^2 / q.  A dropped 1/q, a dropped square or an unsorted spectrum fails one
+    of these."""
+    rng = np.random.default_rng(22)
+    for m, n in [(40, 25), (25, 40)]:
+        w0 = rng.standard_normal((m, n))
+        u, s, v = sp.thin_svd(w0)
+        q = min(m, n)
+        for k, t in [(0, 0.75), (3, -0.01), (q - 1, 0.002)]:
+            w_rec = w0 + t * np.outer(u[:, k], v[:, k])
+            assert np.isclose(sp.spectral_error(w0, w_rec), t * t / q, rtol=1e-9, atol=0)
+        c = 1.3
+        assert np.isclose(sp.spectral_error(w0, c * w0), (c - 1) ** 2 * np.sum(w0 ** 2) / q, rtol=1e-12)
+    # the exact reconstruction has the base's spectrum up to rounding
+    w0 = rng.standard_normal((64, 48))
+    assert sp.spectral_error(w0, sp.svd_reconstruction(w0)) < 1e-26

@@ -162,3 +162,27 @@ def test_trailing_modes_are_masked():
     assert kk == 10
     for xu in res["xu_masked"]:
         assert np.all(xu[:, kk:] == 0) and np.any(xu[:, :kk] != 0)
+
+
+def test_sign_zero_inner_product_keeps_the_expert_gauge():
+    """sign(0) := 1 in the joint canonicalisation (App. E): an expert mode whose left singular
+    vector is orthogonal to the base's is left as the SVD returned it.  W_0 = diag(2, 1) and an
+    expert with U_1 = [e_2, -e_1], V_1 = I (W_1 = R(pi/2) W_0): both inner products are 0.  By
+    hand: xi_U = skew(U_1 - I) = [[0, -1], [1, 0]], xi_V = 0, g = xi_U Sigma_0 = [[0, -1], [2, 0]],
+    Gamma = 5, c = 5 / (5 + ridge), U_* = polar(I + c xi_U) = R(atan c), W_* = R(atan c) W_0.
+    Zeroing the mode (sign(0) = 0) would return W_0; flipping it (sign(0) = -1) R(-atan c) W_0."""
+    s0 = np.array([2.0, 1.0])
+    u0 = np.eye(2)
+    u1 = np.array([[0.0, -1.0], [1.0, 0.0]])
+    uc, vc = sp.canonicalize(u0, u1, np.eye(2))
+    assert np.array_equal(uc, u1) and np.array_equal(vc, np.eye(2))
+    res = sp.iso_merge_factors(u0, s0, np.eye(2), [(u1, s0.copy(), np.eye(2))], rho_keep=1.0)
+    c = 5.0 / (5.0 + 1e-12)
+    assert abs(res["gram"][0, 0] - 5.0) < 1e-14 and abs(res["c"][0] - c) < 1e-14
+    want = rot(math.atan(c)) @ np.diag(s0)
+    assert np.allclose(res["w_star"], want, rtol=0, atol=1e-14)
+    assert not np.allclose(res["w_star"], np.diag(s0), atol=0.1)
+    assert not np.allclose(res["w_star"], rot(-math.atan(c)) @ np.diag(s0), atol=0.1)
+    # an inner product of -0.0 (a sum of signed zeros) is a zero as well
+    uc, _ = sp.canonicalize(np.array([[0.0], [1.0]]), np.array([[-1.0], [0.0]]), np.array([[1.0]]))
+    assert np.array_equal(uc, np.array([[-1.0], [0.0]]))

@@ -64,6 +64,25 @@ def test_descriptor_form_equals_sort_form(dtype):
             assert d[1] + d[2] == k and d[2] >= 1
 
 
+def test_counting_descriptor_equals_brute_force_and_partial_selection():
+    """The linear-time counting form (used on the 10^8-10^9-entry tensors of the whole-stack
+    checks) gives the partial-selection descriptor and the brute-force mask, ties, zeros,
+    subnormals, k = 0, k = N and k > nnz included."""
+    rng = np.random.default_rng(14)
+    for it in range(300):
+        n = int(rng.integers(1, 2500))
+        x = _tie_heavy(rng, n, "bf16") if rng.random() < 0.7 else _store(rng.standard_normal(n), "bf16")
+        k = int(rng.choice([0, n, int(rng.integers(0, n + 1))]))
+        d = ties.topk_descriptor_counting(x, k)
+        assert d == ties.topk_descriptor(x, k, "bf16")
+        want = _brute_topk(list(nm.to_f64(x, "bf16")), k) if n <= 200 else ties.topk_mask(x, k, "bf16")
+        assert np.array_equal(ties.mask_from_descriptor(x, d, "bf16"), want)
+    with pytest.raises(FloatingPointError):
+        ties.topk_descriptor_counting(np.array([0x3F80, 0x7F80], dtype=np.uint16), 1)
+    with pytest.raises(ValueError):
+        ties.topk_descriptor_counting(np.zeros(4, dtype=np.uint16), 5)
+
+
 def test_topk_invariants_and_scale_invariance():
     rng = np.random.default_rng(5)
     for _ in range(50):

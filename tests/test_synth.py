@@ -77,3 +77,10 @@ def test_streams_differ():
                                     ("7b", 7615283200)])
 def test_workload_sizes(name, n):
     assert synth.workload(name).numel == n
+
+
+def test_threaded_fill_is_the_sequential_fill():
+    wl = synth.layer()
+    a = synth.fill_host(wl, 1, 2, first=77, n=(3 << 20) + 5)
+    b = synth.fill_host(wl, 1, 2, first=77, n=(3 << 20) + 5, threads=3)
+    assert np.array_equal(a, b)
