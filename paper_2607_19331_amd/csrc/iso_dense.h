@@ -252,9 +252,11 @@ __global__ void __launch_bounds__(256) k_bjacobi_round(const JacobiJob* __restri
   if (pr >= nbp / 2) return;
   const int bx = (pr == 0) ? 0 : 1 + (pr - 1 + round) % (nbp - 1);
   const int by = 1 + (nbp - 2 - pr + round) % (nbp - 1);
-  if (bx >= nb || by >= nb) return;
-  const int c0 = min(bx, by) * w, c1 = max(bx, by) * w;
-  const int n0 = min(w, c - c0), n1 = min(w, c - c1), nc = n0 + n1;
+  // a block paired with the phantom sweeps its own column pairs (a job of one block has no other
+  // pairs at all)
+  const bool alone = bx >= nb || by >= nb;
+  const int c0 = min(bx, by) * w, c1 = alone ? c0 : max(bx, by) * w;
+  const int n0 = min(w, c - c0), n1 = alone ? 0 : min(w, c - c1), nc = n0 + n1;
   double* A = bsh;                                  // nc columns of r
   double* V = bsh + (int64_t)2 * w * r;             // nc columns of c
   auto gcol = [&](int l) { return (l < n0) ? c0 + l : c1 + (l - n0); };
@@ -382,9 +384,9 @@ __global__ void __launch_bounds__(256) k_bjacobi_gram(const JacobiJob* __restric
   if (pr >= nbp / 2) return;
   const int bx = (pr == 0) ? 0 : 1 + (pr - 1 + round) % (nbp - 1);
   const int by = 1 + (nbp - 2 - pr + round) % (nbp - 1);
-  if (bx >= nb || by >= nb) return;
-  const int c0 = min(bx, by) * kGW, c1 = max(bx, by) * kGW;
-  const int n0 = min(kGW, c - c0), n1 = min(kGW, c - c1), nc = n0 + n1;
+  const bool alone = bx >= nb || by >= nb;        // paired with the phantom: the block's own pairs
+  const int c0 = min(bx, by) * kGW, c1 = alone ? c0 : max(bx, by) * kGW;
+  const int n0 = min(kGW, c - c0), n1 = alone ? 0 : min(kGW, c - c1), nc = n0 + n1;
   if (threadIdx.x < kGN) gc[threadIdx.x] = (threadIdx.x < n0) ? c0 + threadIdx.x : c1 + (threadIdx.x - n0);
   if (threadIdx.x == 0) { s_need = 0; s_rot = 0; }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
@@ -454,11 +456,11 @@ __device__ __forceinline__ GramPair gram_pair_of(int c, int pr, int round) {
   if (round >= nbp - 1 || pr >= nbp / 2) return P;
   const int bx = (pr == 0) ? 0 : 1 + (pr - 1 + round) % (nbp - 1);
   const int by = 1 + (nbp - 2 - pr + round) % (nbp - 1);
-  if (bx >= nb || by >= nb) return P;
+  const bool alone = bx >= nb || by >= nb;        // paired with the phantom: the block's own pairs
   P.c0 = min(bx, by) * kGW;
-  P.c1 = max(bx, by) * kGW;
+  P.c1 = alone ? P.c0 : max(bx, by) * kGW;
   P.n0 = min(kGW, c - P.c0);
-  P.nc = P.n0 + min(kGW, c - P.c1);
+  P.nc = P.n0 + (alone ? 0 : min(kGW, c - P.c1));
   P.ok = 1;
   return P;
 }

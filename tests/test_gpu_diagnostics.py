@@ -16,7 +16,7 @@ from tests.gpu_helpers import Unit, dt_code, from_dev, say
 
 pytestmark = pytest.mark.gpu
 
-SHAPES = [(96, 64, "f32"), (48, 80, "f32"), (130, 65, "bf16"), (512, 384, "bf16")]
+SHAPES = [(96, 64, "f32"), (48, 80, "f32"), (10, 6, "f32"), (130, 65, "bf16"), (512, 384, "bf16"), (7, 20, "bf16")]
 
 
 def _units(rng):

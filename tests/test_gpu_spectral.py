@@ -73,8 +73,12 @@ def test_tiny_workload():
     assert np.allclose(s, ref["s0"], rtol=1e-5)
 
 
+# the small shapes have one column block (q <= 16 on the LDS path, q <= 32 on the Gram path for the
+# 1500-long columns): its pairs are swept by the block paired with the phantom block
 @pytest.mark.parametrize("rows,cols,K,dtype", [(96, 64, 2, "f32"), (48, 80, 3, "f32"), (64, 64, 1, "bf16"),
-                                               (130, 65, 4, "bf16"), (33, 17, 2, "f32")])
+                                               (130, 65, 4, "bf16"), (33, 17, 2, "f32"), (12, 8, 2, "f32"),
+                                               (16, 16, 3, "bf16"), (5, 3, 2, "f32"), (9, 1, 2, "f32"),
+                                               (1500, 24, 2, "f32"), (20, 1500, 2, "f32")])
 def test_shapes(rows, cols, K, dtype):
     rng = np.random.default_rng(rows * 1000 + cols)
     u = _unit(rng, rows, cols, K, dtype)

@@ -55,7 +55,7 @@ def _unit(rng, m, n, dtype, scale=1e-3):
 @pytest.mark.parametrize("dtype,frac", [("f32", 0.9), ("f32", 0.5), ("bf16", 0.9), ("bf16", 1.0)])
 def test_ratios_match_the_oracle(dtype, frac):
     rng = np.random.default_rng(int(frac * 10) + (0 if dtype == "f32" else 100))
-    shapes = [(96, 64), (48, 80), (33, 17), (0, 0), (130, 65), (512, 384)]
+    shapes = [(96, 64), (48, 80), (33, 17), (0, 0), (130, 65), (512, 384), (14, 9)]
     empty = np.zeros(0, np.float32 if dtype == "f32" else np.uint16)
     units = [_unit(rng, m, n, dtype) if m else Unit(0, 0, empty, [empty], dtype) for m, n in shapes]
     say(f"transport ratios {dtype} rank_frac {frac}: {shapes}")
