@@ -218,6 +218,28 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
 #define ISO_SPECTRAL_MAX_DIM 16384
 
 /*
+ * iso_update without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, modes and results as iso_update;
+ * the workspace is a fixed block of ISO_NOALLOC_SCRATCH_BYTES of static device
+ * memory per GPU, which the library holds until the process ends.  The call
+ * allocates nothing.  A call whose workspace (iso_workspace_size of its mode)
+ * exceeds the block is rejected with ISO_ERR_UNSUPPORTED before anything is
+ * queued; 64 MiB covers, e.g., a fused TopKMask + TIES update of one tensor of
+ * about 6M bf16 entries with K = 4.
+ * scratch_out (nullable) receives the device address of the current device's
+ * block: pass it as the workspace of iso_read_device_status and
+ * iso_read_fallback_count after the call.  Every call on one GPU shares that
+ * GPU's block, which keeps the last call's contents: calls that overlap on one
+ * GPU (other streams or threads) race and must be serialised by the caller.
+ * Profiling events (iso_profile_begin) are not recorded by this entry point.
+ */
+#define ISO_NOALLOC_SCRATCH_BYTES (64ull << 20)
+
+iso_status iso_update_noalloc(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_update_args* a,
+                              void** scratch_out, void* stream);
+
+/*
  * Spectral drift diagnostics (Sec. 3), per tensor, in binary64: base = W_0,
  * deltas[0] = Delta W (W_1 = W_0 + Delta W).  out is a device array of 3 n_t
  * doubles, per tensor {delta_Sigma, rho_Sigma, kappa_spec}:

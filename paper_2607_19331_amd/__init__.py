@@ -136,6 +136,25 @@ def iso_update(entries, K, dtype, mode, merge=MERGE_TIES, lam=1.0, eps=1e-5, des
     _check(rc, "iso_update")
 
 
+def iso_update_noalloc(entries, K, dtype, mode, merge=MERGE_TIES, lam=1.0, eps=1e-5, desc=None, tau_in=None,
+                       sign_out=None, rho_keep=0.9, ridge=1e-12, c_min=0.0, c_max=1.5, coef_out=None, stream=None):
+    """iso_update on the library's fixed per-device scratch block (no workspace argument); returns the
+    block's device address, to be passed as ``ws`` to iso_read_device_status / iso_read_fallback_count."""
+    a = _lib.IsoUpdateArgs()
+    a.mode, a.merge, a.lambda_, a.eps_act = mode, merge, float(lam), float(eps)
+    keep = [_ptr_array(tau_in), _ptr_array(sign_out)]
+    a.desc = _ptr(desc)
+    a.tau_in = ctypes.cast(keep[0], ctypes.c_void_p).value if keep[0] is not None else None
+    a.sign_out = ctypes.cast(keep[1], ctypes.c_void_p).value if keep[1] is not None else None
+    a.rho_keep, a.ridge, a.c_min, a.c_max = float(rho_keep), float(ridge), float(c_min), float(c_max)
+    a.coef_out = _ptr(coef_out)
+    scratch = ctypes.c_void_p()
+    rc = _lib.load().iso_update_noalloc(_table(entries), len(entries), K, dtype, ctypes.byref(a),
+                                        ctypes.byref(scratch), _stream(stream))
+    _check(rc, "iso_update_noalloc")
+    return scratch.value
+
+
 def iso_blockdiag_project(entries, K, dtype, rank, alpha, delta_hat=None, ws=None, stream=None):
     wp, wb = _ws(ws)
     rc = _lib.load().iso_blockdiag_project(_table(entries), len(entries), K, dtype, int(rank), float(alpha),

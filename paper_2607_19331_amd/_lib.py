@@ -17,7 +17,7 @@ SYMBOLS = ["iso_workspace_size", "iso_topk_mask", "iso_sign_elect", "iso_merge",
            "iso_blockdiag_project", "iso_blockdiag_project_factors", "iso_workspace_size_tsv", "iso_k_from_density", "iso_read_device_status",
            "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end", "iso_status_string",
            "iso_workspace_size_optimizer", "iso_optimizer_step", "iso_optimizer_step_muon", "iso_spectral_diagnostics",
-           "iso_spectrum_interpolate", "iso_transport_ratios", "iso_spectral_error"]
+           "iso_spectrum_interpolate", "iso_transport_ratios", "iso_spectral_error", "iso_update_noalloc"]
 
 
 class IsoTensor(ctypes.Structure):
@@ -76,6 +76,7 @@ def load():
     L.iso_sign_elect.argtypes = [T, I, I, I, P, P, P, Z, P]
     L.iso_merge.argtypes = [T, I, I, I, I, P, D, D, P, P, Z, P]
     L.iso_update.argtypes = [T, I, I, I, ctypes.POINTER(IsoUpdateArgs), P, Z, P]
+    L.iso_update_noalloc.argtypes = [T, I, I, I, ctypes.POINTER(IsoUpdateArgs), ctypes.POINTER(ctypes.c_void_p), P]
     L.iso_blockdiag_project.argtypes = [T, I, I, I, I, D, P, P, Z, P]
     L.iso_blockdiag_project_factors.argtypes = [T, I, I, I, I, D, ctypes.POINTER(IsoFactors), P, P, Z, P]
     L.iso_workspace_size_tsv.argtypes = [T, I, I, I, I]
@@ -96,7 +97,8 @@ def load():
     L.iso_transport_ratios.argtypes = [T, I, I, ctypes.POINTER(ctypes.c_double), I, P, P, Z, P]
     L.iso_status_string.argtypes = [I]
     L.iso_status_string.restype = ctypes.c_char_p
-    for fn in ("iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update", "iso_blockdiag_project",
+    for fn in ("iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update", "iso_update_noalloc",
+               "iso_blockdiag_project",
                "iso_blockdiag_project_factors", "iso_optimizer_step", "iso_optimizer_step_muon",
                "iso_spectral_diagnostics",
                "iso_spectrum_interpolate", "iso_transport_ratios", "iso_spectral_error",

@@ -14,6 +14,7 @@
 #include "iso_kernels.h"
 #include "iso_spectral.h"
 #include "iso_tsv.h"
+#include "iso_update_call.h"
 
 using namespace iso;
 
@@ -319,6 +320,20 @@ iso_status check_ws(const Layout& L, void* ws, size_t ws_bytes) {
   return ISO_OK;
 }
 
+// The workspace of a call once its layout is known: the caller's, checked, or one handed out by
+// src.acquire (which rejects a layout it cannot hold).
+iso_status take_ws(const WsSource& src, const Layout& L, uint8_t** w) {
+  void* ws = src.ws;
+  size_t bytes = src.bytes;
+  if (src.acquire != nullptr) {
+    const iso_status st = src.acquire(L.total, &ws, &bytes);
+    if (st != ISO_OK) return st;
+  }
+  const iso_status st = check_ws(L, ws, bytes);
+  if (st == ISO_OK) *w = (uint8_t*)ws;
+  return st;
+}
+
 #define HIP_TRY(x)                               \
   do {                                           \
     if ((x) != hipSuccess) return ISO_ERR_HIP;   \
@@ -473,9 +488,23 @@ iso_status iso_merge(const iso_tensor* t, int n_t, int K, iso_dtype dt, iso_merg
 
 iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_update_args* a, void* ws,
                       size_t ws_bytes, void* stream) {
+  WsSource src;
+  src.ws = ws;
+  src.bytes = ws_bytes;
+  return update_call(t, n_t, K, dt, a, src, stream);
+}
+
+}  // extern "C"
+
+namespace iso {
+
+// The body of iso_update.  Arguments are validated first; the workspace is then taken from src
+// (the caller's, or the fixed per-device block of iso_update_noalloc) once its size is known.
+iso_status update_call(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_update_args* a,
+                       const WsSource& src, void* stream) {
   if (a == nullptr) return ISO_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
-  uint8_t* w = (uint8_t*)ws;
+  uint8_t* w = nullptr;
   iso_status st;
   if (a->mode == ISO_UPDATE_APPLY) {
     Need nd;
@@ -485,7 +514,7 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
     if (n_t == 0) return ISO_OK;
     if ((st = check_ptr_array((const void* const*)a->tau_in, n_t, true)) != ISO_OK) return st;
     Layout L = plan(ISO_OP_UPDATE_APPLY, t, n_t, 1, dt);
-    if ((st = check_ws(L, ws, ws_bytes)) != ISO_OK) return st;
+    if ((st = take_ws(src, L, &w)) != ISO_OK) return st;
     HIP_TRY(start_call(w, s));
     HIP_TRY(upload(L, t, n_t, 1, dt, w, (void* const*)a->tau_in, nullptr, nullptr, 0, s));
     HIP_TRY(run_apply((const DevTensor*)(w + L.table), n_t, dt, a->lambda, L.tiles, (uint32_t*)w, s));
@@ -505,7 +534,7 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
     if (want_sign && (st = check_ptr_array((const void* const*)a->sign_out, n_t, true)) != ISO_OK) return st;
     const bool inner_select = ties && a->desc == nullptr;
     Layout L = plan(inner_select ? ISO_OP_UPDATE_FUSED_SELECT : ISO_OP_UPDATE_FUSED, t, n_t, K, dt);
-    if ((st = check_ws(L, ws, ws_bytes)) != ISO_OK) return st;
+    if ((st = take_ws(src, L, &w)) != ISO_OK) return st;
     HIP_TRY(start_call(w, s));
     HIP_TRY(upload(L, t, n_t, K, dt, w, nullptr, want_sign ? (void* const*)a->sign_out : nullptr, nullptr, 0, s));
     MergePlan mp;
@@ -542,7 +571,7 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
       fp.status = (uint32_t*)w;
       fp.sel = select_plan(L, w, n_t, K, dd);
       fp.mrg = mp;
-      prof_take(fp.prof);
+      if (!src.acquire) prof_take(fp.prof);
       HIP_TRY(run_fused(fp, s));
       return ISO_OK;
     }
@@ -551,7 +580,7 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
       HIP_TRY(do_select(L, w, n_t, K, dt, dd, s));
       mp.desc = dd;
     }
-    prof_take(mp.prof);
+    if (!src.acquire) prof_take(mp.prof);
     HIP_TRY(run_merge(mp, dt, s));
     return ISO_OK;
   }
@@ -566,7 +595,7 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
     if (a->coef_out != nullptr && ((uintptr_t)a->coef_out & 7u) != 0) return ISO_ERR_ALIGNMENT;
     if (n_t == 0) return ISO_OK;
     Layout L = plan(ISO_OP_UPDATE_SPECTRAL, t, n_t, K, dt);
-    if ((st = check_ws(L, ws, ws_bytes)) != ISO_OK) return st;
+    if ((st = take_ws(src, L, &w)) != ISO_OK) return st;
     HIP_TRY(start_call(w, s));
     SpectralArgs sa;
     sa.rho_keep = a->rho_keep;
@@ -578,6 +607,10 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
   }
   return ISO_ERR_INVALID_ARG;
 }
+
+}  // namespace iso
+
+extern "C" {
 
 static iso_status check_tsv(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank, bool ptrs) {
   Need nd;

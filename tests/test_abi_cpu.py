@@ -233,3 +233,19 @@ def test_spectral_error_validation():
     assert call(self_recon=1, table=nodelta, ws_bytes=100) == _lib.ERR_WORKSPACE
     big = iso._table([iso.Entry(16385, 8, base=FAKE, deltas=[FAKE + 0x1000], out=None, k=0)])
     assert call(table=big) == _lib.ERR_UNSUPPORTED
+
+
+def test_noalloc_validation():
+    """iso_update_noalloc checks its arguments as iso_update does and refuses, before anything is
+    queued, a call whose workspace exceeds the fixed block."""
+    L = _lib.load()
+    a = _lib.IsoUpdateArgs()
+    a.mode, a.merge, a.lambda_, a.eps_act = iso.UPDATE_FUSED, iso.MERGE_TIES, 1.0, 1e-5
+    t = iso._table([entry(rows=16, cols=16, k=10, K=2)])
+    assert L.iso_update_noalloc(t, 1, 2, iso.BF16, None, None, None) == _lib.ERR_INVALID_ARG
+    assert L.iso_update_noalloc(t, 1, 9, iso.BF16, ctypes.byref(a), None, None) == _lib.ERR_INVALID_ARG
+    assert L.iso_update_noalloc(iso._table([entry(misalign=True)]), 1, 2, iso.BF16, ctypes.byref(a), None,
+                                None) == _lib.ERR_ALIGNMENT
+    big = iso._table([entry(rows=4096, cols=4096, k=10, K=4)])
+    assert L.iso_update_noalloc(big, 1, 4, iso.BF16, ctypes.byref(a), None, None) == _lib.ERR_UNSUPPORTED
+    assert L.iso_update_noalloc(t, 0, 2, iso.BF16, ctypes.byref(a), None, None) == _lib.OK
