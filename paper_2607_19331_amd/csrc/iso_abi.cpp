@@ -214,7 +214,7 @@ Layout plan(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
     L.tflag = off;
     off = align_up(off + sizeof(int) * (size_t)n_t, 256);
     L.tstat = off;
-    off = align_up(off + sizeof(uint32_t) * kFusedStat * (size_t)L.tiles * K, 256);
+    off = align_up(off + sizeof(uint16_t) * fused_stat_words(K) * (size_t)L.tiles, 256);
     L.tinfo = off;
     off = align_up(off + sizeof(uint2) * (size_t)L.tiles, 256);
     L.csum = off;
@@ -559,7 +559,7 @@ iso_status update_call(const iso_tensor* t, int n_t, int K, iso_dtype dt, const 
       fp.groups = L.groups;
       fp.fu = (FusedUnit*)(w + L.fu);
       fp.tflag = (int*)(w + L.tflag);
-      fp.tstat = (uint32_t*)(w + L.tstat);
+      fp.tstat = (uint16_t*)(w + L.tstat);
       fp.tinfo = (uint2*)(w + L.tinfo);
       fp.rec = (uint32_t*)(w + L.rec);
       fp.tile_cap = L.tile_cap;

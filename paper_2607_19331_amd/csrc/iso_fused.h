@@ -15,6 +15,10 @@ constexpr int kFusedGroupTiles = 64;           // tiles per fix-up workgroup
 constexpr int kFusedReduceTiles = 1024;        // tiles per reduction item
 constexpr int kFusedMaxTensors = 65535;        // records carry a 16-bit tensor id
 
+// Tile statistics: K * kFusedStat 16-bit counts per tile (a tile holds 4096 coordinates, so no
+// count exceeds 4096), padded to a multiple of 8 so that each tile's block is 16-byte aligned.
+constexpr int fused_stat_words(int K) { return (K * kFusedStat + 7) / 8 * 8; }
+
 // Per (tensor, delta) state.
 struct FusedUnit {
   uint32_t lo, hi, prov;   // bracket [lo, hi] of magnitude keys and the provisional threshold
@@ -38,7 +42,7 @@ struct FusedPlan {
   int64_t tiles, groups;   // groups: runs of up to kFusedGroupTiles tiles of one tensor (fix-up work)
   FusedUnit* fu;           // n_t * K
   int* tflag;              // n_t: nonzero sends the tensor to the exact two-pass path
-  uint32_t* tstat;         // tiles * K * kFusedStat
+  uint16_t* tstat;         // tiles * fused_stat_words(K): per tile, delta-major counts
   uint2* tinfo;            // tiles: {records, 1 if the tile is to be merged again in binary64}
   uint32_t* rec;           // tiles * tile_cap records of fused_record_bytes(K)
   int64_t tile_cap;

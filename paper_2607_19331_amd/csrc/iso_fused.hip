@@ -357,7 +357,8 @@ struct MainArgs {
   int n_t;
   const FusedUnit* fu;
   int* tflag;
-  uint32_t* tstat;
+  uint16_t* tstat;
+  uint32_t one2;           // 0x00010001, passed in so that min(d, 1) stays one packed min
   uint2* tinfo;
   uint32_t* rec;
   int64_t tile_cap;
@@ -377,7 +378,10 @@ k_fs_main(MainArgs a) {
   __shared__ uint32_t s_wtot[kThreads / 64];
   __shared__ double2 rtab[K + 1];                   // {RN(1/n) / 2, 2n}
   __shared__ float rtab32[K + 1];                   // 1 / 2n for n a power of two, else NaN; 0 for n = 0
-  __shared__ uint4 s_rec[kTileCapK<K> * (RW / 4)];   // the tile's records, staged
+  // the tile's deferred coordinates as staged, one array per word: the K delta words and the
+  // base word of the coordinate's pair, then its offset in the tile (bit 0: which half).  Word
+  // arrays (not one record per slot) so that every word is stored from the register it is in.
+  __shared__ uint32_t s_raw[K + 2][kTileCapK<K> + 1];
   __shared__ int s_skip, s_redo;
   const int64_t tile = blockIdx.x;
   const int j = find_tensor_mapped(a.tab, a.tmap, a.n_t, tile);
@@ -386,8 +390,21 @@ k_fs_main(MainArgs a) {
   // the stream loads first: nothing below delays their issue
   const int64_t n = T.n, nvec = n / 8;
   const int64_t vbeg = (tile - T.tile0) * (int64_t)(kThreads * kVPT);
+  // every vector of the tile whole (all tiles but a tensor's last): the addresses are a uniform
+  // tile base plus the thread's 32-bit offset
+  const bool full = vbeg + kThreads * kVPT <= nvec;
   uint4 dv[kVPT][K], wv[kVPT];
   int nv[kVPT];                                    // valid elements in this thread's vector q
+  if (full) {
+#pragma unroll
+    for (int q = 0; q < kVPT; ++q) {
+      nv[q] = 8;
+      const int64_t v0 = vbeg + (int64_t)q * kThreads;
+#pragma unroll
+      for (int i = 0; i < K; ++i) dv[q][i] = ld_stream(((const uint4*)T.deltas[i] + v0) + threadIdx.x);
+      wv[q] = ld_stream(((const uint4*)T.base + v0) + threadIdx.x);
+    }
+  } else {
 #pragma unroll
   for (int q = 0; q < kVPT; ++q) {
     const int64_t vi = vbeg + (int64_t)q * kThreads + threadIdx.x;
@@ -411,6 +428,7 @@ k_fs_main(MainArgs a) {
       for (int i = 0; i < K; ++i) dv[q][i] = make_uint4(tmp[i][0], tmp[i][1], tmp[i][2], tmp[i][3]);
       wv[q] = make_uint4(tmp[K][0], tmp[K][1], tmp[K][2], tmp[K][3]);
     }
+  }
   }
   // another block may flag this tensor while this one runs: one read, shared by the block
   if (threadIdx.x == 0) {
@@ -458,7 +476,7 @@ k_fs_main(MainArgs a) {
         d = pk_min(d, pk_subsat(pk_sub(key, lo1x2[i]), wm1x2[i]));
       }
       dm[q][h] = d;
-      nd = __builtin_amdgcn_sad_u16(pk_min(d, 0x00010001u), 0u, nd);   // + nonzero halves
+      nd = __builtin_amdgcn_sad_u16(pk_min(d, a.one2), 0u, nd);   // + nonzero halves
     }
     ndef[q] = 8u - nd;
   }
@@ -487,37 +505,23 @@ k_fs_main(MainArgs a) {
     if (!rec_ok) atomicOr(&a.tflag[j], kFlagFull);
   }
   if (rec_ok) {
-    // stage each deferred coordinate's record: halfwords 0-1 index, 2 tensor, 3.. deltas, base
+    // stage each deferred coordinate: the raw words of its pair (no VALU work on them) and its
+    // offset; the record itself is built when the staged slots are written out, by the few
+    // lanes that cover the tile's records
 #pragma unroll
     for (int q = 0; q < kVPT; ++q) {
       uint32_t slot = (q == 0) ? (excl & 0xFFFFu) : tot0 + (excl >> 16);
-      const uint32_t i0 = (uint32_t)((vbeg + (int64_t)q * kThreads + threadIdx.x) * 8);
+      const uint32_t lofs = (uint32_t)(q * kThreads + threadIdx.x) * 8u;
 #pragma unroll
       for (int h = 0; h < 4; ++h) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
           const bool def = ((dm[q][h] >> (16 * c)) & 0xFFFFu) == 0u;
           if (def) {                               // rare per lane: waves with no such lane skip the site
-            // halfword 3 + x holds value x (deltas, then the base); words from 2 on pair two
-            // values, each taken from half c of its vector word with one byte permute
-            uint32_t wds[RW];
 #pragma unroll
-            for (int z = 0; z < RW; ++z) wds[z] = 0;
-            const auto val = [&](int x) { return (x < K) ? word_of(dv[q][x < K ? x : 0], h) : word_of(wv[q], h); };
-            wds[0] = i0 + (uint32_t)(2 * h + c);
-            wds[1] = c ? __builtin_amdgcn_perm(val(0), (uint32_t)j, 0x07060100u)
-                       : __builtin_amdgcn_perm(val(0), (uint32_t)j, 0x05040100u);
-#pragma unroll
-            for (int z = 2; z < RW; ++z) {
-              const int x0 = 2 * z - 3, x1 = 2 * z - 2;
-              if (x1 <= K)
-                wds[z] = __builtin_amdgcn_perm(val(x1), val(x0), c ? 0x07060302u : 0x05040100u);
-              else if (x0 <= K)
-                wds[z] = c ? (val(x0) >> 16) : (val(x0) & 0xFFFFu);
-            }
-#pragma unroll
-            for (int z = 0; z < RW / 4; ++z)
-              s_rec[slot * (RW / 4) + z] = make_uint4(wds[4 * z], wds[4 * z + 1], wds[4 * z + 2], wds[4 * z + 3]);
+            for (int i = 0; i < K; ++i) s_raw[i][slot] = word_of(dv[q][i], h);
+            s_raw[K][slot] = word_of(wv[q], h);
+            s_raw[K + 1][slot] = lofs + (uint32_t)(2 * h + c);
             ++slot;
           }
         }
@@ -556,7 +560,10 @@ k_fs_main(MainArgs a) {
       }
     }
     const int64_t vi = vbeg + (int64_t)q * kThreads + threadIdx.x;
-    if (nv[q] == 8) {
+    if (full) {
+      st_stream(make_uint4(ob[0], ob[1], ob[2], ob[3]), ((uint4*)T.out + (vbeg + (int64_t)q * kThreads)) + threadIdx.x);
+      if (SIGN) *((uint2*)T.aux2 + vi) = make_uint2(sg[0] | (sg[1] << 16), sg[2] | (sg[3] << 16));
+    } else if (nv[q] == 8) {
       st_stream(make_uint4(ob[0], ob[1], ob[2], ob[3]), (uint4*)T.out + vi);
       if (SIGN) *((uint2*)T.aux2 + vi) = make_uint2(sg[0] | (sg[1] << 16), sg[2] | (sg[3] << 16));
     } else {
@@ -587,14 +594,32 @@ k_fs_main(MainArgs a) {
   if (threadIdx.x == 0) a.tinfo[tile].y = (uint32_t)s_redo;
   if (rec_ok) {
     uint4* dst = (uint4*)(a.rec + (size_t)tile * a.tile_cap * RW);
+    const uint32_t ibase = (uint32_t)(vbeg * 8);
     for (uint32_t r = threadIdx.x; r < total; r += kThreads) {
+      // the record: halfwords 0-1 index, 2 tensor, 3 + x value x (deltas, then the base), each
+      // value taken from half c of its pair word with one byte permute
+      uint32_t v[K + 1];
+#pragma unroll
+      for (int x = 0; x <= K; ++x) v[x] = s_raw[x][r];
+      const uint32_t off = s_raw[K + 1][r], c = off & 1u;
+      const uint32_t sel_lo = c ? 0x07060100u : 0x05040100u;   // half c of word 0 over the tensor id
+      const uint32_t sel_pr = c ? 0x07060302u : 0x05040100u;   // half c of two words
       uint32_t wds[RW];
 #pragma unroll
-      for (int z = 0; z < RW / 4; ++z) {
-        const uint4 v = s_rec[r * (RW / 4) + z];
-        wds[4 * z] = v.x; wds[4 * z + 1] = v.y; wds[4 * z + 2] = v.z; wds[4 * z + 3] = v.w;
-        dst[r * (RW / 4) + z] = v;
+      for (int z = 0; z < RW; ++z) wds[z] = 0;
+      wds[0] = ibase + off;
+      wds[1] = __builtin_amdgcn_perm(v[0], (uint32_t)j, sel_lo);
+#pragma unroll
+      for (int z = 2; z < RW; ++z) {
+        const int x0 = 2 * z - 3, x1 = 2 * z - 2;
+        if (x1 <= K)
+          wds[z] = __builtin_amdgcn_perm(v[x1], v[x0], sel_pr);
+        else if (x0 <= K)
+          wds[z] = c ? (v[x0] >> 16) : (v[x0] & 0xFFFFu);
       }
+#pragma unroll
+      for (int z = 0; z < RW / 4; ++z)
+        dst[r * (RW / 4) + z] = make_uint4(wds[4 * z], wds[4 * z + 1], wds[4 * z + 2], wds[4 * z + 3]);
 #pragma unroll
       for (int i = 0; i < K; ++i) {
         const uint32_t key = (wds[(3 + i) >> 1] >> (16 * ((3 + i) & 1))) & 0x7FFFu;
@@ -613,7 +638,7 @@ k_fs_main(MainArgs a) {
     } else {
       v = hcnt[i][c - 1];
     }
-    a.tstat[((size_t)tile * K + i) * kFusedStat + c] = v;
+    a.tstat[(size_t)tile * fused_stat_words(K) + e] = (uint16_t)v;
   }
 }
 
@@ -626,46 +651,45 @@ __device__ __forceinline__ uint32_t rec_half(const uint32_t* r, int h) {
 
 __device__ __forceinline__ int64_t tensor_tiles(const DevTensor& T) { return (T.n + kTileElems - 1) / kTileElems; }
 
-__global__ void __launch_bounds__(256) k_fs_reduce(const DevTensor* __restrict__ tab, int n_t, int K,
-                                                   const int64_t* __restrict__ ritem0, const int* __restrict__ tflag,
-                                                   const uint32_t* __restrict__ tstat, uint32_t* __restrict__ csum,
-                                                   FusedUnit* __restrict__ fu) {
-  __shared__ uint32_t red[kFusedStat][4];
-  const int64_t item = blockIdx.x;
+// One workgroup per (tensor, run of kFusedReduceTiles tiles), all K deltas at once: every
+// tile's block of K * kFusedStat counts is read once, as whole contiguous lines.  Thread
+// (g, s) adds count s of the tiles g, g + G, ...; the G partial sums meet in LDS.  The run's
+// sums go to csum (delta-major per tensor, as the tie search reads them) and onto the units'
+// totals.
+template <int K>
+__global__ void __launch_bounds__(1024) k_fs_reduce(const DevTensor* __restrict__ tab, int n_t,
+                                                    const int64_t* __restrict__ ritem0, const int* __restrict__ tflag,
+                                                    const uint16_t* __restrict__ tstat, uint32_t* __restrict__ csum,
+                                                    FusedUnit* __restrict__ fu) {
+  constexpr int NS = K * kFusedStat, SW = fused_stat_words(K), G = 1024 / NS;
+  __shared__ uint32_t red[G][NS];
+  const int64_t item = blockIdx.x;                 // counts runs over all tensors: ritem0 / K
   int lo = 0, hi = n_t - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (ritem0[mid] <= item) lo = mid; else hi = mid - 1;
+    if (ritem0[mid] / K <= item) lo = mid; else hi = mid - 1;
   }
   const int j = lo;
   if (tflag[j]) return;
   const DevTensor& T = tab[j];
   const int64_t nt = tensor_tiles(T);
   const int64_t nrc = (nt + kFusedReduceTiles - 1) / kFusedReduceTiles;
-  const int64_t local = item - ritem0[j];
-  const int i = (int)(local / nrc);
-  const int64_t r = local - (int64_t)i * nrc;
+  const int64_t r = item - ritem0[j] / K;
   const int64_t t0 = T.tile0 + r * kFusedReduceTiles, t1 = T.tile0 + min(nt, (r + 1) * kFusedReduceTiles);
-  uint32_t acc[kFusedStat];
-#pragma unroll
-  for (int c = 0; c < kFusedStat; ++c) acc[c] = 0;
-  for (int64_t t = t0 + threadIdx.x; t < t1; t += blockDim.x) {
-    const uint32_t* st = tstat + ((size_t)t * K + i) * kFusedStat;
-#pragma unroll
-    for (int c = 0; c < kFusedStat; ++c) acc[c] += st[c];
-  }
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-#pragma unroll
-  for (int c = 0; c < kFusedStat; ++c) {
-    uint32_t x = acc[c];
-    for (int o = 32; o > 0; o >>= 1) x += (uint32_t)__shfl_xor((int)x, o, 64);
-    if (lane == 0) red[c][wid] = x;
+  const int g = threadIdx.x / NS, sidx = threadIdx.x % NS;
+  if (g < G) {
+    uint32_t acc = 0;
+#pragma unroll 8
+    for (int64_t t = t0 + g; t < t1; t += G) acc += tstat[(size_t)t * SW + sidx];
+    red[g][sidx] = acc;
   }
   __syncthreads();
-  if (threadIdx.x < kFusedStat) {
-    const int c = threadIdx.x;
-    const uint32_t v = red[c][0] + red[c][1] + red[c][2] + red[c][3];
-    csum[(size_t)item * kFusedStat + c] = v;
+  if (threadIdx.x < NS) {
+    uint32_t v = 0;
+#pragma unroll
+    for (int q = 0; q < G; ++q) v += red[q][threadIdx.x];
+    const int i = threadIdx.x / kFusedStat, c = threadIdx.x % kFusedStat;
+    csum[(size_t)(ritem0[j] + (int64_t)i * nrc + r) * kFusedStat + c] = v;
     FusedUnit& F = fu[j * K + i];
     if (v) {
       if (c == 0) atomicAdd((unsigned long long*)&F.kept, (unsigned long long)v);
@@ -741,7 +765,7 @@ struct TieArgs {
   const int* tflag;
   const int64_t* ritem0;
   const uint32_t* csum;
-  const uint32_t* tstat;
+  const uint16_t* tstat;
   const uint2* tinfo;
   const uint32_t* rec;
   int64_t tile_cap;
@@ -791,7 +815,8 @@ __global__ void __launch_bounds__(1024) k_fs_tiefind(TieArgs a) {
   const int64_t tn = min<int64_t>(kFusedReduceTiles, nt - rc * kFusedReduceTiles);
   {
     const int64_t t = t0 + threadIdx.x;
-    const int64_t v = (threadIdx.x < tn) ? (int64_t)a.tstat[((size_t)t * K + i) * kFusedStat + ct] : 0;
+    const int64_t v =
+        (threadIdx.x < tn) ? (int64_t)a.tstat[(size_t)t * fused_stat_words(K) + i * kFusedStat + ct] : 0;
     const int64_t incl = before_chunk + block_scan(v, sh);
     if (threadIdx.x < tn && incl - v < quota && incl >= quota) { s_pos = t; s_before = incl - v; }
   }
@@ -864,14 +889,20 @@ __device__ __forceinline__ void store_final(const DevTensor& T, int64_t idx, con
 
 // One workgroup per run of up to 64 tiles of one tensor.  Records whose final mask differs
 // from the provisional one are merged again; a tile whose binary32 sums may have rounded is
-// merged again whole, in binary64, from the inputs.
+// merged again whole, in binary64, from the inputs.  The records are read in batches of
+// 256 NB; each batch first only decides which records changed (a few integer tests per
+// record) and queues those in LDS, so that the binary64 merge runs on the changed records
+// alone, one per lane, instead of once per record position of any lane that needs it.
 template <int K>
 __global__ void __launch_bounds__(256) k_fs_fixup(FixArgs a) {
   constexpr int RW = rec_words<K>();
+  constexpr int NB = 4;                            // records in flight per thread
   __shared__ uint32_t s_pre[kFusedGroupTiles + 1];
   __shared__ uint32_t s_p1[K], s_tk[K];
   __shared__ int64_t s_cut[K];
   __shared__ int s_anyredo;
+  __shared__ uint4 s_q[NB * 256 * (RW / 4)];      // changed records of the batch
+  __shared__ uint32_t s_qn;
   const int64_t g = blockIdx.x;
   int lo = 0, hi = a.n_t - 1;                      // tensor owning run g (group0 ascending)
   while (lo < hi) {
@@ -884,7 +915,7 @@ __global__ void __launch_bounds__(256) k_fs_fixup(FixArgs a) {
   const int64_t nt = tensor_tiles(T);
   const int64_t t0 = T.tile0 + (g - T.group0) * kFusedGroupTiles;
   const int ntl = (int)min<int64_t>(kFusedGroupTiles, T.tile0 + nt - t0);
-  if (threadIdx.x == 0) s_anyredo = 0;
+  if (threadIdx.x == 0) { s_anyredo = 0; s_qn = 0; }
   __syncthreads();
   if (threadIdx.x < 64) {                          // inclusive scan of the record counts (one wave)
     const int l = threadIdx.x;
@@ -912,15 +943,13 @@ __global__ void __launch_bounds__(256) k_fs_fixup(FixArgs a) {
   const uint32_t total = s_pre[kFusedGroupTiles];
   const uint32_t* __restrict__ rec = a.rec;
   uint16_t* __restrict__ out = (uint16_t*)T.out;
-  constexpr int NB = 4;                            // records in flight per thread
+  const int lane = threadIdx.x & 63;
   int l = 0;                                       // tile of the thread's current record (advances monotonically)
-  for (uint32_t r0 = threadIdx.x; r0 < total; r0 += NB * blockDim.x) {
+  for (uint32_t r0 = 0; r0 < total; r0 += NB * 256u) {
     uint4 wv[NB][RW / 4];
-    uint32_t rr[NB];
 #pragma unroll
     for (int m = 0; m < NB; ++m) {
-      const uint32_t r = r0 + (uint32_t)m * blockDim.x;
-      rr[m] = r;
+      const uint32_t r = r0 + (uint32_t)m * 256u + threadIdx.x;
       if (r < total) {
         while (s_pre[l + 1] <= r) ++l;
         const uint4* w = (const uint4*)(rec + ((size_t)(t0 + l) * a.tile_cap + (r - s_pre[l])) * RW);
@@ -930,28 +959,60 @@ __global__ void __launch_bounds__(256) k_fs_fixup(FixArgs a) {
     }
 #pragma unroll
     for (int m = 0; m < NB; ++m) {
-      if (rr[m] >= total) break;
+      const uint32_t r = r0 + (uint32_t)m * 256u + threadIdx.x;
+      bool changed = false;
+      uint32_t kfin = 0;
+      if (r < total) {
+        uint32_t w[RW];
+#pragma unroll
+        for (int z = 0; z < RW / 4; ++z) {
+          w[4 * z] = wv[m][z].x; w[4 * z + 1] = wv[m][z].y; w[4 * z + 2] = wv[m][z].z; w[4 * z + 3] = wv[m][z].w;
+        }
+        uint32_t b[K];
+        uint32_t kprov = 0;
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+          b[i] = rec_half(w, 3 + i);
+          kprov |= (uint32_t)(bkey(b[i]) >= s_p1[i]) << i;
+        }
+        kfin = final_mask<K>(b, (int64_t)w[0], tk, cut);
+        changed = kprov != kfin;
+      }
+      // queue slot: one LDS atomic per wave, then the lane's rank among the changed lanes
+      const uint64_t mask = __ballot(changed);
+      uint32_t qbase = 0;
+      if (lane == 0 && mask) qbase = atomicAdd(&s_qn, (uint32_t)__popcll(mask));
+      qbase = (uint32_t)__shfl((int)qbase, 0, 64);
+      if (changed) {
+        const uint32_t slot = qbase + (uint32_t)__popcll(mask & ((1ull << lane) - 1ull));
+        uint4 v0 = wv[m][0];
+        v0.y = (v0.y & 0xFFFF0000u) | kfin;         // halfword 2 (the tensor id) carries the final mask
+        s_q[slot * (RW / 4)] = v0;
+#pragma unroll
+        for (int z = 1; z < RW / 4; ++z) s_q[slot * (RW / 4) + z] = wv[m][z];
+      }
+    }
+    __syncthreads();
+    const uint32_t nq = s_qn;
+    for (uint32_t qi = threadIdx.x; qi < nq; qi += 256u) {
       uint32_t w[RW];
 #pragma unroll
       for (int z = 0; z < RW / 4; ++z) {
-        w[4 * z] = wv[m][z].x; w[4 * z + 1] = wv[m][z].y; w[4 * z + 2] = wv[m][z].z; w[4 * z + 3] = wv[m][z].w;
+        const uint4 v = s_q[qi * (RW / 4) + z];
+        w[4 * z] = v.x; w[4 * z + 1] = v.y; w[4 * z + 2] = v.z; w[4 * z + 3] = v.w;
       }
-      const int64_t idx = w[0];
       uint32_t b[K];
-      uint32_t kprov = 0;
 #pragma unroll
-      for (int i = 0; i < K; ++i) {
-        b[i] = rec_half(w, 3 + i);
-        kprov |= (uint32_t)(bkey(b[i]) >= s_p1[i]) << i;
-      }
-      const uint32_t kfin = final_mask<K>(b, idx, tk, cut);
-      if (kprov != kfin) {
-        int gam;
-        const double t = ties_general<ISO_BF16, K>(b, kfin, gam);
-        out[idx] = (uint16_t)f64_to_bf16_rne(bits_to_f64<ISO_BF16>(rec_half(w, 3 + K)) + a.lambda * t);
-        if (a.want_sign) ((int8_t*)T.aux2)[idx] = (int8_t)gam;
-      }
+      for (int i = 0; i < K; ++i) b[i] = rec_half(w, 3 + i);
+      const int64_t idx = w[0];
+      int gam;
+      const double t = ties_general<ISO_BF16, K>(b, rec_half(w, 2), gam);
+      out[idx] = (uint16_t)f64_to_bf16_rne(bits_to_f64<ISO_BF16>(rec_half(w, 3 + K)) + a.lambda * t);
+      if (a.want_sign) ((int8_t*)T.aux2)[idx] = (int8_t)gam;
     }
+    __syncthreads();
+    if (threadIdx.x == 0) s_qn = 0;
+    __syncthreads();
   }
   if (!s_anyredo) return;
   uint32_t kmax = 0;
@@ -995,6 +1056,7 @@ hipError_t launch_k(const FusedPlan& pl, hipStream_t s) {
     m.tile_cap = pl.tile_cap;
     m.lambda = pl.lambda;
     m.status = pl.status;
+    m.one2 = 0x00010001u;
     if (pl.prof[0]) (void)hipEventRecord(pl.prof[0], s);
     if (pl.want_sign) k_fs_main<K, false, true><<<(unsigned)pl.tiles, kThreads, 0, s>>>(m);
     else if (pl.lambda == 1.0) k_fs_main<K, true, false><<<(unsigned)pl.tiles, kThreads, 0, s>>>(m);
@@ -1002,7 +1064,8 @@ hipError_t launch_k(const FusedPlan& pl, hipStream_t s) {
     if (pl.prof[1]) (void)hipEventRecord(pl.prof[1], s);
   }
   if (pl.ritems > 0)
-    k_fs_reduce<<<(unsigned)pl.ritems, 256, 0, s>>>(pl.tab, pl.n_t, K, pl.ritem0, pl.tflag, pl.tstat, pl.csum, pl.fu);
+    k_fs_reduce<K><<<(unsigned)(pl.ritems / K), 1024, 0, s>>>(pl.tab, pl.n_t, pl.ritem0, pl.tflag, pl.tstat, pl.csum,
+                                                               pl.fu);
   k_fs_resolve<<<(nu + 255) / 256, 256, 0, s>>>(pl.tab, pl.n_t, K, pl.fu, pl.tflag, pl.status);
   TieArgs ta;
   ta.tab = pl.tab;
