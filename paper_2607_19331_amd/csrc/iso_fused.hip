@@ -5,7 +5,7 @@
 // can be merged.  The two-pass path reads every delta twice (histogram, then merge); this
 // path reads each delta and the base once:
 //   1. sample (one workgroup per delta): the exact key histogram of the whole delta when it
-//      is small, else of 4096 evenly spaced 256-entry blocks.  From it a bracket [lo, hi]
+//      holds at most 2^20 entries, else of 4096 evenly spaced 256-entry blocks (2^20 entries).  From it a bracket [lo, hi]
 //      of keys that holds the threshold with a binomial margin (5 standard deviations of
 //      the sample rank, plus 2) and a provisional threshold prov;
 //   2. main pass: a key above hi is kept, a key below lo is not; a nonzero key inside the
@@ -16,7 +16,7 @@
 //      the tie cutoff (lowest flat indices first) from the per-tile counts and the records,
 //      which hold every entry with the threshold code;
 //   4. fix-up: records whose final mask differs from the provisional one are merged again
-//      and rewritten.
+//      and rewritten where the result changes.
 // A threshold outside its bracket (a misleading sample), a bracket wider than kFusedMaxW
 // codes or a full record region sends the tensor to the exact two-pass path (histogram
 // select, then merge) on the same stream; the result is identical either way.  Zero keys
@@ -37,7 +37,7 @@ constexpr int kVPT = 2;                          // 16-byte vectors per thread p
 constexpr int64_t kTileElems = (int64_t)kThreads * kVPT * 8;
 constexpr int kSampleSpan = 256;                 // entries per sampled block
 constexpr int kSampleBlocks = 4096;              // sampled blocks per delta (1M entries)
-constexpr int64_t kExactMax = 2ll << 20;         // deltas up to this size are histogrammed whole
+constexpr int64_t kExactMax = 1ll << 20;         // deltas up to this size (the sample's) are histogrammed whole
 constexpr double kMarginSd = 5.0;
 constexpr int kBins = 1 << 15;
 
@@ -127,18 +127,21 @@ __global__ void __launch_bounds__(1024) k_fs_sample(const DevTensor* __restrict_
       if (k1) atomicAdd(&bins[k1], 1u);
     }
   };
+  // kInFlight 16-byte loads per thread before any is counted: one workgroup per CU (the
+  // histogram takes 128 KB of LDS), so the loads in flight set the rate
+  constexpr int kInFlight = 16;
   int64_t ns;
   if (exact) {
     const int64_t nvec = n / 8;
-    for (int64_t v = threadIdx.x; v < nvec; v += 4 * (int64_t)blockDim.x) {
-      uint4 a[4];
+    for (int64_t v = threadIdx.x; v < nvec; v += kInFlight * (int64_t)blockDim.x) {
+      uint4 a[kInFlight];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < kInFlight; ++q) {
         const int64_t vv = v + q * (int64_t)blockDim.x;
         a[q] = (vv < nvec) ? ld_stream(pv + vv) : make_uint4(0, 0, 0, 0);
       }
 #pragma unroll
-      for (int q = 0; q < 4; ++q) count8(a[q]);   // the zero fill adds nothing
+      for (int q = 0; q < kInFlight; ++q) count8(a[q]);   // the zero fill adds nothing
     }
     const uint16_t* p = (const uint16_t*)T.deltas[i];
     for (int64_t e = nvec * 8 + threadIdx.x; e < n; e += blockDim.x) {
@@ -153,10 +156,10 @@ __global__ void __launch_bounds__(1024) k_fs_sample(const DevTensor* __restrict_
     constexpr int kVecPerBlock = kSampleSpan / 8;
     const int per_iter = blockDim.x / kVecPerBlock;
     const int lb = threadIdx.x / kVecPerBlock, lv = threadIdx.x % kVecPerBlock;
-    for (int b0 = 0; b0 < kSampleBlocks; b0 += 4 * per_iter) {
-      uint4 a[4];
+    for (int b0 = 0; b0 < kSampleBlocks; b0 += kInFlight * per_iter) {
+      uint4 a[kInFlight];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < kInFlight; ++q) {
         const int b = b0 + q * per_iter + lb;
         if (b < kSampleBlocks) {
           const int64_t blk = (int64_t)b * nb / kSampleBlocks;
@@ -166,7 +169,7 @@ __global__ void __launch_bounds__(1024) k_fs_sample(const DevTensor* __restrict_
         }
       }
 #pragma unroll
-      for (int q = 0; q < 4; ++q) count8(a[q]);
+      for (int q = 0; q < kInFlight; ++q) count8(a[q]);
     }
     ns = (int64_t)kSampleBlocks * kSampleSpan;
   }
@@ -892,7 +895,11 @@ __device__ __forceinline__ void store_final(const DevTensor& T, int64_t idx, con
 // merged again whole, in binary64, from the inputs.  The records are read in batches of
 // 256 NB; each batch first only decides which records changed (a few integer tests per
 // record) and queues those in LDS, so that the binary64 merge runs on the changed records
-// alone, one per lane, instead of once per record position of any lane that needs it.
+// alone, one per lane, instead of once per record position of any lane that needs it.  A
+// coordinate is rewritten only when its output (or elected sign) differs from the value the
+// main pass stored for the provisional mask: a delta that joins or leaves the mean often
+// moves the result by less than the base's bf16 spacing, and the scattered 2-byte writes are
+// the costly part of this kernel.
 template <int K>
 __global__ void __launch_bounds__(256) k_fs_fixup(FixArgs a) {
   constexpr int RW = rec_words<K>();
@@ -938,14 +945,25 @@ __global__ void __launch_bounds__(256) k_fs_fixup(FixArgs a) {
   __syncthreads();
   uint32_t tk[K];
   int64_t cut[K];
+  // When every delta's provisional key is its final threshold key, the two masks differ only
+  // at threshold entries at or past the tie cutoff: no coordinate below the smallest cutoff
+  // changes, and the records of tiles that end there need not be read.
+  int64_t unchanged_below = INT64_MAX;
 #pragma unroll
-  for (int i = 0; i < K; ++i) { tk[i] = s_tk[i]; cut[i] = s_cut[i]; }
+  for (int i = 0; i < K; ++i) {
+    tk[i] = s_tk[i];
+    cut[i] = s_cut[i];
+    unchanged_below = (s_p1[i] == tk[i]) ? min(unchanged_below, cut[i]) : (int64_t)0;
+  }
+  int l0 = 0;                                      // first tile of the run with records to read
+  while (l0 < ntl && (t0 + l0 - T.tile0 + 1) * kTileElems <= unchanged_below) ++l0;
+  const uint32_t first = s_pre[l0];
   const uint32_t total = s_pre[kFusedGroupTiles];
   const uint32_t* __restrict__ rec = a.rec;
   uint16_t* __restrict__ out = (uint16_t*)T.out;
   const int lane = threadIdx.x & 63;
-  int l = 0;                                       // tile of the thread's current record (advances monotonically)
-  for (uint32_t r0 = 0; r0 < total; r0 += NB * 256u) {
+  int l = l0;                                      // tile of the thread's current record (advances monotonically)
+  for (uint32_t r0 = first; r0 < total; r0 += NB * 256u) {
     uint4 wv[NB][RW / 4];
 #pragma unroll
     for (int m = 0; m < NB; ++m) {
@@ -961,7 +979,7 @@ __global__ void __launch_bounds__(256) k_fs_fixup(FixArgs a) {
     for (int m = 0; m < NB; ++m) {
       const uint32_t r = r0 + (uint32_t)m * 256u + threadIdx.x;
       bool changed = false;
-      uint32_t kfin = 0;
+      uint32_t kfin = 0, kprov = 0;
       if (r < total) {
         uint32_t w[RW];
 #pragma unroll
@@ -969,7 +987,6 @@ __global__ void __launch_bounds__(256) k_fs_fixup(FixArgs a) {
           w[4 * z] = wv[m][z].x; w[4 * z + 1] = wv[m][z].y; w[4 * z + 2] = wv[m][z].z; w[4 * z + 3] = wv[m][z].w;
         }
         uint32_t b[K];
-        uint32_t kprov = 0;
 #pragma unroll
         for (int i = 0; i < K; ++i) {
           b[i] = rec_half(w, 3 + i);
@@ -986,7 +1003,8 @@ __global__ void __launch_bounds__(256) k_fs_fixup(FixArgs a) {
       if (changed) {
         const uint32_t slot = qbase + (uint32_t)__popcll(mask & ((1ull << lane) - 1ull));
         uint4 v0 = wv[m][0];
-        v0.y = (v0.y & 0xFFFF0000u) | kfin;         // halfword 2 (the tensor id) carries the final mask
+        // halfword 2 (the tensor id) carries the final mask and, above it, the provisional one
+        v0.y = (v0.y & 0xFFFF0000u) | kfin | (kprov << 8);
         s_q[slot * (RW / 4)] = v0;
 #pragma unroll
         for (int z = 1; z < RW / 4; ++z) s_q[slot * (RW / 4) + z] = wv[m][z];
@@ -1005,10 +1023,16 @@ __global__ void __launch_bounds__(256) k_fs_fixup(FixArgs a) {
 #pragma unroll
       for (int i = 0; i < K; ++i) b[i] = rec_half(w, 3 + i);
       const int64_t idx = w[0];
-      int gam;
-      const double t = ties_general<ISO_BF16, K>(b, rec_half(w, 2), gam);
-      out[idx] = (uint16_t)f64_to_bf16_rne(bits_to_f64<ISO_BF16>(rec_half(w, 3 + K)) + a.lambda * t);
-      if (a.want_sign) ((int8_t*)T.aux2)[idx] = (int8_t)gam;
+      const uint32_t masks = rec_half(w, 2);
+      const double w0 = bits_to_f64<ISO_BF16>(rec_half(w, 3 + K));
+      // the main pass wrote the value of the provisional mask (its binary32 forms give the
+      // binary64 sequence bit for bit): rewrite only what the final mask changes
+      int gam, gam_p;
+      const double t = ties_general<ISO_BF16, K>(b, masks & 0xFFu, gam);
+      const double tp = ties_general<ISO_BF16, K>(b, masks >> 8, gam_p);
+      const uint32_t o = f64_to_bf16_rne(w0 + a.lambda * t);
+      if (o != f64_to_bf16_rne(w0 + a.lambda * tp)) out[idx] = (uint16_t)o;
+      if (a.want_sign && gam != gam_p) ((int8_t*)T.aux2)[idx] = (int8_t)gam;
     }
     __syncthreads();
     if (threadIdx.x == 0) s_qn = 0;

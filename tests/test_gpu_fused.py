@@ -5,7 +5,7 @@ every coordinate once and fixes up the coordinates whose keys fell inside the br
 tensor it cannot settle (misleading sample, bracket too wide, record region full) takes
 the exact two-pass path on the device.  Either way the result must equal the oracle's bit
 for bit; the fallback count says which route a tensor took, so each route is exercised on
-purpose here.  Deltas above 2M entries are sampled (4096 blocks of 256 entries at
+purpose here.  Deltas above 2^20 entries are sampled (4096 blocks of 256 entries at
 floor(b * nb / 4096), nb = n / 256); smaller ones are histogrammed whole.
 """
 import numpy as np
@@ -61,9 +61,10 @@ def test_sampled_and_exact_tensors_settle_in_one_read():
     rng = np.random.default_rng(101)
     units = [normal_unit(rng, 2048, 4096, 4),                 # sampled
              normal_unit(rng, 2049, 1025, 4, rho=0.3),        # sampled, ragged (n % 8 != 0)
-             normal_unit(rng, 512, 3584, 4),                  # whole-delta histogram
+             normal_unit(rng, 512, 3584, 4),                  # sampled, just above 2^20 entries
+             normal_unit(rng, 1024, 1024, 4),                 # whole-delta histogram (2^20 entries)
              normal_unit(rng, 3, 5, 4)]
-    say("fused single read: 2048x4096, 2049x1025, 512x3584, 3x5, K=4")
+    say("fused single read: 2048x4096, 2049x1025, 512x3584, 1024x1024, 3x5, K=4")
     outs, sg, st, fb = fused(units, 4)
     assert st == 0
     assert fb == 0
