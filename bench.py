@@ -21,6 +21,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
+METRICS = {"7b": "merged params/sec and achieved HBM GB/s (% of peak), 7B-shaped K=4 merge",
+           "1.5b": "merged params/sec and achieved HBM GB/s (% of peak), 1.5B-shaped K=4 merge",
+           "layer": "merged params/sec and achieved HBM GB/s (% of peak), single bf16 layer K=2 merge",
+           "7b-tsv": "merged params/sec and achieved HBM GB/s (% of peak), 7B-shaped K=4 merge with TSV on the "
+                     "MLP matrices"}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = {"single-read": ("iso_fused.hip", "iso_merge_math.h", "iso_device.h"),
                   "two-pass": ("iso_merge.hip", "iso_merge_math.h", "iso_device.h")}
@@ -48,29 +53,74 @@ def measured_traffic(key, path):
     return r.get("bytes_per_launch")
 
 
-def cpu_baseline():
-    """The oracle, as it is, on a bounded sample of the same workload: the TIES path
-    (full-sort TopKMask, exact election, disjoint mean, update) over layer 0's k_proj,
-    v_proj, q_proj, o_proj and gate_proj, K = 4, on the host."""
+def _oracle_on_tensor(name, t, barrier=None):
+    """One tensor of a workload through the oracle's TIES path (full-sort TopKMask, exact election,
+    disjoint mean, update); returns (params, seconds of the oracle call, generation excluded).
+    With a barrier, the call starts once every worker has its inputs."""
     import synth
     from oracle import ties
-    wl = synth.stack_7b()
-    picks = [1, 2, 0, 3, 4]
-    n = 0
-    dt = 0.0
-    for t in picks:
-        spec = wl.tensors[t]
-        base = synth.fill_host(wl, t, 0)
-        ds = [synth.fill_host(wl, t, 1 + i) for i in range(wl.K)]
-        k = (spec.numel * wl.density.numerator * 2 + wl.density.denominator) // (2 * wl.density.denominator)
-        t0 = time.perf_counter()
-        ties.merge_unit(base, ds, "bf16", "ties", k=k)
-        dt += time.perf_counter() - t0
-        n += spec.numel
-        del base, ds
-    names = "+".join(wl.tensors[t].name.split(".")[-1] for t in picks)
-    return {"value": n / dt, "unit": "params/s", "cores": 1, "kind": "oracle",
-            "sample": f"layers.0 {names} ({n} params, K=4, TIES density 0.1) in {dt:.1f} s; numpy, one thread"}
+    wl = synth.workload(name)
+    spec = wl.tensors[t]
+    base = synth.fill_host(wl, t, 0)
+    ds = [synth.fill_host(wl, t, 1 + i) for i in range(wl.K)]
+    k = (spec.numel * wl.density.numerator * 2 + wl.density.denominator) // (2 * wl.density.denominator)
+    if barrier is not None:
+        barrier.wait()
+    t0 = time.perf_counter()
+    ties.merge_unit(base, ds, "bf16", "ties", k=k)
+    return spec.numel, time.perf_counter() - t0
+
+
+def _baseline_worker(name, t, barrier, queue):
+    queue.put(_oracle_on_tensor(name, t, barrier))
+
+
+# Bounded oracle samples per workload: (one-thread picks, all-cores picks), tensor indices.  The
+# all-cores sample gives each worker one tensor, in table order.
+BASELINE_PICKS = {
+    "7b": ([1, 2, 0, 3, 4], list(range(16))),
+    "1.5b": (list(range(7)), list(range(16))),
+    "layer": ([0, 1], list(range(7))),
+}
+
+
+def cpu_baseline(name, workers):
+    """The oracle, as it is, on a bounded sample of the same workload, on the host's cores: one
+    thread over a few tensors; then `workers` processes (spawned, so that none inherits a GPU
+    context) with one tensor each, started together once all have generated their inputs, the
+    rate being their summed params over the slowest one's oracle time.  Runs before the
+    benchmark touches the GPU."""
+    import multiprocessing as mp
+    import synth
+    wl = synth.workload(name)
+    one, many = BASELINE_PICKS[name]
+    n1, dt1 = 0, 0.0
+    for t in one:
+        n, dt = _oracle_on_tensor(name, t)
+        n1 += n
+        dt1 += dt
+    names1 = "+".join(sorted({wl.tensors[t].name.split(".")[-1] for t in one}))
+    single = {"value": n1 / dt1, "unit": "params/s", "cores": 1, "kind": "oracle",
+              "sample": f"{len(one)} tensors of layer 0 ({names1}; {n1} params, K={wl.K}) in {dt1:.1f} s; "
+                        f"numpy, one thread"}
+    picks = many[:workers]
+    if len(picks) <= 1:
+        return single, None
+    ctx = mp.get_context("spawn")
+    barrier, queue = ctx.Barrier(len(picks)), ctx.Queue()
+    procs = [ctx.Process(target=_baseline_worker, args=(name, t, barrier, queue)) for t in picks]
+    for p in procs:
+        p.start()
+    res = [queue.get() for _ in procs]
+    for p in procs:
+        p.join()
+    nm_ = sum(r[0] for r in res)
+    slowest = max(r[1] for r in res)
+    allc = {"value": nm_ / slowest, "unit": "params/s", "cores": len(picks), "kind": "oracle",
+            "sample": f"{len(picks)} tensors ({wl.tensors[picks[0]].name} .. {wl.tensors[picks[-1]].name}; {nm_} "
+                      f"params, K={wl.K}), one per process, started together: summed params over the slowest "
+                      f"oracle call ({slowest:.1f} s)"}
+    return allc, single
 
 
 def svd_flops(m, n):
@@ -136,7 +186,7 @@ def bench_tiny(args, iso, synth, torch):
     q = min(m_, n_)
     flops = (K + 1) * svd_flops(m_, n_) + svd_flops(m_, q) + svd_flops(n_, q)
     rec = {
-        "metric": "merged params/sec and achieved HBM GB/s (% of peak), 7B-shaped K=4 merge",
+        "metric": "ISO-Merger params/sec and FP64 TFLOP/s (% of peak), Tiny fp32 256x256 K=3",
         "value": n / (ms_per_step * 1e-3),
         "unit": "params/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
@@ -218,7 +268,7 @@ def bench_layer_spectral(args, iso, synth, torch):
     spec_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
     N = wl.numel
     rec = {
-        "metric": "merged params/sec and achieved HBM GB/s (% of peak), 7B-shaped K=4 merge",
+        "metric": "ISO-Merger params/sec and FP64 TFLOP/s (% of peak), single bf16 layer K=2",
         "value": N / (ms_per_step * 1e-3),
         "unit": "params/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
@@ -309,7 +359,7 @@ def bench_layer_optimizer(args, iso, synth, torch):
     opt_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
     N = wl.numel
     rec = {
-        "metric": "merged params/sec and achieved HBM GB/s (% of peak), 7B-shaped K=4 merge",
+        "metric": f"{name} step params/sec and FP64 TFLOP/s (% of peak), single bf16 layer",
         "value": N / (ms_per_step * 1e-3),
         "unit": "params/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
@@ -347,6 +397,40 @@ def bench_layer_optimizer(args, iso, synth, torch):
     return rec
 
 
+def calibrate_stream(args, torch):
+    """Rate of the fused pass's traffic mix with trivial arithmetic: libiso_calibrate's kernel reads
+    K + 1 = 5 arrays of the 7B stack's size (7,615,283,200 bf16 each) and writes one, with the main
+    pass's launch shape; then the 5 reads alone, then a 1:1 copy.  HIP events on the current stream."""
+    import ctypes
+    import synth
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2607_19331_amd", "libiso_calibrate.so"))
+    lib.iso_calibrate_stream.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
+                                         ctypes.c_int, ctypes.c_void_p]
+    n = synth.stack_7b().numel
+    n_vec = n // 8
+    arrs = [torch.full((n_vec * 8,), i + 1, dtype=torch.int16, device="cuda:0") for i in range(6)]
+    stream = torch.cuda.current_stream()
+    res = {}
+    for name, n_in, write in (("5_read_1_write", 5, 1), ("5_read", 5, 0), ("1_read_1_write", 1, 1)):
+        ptrs = (ctypes.c_void_p * 8)(*[a.data_ptr() for a in arrs[:n_in]])
+        out = arrs[5].data_ptr()
+        for _ in range(2):
+            if lib.iso_calibrate_stream(ptrs, n_in, out, n_vec, write, stream.cuda_stream) != 0:
+                raise RuntimeError("iso_calibrate_stream failed")
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        reps = 5
+        ev[0].record()
+        for _ in range(reps):
+            lib.iso_calibrate_stream(ptrs, n_in, out, n_vec, write, stream.cuda_stream)
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / reps
+        nbytes = n_vec * 16 * (n_in + write)
+        res[name] = {"ms": ms, "bytes": nbytes, "GBps": nbytes / (ms * 1e-3) / 1e9,
+                     "frac_of_8TBps": nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBPS}
+    return {"calibrate_stream": res, "elements_per_array": n_vec * 8}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -361,11 +445,22 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain elementwise copy (1 GiB read, 1 GiB written, 3 launches) to scale "
                          "the HBM byte counters of a profiler")
+    ap.add_argument("--calibrate-stream", action="store_true",
+                    help="run only the streaming calibration kernel over the 7B stack's arrays (K deltas + base "
+                         "read, weights written; then reads only; then a copy) and print the rates")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the merge path is independent per "
               "tensor and is not sharded across GPUs here.", file=sys.stderr)
         sys.exit(2)
+
+    # the oracle baseline of the stack workloads runs first, in processes spawned before anything
+    # in this one touches the GPU
+    baseline = None
+    if not args.no_cpu_baseline and args.config in BASELINE_PICKS and not (args.calibrate_copy or
+                                                                            args.calibrate_stream):
+        workers = min(len(os.sched_getaffinity(0)), 16, len(BASELINE_PICKS[args.config][1]))
+        baseline = cpu_baseline(args.config, workers)
 
     import torch
 
@@ -378,6 +473,10 @@ def main():
             torch.neg(src, out=dst)
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy": {"bytes_read": 2 * n, "bytes_written": 2 * n, "launches": 3}}), flush=True)
+        return
+
+    if args.calibrate_stream:
+        print(json.dumps(calibrate_stream(args, torch)), flush=True)
         return
 
     import paper_2607_19331_amd as iso
@@ -470,7 +569,7 @@ def main():
     if tsv_entries:
         what += f"; TSV rank {wl.tsv_rank} on the {len(tsv_entries)} MLP matrices"
     rec = {
-        "metric": "merged params/sec and achieved HBM GB/s (% of peak), 7B-shaped K=4 merge",
+        "metric": METRICS[args.config],
         "value": N / (ms_per_step * 1e-3),
         "unit": "params/s",
         "n_gpus": 1,
@@ -499,8 +598,10 @@ def main():
         rec["fallback_tensors"] = fallbacks
     if tsv_entries:
         rec["tsv_ms"] = tsv_ms
-    if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline()
+    if baseline is not None:
+        rec["cpu_baseline"] = baseline[0]
+        if baseline[1] is not None:
+            rec["cpu_baseline_one_thread"] = baseline[1]
     print(json.dumps(rec), flush=True)
 
 

@@ -44,6 +44,15 @@ def build(verbose=False, jobs=8):
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
+    # the streaming calibration kernel of bench.py --calibrate-stream (not part of libiso)
+    cal = os.path.join(HERE, "libiso_calibrate.so")
+    cmd = ["hipcc"] + HIPFLAGS + ["-shared", "-x", "hip", os.path.join(CSRC, "iso_calibrate.hip"), "-o", cal + ".tmp"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"compile failed: iso_calibrate.hip\n{r.stdout}\n{r.stderr}")
+    os.replace(cal + ".tmp", cal)
     return LIB
 
 

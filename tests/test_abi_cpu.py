@@ -249,3 +249,18 @@ def test_noalloc_validation():
     big = iso._table([entry(rows=4096, cols=4096, k=10, K=4)])
     assert L.iso_update_noalloc(big, 1, 4, iso.BF16, ctypes.byref(a), None, None) == _lib.ERR_UNSUPPORTED
     assert L.iso_update_noalloc(t, 0, 2, iso.BF16, ctypes.byref(a), None, None) == _lib.OK
+
+
+def test_calibration_library_exports_its_declaration():
+    src = open(os.path.join(ROOT, "include", "iso_calibrate.h")).read()
+    names = re.findall(r"^\s*int\s+(iso_\w+)\s*\(", src, re.M)
+    assert names == ["iso_calibrate_stream"]
+    L = ctypes.CDLL(os.path.join(ROOT, "paper_2607_19331_amd", "libiso_calibrate.so"))
+    f = L.iso_calibrate_stream
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p]
+    ptrs = (ctypes.c_void_p * 8)(*([FAKE] * 8))
+    assert f(None, 5, FAKE, 16, 1, None) == 1                # bad arguments return before any launch
+    assert f(ptrs, 0, FAKE, 16, 1, None) == 1
+    assert f(ptrs, 9, FAKE, 16, 1, None) == 1
+    assert f(ptrs, 5, None, 16, 1, None) == 1
+    assert f(ptrs, 5, FAKE, 0, 1, None) == 1
