@@ -3,16 +3,20 @@
 The truncation to the top r singular triplets is only well defined when sigma_r >
 sigma_{r+1}; the deltas here are planted: Delta_i = P_i diag(s_i) Q_i^T plus small noise,
 rounded to bf16, so the gap is wide and the oracle's exact (LAPACK) truncation is what the
-GPU's randomised subspace iteration must reproduce.  Tolerances come from the GPU arithmetic:
-the last product with the delta and the reconstruction use bf16-split MFMA with binary32
-accumulation (about 2^-16 relative per operand; the earlier sketches of the range finder use the
-bf16 hi part only, which tilts the subspace by about 2^-9 sigma_{r+1}/sigma_r before the next QR
-absorbs it), so the fp32 Delta_hat must agree to 1e-3
-of max|Delta_hat| elementwise and 2e-4 relative in Frobenius norm.  A merged bf16 weight must
-lie within half an ulp of W_0 + alpha*Delta_hat (exact reference) plus |alpha| times that
-Delta_hat bound; where the update is small against the weights (the realistic regime) it is
-also within one bf16 ulp of the oracle's rounded weight, the ulp taken at
-max(|w|, 2^-10 max|w|).
+GPU's randomised subspace iteration must reproduce.  Tolerance from the GPU arithmetic: the
+last product with each delta and the reconstruction take their binary32/binary64 operands as
+bf16 hi + lo pairs (|x - hi - lo| <= 2^-18 |x|; the dropped lo*lo term is as small), so each
+product term carries about 2^-16 relative error and the binary32 sum over K r terms adds at
+most K r 2^-24 of the sum of magnitudes: about 2^-15 of max|Delta_hat| in all.  The fp32
+Delta_hat must therefore agree to 2e-5 of max|Delta_hat| elementwise and 1e-5 relative in
+Frobenius norm (measured: at most 7.8e-6 and 4.7e-6 over these cases), and every merged bf16
+weight must lie within one bf16 ulp of the oracle's rounded weight, the ulp taken at
+max(|w|, 2^-10 max|w|) (a result next to a rounding boundary can round either way), and within
+half an ulp of W_0 + alpha*Delta_hat (exact reference) plus |alpha| times the Delta_hat bound.
+
+On the synthetic 7B deltas themselves (80% zeros, i.i.d. values) the spectrum near rank 64 is
+flat and the top-64 truncation is numerically ill-posed for any fast method: that case is
+checked on what is unique (the spectrum of Delta_hat) in test_workload_matrix_flat_spectrum.
 """
 import numpy as np
 import pytest
@@ -48,17 +52,29 @@ def run_tsv(units, K, r, alpha=1.0):
     return [from_dev(u.dout, u.n, "bf16") for u in units], [d.cpu().numpy()[:u.n] for d, u in zip(dh, units)], st
 
 
+def _report(u, got, ref_dh, out, ref_out):
+    e_max = np.abs(got - ref_dh).max() / np.abs(ref_dh).max()
+    e_fro = np.linalg.norm(got - ref_dh) / np.linalg.norm(ref_dh)
+    ref_v = nm.to_f64(ref_out.ravel(), "bf16")
+    have = nm.to_f64(out, "bf16")
+    mag = np.maximum(np.abs(ref_v), 2.0 ** -10 * np.abs(ref_v).max())
+    ulps = np.abs(have - ref_v) / _ulp_bf16(mag)
+    say(f"tsv {u.rows}x{u.cols}: max|dh err|/max|dh| {e_max:.3e}, frobenius {e_fro:.3e}, "
+        f"output max {ulps.max():.2f} ulp, {np.mean(ulps > 0):.2e} of outputs differ")
+
+
 def _ulp_bf16(v):
     e = np.floor(np.log2(np.maximum(np.abs(v), 2.0 ** -126)))
     return 2.0 ** (e - 7)
 
 
-def check(u, K, r, alpha, out, dh, ulp1=False):
+def check(u, K, r, alpha, out, dh, ulp1=True):
     ref_out, ref_dh, _ = tsv.tsv_merge(u.base, u.deltas, r, alpha, "bf16", shape=(u.rows, u.cols))
     got = dh.astype(np.float64).reshape(u.rows, u.cols)
-    tol = 1e-3 * np.abs(ref_dh).max()
+    _report(u, got, ref_dh, out, ref_out)
+    tol = 2e-5 * np.abs(ref_dh).max()
     assert np.abs(got - ref_dh).max() <= tol
-    assert np.linalg.norm(got - ref_dh) <= 2e-4 * np.linalg.norm(ref_dh)
+    assert np.linalg.norm(got - ref_dh) <= 1e-5 * np.linalg.norm(ref_dh)
     exact = nm.to_f64(u.base, "bf16") + alpha * ref_dh.ravel()
     have = nm.to_f64(out, "bf16")
     assert np.all(np.abs(have - exact) <= 0.5 * _ulp_bf16(exact) + abs(alpha) * tol)
@@ -103,7 +119,7 @@ def test_realistic_scale_is_within_one_ulp():
     say("tsv realistic scale")
     outs, dhs, st = run_tsv([u], K, r)
     assert st == 0
-    check(u, K, r, 1.0, outs[0], dhs[0], ulp1=True)
+    check(u, K, r, 1.0, outs[0], dhs[0])
 
 
 def test_alpha_and_two_matrices():
@@ -144,7 +160,7 @@ def test_argument_errors():
 
 def test_full_mlp_shape():
     """The 7B MLP shape of the TSV workload (3584 x 18944, K = 4, rank 64), planted so that the
-    truncation is well posed; the same tolerance as the small shapes."""
+    truncation is well posed; the same tolerances as the small shapes, one-ulp check included."""
     rng = np.random.default_rng(31)
     R, C, K, r = 3584, 18944, 4, 64
     ds = []
@@ -167,8 +183,9 @@ def test_given_factors_steps_after_the_svd(R, C, K, r):
     """iso_blockdiag_project_factors with the oracle's exact truncated factors: only the
     concatenation, the Procrustes orthogonalisation (binary64 Newton-Schulz) and the bf16-split
     MFMA reconstruction remain, so Delta_hat must match the oracle's to the reconstruction's
-    rounding (about 2^-16 relative per operand): 1e-4 of max|Delta_hat| elementwise, 5e-5
-    relative in Frobenius norm.  No spectral gap is needed: the factors are given."""
+    rounding (the bf16 hi + lo products, about 2^-15 of max|Delta_hat| in all): 2e-5 of
+    max|Delta_hat| elementwise, 1e-5 relative in Frobenius norm.  No spectral gap is needed: the
+    factors are given."""
     import torch
     rng = np.random.default_rng(R * 7 + C + K + r)
     base = nm.f64_to_bf16(rng.standard_normal(R * C) * 0.02)
@@ -186,9 +203,55 @@ def test_given_factors_steps_after_the_svd(R, C, K, r):
     assert iso.iso_read_device_status(ws) == 0
     ref_out, ref_dh, _ = tsv.tsv_merge(base, ds, r, 1.0, "bf16", shape=(R, C), factors=fac)
     got = dh[0].cpu().numpy().astype(np.float64).reshape(R, C)
-    tol = 1e-4 * np.abs(ref_dh).max()
+    _report(u, got, ref_dh, from_dev(u.dout, u.n, "bf16"), ref_out)
+    tol = 2e-5 * np.abs(ref_dh).max()
     assert np.abs(got - ref_dh).max() <= tol
-    assert np.linalg.norm(got - ref_dh) <= 5e-5 * np.linalg.norm(ref_dh)
+    assert np.linalg.norm(got - ref_dh) <= 1e-5 * np.linalg.norm(ref_dh)
     exact = nm.to_f64(base, "bf16") + ref_dh.ravel()
     have = nm.to_f64(from_dev(u.dout, u.n, "bf16"), "bf16")
     assert np.all(np.abs(have - exact) <= 0.5 * _ulp_bf16(exact) + tol)
+
+
+@pytest.mark.timeout(900)
+def test_workload_matrix_flat_spectrum():
+    """One MLP matrix of the 7B+TSV workload as generated (layer 0 gate_proj, 18944 x 3584, K = 4
+    deltas with 80% zeros and i.i.d. N(0, 5e-5) values, rank 64).  Its spectrum near rank 64 is
+    flat (sigma_64 / sigma_65 within a few parts per thousand), so the top-64 subspaces are not
+    determined to working accuracy by any fast method and Delta_hat is not compared entry by
+    entry.  What is unique is checked: Delta_hat = U_perp Sigma V_perp^T with orthonormal U_perp,
+    V_perp has exactly the singular values in Sigma.  The GPU's Sigma_i are those of its
+    projections Q_i Q_i^T Delta_i, which never exceed the true ones (sigma_j(P A) <= sigma_j(A) for
+    an orthogonal projector P), so the sorted values of its Delta_hat must lie at or below the
+    sorted top-64 values of the K deltas (1e-3 relative slack for the bf16 split products); on
+    this flat spectrum the randomised range finder (two power iterations) falls short of them by
+    about 8.5% on average (measured), which bounds the mean shortfall here at 12%."""
+    import synth
+    wl = synth.workload("7b-tsv")
+    t = 4
+    spec = wl.tensors[t]
+    R, C, K, r = spec.rows, spec.cols, wl.K, wl.tsv_rank
+    base = synth.fill_host(wl, t, 0, threads=8)
+    ds = [synth.fill_host(wl, t, 1 + i, threads=8) for i in range(K)]
+    u = Unit(R, C, base, ds, "bf16")
+    say(f"tsv workload matrix {spec.name} {R}x{C} K={K} r={r}")
+    outs, dhs, st = run_tsv([u], K, r)
+    assert st == 0
+    got = dhs[0].astype(np.float64).reshape(R, C)
+    del outs
+    ref = []
+    for i, d in enumerate(ds):
+        say(f"tsv workload matrix: singular values of delta {i} (LAPACK)")
+        s = np.linalg.svd(nm.to_f64(d, "bf16").reshape(R, C), compute_uv=False)
+        ref.append(s[:r])
+        if i == 0:
+            say(f"tsv workload matrix: sigma_{r} / sigma_{r + 1} = {s[r - 1] / s[r]:.5f}")
+    want = np.sort(np.concatenate(ref))[::-1]
+    say("tsv workload matrix: singular values of the GPU's Delta_hat (Gram eigenvalues)")
+    gram = got.T @ got if R >= C else got @ got.T
+    have = np.sqrt(np.maximum(np.linalg.eigvalsh(gram)[::-1][:K * r], 0.0))
+    rel = np.abs(have - want) / want
+    e_energy = abs(np.sum(have ** 2) - np.sum(want ** 2)) / np.sum(want ** 2)
+    say(f"tsv workload matrix: singular values max rel err {rel.max():.3e}, mean {rel.mean():.3e}, "
+        f"energy rel err {e_energy:.3e}")
+    assert np.all(have <= want * (1.0 + 1e-3))
+    assert rel.mean() <= 0.12
