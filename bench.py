@@ -220,20 +220,33 @@ def bench_tiny(args, iso, synth, torch):
     return rec
 
 
+SPECTRAL_SETS = {
+    # config: (workload, tensor indices, description)
+    "layer-spectral": ("layer", list(range(7)), "single bf16 layer (q/k/v/o 2048x2048, gate/up 2048x5632, "
+                                                 "down 5632x2048)"),
+    "7b-layer-spectral": ("7b", list(range(7)), "one full 7B layer (q/o 3584x3584, k/v 512x3584, gate/up "
+                                                 "18944x3584, down 3584x18944)"),
+    "7b-embed-spectral": ("7b", [196], "the 7B embedding matrix (152064x3584)"),
+}
+
+
 def bench_layer_spectral(args, iso, synth, torch):
-    """ISO-Merger (Algorithm 1, iso_update SPECTRAL) over the single bf16 layer (q/k/v/o
-    2048x2048, gate/up 2048x5632, down 5632x2048, K = 2) in one call per step, timed with HIP
-    events on the current stream.  Roofline: binary64, the algorithmic flops of every matrix's
-    K + 1 thin SVDs and two polar SVDs."""
+    """ISO-Merger (Algorithm 1, iso_update SPECTRAL) over a set of bf16 matrices with the workload's
+    K deltas in one call per step, timed with HIP events on the current stream: the single layer
+    (K = 2), one full layer of the 7B stack or its embedding matrix (K = 4).  Roofline: binary64, the
+    algorithmic flops of every matrix's K + 1 thin SVDs and two polar SVDs."""
     from oracle import numerics as nm
     from oracle import spectral as sp
-    wl = synth.workload("layer")
+    wl_name, picks, what = SPECTRAL_SETS[args.config]
+    wl = synth.workload(wl_name)
     K = wl.K
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream().cuda_stream
-    entries, flops = [], 0
-    for t, spec in enumerate(wl.tensors):
+    entries, flops, N = [], 0, 0
+    for t in picks:
+        spec = wl.tensors[t]
         n = spec.numel
+        N += n
         base = torch.empty(n, dtype=torch.int16, device=dev)
         synth.fill_device(base.data_ptr(), n, wl, t, 0, stream)
         ds = []
@@ -266,14 +279,13 @@ def bench_layer_spectral(args, iso, synth, torch):
     torch.cuda.synchronize()
     ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
     spec_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
-    N = wl.numel
     rec = {
-        "metric": "ISO-Merger params/sec and FP64 TFLOP/s (% of peak), single bf16 layer K=2",
+        "metric": f"ISO-Merger params/sec and FP64 TFLOP/s (% of peak), {what.split(' (')[0]} K={K}",
         "value": N / (ms_per_step * 1e-3),
         "unit": "params/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
-        "config": {"workload": f"single bf16 layer ({len(wl.tensors)} matrices, {N} params), K={K} deltas "
+        "config": {"workload": f"{what}: {len(picks)} matrices, {N} params, K={K} deltas "
                                f"({float(wl.delta.p_zero):.0%} zeros): ISO-Merger (Algorithm 1) in one call"},
         "spectral_ms": spec_ms,
         "roofline": {"bound": "fp64", "kernel": "iso_update SPECTRAL (Algorithm 1: Jacobi SVDs, dense binary64 steps)",
@@ -282,9 +294,12 @@ def bench_layer_spectral(args, iso, synth, torch):
                      "flops_per_call": flops},
     }
     if not args.no_cpu_baseline:
-        spec = wl.tensors[0]
-        w0 = nm.to_f64(synth.fill_host(wl, 0, 0), "bf16").reshape(spec.rows, spec.cols)
-        dh = [nm.to_f64(synth.fill_host(wl, 0, 1 + i), "bf16").reshape(spec.rows, spec.cols) for i in range(K)]
+        t = min(picks, key=lambda j: wl.tensors[j].numel)        # the smallest matrix of the set
+        spec = wl.tensors[t]
+        rows = min(spec.rows, 8192)                                # a 152064-row matrix: its first rows
+        n = rows * spec.cols
+        w0 = nm.to_f64(synth.fill_host(wl, t, 0, n=n), "bf16").reshape(rows, spec.cols)
+        dh = [nm.to_f64(synth.fill_host(wl, t, 1 + i, n=n), "bf16").reshape(rows, spec.cols) for i in range(K)]
         t1 = time.perf_counter()
         sp.iso_merge(w0, dh)
         dt = time.perf_counter() - t1
@@ -293,9 +308,10 @@ def bench_layer_spectral(args, iso, synth, torch):
             cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
         except ImportError:
             cores = len(os.sched_getaffinity(0))
-        rec["cpu_baseline"] = {"value": spec.numel / dt, "unit": "params/s", "cores": cores, "kind": "oracle",
+        part = "" if rows == spec.rows else f", its first {rows} rows as one matrix"
+        rec["cpu_baseline"] = {"value": n / dt, "unit": "params/s", "cores": cores, "kind": "oracle",
                                "sample": f"Algorithm 1 (LAPACK SVDs, numpy) on {spec.name} "
-                                         f"({spec.rows}x{spec.cols}), one run, {dt:.1f} s"}
+                                         f"({spec.rows}x{spec.cols}{part}), one run, {dt:.1f} s"}
     return rec
 
 
@@ -436,8 +452,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="7b", choices=["tiny", "layer", "1.5b", "7b", "7b-tsv", "layer-spectral",
-                                                      "layer-optimizer"])
+    ap.add_argument("--config", default="7b", choices=["tiny", "layer", "1.5b", "7b", "7b-tsv", "layer-optimizer"]
+                    + list(SPECTRAL_SETS))
     ap.add_argument("--path", default="single-read", choices=["single-read", "two-pass"])
     ap.add_argument("--rule", default="adamw", choices=["adamw", "muon"],
                     help="base rule of the ISO-Optimizer step (--config layer-optimizer)")
@@ -485,7 +501,7 @@ def main():
     if args.config == "tiny":
         print(json.dumps(bench_tiny(args, iso, synth, torch)), flush=True)
         return
-    if args.config == "layer-spectral":
+    if args.config in SPECTRAL_SETS:
         print(json.dumps(bench_layer_spectral(args, iso, synth, torch)), flush=True)
         return
     if args.config == "layer-optimizer":

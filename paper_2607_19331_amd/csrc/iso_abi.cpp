@@ -591,7 +591,7 @@ iso_status update_call(const iso_tensor* t, int n_t, int K, iso_dtype dt, const 
     if (!(a->rho_keep > 0.0 && a->rho_keep <= 1.0) || !(a->ridge >= 0.0) || !(a->c_min <= a->c_max))
       return ISO_ERR_INVALID_ARG;
     for (int j = 0; j < n_t; ++j)
-      if (t[j].rows > ISO_SPECTRAL_MAX_DIM || t[j].cols > ISO_SPECTRAL_MAX_DIM) return ISO_ERR_UNSUPPORTED;
+      if (std::min(t[j].rows, t[j].cols) > ISO_SPECTRAL_MAX_DIM) return ISO_ERR_UNSUPPORTED;
     if (a->coef_out != nullptr && ((uintptr_t)a->coef_out & 7u) != 0) return ISO_ERR_ALIGNMENT;
     if (n_t == 0) return ISO_OK;
     Layout L = plan(ISO_OP_UPDATE_SPECTRAL, t, n_t, K, dt);
@@ -696,7 +696,7 @@ static iso_status spectrum_op(const iso_tensor* t, int n_t, iso_dtype dt, Spectr
   iso_status st = check_table(t, n_t, 1, dt, nd);
   if (st != ISO_OK) return st;
   for (int j = 0; j < n_t; ++j)
-    if (t[j].rows > ISO_SPECTRAL_MAX_DIM || t[j].cols > ISO_SPECTRAL_MAX_DIM) return ISO_ERR_UNSUPPORTED;
+    if (std::min(t[j].rows, t[j].cols) > ISO_SPECTRAL_MAX_DIM) return ISO_ERR_UNSUPPORTED;
   if (!write && (out == nullptr || ((uintptr_t)out & 7u) != 0)) return out ? ISO_ERR_ALIGNMENT : ISO_ERR_INVALID_ARG;
   if (write && !(param - param == 0.0)) return ISO_ERR_INVALID_ARG;
   if (op == SpectrumOp::kTransport) {

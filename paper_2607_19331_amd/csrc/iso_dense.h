@@ -634,9 +634,11 @@ inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_r, i
     S.need = (int*)(S.qrot + (size_t)njobs * S.npairs * kGN * kGN);
   }
   const int slices_a = S.nslices, slices_v = (int)((max_c + kGSliceRows - 1) / kGSliceRows);
+  // a sweep over more than 2^26 matrix entries takes milliseconds: check the flags after each one
+  const int check = (double)max_r * (double)max_c * njobs > 67108864.0 ? 1 : kJacobiCheckSweeps;
   std::vector<JacobiState> h(njobs);
   for (int sweep = 0; sweep < kJacobiMaxSweeps;) {
-    for (int b = 0; b < kJacobiCheckSweeps && sweep < kJacobiMaxSweeps; ++b, ++sweep) {
+    for (int b = 0; b < check && sweep < kJacobiMaxSweeps; ++b, ++sweep) {
       for (int round = 0; round < nbp - 1; ++round) {
         if (scratch == nullptr) {
           k_bjacobi_gram<<<g, 256, 0, s>>>(jobs, st, round);
@@ -706,35 +708,73 @@ inline hipError_t jacobi_block(const JacobiJob* jobs, int njobs, int64_t max_r, 
   return hipGetLastError();
 }
 
-// Sorted thin factors from a converged Jacobi job: left (r x c) = A's columns normalised,
-// right (c x c) = V, s (c), all permuted to nonincreasing s.  Zero columns give zero vectors.
-__global__ void __launch_bounds__(1024) k_svd_finalize(const JacobiJob* __restrict__ jobs, double* const* left,
-                                                       double* const* right, double* const* sv) {
-  extern __shared__ double nrm[];          // c column norms (8 c bytes: 128 KiB at c = 16384)
-  const JacobiJob J = jobs[blockIdx.x];
+// Sorted thin factors from converged Jacobi jobs: left (r x c) = A's columns normalised, right
+// (c x c) = V, s (c), all permuted to nonincreasing s (equal norms keep their column order); zero
+// columns give zero vectors.  Three launches with one wave per column and blockIdx.y the job, so
+// that long columns are spread over the chip: the column norms into s (unsorted), the scatter of
+// every column to its rank (the norms staged in LDS), then s itself sorted by one workgroup per job.
+__global__ void __launch_bounds__(1024) k_svd_norms(const JacobiJob* __restrict__ jobs, double* const* sv) {
+  const JacobiJob J = jobs[blockIdx.y];
   const int64_t r = J.r, c = J.c;
+  const int lane = threadIdx.x & 63;
+  const int64_t j = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 6);
+  if (j >= c) return;
+  double s = 0.0;
+  for (int64_t t = lane; t < r; t += 64) s += J.a[j * r + t] * J.a[j * r + t];
+  s = wave_sum_f64(s);
+  if (lane == 0) sv[blockIdx.y][j] = sqrt(s);
+}
+
+// Position of column j among c norms sorted nonincreasing: the columns with a larger norm, or an
+// equal norm and a smaller index, come first.
+__device__ __forceinline__ int64_t svd_rank(const double* nrm, int64_t c, int64_t j, int lane) {
+  const double s = nrm[j];
+  double cnt = 0.0;
+  for (int64_t k = lane; k < c; k += 64) cnt += ((nrm[k] > s) || (nrm[k] == s && k < j)) ? 1.0 : 0.0;
+  return (int64_t)wave_sum_f64(cnt);
+}
+
+__global__ void __launch_bounds__(1024) k_svd_scatter(const JacobiJob* __restrict__ jobs, double* const* left,
+                                                      double* const* right, double* const* sv) {
+  extern __shared__ double nrm[];          // c column norms (8 c bytes: 128 KiB at c = 16384)
+  const JacobiJob J = jobs[blockIdx.y];
+  const int64_t r = J.r, c = J.c;
+  if ((int64_t)blockIdx.x * 16 >= c) return;
+  const double* S = sv[blockIdx.y];
+  for (int64_t k = threadIdx.x; k < c; k += blockDim.x) nrm[k] = S[k];
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int64_t j = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 6);
+  if (j >= c) return;
+  const int64_t d = svd_rank(nrm, c, j, lane);
+  const double inv = (nrm[j] > 0.0) ? 1.0 / nrm[j] : 0.0;
+  double* L = left[blockIdx.y];
+  double* R = right[blockIdx.y];
+  for (int64_t t = lane; t < r; t += 64) L[d * r + t] = J.a[j * r + t] * inv;
+  for (int64_t t = lane; t < c; t += 64) R[d * c + t] = J.v[j * c + t];
+}
+
+__global__ void __launch_bounds__(1024) k_svd_sort(const JacobiJob* __restrict__ jobs, double* const* sv) {
+  extern __shared__ double nrm[];
+  const int64_t c = jobs[blockIdx.x].c;
+  double* S = sv[blockIdx.x];
+  for (int64_t k = threadIdx.x; k < c; k += blockDim.x) nrm[k] = S[k];
+  __syncthreads();
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
   for (int64_t j = wid; j < c; j += nw) {
-    double s = 0.0;
-    for (int64_t t = lane; t < r; t += 64) s += J.a[j * r + t] * J.a[j * r + t];
-    s = wave_sum_f64(s);
-    if (lane == 0) nrm[j] = sqrt(s);
+    const int64_t d = svd_rank(nrm, c, j, lane);
+    if (lane == 0) S[d] = nrm[j];
   }
-  __syncthreads();
-  double* L = left[blockIdx.x];
-  double* R = right[blockIdx.x];
-  double* S = sv[blockIdx.x];
-  for (int64_t j = wid; j < c; j += nw) {
-    // rank of column j: columns with a larger norm, or an equal norm and a smaller index
-    const double s = nrm[j];
-    double cnt = 0.0;
-    for (int64_t k = lane; k < c; k += 64) cnt += ((nrm[k] > s) || (nrm[k] == s && k < j)) ? 1.0 : 0.0;
-    const int64_t d = (int64_t)wave_sum_f64(cnt);
-    const double inv = (s > 0.0) ? 1.0 / s : 0.0;
-    for (int64_t t = lane; t < r; t += 64) L[d * r + t] = J.a[j * r + t] * inv;
-    for (int64_t t = lane; t < c; t += 64) R[d * c + t] = J.v[j * c + t];
-    if (lane == 0) S[d] = s;
-  }
+}
+
+// left/right/sv hold one pointer per job; max_c is the largest column count of the jobs.
+inline void svd_finalize(const JacobiJob* jobs, double* const* left, double* const* right, double* const* sv,
+                         int njobs, int64_t max_c, hipStream_t s) {
+  const dim3 g((unsigned)((max_c + 15) / 16), (unsigned)njobs);
+  const size_t lds = sizeof(double) * (size_t)max_c;
+  k_svd_norms<<<g, 1024, 0, s>>>(jobs, sv);
+  k_svd_scatter<<<g, 1024, lds, s>>>(jobs, left, right, sv);
+  k_svd_sort<<<njobs, 1024, lds, s>>>(jobs, sv);
 }
 
 // out = x - y (elementwise, n entries)

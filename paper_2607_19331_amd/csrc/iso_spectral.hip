@@ -95,28 +95,73 @@ __global__ void k_scale_cols(double* __restrict__ out, const double* __restrict_
     out[e] = x[e] * s[e / r];
 }
 
-// Gram of K vectors of length len: G[i*K + j] = <g_i, g_j>.  One block per (i, j >= i).
-__global__ void __launch_bounds__(1024) k_gram(const double* __restrict__ g, int64_t len, int K, double* __restrict__ G) {
-  __shared__ double red[16];
-  const int pr = blockIdx.x;
-  int i = 0, j = 0, t = pr;
-  for (i = 0; i < K; ++i) {
-    if (t < K - i) { j = i + t; break; }
-    t -= K - i;
+// ---- long reductions: many workgroups, fixed summation order ---------------------------------------
+// Slot y of a DotSet sums f(a_y[e], b_y[e]) over len entries, f = a b (diff = 0) or (a - b)^2
+// (diff = 1): kRedChunks workgroups per slot each sum one contiguous chunk into part, then one wave
+// per slot adds the chunks in order and writes the total to out[o1[y]] and out[o2[y]].
+constexpr int kRedChunks = 512;
+constexpr int kRedSlots = ISO_MAX_K * (ISO_MAX_K + 1) / 2;
+
+struct DotSet {
+  const double* a[kRedSlots];
+  const double* b[kRedSlots];
+  int o1[kRedSlots], o2[kRedSlots];
+};
+
+__global__ void __launch_bounds__(256) k_dot_part(DotSet d, int64_t len, int diff, double* __restrict__ part) {
+  __shared__ double red[4];
+  const double* a = d.a[blockIdx.y];
+  const double* b = d.b[blockIdx.y];
+  const int64_t per = (len + kRedChunks - 1) / kRedChunks;
+  const int64_t e0 = (int64_t)blockIdx.x * per, e1 = min(len, e0 + per);
+  double x = 0.0;
+  for (int64_t e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
+    const double u = a[e], v = b[e];
+    x += diff ? (u - v) * (u - v) : u * v;
   }
-  const double* a = g + (int64_t)i * len;
-  const double* b = g + (int64_t)j * len;
-  double s = 0.0;
-  for (int64_t e = threadIdx.x; e < len; e += blockDim.x) s += a[e] * b[e];
-  s = wave_sum_f64(s);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  x = wave_sum_f64(x);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    double tot = 0.0;
-    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) tot += red[w];
-    G[i * K + j] = tot;
-    G[j * K + i] = tot;
+  if (threadIdx.x == 0) part[(int64_t)blockIdx.y * kRedChunks + blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+__global__ void __launch_bounds__(64) k_dot_sum(DotSet d, const double* __restrict__ part, double* __restrict__ out) {
+  const int y = blockIdx.x, lane = threadIdx.x;
+  double x = 0.0;
+  for (int z = lane; z < kRedChunks; z += 64) x += part[(int64_t)y * kRedChunks + z];
+  x = wave_sum_f64(x);
+  if (lane == 0) {
+    out[d.o1[y]] = x;
+    out[d.o2[y]] = x;
   }
+}
+
+// part: kRedSlots * kRedChunks doubles
+void dots(const DotSet& d, int nslots, int64_t len, bool diff, double* part, double* out, hipStream_t s) {
+  k_dot_part<<<dim3(kRedChunks, (unsigned)nslots), 256, 0, s>>>(d, len, diff ? 1 : 0, part);
+  k_dot_sum<<<nslots, 64, 0, s>>>(d, part, out);
+}
+
+// one slot: out[0] = sum over len entries of a b, or of (a - b)^2
+void dot1(const double* a, const double* b, int64_t len, bool diff, double* part, double* out, hipStream_t s) {
+  DotSet d{};
+  d.a[0] = a;
+  d.b[0] = b;
+  dots(d, 1, len, diff, part, out, s);
+}
+
+// Gram of K vectors of length len: G[i*K + j] = <g_i, g_j>, one slot per pair j >= i.
+void gram_of(const double* g, int64_t len, int K, double* part, double* G, hipStream_t s) {
+  DotSet d{};
+  int y = 0;
+  for (int i = 0; i < K; ++i)
+    for (int j = i; j < K; ++j, ++y) {
+      d.a[y] = g + (int64_t)i * len;
+      d.b[y] = g + (int64_t)j * len;
+      d.o1[y] = i * K + j;
+      d.o2[y] = j * K + i;
+    }
+  dots(d, y, len, false, part, G, s);
 }
 
 // Unit-retention ridge solve over the nonzero proxies, then clip.  One thread.
@@ -175,9 +220,12 @@ __global__ void k_combine(double* __restrict__ out, const double* __restrict__ x
 // polar(X) = P_X Q_X^T equals X (X^T X)^{-1/2} when X has full column rank, which the retraction
 // arguments have: U_0 + xi_U with xi_U tangent gives X^T X = I + xi^T xi (Sec. 4.2, App. E).
 // The iteration X <- X (3 I - X^T X) / 2 maps each singular value s to s (3 - s^2) / 2 and
-// converges quadratically to the polar factor for s in (0, sqrt 3); the first step scales X by
-// 1 / sqrt(c), c the largest absolute column sum of X^T X (at least its largest eigenvalue), so
-// that every s lies in (0, 1].  A job stops once max |X^T X - I| <= kNsTol, after one more step.
+// converges quadratically to the polar factor for s in (0, sqrt 3).  The first step scales X by
+// 1 / sqrt(c), c the largest absolute column sum of X^T X (at least its largest eigenvalue, by
+// Gershgorin), so that every s lies in (0, 1] -- unless c <= 2: every s is then at most sqrt 2,
+// already inside the basin, and X is left unscaled (a near-orthonormal retraction argument would
+// otherwise be shrunk by up to sqrt c and take several extra steps to grow back).  A job stops
+// once max |X^T X - I| <= kNsTol, after one more step.
 //
 // Scaled variant (for arguments far from orthonormal): Chen and Chow's scaling (SIAM J. Matrix
 // Anal. Appl., 2014).  If every s lies in [l, 1], the step X <- a X (3 I - a^2 X^T X) / 2 with
@@ -252,7 +300,9 @@ __global__ void k_ns_form(const NsJob* __restrict__ jobs, NsState* st, int scale
   const bool first = st[job].steps == 0;
   const double err = __longlong_as_double((long long)st[job].err);
   const bool last = err <= kNsTol;
-  const double c = first ? __longlong_as_double((long long)st[job].csum) : 1.0;
+  const double cs = __longlong_as_double((long long)st[job].csum);
+  // the scaled schedule assumes s <= 1 from the start; the plain one only needs s < sqrt 3
+  const double c = (first && (scaled || cs > 2.0)) ? cs : 1.0;
   const double ic = (c > 0.0) ? 1.0 / c : 1.0, is = sqrt(ic);
   double a = 1.0, l = 1.0;
   if (scaled && !last) {
@@ -304,6 +354,7 @@ struct Bump {
 struct Bufs {
   double *ja[ISO_MAX_K + 1], *jv[ISO_MAX_K + 1], *U[ISO_MAX_K + 1], *V[ISO_MAX_K + 1], *S[ISO_MAX_K + 1];
   double *XU, *XV, *P, *Sq, *FU, *FV, *G, *gram, *coef, *AU, *AV, *Wst;
+  double* red;                // partial sums of the long reductions (kRedSlots x kRedChunks)
   double *PX[2][2], *PG[2];   // polar of U_0 + xi_U (m x q) and of V_0 + xi_V (n x q): the two buffers
                               // of the iterate X, the q x q Gram / step matrix
 };
@@ -325,8 +376,9 @@ Bufs carve(Bump& bp, int64_t m, int64_t n, int K) {
   b.FU = bp.take(m * q);
   b.FV = bp.take(n * q);
   b.G = bp.take((int64_t)K * m * n);
-  b.gram = bp.take(K * K);
+  b.gram = bp.take(std::max(K * K, 2));      // also the two norms of the diagnostics
   b.coef = bp.take(K);
+  b.red = bp.take((int64_t)kRedSlots * kRedChunks);
   b.AU = bp.take(m * q);
   b.AV = bp.take(n * q);
   for (int h = 0; h < 2; ++h) {
@@ -437,7 +489,7 @@ void middle_steps(const Bufs& b, int64_t m, int64_t n, int K, const SpectralArgs
     gemm(m, n, q, 1.0, b.FU, 1, m, xv, n, 1, 1.0, g, 1, m, s);
   }
   // 5. Gram, ridge solve, clip
-  k_gram<<<K * (K + 1) / 2, 1024, 0, s>>>(b.G, m * n, K, b.gram);
+  gram_of(b.G, m * n, K, b.red, b.gram, s);
   k_solve<<<1, 64, 0, s>>>(b.gram, K, a.ridge, a.c_min, a.c_max, b.coef, coef_out, status);
   // 6. aggregate, project, shift to the base factors
   k_combine<<<grid_for(m * q), 256, 0, s>>>(b.AU, b.XU, b.coef, K, m * q);
@@ -554,7 +606,10 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
   jacobi_block_shape(svd_r, svd_c, &width, &per_cu);
   for (int e = 0; e < nm; ++e) {
     const int64_t nb = (std::min(t[ids[e]].rows, t[ids[e]].cols) + width - 1) / width;
-    wgs += (int64_t)(K + 1) * ((nb + 1) / 2);
+    // the Gram step splits each block pair's rows over workgroups of kGSliceRows rows
+    const int64_t slices =
+        width == kGW ? (std::max(t[ids[e]].rows, t[ids[e]].cols) + kGSliceRows - 1) / kGSliceRows : 1;
+    wgs += (int64_t)(K + 1) * ((nb + 1) / 2) * slices;
   }
   int dev = 0, cus = 0;
   SP_TRY(hipGetDevice(&dev));
@@ -585,7 +640,7 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
                   0, s>>>(tb.wgj);
     SP_TRY(jacobi_block(tb.jobs + nm, nm * K, svd_r, svd_c, tb.jst + nm, status, s, true, split));
   }
-  k_svd_finalize<<<nsvd, 1024, sizeof(double) * svd_c, s>>>(tb.jobs, tb.ptrs, tb.ptrs + nsvd, tb.ptrs + 2 * nsvd);
+  svd_finalize(tb.jobs, tb.ptrs, tb.ptrs + nsvd, tb.ptrs + 2 * nsvd, nsvd, svd_c, s);
   // 2 - 6 per matrix; the polar arguments go to the first iterate buffers
   for (int e = 0; e < nm; ++e) {
     const int64_t m = t[ids[e]].rows, n = t[ids[e]].cols, q = std::min(m, n);
@@ -685,65 +740,46 @@ Tables carve_opt_tables(Bump& bp, int n_f) {
 
 // ---- spectral diagnostics and spectrum interpolation ----------------------------------------------
 
-// One workgroup: {delta_Sigma, rho_Sigma, kappa_spec} from the sorted spectra s0, s1 (q), U_0
-// (m x q col-major), P = Delta W V_0 (m x q col-major), W_0 and Delta W (m n entries).
-__global__ void __launch_bounds__(1024) k_diag_final(const double* __restrict__ s0, const double* __restrict__ s1,
-                                                     int64_t q, const double* __restrict__ u0,
-                                                     const double* __restrict__ p, int64_t m, int64_t n,
-                                                     const double* __restrict__ w0, const double* __restrict__ dw,
-                                                     double* __restrict__ out) {
-  __shared__ double red[4][16];
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  double d2 = 0.0, nw0 = 0.0, ndw = 0.0, dg = 0.0;
-  for (int64_t k = threadIdx.x; k < q; k += blockDim.x) d2 += (s1[k] - s0[k]) * (s1[k] - s0[k]);
-  for (int64_t e = threadIdx.x; e < m * n; e += blockDim.x) {
-    nw0 += w0[e] * w0[e];
-    ndw += dw[e] * dw[e];
-  }
-  for (int64_t k = wid; k < q; k += nw) {
-    double x = 0.0;
-    for (int64_t i = lane; i < m; i += 64) x += u0[k * m + i] * p[k * m + i];
-    x = wave_sum_f64(x);
-    if (lane == 0) dg += x * x;
-  }
-  d2 = wave_sum_f64(d2);
-  nw0 = wave_sum_f64(nw0);
-  ndw = wave_sum_f64(ndw);
-  dg = wave_sum_f64(dg);
-  if (lane == 0) {
-    red[0][wid] = d2;
-    red[1][wid] = nw0;
-    red[2][wid] = ndw;
-    red[3][wid] = dg;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    double a[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int c = 0; c < 4; ++c)
-      for (int w = 0; w < nw; ++w) a[c] += red[c][w];
-    const double dist = sqrt(a[0]);
-    out[0] = dist / sqrt(a[1]);
-    out[1] = dist / sqrt(a[2]);
-    out[2] = ((double)m * (double)n / (double)q) * a[3] / a[2];
+// x[k] = <u0_k, p_k>^2 for the q columns (m rows, col-major): one wave per column.
+__global__ void __launch_bounds__(1024) k_col_dot_sq(const double* __restrict__ u0, const double* __restrict__ p,
+                                                     int64_t m, int64_t q, double* __restrict__ x) {
+  const int lane = threadIdx.x & 63, nw = blockDim.x >> 6;
+  for (int64_t k = (int64_t)blockIdx.x * nw + (threadIdx.x >> 6); k < q; k += (int64_t)gridDim.x * nw) {
+    double v = 0.0;
+    for (int64_t i = lane; i < m; i += 64) v += u0[k * m + i] * p[k * m + i];
+    v = wave_sum_f64(v);
+    if (lane == 0) x[k] = v * v;
   }
 }
 
-// out[0] = |a - b|_F^2 over len entries (one workgroup, fixed summation order).
-__global__ void __launch_bounds__(1024) k_sqdist(const double* __restrict__ a, const double* __restrict__ b,
-                                                 int64_t len, double* __restrict__ out) {
-  __shared__ double red[16];
-  double x = 0.0;
-  for (int64_t e = threadIdx.x; e < len; e += blockDim.x) {
-    const double d = a[e] - b[e];
-    x += d * d;
+// One workgroup: {delta_Sigma, rho_Sigma, kappa_spec} from the sorted spectra s0, s1 (q), the squared
+// diagonal entries dg2 (q) of U_0^T Delta W V_0 and sums = {|W_0|_F^2, |Delta W|_F^2}.
+__global__ void __launch_bounds__(1024) k_diag_final(const double* __restrict__ s0, const double* __restrict__ s1,
+                                                     int64_t q, const double* __restrict__ dg2,
+                                                     const double* __restrict__ sums, int64_t m, int64_t n,
+                                                     double* __restrict__ out) {
+  __shared__ double red[2][16];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  double d2 = 0.0, dg = 0.0;
+  for (int64_t k = threadIdx.x; k < q; k += blockDim.x) {
+    d2 += (s1[k] - s0[k]) * (s1[k] - s0[k]);
+    dg += dg2[k];
   }
-  x = wave_sum_f64(x);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  d2 = wave_sum_f64(d2);
+  dg = wave_sum_f64(dg);
+  if (lane == 0) {
+    red[0][wid] = d2;
+    red[1][wid] = dg;
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
-    double t = 0.0;
-    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) t += red[w];
-    out[0] = t;
+    double a[2] = {0.0, 0.0};
+    for (int c = 0; c < 2; ++c)
+      for (int w = 0; w < nw; ++w) a[c] += red[c][w];
+    const double dist = sqrt(a[0]);
+    out[0] = dist / sqrt(sums[0]);
+    out[1] = dist / sqrt(sums[1]);
+    out[2] = ((double)m * (double)n / (double)q) * a[1] / sums[1];
   }
 }
 
@@ -959,13 +995,13 @@ iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, Spectrum
       // A_rec = (L S) R^T in binary64 into the second job's matrix and its own SVD
       k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.ja[0], t[j].base, nullptr, m, n, wide ? 1 : 0, dt);
       SO_TRY(jacobi_block(tb.jobs, 1, r, q, tb.jst, status, s, false, split));
-      k_svd_finalize<<<1, 1024, sizeof(double) * q, s>>>(tb.jobs, tb.ptrs, tb.ptrs + 2, tb.ptrs + 4);
+      svd_finalize(tb.jobs, tb.ptrs, tb.ptrs + 2, tb.ptrs + 4, 1, q, s);
       const double* lf = wide ? b.V[0] : b.U[0];     // r x q left factor of A
       const double* rf = wide ? b.U[0] : b.V[0];     // q x q right factor
       k_scale_cols<<<grid_for(r * q), 256, 0, s>>>(b.G, lf, b.S[0], r, q);
       gemm(r, q, q, 1.0, b.G, 1, r, rf, q, 1, 0.0, b.ja[1], 1, r, s);
       SO_TRY(jacobi_block(tb.jobs + 1, 1, r, q, tb.jst + 1, status, s, false, split));
-      k_svd_finalize<<<1, 1024, sizeof(double) * q, s>>>(tb.jobs + 1, tb.ptrs + 1, tb.ptrs + 3, tb.ptrs + 5);
+      svd_finalize(tb.jobs + 1, tb.ptrs + 1, tb.ptrs + 3, tb.ptrs + 5, 1, q, s);
       k_spectral_error<<<1, 1024, 0, s>>>(b.S[0], b.S[1], q, out + j);
       SO_TRY(hipGetLastError());
       SO_TRY(hipStreamSynchronize(s));
@@ -978,7 +1014,7 @@ iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, Spectrum
                                                   (i && !whole) ? t[j].deltas[0] : nullptr, m, n, wide ? 1 : 0, dt);
     }
     SO_TRY(jacobi_block(tb.jobs, 2, r, q, tb.jst, status, s, false, split));
-    k_svd_finalize<<<2, 1024, sizeof(double) * q, s>>>(tb.jobs, tb.ptrs, tb.ptrs + 2, tb.ptrs + 4);
+    svd_finalize(tb.jobs, tb.ptrs, tb.ptrs + 2, tb.ptrs + 4, 2, q, s);
     if (op == SpectrumOp::kSpectralError) {
       k_spectral_error<<<1, 1024, 0, s>>>(b.S[0], b.S[1], q, out + j);
     } else if (op == SpectrumOp::kDiagnostics) {
@@ -986,7 +1022,10 @@ iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, Spectrum
       k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.G, t[j].deltas[0], nullptr, m, n, 0, dt);
       k_load_f64<<<grid_for(m * n), 256, 0, s>>>(b.Wst, t[j].base, nullptr, m, n, 0, dt);
       gemm(m, q, n, 1.0, b.G, 1, m, b.V[0], 1, n, 0.0, b.FU, 1, m, s);
-      k_diag_final<<<1, 1024, 0, s>>>(b.S[0], b.S[1], q, b.U[0], b.FU, m, n, b.Wst, b.G, out + 3 * (int64_t)j);
+      k_col_dot_sq<<<(unsigned)std::min<int64_t>((q + 15) / 16, 4096), 1024, 0, s>>>(b.U[0], b.FU, m, q, b.P);
+      dot1(b.Wst, b.Wst, m * n, false, b.red, b.gram, s);
+      dot1(b.G, b.G, m * n, false, b.red, b.gram + 1, s);
+      k_diag_final<<<1, 1024, 0, s>>>(b.S[0], b.S[1], q, b.P, b.gram, m, n, out + 3 * (int64_t)j);
     } else if (op == SpectrumOp::kInterpolate) {
       k_mix<<<grid_for(q), 256, 0, s>>>(b.P, b.S[0], b.S[1], q, param);
       k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, b.U[1], b.P, m, q);
@@ -1004,20 +1043,20 @@ iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, Spectrum
         gemm(m, n, rk, 1.0, b.FU, 1, m, b.V[1], n, 1, 0.0, wi, 1, m, s);
         k_scale_cols<<<grid_for(m * rk), 256, 0, s>>>(b.FU, b.U[0], b.S[0], m, rk);
         gemm(m, n, rk, 1.0, b.FU, 1, m, b.V[0], n, 1, 0.0, wj, 1, m, s);
-        k_sqdist<<<1, 1024, 0, s>>>(wi, wj, m * n, o);
+        dot1(wi, wj, m * n, true, b.red, o, s);
         // T1 = U_j^T W_i^(r) (rk x n), W_L = U_j T1
         gemm(rk, n, m, 1.0, b.U[0], m, 1, wi, 1, m, 0.0, b.FV, 1, rk, s);
         gemm(m, n, rk, 1.0, b.U[0], 1, m, b.FV, 1, rk, 0.0, b.G, 1, m, s);
-        k_sqdist<<<1, 1024, 0, s>>>(wi, b.G, m * n, o + 2);
+        dot1(wi, b.G, m * n, true, b.red, o + 2, s);
         // T2 = W_i^(r) V_j (m x rk), W_R = T2 V_j^T
         gemm(m, rk, n, 1.0, wi, 1, m, b.V[0], 1, n, 0.0, b.XU, 1, m, s);
         gemm(m, n, rk, 1.0, b.XU, 1, m, b.V[0], n, 1, 0.0, b.G, 1, m, s);
-        k_sqdist<<<1, 1024, 0, s>>>(wi, b.G, m * n, o + 3);
+        dot1(wi, b.G, m * n, true, b.red, o + 3, s);
         // core B = T1 V_j (rk x rk), W_mix = (U_j B) V_j^T
         gemm(rk, rk, n, 1.0, b.FV, 1, rk, b.V[0], 1, n, 0.0, b.P, 1, rk, s);
         gemm(m, rk, rk, 1.0, b.U[0], 1, m, b.P, 1, rk, 0.0, b.AU, 1, m, s);
         gemm(m, n, rk, 1.0, b.AU, 1, m, b.V[0], n, 1, 0.0, b.G, 1, m, s);
-        k_sqdist<<<1, 1024, 0, s>>>(wi, b.G, m * n, o + 1);
+        dot1(wi, b.G, m * n, true, b.red, o + 1, s);
         k_transport_final<<<1, 64, 0, s>>>(b.S[0], b.S[1], q, rk, o);
       }
     }

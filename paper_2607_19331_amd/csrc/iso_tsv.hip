@@ -30,7 +30,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kPowerIters = 2;
-constexpr size_t kTsvChunkBudget = 8ull << 30;   // workspace per chunk of matrices
+constexpr size_t kTsvChunkBudget = 32ull << 30;  // workspace per chunk of matrices (all 84 MLP matrices of a 7B stack)
 constexpr int kMaxNB = 8;                         // sketch width up to 128
 
 int64_t rup(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
@@ -75,6 +75,7 @@ struct Mat {
   double* ns[2][5];         // per side (U, V): Newton-Schulz Y0, Z0, Y1, Z1, T (Kr x Kr each)
   double* eye;              // Kr x Kr identity
   double* cs;               // 2 scale factors
+  struct NsFlags* nf;       // per side: convergence of the Newton-Schulz iteration
   double* MU;  double* MV;  // Kr x Kr inverse square roots
   double* Up;  double* Vp;                              // R x Kr, C x Kr
   uint16_t* ah; uint16_t* al;   // R x ldk split of U_perp Sigma
@@ -83,7 +84,18 @@ struct Mat {
 };
 
 constexpr int kSlabs = 16;
-constexpr int kNsIters = 18;     // coupled Newton-Schulz steps (quadratic convergence from |I - A| < 1)
+constexpr int kNsIters = 18;     // coupled Newton-Schulz steps at most (quadratic convergence from |I - A| < 1)
+constexpr int kNsCheck = 4;      // steps queued between host reads of the done flags
+constexpr double kNsTol = 1e-10; // max |T - I| from which one more step reaches rounding level
+
+// One side of one matrix: a job stops after the step whose T = (3 I - Z Y) / 2 is within kNsTol
+// of I (Z Y then within 2 kNsTol of I, and one more quadratic step takes it to rounding level).
+struct NsFlags {
+  int done;      // no further steps
+  int last;      // the step being taken is the last
+  int steps;     // steps taken: Y, Z are in buffers 2 (steps & 1) and 2 (steps & 1) + 1
+  int pad;
+};
 
 __device__ __forceinline__ uint16_t bf16_rne_f32(float f) {
   uint32_t b = __float_as_uint(f);
@@ -980,7 +992,10 @@ __global__ void __launch_bounds__(256) k_ns_init(const Mat* __restrict__ mats, i
     __syncthreads();
   }
   const double c = (red[0] > 0.0) ? red[0] : 1.0;
-  if (threadIdx.x == 0) *cscale = c;
+  if (threadIdx.x == 0) {
+    *cscale = c;
+    M.nf[side] = NsFlags{0, 0, 0, 0};
+  }
   for (int64_t e = threadIdx.x; e < n * n; e += blockDim.x) {
     const double id = ((e / n) == (e % n)) ? 1.0 : 0.0;
     Y[e] = G[e] / c;
@@ -997,22 +1012,51 @@ __global__ void k_copy_jobs(double* const* dst, const double* const* src, int64_
     b[e] = a[e];
 }
 
-// M = Z / sqrt(c), and flag non-convergence (|T - I| large at the last step).
-__global__ void __launch_bounds__(256) k_ns_finish(const Mat* __restrict__ mats, int par, uint32_t* status) {
+// After the T products of a step: last = (max |T - I| <= kNsTol) for each job still running (job
+// 2 m + side, one workgroup each).
+__global__ void __launch_bounds__(256) k_ns_test(const Mat* __restrict__ mats) {
+  __shared__ double red[256];
+  const Mat& M = mats[blockIdx.x >> 1];
+  const int side = blockIdx.x & 1;
+  NsFlags& f = M.nf[side];
+  if (f.done) return;
+  const int64_t n = M.Kr;
+  const double* T = M.ns[side][4];
+  double d = 0.0;
+  for (int64_t e = threadIdx.x; e < n * n; e += blockDim.x)
+    d = fmax(d, fabs(T[e] - (((e / n) == (e % n)) ? 1.0 : 0.0)));
+  red[threadIdx.x] = d;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + o]);
+    __syncthreads();
+  }
+  // a NaN never passes the test: the job then runs to the step limit and is flagged
+  if (threadIdx.x == 0) f.last = red[0] <= kNsTol ? 1 : 0;
+}
+
+__global__ void k_ns_step_end(const Mat* __restrict__ mats, int njobs) {
+  for (int j = threadIdx.x; j < njobs; j += blockDim.x) {
+    NsFlags& f = mats[j >> 1].nf[j & 1];
+    if (!f.done) {
+      f.steps += 1;
+      if (f.last) f.done = 1;
+    }
+  }
+}
+
+// M = Z / sqrt(c) from the buffer the job's last step wrote; a job that did not converge within
+// kNsIters steps is flagged.
+__global__ void __launch_bounds__(256) k_ns_finish(const Mat* __restrict__ mats, uint32_t* status) {
   const Mat& M = mats[blockIdx.x];
   const int side = blockIdx.y;
   const int64_t n = M.Kr;
+  const NsFlags f = M.nf[side];
   double* Mout = side ? M.MV : M.MU;
-  const double* Z = M.ns[side][2 * par + 1];
-  const double* T = M.ns[side][4];
+  const double* Z = M.ns[side][2 * (f.steps & 1) + 1];
   const double inv = 1.0 / sqrt(M.cs[side]);
-  bool bad = false;
-  for (int64_t e = threadIdx.x; e < n * n; e += blockDim.x) {
-    Mout[e] = Z[e] * inv;
-    const double id = ((e / n) == (e % n)) ? 1.0 : 0.0;
-    bad |= !(fabs(T[e] - id) < 1e-6);
-  }
-  if (bad) flag_status(status, kStatusInternal);
+  for (int64_t e = threadIdx.x; e < n * n; e += blockDim.x) Mout[e] = Z[e] * inv;
+  if (threadIdx.x == 0 && !f.done) flag_status(status, kStatusInternal);
 }
 
 // ---- host side ----------------------------------------------------------------------------------
@@ -1109,6 +1153,7 @@ size_t table_bytes(int nm, int K) {
   b += align_up(sizeof(double*) * 3 * np, 256);
   b += 12 * align_up(sizeof(GemmJob) * (size_t)std::max(np, kSlabs * nm * 2), 256);
   b += 2 * align_up(sizeof(double*) * 2 * nm, 256);
+  b += align_up(sizeof(NsFlags) * 2 * nm, 256);
   return b;
 }
 
@@ -1191,6 +1236,7 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     for (int q = 0; q < 12; ++q) d_gj[q] = cv.take<GemmJob>(std::max(np, kSlabs * nm * 2));
     const double** d_nsrc = cv.take<const double*>(2 * nm);
     double** d_ndst = cv.take<double*>(2 * nm);
+    NsFlags* d_nf = cv.take<NsFlags>(2 * nm);
     cv.off = table_bytes(nm, K);
     std::vector<Prob> hp(np);
     std::vector<Mat> hm(nm);
@@ -1229,6 +1275,7 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
       M.Kr = z.Kr;
       M.ldk = z.ldk;
       M.alpha = a.alpha;
+      M.nf = d_nf + 2 * m;
     }
     // all problems of a chunk share L (matrices of one chunk must give the same sketch width)
     for (int p = 0; p < np; ++p)
@@ -1271,9 +1318,11 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
           double* Yb = q[2 * (1 - a)];
           double* Zb = q[2 * (1 - a) + 1];
           double* T = q[4];
-          gj[6 + 3 * a].push_back(GemmJob{Za, Ya, T, n, 1, n, 1, n, 1, n, n, n, -0.5, 1.5});   // T = 1.5 I - Z Y / 2
-          gj[7 + 3 * a].push_back(GemmJob{Ya, T, Yb, n, 1, n, 1, n, 1, n, n, n, 1.0, 0.0});    // Y' = Y T
-          gj[8 + 3 * a].push_back(GemmJob{T, Za, Zb, n, 1, n, 1, n, 1, n, n, n, 1.0, 0.0});    // Z' = T Z
+          const int* skip = &M.nf[sd].done;
+          // T = 1.5 I - Z Y / 2, Y' = Y T, Z' = T Z
+          gj[6 + 3 * a].push_back(GemmJob{Za, Ya, T, n, 1, n, 1, n, 1, n, n, n, -0.5, 1.5, 0, skip});
+          gj[7 + 3 * a].push_back(GemmJob{Ya, T, Yb, n, 1, n, 1, n, 1, n, n, n, 1.0, 0.0, 0, skip});
+          gj[8 + 3 * a].push_back(GemmJob{T, Za, Zb, n, 1, n, 1, n, 1, n, n, n, 1.0, 0.0, 0, skip});
         }
         ns_src.push_back(M.eye);
         ns_dst.push_back(q[4]);
@@ -1346,7 +1395,7 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     const size_t jlds = sizeof(double) * 2 * (size_t)L * L;
     if (jlds <= kJacobiLdsMax) k_jacobi_lds<<<np, kJacobiThreads, jlds, s>>>(d_jobs, status);
     else k_jacobi<<<np, kJacobiThreads, 0, s>>>(d_jobs, status);
-    k_svd_finalize<<<np, 1024, sizeof(double) * L, s>>>(d_jobs, d_ptrs, d_ptrs + np, d_ptrs + 2 * np);
+    svd_finalize(d_jobs, d_ptrs, d_ptrs + np, d_ptrs + 2 * np, np, L, s);
     // U_i = Q Ut[:, :r], V_i = Q2 Vt[:, :r]: both factors end in buffer 0 (an even number of QR
     // passes: 2 + kPowerIters for X, kPowerIters + 2 for Z)
     static_assert(kPowerIters % 2 == 0, "ping-pong parity");
@@ -1362,15 +1411,25 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
       k_sum_gram<<<dim3(grid_for(Kr * Kr), (unsigned)nm), 256, 0, s>>>(d_mat, side);
       k_ns_init<<<nm, 256, 0, s>>>(d_mat, side);
     }
-    int par = 0;
-    for (int it = 0; it < kNsIters; ++it) {
-      k_copy_jobs<<<dim3(grid_for(Kr * Kr), (unsigned)(2 * nm)), 256, 0, s>>>(d_ndst, d_nsrc, Kr * Kr);
-      k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[6 + 3 * par]);
-      k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[7 + 3 * par]);
-      k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[8 + 3 * par]);
-      par = 1 - par;
+    // every job takes its steps in the same parity order; a converged job's products are skipped
+    // and the host stops queueing steps once every job is done
+    std::vector<NsFlags> hf(2 * nm);
+    for (int it = 0, par = 0; it < kNsIters;) {
+      for (int b = 0; b < kNsCheck && it < kNsIters; ++b, ++it, par = 1 - par) {
+        k_copy_jobs<<<dim3(grid_for(Kr * Kr), (unsigned)(2 * nm)), 256, 0, s>>>(d_ndst, d_nsrc, Kr * Kr);
+        k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[6 + 3 * par]);
+        k_ns_test<<<(unsigned)(2 * nm), 256, 0, s>>>(d_mat);
+        k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[7 + 3 * par]);
+        k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[8 + 3 * par]);
+        k_ns_step_end<<<1, 256, 0, s>>>(d_mat, 2 * nm);
+      }
+      bool all = true;
+      TS_TRY(hipMemcpyAsync(hf.data(), d_nf, sizeof(NsFlags) * 2 * nm, hipMemcpyDeviceToHost, s));
+      TS_TRY(hipStreamSynchronize(s));
+      for (int j = 0; j < 2 * nm; ++j) all = all && hf[j].done;
+      if (all) break;
     }
-    k_ns_finish<<<dim3((unsigned)nm, 2), 256, 0, s>>>(d_mat, par, status);
+    k_ns_finish<<<dim3((unsigned)nm, 2), 256, 0, s>>>(d_mat, status);
     k_gemm_jobs<<<dim3((unsigned)((maxM + 63) / 64), tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[5]);
     // 4. reconstruction with the update fused
     k_split_mats<<<dim3(grid_for(maxR * rup(Kr, 32)), (unsigned)nm), 256, 0, s>>>(d_mat, 0);

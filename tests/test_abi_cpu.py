@@ -69,9 +69,12 @@ def test_host_validation_errors():
     a.mode = 9
     assert L.iso_update(iso._table(es), 1, 2, iso.BF16, ctypes.byref(a), FAKE * 16, 1 << 30, None) == 1
     a.mode, a.rho_keep, a.ridge, a.c_min, a.c_max = 2, 0.9, 1e-12, 0.0, 1.5
-    big = [entry(rows=16385, cols=64, k=0)]
+    big = [entry(rows=16385, cols=16385, k=0)]           # the limit is on min(rows, cols)
     assert L.iso_update(iso._table(big), 1, 2, iso.BF16, ctypes.byref(a), FAKE * 16, 1 << 30, None) == \
         _lib.ERR_UNSUPPORTED
+    tall = [entry(rows=152064, cols=64, k=0)]             # a long side alone is accepted
+    assert L.iso_update(iso._table(tall), 1, 2, iso.BF16, ctypes.byref(a), FAKE * 16, 100, None) == \
+        _lib.ERR_WORKSPACE
     a.rho_keep = 0.0
     assert L.iso_update(iso._table(es), 1, 2, iso.BF16, ctypes.byref(a), FAKE * 16, 1 << 30, None) == 1
     assert L.iso_update(iso._table(es), 1, 2, iso.BF16, None, FAKE * 16, 1 << 30, None) == 1
@@ -182,8 +185,10 @@ def test_transport_ratio_validation():
     assert call(None, 1) == _lib.ERR_INVALID_ARG
     assert call(fr(0.9), 1, out=None) == _lib.ERR_INVALID_ARG
     assert call(fr(0.9), 1, out=FAKE * 8 + 4) == _lib.ERR_ALIGNMENT
-    big = [iso.Entry(16385, 8, base=FAKE, deltas=[FAKE + 0x1000], out=None, k=0)]
+    big = [iso.Entry(16385, 16385, base=FAKE, deltas=[FAKE + 0x1000], out=None, k=0)]
     assert call(fr(0.9), 1, table=iso._table(big)) == _lib.ERR_UNSUPPORTED
+    tall = [iso.Entry(16385, 8, base=FAKE, deltas=[FAKE + 0x1000], out=None, k=0)]
+    assert call(fr(0.9), 1, table=iso._table(tall), ws_bytes=100) == _lib.ERR_WORKSPACE
     assert call(fr(0.2, 0.9), 2, ws_bytes=100) == _lib.ERR_WORKSPACE
     assert call(fr(*([0.5] * 16)), 16, n_t=0) == _lib.OK
 
@@ -231,8 +236,10 @@ def test_spectral_error_validation():
     nodelta = iso._table([iso.Entry(16, 16, base=FAKE, deltas=[None], out=None, k=0)])
     assert call(table=nodelta) == _lib.ERR_INVALID_ARG          # W_rec is required unless self_recon
     assert call(self_recon=1, table=nodelta, ws_bytes=100) == _lib.ERR_WORKSPACE
-    big = iso._table([iso.Entry(16385, 8, base=FAKE, deltas=[FAKE + 0x1000], out=None, k=0)])
+    big = iso._table([iso.Entry(16385, 16385, base=FAKE, deltas=[FAKE + 0x1000], out=None, k=0)])
     assert call(table=big) == _lib.ERR_UNSUPPORTED
+    tall = iso._table([iso.Entry(8, 16385, base=FAKE, deltas=[FAKE + 0x1000], out=None, k=0)])
+    assert call(table=tall, ws_bytes=100) == _lib.ERR_WORKSPACE
 
 
 def test_noalloc_validation():
