@@ -210,7 +210,9 @@ typedef struct iso_update_args {
  *            their Gram matrix, ridge solve and clip, aggregate projection,
  *            polar retraction, W_* = U_* Sigma_0 V_*^T (rounded once).
  *            Deltas are the raw expert deltas (no TopKMask).  Supported for
- *            rows, cols <= ISO_SPECTRAL_MAX_DIM.
+ *            min(rows, cols) <= ISO_SPECTRAL_MAX_DIM (the long side is bounded
+ *            only by rows * cols < 2^32 and the workspace: binary64 copies of
+ *            about 4K + 7 matrices of the tensor's size per call batch).
  */
 iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_update_args* a, void* ws,
                       size_t ws_bytes, void* stream);
@@ -247,7 +249,7 @@ iso_status iso_update_noalloc(const iso_tensor* t, int n_t, int K, iso_dtype dt,
  *   rho_Sigma   = |sigma(W_1) - sigma(W_0)|_2 / |Delta W|_F,
  *   kappa_spec  = (rows cols / q) |diag(U_0^T Delta W V_0)|_2^2 / |Delta W|_F^2.
  * Workspace: iso_workspace_size(ISO_OP_UPDATE_SPECTRAL, t, n_t, 1, dt); the
- * size limit of ISO-Merger (rows, cols <= ISO_SPECTRAL_MAX_DIM).
+ * size limit of ISO-Merger (min(rows, cols) <= ISO_SPECTRAL_MAX_DIM).
  */
 iso_status iso_spectral_diagnostics(const iso_tensor* t, int n_t, iso_dtype dt, double* out, void* ws,
                                     size_t ws_bytes, void* stream);

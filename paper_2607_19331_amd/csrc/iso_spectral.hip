@@ -15,7 +15,8 @@
 //   7. W_* = U_* Sigma_0 V_*^T, rounded once to the storage type.
 // Matrices are held column-major in the workspace; dense products use a tiled binary64 GEMM on
 // MFMA.  The matrices of one call go in batches whose SVDs (and then whose polar retractions)
-// run as one Jacobi job set.  Sizes up to ISO_SPECTRAL_MAX_DIM per side.
+// run as one Jacobi job set.  The shorter side is at most ISO_SPECTRAL_MAX_DIM (the column norms
+// of the SVD finalize sit in LDS); the longer side is unbounded but for the workspace.
 #include <cmath>
 #include <vector>
 
