@@ -809,84 +809,7 @@ __global__ void __launch_bounds__(1024) k_normalize_cols(double* __restrict__ L,
 unsigned grid_for(int64_t n) { return (unsigned)std::max<int64_t>(1, std::min<int64_t>((n + 255) / 256, 4096)); }
 
 
-// C(i,j) = alpha * sum_k A(i,k) B(k,j) + beta * C(i,j); X(i,k) at X[i*xs0 + k*xs1].
-// With blockIdx.z > 0 splits: block z sums k in [z*kz, (z+1)*kz) and writes C + z*cz (beta ignored).
 constexpr int GT = 64, GK = 16;
-__global__ void __launch_bounds__(256) k_gemm(int64_t M, int64_t N, int64_t Kd, double alpha, const double* __restrict__ A,
-                                              int64_t as0, int64_t as1, const double* __restrict__ B, int64_t bs0,
-                                              int64_t bs1, double beta, double* __restrict__ C, int64_t cs0,
-                                              int64_t cs1, int64_t kz, int64_t cz) {
-  __shared__ double As[GK][GT + 1];
-  __shared__ double Bs[GK][GT + 1];
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  const int64_t i0 = (int64_t)blockIdx.x * GT, j0 = (int64_t)blockIdx.y * GT;
-  const int64_t kb = (gridDim.z > 1) ? (int64_t)blockIdx.z * kz : 0;
-  const int64_t ke = (gridDim.z > 1) ? std::min(Kd, kb + kz) : Kd;
-  double* Cz = C + ((gridDim.z > 1) ? (int64_t)blockIdx.z * cz : 0);
-  double acc[4][4] = {};
-  for (int64_t k0 = kb; k0 < ke; k0 += GK) {
-    for (int e = threadIdx.x; e < GK * GT; e += 256) {
-      const int kk = e / GT, ii = e % GT;
-      const int64_t gi = i0 + ii, gk = k0 + kk, gj = j0 + ii;
-      As[kk][ii] = (gi < M && gk < ke) ? A[gi * as0 + gk * as1] : 0.0;
-      Bs[kk][ii] = (gj < N && gk < ke) ? B[gk * bs0 + gj * bs1] : 0.0;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < GK; ++kk) {
-      double a[4], b[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) { a[u] = As[kk][tx + 16 * u]; b[u] = Bs[kk][ty + 16 * u]; }
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc[u][v] = acc[u][v] + a[u] * b[v];
-    }
-    __syncthreads();
-  }
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int64_t gi = i0 + tx + 16 * u, gj = j0 + ty + 16 * v;
-      if (gi < M && gj < N) {
-        double* cp = Cz + gi * cs0 + gj * cs1;
-        *cp = (beta == 0.0 || gridDim.z > 1) ? alpha * acc[u][v] : alpha * acc[u][v] + beta * *cp;
-      }
-    }
-}
-
-// out[e] = sum_z parts[z*stride + e], z in order (deterministic split-K reduction)
-__global__ void k_sum_parts(double* __restrict__ out, const double* __restrict__ parts, int nz, int64_t stride,
-                            int64_t n) {
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
-    double s = 0.0;
-    for (int z = 0; z < nz; ++z) s = s + parts[(int64_t)z * stride + e];
-    out[e] = s;
-  }
-}
-
-inline void gemm(int64_t M, int64_t N, int64_t Kd, double alpha, const double* A, int64_t as0, int64_t as1,
-                 const double* B, int64_t bs0, int64_t bs1, double beta, double* C, int64_t cs0, int64_t cs1,
-                 hipStream_t s) {
-  dim3 grid((unsigned)((M + GT - 1) / GT), (unsigned)((N + GT - 1) / GT), 1);
-  k_gemm<<<grid, 256, 0, s>>>(M, N, Kd, alpha, A, as0, as1, B, bs0, bs1, beta, C, cs0, cs1, 0, 0);
-}
-
-// C (M x N, written with strides cs0/cs1 = contiguous parts of size M*N) = A B summed over nz
-// K-slabs; `parts` holds nz * M * N doubles.
-inline void gemm_splitk(int64_t M, int64_t N, int64_t Kd, const double* A, int64_t as0, int64_t as1, const double* B,
-                        int64_t bs0, int64_t bs1, double* C, double* parts, int nz, hipStream_t s) {
-  const int64_t kz = ((Kd + nz - 1) / nz + GK - 1) / GK * GK;
-  nz = (int)std::max<int64_t>(1, (Kd + kz - 1) / kz);
-  dim3 grid((unsigned)((M + GT - 1) / GT), (unsigned)((N + GT - 1) / GT), (unsigned)nz);
-  if (nz == 1) {
-    k_gemm<<<grid, 256, 0, s>>>(M, N, Kd, 1.0, A, as0, as1, B, bs0, bs1, 0.0, C, N, 1, 0, 0);
-    return;
-  }
-  k_gemm<<<grid, 256, 0, s>>>(M, N, Kd, 1.0, A, as0, as1, B, bs0, bs1, 0.0, parts, N, 1, kz, M * N);
-  k_sum_parts<<<grid_for(M * N), 256, 0, s>>>(C, parts, nz, M * N, M * N);
-}
 
 }  // namespace
 }  // namespace iso
@@ -912,80 +835,137 @@ struct GemmJob {
 
 typedef double gemm_f64x4_t __attribute__((ext_vector_type(4)));
 
-// 64 x 64 output tile per workgroup on v_mfma_f64_16x16x4_f64 (lane (ln, g) supplies A[ln][g]
-// and B[g][ln], receives D[g + 4v][ln] in register pair v): four waves as 2 x 2, each a 32 x 32 block of four
-// MFMA tiles; k in steps of 16 staged in LDS.  Operands are loaded along whichever of their
-// strides is 1, so row- and column-major inputs both read whole cache lines.  LDS rows are 80
-// doubles apart, which puts the four k rows of a fragment read on disjoint bank halves.
-constexpr int GJP = 80;
-__global__ void __launch_bounds__(256) k_gemm_jobs(const GemmJob* __restrict__ jobs) {
-  __shared__ double As[GK][GJP];
-  __shared__ double Bs[GK][GJP];
-  const GemmJob J = jobs[blockIdx.z];
-  const int64_t i0 = (int64_t)blockIdx.x * GT, j0 = (int64_t)blockIdx.y * GT;
+// One output tile of C = alpha A B + beta C on v_mfma_f64_16x16x4_f64 (lane (ln, g) supplies
+// A[ln][g] and B[g][ln], receives D[g + 4v][ln] in register pair v).  W MFMA blocks per wave side:
+// the four waves (2 x 2) each own a 16W x 16W block of the 32W x 32W tile; W = 2 gives 64 x 64
+// tiles, W = 4 gives 128 x 128 tiles (16 MFMAs per 4-deep k step per wave, and each k-tile load
+// feeds twice the rows and columns).  k in steps of GK = 16 staged in LDS, double-buffered: the
+// next k-tile is loaded into registers before the current one's MFMAs and written to the other
+// buffer after them, one barrier per step.  Operands are loaded along whichever of their strides
+// is 1, so row- and column-major inputs both read whole cache lines.  LDS rows are padded so that
+// the four k rows of a fragment read fall on different bank halves.
+template <int W>
+struct GemmTile {
+  static constexpr int TM = 32 * W, TW = 16 * W, PAD = (W == 2) ? 80 : TM + 16, PT = GK * TM / 256;
+};
+
+template <int W>
+__device__ __forceinline__ void gemm_tile(const GemmJob& J, int64_t bx, int64_t by) {
+  using T = GemmTile<W>;
+  constexpr int TM = T::TM, TW = T::TW, PAD = T::PAD, PT = T::PT;
+  __shared__ double As[2][GK][PAD];
+  __shared__ double Bs[2][GK][PAD];
+  const int64_t i0 = bx * TM, j0 = by * TM;
   if (i0 >= J.M || j0 >= J.N || (J.upper && i0 > j0)) return;
   if (J.skip != nullptr && *J.skip != 0) return;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
   const int wm = w >> 1, wn = w & 1;
   const bool a_kfast = J.as1 == 1, b_kfast = J.bs0 == 1;
-  gemm_f64x4_t acc[2][2];
+  gemm_f64x4_t acc[W][W];
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
+  for (int rb = 0; rb < W; ++rb)
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = gemm_f64x4_t{0.0, 0.0, 0.0, 0.0};
-  // the next k-tile is loaded into registers while the current one is multiplied
-  constexpr int PT = (GK * GT) / 256;
+    for (int cb = 0; cb < W; ++cb) acc[rb][cb] = gemm_f64x4_t{0.0, 0.0, 0.0, 0.0};
   double pa[PT], pb[PT];
+  // element e of a k-tile: 16 consecutive k of one row (k-fast operand) or TM consecutive rows
+  // of one k (the other)
   auto load = [&](int64_t k0) {
 #pragma unroll
     for (int q = 0; q < PT; ++q) {
       const int e = threadIdx.x + 256 * q;
-      const int ka = a_kfast ? (e & 15) : (e >> 6), ia = a_kfast ? (e >> 4) : (e & 63);
-      const int kb = b_kfast ? (e & 15) : (e >> 6), jb = b_kfast ? (e >> 4) : (e & 63);
+      const int ka = a_kfast ? (e & 15) : (e / TM), ia = a_kfast ? (e >> 4) : (e % TM);
+      const int kb = b_kfast ? (e & 15) : (e / TM), jb = b_kfast ? (e >> 4) : (e % TM);
       const int64_t gi = i0 + ia, gka = k0 + ka, gj = j0 + jb, gkb = k0 + kb;
       pa[q] = (gi < J.M && gka < J.K) ? J.A[gi * J.as0 + gka * J.as1] : 0.0;
       pb[q] = (gj < J.N && gkb < J.K) ? J.B[gkb * J.bs0 + gj * J.bs1] : 0.0;
     }
   };
-  load(0);
-  for (int64_t k0 = 0; k0 < J.K; k0 += GK) {
+  auto store = [&](int buf) {
 #pragma unroll
     for (int q = 0; q < PT; ++q) {
       const int e = threadIdx.x + 256 * q;
-      const int ka = a_kfast ? (e & 15) : (e >> 6), ia = a_kfast ? (e >> 4) : (e & 63);
-      const int kb = b_kfast ? (e & 15) : (e >> 6), jb = b_kfast ? (e >> 4) : (e & 63);
-      As[ka][ia] = pa[q];
-      Bs[kb][jb] = pb[q];
+      const int ka = a_kfast ? (e & 15) : (e / TM), ia = a_kfast ? (e >> 4) : (e % TM);
+      const int kb = b_kfast ? (e & 15) : (e / TM), jb = b_kfast ? (e >> 4) : (e % TM);
+      As[buf][ka][ia] = pa[q];
+      Bs[buf][kb][jb] = pb[q];
     }
-    __syncthreads();
-    if (k0 + GK < J.K) load(k0 + GK);
+  };
+  load(0);
+  store(0);
+  __syncthreads();
+  int buf = 0;
+  for (int64_t k0 = 0; k0 < J.K; k0 += GK) {
+    const bool more = k0 + GK < J.K;
+    if (more) load(k0 + GK);
 #pragma unroll
     for (int sub = 0; sub < GK / 4; ++sub) {
-      double a[2], b[2];
+      double a[W], b[W];
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb) a[rb] = As[4 * sub + g][32 * wm + 16 * rb + ln];
+      for (int rb = 0; rb < W; ++rb) a[rb] = As[buf][4 * sub + g][TW * wm + 16 * rb + ln];
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb) b[cb] = Bs[4 * sub + g][32 * wn + 16 * cb + ln];
+      for (int cb = 0; cb < W; ++cb) b[cb] = Bs[buf][4 * sub + g][TW * wn + 16 * cb + ln];
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
+      for (int rb = 0; rb < W; ++rb)
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
+        for (int cb = 0; cb < W; ++cb)
           acc[rb][cb] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[rb], b[cb], acc[rb][cb], 0, 0, 0);
     }
+    // the other buffer was last read before the previous step's barrier
+    if (more) store(buf ^ 1);
     __syncthreads();
+    buf ^= 1;
   }
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
+  for (int rb = 0; rb < W; ++rb)
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb)
+    for (int cb = 0; cb < W; ++cb)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int64_t gi = i0 + 32 * wm + 16 * rb + g + 4 * v, gj = j0 + 32 * wn + 16 * cb + ln;
+        const int64_t gi = i0 + TW * wm + 16 * rb + g + 4 * v, gj = j0 + TW * wn + 16 * cb + ln;
         if (gi < J.M && gj < J.N) {
           double* cp = J.C + gi * J.cs0 + gj * J.cs1;
           *cp = (J.beta == 0.0) ? J.alpha * acc[rb][cb][v] : J.alpha * acc[rb][cb][v] + J.beta * *cp;
         }
       }
+}
+
+// A batch of jobs: grid.z indexes the job.
+template <int W>
+__global__ void __launch_bounds__(256) k_gemm_jobs(const GemmJob* __restrict__ jobs) {
+  const GemmJob J = jobs[blockIdx.z];
+  gemm_tile<W>(J, blockIdx.x, blockIdx.y);
+}
+
+// One job passed by value.
+template <int W>
+__global__ void __launch_bounds__(256) k_gemm_one(GemmJob J) {
+  gemm_tile<W>(J, blockIdx.x, blockIdx.y);
+}
+
+// 128 x 128 tiles once the outputs are at least 256 on both sides, else 64 x 64.
+inline bool gemm_big(int64_t M, int64_t N) { return M >= 256 && N >= 256; }
+
+// njobs jobs from a device table, at most max_m x max_n outputs each.
+inline void gemm_jobs(const GemmJob* jobs, int njobs, int64_t max_m, int64_t max_n, hipStream_t s) {
+  if (gemm_big(max_m, max_n)) {
+    const dim3 g((unsigned)((max_m + 127) / 128), (unsigned)((max_n + 127) / 128), (unsigned)njobs);
+    k_gemm_jobs<4><<<g, 256, 0, s>>>(jobs);
+  } else {
+    const dim3 g((unsigned)((max_m + 63) / 64), (unsigned)((max_n + 63) / 64), (unsigned)njobs);
+    k_gemm_jobs<2><<<g, 256, 0, s>>>(jobs);
+  }
+}
+
+// C(i,j) = alpha * sum_k A(i,k) B(k,j) + beta * C(i,j); X(i,k) at X[i*xs0 + k*xs1].
+inline void gemm(int64_t M, int64_t N, int64_t Kd, double alpha, const double* A, int64_t as0, int64_t as1,
+                 const double* B, int64_t bs0, int64_t bs1, double beta, double* C, int64_t cs0, int64_t cs1,
+                 hipStream_t s) {
+  const GemmJob J{A, B, C, as0, as1, bs0, bs1, cs0, cs1, M, N, Kd, alpha, beta, 0, nullptr};
+  if (gemm_big(M, N)) {
+    k_gemm_one<4><<<dim3((unsigned)((M + 127) / 128), (unsigned)((N + 127) / 128)), 256, 0, s>>>(J);
+  } else {
+    k_gemm_one<2><<<dim3((unsigned)((M + 63) / 64), (unsigned)((N + 63) / 64)), 256, 0, s>>>(J);
+  }
 }
 
 }  // namespace

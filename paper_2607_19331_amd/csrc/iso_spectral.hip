@@ -505,7 +505,6 @@ void middle_steps(const Bufs& b, int64_t m, int64_t n, int K, const SpectralArgs
 // reads the done flags every kNsCheckSteps steps.  On return hst holds every job's state.
 hipError_t polar_batch(const Tables& tb, int njobs, int64_t max_rows, int64_t max_q, std::vector<NsState>& hst,
                        uint32_t* status, hipStream_t s, bool scaled = false) {
-  const unsigned tq = (unsigned)((max_q + GT - 1) / GT), tr = (unsigned)((max_rows + GT - 1) / GT);
   const unsigned cb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_q + 3) / 4, 1024));
   const unsigned fb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_q * max_q + 255) / 256, 2048));
   k_ns_begin<<<1, 256, 0, s>>>(tb.nst, njobs);
@@ -514,10 +513,10 @@ hipError_t polar_batch(const Tables& tb, int njobs, int64_t max_rows, int64_t ma
     for (int b = 0; b < kNsCheckSteps && step < kNsMaxSteps; ++b, ++step) {
       const int p = step & 1;
       k_ns_reset<<<1, 256, 0, s>>>(tb.nst, njobs);
-      k_gemm_jobs<<<dim3(tq, tq, (unsigned)njobs), 256, 0, s>>>(tb.ngj[2 * p]);
+      gemm_jobs(tb.ngj[2 * p], njobs, max_q, max_q, s);
       k_ns_stats<<<dim3(cb, (unsigned)njobs), 256, 0, s>>>(tb.ns, tb.nst);
       k_ns_form<<<dim3(fb, (unsigned)njobs), 256, 0, s>>>(tb.ns, tb.nst, scaled ? 1 : 0);
-      k_gemm_jobs<<<dim3(tr, tq, (unsigned)njobs), 256, 0, s>>>(tb.ngj[2 * p + 1]);
+      gemm_jobs(tb.ngj[2 * p + 1], njobs, max_rows, max_q, s);
       k_ns_step_end<<<1, 256, 0, s>>>(tb.nst, njobs);
     }
     hipError_t e = hipMemcpyAsync(hst.data(), tb.nst, sizeof(NsState) * njobs, hipMemcpyDeviceToHost, s);
@@ -637,8 +636,7 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
         k_copy<<<grid_for(q * q), 256, 0, s>>>(bs[e].jv[i], bs[e].jv[0], q * q);
       }
     }
-    k_gemm_jobs<<<dim3((unsigned)((svd_r + GT - 1) / GT), (unsigned)((svd_c + GT - 1) / GT), (unsigned)(nm * K)), 256,
-                  0, s>>>(tb.wgj);
+    gemm_jobs(tb.wgj, nm * K, svd_r, svd_c, s);
     SP_TRY(jacobi_block(tb.jobs + nm, nm * K, svd_r, svd_c, tb.jst + nm, status, s, true, split));
   }
   svd_finalize(tb.jobs, tb.ptrs, tb.ptrs + nsvd, tb.ptrs + 2 * nsvd, nsvd, svd_c, s);

@@ -1400,14 +1400,13 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     // passes: 2 + kPowerIters for X, kPowerIters + 2 for Z)
     static_assert(kPowerIters % 2 == 0, "ping-pong parity");
     if (cx != 0 || cz != 0) return ISO_ERR_INTERNAL;
-    k_gemm_jobs<<<dim3((unsigned)((maxR + 63) / 64), (unsigned)((r + 63) / 64), (unsigned)np), 256, 0, s>>>(d_gj[0]);
-    k_gemm_jobs<<<dim3((unsigned)((maxC + 63) / 64), (unsigned)((r + 63) / 64), (unsigned)np), 256, 0, s>>>(d_gj[1]);
+    gemm_jobs(d_gj[0], np, maxR, r, s);
+    gemm_jobs(d_gj[1], np, maxC, r, s);
     k_sigma<<<np, 64, 0, s>>>(d_prob, d_mat, K, r);
     }
     // 3. Procrustes orthogonalisation of U and V: U_perp = U (U^T U)^{-1/2}
-    const unsigned tk = (unsigned)((Kr + 63) / 64);
     for (int side = 0; side < 2; ++side) {
-      k_gemm_jobs<<<dim3(tk, tk, (unsigned)(kSlabs * nm)), 256, 0, s>>>(d_gj[2 + side]);
+      gemm_jobs(d_gj[2 + side], kSlabs * nm, Kr, Kr, s);
       k_sum_gram<<<dim3(grid_for(Kr * Kr), (unsigned)nm), 256, 0, s>>>(d_mat, side);
       k_ns_init<<<nm, 256, 0, s>>>(d_mat, side);
     }
@@ -1417,10 +1416,10 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     for (int it = 0, par = 0; it < kNsIters;) {
       for (int b = 0; b < kNsCheck && it < kNsIters; ++b, ++it, par = 1 - par) {
         k_copy_jobs<<<dim3(grid_for(Kr * Kr), (unsigned)(2 * nm)), 256, 0, s>>>(d_ndst, d_nsrc, Kr * Kr);
-        k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[6 + 3 * par]);
+        gemm_jobs(d_gj[6 + 3 * par], 2 * nm, Kr, Kr, s);
         k_ns_test<<<(unsigned)(2 * nm), 256, 0, s>>>(d_mat);
-        k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[7 + 3 * par]);
-        k_gemm_jobs<<<dim3(tk, tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[8 + 3 * par]);
+        gemm_jobs(d_gj[7 + 3 * par], 2 * nm, Kr, Kr, s);
+        gemm_jobs(d_gj[8 + 3 * par], 2 * nm, Kr, Kr, s);
         k_ns_step_end<<<1, 256, 0, s>>>(d_mat, 2 * nm);
       }
       bool all = true;
@@ -1430,7 +1429,7 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
       if (all) break;
     }
     k_ns_finish<<<dim3((unsigned)nm, 2), 256, 0, s>>>(d_mat, status);
-    k_gemm_jobs<<<dim3((unsigned)((maxM + 63) / 64), tk, (unsigned)(2 * nm)), 256, 0, s>>>(d_gj[5]);
+    gemm_jobs(d_gj[5], 2 * nm, maxM, Kr, s);
     // 4. reconstruction with the update fused
     k_split_mats<<<dim3(grid_for(maxR * rup(Kr, 32)), (unsigned)nm), 256, 0, s>>>(d_mat, 0);
     k_split_mats<<<dim3(grid_for(maxC * rup(Kr, 32)), (unsigned)nm), 256, 0, s>>>(d_mat, 1);
