@@ -29,7 +29,14 @@
  *    the workspace; iso_read_device_status returns ISO_ERR_NONFINITE then (the
  *    outputs of such a call are unspecified).  HIP launch errors are
  *    returned as ISO_ERR_HIP.  Nothing throws across the ABI.
- *  - Results are deterministic and do not depend on launch geometry.
+ *  - Results are deterministic.  Those of the streaming operations
+ *    (TopKMask, sign election, merges, APPLY and FUSED updates) are also
+ *    bit-identical however the tensors are grouped into calls and whichever
+ *    route (single read or two passes) a call takes.  The binary64 dense
+ *    operations (SPECTRAL, TSV, the diagnostics, the optimizer steps) are
+ *    bit-identical across runs of the same call; grouping other matrices into
+ *    the same call can change where an SVD starts (the warm start of the
+ *    experts from the base's factor) and so the last bits of its result.
  *
  * Arithmetic (readings of the paper, which fixes no precision for these
  * operators): every merged coordinate is formed in binary64 -- sums start
@@ -71,6 +78,8 @@ typedef enum iso_status {
   ISO_ERR_INTERNAL = 7     /* a kernel met counts that cannot occur; outputs invalid */
 } iso_status;
 
+/* The enumerations name the values of plain int parameters and fields: the library checks
+ * every such value and answers ISO_ERR_INVALID_ARG to one outside its enumeration. */
 typedef enum iso_dtype { ISO_F32 = 0, ISO_BF16 = 1 } iso_dtype;
 
 /* App. F: Task Arithmetic, TIES-Merging, RAM. */
@@ -139,7 +148,7 @@ typedef struct iso_select_desc {
  * Bytes of workspace the given operation needs for this table (0 on bad
  * arguments).  ISO_OP_BLOCKDIAG also needs the rank: use iso_workspace_size_tsv.
  */
-size_t iso_workspace_size(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt);
+size_t iso_workspace_size(int op, const iso_tensor* t, int n_t, int K, int dt);
 
 /*
  * iso_topk_mask -- TopKMask of every delta of every tensor (App. F, TIES
@@ -149,7 +158,7 @@ size_t iso_workspace_size(int op, const iso_tensor* t, int n_t, int K, iso_dtype
  * uint32 words, bit (p % 32) of word p/32 set iff entry p is kept.  Exact
  * radix selection over the magnitude keys; the result is unique.
  */
-iso_status iso_topk_mask(const iso_tensor* t, int n_t, int K, iso_dtype dt, iso_select_desc* desc,
+iso_status iso_topk_mask(const iso_tensor* t, int n_t, int K, int dt, iso_select_desc* desc,
                          uint32_t* const* mask_bits, void* ws, size_t ws_bytes, void* stream);
 
 /*
@@ -159,7 +168,7 @@ iso_status iso_topk_mask(const iso_tensor* t, int n_t, int K, iso_dtype dt, iso_
  * The sign is that of the exact real sum.  sign_out is a host array of n_t
  * device pointers; tensor j receives N int8 values in {-1, 0, +1}.
  */
-iso_status iso_sign_elect(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_select_desc* desc,
+iso_status iso_sign_elect(const iso_tensor* t, int n_t, int K, int dt, const iso_select_desc* desc,
                           int8_t* const* sign_out, void* ws, size_t ws_bytes, void* stream);
 
 /*
@@ -173,13 +182,13 @@ iso_status iso_sign_elect(const iso_tensor* t, int n_t, int K, iso_dtype dt, con
  * of n_t device pointers to N floats: each is the binary64 u = lambda*t
  * rounded once to binary32.
  */
-iso_status iso_merge(const iso_tensor* t, int n_t, int K, iso_dtype dt, iso_merge_mode mode,
+iso_status iso_merge(const iso_tensor* t, int n_t, int K, int dt, int mode,
                      const iso_select_desc* desc, double lambda, double eps_act, float* const* tau_out, void* ws,
                      size_t ws_bytes, void* stream);
 
 typedef struct iso_update_args {
-  iso_update_mode mode;
-  iso_merge_mode merge;             /* FUSED: which merge                                          */
+  int mode;                         /* an iso_update_mode                                           */
+  int merge;                        /* FUSED: which merge, an iso_merge_mode                      */
   double lambda;                    /* APPLY, FUSED: scale of the merged update (TIES: 1.0)         */
   double eps_act;                   /* FUSED RAM: activity threshold (paper: 1e-5), strict >        */
   const iso_select_desc* desc;      /* FUSED TIES: device descriptors, or NULL to select inside     */
@@ -214,7 +223,7 @@ typedef struct iso_update_args {
  *            only by rows * cols < 2^32 and the workspace: binary64 copies of
  *            about 4K + 7 matrices of the tensor's size per call batch).
  */
-iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_update_args* a, void* ws,
+iso_status iso_update(const iso_tensor* t, int n_t, int K, int dt, const iso_update_args* a, void* ws,
                       size_t ws_bytes, void* stream);
 
 #define ISO_SPECTRAL_MAX_DIM 16384
@@ -238,7 +247,7 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const i
  */
 #define ISO_NOALLOC_SCRATCH_BYTES (64ull << 20)
 
-iso_status iso_update_noalloc(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_update_args* a,
+iso_status iso_update_noalloc(const iso_tensor* t, int n_t, int K, int dt, const iso_update_args* a,
                               void** scratch_out, void* stream);
 
 /*
@@ -251,7 +260,7 @@ iso_status iso_update_noalloc(const iso_tensor* t, int n_t, int K, iso_dtype dt,
  * Workspace: iso_workspace_size(ISO_OP_UPDATE_SPECTRAL, t, n_t, 1, dt); the
  * size limit of ISO-Merger (min(rows, cols) <= ISO_SPECTRAL_MAX_DIM).
  */
-iso_status iso_spectral_diagnostics(const iso_tensor* t, int n_t, iso_dtype dt, double* out, void* ws,
+iso_status iso_spectral_diagnostics(const iso_tensor* t, int n_t, int dt, double* out, void* ws,
                                     size_t ws_bytes, void* stream);
 
 /*
@@ -269,7 +278,7 @@ iso_status iso_spectral_diagnostics(const iso_tensor* t, int n_t, iso_dtype dt, 
  * elements are skipped.  ISO_ERR_INVALID_ARG for self_recon outside {0, 1}.
  * Same workspace and size limits as iso_spectral_diagnostics.
  */
-iso_status iso_spectral_error(const iso_tensor* t, int n_t, iso_dtype dt, int self_recon, double* out, void* ws,
+iso_status iso_spectral_error(const iso_tensor* t, int n_t, int dt, int self_recon, double* out, void* ws,
                               size_t ws_bytes, void* stream);
 
 /*
@@ -278,7 +287,7 @@ iso_status iso_spectral_error(const iso_tensor* t, int n_t, iso_dtype dt, int se
  * (alpha = 0 restores the base spectrum on the trained frames), rounded once.
  * Same workspace and limits as iso_spectral_diagnostics.
  */
-iso_status iso_spectrum_interpolate(const iso_tensor* t, int n_t, iso_dtype dt, double alpha, void* ws,
+iso_status iso_spectrum_interpolate(const iso_tensor* t, int n_t, int dt, double alpha, void* ws,
                                     size_t ws_bytes, void* stream);
 
 /*
@@ -306,7 +315,7 @@ iso_status iso_spectrum_interpolate(const iso_tensor* t, int n_t, iso_dtype dt, 
  */
 #define ISO_MAX_RANK_FRACS 16
 
-iso_status iso_transport_ratios(const iso_tensor* t, int n_t, iso_dtype dt, const double* rank_frac, int n_frac,
+iso_status iso_transport_ratios(const iso_tensor* t, int n_t, int dt, const double* rank_frac, int n_frac,
                                 double* out, void* ws, size_t ws_bytes, void* stream);
 
 /*
@@ -344,7 +353,7 @@ typedef struct iso_adamw {
 } iso_adamw;
 
 size_t iso_workspace_size_optimizer(const iso_frame* f, int n_f);
-iso_status iso_optimizer_step(const iso_frame* f, int n_f, iso_dtype dt, const iso_adamw* opt, void* ws,
+iso_status iso_optimizer_step(const iso_frame* f, int n_f, int dt, const iso_adamw* opt, void* ws,
                               size_t ws_bytes, void* stream);
 
 /*
@@ -367,7 +376,7 @@ typedef struct iso_muon {
   int32_t nesterov;
 } iso_muon;
 
-iso_status iso_optimizer_step_muon(const iso_frame* f, int n_f, iso_dtype dt, const iso_muon* opt, void* ws,
+iso_status iso_optimizer_step_muon(const iso_frame* f, int n_f, int dt, const iso_muon* opt, void* ws,
                                    size_t ws_bytes, void* stream);
 
 /*
@@ -379,10 +388,10 @@ iso_status iso_optimizer_step_muon(const iso_frame* f, int n_f, iso_dtype dt, co
  * K*rank <= min(rows, cols).  If delta_hat is not NULL it is a host array of
  * n_t device pointers receiving U_perp Sigma V_perp^T as N floats.
  */
-iso_status iso_blockdiag_project(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank, double alpha,
+iso_status iso_blockdiag_project(const iso_tensor* t, int n_t, int K, int dt, int rank, double alpha,
                                  float* const* delta_hat, void* ws, size_t ws_bytes, void* stream);
 
-size_t iso_workspace_size_tsv(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank);
+size_t iso_workspace_size_tsv(const iso_tensor* t, int n_t, int K, int dt, int rank);
 
 /* Truncated factors of one delta (App. F, TSV step 1): Delta_i ~ U_i diag(s_i) V_i^T.
  * Device memory, binary64, row-major: u is rows x rank, v is cols x rank, s has rank values. */
@@ -401,7 +410,7 @@ typedef struct iso_factors {
  * The deltas of the table are not read; base and out are.  Same workspace as
  * iso_blockdiag_project (iso_workspace_size_tsv) and the same errors.
  */
-iso_status iso_blockdiag_project_factors(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank, double alpha,
+iso_status iso_blockdiag_project_factors(const iso_tensor* t, int n_t, int K, int dt, int rank, double alpha,
                                          const iso_factors* factors, float* const* delta_hat, void* ws,
                                          size_t ws_bytes, void* stream);
 
@@ -426,7 +435,7 @@ iso_status iso_read_fallback_count(const void* ws, void* stream, int32_t* count)
 iso_status iso_profile_begin(void);
 iso_status iso_profile_end(double* total_ms, int32_t* launches);
 
-const char* iso_status_string(iso_status s);
+const char* iso_status_string(int s);
 
 #ifdef __cplusplus
 }

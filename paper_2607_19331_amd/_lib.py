@@ -3,7 +3,8 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libiso.so")
+# ISO_LIB_PATH selects another build of the same library (the host-sanitized one of build.py)
+LIB_PATH = os.environ.get("ISO_LIB_PATH") or os.path.join(HERE, "libiso.so")
 MAX_K = 8
 
 OK, ERR_INVALID_ARG, ERR_ALIGNMENT, ERR_WORKSPACE, ERR_NONFINITE, ERR_HIP, ERR_UNSUPPORTED, ERR_INTERNAL = range(8)

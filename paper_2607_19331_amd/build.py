@@ -56,5 +56,51 @@ def build(verbose=False, jobs=8):
     return LIB
 
 
+# Host-side sanitizer build of the C ABI layer: iso_abi.cpp (argument checks, workspace
+# planning, table building) instrumented with AddressSanitizer and UndefinedBehaviorSanitizer,
+# linked with the uninstrumented kernel objects of build().  The sanitizer runtime is not linked
+# in: it is preloaded into the host process (asan_runtime() below), which the CPU test of the
+# ABI does.  Device code is never instrumented.
+SANITIZED_LIB = os.path.join(BUILD, "libiso_hostsan.so")
+_CLANG_RT = "/opt/rocm/llvm/lib/clang"
+
+
+def asan_runtime():
+    """Path of the clang AddressSanitizer runtime of the ROCm toolchain, or None."""
+    if not os.path.isdir(_CLANG_RT):
+        return None
+    for ver in sorted(os.listdir(_CLANG_RT), reverse=True):
+        p = os.path.join(_CLANG_RT, ver, "lib", "linux", "libclang_rt.asan-x86_64.so")
+        if os.path.exists(p):
+            return p
+    return None
+
+
+def build_host_sanitized(verbose=False):
+    """Builds SANITIZED_LIB from the objects of build() (which must have run) and a sanitized
+    iso_abi.cpp; returns its path, or None when the toolchain has no ASan runtime."""
+    if asan_runtime() is None:
+        return None
+    obj = os.path.join(BUILD, "iso_abi_hostsan.o")
+    cmd = (["hipcc"] + HIPFLAGS
+           + ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+              "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host", "-fno-omit-frame-pointer", "-g",
+              "-c", os.path.join(CSRC, "iso_abi.cpp"), "-o", obj])
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"compile failed: iso_abi.cpp (sanitized)\n{r.stdout}\n{r.stderr}")
+    objs = [obj] + [os.path.join(BUILD, os.path.splitext(s)[0] + ".o") for s in SOURCES if s != "iso_abi.cpp"]
+    tmp = SANITIZED_LIB + ".tmp"
+    cmd = ["hipcc", "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, SANITIZED_LIB)
+    return SANITIZED_LIB
+
+
 if __name__ == "__main__":
     build(verbose=True)
+    build_host_sanitized(verbose=True)

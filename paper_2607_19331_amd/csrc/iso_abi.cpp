@@ -32,7 +32,7 @@ struct Need {
   bool base = false, deltas = false, out = false, k = false;
 };
 
-iso_status check_table(const iso_tensor* t, int n_t, int K, iso_dtype dt, Need need) {
+iso_status check_table(const iso_tensor* t, int n_t, int K, int dt, Need need) {
   if (n_t < 0 || (n_t > 0 && t == nullptr)) return ISO_ERR_INVALID_ARG;
   if (K < 1 || K > ISO_MAX_K) return ISO_ERR_INVALID_ARG;
   if (dt != ISO_F32 && dt != ISO_BF16) return ISO_ERR_INVALID_ARG;
@@ -110,7 +110,7 @@ GroupMap group_map(const iso_tensor* t, int n_t) {
 
 // Groups are bf16 only, and a group's count cannot exceed its size.  A group may hold more than
 // 2^32 entries (its histogram bins are 64-bit); each member stays within the per-tensor limit.
-iso_status check_groups(const iso_tensor* t, int n_t, iso_dtype dt) {
+iso_status check_groups(const iso_tensor* t, int n_t, int dt) {
   const GroupMap G = group_map(t, n_t);
   if (G.n == 0) return ISO_OK;
   if (dt != ISO_BF16) return ISO_ERR_UNSUPPORTED;
@@ -133,11 +133,11 @@ struct Layout {
 };
 
 // The single-read TIES path serves bf16 calls that select inside iso_update.
-bool fused_eligible(int op, int n_t, iso_dtype dt) {
+bool fused_eligible(int op, int n_t, int dt) {
   return op == ISO_OP_UPDATE_FUSED_SELECT && dt == ISO_BF16 && n_t <= kFusedMaxTensors;
 }
 
-Layout plan(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
+Layout plan(int op, const iso_tensor* t, int n_t, int K, int dt) {
   Layout L;
   size_t off = kStatusBytes;
   L.table = off;
@@ -260,7 +260,7 @@ struct Upload {
 thread_local Upload g_up;   // staging kept alive across calls
 
 // Build [table | hist_item0 | tie_item0 | pointer array] on the host and queue one copy.
-hipError_t upload(const Layout& L, const iso_tensor* t, int n_t, int K, iso_dtype dt, uint8_t* ws,
+hipError_t upload(const Layout& L, const iso_tensor* t, int n_t, int K, int dt, uint8_t* ws,
                   void* const* aux, void* const* aux2, const void* const* ptrs, int n_ptrs, hipStream_t s) {
   g_up.buf.assign(L.upload_end - L.table, 0);
   uint8_t* h = g_up.buf.data();
@@ -371,7 +371,7 @@ SelectPlan select_plan(const Layout& L, uint8_t* ws, int n_t, int K, iso_select_
 
 hipError_t start_call(uint8_t* ws, hipStream_t s) { return fill_u32((uint32_t*)ws, kStatusBytes / 4, 0u, s); }
 
-hipError_t do_select(const Layout& L, uint8_t* ws, int n_t, int K, iso_dtype dt, iso_select_desc* desc,
+hipError_t do_select(const Layout& L, uint8_t* ws, int n_t, int K, int dt, iso_select_desc* desc,
                      hipStream_t s) {
   hipError_t e = fill_u32((uint32_t*)(ws + L.hist), 32768ll * n_t * K, 0u, s);
   if (e != hipSuccess) return e;
@@ -388,7 +388,7 @@ int64_t max_numel(const iso_tensor* t, int n_t) {
 
 extern "C" {
 
-size_t iso_workspace_size(int op, const iso_tensor* t, int n_t, int K, iso_dtype dt) {
+size_t iso_workspace_size(int op, const iso_tensor* t, int n_t, int K, int dt) {
   if (n_t < 0 || (n_t > 0 && !t) || K < 1 || K > ISO_MAX_K) return 0;
   if (op < ISO_OP_TOPK || op > ISO_OP_BLOCKDIAG) return 0;
   for (int j = 0; j < n_t; ++j)
@@ -397,7 +397,7 @@ size_t iso_workspace_size(int op, const iso_tensor* t, int n_t, int K, iso_dtype
   return plan(op, t, n_t, K, dt).total;
 }
 
-iso_status iso_topk_mask(const iso_tensor* t, int n_t, int K, iso_dtype dt, iso_select_desc* desc,
+iso_status iso_topk_mask(const iso_tensor* t, int n_t, int K, int dt, iso_select_desc* desc,
                          uint32_t* const* mask_bits, void* ws, size_t ws_bytes, void* stream) {
   Need nd;
   nd.deltas = true;
@@ -424,7 +424,7 @@ iso_status iso_topk_mask(const iso_tensor* t, int n_t, int K, iso_dtype dt, iso_
   return ISO_OK;
 }
 
-iso_status iso_sign_elect(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_select_desc* desc,
+iso_status iso_sign_elect(const iso_tensor* t, int n_t, int K, int dt, const iso_select_desc* desc,
                           int8_t* const* sign_out, void* ws, size_t ws_bytes, void* stream) {
   Need nd;
   nd.deltas = true;
@@ -453,7 +453,7 @@ iso_status iso_sign_elect(const iso_tensor* t, int n_t, int K, iso_dtype dt, con
   return ISO_OK;
 }
 
-iso_status iso_merge(const iso_tensor* t, int n_t, int K, iso_dtype dt, iso_merge_mode mode,
+iso_status iso_merge(const iso_tensor* t, int n_t, int K, int dt, int mode,
                      const iso_select_desc* desc, double lambda, double eps_act, float* const* tau_out, void* ws,
                      size_t ws_bytes, void* stream) {
   Need nd;
@@ -486,7 +486,7 @@ iso_status iso_merge(const iso_tensor* t, int n_t, int K, iso_dtype dt, iso_merg
   return ISO_OK;
 }
 
-iso_status iso_update(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_update_args* a, void* ws,
+iso_status iso_update(const iso_tensor* t, int n_t, int K, int dt, const iso_update_args* a, void* ws,
                       size_t ws_bytes, void* stream) {
   WsSource src;
   src.ws = ws;
@@ -500,7 +500,7 @@ namespace iso {
 
 // The body of iso_update.  Arguments are validated first; the workspace is then taken from src
 // (the caller's, or the fixed per-device block of iso_update_noalloc) once its size is known.
-iso_status update_call(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_update_args* a,
+iso_status update_call(const iso_tensor* t, int n_t, int K, int dt, const iso_update_args* a,
                        const WsSource& src, void* stream) {
   if (a == nullptr) return ISO_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
@@ -603,7 +603,7 @@ iso_status update_call(const iso_tensor* t, int n_t, int K, iso_dtype dt, const 
     sa.c_min = a->c_min;
     sa.c_max = a->c_max;
     sa.coef_out = a->coef_out;
-    return run_spectral(t, n_t, K, dt, sa, w + L.spectral, (uint32_t*)w, s);
+    return run_spectral(t, n_t, K, (iso_dtype)dt, sa, w + L.spectral, (uint32_t*)w, s);
   }
   return ISO_ERR_INVALID_ARG;
 }
@@ -612,7 +612,7 @@ iso_status update_call(const iso_tensor* t, int n_t, int K, iso_dtype dt, const 
 
 extern "C" {
 
-static iso_status check_tsv(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank, bool ptrs) {
+static iso_status check_tsv(const iso_tensor* t, int n_t, int K, int dt, int rank, bool ptrs) {
   Need nd;
   nd.base = nd.out = nd.deltas = ptrs;
   iso_status st = check_table(t, n_t, K, dt, nd);
@@ -631,12 +631,12 @@ static iso_status check_tsv(const iso_tensor* t, int n_t, int K, iso_dtype dt, i
   return ISO_OK;
 }
 
-size_t iso_workspace_size_tsv(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank) {
+size_t iso_workspace_size_tsv(const iso_tensor* t, int n_t, int K, int dt, int rank) {
   if (check_tsv(t, n_t, K, dt, rank, false) != ISO_OK) return 0;
   return kStatusBytes + tsv_workspace_bytes(t, n_t, K, rank);
 }
 
-iso_status iso_blockdiag_project(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank, double alpha,
+iso_status iso_blockdiag_project(const iso_tensor* t, int n_t, int K, int dt, int rank, double alpha,
                                  float* const* delta_hat, void* ws, size_t ws_bytes, void* stream) {
   iso_status st = check_tsv(t, n_t, K, dt, rank, true);
   if (st != ISO_OK) return st;
@@ -657,7 +657,7 @@ iso_status iso_blockdiag_project(const iso_tensor* t, int n_t, int K, iso_dtype 
   return run_tsv(t, n_t, K, ta, w + kStatusBytes, ws_bytes - kStatusBytes, (uint32_t*)w, s);
 }
 
-iso_status iso_blockdiag_project_factors(const iso_tensor* t, int n_t, int K, iso_dtype dt, int rank, double alpha,
+iso_status iso_blockdiag_project_factors(const iso_tensor* t, int n_t, int K, int dt, int rank, double alpha,
                                          const iso_factors* factors, float* const* delta_hat, void* ws,
                                          size_t ws_bytes, void* stream) {
   iso_status st = check_tsv(t, n_t, K, dt, rank, false);
@@ -686,7 +686,7 @@ iso_status iso_blockdiag_project_factors(const iso_tensor* t, int n_t, int K, is
   return run_tsv(t, n_t, K, ta, w + kStatusBytes, ws_bytes - kStatusBytes, (uint32_t*)w, s);
 }
 
-static iso_status spectrum_op(const iso_tensor* t, int n_t, iso_dtype dt, SpectrumOp op, double* out, double param,
+static iso_status spectrum_op(const iso_tensor* t, int n_t, int dt, SpectrumOp op, double* out, double param,
                               void* ws, size_t ws_bytes, void* stream, const double* fracs = nullptr, int n_frac = 0) {
   const bool write = op == SpectrumOp::kInterpolate;
   Need nd;
@@ -710,7 +710,7 @@ static iso_status spectrum_op(const iso_tensor* t, int n_t, iso_dtype dt, Spectr
   hipStream_t s = (hipStream_t)stream;
   uint8_t* w = (uint8_t*)ws;
   HIP_TRY(start_call(w, s));
-  return run_spectrum_ops(t, n_t, dt, op, out, param, fracs, n_frac, w + L.spectral, (uint32_t*)w, s);
+  return run_spectrum_ops(t, n_t, (iso_dtype)dt, op, out, param, fracs, n_frac, w + L.spectral, (uint32_t*)w, s);
 }
 
 // second_moments: the AdamW state v_u, v_v must be given (Muon does not use them).
@@ -738,7 +738,7 @@ size_t iso_workspace_size_optimizer(const iso_frame* f, int n_f) {
   return kStatusBytes + optimizer_workspace_bytes(f, n_f);
 }
 
-iso_status iso_optimizer_step(const iso_frame* f, int n_f, iso_dtype dt, const iso_adamw* opt, void* ws,
+iso_status iso_optimizer_step(const iso_frame* f, int n_f, int dt, const iso_adamw* opt, void* ws,
                               size_t ws_bytes, void* stream) {
   iso_status st = check_frames(f, n_f);
   if (st != ISO_OK) return st;
@@ -757,10 +757,10 @@ iso_status iso_optimizer_step(const iso_frame* f, int n_f, iso_dtype dt, const i
   hipStream_t s = (hipStream_t)stream;
   uint8_t* w = (uint8_t*)ws;
   HIP_TRY(start_call(w, s));
-  return run_optimizer(f, n_f, dt, opt, nullptr, w + kStatusBytes, (uint32_t*)w, s);
+  return run_optimizer(f, n_f, (iso_dtype)dt, opt, nullptr, w + kStatusBytes, (uint32_t*)w, s);
 }
 
-iso_status iso_optimizer_step_muon(const iso_frame* f, int n_f, iso_dtype dt, const iso_muon* opt, void* ws,
+iso_status iso_optimizer_step_muon(const iso_frame* f, int n_f, int dt, const iso_muon* opt, void* ws,
                                    size_t ws_bytes, void* stream) {
   iso_status st = check_frames(f, n_f, false);
   if (st != ISO_OK) return st;
@@ -778,27 +778,27 @@ iso_status iso_optimizer_step_muon(const iso_frame* f, int n_f, iso_dtype dt, co
   hipStream_t s = (hipStream_t)stream;
   uint8_t* w = (uint8_t*)ws;
   HIP_TRY(start_call(w, s));
-  return run_optimizer(f, n_f, dt, nullptr, opt, w + kStatusBytes, (uint32_t*)w, s);
+  return run_optimizer(f, n_f, (iso_dtype)dt, nullptr, opt, w + kStatusBytes, (uint32_t*)w, s);
 }
 
-iso_status iso_spectral_diagnostics(const iso_tensor* t, int n_t, iso_dtype dt, double* out, void* ws,
+iso_status iso_spectral_diagnostics(const iso_tensor* t, int n_t, int dt, double* out, void* ws,
                                     size_t ws_bytes, void* stream) {
   return spectrum_op(t, n_t, dt, SpectrumOp::kDiagnostics, out, 0.0, ws, ws_bytes, stream);
 }
 
-iso_status iso_spectral_error(const iso_tensor* t, int n_t, iso_dtype dt, int self_recon, double* out, void* ws,
+iso_status iso_spectral_error(const iso_tensor* t, int n_t, int dt, int self_recon, double* out, void* ws,
                               size_t ws_bytes, void* stream) {
   if (self_recon != 0 && self_recon != 1) return ISO_ERR_INVALID_ARG;
   return spectrum_op(t, n_t, dt, self_recon ? SpectrumOp::kSelfSpectralError : SpectrumOp::kSpectralError, out, 0.0,
                      ws, ws_bytes, stream);
 }
 
-iso_status iso_spectrum_interpolate(const iso_tensor* t, int n_t, iso_dtype dt, double alpha, void* ws,
+iso_status iso_spectrum_interpolate(const iso_tensor* t, int n_t, int dt, double alpha, void* ws,
                                     size_t ws_bytes, void* stream) {
   return spectrum_op(t, n_t, dt, SpectrumOp::kInterpolate, nullptr, alpha, ws, ws_bytes, stream);
 }
 
-iso_status iso_transport_ratios(const iso_tensor* t, int n_t, iso_dtype dt, const double* rank_frac, int n_frac,
+iso_status iso_transport_ratios(const iso_tensor* t, int n_t, int dt, const double* rank_frac, int n_frac,
                                 double* out, void* ws, size_t ws_bytes, void* stream) {
   return spectrum_op(t, n_t, dt, SpectrumOp::kTransport, out, 0.0, ws, ws_bytes, stream, rank_frac, n_frac);
 }
@@ -852,7 +852,7 @@ iso_status iso_read_fallback_count(const void* ws, void* stream, int32_t* count)
   return ISO_OK;
 }
 
-const char* iso_status_string(iso_status s) {
+const char* iso_status_string(int s) {
   switch (s) {
     case ISO_OK: return "ok";
     case ISO_ERR_INVALID_ARG: return "invalid argument";

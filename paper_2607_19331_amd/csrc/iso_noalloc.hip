@@ -44,7 +44,7 @@ iso_status acquire_scratch(size_t need, void** ws, size_t* bytes) {
 
 }  // namespace
 
-extern "C" iso_status iso_update_noalloc(const iso_tensor* t, int n_t, int K, iso_dtype dt,
+extern "C" iso_status iso_update_noalloc(const iso_tensor* t, int n_t, int K, int dt,
                                          const iso_update_args* a, void** scratch_out, void* stream) {
   if (scratch_out != nullptr) {
     *scratch_out = nullptr;

@@ -16,7 +16,7 @@ struct WsSource {
   iso_status (*acquire)(size_t need, void** ws, size_t* bytes) = nullptr;
 };
 
-iso_status update_call(const iso_tensor* t, int n_t, int K, iso_dtype dt, const iso_update_args* a,
+iso_status update_call(const iso_tensor* t, int n_t, int K, int dt, const iso_update_args* a,
                        const WsSource& src, void* stream);
 
 }  // namespace iso
