@@ -455,6 +455,9 @@ def main():
     ap.add_argument("--config", default="7b", choices=["tiny", "layer", "1.5b", "7b", "7b-tsv", "layer-optimizer"]
                     + list(SPECTRAL_SETS))
     ap.add_argument("--path", default="single-read", choices=["single-read", "two-pass"])
+    ap.add_argument("--select", default="per-tensor", choices=["per-tensor", "whole-model"],
+                    help="whole-model: one TopKMask over the concatenation of every tensor's delta (all "
+                         "tensors in one select_group; the two-pass path)")
     ap.add_argument("--rule", default="adamw", choices=["adamw", "muon"],
                     help="base rule of the ISO-Optimizer step (--config layer-optimizer)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -473,8 +476,9 @@ def main():
     # the oracle baseline of the stack workloads runs first, in processes spawned before anything
     # in this one touches the GPU
     baseline = None
-    if not args.no_cpu_baseline and args.config in BASELINE_PICKS and not (args.calibrate_copy or
-                                                                            args.calibrate_stream):
+    # (the whole-model selection has no bounded oracle sample: its threshold needs every tensor)
+    if not args.no_cpu_baseline and args.config in BASELINE_PICKS and args.select == "per-tensor" and not (
+            args.calibrate_copy or args.calibrate_stream):
         workers = min(len(os.sched_getaffinity(0)), 16, len(BASELINE_PICKS[args.config][1]))
         baseline = cpu_baseline(args.config, workers)
 
@@ -530,6 +534,11 @@ def main():
         else:
             entries.append(e)
     N = wl.numel
+    whole = args.select == "whole-model"
+    if whole:
+        for e in entries:
+            e.group = 1
+        args.path = "two-pass"
     single = args.path == "single-read"
     if single:
         ws_upd = iso.workspace(iso.OP_UPDATE_FUSED_SELECT, entries, K, iso.BF16, dev)
@@ -582,10 +591,13 @@ def main():
     main_alg = n_elem * (K * 2 + 2 + 2)             # the main kernel's algorithmic bytes per launch
     main_gbps = main_alg / (main_ms * 1e-3) / 1e9
     what = "TopKMask select + elect + disjoint mean + update in one call"
+    if whole:
+        what = ("TopKMask over the whole-model delta (all tensors in one select_group), then elect + disjoint mean "
+                "+ update")
     if tsv_entries:
         what += f"; TSV rank {wl.tsv_rank} on the {len(tsv_entries)} MLP matrices"
     rec = {
-        "metric": METRICS[args.config],
+        "metric": METRICS[args.config] + (", whole-model TopKMask" if whole else ""),
         "value": N / (ms_per_step * 1e-3),
         "unit": "params/s",
         "n_gpus": 1,
@@ -598,8 +610,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"{wl.name}-shaped stack: {len(wl.tensors)} bf16 tensors, {N} params, K={K} deltas "
-                               f"({float(wl.delta.p_zero):.0%} zeros), TIES per-tensor density "
-                               f"{float(wl.density)}, lambda 1: {what}",
+                               f"({float(wl.delta.p_zero):.0%} zeros), TIES density {float(wl.density)} "
+                               f"{'of the whole model' if whole else 'per tensor'}, lambda 1: {what}",
                    "path": args.path},
         "algorithmic_gbps": alg_bytes_step / (ms_per_step * 1e-3) / 1e9,
         "hbm_frac_step": alg_bytes_step / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBPS,
@@ -608,7 +620,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": KERNEL_NAMES[args.path],
                      "achieved": main_gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": main_gbps / PEAK_HBM_GBPS,
-                     "traffic": measured_traffic(f"{args.config}/{args.path}", args.path)},
+                     "traffic": None if whole else measured_traffic(f"{args.config}/{args.path}", args.path)},
     }
     if single:
         rec["fallback_tensors"] = fallbacks

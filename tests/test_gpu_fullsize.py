@@ -124,3 +124,88 @@ def test_full_workload(name, picks, how):
         del base, ds, out
     del entries
     torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+def test_whole_model_group_7b():
+    """TopKMask of the whole-model task vector (App. F, TIES "Trim" with tau_i spanning the model):
+    all 198 tensors of the 7B stack in one select_group, 7.6e9 entries per delta, k the sum of the
+    per-tensor counts at density 0.1.  The joint threshold is checked against a whole-model key
+    histogram counted independently on the device (PyTorch bincount of the 15-bit magnitude keys):
+    a member's n_above is its own count of keys above the joint threshold key T,
+    the tie quota goes to the tied entries in table order, and each member's cutoff keeps exactly
+    its quota of them (a member left with none of the threshold entries describes the same mask
+    by its own smallest key above T, kept whole).  The merged weights of the same selection inside iso_update are then
+    compared with the oracle's merge at a million sampled coordinates of four tensors, given
+    those descriptors."""
+    import time
+
+    import torch
+    wl = synth.workload("7b")
+    K = wl.K
+    entries = _stack(wl)
+    for e in entries:
+        e.group = 1
+    kg = sum(e.k for e in entries)
+    say(f"whole-model group: {len(entries)} tensors, {wl.numel} entries per delta, k = {kg}")
+    ws = iso.workspace(iso.OP_TOPK, entries, K, iso.BF16)
+    desc = iso.desc_tensor(len(entries) * K)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    iso.iso_topk_mask(entries, K, iso.BF16, desc, ws=ws)
+    assert iso.iso_read_device_status(ws) == 0
+    say(f"whole-model group: iso_topk_mask {1e3 * (time.perf_counter() - t0):.1f} ms")
+    del ws
+    g = iso.decode_desc(desc)
+    for i in range(K):
+        hist = torch.zeros(1 << 15, dtype=torch.int64, device="cuda")
+        for e in entries:
+            for piece in e.deltas[i].split(1 << 28):
+                hist += torch.bincount((piece & 0x7FFF).to(torch.int32), minlength=1 << 15)
+        at_or_above = hist.flip(0).cumsum(0).flip(0)
+        T = int(torch.nonzero(at_or_above >= kg).max())
+        quota = kg - (int(at_or_above[T]) - int(hist[T]))
+        say(f"whole-model group: delta {i}: T = {T:#06x}, quota {quota} of {int(hist[T])} tied")
+        left = quota
+        for j, e in enumerate(entries):
+            t_key, key_max, n_above, q, cutoff = g[j * K + i]
+            k16 = e.deltas[i] & 0x7FFF
+            tied = torch.nonzero(k16 == T).flatten()
+            take = min(left, int(tied.numel()))
+            left -= take
+            if t_key == T:
+                # the member keeps its entries above T and the first `take` of its T entries
+                assert n_above == int((k16 > T).sum()), (j, i)
+                assert q == take and int((tied < cutoff).sum()) == take, (j, i)
+            else:
+                # no T entry is left for this member: its own TopKMask of that count then has the
+                # smallest key above T that it holds as threshold, all of whose entries it keeps --
+                # the same mask
+                assert t_key > T and take == 0, (j, i, t_key)
+                assert int(((k16 > T) & (k16 < t_key)).sum()) == 0, (j, i)
+                assert n_above == int((k16 > t_key).sum()), (j, i)
+                assert q == int((k16 == t_key).sum()) and cutoff == e.rows * e.cols, (j, i)
+            del k16, tied
+        assert left == 0
+    say("whole-model group: merge with the selection inside the call")
+    ws = iso.workspace(iso.OP_UPDATE_FUSED_SELECT, entries, K, iso.BF16)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    iso.iso_update(entries, K, iso.BF16, iso.UPDATE_FUSED, merge=iso.MERGE_TIES, lam=1.0, desc=None, ws=ws)
+    assert iso.iso_read_device_status(ws) == 0
+    say(f"whole-model group: iso_update {1e3 * (time.perf_counter() - t0):.1f} ms")
+    del ws
+    rng = np.random.default_rng(11)
+    for t in (1, 4, 6, 196):
+        spec, e = wl.tensors[t], entries[t]
+        want = [tuple(g[t * K + i][j] for j in (0, 2, 3, 4)) for i in range(K)]
+        idx = np.unique(np.concatenate([rng.integers(0, spec.numel, size=1 << 20),
+                                        np.arange(max(0, spec.numel - 4096), spec.numel)]))
+        base = synth.fill_host(wl, t, 0, threads=8)[idx]
+        ds = np.stack([synth.fill_host(wl, t, 1 + i, threads=8)[idx] for i in range(K)])
+        r = ties.merge_at(base, ds, "ties", descs=want, idx=idx, dtype="bf16")
+        out = e.out.cpu().numpy().view(np.uint16)[idx]
+        bad = np.flatnonzero(out != r["out"])
+        assert bad.size == 0, (spec.name, idx[bad[:8]])
+    del entries
+    torch.cuda.empty_cache()
