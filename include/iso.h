@@ -88,7 +88,8 @@ typedef enum iso_merge_mode { ISO_MERGE_TA = 0, ISO_MERGE_TIES = 1, ISO_MERGE_RA
 typedef enum iso_update_mode {
   ISO_UPDATE_APPLY = 0,    /* out = W_0 + lambda * tau_in                                   */
   ISO_UPDATE_FUSED = 1,    /* out = W_0 + merged update, elect + merge + apply in one pass  */
-  ISO_UPDATE_SPECTRAL = 2  /* out = W_* of ISO-Merger (Algorithm 1)                          */
+  ISO_UPDATE_SPECTRAL = 2, /* out = W_* of ISO-Merger (Algorithm 1)                          */
+  ISO_UPDATE_ORTHO = 3     /* out = W_OM of OrthoMerge-G-TIES (App. F)                       */
 } iso_update_mode;
 
 /* Operation codes for iso_workspace_size. */
@@ -100,7 +101,8 @@ typedef enum iso_op {
   ISO_OP_UPDATE_FUSED = 4,     /* FUSED with caller descriptors, or TA / RAM                    */
   ISO_OP_UPDATE_FUSED_SELECT = 5, /* FUSED TIES that selects inside the call (desc == NULL)     */
   ISO_OP_UPDATE_SPECTRAL = 6,
-  ISO_OP_BLOCKDIAG = 7
+  ISO_OP_BLOCKDIAG = 7,
+  ISO_OP_UPDATE_ORTHO = 8
 } iso_op;
 
 /* One weight tensor of the table.  Which pointers are read depends on the call. */
@@ -222,6 +224,19 @@ typedef struct iso_update_args {
  *            min(rows, cols) <= ISO_SPECTRAL_MAX_DIM (the long side is bounded
  *            only by rows * cols < 2^32 and the workspace: binary64 copies of
  *            about 4K + 7 matrices of the tensor's size per call batch).
+ *  ORTHO:    OrthoMerge-G-TIES, App. F, per matrix, the geometry-aware
+ *            baseline: one-sided Procrustes rotations R_i of the input space
+ *            (W_0 R ~ W_i), inverse Cayley maps, magnitude-corrected mean of the
+ *            skew matrices, forward Cayley map, W_rot = W_0 R; the residuals
+ *            W_i - W_0 R_i (binary32) merged by TIES with the tensor's k as the
+ *            TopKMask count (the paper's baseline keeps 20%) and lambda;
+ *            out = W_rot + u, u the merged residual update in binary32, rounded
+ *            once.  Rotations in binary64 (Jacobi SVDs; the Cayley maps through
+ *            symmetric positive definite inverses).  Needs rows >= cols (the
+ *            Procrustes rotation of a wide W_0 is not unique) and cols <=
+ *            ISO_SPECTRAL_MAX_DIM, else ISO_ERR_UNSUPPORTED; a singular
+ *            W_0^T W_i or a rotation with the eigenvalue -1 sets the device
+ *            status (ISO_ERR_INTERNAL).  Workspace: ISO_OP_UPDATE_ORTHO.
  */
 iso_status iso_update(const iso_tensor* t, int n_t, int K, int dt, const iso_update_args* a, void* ws,
                       size_t ws_bytes, void* stream);

@@ -10,8 +10,8 @@ from typing import List, Optional, Sequence
 
 from . import _lib
 from ._lib import (BF16, F32, MERGE_RAM, MERGE_TA, MERGE_TIES, OP_BLOCKDIAG, OP_MERGE, OP_SIGN, OP_TOPK,
-                   OP_UPDATE_APPLY, OP_UPDATE_FUSED, OP_UPDATE_FUSED_SELECT, OP_UPDATE_SPECTRAL, UPDATE_APPLY,
-                   UPDATE_FUSED, UPDATE_SPECTRAL, IsoSelectDesc)
+                   OP_UPDATE_APPLY, OP_UPDATE_FUSED, OP_UPDATE_FUSED_SELECT, OP_UPDATE_ORTHO, OP_UPDATE_SPECTRAL,
+                   UPDATE_APPLY, UPDATE_FUSED, UPDATE_ORTHO, UPDATE_SPECTRAL, IsoSelectDesc)
 
 DESC_BYTES = ctypes.sizeof(IsoSelectDesc)
 

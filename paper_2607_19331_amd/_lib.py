@@ -10,9 +10,9 @@ MAX_K = 8
 OK, ERR_INVALID_ARG, ERR_ALIGNMENT, ERR_WORKSPACE, ERR_NONFINITE, ERR_HIP, ERR_UNSUPPORTED, ERR_INTERNAL = range(8)
 F32, BF16 = 0, 1
 MERGE_TA, MERGE_TIES, MERGE_RAM = 0, 1, 2
-UPDATE_APPLY, UPDATE_FUSED, UPDATE_SPECTRAL = 0, 1, 2
+UPDATE_APPLY, UPDATE_FUSED, UPDATE_SPECTRAL, UPDATE_ORTHO = 0, 1, 2, 3
 (OP_TOPK, OP_SIGN, OP_MERGE, OP_UPDATE_APPLY, OP_UPDATE_FUSED, OP_UPDATE_FUSED_SELECT, OP_UPDATE_SPECTRAL,
- OP_BLOCKDIAG) = range(8)
+ OP_BLOCKDIAG, OP_UPDATE_ORTHO) = range(9)
 
 SYMBOLS = ["iso_workspace_size", "iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update",
            "iso_blockdiag_project", "iso_blockdiag_project_factors", "iso_workspace_size_tsv", "iso_k_from_density", "iso_read_device_status",

@@ -10,7 +10,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libiso.so")
 
 SOURCES = ["iso_abi.cpp", "iso_select.hip", "iso_merge.hip", "iso_fused.hip", "iso_spectral.hip", "iso_tsv.hip",
-           "iso_noalloc.hip"]
+           "iso_noalloc.hip", "iso_ortho.hip"]
 
 HIPFLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -12,6 +12,7 @@
 #include "iso_device.h"
 #include "iso_fused.h"
 #include "iso_kernels.h"
+#include "iso_ortho.h"
 #include "iso_spectral.h"
 #include "iso_tsv.h"
 #include "iso_update_call.h"
@@ -226,6 +227,10 @@ Layout plan(int op, const iso_tensor* t, int n_t, int K, int dt) {
     L.spectral = off;
     off = align_up(off + spectral_workspace_bytes(t, n_t, K), 256);
   }
+  if (op == ISO_OP_UPDATE_ORTHO) {
+    L.spectral = off;
+    off = align_up(off + ortho_workspace_bytes(t, n_t, K), 256);
+  }
   L.total = off;
   return L;
 }
@@ -390,7 +395,7 @@ extern "C" {
 
 size_t iso_workspace_size(int op, const iso_tensor* t, int n_t, int K, int dt) {
   if (n_t < 0 || (n_t > 0 && !t) || K < 1 || K > ISO_MAX_K) return 0;
-  if (op < ISO_OP_TOPK || op > ISO_OP_BLOCKDIAG) return 0;
+  if (op < ISO_OP_TOPK || op > ISO_OP_UPDATE_ORTHO) return 0;
   for (int j = 0; j < n_t; ++j)
     if (t[j].rows < 0 || t[j].cols < 0) return 0;
   if (op == ISO_OP_BLOCKDIAG) return 0;
@@ -604,6 +609,22 @@ iso_status update_call(const iso_tensor* t, int n_t, int K, int dt, const iso_up
     sa.c_max = a->c_max;
     sa.coef_out = a->coef_out;
     return run_spectral(t, n_t, K, (iso_dtype)dt, sa, w + L.spectral, (uint32_t*)w, s);
+  }
+  if (a->mode == ISO_UPDATE_ORTHO) {
+    Need nd;
+    nd.base = nd.out = nd.deltas = nd.k = true;
+    if ((st = check_table(t, n_t, K, dt, nd)) != ISO_OK) return st;
+    if (!(a->lambda - a->lambda == 0.0)) return ISO_ERR_INVALID_ARG;
+    for (int j = 0; j < n_t; ++j) {
+      if (t[j].select_group != 0) return ISO_ERR_UNSUPPORTED;
+      if (t[j].rows * t[j].cols == 0) continue;
+      if (t[j].rows < t[j].cols || t[j].cols > ISO_SPECTRAL_MAX_DIM) return ISO_ERR_UNSUPPORTED;
+    }
+    if (n_t == 0) return ISO_OK;
+    Layout L = plan(ISO_OP_UPDATE_ORTHO, t, n_t, K, dt);
+    if ((st = take_ws(src, L, &w)) != ISO_OK) return st;
+    HIP_TRY(start_call(w, s));
+    return run_ortho(t, n_t, K, (iso_dtype)dt, a->lambda, w + L.spectral, (uint32_t*)w, s);
   }
   return ISO_ERR_INVALID_ARG;
 }

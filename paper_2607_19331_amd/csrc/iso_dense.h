@@ -486,9 +486,22 @@ __global__ void __launch_bounds__(256) k_bjg_part(const JacobiJob* __restrict__ 
   if (!P.ok || row0 >= r) return;
   if (threadIdx.x < kGN) gc[threadIdx.x] = (threadIdx.x < P.n0) ? P.c0 + threadIdx.x : P.c1 + (threadIdx.x - P.n0);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
-  jac_f64x4_t acc[4];
+  // the Gram is symmetric: only its 10 tiles on and above the diagonal are formed, three per wave
+  // for waves 0 and 1 and two for waves 2 and 3 (tile (R, C) as the nibble 4R + C of a packed list)
+  constexpr unsigned kTiles[4] = {0x0 | (0x1 << 4) | (0x2 << 8), 0x3 | (0x5 << 4) | (0x6 << 8),
+                                  0x7 | (0xA << 4), 0xB | (0xF << 4)};
+  const unsigned tl = kTiles[w];
+  const int nt = (w < 2) ? 3 : 2;
+  int tr[3], tc[3];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) acc[t] = jac_f64x4_t{0.0, 0.0, 0.0, 0.0};
+  for (int j = 0; j < 3; ++j) {
+    const unsigned e = (tl >> (4 * j)) & 0xFu;
+    tr[j] = (int)(e >> 2);
+    tc[j] = (int)(e & 3u);
+  }
+  jac_f64x4_t acc[3];
+#pragma unroll
+  for (int j = 0; j < 3; ++j) acc[j] = jac_f64x4_t{0.0, 0.0, 0.0, 0.0};
   __syncthreads();
   double pf[kGChunkPer];
   gram_load(pf, J.a, r, row1, gc, P.nc, row0);
@@ -498,18 +511,30 @@ __global__ void __launch_bounds__(256) k_bjg_part(const JacobiJob* __restrict__ 
     if (k0 + kGN < row1) gram_load(pf, J.a, r, row1, gc, P.nc, k0 + kGN);
 #pragma unroll 4
     for (int s = 0; s < kGN / 4; ++s) {
-      const double a = ch[(16 * w + ln) * kGP + 4 * s + g];
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
-        acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, ch[(16 * t + ln) * kGP + 4 * s + g], acc[t], 0, 0, 0);
+      for (int j = 0; j < 3; ++j) {
+        if (j < nt) {
+          const double a = ch[(16 * tr[j] + ln) * kGP + 4 * s + g];     // X^T[16R + ln][k]
+          const double b = ch[(16 * tc[j] + ln) * kGP + 4 * s + g];     // X[k][16C + ln]
+          acc[j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc[j], 0, 0, 0);
+        }
+      }
     }
     __syncthreads();
   }
+  // G[i][j] at j * kGN + i; a tile above the diagonal also fills its mirror below it
   double* out = S.part + (((size_t)job * S.npairs + pr) * S.nslices + z) * (kGN * kGN);
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
+  for (int j = 0; j < 3; ++j) {
+    if (j < nt) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) out[(16 * t + ln) * kGN + 16 * w + g + 4 * v] = acc[t][v];
+      for (int v = 0; v < 4; ++v) {
+        const int gi = 16 * tr[j] + g + 4 * v, gj = 16 * tc[j] + ln;
+        out[gj * kGN + gi] = acc[j][v];
+        if (tr[j] != tc[j]) out[gi * kGN + gj] = acc[j][v];
+      }
+    }
+  }
 }
 
 // 512 threads: 32 sixteen-lane rows, one per column pair of the 64 x 64 inner sweep

@@ -271,3 +271,30 @@ def test_calibration_library_exports_its_declaration():
     assert f(ptrs, 9, FAKE, 16, 1, None) == 1
     assert f(ptrs, 5, None, 16, 1, None) == 1
     assert f(ptrs, 5, FAKE, 0, 1, None) == 1
+
+
+def test_orthomerge_validation():
+    """iso_update ORTHO refuses, before anything is queued, wide matrices (the Procrustes rotation
+    of a wide W_0 is not unique), a non-finite lambda, joint-selection groups, k above the tensor
+    size and a workspace below iso_workspace_size(ISO_OP_UPDATE_ORTHO)."""
+    import math
+    L = _lib.load()
+    a = _lib.IsoUpdateArgs()
+    a.mode, a.merge, a.lambda_, a.eps_act = 3, 1, 1.0, 0.0
+
+    def call(es, ws_bytes=1 << 40):
+        return L.iso_update(iso._table(es), len(es), 2, iso.BF16, ctypes.byref(a), FAKE * 16, ws_bytes, None)
+
+    assert call([entry(rows=8, cols=16, k=10)]) == _lib.ERR_UNSUPPORTED
+    assert call([entry(rows=16385, cols=16385, k=10)]) == _lib.ERR_UNSUPPORTED
+    g = entry(rows=16, cols=8, k=10)
+    g.group = 1
+    assert call([g]) == _lib.ERR_UNSUPPORTED
+    assert call([entry(rows=16, cols=8, k=129)]) == _lib.ERR_INVALID_ARG
+    assert call([entry(rows=16, cols=8, k=10)], ws_bytes=100) == _lib.ERR_WORKSPACE
+    a.lambda_ = math.inf
+    assert call([entry(rows=16, cols=8, k=10)]) == _lib.ERR_INVALID_ARG
+    a.lambda_ = 1.0
+    assert call([]) == _lib.OK
+    es = [entry(rows=300, cols=128, k=10)]
+    assert L.iso_workspace_size(iso.OP_UPDATE_ORTHO, iso._table(es), 1, 2, iso.BF16) > 0
