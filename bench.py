@@ -315,6 +315,105 @@ def bench_layer_spectral(args, iso, synth, torch):
     return rec
 
 
+ORTHO_SETS = {
+    # config: (workload, tensor indices, description); OrthoMerge needs rows >= cols
+    "layer-ortho": ("layer", [0, 1, 2, 3, 6], "single bf16 layer, its tall and square matrices (q/k/v/o "
+                                               "2048x2048, down 5632x2048)"),
+    "7b-layer-ortho": ("7b", [0, 3, 4, 5], "one 7B layer, its tall and square matrices (q/o 3584x3584, "
+                                            "gate/up 18944x3584)"),
+}
+
+
+def ortho_flops(m, n, K):
+    """Work OrthoMerge-G-TIES prescribes per matrix: Golub & Van Loan's SVD count for each of the K
+    Procrustes SVDs of W_0^T W_i, 2 m n^2 for each product with W_0 (W_0^T W_i, W_0 R_i, W_0 R),
+    and 8/3 n^3 for each of the K + 1 Cayley solves with n right-hand sides (LU, then two
+    triangular solves)."""
+    return K * svd_flops(n, n) + (2 * K + 1) * 2 * m * n * n + (K + 1) * 8 * n ** 3 // 3
+
+
+def bench_ortho(args, iso, synth, torch):
+    """OrthoMerge-G-TIES (App. F; iso_update ORTHO) over a set of bf16 matrices with the workload's
+    K deltas in one call per step, residual TopKMask density 0.2 (the paper's setting), lambda 1;
+    timed with HIP events.  Roofline: binary64, the algorithmic flops of ortho_flops."""
+    from oracle import numerics as nm
+    from oracle import orthomerge as om
+    wl_name, picks, what = ORTHO_SETS[args.config]
+    wl = synth.workload(wl_name)
+    K = wl.K
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream().cuda_stream
+    entries, flops, N = [], 0, 0
+    for t in picks:
+        spec = wl.tensors[t]
+        n = spec.numel
+        N += n
+        base = torch.empty(n, dtype=torch.int16, device=dev)
+        synth.fill_device(base.data_ptr(), n, wl, t, 0, stream)
+        ds = []
+        for i in range(K):
+            d = torch.empty(n, dtype=torch.int16, device=dev)
+            synth.fill_device(d.data_ptr(), n, wl, t, 1 + i, stream)
+            ds.append(d)
+        out = torch.empty(n, dtype=torch.int16, device=dev)
+        k = iso.iso_k_from_density(n, 1, 5)
+        entries.append(iso.Entry(spec.rows, spec.cols, base=base, deltas=ds, out=out, k=k))
+        flops += ortho_flops(spec.rows, spec.cols, K)
+    ws = iso.workspace(iso.OP_UPDATE_ORTHO, entries, K, iso.BF16, dev)
+
+    def step():
+        iso.iso_update(entries, K, iso.BF16, iso.UPDATE_ORTHO, lam=1.0, ws=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if iso.iso_read_device_status(ws) != 0:
+        raise RuntimeError("device status reports an error")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s_ in range(args.steps):
+        ev[s_][0].record()
+        step()
+        ev[s_][1].record()
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    call_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
+    rec = {
+        "metric": f"OrthoMerge-G-TIES params/sec and FP64 TFLOP/s (% of peak), {what.split(',')[0]} K={K}",
+        "value": N / (ms_per_step * 1e-3),
+        "unit": "params/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": f"{what}: {len(picks)} matrices, {N} params, K={K} deltas "
+                               f"({float(wl.delta.p_zero):.0%} zeros), residual TopKMask density 0.2, lambda 1: "
+                               f"OrthoMerge-G-TIES in one call"},
+        "call_ms": call_ms,
+        "roofline": {"bound": "fp64", "kernel": "iso_update ORTHO (Jacobi SVDs, dense binary64 steps, TIES)",
+                     "achieved": flops / (call_ms * 1e-3) / 1e12, "peak": 78.6, "unit": "TFLOP/s",
+                     "frac": flops / (call_ms * 1e-3) / 1e12 / 78.6, "traffic": None, "flops_per_call": flops},
+    }
+    if not args.no_cpu_baseline:
+        t = picks[0]
+        spec = wl.tensors[t]
+        rows, cols = min(spec.rows, 2048), min(spec.cols, 2048)
+        w0 = synth.fill_host(wl, t, 0).reshape(spec.rows, spec.cols)[:rows, :cols]
+        dh = [synth.fill_host(wl, t, 1 + i).reshape(spec.rows, spec.cols)[:rows, :cols] for i in range(K)]
+        t1 = time.perf_counter()
+        om.orthomerge_ties(w0, dh, nm.k_from_density(rows * cols, 0.2), dtype="bf16")
+        dt = time.perf_counter() - t1
+        try:
+            from threadpoolctl import threadpool_info
+            cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        except ImportError:
+            cores = len(os.sched_getaffinity(0))
+        part = "" if (rows, cols) == (spec.rows, spec.cols) else f", its leading {rows}x{cols} block as one matrix"
+        rec["cpu_baseline"] = {"value": rows * cols / dt, "unit": "params/s", "cores": cores, "kind": "oracle",
+                               "sample": f"OrthoMerge-G-TIES (LAPACK SVD, numpy) on {spec.name} "
+                                         f"({spec.rows}x{spec.cols}{part}), one run, {dt:.1f} s"}
+    return rec
+
+
 def bench_layer_optimizer(args, iso, synth, torch):
     """One ISO-AdamW step (iso_optimizer_step) or, with --rule muon, one ISO-Muon step
     (iso_optimizer_step_muon) over the single layer's seven matrices (q/k/v/o 2048x2048, gate/up
@@ -453,7 +552,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="7b", choices=["tiny", "layer", "1.5b", "7b", "7b-tsv", "layer-optimizer"]
-                    + list(SPECTRAL_SETS))
+                    + list(SPECTRAL_SETS) + list(ORTHO_SETS))
     ap.add_argument("--path", default="single-read", choices=["single-read", "two-pass"])
     ap.add_argument("--select", default="per-tensor", choices=["per-tensor", "whole-model"],
                     help="whole-model: one TopKMask over the concatenation of every tensor's delta (all "
@@ -504,6 +603,9 @@ def main():
 
     if args.config == "tiny":
         print(json.dumps(bench_tiny(args, iso, synth, torch)), flush=True)
+        return
+    if args.config in ORTHO_SETS:
+        print(json.dumps(bench_ortho(args, iso, synth, torch)), flush=True)
         return
     if args.config in SPECTRAL_SETS:
         print(json.dumps(bench_layer_spectral(args, iso, synth, torch)), flush=True)

@@ -94,3 +94,36 @@ def test_rotated_experts(K):
         outs, st = _run([u], K, u.dtype, lam=0.5)
         assert st == 0
         _check(u, outs[0], K, u.dtype, 0.5)
+
+
+@pytest.mark.timeout(600)
+def test_single_layer_shapes():
+    """down_proj (5632 x 2048) of the single-layer workload with its K = 2 seeded bf16 deltas (50%
+    zeros), residual density 0.2, and a square 1024 x 1024 base of condition number 3, in one call.
+    (The workload's square Gaussian bases have condition numbers near 2n, so W_0^T W_i has
+    singular values ~1e-7 of its largest, far below the deltas' scale: the Procrustes rotation is
+    then ill-determined in those directions on any implementation, and the Cayley maps amplify
+    that; parity is taken where the rotation is determined.)"""
+    import synth
+    wl = synth.workload("layer")
+    spec = wl.tensors[6]
+    base = synth.fill_host(wl, 6, 0)
+    ds = [synth.fill_host(wl, 6, 1 + i) for i in range(wl.K)]
+    units = [Unit(spec.rows, spec.cols, base, ds, "bf16", nm.k_from_density(spec.numel, 0.2))]
+    rng = np.random.default_rng(61)
+    n = 1024
+    q1, _ = np.linalg.qr(rng.standard_normal((n, n)))
+    q2, _ = np.linalg.qr(rng.standard_normal((n, n)))
+    w0 = (q1 * np.linspace(0.03, 0.01, n)) @ q2.T
+    dsq = []
+    for _ in range(wl.K):
+        d = rng.standard_normal((n, n)) * 1e-4
+        d[rng.random((n, n)) < 0.5] = 0.0
+        dsq.append(nm.from_f64(d.ravel(), "bf16"))
+    units.append(Unit(n, n, nm.from_f64(w0.ravel(), "bf16"), dsq, "bf16", nm.k_from_density(n * n, 0.2)))
+    say("orthomerge single-layer down_proj and a conditioned 1024 x 1024, K=2")
+    outs, st = _run(units, wl.K, "bf16")
+    assert st == 0
+    for u, o in zip(units, outs):
+        say(f"orthomerge {u.rows}x{u.cols}: oracle")
+        _check(u, o, wl.K, "bf16", 1.0)
