@@ -1,4 +1,5 @@
 """Helpers for the GPU parity tests: upload storage arrays, run the C ABI, fetch results."""
+import os
 import sys
 
 import numpy as np
@@ -6,9 +7,21 @@ import numpy as np
 import paper_2607_19331_amd as iso
 
 
+_PROGRESS = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "gpurun_out",
+                         "gpu_case_progress.log")
+
+
 def say(msg):
+    """Progress line: printed (seen with -s) and appended to gpurun_out/gpu_case_progress.log, so that
+    a long case shows progress even when pytest captures its output."""
     print(f"[gpu-case] {msg}", flush=True)
     sys.stdout.flush()
+    try:
+        os.makedirs(os.path.dirname(_PROGRESS), exist_ok=True)
+        with open(_PROGRESS, "a") as f:
+            f.write(f"[gpu-case] {msg}\n")
+    except OSError:
+        pass
 
 
 def dt_code(dtype):

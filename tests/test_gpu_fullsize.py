@@ -168,6 +168,8 @@ def test_whole_model_group_7b():
         say(f"whole-model group: delta {i}: T = {T:#06x}, quota {quota} of {int(hist[T])} tied")
         left = quota
         for j, e in enumerate(entries):
+            if j % 50 == 0:
+                say(f"whole-model group: delta {i}: member {j}")
             t_key, key_max, n_above, q, cutoff = g[j * K + i]
             k16 = e.deltas[i] & 0x7FFF
             tied = torch.nonzero(k16 == T).flatten()
@@ -198,6 +200,7 @@ def test_whole_model_group_7b():
     rng = np.random.default_rng(11)
     for t in (1, 4, 6, 196):
         spec, e = wl.tensors[t], entries[t]
+        say(f"whole-model group: oracle merge at sampled coordinates of {spec.name}")
         want = [tuple(g[t * K + i][j] for j in (0, 2, 3, 4)) for i in range(K)]
         idx = np.unique(np.concatenate([rng.integers(0, spec.numel, size=1 << 20),
                                         np.arange(max(0, spec.numel - 4096), spec.numel)]))
