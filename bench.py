@@ -554,6 +554,9 @@ def main():
     ap.add_argument("--config", default="7b", choices=["tiny", "layer", "1.5b", "7b", "7b-tsv", "layer-optimizer"]
                     + list(SPECTRAL_SETS) + list(ORTHO_SETS))
     ap.add_argument("--path", default="single-read", choices=["single-read", "two-pass"])
+    ap.add_argument("--lam", type=float, default=1.0,
+                    help="lambda of the stack configs' TIES update (the paper's TIES: 1; other values take the "
+                         "general binary64 rounding path of the fused pass)")
     ap.add_argument("--select", default="per-tensor", choices=["per-tensor", "whole-model"],
                     help="whole-model: one TopKMask over the concatenation of every tensor's delta (all "
                          "tensors in one select_group; the two-pass path)")
@@ -657,7 +660,8 @@ def main():
             ev[0].record()
         if not single:
             iso.iso_topk_mask(entries, K, iso.BF16, desc, ws=ws_sel)
-        iso.iso_update(entries, K, iso.BF16, iso.UPDATE_FUSED, merge=iso.MERGE_TIES, lam=1.0, desc=desc, ws=ws_upd)
+        iso.iso_update(entries, K, iso.BF16, iso.UPDATE_FUSED, merge=iso.MERGE_TIES, lam=args.lam, desc=desc,
+                       ws=ws_upd)
         if ev:
             ev[1].record()
         if tsv_entries:
@@ -699,7 +703,8 @@ def main():
     if tsv_entries:
         what += f"; TSV rank {wl.tsv_rank} on the {len(tsv_entries)} MLP matrices"
     rec = {
-        "metric": METRICS[args.config] + (", whole-model TopKMask" if whole else ""),
+        "metric": METRICS[args.config] + (", whole-model TopKMask" if whole else "")
+        + ("" if args.lam == 1.0 else f", lambda {args.lam:g}"),
         "value": N / (ms_per_step * 1e-3),
         "unit": "params/s",
         "n_gpus": 1,
@@ -713,7 +718,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{wl.name}-shaped stack: {len(wl.tensors)} bf16 tensors, {N} params, K={K} deltas "
                                f"({float(wl.delta.p_zero):.0%} zeros), TIES density {float(wl.density)} "
-                               f"{'of the whole model' if whole else 'per tensor'}, lambda 1: {what}",
+                               f"{'of the whole model' if whole else 'per tensor'}, lambda {args.lam:g}: {what}",
                    "path": args.path},
         "algorithmic_gbps": alg_bytes_step / (ms_per_step * 1e-3) / 1e9,
         "hbm_frac_step": alg_bytes_step / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBPS,

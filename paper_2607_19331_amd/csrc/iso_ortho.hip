@@ -1,8 +1,8 @@
-// OrthoMerge-G-TIES (App. F) for 2-D weight matrices with rows >= cols, one matrix at a time, in
-// binary64 on the device:
+// OrthoMerge-G-TIES (App. F) for 2-D weight matrices with rows >= cols, in binary64 on the
+// device, the matrices of a call in batches whose SVDs of each phase run as one Jacobi job set:
 //   1. W_0 and W_i = W_0 + tau_i as column-major binary64; M_i = W_0^T W_i (n x n);
 //   2. the one-sided Procrustes rotation R_i = U V^T from the block-Jacobi SVD M_i = U S V^T
-//      (all K as one job set; a zero singular value makes R_i non-unique and is flagged);
+//      (a zero singular value makes R_i non-unique and is flagged);
 //   3. the inverse Cayley map A_i = (R_i + I)^{-1} (R_i - I).  For orthogonal R both factors are
 //      functions of R and commute, and (R + I)^T (R + I) = 2I + R + R^T, so
 //      A_i = (2I + R_i + R_i^T)^{-1} (R_i - R_i^T): the inverse of a symmetric positive definite
@@ -156,9 +156,6 @@ struct OmBump {
 
 // Device blocks of one matrix (the same take() sequence sizes the workspace).
 struct OmBufs {
-  JacobiJob* jobs;
-  JacobiState* jst;
-  double** ptrs;                       // finalize: left[K], right[K], sv[K]
   iso_select_desc* desc;               // K descriptors of the residual TopKMask
   double *w0, *wrot;                   // m x n col-major
   double* wi[ISO_MAX_K];               // W_i, then delta_i (m x n col-major)
@@ -168,7 +165,6 @@ struct OmBufs {
   double *part, *norm, *coef;
   float* delta[ISO_MAX_K];             // m x n row-major binary32
   float* u;                            // m x n row-major binary32
-  void* split;
   uint8_t* sub;                        // workspace of the residual TIES calls
   size_t sub_bytes;
 };
@@ -185,9 +181,6 @@ size_t ties_sub_bytes(int64_t m, int64_t n, int K, int64_t k) {
 
 OmBufs om_carve(OmBump& bp, int64_t m, int64_t n, int K, int64_t k) {
   OmBufs b{};
-  b.jobs = bp.take<JacobiJob>(K);
-  b.jst = bp.take<JacobiState>(K);
-  b.ptrs = bp.take<double*>(3 * K);
   b.desc = bp.take<iso_select_desc>(K);
   b.w0 = bp.take(m * n);
   b.wrot = bp.take(m * n);
@@ -211,7 +204,6 @@ OmBufs om_carve(OmBump& bp, int64_t m, int64_t n, int K, int64_t k) {
   b.norm = bp.take(K + 1);
   b.coef = bp.take(1);
   b.u = bp.take<float>(m * n);
-  b.split = bp.take<uint8_t>((int64_t)gram_split_bytes(K, n, n));
   b.sub_bytes = ties_sub_bytes(m, n, K, k);
   b.sub = bp.take<uint8_t>((int64_t)b.sub_bytes);
   return b;
@@ -233,16 +225,71 @@ void gemm_ab(int64_t n, const double* A, const double* B, double* C, hipStream_t
   gemm(n, n, n, 1.0, A, 1, n, B, 1, n, 0.0, C, 1, n, s);
 }
 
+// Job tables of a batch of nm matrices: the nm K jobs of the Procrustes and inverse-Cayley job
+// sets (job e K + i: matrix e, expert i, on its ja[i]) and the nm jobs of the forward-Cayley set
+// (job e: matrix e's ja[0]), each with its states and finalize pointers; the split-step scratch.
+struct OmTables {
+  JacobiJob *jobs, *jobs1;
+  JacobiState *jst, *jst1;
+  double **ptrs, **ptrs1;               // left[], right[], sv[] of each set
+  void* split;
+};
+
+OmTables om_tables(OmBump& bp, int nm, int K, int64_t max_n) {
+  OmTables tb{};
+  tb.jobs = bp.take<JacobiJob>((int64_t)nm * K);
+  tb.jst = bp.take<JacobiState>((int64_t)nm * K);
+  tb.ptrs = bp.take<double*>(3 * (int64_t)nm * K);
+  tb.jobs1 = bp.take<JacobiJob>(nm);
+  tb.jst1 = bp.take<JacobiState>(nm);
+  tb.ptrs1 = bp.take<double*>(3 * (int64_t)nm);
+  tb.split = bp.take<uint8_t>((int64_t)gram_split_bytes(nm * K, max_n, max_n));
+  return tb;
+}
+
+constexpr size_t kOrthoBatchBytes = 48ull << 30;   // device blocks of the matrices of one batch
+constexpr int kOrthoBatch = 16;
+
+size_t om_matrix_bytes(const iso_tensor& x, int K) {
+  OmBump bp{nullptr};
+  om_carve(bp, x.rows, x.cols, K, x.k);
+  return bp.off;
+}
+
+// Consecutive non-empty matrices of the table, at most kOrthoBatch and kOrthoBatchBytes a batch.
+std::vector<std::vector<int>> om_batches(const iso_tensor* t, int n_t, int K) {
+  std::vector<std::vector<int>> out;
+  std::vector<int> cur;
+  size_t bytes = 0;
+  for (int j = 0; j < n_t; ++j) {
+    if (t[j].rows == 0 || t[j].cols == 0) continue;
+    const size_t mb = om_matrix_bytes(t[j], K);
+    if (!cur.empty() && ((int)cur.size() == kOrthoBatch || bytes + mb > kOrthoBatchBytes)) {
+      out.push_back(cur);
+      cur.clear();
+      bytes = 0;
+    }
+    cur.push_back(j);
+    bytes += mb;
+  }
+  if (!cur.empty()) out.push_back(cur);
+  return out;
+}
+
+size_t om_batch_bytes(const iso_tensor* t, const std::vector<int>& ids, int K) {
+  int64_t max_n = 1;
+  for (int j : ids) max_n = std::max(max_n, t[j].cols);
+  OmBump bp{nullptr};
+  om_tables(bp, (int)ids.size(), K, max_n);
+  for (int j : ids) om_carve(bp, t[j].rows, t[j].cols, K, t[j].k);
+  return bp.off;
+}
+
 }  // namespace
 
 size_t ortho_workspace_bytes(const iso_tensor* t, int n_t, int K) {
   size_t most = 0;
-  for (int j = 0; j < n_t; ++j) {
-    if (t[j].rows == 0 || t[j].cols == 0) continue;
-    OmBump bp{nullptr};
-    om_carve(bp, t[j].rows, t[j].cols, K, t[j].k);
-    most = std::max(most, bp.off);
-  }
+  for (const auto& ids : om_batches(t, n_t, K)) most = std::max(most, om_batch_bytes(t, ids, K));
   return most;
 }
 
@@ -253,88 +300,121 @@ iso_status run_ortho(const iso_tensor* t, int n_t, int K, iso_dtype dt, double l
     if ((x) != hipSuccess) return ISO_ERR_HIP;   \
   } while (0)
   std::vector<uint8_t> host;
-  for (int j = 0; j < n_t; ++j) {
-    const iso_tensor& x = t[j];
-    const int64_t m = x.rows, n = x.cols;
-    if (m == 0 || n == 0) continue;
+  for (const auto& ids : om_batches(t, n_t, K)) {
+    const int nm = (int)ids.size(), nj = nm * K;
+    int64_t max_n = 1;
+    for (int j : ids) max_n = std::max(max_n, t[j].cols);
     OmBump bp{ws};
-    const OmBufs b = om_carve(bp, m, n, K, x.k);
-    // Jacobi table: job i on ja[i] (n x n) with rotations in jv[i]; finalize into U, V, S
-    const size_t tab_bytes = (size_t)((uint8_t*)b.desc - ws);
+    const OmTables tb = om_tables(bp, nm, K, max_n);
+    const size_t tab_bytes = bp.off;
+    std::vector<OmBufs> bs(nm);
+    for (int e = 0; e < nm; ++e) bs[e] = om_carve(bp, t[ids[e]].rows, t[ids[e]].cols, K, t[ids[e]].k);
+    // job tables (host image, same layout as on the device)
     host.assign(tab_bytes, 0);
-    JacobiJob* hj = (JacobiJob*)(host.data() + ((uint8_t*)b.jobs - ws));
-    double** hp = (double**)(host.data() + ((uint8_t*)b.ptrs - ws));
-    for (int i = 0; i < K; ++i) {
-      hj[i] = JacobiJob{b.ja[i], b.jv[i], n, n};
-      hp[i] = b.U[i];
-      hp[K + i] = b.V[i];
-      hp[2 * K + i] = b.S[i];
+    const auto at = [&](const void* dev) { return host.data() + ((const uint8_t*)dev - ws); };
+    JacobiJob* hj = (JacobiJob*)at(tb.jobs);
+    JacobiJob* hj1 = (JacobiJob*)at(tb.jobs1);
+    double** hp = (double**)at(tb.ptrs);
+    double** hp1 = (double**)at(tb.ptrs1);
+    for (int e = 0; e < nm; ++e) {
+      const OmBufs& b = bs[e];
+      const int64_t n = t[ids[e]].cols;
+      for (int i = 0; i < K; ++i) {
+        const int q = e * K + i;
+        hj[q] = JacobiJob{b.ja[i], b.jv[i], n, n};
+        hp[q] = b.U[i];
+        hp[nj + q] = b.V[i];
+        hp[2 * nj + q] = b.S[i];
+      }
+      hj1[e] = JacobiJob{b.ja[0], b.jv[0], n, n};
+      hp1[e] = b.U[0];
+      hp1[nm + e] = b.V[0];
+      hp1[2 * nm + e] = b.S[0];
     }
     OM_TRY(hipMemcpyAsync(ws, host.data(), tab_bytes, hipMemcpyHostToDevice, s));
-    const unsigned gmn = grid_for(m * n), gnn = grid_for(n * n);
     // 1. W_0, W_i (col-major binary64); M_i = W_0^T W_i into the Jacobi matrices
-    k_om_load<<<gmn, 256, 0, s>>>(b.w0, x.base, nullptr, m, n, dt);
-    for (int i = 0; i < K; ++i) {
-      k_om_load<<<gmn, 256, 0, s>>>(b.wi[i], x.base, x.deltas[i], m, n, dt);
-      gemm(n, n, m, 1.0, b.w0, m, 1, b.wi[i], 1, m, 0.0, b.ja[i], 1, n, s);
+    for (int e = 0; e < nm; ++e) {
+      const iso_tensor& x = t[ids[e]];
+      const OmBufs& b = bs[e];
+      const int64_t m = x.rows, n = x.cols;
+      const unsigned gmn = grid_for(m * n);
+      k_om_load<<<gmn, 256, 0, s>>>(b.w0, x.base, nullptr, m, n, dt);
+      for (int i = 0; i < K; ++i) {
+        k_om_load<<<gmn, 256, 0, s>>>(b.wi[i], x.base, x.deltas[i], m, n, dt);
+        gemm(n, n, m, 1.0, b.w0, m, 1, b.wi[i], 1, m, 0.0, b.ja[i], 1, n, s);
+      }
     }
-    // 2. R_i = U V^T from the SVDs of M_i
-    OM_TRY(jacobi_block(b.jobs, K, n, n, b.jst, status, s, false, b.split));
-    svd_finalize(b.jobs, b.ptrs, b.ptrs + K, b.ptrs + 2 * K, K, n, s);
-    for (int i = 0; i < K; ++i) {
-      k_om_check_min<<<1, 64, 0, s>>>(b.S[i], n, status);
-      gemm_abt(n, b.U[i], b.V[i], b.R[i], s);
+    // 2. R_i = U V^T from the SVDs of M_i, every matrix's K SVDs as one job set
+    OM_TRY(jacobi_block(tb.jobs, nj, max_n, max_n, tb.jst, status, s, false, tb.split));
+    svd_finalize(tb.jobs, tb.ptrs, tb.ptrs + nj, tb.ptrs + 2 * nj, nj, max_n, s);
+    for (int e = 0; e < nm; ++e) {
+      const OmBufs& b = bs[e];
+      const int64_t n = t[ids[e]].cols;
+      for (int i = 0; i < K; ++i) {
+        k_om_check_min<<<1, 64, 0, s>>>(b.S[i], n, status);
+        gemm_abt(n, b.U[i], b.V[i], b.R[i], s);
+        // 3. the SPD matrix 2I + R + R^T into the Jacobi matrix, R - R^T into A_i
+        k_om_sym_skew<<<grid_for(n * n), 256, 0, s>>>(b.ja[i], b.A[i], b.R[i], n);
+      }
     }
     // 3. A_i = (2I + R_i + R_i^T)^{-1} (R_i - R_i^T), the inverse as V S^{-1} U^T of its SVD
-    for (int i = 0; i < K; ++i) k_om_sym_skew<<<gnn, 256, 0, s>>>(b.ja[i], b.A[i], b.R[i], n);
-    OM_TRY(jacobi_block(b.jobs, K, n, n, b.jst, status, s, false, b.split));
-    svd_finalize(b.jobs, b.ptrs, b.ptrs + K, b.ptrs + 2 * K, K, n, s);
-    for (int i = 0; i < K; ++i) {
-      gemm(n, n, n, 1.0, b.U[i], n, 1, b.A[i], 1, n, 0.0, b.T, 1, n, s);     // T = U^T D
-      k_om_div_cols<<<gnn, 256, 0, s>>>(b.V[i], b.V[i], b.S[i], n, n, status);
-      gemm_ab(n, b.V[i], b.T, b.A[i], s);                                      // A_i = V S^{-1} T
+    OM_TRY(jacobi_block(tb.jobs, nj, max_n, max_n, tb.jst, status, s, false, tb.split));
+    svd_finalize(tb.jobs, tb.ptrs, tb.ptrs + nj, tb.ptrs + 2 * nj, nj, max_n, s);
+    for (int e = 0; e < nm; ++e) {
+      const OmBufs& b = bs[e];
+      const int64_t n = t[ids[e]].cols;
+      const unsigned gnn = grid_for(n * n);
+      for (int i = 0; i < K; ++i) {
+        gemm(n, n, n, 1.0, b.U[i], n, 1, b.A[i], 1, n, 0.0, b.T, 1, n, s);     // T = U^T D
+        k_om_div_cols<<<gnn, 256, 0, s>>>(b.V[i], b.V[i], b.S[i], n, n, status);
+        gemm_ab(n, b.V[i], b.T, b.A[i], s);                                      // A_i = V S^{-1} T
+      }
+      // 4. A = (mean |A_i|) sum A_i / |sum A_i|
+      for (int i = 0; i < K; ++i) om_norms(b.A[i], 0, n * n, 1, b.part, b.norm + i, s);
+      k_copy<<<gnn, 256, 0, s>>>(b.asum, b.A[0], n * n);
+      for (int i = 1; i < K; ++i) k_add<<<gnn, 256, 0, s>>>(b.asum, b.asum, b.A[i], n * n);
+      om_norms(b.asum, 0, n * n, 1, b.part, b.norm + K, s);
+      k_om_coef<<<1, 64, 0, s>>>(b.norm, K, b.coef);
+      k_om_scale<<<gnn, 256, 0, s>>>(b.asum, b.coef, n * n);
+      // 5. I - A^2 into the Jacobi matrix, I + A into P
+      gemm_ab(n, b.asum, b.asum, b.T, s);
+      k_om_forward_parts<<<gnn, 256, 0, s>>>(b.ja[0], b.P, b.T, b.asum, n);
     }
-    // 4. A = (mean |A_i|) sum A_i / |sum A_i|
-    for (int i = 0; i < K; ++i) om_norms(b.A[i], 0, n * n, 1, b.part, b.norm + i, s);
-    k_copy<<<gnn, 256, 0, s>>>(b.asum, b.A[0], n * n);
-    for (int i = 1; i < K; ++i) k_add<<<gnn, 256, 0, s>>>(b.asum, b.asum, b.A[i], n * n);
-    om_norms(b.asum, 0, n * n, 1, b.part, b.norm + K, s);
-    k_om_coef<<<1, 64, 0, s>>>(b.norm, K, b.coef);
-    k_om_scale<<<gnn, 256, 0, s>>>(b.asum, b.coef, n * n);
     // 5. R = (I + A)^2 (I - A^2)^{-1}, W_rot = W_0 R
-    gemm_ab(n, b.asum, b.asum, b.T, s);
-    k_om_forward_parts<<<gnn, 256, 0, s>>>(b.ja[0], b.P, b.T, b.asum, n);
-    OM_TRY(jacobi_block(b.jobs, 1, n, n, b.jst, status, s, false, b.split));
-    svd_finalize(b.jobs, b.ptrs, b.ptrs + K, b.ptrs + 2 * K, 1, n, s);
-    k_om_div_cols<<<gnn, 256, 0, s>>>(b.V[0], b.V[0], b.S[0], n, n, status);
-    gemm_abt(n, b.V[0], b.U[0], b.T, s);                                       // (I - A^2)^{-1}
-    gemm_ab(n, b.P, b.P, b.PP, s);
-    gemm_ab(n, b.PP, b.T, b.Rm, s);
-    gemm(m, n, n, 1.0, b.w0, 1, m, b.Rm, 1, n, 0.0, b.wrot, 1, m, s);
-    // 6. residuals delta_i = W_i - W_0 R_i (binary32, row-major) and their TIES merge
-    float* dptr[ISO_MAX_K];
-    for (int i = 0; i < K; ++i) {
-      gemm(m, n, n, -1.0, b.w0, 1, m, b.R[i], 1, n, 1.0, b.wi[i], 1, m, s);
-      k_om_to_f32<<<gmn, 256, 0, s>>>(b.delta[i], b.wi[i], m, n);
-      dptr[i] = b.delta[i];
+    OM_TRY(jacobi_block(tb.jobs1, nm, max_n, max_n, tb.jst1, status, s, false, tb.split));
+    svd_finalize(tb.jobs1, tb.ptrs1, tb.ptrs1 + nm, tb.ptrs1 + 2 * nm, nm, max_n, s);
+    for (int e = 0; e < nm; ++e) {
+      const iso_tensor& x = t[ids[e]];
+      const OmBufs& b = bs[e];
+      const int64_t m = x.rows, n = x.cols;
+      k_om_div_cols<<<grid_for(n * n), 256, 0, s>>>(b.V[0], b.V[0], b.S[0], n, n, status);
+      gemm_abt(n, b.V[0], b.U[0], b.T, s);                                     // (I - A^2)^{-1}
+      gemm_ab(n, b.P, b.P, b.PP, s);
+      gemm_ab(n, b.PP, b.T, b.Rm, s);
+      gemm(m, n, n, 1.0, b.w0, 1, m, b.Rm, 1, n, 0.0, b.wrot, 1, m, s);
+      // 6. residuals delta_i = W_i - W_0 R_i (binary32, row-major) and their TIES merge
+      for (int i = 0; i < K; ++i) {
+        gemm(m, n, n, -1.0, b.w0, 1, m, b.R[i], 1, n, 1.0, b.wi[i], 1, m, s);
+        k_om_to_f32<<<grid_for(m * n), 256, 0, s>>>(b.delta[i], b.wi[i], m, n);
+      }
+      OM_TRY(hipGetLastError());
+      iso_tensor tt{};
+      tt.base = b.delta[0];
+      for (int i = 0; i < K; ++i) tt.deltas[i] = b.delta[i];
+      tt.rows = m;
+      tt.cols = n;
+      tt.k = x.k;
+      iso_status st = iso_topk_mask(&tt, 1, K, ISO_F32, b.desc, nullptr, b.sub, b.sub_bytes, s);
+      if (st != ISO_OK) return st;
+      float* uptr[1] = {b.u};
+      st = iso_merge(&tt, 1, K, ISO_F32, ISO_MERGE_TIES, b.desc, lambda, 0.0, uptr, b.sub, b.sub_bytes, s);
+      if (st != ISO_OK) return st;
+      k_om_or_status<<<1, 64, 0, s>>>(status, (const uint32_t*)b.sub);
+      // 7. out = round(W_rot + u)
+      k_om_out<<<grid_for(m * n), 256, 0, s>>>(x.out, b.wrot, b.u, m, n, dt, status);
     }
     OM_TRY(hipGetLastError());
-    iso_tensor tt{};
-    tt.base = b.delta[0];
-    for (int i = 0; i < K; ++i) tt.deltas[i] = dptr[i];
-    tt.rows = m;
-    tt.cols = n;
-    tt.k = x.k;
-    iso_status st = iso_topk_mask(&tt, 1, K, ISO_F32, b.desc, nullptr, b.sub, b.sub_bytes, s);
-    if (st != ISO_OK) return st;
-    float* uptr[1] = {b.u};
-    st = iso_merge(&tt, 1, K, ISO_F32, ISO_MERGE_TIES, b.desc, lambda, 0.0, uptr, b.sub, b.sub_bytes, s);
-    if (st != ISO_OK) return st;
-    k_om_or_status<<<1, 64, 0, s>>>(status, (const uint32_t*)b.sub);
-    // 7. out = round(W_rot + u)
-    k_om_out<<<gmn, 256, 0, s>>>(x.out, b.wrot, b.u, m, n, dt, status);
-    OM_TRY(hipGetLastError());
-    // the next matrix reuses the workspace and the host staging
+    // the next batch reuses the workspace and the host staging
     OM_TRY(hipStreamSynchronize(s));
   }
   return ISO_OK;
