@@ -381,10 +381,14 @@ iso_status iso_optimizer_step(const iso_frame* f, int n_f, int dt, const iso_ada
  * where rows_x is rows for U and cols for V.  Muon itself approximates
  * polar(d) by a few quintic Newton-Schulz steps; here o is the polar factor,
  * computed as for the retraction.  v_u and v_v are not used (they may be
- * NULL).  d needs full column rank: otherwise (a zero gradient, say) it has
- * no unique polar factor, the iteration does not converge and
- * iso_read_device_status reports ISO_ERR_INTERNAL.  Workspace:
- * iso_workspace_size_optimizer.
+ * NULL).  The zero direction (a zero gradient on a zero buffer) takes
+ * o = 0, so x only decays; so does a d whose Gram d^T d is exactly zero in
+ * binary64 (entries below ~1e-154).  Any other d needs full column rank:
+ * otherwise it has no unique polar factor, the iteration does not converge
+ * within 48 steps and iso_read_device_status reports ISO_ERR_INTERNAL (a
+ * full-rank d converges within the cap up to condition numbers near 1e10:
+ * about 20 steps up to 1e5, 35 at 1e8).
+ * Workspace: iso_workspace_size_optimizer.
  */
 typedef struct iso_muon {
   double lr, momentum, weight_decay;

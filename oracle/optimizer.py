@@ -18,7 +18,8 @@ shape rows x q with momentum buffer b:
   b <- mu b + g;  d = g + mu b (Nesterov) or d = b;  o = polar(d);
   x <- x - lr (sqrt(max(1, rows / q)) o + wd x).
 Muon approximates polar(d) with a few quintic Newton-Schulz steps; here o is the polar factor
-itself.
+itself.  The zero direction (a zero gradient on a zero momentum buffer) has no polar factor: it
+takes o = 0, as the sign of zero is zero, so x only decays by lr wd x.
 """
 import numpy as np
 
@@ -55,7 +56,7 @@ def muon(x, g, b, lr, mu, wd, nesterov=True):
     """One Muon update of x (rows x q) with momentum buffer b; returns (x, b), new arrays."""
     b = mu * b + g
     d = g + mu * b if nesterov else b
-    o = polar(d)
+    o = polar(d) if d.any() else np.zeros_like(d)
     scale = np.sqrt(max(1.0, x.shape[0] / x.shape[1]))
     return x - lr * (scale * o + wd * x), b
 

@@ -235,6 +235,7 @@ __global__ void k_combine(double* __restrict__ out, const double* __restrict__ x
 // The schedule starts from kNsScaledL0 (a singular value below kNsScaledL0 times the largest
 // still grows at least 1.5-fold per step); from the second step on, l is raised to the bound
 // s_min^2 >= 1 - q max |X^T X - I| when that is larger, and the last step is a plain one.
+// A matrix whose Gram X^T X is exactly zero maps to the zero matrix (one step with T = 0).
 struct NsJob {
   double* g;        // q x q: X^T X, then the step matrix T in place
   int64_t q;
@@ -300,8 +301,11 @@ __global__ void k_ns_form(const NsJob* __restrict__ jobs, NsState* st, int scale
   const NsJob J = jobs[job];
   const bool first = st[job].steps == 0;
   const double err = __longlong_as_double((long long)st[job].err);
-  const bool last = err <= kNsTol;
   const double cs = __longlong_as_double((long long)st[job].csum);
+  // X^T X == 0 on entry (the zero matrix, or entries whose squares underflow): no polar factor;
+  // the result is the zero matrix, taken in this one step with T = 0
+  const bool zero = first && cs == 0.0;
+  const bool last = err <= kNsTol || zero;
   // the scaled schedule assumes s <= 1 from the start; the plain one only needs s < sqrt 3
   const double c = (first && (scaled || cs > 2.0)) ? cs : 1.0;
   const double ic = (c > 0.0) ? 1.0 / c : 1.0, is = sqrt(ic);
@@ -316,7 +320,7 @@ __global__ void k_ns_form(const NsJob* __restrict__ jobs, NsState* st, int scale
   const int64_t n = J.q * J.q;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
     const int64_t i = e % J.q, j = e / J.q;
-    J.g[e] = ((i == j ? 3.0 : 0.0) - J.g[e] * (a2 * ic)) * (0.5 * a * is);
+    J.g[e] = zero ? 0.0 : ((i == j ? 3.0 : 0.0) - J.g[e] * (a2 * ic)) * (0.5 * a * is);
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     st[job].last = last;

@@ -117,3 +117,58 @@ def test_muon_three_steps_match_the_oracle(dtype, nesterov):
             else:
                 want = nm.f64_to_bf16(w_ref.ravel()).astype(np.int32)
                 assert np.max(np.abs(w.astype(np.int32) - want)) <= 1
+
+
+def test_muon_zero_and_ill_conditioned_directions():
+    """Three frames in one ISO-Muon call: a zero gradient (both directions zero: o = 0, the frames
+    only decay and are retracted back), a gradient whose U-side direction has condition number
+    ~1e8 (singular values 1 .. 1e-8 before the storage rounding; the scaled iteration needs ~35
+    of its 48 steps), and a Gaussian one.  Status OK and the oracle's frames and weights to the bars
+    above; lr 1e-3 keeps the ill-conditioned polar factor's rounding-level differences (~eps cond)
+    far below the frame bar."""
+    import torch
+    rng = np.random.default_rng(33)
+    dtype = "f32"
+    specs = [("zero", 64, 48, 48), ("illcond", 96, 64, 64), ("gauss", 80, 72, 72)]
+    frames, ref = [], []
+    for kind, m, n, q in specs:
+        u, _ = np.linalg.qr(rng.standard_normal((m, q)))
+        v, _ = np.linalg.qr(rng.standard_normal((n, q)))
+        s = np.sort(rng.uniform(0.5, 2.0, q))[::-1].copy()
+        if kind == "zero":
+            g = np.zeros((m, n))
+        elif kind == "illcond":
+            # G_W V Sigma_0 = U D Q^T with D from 1 down to 1e-8 (n = q: V is square orthogonal)
+            qq, _ = np.linalg.qr(rng.standard_normal((q, q)))
+            a = (u * np.logspace(0, -8, q)) @ qq.T
+            g = (a / s) @ v.T
+        else:
+            g = rng.standard_normal((m, n)) * 0.1
+        g_store = nm.from_f64(g.ravel(), dtype)
+        g = nm.to_f64(g_store, dtype).reshape(m, n)
+        z = (np.zeros((m, q)), np.zeros((n, q)))
+        dev = dict(u=_colmajor(u), v=_colmajor(v), sigma=torch.tensor(s, device="cuda"),
+                   m_u=_colmajor(z[0]), v_u=None, m_v=_colmajor(z[1]), v_v=None, grad=to_dev(g_store),
+                   w_out=torch.empty(m * n, dtype=torch.int32, device="cuda"))
+        frames.append(iso.Frame(rows=m, cols=n, rank=q, **dev))
+        ref.append(dict(u=u, v=v, s=s, g=g, st=z))
+    gu = ref[1]["g"] @ ref[1]["v"] * ref[1]["s"]
+    sv = np.linalg.svd(gu, compute_uv=False)
+    say(f"iso-muon zero / ill-conditioned (cond {sv[0] / sv[-1]:.2e}) / gaussian directions")
+    ws = iso.optimizer_workspace(frames)
+    hp = dict(lr=1e-3, momentum=0.9, weight_decay=0.01)
+    for t in (1, 2):
+        iso.iso_optimizer_step_muon(frames, iso.F32, nesterov=True, ws=ws, **hp)
+        assert iso.iso_read_device_status(ws) == 0
+        for (kind, *_), F, R in zip(specs, frames, ref):
+            R["u"], R["v"], w_ref, R["st"] = op.iso_muon_step(R["u"], R["v"], R["s"], R["g"], R["st"], hp["lr"],
+                                                              hp["momentum"], hp["weight_decay"], True)
+            m, n, q = F.rows, F.cols, F.rank
+            assert np.abs(_back(F.u, m, q) - R["u"]).max() <= 1e-10, (kind, t)
+            assert np.abs(_back(F.v, n, q) - R["v"]).max() <= 1e-10, (kind, t)
+            if kind == "zero":
+                assert not _back(F.m_u, m, q).any() and not _back(F.m_v, n, q).any()
+            w = from_dev(F.w_out, m * n, dtype)
+            ref_w = w_ref.ravel()
+            scale = np.maximum(np.abs(ref_w), 2.0 ** -10 * np.abs(ref_w).max())
+            assert np.max(np.abs(w.astype(np.float64) - ref_w) / scale) <= 1e-6, (kind, t)

@@ -140,3 +140,19 @@ def test_iso_muon_keeps_the_spectrum_and_ignores_the_gradient_scale():
     u1, v1, w1, _ = op.iso_muon_step(u0, v0, s0, rng.standard_normal((12, 9)), (np.zeros((12, 9)), np.zeros((9, 9))),
                                      lr=0.0, wd=0.3)
     assert np.allclose(w1, (u0 * s0) @ v0.T, atol=1e-13)
+
+
+def test_muon_zero_direction_only_decays():
+    """A zero gradient on a zero buffer has no polar factor; the step is the decoupled decay alone,
+    x (1 - lr wd), and ISO-Muon without decay then returns the weights it was given."""
+    rng = np.random.default_rng(24)
+    x = rng.standard_normal((10, 4))
+    z = np.zeros_like(x)
+    x1, b1 = op.muon(x, z, z, lr=0.1, mu=0.9, wd=0.05)
+    assert np.array_equal(x1, x - 0.1 * (0.05 * x))
+    assert not b1.any()
+    m, n, q = 14, 9, 9
+    u, v, s = _frames(rng, m, n, q)
+    up, vp, wp, st = op.iso_muon_step(u, v, s, np.zeros((m, n)), (np.zeros((m, q)), np.zeros((n, q))), lr=0.3)
+    assert np.allclose(wp, (u * s) @ v.T, atol=1e-13)
+    assert np.allclose(up, u, atol=1e-13) and np.allclose(vp, v, atol=1e-13)
