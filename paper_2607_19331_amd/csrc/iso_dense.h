@@ -867,19 +867,26 @@ typedef double gemm_f64x4_t __attribute__((ext_vector_type(4)));
 // feeds twice the rows and columns).  k in steps of GK = 16 staged in LDS, double-buffered: the
 // next k-tile is loaded into registers before the current one's MFMAs and written to the other
 // buffer after them, one barrier per step.  Operands are loaded along whichever of their strides
-// is 1, so row- and column-major inputs both read whole cache lines.  LDS rows are padded so that
-// the four k rows of a fragment read fall on different bank halves.
+// is 1, so row- and column-major inputs both read whole cache lines, and staged in the layout that
+// load writes without bank conflicts: k-major ([k][i], rows of PAD doubles, padded so that the four
+// k rows of a fragment read fall on different bank halves) for an operand read along i, i-major
+// ([i][k], rows of SK = GK + 2 doubles) for one read along k.  In the i-major layout the sixteen
+// rows of a fragment read start 36 banks apart (mod 64), so they and the two k of a half-wave
+// cover the 64 banks once; a k-major store of a k-fast operand would put 16 k rows 1152 bytes apart
+// (8-way conflicts).
 template <int W>
 struct GemmTile {
   static constexpr int TM = 32 * W, TW = 16 * W, PAD = (W == 2) ? 80 : TM + 16, PT = GK * TM / 256;
+  static constexpr int SK = GK + 2;
+  static constexpr int BUF = (GK * PAD > TM * SK) ? GK * PAD : TM * SK;
 };
 
 template <int W>
 __device__ __forceinline__ void gemm_tile(const GemmJob& J, int64_t bx, int64_t by) {
   using T = GemmTile<W>;
-  constexpr int TM = T::TM, TW = T::TW, PAD = T::PAD, PT = T::PT;
-  __shared__ double As[2][GK][PAD];
-  __shared__ double Bs[2][GK][PAD];
+  constexpr int TM = T::TM, TW = T::TW, PAD = T::PAD, PT = T::PT, SK = T::SK, BUF = T::BUF;
+  __shared__ double As[2][BUF];
+  __shared__ double Bs[2][BUF];
   const int64_t i0 = bx * TM, j0 = by * TM;
   if (i0 >= J.M || j0 >= J.N || (J.upper && i0 > j0)) return;
   if (J.skip != nullptr && *J.skip != 0) return;
@@ -911,8 +918,8 @@ __device__ __forceinline__ void gemm_tile(const GemmJob& J, int64_t bx, int64_t 
       const int e = threadIdx.x + 256 * q;
       const int ka = a_kfast ? (e & 15) : (e / TM), ia = a_kfast ? (e >> 4) : (e % TM);
       const int kb = b_kfast ? (e & 15) : (e / TM), jb = b_kfast ? (e >> 4) : (e % TM);
-      As[buf][ka][ia] = pa[q];
-      Bs[buf][kb][jb] = pb[q];
+      As[buf][a_kfast ? ia * SK + ka : ka * PAD + ia] = pa[q];
+      Bs[buf][b_kfast ? jb * SK + kb : kb * PAD + jb] = pb[q];
     }
   };
   load(0);
@@ -926,9 +933,15 @@ __device__ __forceinline__ void gemm_tile(const GemmJob& J, int64_t bx, int64_t 
     for (int sub = 0; sub < GK / 4; ++sub) {
       double a[W], b[W];
 #pragma unroll
-      for (int rb = 0; rb < W; ++rb) a[rb] = As[buf][4 * sub + g][TW * wm + 16 * rb + ln];
+      for (int rb = 0; rb < W; ++rb) {
+        const int i = TW * wm + 16 * rb + ln, k = 4 * sub + g;
+        a[rb] = As[buf][a_kfast ? i * SK + k : k * PAD + i];
+      }
 #pragma unroll
-      for (int cb = 0; cb < W; ++cb) b[cb] = Bs[buf][4 * sub + g][TW * wn + 16 * cb + ln];
+      for (int cb = 0; cb < W; ++cb) {
+        const int j = TW * wn + 16 * cb + ln, k = 4 * sub + g;
+        b[cb] = Bs[buf][b_kfast ? j * SK + k : k * PAD + j];
+      }
 #pragma unroll
       for (int rb = 0; rb < W; ++rb)
 #pragma unroll
