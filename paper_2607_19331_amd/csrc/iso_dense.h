@@ -503,12 +503,14 @@ __global__ void __launch_bounds__(256) k_bjg_part(const JacobiJob* __restrict__ 
 #pragma unroll
   for (int j = 0; j < 3; ++j) acc[j] = jac_f64x4_t{0.0, 0.0, 0.0, 0.0};
   __syncthreads();
-  double pf[kGChunkPer];
-  gram_load(pf, J.a, r, row1, gc, P.nc, row0);
-  for (int k0 = row0; k0 < row1; k0 += kGN) {
+  // two row chunks in flight, as in k_bjg_apply
+  double pf0[kGChunkPer], pf1[kGChunkPer];
+  gram_load(pf0, J.a, r, row1, gc, P.nc, row0);
+  if (row0 + kGN < row1) gram_load(pf1, J.a, r, row1, gc, P.nc, row0 + kGN);
+  auto chunk = [&](int k0, double (&pf)[kGChunkPer]) {
     gram_stage(ch, pf);
     __syncthreads();
-    if (k0 + kGN < row1) gram_load(pf, J.a, r, row1, gc, P.nc, k0 + kGN);
+    if (k0 + 2 * kGN < row1) gram_load(pf, J.a, r, row1, gc, P.nc, k0 + 2 * kGN);
 #pragma unroll 4
     for (int s = 0; s < kGN / 4; ++s) {
 #pragma unroll
@@ -521,6 +523,10 @@ __global__ void __launch_bounds__(256) k_bjg_part(const JacobiJob* __restrict__ 
       }
     }
     __syncthreads();
+  };
+  for (int k0 = row0; k0 < row1; k0 += 2 * kGN) {
+    chunk(k0, pf0);
+    if (k0 + kGN < row1) chunk(k0 + kGN, pf1);
   }
   // G[i][j] at j * kGN + i; a tile above the diagonal also fills its mirror below it
   double* out = S.part + (((size_t)job * S.npairs + pr) * S.nslices + z) * (kGN * kGN);
@@ -583,7 +589,9 @@ __global__ void __launch_bounds__(512) k_bjg_rot(const JacobiJob* __restrict__ j
 
 __global__ void __launch_bounds__(256) k_bjg_apply(const JacobiJob* __restrict__ jobs, const JacobiState* st,
                                                    int round, GramSplit S, int slices_a, int slices_v) {
-  __shared__ double ch[kGN * kGP];
+  constexpr int QS = kGN + 2;                      // Q row stride: the 16 rows of a fragment read
+  __shared__ double ch[kGN * kGP];                 // start 4 banks apart, so a half-wave is conflict-free
+  __shared__ double qs[kGN * QS];
   __shared__ int gc[kGN];
   const int job = blockIdx.y;
   if (st[job].done) return;
@@ -599,21 +607,19 @@ __global__ void __launch_bounds__(256) k_bjg_apply(const JacobiJob* __restrict__
   if (row0 >= rows) return;
   if (threadIdx.x < kGN) gc[threadIdx.x] = (threadIdx.x < P.n0) ? P.c0 + threadIdx.x : P.c1 + (threadIdx.x - P.n0);
   const double* q = S.qrot + ((size_t)job * S.npairs + pr) * (kGN * kGN);
-  // this lane's MFMA operands of Q (the same for every chunk) in registers
+  // Q (the same for every chunk) in LDS, which leaves the registers to the chunks in flight
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
-  double qr[kGN / 4][4];
-#pragma unroll
-  for (int s4 = 0; s4 < kGN / 4; ++s4)
-#pragma unroll
-    for (int t = 0; t < 4; ++t) qr[s4][t] = q[(16 * t + ln) * kGN + 4 * s4 + g];
+  for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) qs[(e / kGN) * QS + e % kGN] = q[e];
   __syncthreads();
   double* X = on_a ? J.a : J.v;
-  double pf[kGChunkPer];
-  gram_load(pf, X, rows, row1, gc, P.nc, row0);
-  for (int k0 = row0; k0 < row1; k0 += kGN) {
+  // two row chunks in flight: chunk k is loaded into pf[k & 1] while chunk k - 1 is rotated
+  double pf0[kGChunkPer], pf1[kGChunkPer];
+  gram_load(pf0, X, rows, row1, gc, P.nc, row0);
+  if (row0 + kGN < row1) gram_load(pf1, X, rows, row1, gc, P.nc, row0 + kGN);
+  auto chunk = [&](int k0, double (&pf)[kGChunkPer]) {
     gram_stage(ch, pf);
     __syncthreads();
-    if (k0 + kGN < row1) gram_load(pf, X, rows, row1, gc, P.nc, k0 + kGN);
+    if (k0 + 2 * kGN < row1) gram_load(pf, X, rows, row1, gc, P.nc, k0 + 2 * kGN);
     jac_f64x4_t acc[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[t] = jac_f64x4_t{0.0, 0.0, 0.0, 0.0};
@@ -621,7 +627,8 @@ __global__ void __launch_bounds__(256) k_bjg_apply(const JacobiJob* __restrict__
     for (int s4 = 0; s4 < kGN / 4; ++s4) {
       const double a = ch[(4 * s4 + g) * kGP + 16 * w + ln];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, qr[s4][t], acc[t], 0, 0, 0);
+      for (int t = 0; t < 4; ++t)
+        acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, qs[(16 * t + ln) * QS + 4 * s4 + g], acc[t], 0, 0, 0);
     }
     __syncthreads();
 #pragma unroll
@@ -634,6 +641,10 @@ __global__ void __launch_bounds__(256) k_bjg_apply(const JacobiJob* __restrict__
       if (l < P.nc && k0 + i < row1) X[(int64_t)gc[l] * rows + k0 + i] = ch[l * kGP + i];
     }
     __syncthreads();
+  };
+  for (int k0 = row0; k0 < row1; k0 += 2 * kGN) {
+    chunk(k0, pf0);
+    if (k0 + kGN < row1) chunk(k0 + kGN, pf1);
   }
 }
 
