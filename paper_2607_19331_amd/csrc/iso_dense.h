@@ -438,12 +438,23 @@ __global__ void __launch_bounds__(256) k_bjacobi_gram(const JacobiJob* __restric
 }
 
 // ---- the same step with the rows of a block pair split over workgroups ---------------------------
-// Three launches per round: partial Grams of kGSliceRows-row slices of A (one workgroup per pair
+// Three launches per round: partial Grams of row slices of A (one workgroup per pair
 // and slice), the sum of a pair's partials in slice order with the rotation test and the inner
 // sweep (one workgroup per pair; the rotation and a flag go to global memory), and the rotation of
 // every slice of A and of V (one workgroup per pair and slice).  Long columns then take many
 // short workgroups instead of one long one; the result is the same step.
-constexpr int kGSliceRows = 1024;
+// Rows per slice, one value for a whole job set: 512 while the set's longest column is at most
+// 8192 rows (more workgroups per round for the mid-sized matrices, where the rounds are short),
+// 1024 beyond (fewer partial Grams for each rotation step to sum).
+constexpr int64_t kGSliceSmallMax = 8192;
+inline int gram_slice_rows(int64_t max_r) { return max_r <= kGSliceSmallMax ? 512 : 1024; }
+// Slices of a job set of at most max_r rows, or of any set with fewer rows (which may take the
+// smaller slice): the count the split scratch is sized for.
+inline int64_t gram_slices_bound(int64_t max_r) {
+  const int64_t own = (max_r + gram_slice_rows(max_r) - 1) / gram_slice_rows(max_r);
+  const int64_t small = (std::min(max_r, kGSliceSmallMax) + 511) / 512;
+  return std::max(own, small);
+}
 
 struct GramPair {     // the block pair a workgroup of round `round` works on, or none
   int ok, nc;
@@ -470,6 +481,7 @@ struct GramSplit {
   double* qrot;     // njobs x npairs x kGN^2: rotations
   int* need;        // njobs x npairs: 1 if the pair rotates this round
   int npairs, nslices;
+  int slice;        // rows per slice (gram_slice_rows of the set)
 };
 
 __global__ void __launch_bounds__(256) k_bjg_part(const JacobiJob* __restrict__ jobs, const JacobiState* st,
@@ -482,7 +494,7 @@ __global__ void __launch_bounds__(256) k_bjg_part(const JacobiJob* __restrict__ 
   const int r = (int)J.r, c = (int)J.c;
   const int pr = blockIdx.x / S.nslices, z = blockIdx.x % S.nslices;
   const GramPair P = gram_pair_of(c, pr, round);
-  const int row0 = z * kGSliceRows, row1 = min(r, row0 + kGSliceRows);
+  const int row0 = z * S.slice, row1 = min(r, row0 + S.slice);
   if (!P.ok || row0 >= r) return;
   if (threadIdx.x < kGN) gc[threadIdx.x] = (threadIdx.x < P.n0) ? P.c0 + threadIdx.x : P.c1 + (threadIdx.x - P.n0);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
@@ -559,7 +571,7 @@ __global__ void __launch_bounds__(512) k_bjg_rot(const JacobiJob* __restrict__ j
     if (threadIdx.x == 0 && pr < S.npairs) *need = 0;
     return;
   }
-  const int ns = (r + kGSliceRows - 1) / kGSliceRows;
+  const int ns = (r + S.slice - 1) / S.slice;
   const double* part = S.part + ((size_t)job * S.npairs + pr) * S.nslices * (kGN * kGN);
   for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
     double x = 0.0;
@@ -603,7 +615,7 @@ __global__ void __launch_bounds__(256) k_bjg_apply(const JacobiJob* __restrict__
   if (!P.ok || S.need[(size_t)job * S.npairs + pr] == 0) return;
   const bool on_a = z < slices_a;
   const int rows = on_a ? r : c;
-  const int row0 = (on_a ? z : z - slices_a) * kGSliceRows, row1 = min(rows, row0 + kGSliceRows);
+  const int row0 = (on_a ? z : z - slices_a) * S.slice, row1 = min(rows, row0 + S.slice);
   if (row0 >= rows) return;
   if (threadIdx.x < kGN) gc[threadIdx.x] = (threadIdx.x < P.n0) ? P.c0 + threadIdx.x : P.c1 + (threadIdx.x - P.n0);
   const double* q = S.qrot + ((size_t)job * S.npairs + pr) * (kGN * kGN);
@@ -651,7 +663,7 @@ __global__ void __launch_bounds__(256) k_bjg_apply(const JacobiJob* __restrict__
 // Scratch of the split step for njobs jobs of at most max_r rows and max_c columns.
 inline size_t gram_split_bytes(int njobs, int64_t max_r, int64_t max_c) {
   const int64_t nb = (max_c + kGW - 1) / kGW, np = (nb + (nb & 1)) / 2;
-  const int64_t ns = (max_r + kGSliceRows - 1) / kGSliceRows;
+  const int64_t ns = gram_slices_bound(max_r);
   return ((size_t)njobs * np * (size_t)(ns + 1) * kGN * kGN) * sizeof(double) + (size_t)njobs * np * sizeof(int) + 256;
 }
 
@@ -664,12 +676,13 @@ inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_r, i
   GramSplit S{};
   if (scratch != nullptr) {
     S.npairs = std::max(1, nbp / 2);
-    S.nslices = (int)((max_r + kGSliceRows - 1) / kGSliceRows);
+    S.slice = gram_slice_rows(max_r);
+    S.nslices = (int)((max_r + S.slice - 1) / S.slice);
     S.part = (double*)scratch;
     S.qrot = S.part + (size_t)njobs * S.npairs * S.nslices * kGN * kGN;
     S.need = (int*)(S.qrot + (size_t)njobs * S.npairs * kGN * kGN);
   }
-  const int slices_a = S.nslices, slices_v = (int)((max_c + kGSliceRows - 1) / kGSliceRows);
+  const int slices_a = S.nslices, slices_v = S.slice ? (int)((max_c + S.slice - 1) / S.slice) : 0;
   // a sweep over more than 2^26 matrix entries takes milliseconds: check the flags after each one
   const int check = (double)max_r * (double)max_c * njobs > 67108864.0 ? 1 : kJacobiCheckSweeps;
   std::vector<JacobiState> h(njobs);

@@ -610,9 +610,9 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
   jacobi_block_shape(svd_r, svd_c, &width, &per_cu);
   for (int e = 0; e < nm; ++e) {
     const int64_t nb = (std::min(t[ids[e]].rows, t[ids[e]].cols) + width - 1) / width;
-    // the Gram step splits each block pair's rows over workgroups of kGSliceRows rows
-    const int64_t slices =
-        width == kGW ? (std::max(t[ids[e]].rows, t[ids[e]].cols) + kGSliceRows - 1) / kGSliceRows : 1;
+    // the Gram step splits each block pair's rows over workgroups of gram_slice_rows rows
+    const int64_t sl = gram_slice_rows(svd_r);
+    const int64_t slices = width == kGW ? (std::max(t[ids[e]].rows, t[ids[e]].cols) + sl - 1) / sl : 1;
     wgs += (int64_t)(K + 1) * ((nb + 1) / 2) * slices;
   }
   int dev = 0, cus = 0;
