@@ -418,9 +418,9 @@ def bench_layer_optimizer(args, iso, synth, torch):
     """One ISO-AdamW step (iso_optimizer_step) or, with --rule muon, one ISO-Muon step
     (iso_optimizer_step_muon) over the single layer's seven matrices (q/k/v/o 2048x2048, gate/up
     2048x5632, down 5632x2048) with full-rank frames, bf16 weights and gradients, timed with HIP
-    events.  Roofline: binary64, the algorithmic flops of the two factor-gradient products, the
-    two polar SVDs of the retraction (Golub & Van Loan's count; Muon adds two for its
-    directions) and W+."""
+    events.  Roofline: the dominant work, the Newton-Schulz polar iterations (binary64 MFMA
+    products): the flops their steps performed, as the library counts them, over their time
+    from the library's profiling events in the same run."""
     import numpy as np
     from oracle import optimizer as op
     wl = synth.workload("layer")
@@ -428,7 +428,7 @@ def bench_layer_optimizer(args, iso, synth, torch):
     stream = torch.cuda.current_stream().cuda_stream
     gen = torch.Generator(device=dev)
     gen.manual_seed(0)
-    frames, flops = [], 0
+    frames = []
     for t, spec in enumerate(wl.tensors):
         m, n = spec.rows, spec.cols
         q = min(m, n)
@@ -441,8 +441,6 @@ def bench_layer_optimizer(args, iso, synth, torch):
         frames.append(iso.Frame(u=u.t().contiguous().view(-1), v=v.t().contiguous().view(-1), sigma=s,
                                 m_u=z(m), v_u=z(m), m_v=z(n), v_v=z(n), grad=grad,
                                 w_out=torch.empty(m * n, dtype=torch.int16, device=dev), rows=m, cols=n, rank=q))
-        polars = 2 if args.rule == "adamw" else 4
-        flops += 2 * (2 * m * n * q) + polars // 2 * (svd_flops(m, q) + svd_flops(n, q)) + 2 * m * n * q
     ws = iso.optimizer_workspace(frames, dev)
     muon = args.rule == "muon"
     hp = dict(lr=1e-6, weight_decay=0.0) if muon else dict(lr=1e-6, beta1=0.9, beta2=0.999, eps=1e-8,
@@ -464,6 +462,7 @@ def bench_layer_optimizer(args, iso, synth, torch):
         raise RuntimeError("device status reports an error")
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
     torch.cuda.synchronize()
+    iso.iso_profile_begin()
     t0 = time.perf_counter()
     for s_ in range(args.steps):
         ev[s_][0].record()
@@ -471,6 +470,8 @@ def bench_layer_optimizer(args, iso, synth, torch):
         ev[s_][1].record()
     torch.cuda.synchronize()
     ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    ns_flops = iso.iso_profile_flops()
+    ns_ms, ns_regions = iso.iso_profile_end()
     opt_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
     N = wl.numel
     rec = {
@@ -483,10 +484,13 @@ def bench_layer_optimizer(args, iso, synth, torch):
                                f"(factor gradients, {'Muon with polar directions' if muon else 'AdamW'}, polar "
                                "retraction, W+) on full-rank frames"},
         "optimizer_ms": opt_ms,
-        "roofline": {"bound": "fp64", "kernel": ("iso_optimizer_step_muon" if muon else "iso_optimizer_step") +
-                     " (binary64 GEMMs and Newton-Schulz polar)",
-                     "achieved": flops / (opt_ms * 1e-3) / 1e12, "peak": 78.6, "unit": "TFLOP/s",
-                     "frac": flops / (opt_ms * 1e-3) / 1e12 / 78.6, "traffic": None, "flops_per_call": flops},
+        "newton_schulz_ms": ns_ms / args.steps,
+        "roofline": {"bound": "fp64", "kernel": "Newton-Schulz polar iterations (k_gemm_jobs binary64 MFMA "
+                     "products with their step kernels; " + ("directions and retraction" if muon else "retraction") +
+                     f", {ns_regions // args.steps} per step)",
+                     "achieved": ns_flops / (ns_ms * 1e-3) / 1e12, "peak": 78.6, "unit": "TFLOP/s",
+                     "frac": ns_flops / (ns_ms * 1e-3) / 1e12 / 78.6, "traffic": None,
+                     "flops_per_call": ns_flops / args.steps},
     }
     if not args.no_cpu_baseline:
         spec = wl.tensors[0]

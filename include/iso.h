@@ -448,11 +448,17 @@ iso_status iso_read_fallback_count(const void* ws, void* stream, int32_t* count)
 /* Benchmark timing.  Between iso_profile_begin and iso_profile_end, every iso_update
  * FUSED call records a pair of HIP events on its stream around its main streaming kernel
  * (the single-read pass of the bf16 TIES path with inner selection, else the merge
- * kernel).  iso_profile_end waits for those events and returns the summed elapsed time in
- * milliseconds and the number of launches timed; the library keeps its events for reuse.
- * Calls on several host threads at once are timed too, in no particular order. */
+ * kernel), and iso_optimizer_step / iso_optimizer_step_muon record a pair around each of
+ * their Newton-Schulz polar iterations (the retraction; Muon's directions too).
+ * iso_profile_end waits for those events and returns the summed elapsed time in
+ * milliseconds and the number of regions timed; the library keeps its events for reuse.
+ * Calls on several host threads at once are timed too, in no particular order.
+ * iso_profile_flops returns the binary64 flops the timed polar iterations performed since
+ * iso_profile_begin: per job (frame side of rows x rank, m x q) and step taken, 2 m q^2 for
+ * the Gram X^T X (formed whole) and 2 m q^2 for the product X T (0 for the merge paths). */
 iso_status iso_profile_begin(void);
 iso_status iso_profile_end(double* total_ms, int32_t* launches);
+iso_status iso_profile_flops(double* flops);
 
 const char* iso_status_string(int s);
 

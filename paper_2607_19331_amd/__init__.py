@@ -284,6 +284,17 @@ def iso_profile_begin():
         raise IsoError(st, "iso_profile_begin")
 
 
+def iso_profile_flops():
+    """Binary64 flops the optimizer steps' timed Newton-Schulz iterations performed since
+    iso_profile_begin."""
+    import ctypes
+    f = ctypes.c_double(0.0)
+    st = _lib.load().iso_profile_flops(ctypes.byref(f))
+    if st != 0:
+        raise IsoError(st, "iso_profile_flops")
+    return f.value
+
+
 def iso_profile_end():
     """(total milliseconds, launches) of the main kernels timed since iso_profile_begin."""
     import ctypes

@@ -16,7 +16,7 @@ UPDATE_APPLY, UPDATE_FUSED, UPDATE_SPECTRAL, UPDATE_ORTHO = 0, 1, 2, 3
 
 SYMBOLS = ["iso_workspace_size", "iso_topk_mask", "iso_sign_elect", "iso_merge", "iso_update",
            "iso_blockdiag_project", "iso_blockdiag_project_factors", "iso_workspace_size_tsv", "iso_k_from_density", "iso_read_device_status",
-           "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end", "iso_status_string",
+           "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end", "iso_profile_flops", "iso_status_string",
            "iso_workspace_size_optimizer", "iso_optimizer_step", "iso_optimizer_step_muon", "iso_spectral_diagnostics",
            "iso_spectrum_interpolate", "iso_transport_ratios", "iso_spectral_error", "iso_update_noalloc"]
 
@@ -88,6 +88,7 @@ def load():
     L.iso_read_fallback_count.argtypes = [P, P, ctypes.POINTER(ctypes.c_int32)]
     L.iso_profile_begin.argtypes = []
     L.iso_profile_end.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32)]
+    L.iso_profile_flops.argtypes = [ctypes.POINTER(ctypes.c_double)]
     L.iso_workspace_size_optimizer.argtypes = [ctypes.POINTER(IsoFrame), I]
     L.iso_workspace_size_optimizer.restype = Z
     L.iso_optimizer_step.argtypes = [ctypes.POINTER(IsoFrame), I, I, ctypes.POINTER(IsoAdamW), P, Z, P]
@@ -103,7 +104,8 @@ def load():
                "iso_blockdiag_project_factors", "iso_optimizer_step", "iso_optimizer_step_muon",
                "iso_spectral_diagnostics",
                "iso_spectrum_interpolate", "iso_transport_ratios", "iso_spectral_error",
-               "iso_read_device_status", "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end"):
+               "iso_read_device_status", "iso_read_fallback_count", "iso_profile_begin", "iso_profile_end",
+               "iso_profile_flops"):
         getattr(L, fn).restype = I
     _lib = L
     return L

@@ -241,6 +241,7 @@ struct Profiler {
   bool on = false;
   std::vector<hipEvent_t> pool;   // 2 per call
   size_t used = 0;
+  double flops = 0.0;             // binary64 flops performed inside the timed regions
 };
 Profiler g_prof;
 
@@ -502,6 +503,13 @@ iso_status iso_update(const iso_tensor* t, int n_t, int K, int dt, const iso_upd
 }  // extern "C"
 
 namespace iso {
+
+void profile_region(hipEvent_t (&ev)[2]) { prof_take(ev); }
+
+void profile_add_flops(double flops) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (g_prof.on) g_prof.flops += flops;
+}
 
 // The body of iso_update.  Arguments are validated first; the workspace is then taken from src
 // (the caller's, or the fixed per-device block of iso_update_noalloc) once its size is known.
@@ -844,6 +852,14 @@ iso_status iso_profile_begin(void) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
   g_prof.on = true;
   g_prof.used = 0;
+  g_prof.flops = 0.0;
+  return ISO_OK;
+}
+
+iso_status iso_profile_flops(double* flops) {
+  if (flops == nullptr) return ISO_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  *flops = g_prof.flops;
   return ISO_OK;
 }
 

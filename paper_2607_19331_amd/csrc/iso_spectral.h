@@ -31,6 +31,10 @@ inline int64_t transport_rank(int64_t q, double frac) {
 // W_rec = deltas[0], or the reconstruction from the library's own SVD of the base).
 iso_status run_spectrum_ops(const iso_tensor* t, int n_t, iso_dtype dt, SpectrumOp op, double* out, double param,
                             const double* fracs, int n_frac, uint8_t* ws, uint32_t* status, hipStream_t s);
+// Benchmark timing hooks of the library (defined with iso_profile_begin): the next event pair
+// ({null, null} when profiling is off) and the flops performed inside a timed region.
+void profile_region(hipEvent_t (&ev)[2]);
+void profile_add_flops(double flops);
 // One ISO-Optimizer step with AdamW (adam != nullptr) or Muon (muon != nullptr) as the base rule.
 iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_adamw* adam, const iso_muon* muon,
                          uint8_t* ws, uint32_t* status, hipStream_t s);

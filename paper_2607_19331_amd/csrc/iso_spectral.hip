@@ -855,6 +855,28 @@ iso_status run_spectral(const iso_tensor* t, int n_t, int K, iso_dtype dt, const
   return ISO_OK;
 }
 
+// polar_batch over the frames' 2 n_f jobs (frame e's U side at 2 e, V side at 2 e + 1) inside a
+// profiling region, counting the binary64 flops its steps performed: per job of m x q and step
+// taken, 2 m q^2 for the Gram (formed whole) and 2 m q^2 for the product.
+hipError_t timed_polar(const Tables& tb, const iso_frame* f, int n_f, int64_t max_rows, int64_t max_q,
+                       std::vector<NsState>& hst, uint32_t* status, hipStream_t s, bool scaled) {
+  hipEvent_t ev[2];
+  profile_region(ev);
+  hipError_t e = hipSuccess;
+  if (ev[0] != nullptr && (e = hipEventRecord(ev[0], s)) != hipSuccess) return e;
+  if ((e = polar_batch(tb, 2 * n_f, max_rows, max_q, hst, status, s, scaled)) != hipSuccess) return e;
+  if (ev[1] != nullptr && (e = hipEventRecord(ev[1], s)) != hipSuccess) return e;
+  if (ev[0] != nullptr) {
+    double flops = 0.0;
+    for (int j = 0; j < 2 * n_f; ++j) {
+      const double m = (double)((j & 1) ? f[j / 2].cols : f[j / 2].rows), q = (double)f[j / 2].rank;
+      flops += (double)hst[j].steps * (4.0 * m * q * q);
+    }
+    profile_add_flops(flops);
+  }
+  return hipSuccess;
+}
+
 size_t optimizer_workspace_bytes(const iso_frame* f, int n_f) {
   Bump bp{nullptr};
   carve_opt_tables(bp, n_f);
@@ -930,7 +952,7 @@ iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_ad
   if (muon) {
     // o = polar(d) for every frame's two directions (far from orthonormal: the scaled iteration),
     // then the step and the tentative frames
-    OP_TRY(polar_batch(tb, 2 * n_f, max_rows, max_q, hst, status, s, true));
+    OP_TRY(timed_polar(tb, f, n_f, max_rows, max_q, hst, status, s, true));
     for (int e = 0; e < n_f; ++e) {
       const iso_frame& F = f[e];
       const int64_t m = F.rows, n = F.cols, q = F.rank;
@@ -946,7 +968,7 @@ iso_status run_optimizer(const iso_frame* f, int n_f, iso_dtype dt, const iso_ad
     }
   }
   // U+ = polar(U), V+ = polar(V)
-  OP_TRY(polar_batch(tb, 2 * n_f, max_rows, max_q, hst, status, s));
+  OP_TRY(timed_polar(tb, f, n_f, max_rows, max_q, hst, status, s, false));
   for (int e = 0; e < n_f; ++e) {
     const iso_frame& F = f[e];
     const int64_t m = F.rows, n = F.cols, q = F.rank;

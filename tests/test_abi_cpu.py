@@ -298,3 +298,13 @@ def test_orthomerge_validation():
     assert call([]) == _lib.OK
     es = [entry(rows=300, cols=128, k=10)]
     assert L.iso_workspace_size(iso.OP_UPDATE_ORTHO, iso._table(es), 1, 2, iso.BF16) > 0
+
+
+def test_profile_flops_counter_without_a_gpu():
+    """iso_profile_flops: a NULL output is refused; after iso_profile_begin the counter reads 0 and
+    iso_profile_end with nothing timed returns no regions (no HIP call is made)."""
+    L = _lib.load()
+    assert L.iso_profile_flops(None) == _lib.ERR_INVALID_ARG
+    iso.iso_profile_begin()
+    assert iso.iso_profile_flops() == 0.0
+    assert iso.iso_profile_end() == (0.0, 0)

@@ -158,8 +158,15 @@ def test_muon_zero_and_ill_conditioned_directions():
     ws = iso.optimizer_workspace(frames)
     hp = dict(lr=1e-3, momentum=0.9, weight_decay=0.01)
     for t in (1, 2):
+        iso.iso_profile_begin()
         iso.iso_optimizer_step_muon(frames, iso.F32, nesterov=True, ws=ws, **hp)
+        flops = iso.iso_profile_flops()
+        ms, regions = iso.iso_profile_end()
         assert iso.iso_read_device_status(ws) == 0
+        # two timed polar iterations (directions, retraction), every job at least one step of
+        # 4 m q^2 flops in each
+        unit = sum(4.0 * r * q * q for _, m, n, q in specs for r in (m, n))
+        assert regions == 2 and ms > 0.0 and flops >= 2 * unit
         for (kind, *_), F, R in zip(specs, frames, ref):
             R["u"], R["v"], w_ref, R["st"] = op.iso_muon_step(R["u"], R["v"], R["s"], R["g"], R["st"], hp["lr"],
                                                               hp["momentum"], hp["weight_decay"], True)
