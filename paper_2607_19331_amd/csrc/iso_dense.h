@@ -759,7 +759,7 @@ inline hipError_t jacobi_block(const JacobiJob* jobs, int njobs, int64_t max_r, 
 
 // Sorted thin factors from converged Jacobi jobs: left (r x c) = A's columns normalised, right
 // (c x c) = V, s (c), all permuted to nonincreasing s (equal norms keep their column order); zero
-// columns give zero vectors.  Three launches with one wave per column and blockIdx.y the job, so
+// columns give zero vectors; a null left pointer skips that job's left factor.  Three launches with one wave per column and blockIdx.y the job, so
 // that long columns are spread over the chip: the column norms into s (unsorted), the scatter of
 // every column to its rank (the norms staged in LDS), then s itself sorted by one workgroup per job.
 __global__ void __launch_bounds__(1024) k_svd_norms(const JacobiJob* __restrict__ jobs, double* const* sv) {
@@ -799,7 +799,8 @@ __global__ void __launch_bounds__(1024) k_svd_scatter(const JacobiJob* __restric
   const double inv = (nrm[j] > 0.0) ? 1.0 / nrm[j] : 0.0;
   double* L = left[blockIdx.y];
   double* R = right[blockIdx.y];
-  for (int64_t t = lane; t < r; t += 64) L[d * r + t] = J.a[j * r + t] * inv;
+  if (L != nullptr)
+    for (int64_t t = lane; t < r; t += 64) L[d * r + t] = J.a[j * r + t] * inv;
   for (int64_t t = lane; t < c; t += 64) R[d * c + t] = J.v[j * c + t];
 }
 
@@ -1028,6 +1029,114 @@ inline void gemm(int64_t M, int64_t N, int64_t Kd, double alpha, const double* A
   } else {
     k_gemm_one<2><<<dim3((unsigned)((M + 63) / 64), (unsigned)((N + 63) / 64)), 256, 0, s>>>(J);
   }
+}
+
+// One job with every field given (a sub-block product, the `upper` tiles).
+inline void gemm_job(const GemmJob& J, hipStream_t s) {
+  if (gemm_big(J.M, J.N)) {
+    k_gemm_one<4><<<dim3((unsigned)((J.M + 127) / 128), (unsigned)((J.N + 127) / 128)), 256, 0, s>>>(J);
+  } else {
+    k_gemm_one<2><<<dim3((unsigned)((J.M + 63) / 64), (unsigned)((J.N + 63) / 64)), 256, 0, s>>>(J);
+  }
+}
+
+// ---- Cholesky factor of a symmetric positive definite matrix ------------------------------------
+// G = R^T R with R upper triangular, G q x q col-major and only its upper triangle read, R written
+// over it (zeros below the diagonal).  Right-looking in 64-column panels: the diagonal block
+// factored in LDS by one workgroup, the panel's block row solved against it (one thread per
+// column), the trailing upper triangle updated on the MFMA GEMM.  A pivot that is not positive and
+// finite sets *fail (the factor is then zeroed, so that what follows stays finite).
+constexpr int kCholB = 64;
+
+__global__ void __launch_bounds__(256) k_chol_diag(double* __restrict__ g, int64_t q, int64_t kb, int nb,
+                                                   int* __restrict__ fail) {
+  __shared__ double a[kCholB][kCholB + 1];        // a[i][l] = G(kb + i, kb + l), i <= l
+  __shared__ int bad;
+  for (int e = threadIdx.x; e < nb * nb; e += blockDim.x) {
+    const int i = e % nb, l = e / nb;
+    a[i][l] = (i <= l) ? g[(kb + i) + (kb + l) * q] : 0.0;
+  }
+  if (threadIdx.x == 0) bad = 0;
+  __syncthreads();
+  for (int j = 0; j < nb; ++j) {
+    if (threadIdx.x == 0) {
+      double d = a[j][j];
+      if (!(d > 0.0) || !isfinite(d)) {
+        bad = 1;
+        d = 1.0;
+      }
+      a[j][j] = sqrt(d);
+    }
+    __syncthreads();
+    const double rjj = a[j][j];
+    for (int l = j + 1 + (int)threadIdx.x; l < nb; l += blockDim.x) a[j][l] /= rjj;
+    __syncthreads();
+    for (int e = threadIdx.x; e < nb * nb; e += blockDim.x) {
+      const int i = e % nb, l = e / nb;
+      if (i > j && i <= l) a[i][l] -= a[j][i] * a[j][l];
+    }
+    __syncthreads();
+  }
+  for (int e = threadIdx.x; e < nb * nb; e += blockDim.x) {
+    const int i = e % nb, l = e / nb;
+    g[(kb + i) + (kb + l) * q] = (i <= l) ? a[i][l] : 0.0;
+  }
+  if (threadIdx.x == 0 && bad) *fail = 1;
+}
+
+// Block row kb of R right of the diagonal block: R(kb:kb+nb, c) = R_kk^{-T} G(kb:kb+nb, c), forward
+// substitution with the column in registers.
+__global__ void __launch_bounds__(256) k_chol_panel(double* __restrict__ g, int64_t q, int64_t kb, int nb) {
+  __shared__ double rk[kCholB][kCholB + 1];
+  for (int e = threadIdx.x; e < kCholB * kCholB; e += blockDim.x) {
+    const int i = e % kCholB, l = e / kCholB;
+    rk[i][l] = (i < nb && l < nb && i <= l) ? g[(kb + i) + (kb + l) * q] : 0.0;
+  }
+  __syncthreads();
+  for (int64_t c = kb + nb + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < q;
+       c += (int64_t)gridDim.x * blockDim.x) {
+    double* col = g + kb + c * q;
+    double x[kCholB];
+#pragma unroll
+    for (int i = 0; i < kCholB; ++i) x[i] = (i < nb) ? col[i] : 0.0;
+#pragma unroll
+    for (int i = 0; i < kCholB; ++i) {
+      if (i < nb) {
+        double t = x[i];
+#pragma unroll
+        for (int l = 0; l < i; ++l) t -= rk[l][i] * x[l];
+        x[i] = t / rk[i][i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kCholB; ++i)
+      if (i < nb) col[i] = x[i];
+  }
+}
+
+__global__ void k_chol_finish(double* __restrict__ g, int64_t q, const int* __restrict__ fail) {
+  const bool zero = *fail != 0;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < q * q; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = e % q, j = e / q;
+    if (zero || i > j) g[e] = 0.0;
+  }
+}
+
+// In place on g (q x q col-major, upper triangle holding G); *fail must be 0 on entry.
+inline void cholesky_upper(double* g, int64_t q, int* fail, hipStream_t s) {
+  for (int64_t kb = 0; kb < q; kb += kCholB) {
+    const int nb = (int)std::min<int64_t>(kCholB, q - kb);
+    k_chol_diag<<<1, 256, 0, s>>>(g, q, kb, nb, fail);
+    const int64_t t0 = kb + nb, rem = q - t0;
+    if (rem <= 0) break;
+    k_chol_panel<<<(unsigned)((rem + 255) / 256), 256, 0, s>>>(g, q, kb, nb);
+    // G(t0:, t0:) -= R(kb:kb+nb, t0:)^T R(kb:kb+nb, t0:), tiles on and above the diagonal
+    const double* rp = g + kb + t0 * q;
+    const GemmJob J{rp, rp, g + t0 + t0 * q, q, 1, 1, q, 1, q, rem, rem, nb, -1.0, 1.0, 1, nullptr};
+    gemm_job(J, s);
+  }
+  const int64_t n = q * q;
+  k_chol_finish<<<(unsigned)std::max<int64_t>(1, std::min<int64_t>((n + 255) / 256, 4096)), 256, 0, s>>>(g, q, fail);
 }
 
 }  // namespace

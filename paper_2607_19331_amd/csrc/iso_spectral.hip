@@ -96,6 +96,30 @@ __global__ void k_scale_cols(double* __restrict__ out, const double* __restrict_
     out[e] = x[e] * s[e / r];
 }
 
+// X[:, j] /= s[j] (a zero s gives a zero column), X r x q col-major.
+__global__ void k_unit_cols(double* __restrict__ x, const double* __restrict__ s, int64_t r, int64_t q) {
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < r * q; e += (int64_t)gridDim.x * blockDim.x) {
+    const double d = s[e / r];
+    x[e] = (d > 0.0) ? x[e] / d : 0.0;
+  }
+}
+
+// Tall matrices whose SVDs came from R: singular values from the Gram carry a relative error of
+// about eps (s_max / s_j)^2 / 2, so a matrix with any factor that failed, or with a condition
+// number above kQrMaxCond (error bound ~6e-11), is marked for plain Jacobi on A.
+constexpr double kQrMaxCond = 1e3;
+
+__global__ void k_qr_guard(const JacobiJob* __restrict__ jobs, double* const* sv, const int* __restrict__ fail,
+                           const int* __restrict__ jmat, int njobs, int* __restrict__ bad) {
+  for (int j = threadIdx.x; j < njobs; j += blockDim.x) {
+    if (jmat[j] < 0) continue;
+    const double* S = sv[j];
+    const int64_t q = jobs[j].c;
+    const bool ok = fail[j] == 0 && S[q - 1] > 0.0 && S[0] <= kQrMaxCond * S[q - 1];
+    if (!ok) atomicOr(&bad[jmat[j]], 1);
+  }
+}
+
 // ---- long reductions: many workgroups, fixed summation order ---------------------------------------
 // Slot y of a DotSet sums f(a_y[e], b_y[e]) over len entries, f = a b (diff = 0) or (a - b)^2
 // (diff = 1): kRedChunks workgroups per slot each sum one contiguous chunk into part, then one wave
@@ -358,16 +382,25 @@ struct Bump {
 // Device blocks of one matrix; the same sequence of take() calls sizes the workspace.
 struct Bufs {
   double *ja[ISO_MAX_K + 1], *jv[ISO_MAX_K + 1], *U[ISO_MAX_K + 1], *V[ISO_MAX_K + 1], *S[ISO_MAX_K + 1];
+  double* jr[ISO_MAX_K + 1];  // tall matrices: the q x q Cholesky factor R of A^T A (the Jacobi matrix)
   double *XU, *XV, *P, *Sq, *FU, *FV, *G, *gram, *coef, *AU, *AV, *Wst;
   double* red;                // partial sums of the long reductions (kRedSlots x kRedChunks)
   double *PX[2][2], *PG[2];   // polar of U_0 + xi_U (m x q) and of V_0 + xi_V (n x q): the two buffers
                               // of the iterate X, the q x q Gram / step matrix
 };
 
+// A matrix whose Jacobi runs on the Cholesky factor of A^T A instead of on A: tall enough that the
+// q x q factor moves far fewer bytes per round than the r x q A.
+bool qr_pre(int64_t m, int64_t n) {
+  const int64_t q = std::min(m, n), r = std::max(m, n);
+  return r >= 2 * q && r >= 1024;
+}
+
 Bufs carve(Bump& bp, int64_t m, int64_t n, int K) {
   const int64_t q = std::min(m, n), r = std::max(m, n);
   Bufs b;
   for (int i = 0; i <= K; ++i) {
+    b.jr[i] = qr_pre(m, n) ? bp.take(q * q) : nullptr;
     b.ja[i] = bp.take(r * q);
     b.jv[i] = bp.take(q * q);
     b.U[i] = bp.take(m * q);
@@ -408,6 +441,9 @@ struct Tables {
   NsState* nst;
   GemmJob* ngj[4];   // [2 p]: G = X_p^T X_p, [2 p + 1]: X_{1-p} = X_p T
   GemmJob* wgj;      // warm start of the expert SVDs: A_i V_0
+  int* qfail;        // per SVD: its Cholesky factor failed (tall matrices)
+  int* qmat;         // per SVD: its matrix's index in the batch if the Jacobi ran on R, else -1
+  int* qbad;         // per matrix: its SVDs go to plain Jacobi on A
 };
 
 Tables carve_tables(Bump& bp, int nm, int K) {
@@ -419,6 +455,9 @@ Tables carve_tables(Bump& bp, int nm, int K) {
   tb.nst = bp.take<NsState>(2 * nm);
   for (int k = 0; k < 4; ++k) tb.ngj[k] = bp.take<GemmJob>(2 * nm);
   tb.wgj = bp.take<GemmJob>((int64_t)nm * K);
+  tb.qfail = bp.take<int>((int64_t)nm * (K + 1));
+  tb.qmat = bp.take<int>((int64_t)nm * (K + 1));
+  tb.qbad = bp.take<int>(nm);
   return tb;
 }
 
@@ -565,22 +604,30 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
   GemmJob* hg[4];
   for (int k = 0; k < 4; ++k) hg[k] = (GemmJob*)at(tb.ngj[k]);
   GemmJob* hw = (GemmJob*)at(tb.wgj);
+  int* hqm = (int*)at(tb.qmat);
   int64_t svd_r = 1, svd_c = 1;
+  std::vector<char> pre(nm);
   for (int e = 0; e < nm; ++e) {
     const int64_t m = t[ids[e]].rows, n = t[ids[e]].cols, q = std::min(m, n), r = std::max(m, n);
     const bool wide = m < n;
     const Bufs& b = bs[e];
+    pre[e] = qr_pre(m, n);
+    // a tall matrix's Jacobi runs on R (q x q, R^T R = A^T A): the same V and singular values, its
+    // left factor formed afterwards as A V S^{-1}
+    const int64_t jr_rows = pre[e] ? q : r;
     for (int i = 0; i <= K; ++i) {
       const int j = i ? nm + e * K + i - 1 : e;
-      hj[j] = JacobiJob{b.ja[i], b.jv[i], r, q};
-      hp[j] = wide ? b.V[i] : b.U[i];                 // left factor of the Jacobi matrix
-      hp[nsvd + j] = wide ? b.U[i] : b.V[i];          // right factor
+      hj[j] = JacobiJob{pre[e] ? b.jr[i] : b.ja[i], b.jv[i], jr_rows, q};
+      hp[j] = pre[e] ? nullptr : (wide ? b.V[i] : b.U[i]);   // left factor of the Jacobi matrix
+      hp[nsvd + j] = wide ? b.U[i] : b.V[i];                  // right factor
       hp[2 * nsvd + j] = b.S[i];
+      hqm[j] = pre[e] ? e : -1;
     }
     // A_i V_0 as (A_0 V_0) + T_i V_0 (r x q), the first term the base's converged Jacobi matrix,
-    // T_i (tau_i or its transpose) staged in the proxy buffer
+    // T_i (tau_i or its transpose) staged in the proxy buffer; on R: R_0 V_0 + (R_i - R_0) V_0
     for (int i = 1; i <= K; ++i)
-      hw[e * K + i - 1] = GemmJob{b.G + (int64_t)(i - 1) * m * n, b.jv[0], b.ja[i], 1, r, 1, q, 1, r, r, q, q, 1.0, 1.0};
+      hw[e * K + i - 1] = GemmJob{b.G + (int64_t)(i - 1) * (pre[e] ? q * q : m * n), b.jv[0],
+                                  pre[e] ? b.jr[i] : b.ja[i], 1, jr_rows, 1, q, 1, jr_rows, jr_rows, q, q, 1.0, 1.0};
     for (int h = 0; h < 2; ++h) {
       const int pj = 2 * e + h;
       const int64_t rows = h ? n : m;
@@ -595,7 +642,7 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
         hg[2 * p + 1][pj] = GemmJob{X, b.PG[h], Y, 1, rows, 1, q, 1, rows, rows, q, q, 1.0, 0.0, 0, skip};
       }
     }
-    svd_r = std::max(svd_r, r);
+    svd_r = std::max(svd_r, jr_rows);
     svd_c = std::max(svd_c, q);
   }
   SP_TRY(hipMemcpyAsync(ws, host.data(), tables_end, hipMemcpyHostToDevice, s));
@@ -609,10 +656,12 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
   int64_t width = 0, per_cu = 0, wgs = 0;
   jacobi_block_shape(svd_r, svd_c, &width, &per_cu);
   for (int e = 0; e < nm; ++e) {
-    const int64_t nb = (std::min(t[ids[e]].rows, t[ids[e]].cols) + width - 1) / width;
+    const int64_t q = std::min(t[ids[e]].rows, t[ids[e]].cols);
+    const int64_t nb = (q + width - 1) / width;
     // the Gram step splits each block pair's rows over workgroups of gram_slice_rows rows
     const int64_t sl = gram_slice_rows(svd_r);
-    const int64_t slices = width == kGW ? (std::max(t[ids[e]].rows, t[ids[e]].cols) + sl - 1) / sl : 1;
+    const int64_t rows = pre[e] ? q : std::max(t[ids[e]].rows, t[ids[e]].cols);
+    const int64_t slices = width == kGW ? (rows + sl - 1) / sl : 1;
     wgs += (int64_t)(K + 1) * ((nb + 1) / 2) * slices;
   }
   int dev = 0, cus = 0;
@@ -621,9 +670,25 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
   const bool warm = wgs > per_cu * (int64_t)cus;
   for (int e = 0; e < nm; ++e) {
     const iso_tensor& x = t[ids[e]];
-    for (int i = 0; i <= (warm ? 0 : K); ++i)
+    for (int i = 0; i <= ((warm && !pre[e]) ? 0 : K); ++i)
       k_load_f64<<<grid_for(x.rows * x.cols), 256, 0, s>>>(bs[e].ja[i], x.base, i ? x.deltas[i - 1] : nullptr, x.rows,
                                                            x.cols, x.rows < x.cols ? 1 : 0, dt);
+  }
+  // tall matrices: R_i from the Gram A_i^T A_i (its upper triangle), then, for the warm start,
+  // R_i - R_0 in the proxy buffer
+  for (int e = 0; e < nm; ++e) {
+    if (!pre[e]) continue;
+    const iso_tensor& x = t[ids[e]];
+    const int64_t q = std::min(x.rows, x.cols), r = std::max(x.rows, x.cols);
+    const Bufs& b = bs[e];
+    for (int i = 0; i <= K; ++i) {
+      const int j = i ? nm + e * K + i - 1 : e;
+      gemm_job(GemmJob{b.ja[i], b.ja[i], b.jr[i], r, 1, 1, r, 1, q, q, q, r, 1.0, 0.0, 1, nullptr}, s);
+      cholesky_upper(b.jr[i], q, tb.qfail + j, s);
+    }
+    if (warm)
+      for (int i = 1; i <= K; ++i)
+        k_sub<<<grid_for(q * q), 256, 0, s>>>(b.G + (int64_t)(i - 1) * q * q, b.jr[i], b.jr[0], q * q);
   }
   if (!warm) {
     SP_TRY(jacobi_block(tb.jobs, nsvd, svd_r, svd_c, tb.jst, status, s, false, split));
@@ -633,10 +698,14 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
       const iso_tensor& x = t[ids[e]];
       const int64_t q = std::min(x.rows, x.cols);
       for (int i = 1; i <= K; ++i) {
-        k_load_f64<<<grid_for(x.rows * x.cols), 256, 0, s>>>(bs[e].G + (int64_t)(i - 1) * x.rows * x.cols,
-                                                             x.deltas[i - 1], nullptr, x.rows, x.cols,
-                                                             x.rows < x.cols ? 1 : 0, dt);
-        k_copy<<<grid_for(x.rows * x.cols), 256, 0, s>>>(bs[e].ja[i], bs[e].ja[0], x.rows * x.cols);
+        if (pre[e]) {
+          k_copy<<<grid_for(q * q), 256, 0, s>>>(bs[e].jr[i], bs[e].jr[0], q * q);
+        } else {
+          k_load_f64<<<grid_for(x.rows * x.cols), 256, 0, s>>>(bs[e].G + (int64_t)(i - 1) * x.rows * x.cols,
+                                                               x.deltas[i - 1], nullptr, x.rows, x.cols,
+                                                               x.rows < x.cols ? 1 : 0, dt);
+          k_copy<<<grid_for(x.rows * x.cols), 256, 0, s>>>(bs[e].ja[i], bs[e].ja[0], x.rows * x.cols);
+        }
         k_copy<<<grid_for(q * q), 256, 0, s>>>(bs[e].jv[i], bs[e].jv[0], q * q);
       }
     }
@@ -644,6 +713,56 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
     SP_TRY(jacobi_block(tb.jobs + nm, nm * K, svd_r, svd_c, tb.jst + nm, status, s, true, split));
   }
   svd_finalize(tb.jobs, tb.ptrs, tb.ptrs + nsvd, tb.ptrs + 2 * nsvd, nsvd, svd_c, s);
+  // tall matrices: left factor A_i V_i S_i^{-1}; a matrix whose factors fail the guard goes to
+  // plain Jacobi on A (its A_i are still in the Jacobi buffers)
+  bool any_pre = false;
+  for (int e = 0; e < nm; ++e) {
+    if (!pre[e]) continue;
+    any_pre = true;
+    const int64_t m = t[ids[e]].rows, n = t[ids[e]].cols, q = std::min(m, n), r = std::max(m, n);
+    const bool wide = m < n;
+    const Bufs& b = bs[e];
+    for (int i = 0; i <= K; ++i) {
+      double* L = wide ? b.V[i] : b.U[i];
+      const double* Vs = wide ? b.U[i] : b.V[i];
+      gemm(r, q, q, 1.0, b.ja[i], 1, r, Vs, 1, q, 0.0, L, 1, r, s);
+      k_unit_cols<<<grid_for(r * q), 256, 0, s>>>(L, b.S[i], r, q);
+    }
+  }
+  if (any_pre) {
+    k_qr_guard<<<1, 256, 0, s>>>(tb.jobs, tb.ptrs + 2 * nsvd, tb.qfail, tb.qmat, nsvd, tb.qbad);
+    std::vector<int> bad(nm, 0);
+    SP_TRY(hipMemcpyAsync(bad.data(), tb.qbad, sizeof(int) * nm, hipMemcpyDeviceToHost, s));
+    SP_TRY(hipStreamSynchronize(s));
+    std::vector<int> redo;
+    for (int e = 0; e < nm; ++e)
+      if (bad[e]) redo.push_back(e);
+    if (!redo.empty()) {
+      // the Jacobi job table and pointers are free again (the stream has drained; the host image
+      // still holds the polar and warm-start tables, which go up unchanged): the redone matrices'
+      // SVDs as one plain job set on A from the identity
+      const int nr = (int)redo.size() * (K + 1);
+      int64_t rr = 1, rq = 1;
+      for (int x = 0; x < (int)redo.size(); ++x) {
+        const int e = redo[x];
+        const int64_t m = t[ids[e]].rows, n = t[ids[e]].cols, q = std::min(m, n), r = std::max(m, n);
+        const bool wide = m < n;
+        const Bufs& b = bs[e];
+        for (int i = 0; i <= K; ++i) {
+          const int j = x * (K + 1) + i;
+          hj[j] = JacobiJob{b.ja[i], b.jv[i], r, q};
+          hp[j] = wide ? b.V[i] : b.U[i];
+          hp[nr + j] = wide ? b.U[i] : b.V[i];
+          hp[2 * nr + j] = b.S[i];
+        }
+        rr = std::max(rr, r);
+        rq = std::max(rq, q);
+      }
+      SP_TRY(hipMemcpyAsync(ws, host.data(), tables_end, hipMemcpyHostToDevice, s));
+      SP_TRY(jacobi_block(tb.jobs, nr, rr, rq, tb.jst, status, s, false, split));
+      svd_finalize(tb.jobs, tb.ptrs, tb.ptrs + nr, tb.ptrs + 2 * nr, nr, rq, s);
+    }
+  }
   // 2 - 6 per matrix; the polar arguments go to the first iterate buffers
   for (int e = 0; e < nm; ++e) {
     const int64_t m = t[ids[e]].rows, n = t[ids[e]].cols, q = std::min(m, n);
@@ -654,7 +773,8 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
   }
   // 6'. U_* = polar(U_0 + xi_U*), V_* = polar(V_0 + xi_V*)
   std::vector<NsState> hst;
-  SP_TRY(polar_batch(tb, npol, svd_r, svd_c, hst, status, s));
+  // (the frames have max(rows, cols) rows: split_r, not the Jacobi matrices' svd_r)
+  SP_TRY(polar_batch(tb, npol, split_r, svd_c, hst, status, s));
   for (int e = 0; e < nm; ++e) {
     const iso_tensor& x = t[ids[e]];
     const int64_t m = x.rows, n = x.cols, q = std::min(m, n);

@@ -240,3 +240,48 @@ def test_sign_zero_inner_product():
     got = outs[0].astype(np.float64).reshape(m, n)
     for wrong in (cand(0.0), cand(-1.0)):
         assert np.max(np.abs(got - wrong["w_star"])) > 0.1
+
+
+def test_tall_matrices_on_the_cholesky_factor():
+    """Tall and wide matrices (longer side >= 1024 and >= twice the shorter) run their Jacobi on the
+    Cholesky factor R of A^T A and form U as A V S^{-1}; one call with two of them (fp32 tall
+    2048 x 256, and 200 x 1100 with 64-column panels and a ragged last panel) beside a square one,
+    K = 3, against the oracle to the usual bars."""
+    rng = np.random.default_rng(77)
+    K = 3
+    units = [_unit(rng, 2048, 256, K, "f32"), _unit(rng, 200, 1100, K, "f32"), _unit(rng, 160, 160, K, "f32")]
+    say("spectral cholesky-preconditioned batch: 2048x256, 200x1100, 160x160, K=3")
+    outs, coef, st = run_spectral(units, K, "f32")
+    assert st == 0
+    for u, o, c in zip(units, outs, coef):
+        ref = _ref(u, K, "f32")
+        assert _close(o, "f32", ref["w_star"]), (u.rows, u.cols)
+        assert np.allclose(c, ref["c"], rtol=1e-9, atol=1e-12), (u.rows, u.cols)
+
+
+def test_ill_conditioned_tall_matrix_falls_back_to_plain_jacobi():
+    """A tall fp32 base with singular values from 1 down to 1e-5: the Gram route would lose up to
+    eps cond^2 of its small singular values, so the guard (condition number above 1e3) sends that
+    matrix back to plain Jacobi on A, while a well-conditioned tall matrix of the same call keeps
+    the Cholesky route; both against the oracle to the usual bars."""
+    rng = np.random.default_rng(78)
+    K = 2
+    m, n = 1536, 128
+    p, _ = np.linalg.qr(rng.standard_normal((m, n)))
+    qq, _ = np.linalg.qr(rng.standard_normal((n, n)))
+    w0 = (p * np.logspace(0, -5, n)) @ qq.T * 0.05
+    ds = []
+    for _ in range(K):
+        v = rng.standard_normal(m * n) * 1e-4
+        v[rng.random(m * n) > 0.3] = 0.0
+        ds.append(nm.from_f64(v, "f32"))
+    bad = Unit(m, n, nm.from_f64(w0.ravel(), "f32"), ds, "f32")
+    good = _unit(rng, 1280, 96, K, "f32")
+    s = np.linalg.svd(nm.to_f64(bad.base, "f32").reshape(m, n), compute_uv=False)
+    say(f"spectral ill-conditioned tall {m}x{n} (cond {s[0] / s[-1]:.1e}) beside a well-conditioned 1280x96, K={K}")
+    outs, coef, st = run_spectral([bad, good], K, "f32")
+    assert st == 0
+    for u, o, c in zip((bad, good), outs, coef):
+        ref = _ref(u, K, "f32")
+        assert _close(o, "f32", ref["w_star"]), (u.rows, u.cols)
+        assert np.allclose(c, ref["c"], rtol=1e-9, atol=1e-12), (u.rows, u.cols)
