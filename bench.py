@@ -124,10 +124,11 @@ def cpu_baseline(name, workers):
 
 
 def svd_flops(m, n):
-    """Golub & Van Loan's operation count for an SVD with both factors (m >= n):
-    4 m^2 n + 8 m n^2 + 9 n^3."""
+    """Golub & Van Loan's operation count for the thin SVD with both factors (m >= n; U is m x n,
+    as Algorithm 1 uses it): the cheaper of Golub-Reinsch, 14 m n^2 + 8 n^3, and R-SVD,
+    6 m n^2 + 20 n^3."""
     m, n = max(m, n), min(m, n)
-    return 4 * m * m * n + 8 * m * n * n + 9 * n ** 3
+    return min(14 * m * n * n + 8 * n ** 3, 6 * m * n * n + 20 * n ** 3)
 
 
 def bench_tiny(args, iso, synth, torch):
