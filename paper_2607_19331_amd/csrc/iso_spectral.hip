@@ -263,6 +263,9 @@ __global__ void k_combine(double* __restrict__ out, const double* __restrict__ x
 struct NsJob {
   double* g;        // q x q: X^T X, then the step matrix T in place
   int64_t q;
+  double* t;        // q-space iteration (see polar_gram_batch): T goes here, G is kept; else null
+  double* pp[2];    // q-space iteration: the accumulated P_k, ping-pong
+  int gs;           // 1: a q-space job (the X-form batch skips it), 0: an X-form job
 };
 
 struct NsState {
@@ -281,9 +284,19 @@ constexpr int kNsMaxSteps = 48;
 constexpr int kNsCheckSteps = 4;   // steps queued between host reads of the done flags
 constexpr double kNsScaledL0 = 1e-6;
 
-__global__ void k_ns_begin(NsState* st, int njobs) {
+// gs_run: the batch runs the jobs with NsJob::gs equal to it; the others start (and stay) done
+__global__ void k_ns_begin(const NsJob* __restrict__ jobs, NsState* st, int njobs, int gs_run) {
   for (int j = threadIdx.x; j < njobs; j += blockDim.x)
-    st[j] = NsState{0ull, 0ull, 0, 0, 0, 0, kNsScaledL0, kNsScaledL0};
+    st[j] = NsState{0ull, 0ull, jobs[j].gs != gs_run ? 1 : 0, 0, 0, 0, kNsScaledL0, kNsScaledL0};
+}
+
+// q-space jobs: P_0 = I
+__global__ void k_ns_eye(const NsJob* __restrict__ jobs, const NsState* st) {
+  const int job = blockIdx.y;
+  if (st[job].done) return;
+  const NsJob J = jobs[job];
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < J.q * J.q; e += (int64_t)gridDim.x * blockDim.x)
+    J.pp[0][e] = ((e % J.q) == (e / J.q)) ? 1.0 : 0.0;
 }
 
 __global__ void k_ns_reset(NsState* st, int njobs) {
@@ -316,7 +329,8 @@ __global__ void __launch_bounds__(256) k_ns_stats(const NsJob* __restrict__ jobs
   }
 }
 
-// G <- T = (3 I - G / c) / (2 sqrt c), c the scale on the first step and 1 after it; with
+// G <- T = (3 I - G / c) / (2 sqrt c) (into J.t instead for a q-space job), c the scale on the first
+// step and 1 after it; with
 // `scaled`, T = a (3 I - a^2 G / c) / (2 sqrt c) with a from the job's lower bound (a = 1 on the
 // last step).
 __global__ void k_ns_form(const NsJob* __restrict__ jobs, NsState* st, int scaled) {
@@ -344,7 +358,7 @@ __global__ void k_ns_form(const NsJob* __restrict__ jobs, NsState* st, int scale
   const int64_t n = J.q * J.q;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
     const int64_t i = e % J.q, j = e / J.q;
-    J.g[e] = zero ? 0.0 : ((i == j ? 3.0 : 0.0) - J.g[e] * (a2 * ic)) * (0.5 * a * is);
+    (J.t != nullptr ? J.t : J.g)[e] = zero ? 0.0 : ((i == j ? 3.0 : 0.0) - J.g[e] * (a2 * ic)) * (0.5 * a * is);
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     st[job].last = last;
@@ -387,6 +401,7 @@ struct Bufs {
   double* red;                // partial sums of the long reductions (kRedSlots x kRedChunks)
   double *PX[2][2], *PG[2];   // polar of U_0 + xi_U (m x q) and of V_0 + xi_V (n x q): the two buffers
                               // of the iterate X, the q x q Gram / step matrix
+  double *QT, *QH, *QP[2];    // the tall side's polar in q space (qr_pre matrices): T, G T, P_k
 };
 
 // A matrix whose Jacobi runs on the Cholesky factor of A^T A instead of on A: tall enough that the
@@ -426,6 +441,13 @@ Bufs carve(Bump& bp, int64_t m, int64_t n, int K) {
     b.PG[h] = bp.take(q * q);
   }
   b.Wst = bp.take(m * n);
+  b.QT = b.QH = b.QP[0] = b.QP[1] = nullptr;
+  if (qr_pre(m, n)) {
+    b.QT = bp.take(q * q);
+    b.QH = bp.take(q * q);
+    b.QP[0] = bp.take(q * q);
+    b.QP[1] = bp.take(q * q);
+  }
   return b;
 }
 
@@ -441,6 +463,7 @@ struct Tables {
   NsState* nst;
   GemmJob* ngj[4];   // [2 p]: G = X_p^T X_p, [2 p + 1]: X_{1-p} = X_p T
   GemmJob* wgj;      // warm start of the expert SVDs: A_i V_0
+  GemmJob* qgj[5];   // q-space polar: G_0 = X_0^T X_0, H = G T, G = T H, P_1 = P_0 T, P_0 = P_1 T
   int* qfail;        // per SVD: its Cholesky factor failed (tall matrices)
   int* qmat;         // per SVD: its matrix's index in the batch if the Jacobi ran on R, else -1
   int* qbad;         // per matrix: its SVDs go to plain Jacobi on A
@@ -455,6 +478,7 @@ Tables carve_tables(Bump& bp, int nm, int K) {
   tb.nst = bp.take<NsState>(2 * nm);
   for (int k = 0; k < 4; ++k) tb.ngj[k] = bp.take<GemmJob>(2 * nm);
   tb.wgj = bp.take<GemmJob>((int64_t)nm * K);
+  for (int k = 0; k < 5; ++k) tb.qgj[k] = bp.take<GemmJob>(2 * nm);
   tb.qfail = bp.take<int>((int64_t)nm * (K + 1));
   tb.qmat = bp.take<int>((int64_t)nm * (K + 1));
   tb.qbad = bp.take<int>(nm);
@@ -550,7 +574,7 @@ hipError_t polar_batch(const Tables& tb, int njobs, int64_t max_rows, int64_t ma
                        uint32_t* status, hipStream_t s, bool scaled = false) {
   const unsigned cb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_q + 3) / 4, 1024));
   const unsigned fb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_q * max_q + 255) / 256, 2048));
-  k_ns_begin<<<1, 256, 0, s>>>(tb.nst, njobs);
+  k_ns_begin<<<1, 256, 0, s>>>(tb.ns, tb.nst, njobs, 0);
   hst.assign(njobs, NsState{});
   for (int step = 0; step < kNsMaxSteps;) {
     for (int b = 0; b < kNsCheckSteps && step < kNsMaxSteps; ++b, ++step) {
@@ -560,6 +584,44 @@ hipError_t polar_batch(const Tables& tb, int njobs, int64_t max_rows, int64_t ma
       k_ns_stats<<<dim3(cb, (unsigned)njobs), 256, 0, s>>>(tb.ns, tb.nst);
       k_ns_form<<<dim3(fb, (unsigned)njobs), 256, 0, s>>>(tb.ns, tb.nst, scaled ? 1 : 0);
       gemm_jobs(tb.ngj[2 * p + 1], njobs, max_rows, max_q, s);
+      k_ns_step_end<<<1, 256, 0, s>>>(tb.nst, njobs);
+    }
+    hipError_t e = hipMemcpyAsync(hst.data(), tb.nst, sizeof(NsState) * njobs, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return e;
+    bool all = true;
+    for (int j = 0; j < njobs; ++j) all = all && hst[j].done;
+    if (all) return hipGetLastError();
+  }
+  k_ns_check<<<1, 256, 0, s>>>(tb.nst, njobs, status);
+  return hipGetLastError();
+}
+
+// The same Newton-Schulz iteration for the jobs with NsJob::gs set, carried in q space: with
+// X_k = X_0 P_k, the Gram G_k = X_k^T X_k and the step matrix T_k (a polynomial in G_k) give
+// G_{k+1} = T_k G_k T_k and P_{k+1} = P_k T_k, three q x q products per step instead of two
+// rows x q ones, then X = X_0 P once.  The same steps, statistics and stopping test as the X form;
+// the Gram is not re-formed from an iterate, so rounding drifts by a few units of eps cond(G_0)
+// per step, negligible for the near-orthonormal retraction arguments (X^T X = I + xi^T xi) it
+// serves.  On return hst holds every job's state; the result is X_0 P in the job's P buffer
+// (steps & 1), formed by the caller.
+hipError_t polar_gram_batch(const Tables& tb, int njobs, int64_t max_q, std::vector<NsState>& hst, uint32_t* status,
+                            hipStream_t s) {
+  const unsigned cb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_q + 3) / 4, 1024));
+  const unsigned fb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_q * max_q + 255) / 256, 2048));
+  k_ns_begin<<<1, 256, 0, s>>>(tb.ns, tb.nst, njobs, 1);
+  k_ns_eye<<<dim3(fb, (unsigned)njobs), 256, 0, s>>>(tb.ns, tb.nst);
+  gemm_jobs(tb.qgj[0], njobs, max_q, max_q, s);
+  hst.assign(njobs, NsState{});
+  for (int step = 0; step < kNsMaxSteps;) {
+    for (int b = 0; b < kNsCheckSteps && step < kNsMaxSteps; ++b, ++step) {
+      const int p = step & 1;
+      k_ns_reset<<<1, 256, 0, s>>>(tb.nst, njobs);
+      k_ns_stats<<<dim3(cb, (unsigned)njobs), 256, 0, s>>>(tb.ns, tb.nst);
+      k_ns_form<<<dim3(fb, (unsigned)njobs), 256, 0, s>>>(tb.ns, tb.nst, 0);
+      gemm_jobs(tb.qgj[1], njobs, max_q, max_q, s);
+      gemm_jobs(tb.qgj[2], njobs, max_q, max_q, s);
+      gemm_jobs(tb.qgj[3 + p], njobs, max_q, max_q, s);
       k_ns_step_end<<<1, 256, 0, s>>>(tb.nst, njobs);
     }
     hipError_t e = hipMemcpyAsync(hst.data(), tb.nst, sizeof(NsState) * njobs, hipMemcpyDeviceToHost, s);
@@ -604,6 +666,8 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
   GemmJob* hg[4];
   for (int k = 0; k < 4; ++k) hg[k] = (GemmJob*)at(tb.ngj[k]);
   GemmJob* hw = (GemmJob*)at(tb.wgj);
+  GemmJob* hq[5];
+  for (int k = 0; k < 5; ++k) hq[k] = (GemmJob*)at(tb.qgj[k]);
   int* hqm = (int*)at(tb.qmat);
   int64_t svd_r = 1, svd_c = 1;
   std::vector<char> pre(nm);
@@ -632,7 +696,16 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
       const int pj = 2 * e + h;
       const int64_t rows = h ? n : m;
       const int* skip = &tb.nst[pj].done;
-      hn[pj] = NsJob{b.PG[h], q};
+      // the tall side of a tall matrix iterates in q space
+      const bool gs = pre[e] && rows > q;
+      hn[pj] = gs ? NsJob{b.PG[h], q, b.QT, {b.QP[0], b.QP[1]}, 1} : NsJob{b.PG[h], q};
+      if (gs) {
+        hq[0][pj] = GemmJob{b.PX[h][0], b.PX[h][0], b.PG[h], rows, 1, 1, rows, 1, q, q, q, rows, 1.0, 0.0, 0, skip};
+        hq[1][pj] = GemmJob{b.PG[h], b.QT, b.QH, 1, q, 1, q, 1, q, q, q, q, 1.0, 0.0, 0, skip};
+        hq[2][pj] = GemmJob{b.QT, b.QH, b.PG[h], 1, q, 1, q, 1, q, q, q, q, 1.0, 0.0, 0, skip};
+        hq[3][pj] = GemmJob{b.QP[0], b.QT, b.QP[1], 1, q, 1, q, 1, q, q, q, q, 1.0, 0.0, 0, skip};
+        hq[4][pj] = GemmJob{b.QP[1], b.QT, b.QP[0], 1, q, 1, q, 1, q, q, q, q, 1.0, 0.0, 0, skip};
+      }
       for (int p = 0; p < 2; ++p) {
         const double* X = b.PX[h][p];
         double* Y = b.PX[h][1 - p];
@@ -772,15 +845,31 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
     k_copy<<<grid_for(n * q), 256, 0, s>>>(b.PX[1][0], b.AV, n * q);
   }
   // 6'. U_* = polar(U_0 + xi_U*), V_* = polar(V_0 + xi_V*)
-  std::vector<NsState> hst;
+  //     the tall side of a tall matrix in q space (then X_0 P into the second iterate buffer),
+  //     the others in X form
+  std::vector<NsState> hst, hsq;
+  bool any_gs = false;
+  for (int e = 0; e < nm; ++e) any_gs = any_gs || pre[e];
   // (the frames have max(rows, cols) rows: split_r, not the Jacobi matrices' svd_r)
   SP_TRY(polar_batch(tb, npol, split_r, svd_c, hst, status, s));
+  if (any_gs) {
+    SP_TRY(polar_gram_batch(tb, npol, svd_c, hsq, status, s));
+    for (int e = 0; e < nm; ++e) {
+      if (!pre[e]) continue;
+      const int64_t m = t[ids[e]].rows, n = t[ids[e]].cols, q = std::min(m, n);
+      const int h = m > n ? 0 : 1;
+      const int64_t rows = h ? n : m;
+      const Bufs& b = bs[e];
+      gemm(rows, q, q, 1.0, b.PX[h][0], 1, rows, b.QP[hsq[2 * e + h].steps & 1], 1, q, 0.0, b.PX[h][1], 1, rows, s);
+    }
+  }
   for (int e = 0; e < nm; ++e) {
     const iso_tensor& x = t[ids[e]];
     const int64_t m = x.rows, n = x.cols, q = std::min(m, n);
     const Bufs& b = bs[e];
-    const double* Us = b.PX[0][hst[2 * e].steps & 1];
-    const double* Vs = b.PX[1][hst[2 * e + 1].steps & 1];
+    const bool gu = pre[e] && m > n, gv = pre[e] && n > m;
+    const double* Us = b.PX[0][gu ? 1 : (hst[2 * e].steps & 1)];
+    const double* Vs = b.PX[1][gv ? 1 : (hst[2 * e + 1].steps & 1)];
     // 7. W_* = U_* Sigma_0 V_*^T
     k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, Us, b.S[0], m, q);
     gemm(m, n, q, 1.0, b.FU, 1, m, Vs, n, 1, 0.0, b.Wst, 1, m, s);
