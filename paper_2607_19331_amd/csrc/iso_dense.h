@@ -906,18 +906,16 @@ struct GemmTile {
   static constexpr int BUF = (GK * PAD > TM * SK) ? GK * PAD : TM * SK;
 };
 
-template <int W>
-__device__ __forceinline__ void gemm_tile(const GemmJob& J, int64_t bx, int64_t by) {
+// AK / BK: A / B is read along k, else along its rows / columns; a template parameter, so that
+// each instantiation holds only its own address arithmetic.
+template <int W, bool AK, bool BK>
+__device__ __forceinline__ void gemm_tile_l(const GemmJob& J, int64_t i0, int64_t j0, double (*As)[GemmTile<W>::BUF],
+                                            double (*Bs)[GemmTile<W>::BUF]) {
   using T = GemmTile<W>;
-  constexpr int TM = T::TM, TW = T::TW, PAD = T::PAD, PT = T::PT, SK = T::SK, BUF = T::BUF;
-  __shared__ double As[2][BUF];
-  __shared__ double Bs[2][BUF];
-  const int64_t i0 = bx * TM, j0 = by * TM;
-  if (i0 >= J.M || j0 >= J.N || (J.upper && i0 > j0)) return;
-  if (J.skip != nullptr && *J.skip != 0) return;
+  constexpr int TM = T::TM, TW = T::TW, PAD = T::PAD, PT = T::PT, SK = T::SK;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, ln = lane & 15;
   const int wm = w >> 1, wn = w & 1;
-  const bool a_kfast = J.as1 == 1, b_kfast = J.bs0 == 1;
+  constexpr bool a_kfast = AK, b_kfast = BK;
   gemm_f64x4_t acc[W][W];
 #pragma unroll
   for (int rb = 0; rb < W; ++rb)
@@ -956,6 +954,7 @@ __device__ __forceinline__ void gemm_tile(const GemmJob& J, int64_t bx, int64_t 
     if (more) load(k0 + GK);
 #pragma unroll
     for (int sub = 0; sub < GK / 4; ++sub) {
+      __builtin_amdgcn_sched_barrier(0);
       double a[W], b[W];
 #pragma unroll
       for (int rb = 0; rb < W; ++rb) {
@@ -979,7 +978,8 @@ __device__ __forceinline__ void gemm_tile(const GemmJob& J, int64_t bx, int64_t 
     buf ^= 1;
   }
 #pragma unroll
-  for (int rb = 0; rb < W; ++rb)
+  for (int rb = 0; rb < W; ++rb) {
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int cb = 0; cb < W; ++cb)
 #pragma unroll
@@ -990,18 +990,36 @@ __device__ __forceinline__ void gemm_tile(const GemmJob& J, int64_t bx, int64_t 
           *cp = (J.beta == 0.0) ? J.alpha * acc[rb][cb][v] : J.alpha * acc[rb][cb][v] + J.beta * *cp;
         }
       }
+  }
+}
+
+template <int W>
+__device__ __forceinline__ void gemm_tile(const GemmJob& J, int64_t bx, int64_t by) {
+  using T = GemmTile<W>;
+  __shared__ double As[2][T::BUF];
+  __shared__ double Bs[2][T::BUF];
+  const int64_t i0 = bx * T::TM, j0 = by * T::TM;
+  if (i0 >= J.M || j0 >= J.N || (J.upper && i0 > j0)) return;
+  if (J.skip != nullptr && *J.skip != 0) return;
+  if (J.as1 == 1) {
+    if (J.bs0 == 1) gemm_tile_l<W, true, true>(J, i0, j0, As, Bs);
+    else gemm_tile_l<W, true, false>(J, i0, j0, As, Bs);
+  } else {
+    if (J.bs0 == 1) gemm_tile_l<W, false, true>(J, i0, j0, As, Bs);
+    else gemm_tile_l<W, false, false>(J, i0, j0, As, Bs);
+  }
 }
 
 // A batch of jobs: grid.z indexes the job.
 template <int W>
-__global__ void __launch_bounds__(256) k_gemm_jobs(const GemmJob* __restrict__ jobs) {
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_gemm_jobs(const GemmJob* __restrict__ jobs) {
   const GemmJob J = jobs[blockIdx.z];
   gemm_tile<W>(J, blockIdx.x, blockIdx.y);
 }
 
 // One job passed by value.
 template <int W>
-__global__ void __launch_bounds__(256) k_gemm_one(GemmJob J) {
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_gemm_one(GemmJob J) {
   gemm_tile<W>(J, blockIdx.x, blockIdx.y);
 }
 
