@@ -138,11 +138,18 @@ __device__ bool jacobi_sweeps(double* A, double* V, int r, int c, int* s_rot, in
 }
 
 // A: r x c col-major (r >= c), overwritten by A V = U Sigma; V: c x c col-major, written.
+// tr: the row count that scales the convergence test (r * u), when A stands for a taller matrix
+// with the same Gram (a Cholesky factor of its A^T A); 0: r itself.
 struct JacobiJob {
   double* a;
   double* v;
   int64_t r, c;
+  int64_t tr;
 };
+
+__device__ __forceinline__ double jacobi_tol(const JacobiJob& J) {
+  return (double)(J.tr > 0 ? J.tr : J.r) * 1.1102230246251565e-16;
+}
 
 __global__ void __launch_bounds__(kJacobiThreads) k_jacobi(const JacobiJob* __restrict__ jobs, uint32_t* status) {
   __shared__ int s_rot;
@@ -184,7 +191,7 @@ __global__ void __launch_bounds__(256) k_jacobi_round(const JacobiJob* __restric
   const int x = (pr == 0) ? 0 : 1 + (pr - 1 + round) % (cp - 1);
   const int y = 1 + (cp - 2 - pr + round) % (cp - 1);
   if (x >= c || y >= c) return;
-  const double tol = (double)r * 1.1102230246251565e-16;
+  const double tol = jacobi_tol(J);
   const bool rot = (r <= 256) ? jacobi_pair<16>(J.a, J.v, r, c, min(x, y), max(x, y), sub, tol)
                               : jacobi_pair<0>(J.a, J.v, r, c, min(x, y), max(x, y), sub, tol);
   if (rot && sub == 0) st[job].rot = 1;                // every writer stores 1
@@ -269,7 +276,7 @@ __global__ void __launch_bounds__(256) k_bjacobi_round(const JacobiJob* __restri
   __syncthreads();
   const int sub = threadIdx.x & 15, grp = threadIdx.x >> 4, ngrp = blockDim.x >> 4;
   const int cp = nc + (nc & 1);
-  const double tol = (double)r * 1.1102230246251565e-16;
+  const double tol = jacobi_tol(J);
   for (int ir = 0; ir < cp - 1; ++ir) {
     for (int q = grp; q < cp / 2; q += ngrp) {
       const int x = (q == 0) ? 0 : 1 + (q - 1 + ir) % (cp - 1);
@@ -416,7 +423,7 @@ __global__ void __launch_bounds__(256) k_bjacobi_gram(const JacobiJob* __restric
     for (int v = 0; v < 4; ++v) G[(16 * t + ln) * kGN + 16 * w + g + 4 * v] = acc[t][v];   // G[i][j] at j*64+i
   __syncthreads();
   // 2. rotation test on every column pair (the test of jacobi_pair)
-  const double tol = (double)r * 1.1102230246251565e-16;
+  const double tol = jacobi_tol(J);
   for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
     const int i = e % kGN, j = e / kGN;
     if (i < j && j < nc) {
@@ -580,7 +587,7 @@ __global__ void __launch_bounds__(512) k_bjg_rot(const JacobiJob* __restrict__ j
   }
   if (threadIdx.x == 0) { s_need = 0; s_rot = 0; }
   __syncthreads();
-  const double tol = (double)r * 1.1102230246251565e-16;
+  const double tol = jacobi_tol(J);
   for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
     const int i = e % kGN, j = e / kGN;
     if (i < j && j < P.nc) {

@@ -681,7 +681,8 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
     const int64_t jr_rows = pre[e] ? q : r;
     for (int i = 0; i <= K; ++i) {
       const int j = i ? nm + e * K + i - 1 : e;
-      hj[j] = JacobiJob{pre[e] ? b.jr[i] : b.ja[i], b.jv[i], jr_rows, q};
+      // on R the convergence test keeps A's scale (r u): R's columns have A's inner products
+      hj[j] = JacobiJob{pre[e] ? b.jr[i] : b.ja[i], b.jv[i], jr_rows, q, pre[e] ? r : 0};
       hp[j] = pre[e] ? nullptr : (wide ? b.V[i] : b.U[i]);   // left factor of the Jacobi matrix
       hp[nsvd + j] = wide ? b.U[i] : b.V[i];                  // right factor
       hp[2 * nsvd + j] = b.S[i];
