@@ -1067,16 +1067,27 @@ inline void gemm_job(const GemmJob& J, hipStream_t s) {
 
 // ---- Cholesky factor of a symmetric positive definite matrix ------------------------------------
 // G = R^T R with R upper triangular, G q x q col-major and only its upper triangle read, R written
-// over it (zeros below the diagonal).  Right-looking in 64-column panels: the diagonal block
-// factored in LDS by one workgroup, the panel's block row solved against it (one thread per
-// column), the trailing upper triangle updated on the MFMA GEMM.  A pivot that is not positive and
-// finite sets *fail (the factor is then zeroed, so that what follows stays finite).
+// over it (zeros below the diagonal), for a table of jobs at once.  Right-looking in 64-column
+// panels: each job's diagonal block factored in LDS by one workgroup, its panel's block row solved
+// against it (one thread per column), the trailing upper triangles updated on the batched MFMA
+// GEMM.  A pivot that is not positive and finite sets the job's fail flag (its factor is then
+// zeroed, so that what follows stays finite).
 constexpr int kCholB = 64;
 
-__global__ void __launch_bounds__(256) k_chol_diag(double* __restrict__ g, int64_t q, int64_t kb, int nb,
-                                                   int* __restrict__ fail) {
-  __shared__ double a[kCholB][kCholB + 1];        // a[i][l] = G(kb + i, kb + l), i <= l
+struct CholJob {
+  double* g;          // q x q col-major, upper triangle holding G on entry, R on exit
+  int64_t q;
+  int* fail;          // 0 on entry
+};
+
+__global__ void __launch_bounds__(256) k_chol_diag_jobs(const CholJob* __restrict__ jobs, int64_t kb) {
+  const CholJob J = jobs[blockIdx.x];
+  if (kb >= J.q) return;
+  __shared__ double a[kCholB][kCholB + 1];
   __shared__ int bad;
+  const int nb = (int)min<int64_t>(kCholB, J.q - kb);
+  double* g = J.g;
+  const int64_t q = J.q;
   for (int e = threadIdx.x; e < nb * nb; e += blockDim.x) {
     const int i = e % nb, l = e / nb;
     a[i][l] = (i <= l) ? g[(kb + i) + (kb + l) * q] : 0.0;
@@ -1106,63 +1117,79 @@ __global__ void __launch_bounds__(256) k_chol_diag(double* __restrict__ g, int64
     const int i = e % nb, l = e / nb;
     g[(kb + i) + (kb + l) * q] = (i <= l) ? a[i][l] : 0.0;
   }
-  if (threadIdx.x == 0 && bad) *fail = 1;
+  if (threadIdx.x == 0 && bad) *J.fail = 1;
 }
 
-// Block row kb of R right of the diagonal block: R(kb:kb+nb, c) = R_kk^{-T} G(kb:kb+nb, c), forward
-// substitution with the column in registers.
-__global__ void __launch_bounds__(256) k_chol_panel(double* __restrict__ g, int64_t q, int64_t kb, int nb) {
+__global__ void __launch_bounds__(256) k_chol_panel_jobs(const CholJob* __restrict__ jobs, int64_t kb) {
+  const CholJob J = jobs[blockIdx.y];
+  if (kb + kCholB >= J.q) return;                  // no columns right of this job's last panel
   __shared__ double rk[kCholB][kCholB + 1];
+  double* g = J.g;
+  const int64_t q = J.q;
   for (int e = threadIdx.x; e < kCholB * kCholB; e += blockDim.x) {
     const int i = e % kCholB, l = e / kCholB;
-    rk[i][l] = (i < nb && l < nb && i <= l) ? g[(kb + i) + (kb + l) * q] : 0.0;
+    rk[i][l] = (i <= l) ? g[(kb + i) + (kb + l) * q] : 0.0;
   }
   __syncthreads();
-  for (int64_t c = kb + nb + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < q;
+  for (int64_t c = kb + kCholB + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < q;
        c += (int64_t)gridDim.x * blockDim.x) {
     double* col = g + kb + c * q;
     double x[kCholB];
 #pragma unroll
-    for (int i = 0; i < kCholB; ++i) x[i] = (i < nb) ? col[i] : 0.0;
+    for (int i = 0; i < kCholB; ++i) x[i] = col[i];
 #pragma unroll
     for (int i = 0; i < kCholB; ++i) {
-      if (i < nb) {
-        double t = x[i];
+      double t = x[i];
 #pragma unroll
-        for (int l = 0; l < i; ++l) t -= rk[l][i] * x[l];
-        x[i] = t / rk[i][i];
-      }
+      for (int l = 0; l < i; ++l) t -= rk[l][i] * x[l];
+      x[i] = t / rk[i][i];
     }
 #pragma unroll
-    for (int i = 0; i < kCholB; ++i)
-      if (i < nb) col[i] = x[i];
+    for (int i = 0; i < kCholB; ++i) col[i] = x[i];
   }
 }
 
-__global__ void k_chol_finish(double* __restrict__ g, int64_t q, const int* __restrict__ fail) {
-  const bool zero = *fail != 0;
+// The trailing-update products of panel kb, one per job (M = 0 for a job with nothing right of it).
+__global__ void k_chol_trail_jobs(const CholJob* __restrict__ jobs, int njobs, int64_t kb, GemmJob* __restrict__ out) {
+  for (int j = threadIdx.x; j < njobs; j += blockDim.x) {
+    const CholJob J = jobs[j];
+    const int64_t t0 = kb + kCholB, rem = J.q - t0;
+    GemmJob G{};
+    if (rem > 0) {
+      const double* rp = J.g + kb + t0 * J.q;
+      G = GemmJob{rp, rp, J.g + t0 + t0 * J.q, J.q, 1, 1, J.q, 1, J.q, rem, rem, kCholB, -1.0, 1.0, 1, nullptr};
+    }
+    out[j] = G;
+  }
+}
+
+__global__ void k_chol_finish_jobs(const CholJob* __restrict__ jobs) {
+  const CholJob J = jobs[blockIdx.y];
+  const bool zero = *J.fail != 0;
+  const int64_t q = J.q;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < q * q; e += (int64_t)gridDim.x * blockDim.x) {
     const int64_t i = e % q, j = e / q;
-    if (zero || i > j) g[e] = 0.0;
+    if (zero || i > j) J.g[e] = 0.0;
   }
 }
 
-// In place on g (q x q col-major, upper triangle holding G); *fail must be 0 on entry.
-inline void cholesky_upper(double* g, int64_t q, int* fail, hipStream_t s) {
-  for (int64_t kb = 0; kb < q; kb += kCholB) {
-    const int nb = (int)std::min<int64_t>(kCholB, q - kb);
-    k_chol_diag<<<1, 256, 0, s>>>(g, q, kb, nb, fail);
-    const int64_t t0 = kb + nb, rem = q - t0;
-    if (rem <= 0) break;
-    k_chol_panel<<<(unsigned)((rem + 255) / 256), 256, 0, s>>>(g, q, kb, nb);
-    // G(t0:, t0:) -= R(kb:kb+nb, t0:)^T R(kb:kb+nb, t0:), tiles on and above the diagonal
-    const double* rp = g + kb + t0 * q;
-    const GemmJob J{rp, rp, g + t0 + t0 * q, q, 1, 1, q, 1, q, rem, rem, nb, -1.0, 1.0, 1, nullptr};
-    gemm_job(J, s);
+// The factors of njobs jobs (device table; max_q the largest q; trail: scratch for njobs GemmJobs),
+// panel by panel over all jobs at once.  A job's last panel may be short (the diagonal kernel takes
+// any width up to 64); it has no columns to its right, so the panel solve and the trailing update
+// only ever see full panels.
+inline void cholesky_upper_jobs(const CholJob* jobs, int njobs, int64_t max_q, GemmJob* trail, hipStream_t s) {
+  for (int64_t kb = 0; kb < max_q; kb += kCholB) {
+    k_chol_diag_jobs<<<(unsigned)njobs, 256, 0, s>>>(jobs, kb);
+    const int64_t rem = max_q - kb - kCholB;
+    if (rem <= 0) continue;
+    k_chol_panel_jobs<<<dim3((unsigned)((rem + 255) / 256), (unsigned)njobs), 256, 0, s>>>(jobs, kb);
+    k_chol_trail_jobs<<<1, 256, 0, s>>>(jobs, njobs, kb, trail);
+    gemm_jobs(trail, njobs, rem, rem, s);
   }
-  const int64_t n = q * q;
-  k_chol_finish<<<(unsigned)std::max<int64_t>(1, std::min<int64_t>((n + 255) / 256, 4096)), 256, 0, s>>>(g, q, fail);
+  k_chol_finish_jobs<<<dim3((unsigned)std::max<int64_t>(1, std::min<int64_t>((max_q * max_q + 255) / 256, 4096)),
+                            (unsigned)njobs), 256, 0, s>>>(jobs);
 }
+
 
 }  // namespace
 }  // namespace iso

@@ -464,6 +464,8 @@ struct Tables {
   GemmJob* ngj[4];   // [2 p]: G = X_p^T X_p, [2 p + 1]: X_{1-p} = X_p T
   GemmJob* wgj;      // warm start of the expert SVDs: A_i V_0
   GemmJob* qgj[5];   // q-space polar: G_0 = X_0^T X_0, H = G T, G = T H, P_1 = P_0 T, P_0 = P_1 T
+  CholJob* qch;      // the Cholesky factors of the tall matrices' SVDs (first nch entries)
+  GemmJob* qtrail;   // their trailing updates, one panel at a time
   int* qfail;        // per SVD: its Cholesky factor failed (tall matrices)
   int* qmat;         // per SVD: its matrix's index in the batch if the Jacobi ran on R, else -1
   int* qbad;         // per matrix: its SVDs go to plain Jacobi on A
@@ -479,6 +481,8 @@ Tables carve_tables(Bump& bp, int nm, int K) {
   for (int k = 0; k < 4; ++k) tb.ngj[k] = bp.take<GemmJob>(2 * nm);
   tb.wgj = bp.take<GemmJob>((int64_t)nm * K);
   for (int k = 0; k < 5; ++k) tb.qgj[k] = bp.take<GemmJob>(2 * nm);
+  tb.qch = bp.take<CholJob>((int64_t)nm * (K + 1));
+  tb.qtrail = bp.take<GemmJob>((int64_t)nm * (K + 1));
   tb.qfail = bp.take<int>((int64_t)nm * (K + 1));
   tb.qmat = bp.take<int>((int64_t)nm * (K + 1));
   tb.qbad = bp.take<int>(nm);
@@ -669,6 +673,9 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
   GemmJob* hq[5];
   for (int k = 0; k < 5; ++k) hq[k] = (GemmJob*)at(tb.qgj[k]);
   int* hqm = (int*)at(tb.qmat);
+  CholJob* hch = (CholJob*)at(tb.qch);
+  int nch = 0;
+  int64_t ch_q = 1;
   int64_t svd_r = 1, svd_c = 1;
   std::vector<char> pre(nm);
   for (int e = 0; e < nm; ++e) {
@@ -687,6 +694,10 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
       hp[nsvd + j] = wide ? b.U[i] : b.V[i];                  // right factor
       hp[2 * nsvd + j] = b.S[i];
       hqm[j] = pre[e] ? e : -1;
+      if (pre[e]) {
+        hch[nch++] = CholJob{b.jr[i], q, tb.qfail + j};
+        ch_q = std::max(ch_q, q);
+      }
     }
     // A_i V_0 as (A_0 V_0) + T_i V_0 (r x q), the first term the base's converged Jacobi matrix,
     // T_i (tau_i or its transpose) staged in the proxy buffer; on R: R_0 V_0 + (R_i - R_0) V_0
@@ -755,14 +766,16 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
     const iso_tensor& x = t[ids[e]];
     const int64_t q = std::min(x.rows, x.cols), r = std::max(x.rows, x.cols);
     const Bufs& b = bs[e];
-    for (int i = 0; i <= K; ++i) {
-      const int j = i ? nm + e * K + i - 1 : e;
+    for (int i = 0; i <= K; ++i)
       gemm_job(GemmJob{b.ja[i], b.ja[i], b.jr[i], r, 1, 1, r, 1, q, q, q, r, 1.0, 0.0, 1, nullptr}, s);
-      cholesky_upper(b.jr[i], q, tb.qfail + j, s);
-    }
-    if (warm)
-      for (int i = 1; i <= K; ++i)
-        k_sub<<<grid_for(q * q), 256, 0, s>>>(b.G + (int64_t)(i - 1) * q * q, b.jr[i], b.jr[0], q * q);
+  }
+  if (nch > 0) cholesky_upper_jobs(tb.qch, nch, ch_q, tb.qtrail, s);
+  for (int e = 0; e < nm; ++e) {
+    if (!pre[e] || !warm) continue;
+    const int64_t q = std::min(t[ids[e]].rows, t[ids[e]].cols);
+    const Bufs& b = bs[e];
+    for (int i = 1; i <= K; ++i)
+      k_sub<<<grid_for(q * q), 256, 0, s>>>(b.G + (int64_t)(i - 1) * q * q, b.jr[i], b.jr[0], q * q);
   }
   if (!warm) {
     SP_TRY(jacobi_block(tb.jobs, nsvd, svd_r, svd_c, tb.jst, status, s, false, split));
