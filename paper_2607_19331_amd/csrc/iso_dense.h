@@ -323,7 +323,7 @@ __device__ __forceinline__ void gram_load(double (&pf)[kGChunkPer], const double
 #pragma unroll
   for (int u = 0; u < kGChunkPer; ++u) {
     const int e = threadIdx.x + 256 * u, l = e / kGN, i = e % kGN;
-    pf[u] = (l < nc && k0 + i < nrows) ? X[(int64_t)gc[l] * ld + k0 + i] : 0.0;
+    pf[u] = (l < nc && k0 + i < nrows) ? gmem(X)[(int64_t)gc[l] * ld + k0 + i] : 0.0;
   }
 }
 
@@ -365,7 +365,7 @@ __device__ __forceinline__ void gram_apply(double* X, int64_t ld, int row0, int 
     __syncthreads();
     for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
       const int l = e / kGN, i = e % kGN;
-      if (l < nc && k0 + i < nrows) X[(int64_t)gc[l] * ld + k0 + i] = ch[l * kGP + i];
+      if (l < nc && k0 + i < nrows) gmem(X)[(int64_t)gc[l] * ld + k0 + i] = ch[l * kGP + i];
     }
     __syncthreads();
   }
@@ -657,7 +657,7 @@ __global__ void __launch_bounds__(256) k_bjg_apply(const JacobiJob* __restrict__
     __syncthreads();
     for (int e = threadIdx.x; e < kGN * kGN; e += blockDim.x) {
       const int l = e / kGN, i = e % kGN;
-      if (l < P.nc && k0 + i < row1) X[(int64_t)gc[l] * rows + k0 + i] = ch[l * kGP + i];
+      if (l < P.nc && k0 + i < row1) gmem(X)[(int64_t)gc[l] * rows + k0 + i] = ch[l * kGP + i];
     }
     __syncthreads();
   };
@@ -938,8 +938,8 @@ __device__ __forceinline__ void gemm_tile_l(const GemmJob& J, int64_t i0, int64_
       const int ka = a_kfast ? (e & 15) : (e / TM), ia = a_kfast ? (e >> 4) : (e % TM);
       const int kb = b_kfast ? (e & 15) : (e / TM), jb = b_kfast ? (e >> 4) : (e % TM);
       const int64_t gi = i0 + ia, gka = k0 + ka, gj = j0 + jb, gkb = k0 + kb;
-      pa[q] = (gi < J.M && gka < J.K) ? J.A[gi * J.as0 + gka * J.as1] : 0.0;
-      pb[q] = (gj < J.N && gkb < J.K) ? J.B[gkb * J.bs0 + gj * J.bs1] : 0.0;
+      pa[q] = (gi < J.M && gka < J.K) ? gmem(J.A)[gi * J.as0 + gka * J.as1] : 0.0;
+      pb[q] = (gj < J.N && gkb < J.K) ? gmem(J.B)[gkb * J.bs0 + gj * J.bs1] : 0.0;
     }
   };
   auto store = [&](int buf) {
@@ -993,7 +993,7 @@ __device__ __forceinline__ void gemm_tile_l(const GemmJob& J, int64_t i0, int64_
       for (int v = 0; v < 4; ++v) {
         const int64_t gi = i0 + TW * wm + 16 * rb + g + 4 * v, gj = j0 + TW * wn + 16 * cb + ln;
         if (gi < J.M && gj < J.N) {
-          double* cp = J.C + gi * J.cs0 + gj * J.cs1;
+          auto cp = gmem(J.C) + gi * J.cs0 + gj * J.cs1;
           *cp = (J.beta == 0.0) ? J.alpha * acc[rb][cb][v] : J.alpha * acc[rb][cb][v] + J.beta * *cp;
         }
       }
@@ -1133,7 +1133,7 @@ __global__ void __launch_bounds__(256) k_chol_panel_jobs(const CholJob* __restri
   __syncthreads();
   for (int64_t c = kb + kCholB + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < q;
        c += (int64_t)gridDim.x * blockDim.x) {
-    double* col = g + kb + c * q;
+    auto col = gmem(g) + kb + c * q;
     double x[kCholB];
 #pragma unroll
     for (int i = 0; i < kCholB; ++i) x[i] = col[i];

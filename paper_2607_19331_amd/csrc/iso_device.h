@@ -17,6 +17,20 @@ constexpr uint32_t kStatusInternal = 2u;   // a kernel found counts that cannot 
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Global-memory view of a generic pointer (one that points into device memory).  A pointer read
+// from a job or problem table is generic, and accesses through it compile to flat instructions,
+// which count against the LDS wait counter as well as the vector-memory one: every wait for an LDS
+// read then also waits for the global loads in flight, so a prefetch issued before the LDS reads
+// of the current step is drained by them.  Through this view they compile to global instructions.
+template <typename T>
+__device__ __forceinline__ const __attribute__((address_space(1))) T* gmem(const T* p) {
+  return (const __attribute__((address_space(1))) T*)p;
+}
+template <typename T>
+__device__ __forceinline__ __attribute__((address_space(1))) T* gmem(T* p) {
+  return (__attribute__((address_space(1))) T*)p;
+}
+
 // Table entry as the kernels see it.
 struct DevTensor {
   const void* base;

@@ -28,6 +28,7 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int kPowerIters = 2;
 constexpr size_t kTsvChunkBudget = 32ull << 30;  // workspace per chunk of matrices (all 84 MLP matrices of a 7B stack)
@@ -104,8 +105,7 @@ __device__ __forceinline__ uint16_t bf16_rne_f32(float f) {
 __device__ __forceinline__ float f32_of_bf16(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
 __device__ __forceinline__ bf16x8_t ld_bf16x8(const uint16_t* p) {
-  uint4 v = *(const uint4*)p;
-  return __builtin_bit_cast(bf16x8_t, v);
+  return *gmem((const bf16x8_t*)p);
 }
 
 // Row `row` of a row-major bf16 matrix with `ncols` columns: 8 entries from column k (zero
@@ -117,7 +117,7 @@ __device__ __forceinline__ bf16x8_t ld_row8(const uint16_t* base, int64_t nrows,
     if (vec && k + 8 <= ncols) return ld_bf16x8(p);
     uint16_t t[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) t[e] = (k + e < ncols) ? p[e] : (uint16_t)0;
+    for (int e = 0; e < 8; ++e) t[e] = (k + e < ncols) ? gmem(p)[e] : (uint16_t)0;
     return __builtin_bit_cast(bf16x8_t, *(uint4*)t);
   }
   return __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0));
@@ -275,7 +275,7 @@ __global__ void __launch_bounds__(256) k_sk_nn(const Prob* __restrict__ probs, i
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int64_t r = wrow + 16 * rb + 4 * g + e;
-        if (r < R) X[r * P.L + cb * 16 + ln] = (double)acc[rb][cb][e];
+        if (r < R) gmem(X)[r * P.L + cb * 16 + ln] = (double)acc[rb][cb][e];
       }
 }
 
@@ -386,7 +386,7 @@ __global__ void __launch_bounds__(256) k_sk_tn(const Prob* __restrict__ probs, i
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int64_t r = i0 + 64 * w + 16 * rb + 4 * g + e;
-        if (r < C) Z[r * P.L + cb * 16 + ln] = (double)acc[rb][cb][e];
+        if (r < C) gmem(Z)[r * P.L + cb * 16 + ln] = (double)acc[rb][cb][e];
       }
 }
 
@@ -465,7 +465,7 @@ __global__ void __launch_bounds__(256) k_sk_tn_any(const Prob* __restrict__ prob
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int64_t r = i0 + 64 * w + 16 * rb + 4 * g + e;
-        if (r < C) Z[r * P.L + cb * 16 + ln] = (double)acc[rb][cb][e];
+        if (r < C) gmem(Z)[r * P.L + cb * 16 + ln] = (double)acc[rb][cb][e];
       }
 }
 
@@ -535,8 +535,8 @@ __device__ __forceinline__ void gram_wave(const double* __restrict__ X, int64_t 
       const int64_t ra = k0 + g, rc = k0 + 4 + g;
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
-        x0[j] = (ra < r1) ? X[ra * L + 16 * j + ln] : 0.0;
-        x1[j] = (rc < r1) ? X[rc * L + 16 * j + ln] : 0.0;
+        x0[j] = (ra < r1) ? gmem(X)[ra * L + 16 * j + ln] : 0.0;
+        x1[j] = (rc < r1) ? gmem(X)[rc * L + 16 * j + ln] : 0.0;
       }
       gram_mfmas<NB, W>(acc, x0, Seq{});
       gram_mfmas<NB, W>(acc, x1, Seq{});
@@ -676,7 +676,7 @@ __global__ void __launch_bounds__(256) k_apply_mf(const Prob* __restrict__ probs
     const int64_t r = chunk * 64 + 16 * w + lrow;
     const bool ok = chunk < nchunks && r < M;
 #pragma unroll
-    for (int s = 0; s < 4 * NB; ++s) x[s] = ok ? X[r * L + 4 * s + g] : 0.0;
+    for (int s = 0; s < 4 * NB; ++s) x[s] = ok ? gmem(X)[r * L + 4 * s + g] : 0.0;
   };
   int64_t chunk = blockIdx.x;
   load(chunk, xa);
@@ -691,7 +691,7 @@ __global__ void __launch_bounds__(256) k_apply_mf(const Prob* __restrict__ probs
 #pragma unroll
     for (int s = 0; s < 4 * NB; ++s) {
       const double a = xa[s];
-      xa[s] = nok ? X[rn * L + 4 * s + g] : 0.0;      // the next chunk's fragment, one chunk ahead
+      xa[s] = nok ? gmem(X)[rn * L + 4 * s + g] : 0.0;      // the next chunk's fragment, one chunk ahead
 #pragma unroll
       for (int cb = s / 4; cb < NB; ++cb) acc[cb] = mfma64(a, ri[4 * s + g][16 * cb + ln], acc[cb]);
     }
@@ -700,7 +700,7 @@ __global__ void __launch_bounds__(256) k_apply_mf(const Prob* __restrict__ probs
     for (int cb = 0; cb < NB; ++cb) {
 #pragma unroll
       for (int v = 0; v < 4; ++v)
-        if (row0 + v < M) Y[(row0 + v) * L + 16 * cb + ln] = acc[cb][v];
+        if (row0 + v < M) gmem(Y)[(row0 + v) * L + 16 * cb + ln] = acc[cb][v];
       if (split) {
         uint16_t h[4], l[4];
 #pragma unroll
@@ -710,8 +710,8 @@ __global__ void __launch_bounds__(256) k_apply_mf(const Prob* __restrict__ probs
           l[v] = bf16_rne_f32(f - f32_of_bf16(h[v]));
         }
         const int64_t o = (int64_t)(16 * cb + ln) * P.ldb + row0;
-        *(uint2*)(P.bh + o) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
-        *(uint2*)(P.bl + o) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
+        *gmem((u32x2_t*)(P.bh + o)) = u32x2_t{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16)};
+        *gmem((u32x2_t*)(P.bl + o)) = u32x2_t{l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16)};
       }
     }
   }
@@ -864,7 +864,7 @@ __global__ void __launch_bounds__(256) k_mfma_recon(const Mat* __restrict__ mats
   store(0);
   __syncthreads();
   const bool vec = (C % 4) == 0;
-  uint2 wv[4][4];
+  u32x2_t wv[4][4];
   for (int64_t s = 0; s < steps; ++s) {
     const bool more = s + 1 < steps;
     if (more) load((s + 1) * kRecK);
@@ -875,7 +875,7 @@ __global__ void __launch_bounds__(256) k_mfma_recon(const Mat* __restrict__ mats
 #pragma unroll
         for (int cb = 0; cb < 4; ++cb) {
           const int64_t r = min(R - 1, m0 + 64 * wm + 16 * rb + ln), c0 = min(C - 4, n0 + 64 * wn + 16 * cb + 4 * g);
-          wv[rb][cb] = *(const uint2*)(M.w0 + r * C + c0);
+          wv[rb][cb] = *gmem((const u32x2_t*)(M.w0 + r * C + c0));
         }
     }
     const int buf = (int)(s & 1);
@@ -915,14 +915,14 @@ __global__ void __launch_bounds__(256) k_mfma_recon(const Mat* __restrict__ mats
         uint32_t o[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) o[e] = bf16_of_sum(__uint_as_float(wi[e]), alpha * acc[rb][cb][e]);
-        *(uint2*)(M.out + idx) = make_uint2(o[0] | (o[1] << 16), o[2] | (o[3] << 16));
-        if (M.dhat) *(float4*)(M.dhat + idx) = make_float4(acc[rb][cb][0], acc[rb][cb][1], acc[rb][cb][2], acc[rb][cb][3]);
+        *gmem((u32x2_t*)(M.out + idx)) = u32x2_t{o[0] | (o[1] << 16), o[2] | (o[3] << 16)};
+        if (M.dhat) *gmem((f32x4_t*)(M.dhat + idx)) = acc[rb][cb];
       } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
           if (c0 + e < C) {
-            M.out[idx + e] = (uint16_t)bf16_of_sum(f32_of_bf16(M.w0[idx + e]), alpha * acc[rb][cb][e]);
-            if (M.dhat) M.dhat[idx + e] = acc[rb][cb][e];
+            gmem(M.out)[idx + e] = (uint16_t)bf16_of_sum(f32_of_bf16(gmem(M.w0)[idx + e]), alpha * acc[rb][cb][e]);
+            if (M.dhat) gmem(M.dhat)[idx + e] = acc[rb][cb][e];
           }
       }
     }
