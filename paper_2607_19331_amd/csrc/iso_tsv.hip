@@ -15,6 +15,7 @@
 //      epilogue.
 // The randomised sketch draws its test matrix from a counter-based hash (SplitMix64); the
 // result does not depend on it to the accuracy of the truncation where the spectrum has a gap.
+#include <algorithm>
 #include <cstring>
 #include <utility>
 #include <vector>
@@ -31,6 +32,8 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int kPowerIters = 2;
+// Ping-pong buffer of the last X-side factor: one Cholesky-QR pass per X-side sketch
+constexpr int kXLast = (1 + kPowerIters) & 1;
 constexpr size_t kTsvChunkBudget = 32ull << 30;  // workspace per chunk of matrices (all 84 MLP matrices of a 7B stack)
 constexpr int kMaxNB = 8;                         // sketch width up to 128
 
@@ -203,11 +206,12 @@ struct SkB {
 // C are clamped into the row (B is zero there), otherwise entries are loaded one by one and
 // zero-filled.
 template <int NB>
-__global__ void __launch_bounds__(256) k_sk_nn(const Prob* __restrict__ probs, int out, int64_t nbx) {
+__global__ void __launch_bounds__(256) k_sk_nn(const Prob* __restrict__ probs, const int* __restrict__ order, int out,
+                                               int64_t nbx) {
   constexpr int KS = 64, KG = KS / 8, H = 1;
   __shared__ bf16x8_t bsh[2][H][NB * 16][KG + 1];
   const int64_t lb = xcd_logical_block(blockIdx.x + (int64_t)gridDim.x * blockIdx.z, (int64_t)gridDim.x * gridDim.z);
-  const Prob& P = probs[lb / nbx];
+  const Prob& P = probs[order[lb / nbx]];
   const int64_t R = P.R, C = P.C;
   const int64_t m0 = (lb % nbx) * kSkRows;
   if (m0 >= R) return;
@@ -297,12 +301,13 @@ typedef __bf16 bf16x4v_t __attribute__((__vector_size__(4 * sizeof(__bf16))));
 // there); columns past C are clamped and not stored.  Requires C % 8 == 0 (the host routes other
 // shapes to k_sk_tn_any).
 template <int NB, bool LO>
-__global__ void __launch_bounds__(256) k_sk_tn(const Prob* __restrict__ probs, int out, int64_t nbx) {
+__global__ void __launch_bounds__(256) k_sk_tn(const Prob* __restrict__ probs, const int* __restrict__ order, int out,
+                                               int64_t nbx) {
   constexpr int KS = 32, KG = KS / 8, H = LO ? 2 : 1;
   __shared__ __align__(16) uint16_t atile[2][KS][kSkRows];
   __shared__ bf16x8_t bsh[2][H][NB * 16][KG + 1];
   const int64_t lb = xcd_logical_block(blockIdx.x + (int64_t)gridDim.x * blockIdx.z, (int64_t)gridDim.x * gridDim.z);
-  const Prob& P = probs[lb / nbx];
+  const Prob& P = probs[order[lb / nbx]];
   const int64_t R = P.R, C = P.C;
   const int64_t i0 = (lb % nbx) * kSkRows;
   if (i0 >= C) return;
@@ -1154,23 +1159,24 @@ size_t table_bytes(int nm, int K) {
   b += 12 * align_up(sizeof(GemmJob) * (size_t)std::max(np, kSlabs * nm * 2), 256);
   b += 2 * align_up(sizeof(double*) * 2 * nm, 256);
   b += align_up(sizeof(NsFlags) * 2 * nm, 256);
+  b += align_up(sizeof(int) * 2 * (size_t)np, 256);
   return b;
 }
 
 template <int NB>
-void launch_nn(const Prob* d, int np, int64_t maxR, int out, hipStream_t s) {
+void launch_nn(const Prob* d, const int* order, int np, int64_t maxR, int out, hipStream_t s) {
   const int64_t nbx = (maxR + kSkRows - 1) / kSkRows;
-  k_sk_nn<NB><<<dim3((unsigned)nbx, 1, (unsigned)np), 256, 0, s>>>(d, out, nbx);
+  k_sk_nn<NB><<<dim3((unsigned)nbx, 1, (unsigned)np), 256, 0, s>>>(d, order, out, nbx);
 }
 // lo: include the lo part of B (the last product, whose values form the result)
 // aligned: every delta of the chunk has C % 8 == 0 (rows start 16-byte aligned)
 template <int NB>
-void launch_tn(const Prob* d, int np, int64_t maxC, int out, bool lo, bool aligned, hipStream_t s) {
+void launch_tn(const Prob* d, const int* order, int np, int64_t maxC, int out, bool lo, bool aligned, hipStream_t s) {
   const int64_t nbx = (maxC + kSkRows - 1) / kSkRows;
   const dim3 grid((unsigned)nbx, 1, (unsigned)np);
   if (!aligned) k_sk_tn_any<NB><<<grid, 256, 0, s>>>(d, out);
-  else if (lo) k_sk_tn<NB, true><<<grid, 256, 0, s>>>(d, out, nbx);
-  else k_sk_tn<NB, false><<<grid, 256, 0, s>>>(d, out, nbx);
+  else if (lo) k_sk_tn<NB, true><<<grid, 256, 0, s>>>(d, order, out, nbx);
+  else k_sk_tn<NB, false><<<grid, 256, 0, s>>>(d, order, out, nbx);
 }
 template <int NB>
 void launch_gram(const Prob* d, int np, int which, int cur, hipStream_t s) {
@@ -1237,6 +1243,7 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     const double** d_nsrc = cv.take<const double*>(2 * nm);
     double** d_ndst = cv.take<double*>(2 * nm);
     NsFlags* d_nf = cv.take<NsFlags>(2 * nm);
+    int* d_ord = cv.take<int>(2 * np);
     cv.off = table_bytes(nm, K);
     std::vector<Prob> hp(np);
     std::vector<Mat> hm(nm);
@@ -1293,7 +1300,7 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
       const Prob& P = hp[p];
       const Mat& M = hm[p / K];
       const int i = p % K;
-      gj[0].push_back(GemmJob{P.X[0], P.Ut, M.U + i * r, P.L, 1, 1, P.L, M.ldk, 1, P.R, r, P.L, 1.0, 0.0});
+      gj[0].push_back(GemmJob{P.X[kXLast], P.Ut, M.U + i * r, P.L, 1, 1, P.L, M.ldk, 1, P.R, r, P.L, 1.0, 0.0});
       gj[1].push_back(GemmJob{P.Z[0], P.Vt, M.V + i * r, P.L, 1, 1, P.L, M.ldk, 1, P.C, r, P.L, 1.0, 0.0});
     }
     for (int m = 0; m < nm; ++m) {
@@ -1343,6 +1350,22 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
       for (int q = 0; q < 12; ++q) h_gj[q] = hc.take<GemmJob>(std::max(np, kSlabs * nm * 2));
       const double** h_nsrc = hc.take<const double*>(2 * nm);
       double** h_ndst = hc.take<double*>(2 * nm);
+      hc.take<NsFlags>(2 * nm);
+      int* h_ord = hc.take<int>(2 * np);
+      // launch order of the skinny products.  Each XCD works through its own contiguous range of
+      // the order; the problems, sorted by the walk of one workgroup (k = C for Delta B, k = R for
+      // Delta^T B), are dealt round-robin to the eight ranges, so that each XCD gets the same mix,
+      // longest first, and the short ones fill the tail.
+      auto deal = [&](int* o, bool by_c) {
+        std::vector<int> srt(np);
+        for (int p = 0; p < np; ++p) srt[p] = p;
+        std::stable_sort(srt.begin(), srt.end(), [&](int x, int y) { return by_c ? hp[x].C > hp[y].C : hp[x].R > hp[y].R; });
+        int n = 0;
+        for (int x = 0; x < kXcds; ++x)
+          for (int j = x; j < np; j += kXcds) o[n++] = srt[j];
+      };
+      deal(h_ord, true);
+      deal(h_ord + np, false);
       std::memcpy(h_prob, hp.data(), sizeof(Prob) * np);
       std::memcpy(h_mat, hm.data(), sizeof(Mat) * nm);
       for (int p = 0; p < np; ++p) {
@@ -1374,32 +1397,32 @@ iso_status run_tsv(const iso_tensor* t, int n_t, int K, const TsvArgs& a, uint8_
     // 1. range finder with subspace iteration
     int cx = 0, cz = 0;
     k_omega<<<dim3(gx, np), 256, 0, s>>>(d_prob);
-    // Cholesky-QR2 where orthogonality is carried forward (first sketch, final factor); one
-    // pass inside the power iteration, whose next product and QR absorb its rounding
+    // One Cholesky-QR pass for every sketch of the range finder (its next product and QR absorb
+    // the rounding), Cholesky-QR2 for the factor of the last product, whose R forms the core.
     // The sketches of the range finder only have to span the dominant subspace: rounding their
     // right operand to bf16 (relative 2^-9) tilts the next iterate by about 2^-9 sigma_{r+1} /
     // sigma_r, which the following QR and product absorb; the last product, whose values form
     // the result, takes both parts (relative 2^-17).
-    DISPATCH_NB(NB, launch_nn, d_prob, np, maxR, cx, s);
-    cholqr(0, cx, 0, 0, 2, 1);
+    DISPATCH_NB(NB, launch_nn, d_prob, d_ord, np, maxR, cx, s);
+    cholqr(0, cx, 0, 0, 1, 1);
     for (int it = 0; it < kPowerIters; ++it) {
-      DISPATCH_NB(NB, launch_tn, d_prob, np, maxC, cz, false, aligned, s);
+      DISPATCH_NB(NB, launch_tn, d_prob, d_ord + np, np, maxC, cz, false, aligned, s);
       cholqr(1, cz, 0, 0, 1, 1);
-      DISPATCH_NB(NB, launch_nn, d_prob, np, maxR, cx, s);
+      DISPATCH_NB(NB, launch_nn, d_prob, d_ord, np, maxR, cx, s);
       cholqr(0, cx, 0, 0, 1, 1);
     }
     // 2. B^T = Delta^T Q, its QR (R2 accumulated), SVD of the L x L core R2^T
-    DISPATCH_NB(NB, launch_tn, d_prob, np, maxC, cz, true, aligned, s);
+    DISPATCH_NB(NB, launch_tn, d_prob, d_ord + np, np, maxC, cz, true, aligned, s);
     cholqr(1, cz, 1, 1, 2, 0);
     k_core_load<<<np, 256, 0, s>>>(d_prob, d_jobs);
     const size_t jlds = sizeof(double) * 2 * (size_t)L * L;
     if (jlds <= kJacobiLdsMax) k_jacobi_lds<<<np, kJacobiThreads, jlds, s>>>(d_jobs, status);
     else k_jacobi<<<np, kJacobiThreads, 0, s>>>(d_jobs, status);
     svd_finalize(d_jobs, d_ptrs, d_ptrs + np, d_ptrs + 2 * np, np, L, s);
-    // U_i = Q Ut[:, :r], V_i = Q2 Vt[:, :r]: both factors end in buffer 0 (an even number of QR
-    // passes: 2 + kPowerIters for X, kPowerIters + 2 for Z)
+    // U_i = Q Ut[:, :r], V_i = Q2 Vt[:, :r]: Q ends in buffer kXLast (1 + kPowerIters QR passes),
+    // Q2 in buffer 0 (kPowerIters + 2 passes)
     static_assert(kPowerIters % 2 == 0, "ping-pong parity");
-    if (cx != 0 || cz != 0) return ISO_ERR_INTERNAL;
+    if (cx != kXLast || cz != 0) return ISO_ERR_INTERNAL;
     gemm_jobs(d_gj[0], np, maxR, r, s);
     gemm_jobs(d_gj[1], np, maxC, r, s);
     k_sigma<<<np, 64, 0, s>>>(d_prob, d_mat, K, r);
