@@ -4,6 +4,7 @@
 #pragma once
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "iso_device.h"
@@ -674,6 +675,25 @@ inline size_t gram_split_bytes(int njobs, int64_t max_r, int64_t max_c) {
   return ((size_t)njobs * np * (size_t)(ns + 1) * kGN * kGN) * sizeof(double) + (size_t)njobs * np * sizeof(int) + 256;
 }
 
+// A second stream of the current device (default priority, created on first use and kept until
+// the process ends), or null if it cannot be created.
+inline hipStream_t aux_stream() {
+  constexpr int kMaxDev = 64;
+  static std::mutex mu;
+  static hipStream_t per[kMaxDev] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (per[dev] == nullptr && hipStreamCreateWithFlags(&per[dev], hipStreamNonBlocking) != hipSuccess) per[dev] = nullptr;
+  return per[dev];
+}
+
+// With scratch (the split step) and at least two jobs, the job set runs as two halves, the second
+// on aux_stream(): a round's rotation launch has one workgroup per block pair and leaves most of
+// the chip idle, and the other half's Gram and apply launches fill it meanwhile.  The halves share
+// no job, state entry or scratch; in each block of sweeps between host checks, the second forks
+// from s after the first half's first Gram launch and joins s before the check.  Concurrent calls on one device share the second stream, which
+// orders their halves but keeps each call's dependencies on its own events.
 inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_r, int64_t max_c, JacobiState* st,
                               uint32_t* status, hipStream_t s, bool v_given, void* scratch) {
   const unsigned gb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_c * max_c + 255) / 256, 4096));
@@ -692,28 +712,81 @@ inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_r, i
   const int slices_a = S.nslices, slices_v = S.slice ? (int)((max_c + S.slice - 1) / S.slice) : 0;
   // a sweep over more than 2^26 matrix entries takes milliseconds: check the flags after each one
   const int check = (double)max_r * (double)max_c * njobs > 67108864.0 ? 1 : kJacobiCheckSweeps;
-  std::vector<JacobiState> h(njobs);
-  for (int sweep = 0; sweep < kJacobiMaxSweeps;) {
-    for (int b = 0; b < check && sweep < kJacobiMaxSweeps; ++b, ++sweep) {
-      for (int round = 0; round < nbp - 1; ++round) {
-        if (scratch == nullptr) {
-          k_bjacobi_gram<<<g, 256, 0, s>>>(jobs, st, round);
-        } else {
-          k_bjg_part<<<dim3((unsigned)(S.npairs * S.nslices), (unsigned)njobs), 256, 0, s>>>(jobs, st, round, S);
-          k_bjg_rot<<<dim3((unsigned)S.npairs, (unsigned)njobs), 512, 0, s>>>(jobs, st, round, S);
-          k_bjg_apply<<<dim3((unsigned)(S.npairs * (slices_a + slices_v)), (unsigned)njobs), 256, 0, s>>>(
-              jobs, st, round, S, slices_a, slices_v);
+  struct Half {
+    const JacobiJob* jobs;
+    JacobiState* st;
+    GramSplit S;
+    int n;
+    hipStream_t s;
+  };
+  Half half[2] = {{jobs, st, S, njobs, s}, {}};
+  hipStream_t s2 = (scratch != nullptr && njobs >= 2) ? aux_stream() : nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  if (s2 != nullptr && (hipEventCreateWithFlags(&fork, hipEventDisableTiming) != hipSuccess ||
+                        hipEventCreateWithFlags(&join, hipEventDisableTiming) != hipSuccess)) {
+    if (fork != nullptr) (void)hipEventDestroy(fork);
+    fork = nullptr;
+    s2 = nullptr;
+  }
+  const int nh = (s2 != nullptr) ? 2 : 1;
+  if (nh == 2) {
+    const int n0 = njobs / 2;
+    GramSplit S1 = S;
+    S1.part += (size_t)n0 * S.npairs * S.nslices * kGN * kGN;
+    S1.qrot += (size_t)n0 * S.npairs * kGN * kGN;
+    S1.need += (size_t)n0 * S.npairs;
+    half[0].n = n0;
+    half[1] = Half{jobs + n0, st + n0, S1, njobs - n0, s2};
+  }
+  auto run = [&]() -> hipError_t {
+    std::vector<JacobiState> h(njobs);
+    for (int sweep = 0; sweep < kJacobiMaxSweeps;) {
+      hipError_t e = hipSuccess;
+      const int sweep0 = sweep;
+      for (int hi = 0; hi < nh; ++hi) {
+        const Half& H = half[hi];
+        // the second half starts once the first half's first Gram launch of this block is done,
+        // a phase apart, so that each half's rotations overlap the other's Gram or apply work
+        if (hi == 1 && (e = hipStreamWaitEvent(s2, fork, 0)) != hipSuccess) return e;
+        for (int b = 0, sw = sweep0; b < check && sw < kJacobiMaxSweeps; ++b, ++sw) {
+          for (int round = 0; round < nbp - 1; ++round) {
+            if (scratch == nullptr) {
+              k_bjacobi_gram<<<g, 256, 0, H.s>>>(H.jobs, H.st, round);
+            } else {
+              k_bjg_part<<<dim3((unsigned)(H.S.npairs * H.S.nslices), (unsigned)H.n), 256, 0, H.s>>>(H.jobs, H.st,
+                                                                                                     round, H.S);
+              if (nh == 2 && hi == 0 && b == 0 && round == 0 && (e = hipEventRecord(fork, s)) != hipSuccess) return e;
+              k_bjg_rot<<<dim3((unsigned)H.S.npairs, (unsigned)H.n), 512, 0, H.s>>>(H.jobs, H.st, round, H.S);
+              k_bjg_apply<<<dim3((unsigned)(H.S.npairs * (slices_a + slices_v)), (unsigned)H.n), 256, 0, H.s>>>(
+                  H.jobs, H.st, round, H.S, slices_a, slices_v);
+            }
+          }
+          k_jacobi_sweep_end<<<1, 256, 0, H.s>>>(H.st, H.n);
         }
       }
-      k_jacobi_sweep_end<<<1, 256, 0, s>>>(st, njobs);
+      for (int b = 0; b < check && sweep < kJacobiMaxSweeps; ++b) ++sweep;
+      if (nh == 2) {
+        e = hipEventRecord(join, s2);
+        if (e == hipSuccess) e = hipStreamWaitEvent(s, join, 0);
+        if (e != hipSuccess) return e;
+      }
+      e = hipMemcpyAsync(h.data(), st, sizeof(JacobiState) * njobs, hipMemcpyDeviceToHost, s);
+      if (e == hipSuccess) e = hipStreamSynchronize(s);
+      if (e != hipSuccess) return e;
+      bool all = true;
+      for (int j = 0; j < njobs; ++j) all = all && h[j].done;
+      if (all) break;
     }
-    hipError_t e = hipMemcpyAsync(h.data(), st, sizeof(JacobiState) * njobs, hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
-    if (e != hipSuccess) return e;
-    bool all = true;
-    for (int j = 0; j < njobs; ++j) all = all && h[j].done;
-    if (all) break;
+    return hipSuccess;
+  };
+  hipError_t e = run();
+  if (nh == 2) {
+    // the join is recorded before every host check, so s2 has drained when run() returns normally
+    if (e != hipSuccess) (void)hipStreamSynchronize(s2);
+    (void)hipEventDestroy(fork);
+    (void)hipEventDestroy(join);
   }
+  if (e != hipSuccess) return e;
   k_jacobi_check<<<1, 256, 0, s>>>(st, njobs, status);
   return hipGetLastError();
 }
