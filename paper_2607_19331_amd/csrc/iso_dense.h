@@ -675,25 +675,31 @@ inline size_t gram_split_bytes(int njobs, int64_t max_r, int64_t max_c) {
   return ((size_t)njobs * np * (size_t)(ns + 1) * kGN * kGN) * sizeof(double) + (size_t)njobs * np * sizeof(int) + 256;
 }
 
-// A second stream of the current device (default priority, created on first use and kept until
-// the process ends), or null if it cannot be created.
-inline hipStream_t aux_stream() {
+// Job groups of the split Jacobi step, each on a stream of its own.
+constexpr int kJacobiGroups = 4;
+
+// Stream i (0 <= i < kJacobiGroups - 1) of the current device besides the caller's (default
+// priority, created on first use and kept until the process ends), or null if it cannot be created.
+inline hipStream_t aux_stream(int i) {
   constexpr int kMaxDev = 64;
   static std::mutex mu;
-  static hipStream_t per[kMaxDev] = {};
+  static hipStream_t per[kMaxDev][kJacobiGroups] = {};
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) return nullptr;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev || i < 0 || i >= kJacobiGroups) return nullptr;
   std::lock_guard<std::mutex> lock(mu);
-  if (per[dev] == nullptr && hipStreamCreateWithFlags(&per[dev], hipStreamNonBlocking) != hipSuccess) per[dev] = nullptr;
-  return per[dev];
+  if (per[dev][i] == nullptr && hipStreamCreateWithFlags(&per[dev][i], hipStreamNonBlocking) != hipSuccess)
+    per[dev][i] = nullptr;
+  return per[dev][i];
 }
 
-// With scratch (the split step) and at least two jobs, the job set runs as two halves, the second
-// on aux_stream(): a round's rotation launch has one workgroup per block pair and leaves most of
-// the chip idle, and the other half's Gram and apply launches fill it meanwhile.  The halves share
-// no job, state entry or scratch; in each block of sweeps between host checks, the second forks
-// from s after the first half's first Gram launch and joins s before the check.  Concurrent calls on one device share the second stream, which
-// orders their halves but keeps each call's dependencies on its own events.
+// With scratch (the split step) and at least two jobs, the job set runs as up to kJacobiGroups
+// contiguous groups, group 0 on s and the others on aux_stream(): a round's rotation launch has
+// one workgroup per block pair and leaves most of the chip idle, and the other groups' Gram and
+// apply launches fill it meanwhile.  The groups share no job, state entry or scratch.  In each
+// block of sweeps between host checks, group g + 1 starts once group g's first Gram launch of the
+// block is done (a phase apart), and every group joins s before the check.  Concurrent calls on
+// one device share the extra streams, which orders their groups but keeps each call's
+// dependencies on its own events.
 inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_r, int64_t max_c, JacobiState* st,
                               uint32_t* status, hipStream_t s, bool v_given, void* scratch) {
   const unsigned gb = (unsigned)std::max<int64_t>(1, std::min<int64_t>((max_c * max_c + 255) / 256, 4096));
@@ -712,62 +718,76 @@ inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_r, i
   const int slices_a = S.nslices, slices_v = S.slice ? (int)((max_c + S.slice - 1) / S.slice) : 0;
   // a sweep over more than 2^26 matrix entries takes milliseconds: check the flags after each one
   const int check = (double)max_r * (double)max_c * njobs > 67108864.0 ? 1 : kJacobiCheckSweeps;
-  struct Half {
+  struct Group {
     const JacobiJob* jobs;
     JacobiState* st;
     GramSplit S;
     int n;
     hipStream_t s;
+    hipEvent_t started, joined;   // after the group's first Gram launch of a block; at its end
   };
-  Half half[2] = {{jobs, st, S, njobs, s}, {}};
-  hipStream_t s2 = (scratch != nullptr && njobs >= 2) ? aux_stream() : nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
-  if (s2 != nullptr && (hipEventCreateWithFlags(&fork, hipEventDisableTiming) != hipSuccess ||
-                        hipEventCreateWithFlags(&join, hipEventDisableTiming) != hipSuccess)) {
-    if (fork != nullptr) (void)hipEventDestroy(fork);
-    fork = nullptr;
-    s2 = nullptr;
+  Group grp[kJacobiGroups] = {};
+  int ng = (scratch != nullptr) ? std::min(kJacobiGroups, njobs) : 1;
+  for (int i = 0; i < ng; ++i) {
+    hipStream_t si = (i == 0) ? s : aux_stream(i - 1);      // s may be the null stream
+    if ((i > 0 && si == nullptr) || (ng > 1 && (hipEventCreateWithFlags(&grp[i].started, hipEventDisableTiming) != hipSuccess ||
+                                     hipEventCreateWithFlags(&grp[i].joined, hipEventDisableTiming) != hipSuccess))) {
+      ng = i;            // run with the groups set up so far (at least group 0 on s)
+      break;
+    }
+    grp[i].s = si;
   }
-  const int nh = (s2 != nullptr) ? 2 : 1;
-  if (nh == 2) {
-    const int n0 = njobs / 2;
-    GramSplit S1 = S;
-    S1.part += (size_t)n0 * S.npairs * S.nslices * kGN * kGN;
-    S1.qrot += (size_t)n0 * S.npairs * kGN * kGN;
-    S1.need += (size_t)n0 * S.npairs;
-    half[0].n = n0;
-    half[1] = Half{jobs + n0, st + n0, S1, njobs - n0, s2};
+  if (ng == 0) ng = 1;
+  if (ng == 1) {
+    for (int i = 0; i < kJacobiGroups; ++i) {
+      if (grp[i].started != nullptr) (void)hipEventDestroy(grp[i].started);
+      if (grp[i].joined != nullptr) (void)hipEventDestroy(grp[i].joined);
+      grp[i].started = grp[i].joined = nullptr;
+    }
+  }
+  for (int i = 0, j0 = 0; i < ng; ++i) {
+    const int j1 = (int)((int64_t)njobs * (i + 1) / ng);
+    GramSplit Si = S;
+    if (scratch != nullptr) {
+      Si.part += (size_t)j0 * S.npairs * S.nslices * kGN * kGN;
+      Si.qrot += (size_t)j0 * S.npairs * kGN * kGN;
+      Si.need += (size_t)j0 * S.npairs;
+    }
+    grp[i].jobs = jobs + j0;
+    grp[i].st = st + j0;
+    grp[i].S = Si;
+    grp[i].n = j1 - j0;
+    grp[i].s = (i == 0) ? s : grp[i].s;
+    j0 = j1;
   }
   auto run = [&]() -> hipError_t {
     std::vector<JacobiState> h(njobs);
     for (int sweep = 0; sweep < kJacobiMaxSweeps;) {
       hipError_t e = hipSuccess;
       const int sweep0 = sweep;
-      for (int hi = 0; hi < nh; ++hi) {
-        const Half& H = half[hi];
-        // the second half starts once the first half's first Gram launch of this block is done,
-        // a phase apart, so that each half's rotations overlap the other's Gram or apply work
-        if (hi == 1 && (e = hipStreamWaitEvent(s2, fork, 0)) != hipSuccess) return e;
+      for (int gi = 0; gi < ng; ++gi) {
+        const Group& G = grp[gi];
+        if (gi > 0 && (e = hipStreamWaitEvent(G.s, grp[gi - 1].started, 0)) != hipSuccess) return e;
         for (int b = 0, sw = sweep0; b < check && sw < kJacobiMaxSweeps; ++b, ++sw) {
           for (int round = 0; round < nbp - 1; ++round) {
             if (scratch == nullptr) {
-              k_bjacobi_gram<<<g, 256, 0, H.s>>>(H.jobs, H.st, round);
+              k_bjacobi_gram<<<g, 256, 0, G.s>>>(G.jobs, G.st, round);
             } else {
-              k_bjg_part<<<dim3((unsigned)(H.S.npairs * H.S.nslices), (unsigned)H.n), 256, 0, H.s>>>(H.jobs, H.st,
-                                                                                                     round, H.S);
-              if (nh == 2 && hi == 0 && b == 0 && round == 0 && (e = hipEventRecord(fork, s)) != hipSuccess) return e;
-              k_bjg_rot<<<dim3((unsigned)H.S.npairs, (unsigned)H.n), 512, 0, H.s>>>(H.jobs, H.st, round, H.S);
-              k_bjg_apply<<<dim3((unsigned)(H.S.npairs * (slices_a + slices_v)), (unsigned)H.n), 256, 0, H.s>>>(
-                  H.jobs, H.st, round, H.S, slices_a, slices_v);
+              k_bjg_part<<<dim3((unsigned)(G.S.npairs * G.S.nslices), (unsigned)G.n), 256, 0, G.s>>>(G.jobs, G.st,
+                                                                                                     round, G.S);
+              if (ng > 1 && b == 0 && round == 0 && (e = hipEventRecord(G.started, G.s)) != hipSuccess) return e;
+              k_bjg_rot<<<dim3((unsigned)G.S.npairs, (unsigned)G.n), 512, 0, G.s>>>(G.jobs, G.st, round, G.S);
+              k_bjg_apply<<<dim3((unsigned)(G.S.npairs * (slices_a + slices_v)), (unsigned)G.n), 256, 0, G.s>>>(
+                  G.jobs, G.st, round, G.S, slices_a, slices_v);
             }
           }
-          k_jacobi_sweep_end<<<1, 256, 0, H.s>>>(H.st, H.n);
+          k_jacobi_sweep_end<<<1, 256, 0, G.s>>>(G.st, G.n);
         }
       }
       for (int b = 0; b < check && sweep < kJacobiMaxSweeps; ++b) ++sweep;
-      if (nh == 2) {
-        e = hipEventRecord(join, s2);
-        if (e == hipSuccess) e = hipStreamWaitEvent(s, join, 0);
+      for (int gi = 1; gi < ng; ++gi) {
+        e = hipEventRecord(grp[gi].joined, grp[gi].s);
+        if (e == hipSuccess) e = hipStreamWaitEvent(s, grp[gi].joined, 0);
         if (e != hipSuccess) return e;
       }
       e = hipMemcpyAsync(h.data(), st, sizeof(JacobiState) * njobs, hipMemcpyDeviceToHost, s);
@@ -780,11 +800,12 @@ inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_r, i
     return hipSuccess;
   };
   hipError_t e = run();
-  if (nh == 2) {
-    // the join is recorded before every host check, so s2 has drained when run() returns normally
-    if (e != hipSuccess) (void)hipStreamSynchronize(s2);
-    (void)hipEventDestroy(fork);
-    (void)hipEventDestroy(join);
+  for (int gi = 0; gi < kJacobiGroups; ++gi) {
+    // every group joins s before each host check, so the extra streams have drained when run()
+    // returns normally
+    if (e != hipSuccess && gi > 0 && gi < ng) (void)hipStreamSynchronize(grp[gi].s);
+    if (grp[gi].started != nullptr) (void)hipEventDestroy(grp[gi].started);
+    if (grp[gi].joined != nullptr) (void)hipEventDestroy(grp[gi].joined);
   }
   if (e != hipSuccess) return e;
   k_jacobi_check<<<1, 256, 0, s>>>(st, njobs, status);
