@@ -692,6 +692,58 @@ inline hipStream_t aux_stream(int i) {
   return per[dev][i];
 }
 
+// Independent per-item work fanned out over the caller's stream s and the extra streams of this
+// device: begin() makes the extra streams wait for what s holds so far, at(e) is item e's stream
+// (round-robin), end() makes s wait for all of them.  Without the extra streams or their events,
+// everything stays on s.  If end() was not reached (an error return), the destructor waits for the
+// extra streams, so that no work of this call is left running.
+struct Fan {
+  hipStream_t st[kJacobiGroups] = {};
+  hipEvent_t fork = nullptr, join[kJacobiGroups] = {};
+  int n = 1;
+  bool open = false;
+  hipError_t begin(hipStream_t s, int items) {
+    st[0] = s;
+    n = 1;
+    const int want = std::min(kJacobiGroups, std::max(1, items));
+    if (want < 2 || hipEventCreateWithFlags(&fork, hipEventDisableTiming) != hipSuccess) {
+      fork = nullptr;
+      return hipSuccess;
+    }
+    for (int i = 1; i < want; ++i) {
+      hipStream_t x = aux_stream(i - 1);
+      if (x == nullptr || hipEventCreateWithFlags(&join[i], hipEventDisableTiming) != hipSuccess) {
+        join[i] = nullptr;
+        break;
+      }
+      st[i] = x;
+      n = i + 1;
+    }
+    if (n < 2) return hipSuccess;
+    open = true;
+    hipError_t e = hipEventRecord(fork, s);
+    for (int i = 1; i < n && e == hipSuccess; ++i) e = hipStreamWaitEvent(st[i], fork, 0);
+    return e;
+  }
+  hipStream_t at(int e) const { return st[e % n]; }
+  hipError_t end() {
+    hipError_t e = hipSuccess;
+    for (int i = 1; i < n && e == hipSuccess; ++i) {
+      e = hipEventRecord(join[i], st[i]);
+      if (e == hipSuccess) e = hipStreamWaitEvent(st[0], join[i], 0);
+    }
+    if (e == hipSuccess) open = false;
+    return e;
+  }
+  ~Fan() {
+    if (open)
+      for (int i = 1; i < n; ++i) (void)hipStreamSynchronize(st[i]);
+    if (fork != nullptr) (void)hipEventDestroy(fork);
+    for (int i = 0; i < kJacobiGroups; ++i)
+      if (join[i] != nullptr) (void)hipEventDestroy(join[i]);
+  }
+};
+
 // With scratch (the split step) and at least two jobs, the job set runs as up to kJacobiGroups
 // contiguous groups, group 0 on s and the others on aux_stream(): a round's rotation launch has
 // one workgroup per block pair and leaves most of the chip idle, and the other groups' Gram and

@@ -803,18 +803,24 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
   // tall matrices: left factor A_i V_i S_i^{-1}; a matrix whose factors fail the guard goes to
   // plain Jacobi on A (its A_i are still in the Jacobi buffers)
   bool any_pre = false;
-  for (int e = 0; e < nm; ++e) {
-    if (!pre[e]) continue;
-    any_pre = true;
-    const int64_t m = t[ids[e]].rows, n = t[ids[e]].cols, q = std::min(m, n), r = std::max(m, n);
-    const bool wide = m < n;
-    const Bufs& b = bs[e];
-    for (int i = 0; i <= K; ++i) {
-      double* L = wide ? b.V[i] : b.U[i];
-      const double* Vs = wide ? b.U[i] : b.V[i];
-      gemm(r, q, q, 1.0, b.ja[i], 1, r, Vs, 1, q, 0.0, L, 1, r, s);
-      k_unit_cols<<<grid_for(r * q), 256, 0, s>>>(L, b.S[i], r, q);
+  {
+    Fan fan;
+    SP_TRY(fan.begin(s, nm));
+    for (int e = 0; e < nm; ++e) {
+      if (!pre[e]) continue;
+      any_pre = true;
+      const int64_t m = t[ids[e]].rows, n = t[ids[e]].cols, q = std::min(m, n), r = std::max(m, n);
+      const bool wide = m < n;
+      const Bufs& b = bs[e];
+      hipStream_t se = fan.at(e);
+      for (int i = 0; i <= K; ++i) {
+        double* L = wide ? b.V[i] : b.U[i];
+        const double* Vs = wide ? b.U[i] : b.V[i];
+        gemm(r, q, q, 1.0, b.ja[i], 1, r, Vs, 1, q, 0.0, L, 1, r, se);
+        k_unit_cols<<<grid_for(r * q), 256, 0, se>>>(L, b.S[i], r, q);
+      }
     }
+    SP_TRY(fan.end());
   }
   if (any_pre) {
     k_qr_guard<<<1, 256, 0, s>>>(tb.jobs, tb.ptrs + 2 * nsvd, tb.qfail, tb.qmat, nsvd, tb.qbad);
@@ -850,13 +856,20 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
       svd_finalize(tb.jobs, tb.ptrs, tb.ptrs + nr, tb.ptrs + 2 * nr, nr, rq, s);
     }
   }
-  // 2 - 6 per matrix; the polar arguments go to the first iterate buffers
-  for (int e = 0; e < nm; ++e) {
-    const int64_t m = t[ids[e]].rows, n = t[ids[e]].cols, q = std::min(m, n);
-    const Bufs& b = bs[e];
-    middle_steps(b, m, n, K, a, a.coef_out ? a.coef_out + (int64_t)ids[e] * K : nullptr, status, s);
-    k_copy<<<grid_for(m * q), 256, 0, s>>>(b.PX[0][0], b.AU, m * q);
-    k_copy<<<grid_for(n * q), 256, 0, s>>>(b.PX[1][0], b.AV, n * q);
+  // 2 - 6 per matrix (each matrix's own buffers, so the matrices run on several streams); the
+  // polar arguments go to the first iterate buffers
+  {
+    Fan fan;
+    SP_TRY(fan.begin(s, nm));
+    for (int e = 0; e < nm; ++e) {
+      const int64_t m = t[ids[e]].rows, n = t[ids[e]].cols, q = std::min(m, n);
+      const Bufs& b = bs[e];
+      hipStream_t se = fan.at(e);
+      middle_steps(b, m, n, K, a, a.coef_out ? a.coef_out + (int64_t)ids[e] * K : nullptr, status, se);
+      k_copy<<<grid_for(m * q), 256, 0, se>>>(b.PX[0][0], b.AU, m * q);
+      k_copy<<<grid_for(n * q), 256, 0, se>>>(b.PX[1][0], b.AV, n * q);
+    }
+    SP_TRY(fan.end());
   }
   // 6'. U_* = polar(U_0 + xi_U*), V_* = polar(V_0 + xi_V*)
   //     the tall side of a tall matrix in q space (then X_0 P into the second iterate buffer),
@@ -877,17 +890,23 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
       gemm(rows, q, q, 1.0, b.PX[h][0], 1, rows, b.QP[hsq[2 * e + h].steps & 1], 1, q, 0.0, b.PX[h][1], 1, rows, s);
     }
   }
-  for (int e = 0; e < nm; ++e) {
-    const iso_tensor& x = t[ids[e]];
-    const int64_t m = x.rows, n = x.cols, q = std::min(m, n);
-    const Bufs& b = bs[e];
-    const bool gu = pre[e] && m > n, gv = pre[e] && n > m;
-    const double* Us = b.PX[0][gu ? 1 : (hst[2 * e].steps & 1)];
-    const double* Vs = b.PX[1][gv ? 1 : (hst[2 * e + 1].steps & 1)];
-    // 7. W_* = U_* Sigma_0 V_*^T
-    k_scale_cols<<<grid_for(m * q), 256, 0, s>>>(b.FU, Us, b.S[0], m, q);
-    gemm(m, n, q, 1.0, b.FU, 1, m, Vs, n, 1, 0.0, b.Wst, 1, m, s);
-    k_store_w<<<grid_for(m * n), 256, 0, s>>>(x.out, b.Wst, m, n, dt, status);
+  {
+    Fan fan;
+    SP_TRY(fan.begin(s, nm));
+    for (int e = 0; e < nm; ++e) {
+      const iso_tensor& x = t[ids[e]];
+      const int64_t m = x.rows, n = x.cols, q = std::min(m, n);
+      const Bufs& b = bs[e];
+      const bool gu = pre[e] && m > n, gv = pre[e] && n > m;
+      const double* Us = b.PX[0][gu ? 1 : (hst[2 * e].steps & 1)];
+      const double* Vs = b.PX[1][gv ? 1 : (hst[2 * e + 1].steps & 1)];
+      hipStream_t se = fan.at(e);
+      // 7. W_* = U_* Sigma_0 V_*^T
+      k_scale_cols<<<grid_for(m * q), 256, 0, se>>>(b.FU, Us, b.S[0], m, q);
+      gemm(m, n, q, 1.0, b.FU, 1, m, Vs, n, 1, 0.0, b.Wst, 1, m, se);
+      k_store_w<<<grid_for(m * n), 256, 0, se>>>(x.out, b.Wst, m, n, dt, status);
+    }
+    SP_TRY(fan.end());
   }
   SP_TRY(hipGetLastError());
   // the next batch reuses the workspace and the host staging: let this one finish first
