@@ -768,8 +768,10 @@ inline hipError_t jacobi_gram(const JacobiJob* jobs, int njobs, int64_t max_r, i
     S.need = (int*)(S.qrot + (size_t)njobs * S.npairs * kGN * kGN);
   }
   const int slices_a = S.nslices, slices_v = S.slice ? (int)((max_c + S.slice - 1) / S.slice) : 0;
-  // a sweep over more than 2^26 matrix entries takes milliseconds: check the flags after each one
-  const int check = (double)max_r * (double)max_c * njobs > 67108864.0 ? 1 : kJacobiCheckSweeps;
+  // a sweep of the split step is three launches per round and job group, milliseconds even once
+  // every job has converged (their launches return at once), and so is a sweep over more than
+  // 2^26 matrix entries: check the flags after each one
+  const int check = (scratch != nullptr || (double)max_r * (double)max_c * njobs > 67108864.0) ? 1 : kJacobiCheckSweeps;
   struct Group {
     const JacobiJob* jobs;
     JacobiState* st;
