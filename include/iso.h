@@ -21,8 +21,18 @@
  *    iso_workspace_size(op, ...) bytes, 256-byte aligned, that must stay
  *    alive until the stream work has finished.  Its contents on entry do not
  *    matter.  The library allocates no device memory.
- *  - stream: a hipStream_t (NULL = the default stream).  Work is queued
- *    asynchronously on it; only iso_read_device_status synchronises.
+ *  - stream: a hipStream_t (NULL = the default stream).  Work is queued on
+ *    it.  The streaming operations (TopKMask, sign election, merges, APPLY
+ *    and FUSED updates) are asynchronous.  The binary64 dense operations
+ *    (SPECTRAL, ORTHO, TSV, the diagnostics, the optimizer steps) read
+ *    convergence flags on the host between blocks of iterations, so they
+ *    synchronise the stream during the call.  Some of their independent
+ *    pieces (groups of Jacobi jobs, per-matrix steps) run on streams the
+ *    library creates once per device (default priority, kept until the
+ *    process ends), forked from `stream` and joined back into it before the
+ *    call returns: the call stays ordered on `stream` like any other work.
+ *    Concurrent calls on one device share those streams (each keeps its own
+ *    dependencies).
  *  - Errors: argument, shape, alignment and workspace-size errors are found
  *    on the host before anything is queued and returned directly.  A
  *    non-finite base or delta value found by a kernel sets a status word in
