@@ -285,3 +285,32 @@ def test_ill_conditioned_tall_matrix_falls_back_to_plain_jacobi():
         ref = _ref(u, K, "f32")
         assert _close(o, "f32", ref["w_star"]), (u.rows, u.cols)
         assert np.allclose(c, ref["c"], rtol=1e-9, atol=1e-12), (u.rows, u.cols)
+
+
+def test_repeat_calls_bit_identical():
+    """Six matrices of mixed shapes (three tall enough for the Cholesky route) in one call, twice on
+    the same workspace: the Jacobi job sets run as concurrent groups on several streams and the
+    per-matrix steps are spread over them, so a race between them would show as a difference
+    between the two calls.  Outputs and coefficients must be bit-identical, and one matrix of each
+    route still matches the oracle."""
+    import torch
+    rng = np.random.default_rng(77)
+    shapes = [(512, 512), (1536, 384), (1024, 256), (640, 640), (300, 700), (1200, 400)]
+    K = 2
+    units = [_unit(rng, r, c, K, "f32") for r, c in shapes]
+    es = [u.entry() for u in units]
+    ws = iso.workspace(iso.OP_UPDATE_SPECTRAL, es, K, dt_code("f32"))
+    runs = []
+    for rep in range(2):
+        say(f"spectral repeat call {rep}: {len(units)} matrices {shapes}")
+        coef = torch.zeros(len(units) * K, dtype=torch.float64, device="cuda")
+        iso.iso_update(es, K, dt_code("f32"), iso.UPDATE_SPECTRAL, rho_keep=0.9, ridge=1e-12, c_min=0.0,
+                       c_max=1.5, coef_out=coef, ws=ws)
+        assert iso.iso_read_device_status(ws) == 0
+        runs.append(([from_dev(u.dout, u.n, "f32").copy() for u in units], coef.cpu().numpy().copy()))
+    for t in range(len(units)):
+        assert np.array_equal(runs[0][0][t].view(np.uint32), runs[1][0][t].view(np.uint32)), shapes[t]
+    assert np.array_equal(runs[0][1].view(np.uint64), runs[1][1].view(np.uint64))
+    for t in (0, 1):
+        ref = _ref(units[t], K, "f32")
+        assert _close(runs[1][0][t], "f32", ref["w_star"]), shapes[t]
