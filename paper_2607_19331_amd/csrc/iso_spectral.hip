@@ -753,22 +753,27 @@ iso_status run_batch(const iso_tensor* t, const std::vector<int>& ids, int K, is
   SP_TRY(hipGetDevice(&dev));
   SP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
   const bool warm = wgs > per_cu * (int64_t)cus;
-  for (int e = 0; e < nm; ++e) {
-    const iso_tensor& x = t[ids[e]];
-    for (int i = 0; i <= ((warm && !pre[e]) ? 0 : K); ++i)
-      k_load_f64<<<grid_for(x.rows * x.cols), 256, 0, s>>>(bs[e].ja[i], x.base, i ? x.deltas[i - 1] : nullptr, x.rows,
-                                                           x.cols, x.rows < x.cols ? 1 : 0, dt);
+  // the Jacobi matrices in binary64, and for the tall matrices the Grams A_i^T A_i (upper
+  // triangles) whose Cholesky factors R_i they run on; each matrix's own buffers, so the matrices
+  // are spread over the streams
+  {
+    Fan fan;
+    SP_TRY(fan.begin(s, nm));
+    for (int e = 0; e < nm; ++e) {
+      const iso_tensor& x = t[ids[e]];
+      hipStream_t se = fan.at(e);
+      for (int i = 0; i <= ((warm && !pre[e]) ? 0 : K); ++i)
+        k_load_f64<<<grid_for(x.rows * x.cols), 256, 0, se>>>(bs[e].ja[i], x.base, i ? x.deltas[i - 1] : nullptr,
+                                                              x.rows, x.cols, x.rows < x.cols ? 1 : 0, dt);
+      if (!pre[e]) continue;
+      const int64_t q = std::min(x.rows, x.cols), r = std::max(x.rows, x.cols);
+      const Bufs& b = bs[e];
+      for (int i = 0; i <= K; ++i)
+        gemm_job(GemmJob{b.ja[i], b.ja[i], b.jr[i], r, 1, 1, r, 1, q, q, q, r, 1.0, 0.0, 1, nullptr}, se);
+    }
+    SP_TRY(fan.end());
   }
-  // tall matrices: R_i from the Gram A_i^T A_i (its upper triangle), then, for the warm start,
-  // R_i - R_0 in the proxy buffer
-  for (int e = 0; e < nm; ++e) {
-    if (!pre[e]) continue;
-    const iso_tensor& x = t[ids[e]];
-    const int64_t q = std::min(x.rows, x.cols), r = std::max(x.rows, x.cols);
-    const Bufs& b = bs[e];
-    for (int i = 0; i <= K; ++i)
-      gemm_job(GemmJob{b.ja[i], b.ja[i], b.jr[i], r, 1, 1, r, 1, q, q, q, r, 1.0, 0.0, 1, nullptr}, s);
-  }
+  // then, for the warm start, R_i - R_0 in the proxy buffer
   if (nch > 0) cholesky_upper_jobs(tb.qch, nch, ch_q, tb.qtrail, s);
   for (int e = 0; e < nm; ++e) {
     if (!pre[e] || !warm) continue;
